@@ -1,0 +1,478 @@
+"""CPU oracle for HeRo's history-aware routed FFN stack.  TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the smoke check and the CPU-baseline leg of the benchmark may
+import this module.  The product (the HIP library and its Python binding) never
+does, and this module imports nothing from the product.
+
+What it is: the method of the paper (HeRo, "History-Aware Routing", arxiv
+2609.08189, Sec. 3), written out step by step in plain float64 numpy, one
+function per equation, in the paper's order and notation.  There is no
+blocking, fusion or reordering; a matrix product over a batch of tokens is the
+only library primitive used, and each token's row is independent of the others
+except for the skip-budget selection.
+
+Readings of points the paper leaves open (each one is a named argument or
+constant here):
+  * the routed FFN stack has no attention between routed layers, so the next
+    layer's post-attention state is this layer's output (hbar_{j+1} = h_j);
+  * the frozen FFN is Llama's bias-free SwiGLU W_d (SiLU(W_g u) * (W_u u)), and
+    LN^ffn is Llama's RMSNorm with gain w and eps_norm;
+  * the router's own RMSNorm (hidden encoder) has unit gain and eps_norm;
+  * every router/adapter linear map is bias-free; FFN_path is
+    Linear(6->d_p) -> SiLU -> Linear(d_p->d_a); f_theta and f_psi are
+    Linear(in->d_head) -> SiLU -> Linear(d_head->1);
+  * the comparison space of W_n and W_c has width d_m; the three epsilons of the
+    transition cosine, the memory read and the history cosine are one eps, and
+    both cosines use <a,b> / (|a||b| + eps);
+  * phi(x) = x + 1 for x > 0 and exp(x) otherwise (ELU + 1 evaluated directly);
+  * the gate decision g >= tau_exec is taken in logit space, logit >= ln(tau/(1-tau)),
+    on the float32 rounding of the logit (the precision the kernels decide in);
+    ties go to the FFN;
+  * an optional per-token logit bias beta enters the gate only: g = sigma(a + b + beta);
+  * skip-budget mode (not in the paper; needed because untrained routers give
+    gates near 1/2): per layer, n_skip = floor(budget * T + 1/2) tokens with the
+    smallest (float32 logit, token index) take the adapter;
+  * at layer j = 1 the state is the paper's initial value (S = 0, zeta = 0,
+    p = m = 1) whatever the incoming buffers hold;
+  * hidden-state outputs are rounded to the storage dtype (bfloat16 nearest-even
+    for bf16 workloads) at every layer boundary; nothing else is rounded.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional
+
+import numpy as np
+
+f64 = np.float64
+
+
+# ---------------------------------------------------------------------------
+# elementary functions
+# ---------------------------------------------------------------------------
+
+
+def sigmoid(x):
+    """Logistic function sigma(x) = 1 / (1 + e^-x), evaluated without overflow."""
+    x = np.asarray(x, dtype=f64)
+    out = np.empty_like(x)
+    pos = x >= 0
+    out[pos] = 1.0 / (1.0 + np.exp(-x[pos]))
+    ex = np.exp(x[~pos])
+    out[~pos] = ex / (1.0 + ex)
+    return out
+
+
+def silu(x):
+    """SiLU(x) = x * sigma(x)."""
+    x = np.asarray(x, dtype=f64)
+    return x * sigmoid(x)
+
+
+def phi(x):
+    """Positive feature map ELU(x) + 1 of the linear-attention memory (Sec. 3.2, router memory)."""
+    x = np.asarray(x, dtype=f64)
+    return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))
+
+
+def cosine_eps(a, b, eps):
+    """<a, b> / (|a| |b| + eps), row-wise over the last axis."""
+    num = np.sum(a * b, axis=-1)
+    den = np.linalg.norm(a, axis=-1) * np.linalg.norm(b, axis=-1) + eps
+    return num / den
+
+
+def round_bf16(x):
+    """Round float64 values to the nearest bfloat16 (8 significant bits), ties to even.
+
+    Written from the definition of the format (same exponent range as IEEE
+    binary32, 7 stored fraction bits).  Values in this workload never reach the
+    subnormal or overflow range; those are not handled.
+    """
+    x = np.asarray(x, dtype=f64)
+    m, e = np.frexp(x)                      # x = m * 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)
+
+
+def round_io(x, dtype):
+    if dtype == "bf16":
+        return round_bf16(x)
+    if dtype == "f32":
+        return np.asarray(x, dtype=np.float32).astype(f64)
+    raise ValueError(dtype)
+
+
+# ---------------------------------------------------------------------------
+# parameters
+# ---------------------------------------------------------------------------
+
+
+@dataclasses.dataclass
+class Dims:
+    d: int
+    d_ff: int
+    d_r: int
+    L_R: int
+    d_m: int
+    d_s: int = 64
+    d_h: int = 48
+    d_a: int = 16
+    d_e: int = 256
+    d_p: int = 64
+    d_head: int = 256
+    eps_norm: float = 1e-5
+    eps: float = 1e-6
+    T_hist: float = 0.9
+    io_dtype: str = "f32"
+
+
+@dataclasses.dataclass
+class RouterParams:
+    """Router parameters shared by every routed layer (Sec. 3.2, last sentence of 'Router memory')."""
+    w_hd: np.ndarray   # [d_e, d]        hidden encoder, down
+    w_hu: np.ndarray   # [d_h, d_e]      hidden encoder, up
+    w_p1: np.ndarray   # [d_p, 6]        path encoder FFN_path, first layer
+    w_p2: np.ndarray   # [d_a, d_p]      path encoder, second layer
+    w_q: np.ndarray    # [d_m, d_s]
+    w_k: np.ndarray    # [d_m, d_s]
+    w_v: np.ndarray    # [d_m, d_s]
+    w_n: np.ndarray    # [d_m, d_s]      state -> comparison space
+    w_c: np.ndarray    # [d_m, d_m]      context -> comparison space
+    th1: np.ndarray    # [d_head, d_s + d_m + 1]  history head f_theta
+    th2: np.ndarray    # [d_head]
+    ps1: np.ndarray    # [d_head, d]     local head f_psi
+    ps2: np.ndarray    # [d_head]
+
+
+@dataclasses.dataclass
+class FFNParams:
+    norm_w: np.ndarray  # [d]          LN^ffn gain
+    w_gate: np.ndarray  # [d_ff, d]
+    w_up: np.ndarray    # [d_ff, d]
+    w_down: np.ndarray  # [d, d_ff]
+
+
+@dataclasses.dataclass
+class AdapterParams:
+    w1: np.ndarray      # [d_r, d]     down projection W_1
+    w2: np.ndarray      # [d, d_r]     up projection W_2
+
+
+@dataclasses.dataclass
+class State:
+    """Per-token router state carried across routed layers."""
+    S: np.ndarray       # [T, d_m, d_m]  memory matrix, key index first
+    zeta: np.ndarray    # [T, d_m]       normaliser
+    p_hist: np.ndarray  # [T]            previous history score
+    m_hist: np.ndarray  # [T]            cumulative history score
+
+    @staticmethod
+    def initial(T, d_m):
+        """Zero memory and p = m = 1 at the start of a forward pass (Sec. 3.2)."""
+        return State(np.zeros((T, d_m, d_m)), np.zeros((T, d_m)), np.ones(T), np.ones(T))
+
+    def copy(self):
+        return State(self.S.copy(), self.zeta.copy(), self.p_hist.copy(), self.m_hist.copy())
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.1  Router computation: FFN input, branches, routed output
+# ---------------------------------------------------------------------------
+
+
+def rmsnorm(h, gain, eps_norm):
+    """RMSNorm h / sqrt(mean(h^2) + eps) * gain, per token row."""
+    h = np.asarray(h, dtype=f64)
+    r = 1.0 / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + eps_norm)
+    out = h * r
+    if gain is not None:
+        out = out * gain
+    return out
+
+
+def ffn_input(hbar, ffn: FFNParams, dims: Dims):
+    """u = LN^ffn(hbar), the normalised FFN input (Sec. 3.1, eq:dense_attention second line)."""
+    return rmsnorm(hbar, ffn.norm_w, dims.eps_norm)
+
+
+def frozen_ffn(u, ffn: FFNParams):
+    """Frozen pretrained FFN, read as Llama SwiGLU: W_d (SiLU(W_g u) * (W_u u))."""
+    gate = u @ ffn.w_gate.T
+    up = u @ ffn.w_up.T
+    return (silu(gate) * up) @ ffn.w_down.T
+
+
+def adapter(u, ad: AdapterParams):
+    """Bottleneck adapter W_2 SiLU(W_1 u) (Sec. 3.1, adapter equation)."""
+    return silu(u @ ad.w1.T) @ ad.w2.T
+
+
+def routed_output(hbar, g, use_ffn, ffn_out, adapter_out):
+    """Thresholded single-branch output (Sec. 3.1, eq:ffn_route).
+
+    FFN tokens: hbar + g * FFN(u); adapter tokens: hbar + (1 - g) * Adapter(u).
+    ``ffn_out``/``adapter_out`` only need valid rows where the branch is taken.
+    """
+    g = g[:, None]
+    return np.where(use_ffn[:, None], hbar + g * ffn_out, hbar + (1.0 - g) * adapter_out)
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.2  HeRo router: router state
+# ---------------------------------------------------------------------------
+
+
+def hidden_encoder(hbar, R: RouterParams, dims: Dims):
+    """z^h = W_hu SiLU(W_hd RMSNorm(hbar)) in R^{d_h} (Sec. 3.2, 'Router state')."""
+    return silu(rmsnorm(hbar, None, dims.eps_norm) @ R.w_hd.T) @ R.w_hu.T
+
+
+def depth_features(j, L_R):
+    """Routing progress r = j / L_R and remaining fraction q_rem = (L_R - j) / L_R."""
+    return j / L_R, (L_R - j) / L_R
+
+
+def residual_transitions(j, hbar, hbar_prev1, hbar_prev2, eps):
+    """delta_j = hbar_j - hbar_{j-1} (zero at j = 1), d_j = |delta_j|, and
+    gamma_j = cos(delta_j, delta_{j-1}) with eps (zero for j <= 2)
+    (Sec. 3.2, transition equation and eq:transition_features)."""
+    T = hbar.shape[0]
+    if j < 2:
+        return np.zeros(T), np.zeros(T)
+    delta = hbar - hbar_prev1
+    d_j = np.linalg.norm(delta, axis=-1)
+    if j <= 2:
+        return d_j, np.zeros(T)
+    delta_prev = hbar_prev1 - hbar_prev2
+    return d_j, cosine_eps(delta, delta_prev, eps)
+
+
+def path_vector(j, L_R, d_j, gamma_j, p_prev, m_prev):
+    """x^path = [r, q_rem, d, gamma, p^hist_{j-1}, m^hist_{j-1}] in R^6 (eq:path_vector)."""
+    T = d_j.shape[0]
+    r, q_rem = depth_features(j, L_R)
+    return np.stack([np.full(T, r), np.full(T, q_rem), d_j, gamma_j, p_prev, m_prev], axis=-1)
+
+
+def path_encoder(x_path, R: RouterParams):
+    """z^a = FFN_path(x^path) in R^{d_a}."""
+    return silu(x_path @ R.w_p1.T) @ R.w_p2.T
+
+
+def router_state(z_h, z_a):
+    """s = [z^h; z^a] in R^{d_s} (eq:router_state)."""
+    return np.concatenate([z_h, z_a], axis=-1)
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.2  HeRo router: router memory (linear attention over depth)
+# ---------------------------------------------------------------------------
+
+
+def memory_projections(s, R: RouterParams):
+    """q = W_q s, k = W_k s, v = W_v s in R^{d_m}."""
+    return s @ R.w_q.T, s @ R.w_k.T, s @ R.w_v.T
+
+
+def memory_read(q, S_prev, zeta_prev, eps):
+    """c = phi(q)^T S_{j-1} / (phi(q)^T zeta_{j-1} + eps) (eq:memory_read)."""
+    fq = phi(q)
+    num = np.einsum("tk,tkv->tv", fq, S_prev)
+    den = np.sum(fq * zeta_prev, axis=-1) + eps
+    return num / den[:, None]
+
+
+def memory_write(k, v, S_prev, zeta_prev, rho):
+    """S_j = rho S_{j-1} + phi(k) v^T,  zeta_j = rho zeta_{j-1} + phi(k) (eq:memory_update)."""
+    fk = phi(k)
+    S = rho * S_prev + fk[:, :, None] * v[:, None, :]
+    zeta = rho * zeta_prev + fk
+    return S, zeta
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.2  HeRo router: gate computation
+# ---------------------------------------------------------------------------
+
+
+def history_dissimilarity(j, s, c, R: RouterParams, eps):
+    """nu = 1 - cos(W_n s, W_c c) for j > 1, nu = 0 at the first routed layer."""
+    if j == 1:
+        return np.zeros(s.shape[0])
+    return 1.0 - cosine_eps(s @ R.w_n.T, c @ R.w_c.T, eps)
+
+
+def history_head(s, c, nu, R: RouterParams, T_hist):
+    """a = f_theta([s; c; nu]) and p^hist = sigma(a / T_hist)."""
+    x = np.concatenate([s, c, nu[:, None]], axis=-1)
+    a = silu(x @ R.th1.T) @ R.th2
+    return a, sigmoid(a / T_hist)
+
+
+def cumulative_history(m_prev, p):
+    """m^hist_j = m^hist_{j-1} * p^hist_j."""
+    return m_prev * p
+
+
+def local_head(hbar, R: RouterParams):
+    """b = f_psi(hbar), on the post-attention representation itself (eq:final_gate)."""
+    return silu(hbar @ R.ps1.T) @ R.ps2
+
+
+def execution_gate(a, b, beta=None):
+    """Logit a + b (+ optional per-token bias) and gate g = sigma(logit) (eq:final_gate)."""
+    ell = a + b
+    if beta is not None:
+        ell = ell + beta
+    return ell, sigmoid(ell)
+
+
+# ---------------------------------------------------------------------------
+# branch decision
+# ---------------------------------------------------------------------------
+
+
+def logit_f32(ell):
+    return np.asarray(ell, dtype=np.float32).astype(f64)
+
+
+def decide_threshold(ell, tau):
+    """g >= tau_exec taken as logit >= ln(tau / (1 - tau)) on float32 logits; ties -> FFN (eq:ffn_route)."""
+    lam = math.log(tau / (1.0 - tau))
+    use_ffn = logit_f32(ell) >= np.float32(lam)
+    return use_ffn, float(np.float32(lam))
+
+
+def n_skip_for(budget, T):
+    return int(math.floor(budget * T + 0.5))
+
+
+def decide_budget(ell, budget):
+    """The n_skip smallest (float32 logit, token index) take the adapter.
+
+    Returns (use_ffn, lambda) where lambda is the smallest logit left on the FFN
+    branch (+inf when every token skips).
+    """
+    T = ell.shape[0]
+    k = n_skip_for(budget, T)
+    l32 = logit_f32(ell)
+    order = np.lexsort((np.arange(T), l32))     # primary: logit, secondary: index
+    use_ffn = np.ones(T, dtype=bool)
+    use_ffn[order[:k]] = False
+    lam = float(l32[order[k]]) if k < T else math.inf
+    return use_ffn, lam
+
+
+# ---------------------------------------------------------------------------
+# one routed layer and the routed stack
+# ---------------------------------------------------------------------------
+
+
+@dataclasses.dataclass
+class LayerResult:
+    h: np.ndarray          # [T, d] layer output (rounded to the storage dtype)
+    state: State           # updated router state
+    logit: np.ndarray      # [T]
+    gate: np.ndarray       # [T]
+    use_ffn: np.ndarray    # [T] bool: the branch actually taken
+    own_ffn: np.ndarray    # [T] bool: the oracle's own decision
+    lam: float
+    debug: Dict[str, np.ndarray]
+
+
+def routed_layer(j, dims: Dims, hbar, hbar_prev1, hbar_prev2, state: State,
+                 ffn: FFNParams, R: RouterParams, ad: AdapterParams, eta,
+                 mode="budget", budget=0.0, tau=0.5, beta=None,
+                 forced_ffn=None, round_output=True, compute_rows=None, lam_given=None):
+    """Routed layer l_j for a batch of tokens, in the order of Sec. 3 (overview paragraph).
+
+    ``forced_ffn`` (bool [T]) makes the branch follow a given decision (teacher
+    forcing); the oracle's own decision is still returned.  ``compute_rows``
+    (bool [T]) restricts the expensive branch evaluation to those rows; other
+    rows of ``h`` are left as NaN.  ``lam_given`` (budget mode on a subset of a
+    larger batch) replaces the subset's own quantile: a token's own decision is
+    then FFN iff its float32 logit >= lam_given.
+    """
+    hbar = np.asarray(hbar, dtype=f64)
+    T = hbar.shape[0]
+    if j == 1:
+        state = State.initial(T, dims.d_m)
+    # router state (eq:path_vector .. eq:router_state)
+    z_h = hidden_encoder(hbar, R, dims)
+    d_j, gamma_j = residual_transitions(j, hbar, hbar_prev1, hbar_prev2, dims.eps)
+    x_path = path_vector(j, dims.L_R, d_j, gamma_j, state.p_hist, state.m_hist)
+    z_a = path_encoder(x_path, R)
+    s = router_state(z_h, z_a)
+    # memory: read before write
+    q, k, v = memory_projections(s, R)
+    c = memory_read(q, state.S, state.zeta, dims.eps)
+    rho = float(sigmoid(np.array([eta]))[0])
+    S_new, zeta_new = memory_write(k, v, state.S, state.zeta, rho)
+    # gate
+    nu = history_dissimilarity(j, s, c, R, dims.eps)
+    a, p = history_head(s, c, nu, R, dims.T_hist)
+    m = cumulative_history(state.m_hist, p)
+    b = local_head(hbar, R)
+    ell, g = execution_gate(a, b, beta)
+    # decision
+    if mode == "threshold":
+        own, lam = decide_threshold(ell, tau)
+    elif mode == "budget" and lam_given is not None:
+        own, lam = logit_f32(ell) >= np.float32(lam_given), float(lam_given)
+    elif mode == "budget":
+        own, lam = decide_budget(ell, budget)
+    else:
+        raise ValueError(mode)
+    use_ffn = own if forced_ffn is None else np.asarray(forced_ffn, dtype=bool)
+    # branches and routed output (eq:ffn_route)
+    rows = np.ones(T, dtype=bool) if compute_rows is None else np.asarray(compute_rows, bool)
+    ffn_out = np.full(hbar.shape, np.nan)
+    adapter_out = np.full(hbar.shape, np.nan)
+    fr = np.nonzero(rows & use_ffn)[0]
+    ar = np.nonzero(rows & ~use_ffn)[0]
+    if fr.size:
+        ffn_out[fr] = frozen_ffn(ffn_input(hbar[fr], ffn, dims), ffn)
+    if ar.size:
+        adapter_out[ar] = adapter(ffn_input(hbar[ar], ffn, dims), ad)
+    h = routed_output(hbar, g, use_ffn, ffn_out, adapter_out)
+    h[~rows] = np.nan
+    if round_output:
+        h = round_io(h, dims.io_dtype)
+    debug = dict(z_h=z_h, d=d_j, gamma=gamma_j, x_path=x_path, z_a=z_a, s=s, q=q, k=k, v=v,
+                 c=c, nu=nu, a=a, b=b, rho=rho)
+    return LayerResult(h, State(S_new, zeta_new, p, m), ell, g, use_ffn, own, lam, debug)
+
+
+@dataclasses.dataclass
+class StackResult:
+    h: np.ndarray
+    state: State
+    layers: List[LayerResult]
+
+
+def routed_stack(dims: Dims, h_in, ffns: List[FFNParams], R: RouterParams,
+                 adapters: List[AdapterParams], etas, mode="budget", budget=0.0, tau=0.5,
+                 beta=None, forced_ffn=None, lam_given=None):
+    """L_R routed layers with zero initial state; hbar_{j+1} = h_j between them.
+
+    ``forced_ffn`` is an optional list (one bool [T] per layer) for teacher
+    forcing, ``lam_given`` an optional list of per-layer budget thresholds (for
+    a token subset of a larger batch).
+    """
+    T = h_in.shape[0]
+    state = State.initial(T, dims.d_m)
+    hist = [None, None]                  # hbar_{j-1}, hbar_{j-2}
+    hbar = np.asarray(h_in, dtype=f64)
+    layers = []
+    for j in range(1, dims.L_R + 1):
+        ff = None if forced_ffn is None else forced_ffn[j - 1]
+        lg = None if lam_given is None else lam_given[j - 1]
+        res = routed_layer(j, dims, hbar, hist[0], hist[1], state, ffns[j - 1], R,
+                           adapters[j - 1], etas[j - 1], mode, budget, tau, beta, ff,
+                           lam_given=lg)
+        layers.append(res)
+        state = res.state
+        hist = [hbar, hist[0]]
+        hbar = res.h
+    return StackResult(hbar, state, layers)

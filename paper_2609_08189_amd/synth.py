@@ -1,0 +1,342 @@
+"""Seeded synthetic inputs for the HeRo routed FFN stack.
+
+This module is the one piece shared by the GPU harness and the CPU oracle's
+callers.  It draws hidden states, frozen-backbone weights, router weights,
+adapter weights and (for a mid-stack layer call) a plausible incoming router
+state, and stores them in the storage dtype of a workload.  It holds none of the
+method's arithmetic: no feature map, no norm, no gate, no routing.  Inputs are
+returned twice over: ``store`` arrays (np.float32, or np.uint16 bf16 bit
+patterns) to upload to the device, and exact float64 decodings of those same
+stored values for the oracle.
+
+Recipe (the paper trains Llama backbones on instruction data; neither the
+weights nor the data are available, so Gaussian stand-ins of the same shapes
+are used):
+  * hidden states ~ N(0, 1);
+  * every weight matrix ~ N(0, 0.02), frozen FFN gate/up/down included;
+  * the FFN-input RMSNorm gain ~ 1 + N(0, 0.02) (a gain near zero would all but
+    switch the FFN branch off);
+  * forgetting parameter eta = ln 49 for every routed layer, so that
+    sigma(eta) = 0.98, the initial value the paper states for rho (Sec. 4.1);
+  * a mid-stack layer call (layer j > 1) also draws an incoming state: a
+    geometrically decayed sum of j-1 outer products a_i b_i^T with strictly
+    positive a_i (log-normal), its matching normaliser sum, history scores
+    p ~ U(0.2, 0.8), m ~ U(0, p), and two earlier post-attention states that
+    differ from the current one by N(0, 0.5^2) steps;
+  * the 13B prefill workload adds a per-token logit bias that is constant over
+    runs of 64 positions: a seeded 29 % of the runs draw N(-2, 1), the rest
+    N(2, 1), so that skip decisions cluster by position.
+Every draw comes from numpy's PCG64 keyed by (seed, tensor id, layer), drawn in
+float32 and rounded once, round-to-nearest-even, to the storage dtype.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional
+
+import numpy as np
+
+# ---------------------------------------------------------------------------
+# workload definitions
+# ---------------------------------------------------------------------------
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    dtype: str                 # "f32" or "bf16": hidden states and every weight
+    d: int                     # model width
+    d_ff: int                  # SwiGLU intermediate width
+    d_r: int                   # adapter rank
+    L_R: int                   # number of routed layers
+    d_m: int                   # router-memory key/value width
+    T: int                     # tokens per call (batch x positions, flattened)
+    mode: str                  # "budget" or "threshold"
+    budget: float = 0.0        # skip fraction (budget mode)
+    tau: float = 0.5           # execution threshold (threshold mode)
+    layer_j: int = 0           # >0: a single layer call at routed index j
+    bias: str = "none"         # "none" or "bimodal_runs"
+    batch: int = 1
+    seq: int = 0
+    # router sub-network widths (Sec. 4.1 gives d_s=64 = 48 + 16 and heads of 256)
+    d_s: int = 64
+    d_h: int = 48
+    d_a: int = 16
+    d_e: int = 256
+    d_p: int = 64
+    d_head: int = 256
+    eps_norm: float = 1e-5
+    eps: float = 1e-6
+    T_hist: float = 0.9
+
+    @property
+    def d_c(self) -> int:
+        return self.d_m
+
+    def replace(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+WORKLOADS: Dict[str, Workload] = {
+    # tiny fp32 stack: 4 routed layers, d=256, d_ff=688, r=16, d_m=32, T=64, ~27 % skip
+    "tiny_f32_stack": Workload("tiny_f32_stack", "f32", 256, 688, 16, 4, 32, 64,
+                               "budget", budget=0.27, batch=1, seq=64),
+    # Llama-3.1-8B shape, one routed layer (j=17 of 32), bf16, T=4096 prefill tokens
+    "llama31_8b_layer": Workload("llama31_8b_layer", "bf16", 4096, 14336, 64, 32, 128,
+                                 4096, "budget", budget=0.2687, layer_j=17,
+                                 batch=1, seq=4096),
+    # Llama-3.1-8B shape, 32-layer routed stack, 16 x 2048 tokens, tight budget
+    "llama31_8b_stack": Workload("llama31_8b_stack", "bf16", 4096, 14336, 64, 32, 128,
+                                 32768, "budget", budget=0.3882, batch=16, seq=2048),
+    # Llama-2-7B shape, 32-layer decode step, 256 sequences x 1 token
+    "llama2_7b_decode": Workload("llama2_7b_decode", "bf16", 4096, 11008, 64, 32, 128,
+                                 256, "budget", budget=0.27, batch=256, seq=1),
+    # Llama-2-13B shape, 40-layer prefill, 8 x 4096 tokens, bimodal position-clustered bias
+    "llama2_13b_prefill": Workload("llama2_13b_prefill", "bf16", 5120, 13824, 64, 40, 128,
+                                   32768, "threshold", tau=0.5, bias="bimodal_runs",
+                                   batch=8, seq=4096),
+}
+
+# ---------------------------------------------------------------------------
+# storage rounding (input preparation only)
+# ---------------------------------------------------------------------------
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bfloat16 (nearest, ties to even); return the bits."""
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounded = (b + np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return rounded.astype(np.uint16)
+
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Exact float64 value of stored bfloat16 bit patterns."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def to_store(x32: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == "f32":
+        return np.ascontiguousarray(x32, dtype=np.float32)
+    if dtype == "bf16":
+        return f32_to_bf16_bits(x32)
+    raise ValueError(dtype)
+
+
+def store_to_f64(a: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == "f32":
+        return np.asarray(a, dtype=np.float32).astype(np.float64)
+    if dtype == "bf16":
+        return bf16_bits_to_f64(a)
+    raise ValueError(dtype)
+
+
+# ---------------------------------------------------------------------------
+# seeded draws
+# ---------------------------------------------------------------------------
+
+# fixed tensor ids: they key the random streams, so they never change
+_TID = {
+    "hbar": 1, "hbar_prev1": 2, "hbar_prev2": 3,
+    "norm_w": 10, "w_gate": 11, "w_up": 12, "w_down": 13,
+    "w1": 20, "w2": 21,
+    "w_hd": 30, "w_hu": 31, "w_p1": 32, "w_p2": 33, "w_q": 34, "w_k": 35, "w_v": 36,
+    "w_n": 37, "w_c": 38, "th1": 39, "th2": 40, "ps1": 41, "ps2": 42,
+    "state_a": 50, "state_b": 51, "p_hist": 52, "m_hist": 53,
+    "bias_runs": 60, "bias_vals": 61,
+}
+
+
+def _rng(seed: int, name: str, layer: int = 0) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64([seed, _TID[name], layer]))
+
+
+def normal32(seed: int, name: str, shape, std: float = 1.0, mean: float = 0.0,
+             layer: int = 0) -> np.ndarray:
+    g = _rng(seed, name, layer)
+    x = g.standard_normal(size=shape, dtype=np.float32)
+    if std != 1.0:
+        x *= np.float32(std)
+    if mean != 0.0:
+        x += np.float32(mean)
+    return x
+
+
+class Tensor:
+    """A stored tensor plus the exact float64 decoding of what was stored."""
+
+    __slots__ = ("store", "dtype", "_f64")
+
+    def __init__(self, store: np.ndarray, dtype: str):
+        self.store = store
+        self.dtype = dtype
+        self._f64 = None
+
+    @property
+    def f64(self) -> np.ndarray:
+        if self._f64 is None:
+            self._f64 = store_to_f64(self.store, self.dtype)
+        return self._f64
+
+    @property
+    def shape(self):
+        return self.store.shape
+
+
+def _t(x32: np.ndarray, dtype: str) -> Tensor:
+    return Tensor(to_store(x32, dtype), dtype)
+
+
+ROUTER_SHAPES = {
+    "w_hd": lambda w: (w.d_e, w.d),
+    "w_hu": lambda w: (w.d_h, w.d_e),
+    "w_p1": lambda w: (w.d_p, 6),
+    "w_p2": lambda w: (w.d_a, w.d_p),
+    "w_q": lambda w: (w.d_m, w.d_s),
+    "w_k": lambda w: (w.d_m, w.d_s),
+    "w_v": lambda w: (w.d_m, w.d_s),
+    "w_n": lambda w: (w.d_c, w.d_s),
+    "w_c": lambda w: (w.d_c, w.d_m),
+    "th1": lambda w: (w.d_head, w.d_s + w.d_m + 1),
+    "th2": lambda w: (w.d_head,),
+    "ps1": lambda w: (w.d_head, w.d),
+    "ps2": lambda w: (w.d_head,),
+}
+
+
+def router_weights(w: Workload, seed: int = 0, std: float = 0.02) -> Dict[str, Tensor]:
+    return {k: _t(normal32(seed, k, fn(w), std), w.dtype) for k, fn in ROUTER_SHAPES.items()}
+
+
+def ffn_layer(w: Workload, layer: int, seed: int = 0) -> Dict[str, Tensor]:
+    return {
+        "norm_w": _t(normal32(seed, "norm_w", (w.d,), 0.02, 1.0, layer), w.dtype),
+        "w_gate": _t(normal32(seed, "w_gate", (w.d_ff, w.d), 0.02, layer=layer), w.dtype),
+        "w_up": _t(normal32(seed, "w_up", (w.d_ff, w.d), 0.02, layer=layer), w.dtype),
+        "w_down": _t(normal32(seed, "w_down", (w.d, w.d_ff), 0.02, layer=layer), w.dtype),
+    }
+
+
+def adapter_layer(w: Workload, layer: int, seed: int = 0) -> Dict[str, Tensor]:
+    return {
+        "w1": _t(normal32(seed, "w1", (w.d_r, w.d), 0.02, layer=layer), w.dtype),
+        "w2": _t(normal32(seed, "w2", (w.d, w.d_r), 0.02, layer=layer), w.dtype),
+    }
+
+
+def eta_values(w: Workload) -> np.ndarray:
+    return np.full(w.L_R, math.log(49.0), dtype=np.float32)
+
+
+def hidden(w: Workload, seed: int = 0, T: Optional[int] = None) -> Tensor:
+    T = w.T if T is None else T
+    return _t(normal32(seed, "hbar", (T, w.d)), w.dtype)
+
+
+def incoming_history(w: Workload, hbar: Tensor, seed: int = 0):
+    """Earlier post-attention states for a mid-stack layer call (j >= 2)."""
+    T = hbar.shape[0]
+    h0 = store_to_f64(hbar.store, w.dtype).astype(np.float32)
+    p1 = h0 - normal32(seed, "hbar_prev1", (T, w.d), 0.5)
+    prev1 = _t(p1, w.dtype)
+    p2 = store_to_f64(prev1.store, w.dtype).astype(np.float32) - normal32(seed, "hbar_prev2", (T, w.d), 0.5)
+    prev2 = _t(p2, w.dtype)
+    return prev1, prev2
+
+
+def incoming_state(w: Workload, j: int, T: int, seed: int = 0, decay: float = 0.98):
+    """A plausible router state as it stands before routed layer j (fp32 storage).
+
+    S = sum_{i<j} decay^(j-1-i) a_i b_i^T and zeta = sum_{i<j} decay^(j-1-i) a_i with
+    log-normal (strictly positive) a_i and Gaussian b_i; p ~ U(0.2, 0.8), m ~ U(0, p).
+    For j == 1 the state is the all-zero matrix/normaliser with p = m = 1.
+    """
+    dm = w.d_m
+    S = np.zeros((T, dm, dm), dtype=np.float32)
+    zeta = np.zeros((T, dm), dtype=np.float32)
+    if j <= 1:
+        return S, zeta, np.ones(T, np.float32), np.ones(T, np.float32)
+    ga = _rng(seed, "state_a")
+    gb = _rng(seed, "state_b")
+    for i in range(1, j):
+        wgt = np.float32(decay ** (j - 1 - i))
+        a = np.exp(np.float32(0.5) * ga.standard_normal((T, dm), dtype=np.float32))
+        b = gb.standard_normal((T, dm), dtype=np.float32)
+        S += wgt * (a[:, :, None] * b[:, None, :])
+        zeta += wgt * a
+    gp = _rng(seed, "p_hist")
+    p = gp.uniform(0.2, 0.8, size=T).astype(np.float32)
+    gm = _rng(seed, "m_hist")
+    m = (gm.uniform(0.0, 1.0, size=T).astype(np.float32) * p).astype(np.float32)
+    return S, zeta, p, m
+
+
+def logit_bias(w: Workload, seed: int = 0, T: Optional[int] = None) -> Optional[np.ndarray]:
+    """Per-token logit bias for the position-clustered bimodal workload, else None."""
+    if w.bias == "none":
+        return None
+    T = w.T if T is None else T
+    run = 64
+    n_runs = (T + run - 1) // run
+    n_neg = int(math.floor(0.29 * n_runs + 0.5))
+    perm = _rng(seed, "bias_runs").permutation(n_runs)
+    neg = np.zeros(n_runs, dtype=bool)
+    neg[perm[:n_neg]] = True
+    vals = _rng(seed, "bias_vals").standard_normal(T, dtype=np.float32)
+    run_of = np.arange(T) // run
+    beta = np.where(neg[run_of], vals - np.float32(2.0), vals + np.float32(2.0)).astype(np.float32)
+    return beta
+
+
+# ---------------------------------------------------------------------------
+# a whole problem instance
+# ---------------------------------------------------------------------------
+
+
+@dataclasses.dataclass
+class Problem:
+    w: Workload
+    hbar: Tensor                      # [T, d]: h_in for a stack, hbar_j for a layer call
+    hbar_prev1: Optional[Tensor]
+    hbar_prev2: Optional[Tensor]
+    S: np.ndarray                     # [T, d_m, d_m] f32 (incoming, layer calls)
+    zeta: np.ndarray                  # [T, d_m] f32
+    p_hist: np.ndarray                # [T] f32
+    m_hist: np.ndarray                # [T] f32
+    router: Dict[str, Tensor]
+    ffn: List[Dict[str, Tensor]]      # one per routed layer (a layer call: one entry)
+    adapter: List[Dict[str, Tensor]]
+    eta: np.ndarray                   # [L_R] f32 (a layer call uses eta[j-1])
+    beta: Optional[np.ndarray]        # [T] f32 or None
+
+
+def make_problem(w: Workload, seed: int = 0, T: Optional[int] = None,
+                 layer_j: Optional[int] = None) -> Problem:
+    """Draw every input of a workload.  ``layer_j`` overrides the workload's layer index."""
+    T = w.T if T is None else T
+    j = w.layer_j if layer_j is None else layer_j
+    hb = hidden(w, seed, T)
+    prev1 = prev2 = None
+    if j >= 1:
+        # a single routed-layer call at index j
+        if j >= 2:
+            prev1, prev2 = incoming_history(w, hb, seed)
+            if j == 2:
+                prev2 = None
+        S, zeta, p, m = incoming_state(w, j, T, seed)
+        layers = [j - 1]
+    else:
+        S = np.zeros((T, w.d_m, w.d_m), np.float32)
+        zeta = np.zeros((T, w.d_m), np.float32)
+        p = np.ones(T, np.float32)
+        m = np.ones(T, np.float32)
+        layers = list(range(w.L_R))
+    return Problem(
+        w=w, hbar=hb, hbar_prev1=prev1, hbar_prev2=prev2,
+        S=S, zeta=zeta, p_hist=p, m_hist=m,
+        router=router_weights(w, seed),
+        ffn=[ffn_layer(w, l, seed) for l in layers],
+        adapter=[adapter_layer(w, l, seed) for l in layers],
+        eta=eta_values(w),
+        beta=logit_bias(w, seed, T),
+    )
