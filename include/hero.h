@@ -1,0 +1,203 @@
+/*
+ * hero.h -- C ABI of the HeRo routed FFN stack for AMD Instinct MI355X (gfx950).
+ *
+ * HeRo ("History-Aware Routing", arxiv 2609.08189) routes every token at every
+ * routed layer either to the frozen backbone's FFN or to a small adapter
+ * (Sec. 3.1, eq:ffn_route).  The router scores the token from its
+ * post-attention state and a per-token linear-attention memory over depth
+ * (Sec. 3.2), reads that memory before writing the layer's router state into
+ * it, and carries four pieces of per-token state to the next routed layer: the
+ * memory matrix S, its normaliser zeta, and the history scores p and m.
+ *
+ * This library runs that hot path on one GPU.  It is a plain C interface:
+ *   - every tensor argument is a DEVICE pointer to caller-owned memory unless a
+ *     comment says "host"; the library allocates nothing and keeps no state
+ *     between calls;
+ *   - calls are asynchronous: they validate their arguments on the host, enqueue
+ *     kernels on `stream` (a hipStream_t passed as void*, NULL = the null
+ *     stream) and return; results are valid once the stream has synchronised;
+ *   - calls return a hero_status; they never abort.  Argument checks run before
+ *     anything touches the GPU, so a bad argument never launches a kernel.
+ *     Device faults surface at the caller's next synchronisation.
+ *   - calls on different streams are independent when their buffers are
+ *     disjoint; two calls sharing a workspace must be ordered by the caller.
+ *
+ * Layouts (row-major throughout, token-major for per-token data):
+ *   hidden states           [T][d]                 dtype = dims.dtype
+ *   weights                 [out][in] (nn.Linear)  dtype = dims.dtype
+ *   memory matrix S         [T][d_m][d_m] fp32, key index first, so the read is
+ *                           c[v] = sum_k phi(q)[k] S[k][v] / (phi(q).zeta + eps)
+ *   normaliser zeta         [T][d_m] fp32
+ *   history scores p, m     [T] fp32
+ * All device pointers must be 16-byte aligned.
+ */
+#ifndef HERO_H
+#define HERO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HERO_ABI_VERSION 1
+
+typedef enum hero_status {
+  HERO_OK = 0,
+  HERO_E_NULL = 1,        /* a required pointer is NULL                               */
+  HERO_E_DIM = 2,         /* a size is non-positive or inconsistent (d_s != d_h + d_a) */
+  HERO_E_RANGE = 3,       /* j outside 1..L_R, tau outside (0,1), budget outside [0,1] */
+  HERO_E_DTYPE = 4,       /* unknown dtype code                                        */
+  HERO_E_ALIGN = 5,       /* a device pointer is not 16-byte aligned                  */
+  HERO_E_ALIAS = 6,       /* an output buffer overlaps an input it must not overlap   */
+  HERO_E_WORKSPACE = 7,   /* workspace NULL or smaller than hero_workspace_size()      */
+  HERO_E_UNSUPPORTED = 8, /* valid shape that the kernels do not implement            */
+  HERO_E_LAUNCH = 9,      /* a kernel launch was rejected by the runtime              */
+  HERO_E_DEVICE = 10      /* no usable gfx950 device is current                       */
+} hero_status;
+
+typedef enum hero_dtype { HERO_F32 = 0, HERO_BF16 = 1 } hero_dtype;
+
+typedef enum hero_mode {
+  HERO_MODE_THRESHOLD = 0, /* FFN iff g >= tau (Sec. 3.1, eq:ffn_route), tau_exec = 0.5 in Sec. 4.1 */
+  HERO_MODE_BUDGET = 1     /* per layer, floor(budget*T + 1/2) tokens with the smallest
+                              (logit, token index) take the adapter; not in the paper, it
+                              fixes the skip fraction of untrained routers              */
+} hero_mode;
+
+/*
+ * Shapes and constants.  d_s = d_h + d_a is the router-state width (Sec. 4.1:
+ * 64 = 48 + 16); d_e is the hidden encoder's inner width, d_p the path
+ * encoder's, d_head the history/local heads' hidden width (Sec. 4.1: 256); the
+ * comparison space of W_n, W_c has width d_m.
+ * Supported: d % 256 == 0 (bf16) or d % 128 == 0 (f32); bf16 also needs
+ * d_ff % 128 == 0, d_r % 64 == 0 and (d_e + d_head) % 128 == 0; d_m in
+ * {32, 64, 128, 256}; d_s <= 128; d_e, d_head <= 512; d_p <= 128.
+ */
+typedef struct hero_dims {
+  int d, d_ff, d_r, L_R;
+  int d_m, d_s, d_h, d_a;
+  int d_e, d_p, d_head;
+  int dtype;          /* hero_dtype of hidden states and every weight            */
+  float eps_norm;     /* RMSNorm epsilon (1e-5)                                   */
+  float eps;          /* epsilon of the two cosines and the memory read (1e-6)   */
+  float T_hist;       /* history temperature (Sec. 4.1: 0.9)                      */
+} hero_dims;
+
+/* Frozen backbone FFN of one routed layer: LN^ffn gain [d], W_g, W_u [d_ff][d], W_d [d][d_ff]. */
+typedef struct hero_ffn_weights {
+  const void *norm_w, *w_gate, *w_up, *w_down;
+} hero_ffn_weights;
+
+/* Bottleneck adapter of one routed layer (Sec. 3.1): W_1 [d_r][d], W_2 [d][d_r]. */
+typedef struct hero_adapter_weights {
+  const void *w1, *w2;
+} hero_adapter_weights;
+
+/*
+ * Router weights shared by every routed layer (Sec. 3.2), bias-free:
+ *   w_hd [d_e][d], w_hu [d_h][d_e]         hidden encoder z_h = W_hu SiLU(W_hd RMSNorm(hbar))
+ *   w_p1 [d_p][6], w_p2 [d_a][d_p]         path encoder z_a = FFN_path(x_path)
+ *   w_q, w_k, w_v [d_m][d_s]               memory projections
+ *   w_n [d_m][d_s], w_c [d_m][d_m]         comparison projections of nu
+ *   th1 [d_head][d_s + d_m + 1], th2 [d_head]   history head f_theta([s; c; nu])
+ *   ps1 [d_head][d], ps2 [d_head]          local head f_psi(hbar)
+ */
+typedef struct hero_router_weights {
+  const void *w_hd, *w_hu, *w_p1, *w_p2, *w_q, *w_k, *w_v, *w_n, *w_c;
+  const void *th1, *th2, *ps1, *ps2;
+} hero_router_weights;
+
+/* Per-token router state (fp32), read and written in place. */
+typedef struct hero_state {
+  float *S;       /* [T][d_m][d_m] */
+  float *zeta;    /* [T][d_m]      */
+  float *p_hist;  /* [T]           */
+  float *m_hist;  /* [T]           */
+} hero_state;
+
+typedef struct hero_routing {
+  int mode;                 /* hero_mode                                                */
+  float tau;                /* threshold mode: tau_exec in (0,1)                        */
+  double budget;            /* budget mode: skip fraction in [0,1]                      */
+  const float *logit_bias;  /* optional device [T] fp32 added to the gate logit only;
+                               NULL = none                                               */
+} hero_routing;
+
+/*
+ * Optional per-layer outputs; every field may be NULL.
+ *   mask    [T] u8     1 = FFN branch, 0 = adapter
+ *   idx_ffn [T] i32    FFN tokens, ascending; entries past counts[0] are undefined
+ *   idx_ad  [T] i32    adapter tokens, ascending; entries past counts[1] are undefined
+ *   counts  [2] i32    n_ffn, n_adapter
+ *   logit   [T] f32    a + b (+ bias)
+ *   gate    [T] f32    g = sigma(logit)
+ *   lambda  [1] f32    threshold mode: ln(tau/(1-tau)); budget mode: the smallest
+ *                      logit on the FFN branch (+inf if none)
+ */
+typedef struct hero_layer_stats {
+  uint8_t *mask;
+  int32_t *idx_ffn, *idx_ad, *counts;
+  float *logit, *gate, *lambda;
+} hero_layer_stats;
+
+/* Static string for a status code (host). */
+const char *hero_status_string(int status);
+
+/* ABI version (HERO_ABI_VERSION). */
+int hero_abi_version(void);
+
+/*
+ * Workspace bytes needed by hero_routed_layer (for_stack = 0) or
+ * hero_routed_stack (for_stack = 1) with T tokens.  Host-only; validates dims.
+ */
+int hero_workspace_size(const hero_dims *dims, int T, int for_stack, size_t *bytes);
+
+/*
+ * One routed layer l_j, j in 1..L_R (Sec. 3, overview paragraph, and
+ * Sec. 3.1-3.2).  For every token t:
+ *   router state s from hbar, (hbar - hbar_prev1), (hbar_prev1 - hbar_prev2), p, m
+ *   (eq:path_vector, eq:transition_features, eq:router_state);
+ *   memory read c from S, zeta, then memory write S <- rho S + phi(k) v^T,
+ *   zeta <- rho zeta + phi(k), rho = sigma(eta) (eq:memory_read, eq:memory_update);
+ *   nu, a, p <- sigma(a/T_hist), m <- m p; b; logit = a + b (+bias), g = sigma(logit)
+ *   (Sec. 3.2 gate computation, eq:final_gate);
+ *   branch decision (threshold or budget mode) and
+ *   h_out = hbar + g FFN(u) or hbar + (1 - g) Adapter(u), u = RMSNorm_w(hbar)
+ *   (eq:dense_attention, eq:ffn_route).
+ * hbar_prev1 is read for j >= 2, hbar_prev2 for j >= 3 (NULL otherwise).  At
+ * j = 1 the incoming state is taken as the paper's initial value (S = 0,
+ * zeta = 0, p = m = 1) whatever the buffers hold, and is then overwritten.
+ * h_out must not overlap hbar, hbar_prev1 or hbar_prev2.
+ * Output rounding: h_out is rounded once to dims.dtype; all arithmetic is fp32.
+ */
+int hero_routed_layer(const hero_dims *dims, int j, int T,
+                      const void *hbar, const void *hbar_prev1, const void *hbar_prev2,
+                      void *h_out, const hero_state *state,
+                      const hero_ffn_weights *ffn, const hero_router_weights *router,
+                      const hero_adapter_weights *adapter, float eta,
+                      const hero_routing *routing, const hero_layer_stats *stats,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * The whole routed stack: L_R chained routed layers with no attention between
+ * them, hbar_1 = h_in and hbar_{j+1} = h_j; the state starts from the paper's
+ * initial value (Sec. 3.2: zero memory at the start of a forward pass) and its
+ * final value is left in `state`.  ffn, adapter and eta are HOST arrays of
+ * L_R entries (device weight pointers inside); stats is a HOST array of L_R
+ * entries or NULL.  The result equals L_R chained hero_routed_layer calls bit
+ * for bit.  h_out must not overlap h_in.
+ */
+int hero_routed_stack(const hero_dims *dims, int T, const void *h_in, void *h_out,
+                      const hero_state *state, const hero_ffn_weights *ffn,
+                      const hero_router_weights *router, const hero_adapter_weights *adapter,
+                      const float *eta, const hero_routing *routing,
+                      const hero_layer_stats *stats,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HERO_H */

@@ -1,0 +1,354 @@
+// C ABI of the HeRo routed FFN stack: argument validation, workspace layout and
+// the per-layer kernel sequence.  Every argument check runs on the host before
+// any HIP call, so invalid calls never reach the GPU.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <atomic>
+
+#include "../../include/hero.h"
+#include "hero_kernels.h"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+size_t esize(int dtype) { return dtype == HERO_BF16 ? 2 : 4; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+struct Layout {
+  size_t u, P, rowstat, logit, gate, mask, idx_ffn, idx_ad, counts, lambda, act, part, ring, total;
+};
+
+Layout layout_of(const hero_dims& d, int T, bool stack) {
+  const size_t es = esize(d.dtype), t = static_cast<size_t>(T);
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.u = take(t * d.d * es);
+  L.P = take(t * (d.d_e + d.d_head) * 4);
+  L.rowstat = take(t * 16);
+  L.logit = take(t * 4);
+  L.gate = take(t * 4);
+  L.mask = take(t);
+  L.idx_ffn = take(t * 4);
+  L.idx_ad = take(t * 4);
+  L.counts = take(16);
+  L.lambda = take(16);
+  L.act = take(t * d.d_ff * es);
+  L.part = take(hero::adapter_part_floats(d.dtype, d.d, d.d_r, T) * 4);
+  L.ring = stack ? take(3 * t * d.d * es) : 0;
+  L.total = off;
+  return L;
+}
+
+int check_dims(const hero_dims* d) {
+  if (!d) return HERO_E_NULL;
+  if (d->dtype != HERO_F32 && d->dtype != HERO_BF16) return HERO_E_DTYPE;
+  if (d->d <= 0 || d->d_ff <= 0 || d->d_r <= 0 || d->L_R <= 0 || d->d_m <= 0 || d->d_s <= 0 ||
+      d->d_h <= 0 || d->d_a <= 0 || d->d_e <= 0 || d->d_p <= 0 || d->d_head <= 0)
+    return HERO_E_DIM;
+  if (d->d_s != d->d_h + d->d_a) return HERO_E_DIM;
+  if (!(d->eps_norm >= 0.f) || !(d->eps > 0.f) || !(d->T_hist > 0.f)) return HERO_E_RANGE;
+  // kernel support
+  if (d->d_m != 32 && d->d_m != 64 && d->d_m != 128 && d->d_m != 256) return HERO_E_UNSUPPORTED;
+  if (d->d_s > 128 || d->d_e > 512 || d->d_head > 512 || d->d_p > 128) return HERO_E_UNSUPPORTED;
+  if (d->dtype == HERO_BF16) {
+    if (d->d % 256 || d->d_ff % 128 || (d->d_e + d->d_head) % 128) return HERO_E_UNSUPPORTED;
+    if (d->d_r % 32 || d->d_r > 128) return HERO_E_UNSUPPORTED;
+  } else {
+    if (d->d % 128) return HERO_E_UNSUPPORTED;
+  }
+  return HERO_OK;
+}
+
+int check_routing(const hero_routing* r) {
+  if (!r) return HERO_E_NULL;
+  if (r->mode == HERO_MODE_THRESHOLD) {
+    if (!(r->tau > 0.f && r->tau < 1.f)) return HERO_E_RANGE;
+  } else if (r->mode == HERO_MODE_BUDGET) {
+    if (!(r->budget >= 0.0 && r->budget <= 1.0)) return HERO_E_RANGE;
+  } else {
+    return HERO_E_RANGE;
+  }
+  if (r->logit_bias && !aligned16(r->logit_bias)) return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+int check_weights(const hero_ffn_weights* f, const hero_router_weights* r, const hero_adapter_weights* a) {
+  if (!f || !r || !a) return HERO_E_NULL;
+  const void* ptrs[] = {f->norm_w, f->w_gate, f->w_up, f->w_down, a->w1, a->w2,
+                        r->w_hd, r->w_hu, r->w_p1, r->w_p2, r->w_q, r->w_k, r->w_v,
+                        r->w_n, r->w_c, r->th1, r->th2, r->ps1, r->ps2};
+  for (const void* p : ptrs)
+    if (!p) return HERO_E_NULL;
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+int check_state(const hero_state* s) {
+  if (!s || !s->S || !s->zeta || !s->p_hist || !s->m_hist) return HERO_E_NULL;
+  if (!aligned16(s->S) || !aligned16(s->zeta) || !aligned16(s->p_hist) || !aligned16(s->m_hist))
+    return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+int check_stats(const hero_layer_stats* s) {
+  if (!s) return HERO_OK;
+  const void* ptrs[] = {s->mask, s->idx_ffn, s->idx_ad, s->counts, s->logit, s->gate, s->lambda};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+// The current device must be gfx950; checked once per device.
+int check_device() {
+  static std::atomic<int> known[64];  // 0 unknown, 1 ok, 2 not gfx950
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return HERO_E_DEVICE;
+  if (dev < 64) {
+    const int k = known[dev].load(std::memory_order_acquire);
+    if (k != 0) return k == 1 ? HERO_OK : HERO_E_DEVICE;
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return HERO_E_DEVICE;
+  const bool ok = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+  if (dev < 64) known[dev].store(ok ? 1 : 2, std::memory_order_release);
+  return ok ? HERO_OK : HERO_E_DEVICE;
+}
+
+struct LayerCall {
+  const hero_dims* dims;
+  int j, T;
+  const void *hbar, *prev1, *prev2;
+  void* h_out;
+  const hero_state* st;
+  const hero_ffn_weights* ffn;
+  const hero_router_weights* rt;
+  const hero_adapter_weights* ad;
+  float eta;
+  const hero_routing* rc;
+  const hero_layer_stats* stats;
+  unsigned char* ws;
+  const Layout* L;
+  hipStream_t stream;
+};
+
+int run_layer(const LayerCall& c) {
+  using namespace hero;
+  const hero_dims& D = *c.dims;
+  const int T = c.T;
+  unsigned char* ws = c.ws;
+  const Layout& L = *c.L;
+  const hero_layer_stats* S = c.stats;
+  float* logit = (S && S->logit) ? S->logit : reinterpret_cast<float*>(ws + L.logit);
+  float* gate = (S && S->gate) ? S->gate : reinterpret_cast<float*>(ws + L.gate);
+  uint8_t* mask = (S && S->mask) ? S->mask : reinterpret_cast<uint8_t*>(ws + L.mask);
+  int* idx_ffn = (S && S->idx_ffn) ? S->idx_ffn : reinterpret_cast<int*>(ws + L.idx_ffn);
+  int* idx_ad = (S && S->idx_ad) ? S->idx_ad : reinterpret_cast<int*>(ws + L.idx_ad);
+  int* counts = (S && S->counts) ? S->counts : reinterpret_cast<int*>(ws + L.counts);
+  float* lambda = (S && S->lambda) ? S->lambda : reinterpret_cast<float*>(ws + L.lambda);
+  void* u = ws + L.u;
+  float* P = reinterpret_cast<float*>(ws + L.P);
+  float* rowstat = reinterpret_cast<float*>(ws + L.rowstat);
+
+  hipError_t e = launch_rowstats(D.dtype, c.hbar, c.j >= 2 ? c.prev1 : nullptr,
+                                 c.j >= 3 ? c.prev2 : nullptr, c.ffn->norm_w, T, D.d, c.j,
+                                 D.eps_norm, rowstat, u, c.stream);
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = launch_router_gemm(D.dtype, c.hbar, c.rt->w_hd, c.rt->ps1, T, D.d, D.d_e, D.d_head, P, c.stream);
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+
+  RouterTailArgs ra{};
+  ra.dtype = D.dtype;
+  ra.T = T;
+  ra.j = c.j;
+  ra.L_R = D.L_R;
+  ra.d_m = D.d_m;
+  ra.d_s = D.d_s;
+  ra.d_h = D.d_h;
+  ra.d_a = D.d_a;
+  ra.d_e = D.d_e;
+  ra.d_p = D.d_p;
+  ra.d_head = D.d_head;
+  ra.eps = D.eps;
+  ra.T_hist = D.T_hist;
+  ra.eta = c.eta;
+  ra.P = P;
+  ra.rowstat = rowstat;
+  ra.w_hu = c.rt->w_hu;
+  ra.w_p1 = c.rt->w_p1;
+  ra.w_p2 = c.rt->w_p2;
+  ra.w_q = c.rt->w_q;
+  ra.w_k = c.rt->w_k;
+  ra.w_v = c.rt->w_v;
+  ra.w_n = c.rt->w_n;
+  ra.w_c = c.rt->w_c;
+  ra.th1 = c.rt->th1;
+  ra.th2 = c.rt->th2;
+  ra.ps2 = c.rt->ps2;
+  ra.beta = c.rc->logit_bias;
+  ra.S = c.st->S;
+  ra.zeta = c.st->zeta;
+  ra.p_hist = c.st->p_hist;
+  ra.m_hist = c.st->m_hist;
+  ra.logit = logit;
+  ra.gate = gate;
+  e = launch_router_tail(ra, c.stream);
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+
+  SelectArgs sa{};
+  sa.logit = logit;
+  sa.T = T;
+  sa.mode = c.rc->mode;
+  sa.thr = static_cast<float>(log(static_cast<double>(c.rc->tau) / (1.0 - static_cast<double>(c.rc->tau))));
+  const int n_skip = c.rc->mode == HERO_MODE_BUDGET
+                         ? static_cast<int>(floor(c.rc->budget * static_cast<double>(T) + 0.5))
+                         : 0;
+  sa.n_skip = n_skip;
+  sa.mask = mask;
+  sa.idx_ffn = idx_ffn;
+  sa.idx_ad = idx_ad;
+  sa.counts = counts;
+  sa.lambda = lambda;
+  e = launch_select(sa, c.stream);
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+
+  // grid sizes: exact in budget mode, T in threshold mode (tiles past the device count exit)
+  const int n_ffn_max = c.rc->mode == HERO_MODE_BUDGET ? T - n_skip : T;
+  const int n_ad_max = c.rc->mode == HERO_MODE_BUDGET ? n_skip : T;
+  e = launch_ffn(D.dtype, u, idx_ffn, counts, n_ffn_max, c.ffn->w_gate, c.ffn->w_up, c.ffn->w_down,
+                 ws + L.act, c.hbar, gate, c.h_out, D.d, D.d_ff, c.stream);
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = launch_adapter(D.dtype, u, idx_ad, counts + 1, n_ad_max, c.ad->w1, c.ad->w2,
+                     reinterpret_cast<float*>(ws + L.part), c.hbar, gate, c.h_out, D.d, D.d_r,
+                     c.stream);
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  return HERO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hero_status_string(int status) {
+  switch (status) {
+    case HERO_OK: return "ok";
+    case HERO_E_NULL: return "a required pointer is NULL";
+    case HERO_E_DIM: return "a size is non-positive or inconsistent";
+    case HERO_E_RANGE: return "an argument is out of range";
+    case HERO_E_DTYPE: return "unknown dtype";
+    case HERO_E_ALIGN: return "a device pointer is not 16-byte aligned";
+    case HERO_E_ALIAS: return "an output overlaps an input";
+    case HERO_E_WORKSPACE: return "workspace missing or too small";
+    case HERO_E_UNSUPPORTED: return "shape not supported by the kernels";
+    case HERO_E_LAUNCH: return "kernel launch failed";
+    case HERO_E_DEVICE: return "no usable gfx950 device";
+    default: return "unknown status";
+  }
+}
+
+int hero_abi_version(void) { return HERO_ABI_VERSION; }
+
+int hero_workspace_size(const hero_dims* dims, int T, int for_stack, size_t* bytes) {
+  if (!bytes) return HERO_E_NULL;
+  const int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if (T <= 0) return HERO_E_DIM;
+  *bytes = layout_of(*dims, T, for_stack != 0).total;
+  return HERO_OK;
+}
+
+int hero_routed_layer(const hero_dims* dims, int j, int T, const void* hbar, const void* hbar_prev1,
+                      const void* hbar_prev2, void* h_out, const hero_state* state,
+                      const hero_ffn_weights* ffn, const hero_router_weights* router,
+                      const hero_adapter_weights* adapter, float eta, const hero_routing* routing,
+                      const hero_layer_stats* stats, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if (T <= 0) return HERO_E_DIM;
+  if (j < 1 || j > dims->L_R) return HERO_E_RANGE;
+  if (!hbar || !h_out) return HERO_E_NULL;
+  if (j >= 2 && !hbar_prev1) return HERO_E_NULL;
+  if (j >= 3 && !hbar_prev2) return HERO_E_NULL;
+  if (!aligned16(hbar) || !aligned16(h_out) || (j >= 2 && !aligned16(hbar_prev1)) ||
+      (j >= 3 && !aligned16(hbar_prev2)))
+    return HERO_E_ALIGN;
+  if ((st = check_state(state)) != HERO_OK) return st;
+  if ((st = check_weights(ffn, router, adapter)) != HERO_OK) return st;
+  if ((st = check_routing(routing)) != HERO_OK) return st;
+  if ((st = check_stats(stats)) != HERO_OK) return st;
+  if (!(eta == eta)) return HERO_E_RANGE;
+  const size_t hb = static_cast<size_t>(T) * dims->d * esize(dims->dtype);
+  if (overlap(h_out, hb, hbar, hb) || (j >= 2 && overlap(h_out, hb, hbar_prev1, hb)) ||
+      (j >= 3 && overlap(h_out, hb, hbar_prev2, hb)))
+    return HERO_E_ALIAS;
+  const Layout L = layout_of(*dims, T, false);
+  if (!workspace) return HERO_E_WORKSPACE;
+  if (workspace_bytes < L.total) return HERO_E_WORKSPACE;
+  if (!aligned16(workspace)) return HERO_E_ALIGN;
+  if ((st = check_device()) != HERO_OK) return st;
+  LayerCall c{dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, state, ffn, router, adapter, eta,
+              routing, stats, static_cast<unsigned char*>(workspace), &L,
+              static_cast<hipStream_t>(stream)};
+  return run_layer(c);
+}
+
+int hero_routed_stack(const hero_dims* dims, int T, const void* h_in, void* h_out,
+                      const hero_state* state, const hero_ffn_weights* ffn,
+                      const hero_router_weights* router, const hero_adapter_weights* adapter,
+                      const float* eta, const hero_routing* routing, const hero_layer_stats* stats,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if (T <= 0) return HERO_E_DIM;
+  if (!h_in || !h_out || !ffn || !adapter || !eta) return HERO_E_NULL;
+  if (!aligned16(h_in) || !aligned16(h_out)) return HERO_E_ALIGN;
+  if ((st = check_state(state)) != HERO_OK) return st;
+  if ((st = check_routing(routing)) != HERO_OK) return st;
+  for (int l = 0; l < dims->L_R; ++l) {
+    if ((st = check_weights(&ffn[l], router, &adapter[l])) != HERO_OK) return st;
+    if (!(eta[l] == eta[l])) return HERO_E_RANGE;
+    if (stats && (st = check_stats(&stats[l])) != HERO_OK) return st;
+  }
+  const size_t hb = static_cast<size_t>(T) * dims->d * esize(dims->dtype);
+  if (overlap(h_out, hb, h_in, hb)) return HERO_E_ALIAS;
+  const Layout L = layout_of(*dims, T, true);
+  if (!workspace) return HERO_E_WORKSPACE;
+  if (workspace_bytes < L.total) return HERO_E_WORKSPACE;
+  if (!aligned16(workspace)) return HERO_E_ALIGN;
+  if (overlap(h_out, hb, workspace, L.total)) return HERO_E_ALIAS;
+  if ((st = check_device()) != HERO_OK) return st;
+
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  const void* ring[3] = {ws + L.ring, ws + L.ring + hb, ws + L.ring + 2 * hb};
+  auto hbar_of = [&](int jj) -> const void* {  // post-attention state entering routed layer jj
+    return jj == 1 ? h_in : ring[(jj - 2) % 3];
+  };
+  for (int j = 1; j <= dims->L_R; ++j) {
+    void* out = j == dims->L_R ? h_out : const_cast<void*>(ring[(j - 1) % 3]);
+    LayerCall c{dims, j, T, hbar_of(j), j >= 2 ? hbar_of(j - 1) : nullptr,
+                j >= 3 ? hbar_of(j - 2) : nullptr, out, state, &ffn[j - 1], router,
+                &adapter[j - 1], eta[j - 1], routing, stats ? &stats[j - 1] : nullptr, ws, &L,
+                static_cast<hipStream_t>(stream)};
+    if ((st = run_layer(c)) != HERO_OK) return st;
+  }
+  return HERO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,67 @@
+// Host-side launchers of the HeRo kernels (one translation unit per kernel family).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hero {
+
+// Row statistics of the post-attention states and the FFN input:
+//   rowstat[t] = {1/rms(hbar_t), |delta_j|^2, <delta_j, delta_{j-1}>, |delta_{j-1}|^2}
+//   u[t] = RMSNorm_w(hbar_t) in the storage dtype.
+hipError_t launch_rowstats(int dtype, const void* hbar, const void* prev1, const void* prev2,
+                           const void* norm_w, int T, int d, int j, float eps_norm,
+                           float* rowstat, void* u, hipStream_t s);
+
+// Router pre-activations P[t] = [W_hd hbar_t ; psi_1 hbar_t] (fp32, [T][d_e + d_head]).
+hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, const void* ps1,
+                              int T, int d, int d_e, int d_head, float* P, hipStream_t s);
+
+struct RouterTailArgs {
+  int dtype;
+  int T, j, L_R;
+  int d_m, d_s, d_h, d_a, d_e, d_p, d_head;
+  float eps, T_hist, eta;
+  const float* P;         // [T][d_e + d_head]
+  const float* rowstat;   // [T][4]
+  const void *w_hu, *w_p1, *w_p2, *w_q, *w_k, *w_v, *w_n, *w_c, *th1, *th2, *ps2;
+  const float* beta;      // [T] or null
+  float* S;               // [T][d_m][d_m]   in/out
+  float* zeta;            // [T][d_m]        in/out
+  float* p_hist;          // [T]             in/out
+  float* m_hist;          // [T]             in/out
+  float* logit;           // [T]
+  float* gate;            // [T]
+};
+hipError_t launch_router_tail(const RouterTailArgs& a, hipStream_t s);
+
+// Branch decision and ordered compaction (one workgroup).
+struct SelectArgs {
+  const float* logit;
+  int T;
+  int mode;        // 0 threshold, 1 budget
+  float thr;       // threshold mode: logit threshold
+  int n_skip;      // budget mode
+  uint8_t* mask;
+  int* idx_ffn;
+  int* idx_ad;
+  int* counts;     // [2]
+  float* lambda;   // [1]
+};
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+
+// FFN branch: act = SiLU(W_g u) * (W_u u) over gathered rows, then
+// h_out[t] = hbar[t] + g[t] * (W_d act) for t in idx_ffn.
+hipError_t launch_ffn(int dtype, const void* u, const int* idx_ffn, const int* counts, int n_max,
+                      const void* w_gate, const void* w_up, const void* w_down, void* act,
+                      const void* hbar, const float* gate, void* h_out, int d, int d_ff,
+                      hipStream_t s);
+
+// Adapter branch: h_out[t] = hbar[t] + (1 - g[t]) * W_2 SiLU(W_1 u) for t in idx_ad.
+// part: fp32 scratch of adapter_part_floats(d, d_r, T).
+size_t adapter_part_floats(int dtype, int d, int d_r, int T);
+hipError_t launch_adapter(int dtype, const void* u, const int* idx_ad, const int* counts, int n_max,
+                          const void* w1, const void* w2, float* part, const void* hbar,
+                          const float* gate, void* h_out, int d, int d_r, hipStream_t s);
+
+}  // namespace hero

@@ -1,0 +1,560 @@
+// Dense contractions of the routed layer.
+//
+//   router pre-activations   P = hbar [W_hd; psi_1]^T                 (Sec. 3.2, z^h and f_psi)
+//   FFN gate/up              act = SiLU(u W_g^T) * (u W_u^T)          (frozen SwiGLU FFN)
+//   FFN down + scatter       h_out[t] = hbar[t] + g_t (act W_d^T)     (Sec. 3.1, eq:ffn_route)
+//   adapter down             hid = SiLU(u W_1^T)                      (Sec. 3.1, adapter)
+//   adapter up + scatter     h_out[t] = hbar[t] + (1 - g_t) (hid W_2^T)
+//
+// bf16 path: v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  A and B are both
+// K-contiguous ("x W^T" with nn.Linear weights).  A k-tile of 64 elements
+// (128 bytes per row) of A and B is staged through LDS, double buffered, with
+// the 16-byte chunks of each row XOR-swizzled by (row & 7) so that the 32-row
+// fragment reads of one MFMA hit distinct banks.  A rows may be gathered through
+// an index list whose length lives on the device (tiles past it exit at once).
+// Workgroups are mapped to tiles so that each XCD (8 per MI355X, round-robin
+// dispatch) owns a contiguous run of tiles that share weight panels in its L2.
+//
+// f32 path: a plain LDS-tiled VALU GEMM with full bounds checks (small shapes).
+#include <limits.h>
+
+#include "hero_device.h"
+#include "hero_kernels.h"
+
+namespace hero {
+namespace {
+
+constexpr int BK = 64;     // k elements per tile
+constexpr int ROWB = 128;  // bytes of one row of a bf16 k-tile
+
+__device__ __forceinline__ int swz(int row, int ch) { return row * ROWB + ((ch ^ (row & 7)) << 4); }
+
+template <int BM_, int BN_, int WM_, int WN_, bool DUAL_>
+struct Tile {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+  static constexpr bool DUAL = DUAL_;
+  static constexpr int NT = 64 * WM * WN;
+  static constexpr int WTM = BM / WM, WTN = BN / WN;
+  static constexpr int TM = WTM / 32, TN = WTN / 32;
+  static constexpr int A_CH = BM * 8 / NT, B_CH = BN * 8 / NT;
+  static constexpr int STAGE = (BM + BN) * ROWB;
+  static constexpr int OUT_N = DUAL ? BN / 2 : BN;  // output columns per tile
+  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole MFMA tiles");
+  static_assert(!DUAL || TN % 2 == 0, "gate/up tiles come in pairs");
+  static_assert((BM * 8) % NT == 0 && (BN * 8) % NT == 0, "loader split");
+};
+
+template <typename T>
+struct ARows {
+  const T* base;
+  const int* idx;  // null: identity
+  int ld;
+  __device__ __forceinline__ const T* row(int m) const {
+    return base + static_cast<size_t>(idx ? idx[m] : m) * ld;
+  }
+};
+
+// B rows: [0, split) from b0, [split, ...) from b1 (router: W_hd then psi_1);
+// for the gate/up product b0 = W_g, b1 = W_u and rows are addressed by column.
+template <typename T>
+struct BRows {
+  const T* b0;
+  const T* b1;
+  int split;
+  int ld;
+  __device__ __forceinline__ const T* row(int n) const {
+    return n < split ? b0 + static_cast<size_t>(n) * ld : b1 + static_cast<size_t>(n - split) * ld;
+  }
+  __device__ __forceinline__ const T* gate_row(int c) const { return b0 + static_cast<size_t>(c) * ld; }
+  __device__ __forceinline__ const T* up_row(int c) const { return b1 + static_cast<size_t>(c) * ld; }
+};
+
+// ---------------------------------------------------------------------------
+// epilogues
+// ---------------------------------------------------------------------------
+
+struct EpiStoreF32 {  // P[m][n] = acc
+  float* out;
+  int ld;
+  __device__ __forceinline__ void store(int m, int n, float v) const {
+    out[static_cast<size_t>(m) * ld + n] = v;
+  }
+};
+
+template <typename T>
+struct EpiSwiGLU {  // act[m][c] = SiLU(gate) * up
+  T* act;
+  int ld;
+  __device__ __forceinline__ void store2(int m, int c, float g, float u) const {
+    stf(act + static_cast<size_t>(m) * ld + c, siluf_(g) * u);
+  }
+};
+
+template <typename T>
+struct EpiSiLU {  // hid[m][n] = SiLU(acc)
+  T* out;
+  int ld;
+  __device__ __forceinline__ void store(int m, int n, float v) const {
+    stf(out + static_cast<size_t>(m) * ld + n, siluf_(v));
+  }
+};
+
+// h_out[t][n] = hbar[t][n] + scale(g_t) * acc, t = idx[m]; FFN scales by g, adapter by 1 - g.
+template <typename T, bool ADAPTER>
+struct EpiScatter {
+  const int* idx;
+  const T* hbar;
+  const float* gate;
+  T* out;
+  int ld;
+  __device__ __forceinline__ void store(int m, int n, float v) const {
+    const int t = idx[m];
+    const float g = gate[t];
+    const float sc = ADAPTER ? 1.0f - g : g;
+    const size_t o = static_cast<size_t>(t) * ld + n;
+    stf(out + o, ldf(hbar + o) + sc * v);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA GEMM
+// ---------------------------------------------------------------------------
+
+template <class C, class Epi>
+__global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi,
+                                                  const int* __restrict__ m_count, int M_fixed,
+                                                  int K, int mt_max, int n_tiles) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE];
+  const int per = gridDim.x >> 3;
+  const int tile = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+  if (tile >= mt_max * n_tiles) return;
+  const int mt = tile % mt_max, nt = tile / mt_max;
+  const int M = m_count ? *m_count : M_fixed;
+  const int m0 = mt * C::BM;
+  if (m0 >= M) return;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / C::WN, wn = wave % C::WN;
+
+  // per-thread global sources and LDS destinations of the 16-byte chunks it moves
+  const bf16_t* a_src[C::A_CH];
+  int a_dst[C::A_CH];
+#pragma unroll
+  for (int i = 0; i < C::A_CH; ++i) {
+    const int c = tid + i * C::NT, row = c >> 3, ch = c & 7;
+    const int m = min(m0 + row, M - 1);
+    a_src[i] = A.row(m) + ch * 8;
+    a_dst[i] = swz(row, ch);
+  }
+  const bf16_t* b_src[C::B_CH];
+  int b_dst[C::B_CH];
+#pragma unroll
+  for (int i = 0; i < C::B_CH; ++i) {
+    const int c = tid + i * C::NT, row = c >> 3, ch = c & 7;
+    const bf16_t* p;
+    if (C::DUAL) {
+      const int wb = row / C::WTN, q = row % C::WTN, h = C::WTN / 2;
+      const int col = nt * C::OUT_N + wb * h + (q % h);
+      p = (q < h) ? B.gate_row(col) : B.up_row(col);
+    } else {
+      p = B.row(nt * C::BN + row);
+    }
+    b_src[i] = p + ch * 8;
+    b_dst[i] = C::BM * ROWB + swz(row, ch);
+  }
+
+  u32x4 ra[C::A_CH], rb[C::B_CH];
+  f32x16 acc[C::TM][C::TN];
+#pragma unroll
+  for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+    for (int b = 0; b < C::TN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  const int nk = K / BK;
+#pragma unroll
+  for (int i = 0; i < C::A_CH; ++i) ra[i] = *reinterpret_cast<const u32x4*>(a_src[i]);
+#pragma unroll
+  for (int i = 0; i < C::B_CH; ++i) rb[i] = *reinterpret_cast<const u32x4*>(b_src[i]);
+#pragma unroll
+  for (int i = 0; i < C::A_CH; ++i) *reinterpret_cast<u32x4*>(smem + a_dst[i]) = ra[i];
+#pragma unroll
+  for (int i = 0; i < C::B_CH; ++i) *reinterpret_cast<u32x4*>(smem + b_dst[i]) = rb[i];
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const bool more = kt + 1 < nk;
+    if (more) {
+      const int k1 = (kt + 1) * BK;
+#pragma unroll
+      for (int i = 0; i < C::A_CH; ++i) ra[i] = *reinterpret_cast<const u32x4*>(a_src[i] + k1);
+#pragma unroll
+      for (int i = 0; i < C::B_CH; ++i) rb[i] = *reinterpret_cast<const u32x4*>(b_src[i] + k1);
+    }
+    const unsigned char* sa = smem + (kt & 1) * C::STAGE;
+    const unsigned char* sb = sa + C::BM * ROWB;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int ch = 2 * ks + (lane >> 5);
+      bf16x8 fa[C::TM], fb[C::TN];
+#pragma unroll
+      for (int a = 0; a < C::TM; ++a) {
+        const int row = wm * C::WTM + a * 32 + (lane & 31);
+        fa[a] = *reinterpret_cast<const bf16x8*>(sa + swz(row, ch));
+      }
+#pragma unroll
+      for (int b = 0; b < C::TN; ++b) {
+        const int row = wn * C::WTN + b * 32 + (lane & 31);
+        fb[b] = *reinterpret_cast<const bf16x8*>(sb + swz(row, ch));
+      }
+#pragma unroll
+      for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+        for (int b = 0; b < C::TN; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+    }
+    if (more) {
+      unsigned char* nxt = smem + ((kt + 1) & 1) * C::STAGE;
+#pragma unroll
+      for (int i = 0; i < C::A_CH; ++i) *reinterpret_cast<u32x4*>(nxt + a_dst[i]) = ra[i];
+#pragma unroll
+      for (int i = 0; i < C::B_CH; ++i) *reinterpret_cast<u32x4*>(nxt + b_dst[i]) = rb[i];
+    }
+    __syncthreads();
+  }
+
+  // epilogue: D[i][j] of an MFMA tile sits in lane j + 32*((i/4)&1), register 4*(i/8) + i%4
+#pragma unroll
+  for (int a = 0; a < C::TM; ++a) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = wm * C::WTM + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      const int m = m0 + i;
+      if (m >= M) continue;
+      if constexpr (C::DUAL) {
+#pragma unroll
+        for (int b = 0; b < C::TN / 2; ++b) {
+          const int c = nt * C::OUT_N + wn * (C::WTN / 2) + b * 32 + (lane & 31);
+          epi.store2(m, c, acc[a][b][r], acc[a][b + C::TN / 2][r]);
+        }
+      } else {
+#pragma unroll
+        for (int b = 0; b < C::TN; ++b) {
+          const int n = nt * C::BN + wn * C::WTN + b * 32 + (lane & 31);
+          epi.store(m, n, acc[a][b][r]);
+        }
+      }
+    }
+  }
+}
+
+template <class C, class Epi>
+hipError_t run_mfma(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_count, int M_max,
+                    int N_out, int K, hipStream_t s) {
+  const int mt_max = (M_max + C::BM - 1) / C::BM;
+  const int n_tiles = N_out / C::OUT_N;
+  const int total = mt_max * n_tiles;
+  if (total == 0) return hipSuccess;
+  const int grid = (total + 7) / 8 * 8;
+  mfma_gemm<C, Epi><<<grid, C::NT, 0, s>>>(A, B, epi, m_count, M_max, K, mt_max, n_tiles);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// fp32 VALU GEMM (64 x 64 tile, 4 x 4 outputs per thread, full bounds checks)
+// ---------------------------------------------------------------------------
+
+template <bool DUAL, class Epi>
+__global__ __launch_bounds__(256) void f32_gemm(ARows<float> A, BRows<float> B, Epi epi,
+                                               const int* __restrict__ m_count, int M_fixed,
+                                               int N, int K) {
+  __shared__ float As[16][68];
+  __shared__ float Bs[16][68];
+  __shared__ float Us[DUAL ? 16 : 1][68];
+  const int M = m_count ? *m_count : M_fixed;
+  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  if (m0 >= M) return;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  float acc[4][4], acu[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = acu[i][j] = 0.f;
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    for (int e = threadIdx.x; e < 64 * 16; e += 256) {
+      const int r = e >> 4, kk = e & 15, k = k0 + kk;
+      const int m = m0 + r, n = n0 + r;
+      As[kk][r] = (m < M && k < K) ? A.row(m)[k] : 0.f;
+      if (DUAL) {
+        Bs[kk][r] = (n < N && k < K) ? B.gate_row(n)[k] : 0.f;
+        Us[kk][r] = (n < N && k < K) ? B.up_row(n)[k] : 0.f;
+      } else {
+        Bs[kk][r] = (n < N && k < K) ? B.row(n)[k] : 0.f;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4], u[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = As[kk][ty * 4 + i];
+        b[i] = Bs[kk][tx * 4 + i];
+        if (DUAL) u[i] = Us[kk][tx * 4 + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+          if (DUAL) acu[i][j] = fmaf(a[i], u[j], acu[i][j]);
+        }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + ty * 4 + i;
+    if (m >= M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + tx * 4 + j;
+      if (n >= N) continue;
+      if constexpr (DUAL) {
+        epi.store2(m, n, acc[i][j], acu[i][j]);
+      } else {
+        epi.store(m, n, acc[i][j]);
+      }
+    }
+  }
+}
+
+template <bool DUAL, class Epi>
+hipError_t run_f32(ARows<float> A, BRows<float> B, Epi epi, const int* m_count, int M_max, int N,
+                   int K, hipStream_t s) {
+  if (M_max <= 0 || N <= 0) return hipSuccess;
+  dim3 grid((N + 63) / 64, (M_max + 63) / 64);
+  f32_gemm<DUAL, Epi><<<grid, 256, 0, s>>>(A, B, epi, m_count, M_max, N, K);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// bf16 adapter: skinny GEMMs with MFMA fragments loaded straight from memory
+// ---------------------------------------------------------------------------
+
+// Adapter down-projection partial sums.  Workgroup (row tile of 32, k-group g) has
+// 4 waves, each over a quarter of the group's k range; the 4 partial 32 x d_r
+// tiles are summed in LDS and written to part[g][m][n] (fp32).
+template <int TN>
+__global__ __launch_bounds__(256) void adapter_down_bf16(const bf16_t* __restrict__ u,
+                                                         const int* __restrict__ idx,
+                                                         const int* __restrict__ m_count,
+                                                         const bf16_t* __restrict__ w1,
+                                                         float* __restrict__ part, int T, int K,
+                                                         int k_group) {
+  constexpr int R = TN * 32;
+  __shared__ float red[4][32][R + 1];
+  const int M = *m_count;
+  const int m0 = blockIdx.x * 32;
+  if (m0 >= M) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = blockIdx.y;
+  const int kw = k_group / 4;
+  const int kbeg = g * k_group + wave * kw;
+  const int m = min(m0 + (lane & 31), M - 1);
+  const bf16_t* arow = u + static_cast<size_t>(idx[m]) * K + 8 * (lane >> 5);
+  f32x16 acc[TN];
+#pragma unroll
+  for (int b = 0; b < TN; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
+  for (int k = kbeg; k < kbeg + kw; k += 16) {
+    const bf16x8 fa = *reinterpret_cast<const bf16x8*>(arow + k);
+#pragma unroll
+    for (int b = 0; b < TN; ++b) {
+      const bf16x8 fb = *reinterpret_cast<const bf16x8*>(
+          w1 + static_cast<size_t>(b * 32 + (lane & 31)) * K + 8 * (lane >> 5) + k);
+      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, acc[b], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < TN; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      red[wave][i][b * 32 + (lane & 31)] = acc[b][r];
+    }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 32 * R; e += 256) {
+    const int i = e / R, n = e % R;
+    if (m0 + i >= M) continue;
+    const float v = red[0][i][n] + red[1][i][n] + red[2][i][n] + red[3][i][n];
+    part[(static_cast<size_t>(g) * T + m0 + i) * R + n] = v;
+  }
+}
+
+// Adapter up-projection with scatter: hid = SiLU(sum_g part[g]) rounded to bf16 as the
+// MFMA A operand; workgroup (row tile of 32, column tile of 256), wave = 64 columns.
+template <int KR>
+__global__ __launch_bounds__(256) void adapter_up_bf16(const float* __restrict__ part, int G,
+                                                       const int* __restrict__ idx,
+                                                       const int* __restrict__ m_count,
+                                                       const bf16_t* __restrict__ w2,
+                                                       const bf16_t* __restrict__ hbar,
+                                                       const float* __restrict__ gate,
+                                                       bf16_t* __restrict__ out, int T, int d) {
+  const int M = *m_count;
+  const int m0 = blockIdx.x * 32;
+  if (m0 >= M) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.y * 256 + wave * 64;
+  const int mr = min(m0 + (lane & 31), M - 1);
+  f32x16 acc[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
+#pragma unroll
+  for (int k = 0; k < KR; k += 16) {
+    const int kk = k + 8 * (lane >> 5);
+    float h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = 0.f;
+    for (int g = 0; g < G; ++g) {
+      const float* p = part + (static_cast<size_t>(g) * T + mr) * KR + kk;
+      const f32x4 x0 = *reinterpret_cast<const f32x4*>(p);
+      const f32x4 x1 = *reinterpret_cast<const f32x4*>(p + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        h[e] += x0[e];
+        h[4 + e] += x1[e];
+      }
+    }
+    bf16x8 fa;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) fa[e] = static_cast<__bf16>(siluf_(h[e]));
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const bf16x8 fb = *reinterpret_cast<const bf16x8*>(
+          w2 + static_cast<size_t>(n0 + b * 32 + (lane & 31)) * KR + kk);
+      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, acc[b], 0, 0, 0);
+    }
+  }
+  EpiScatter<bf16_t, true> epi{idx, hbar, gate, out, d};
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int m = m0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    if (m >= M) continue;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) epi.store(m, n0 + b * 32 + (lane & 31), acc[b][r]);
+  }
+}
+
+int adapter_groups(int K) {
+  int G = 1;
+  while (K % (2 * G * 64) == 0 && K / (2 * G) >= 1024) G *= 2;
+  return G;
+}
+
+// tile shapes
+using TileRouter = Tile<64, 128, 2, 2, false>;
+using TileGateUp = Tile<256, 256, 2, 2, true>;
+using TileDown = Tile<256, 256, 2, 2, false>;
+
+}  // namespace
+
+hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, const void* ps1, int T,
+                              int d, int d_e, int d_head, float* P, hipStream_t s) {
+  const int N = d_e + d_head;
+  EpiStoreF32 epi{P, N};
+  if (dtype == 1) {
+    ARows<bf16_t> A{static_cast<const bf16_t*>(hbar), nullptr, d};
+    BRows<bf16_t> B{static_cast<const bf16_t*>(w_hd), static_cast<const bf16_t*>(ps1), d_e, d};
+    return run_mfma<TileRouter>(A, B, epi, nullptr, T, N, d, s);
+  }
+  ARows<float> A{static_cast<const float*>(hbar), nullptr, d};
+  BRows<float> B{static_cast<const float*>(w_hd), static_cast<const float*>(ps1), d_e, d};
+  return run_f32<false>(A, B, epi, nullptr, T, N, d, s);
+}
+
+hipError_t launch_ffn(int dtype, const void* u, const int* idx_ffn, const int* counts, int n_max,
+                      const void* w_gate, const void* w_up, const void* w_down, void* act,
+                      const void* hbar, const float* gate, void* h_out, int d, int d_ff,
+                      hipStream_t s) {
+  if (n_max <= 0) return hipSuccess;
+  hipError_t e;
+  if (dtype == 1) {
+    ARows<bf16_t> A{static_cast<const bf16_t*>(u), idx_ffn, d};
+    BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), INT_MAX, d};
+    e = run_mfma<TileGateUp>(A, B, EpiSwiGLU<bf16_t>{static_cast<bf16_t*>(act), d_ff}, counts,
+                             n_max, d_ff, d, s);
+    if (e != hipSuccess) return e;
+    ARows<bf16_t> A2{static_cast<const bf16_t*>(act), nullptr, d_ff};
+    BRows<bf16_t> B2{static_cast<const bf16_t*>(w_down), nullptr, INT_MAX, d_ff};
+    EpiScatter<bf16_t, false> epi{idx_ffn, static_cast<const bf16_t*>(hbar), gate,
+                                  static_cast<bf16_t*>(h_out), d};
+    return run_mfma<TileDown>(A2, B2, epi, counts, n_max, d, d_ff, s);
+  }
+  ARows<float> A{static_cast<const float*>(u), idx_ffn, d};
+  BRows<float> B{static_cast<const float*>(w_gate), static_cast<const float*>(w_up), INT_MAX, d};
+  e = run_f32<true>(A, B, EpiSwiGLU<float>{static_cast<float*>(act), d_ff}, counts, n_max, d_ff, d, s);
+  if (e != hipSuccess) return e;
+  ARows<float> A2{static_cast<const float*>(act), nullptr, d_ff};
+  BRows<float> B2{static_cast<const float*>(w_down), nullptr, INT_MAX, d_ff};
+  EpiScatter<float, false> epi{idx_ffn, static_cast<const float*>(hbar), gate,
+                               static_cast<float*>(h_out), d};
+  return run_f32<false>(A2, B2, epi, counts, n_max, d, d_ff, s);
+}
+
+size_t adapter_part_floats(int dtype, int d, int d_r, int T) {
+  const int G = dtype == 1 ? adapter_groups(d) : 1;
+  return static_cast<size_t>(G) * T * d_r;
+}
+
+hipError_t launch_adapter(int dtype, const void* u, const int* idx_ad, const int* counts, int n_max,
+                          const void* w1, const void* w2, float* part, const void* hbar,
+                          const float* gate, void* h_out, int d, int d_r, hipStream_t s) {
+  if (n_max <= 0) return hipSuccess;
+  if (dtype == 1) {
+    const int G = adapter_groups(d);
+    const int K = d;
+    dim3 g1((n_max + 31) / 32, G);
+    const bf16_t* uu = static_cast<const bf16_t*>(u);
+    const bf16_t* ww1 = static_cast<const bf16_t*>(w1);
+    // the adapter rank is a compile-time tile count (32-column MFMA tiles)
+    switch (d_r) {
+      case 32: adapter_down_bf16<1><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww1, part, n_max, K, K / G); break;
+      case 64: adapter_down_bf16<2><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww1, part, n_max, K, K / G); break;
+      case 96: adapter_down_bf16<3><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww1, part, n_max, K, K / G); break;
+      case 128: adapter_down_bf16<4><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww1, part, n_max, K, K / G); break;
+      default: return hipErrorInvalidValue;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dim3 g2((n_max + 31) / 32, d / 256);
+    const bf16_t* ww2 = static_cast<const bf16_t*>(w2);
+    const bf16_t* hb = static_cast<const bf16_t*>(hbar);
+    bf16_t* ho = static_cast<bf16_t*>(h_out);
+    switch (d_r) {
+      case 32: adapter_up_bf16<32><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww2, hb, gate, ho, n_max, d); break;
+      case 64: adapter_up_bf16<64><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww2, hb, gate, ho, n_max, d); break;
+      case 96: adapter_up_bf16<96><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww2, hb, gate, ho, n_max, d); break;
+      case 128: adapter_up_bf16<128><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww2, hb, gate, ho, n_max, d); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
+  // fp32: hid = SiLU(u W_1^T) into part[m][n], then the up-projection with scatter
+  ARows<float> A{static_cast<const float*>(u), idx_ad, d};
+  BRows<float> B{static_cast<const float*>(w1), nullptr, INT_MAX, d};
+  hipError_t e = run_f32<false>(A, B, EpiSiLU<float>{part, d_r}, counts, n_max, d_r, d, s);
+  if (e != hipSuccess) return e;
+  ARows<float> A2{part, nullptr, d_r};
+  BRows<float> B2{static_cast<const float*>(w2), nullptr, INT_MAX, d_r};
+  EpiScatter<float, true> epi{idx_ad, static_cast<const float*>(hbar), gate,
+                              static_cast<float*>(h_out), d};
+  return run_f32<false>(A2, B2, epi, counts, n_max, d, d_r, s);
+}
+
+}  // namespace hero

@@ -1,0 +1,131 @@
+"""Device-side harness: uploads a seeded problem with torch and drives the C ABI.
+
+torch supplies device memory and the stream; every step of the routed layer runs
+in libhero.so.  This module only allocates buffers, fills the ABI structs and
+copies results back for inspection.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional
+
+import numpy as np
+import torch
+
+from . import hero as H
+from . import synth
+
+
+def upload(t: synth.Tensor, device) -> torch.Tensor:
+    if t.dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(t.store).view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(t.store)).to(device)
+
+
+def download_f64(x: torch.Tensor) -> np.ndarray:
+    """Exact float64 values of a bf16 or fp32 device tensor."""
+    if x.dtype == torch.bfloat16:
+        return synth.bf16_bits_to_f64(x.view(torch.int16).cpu().numpy().view(np.uint16))
+    return x.float().cpu().numpy().astype(np.float64)
+
+
+def dims_struct(w: synth.Workload) -> H.hero_dims:
+    return H.hero_dims(d=w.d, d_ff=w.d_ff, d_r=w.d_r, L_R=w.L_R, d_m=w.d_m, d_s=w.d_s, d_h=w.d_h,
+                       d_a=w.d_a, d_e=w.d_e, d_p=w.d_p, d_head=w.d_head,
+                       dtype=H.HERO_BF16 if w.dtype == "bf16" else H.HERO_F32,
+                       eps_norm=w.eps_norm, eps=w.eps, T_hist=w.T_hist)
+
+
+class LayerStats:
+    """Per-layer device outputs of the ABI's optional stats."""
+
+    def __init__(self, T: int, device):
+        self.mask = torch.empty(T, dtype=torch.uint8, device=device)
+        self.idx_ffn = torch.empty(T, dtype=torch.int32, device=device)
+        self.idx_ad = torch.empty(T, dtype=torch.int32, device=device)
+        self.counts = torch.empty(4, dtype=torch.int32, device=device)
+        self.logit = torch.empty(T, dtype=torch.float32, device=device)
+        self.gate = torch.empty(T, dtype=torch.float32, device=device)
+        self.lam = torch.empty(4, dtype=torch.float32, device=device)
+        self.struct = H.hero_layer_stats(self.mask.data_ptr(), self.idx_ffn.data_ptr(),
+                                         self.idx_ad.data_ptr(), self.counts.data_ptr(),
+                                         self.logit.data_ptr(), self.gate.data_ptr(), self.lam.data_ptr())
+
+    def host(self) -> Dict[str, np.ndarray]:
+        c = self.counts.cpu().numpy()
+        return dict(mask=self.mask.cpu().numpy().astype(bool), idx_ffn=self.idx_ffn.cpu().numpy(),
+                    idx_ad=self.idx_ad.cpu().numpy(), n_ffn=int(c[0]), n_ad=int(c[1]),
+                    logit=self.logit.cpu().numpy(), gate=self.gate.cpu().numpy(),
+                    lam=float(self.lam.cpu().numpy()[0]))
+
+
+class DeviceProblem:
+    """A synth.Problem resident on the GPU with the ABI structs that point at it."""
+
+    def __init__(self, prob: synth.Problem, device: str = "cuda:0", stats: bool = True,
+                 for_stack: Optional[bool] = None):
+        w = prob.w
+        self.w = w
+        self.device = device
+        self.T = T = prob.hbar.shape[0]
+        self.dims = dims_struct(w)
+        self.hbar = upload(prob.hbar, device)
+        self.prev1 = upload(prob.hbar_prev1, device) if prob.hbar_prev1 is not None else None
+        self.prev2 = upload(prob.hbar_prev2, device) if prob.hbar_prev2 is not None else None
+        self.h_out = torch.empty_like(self.hbar)
+        self.router = {k: upload(v, device) for k, v in prob.router.items()}
+        self.router_s = H.hero_router_weights(**{k: self.router[k].data_ptr() for k in H.ROUTER_FIELDS})
+        self.ffn = [{k: upload(v, device) for k, v in layer.items()} for layer in prob.ffn]
+        self.ffn_s = [H.hero_ffn_weights(f["norm_w"].data_ptr(), f["w_gate"].data_ptr(),
+                                         f["w_up"].data_ptr(), f["w_down"].data_ptr()) for f in self.ffn]
+        self.adapter = [{k: upload(v, device) for k, v in layer.items()} for layer in prob.adapter]
+        self.adapter_s = [H.hero_adapter_weights(a["w1"].data_ptr(), a["w2"].data_ptr()) for a in self.adapter]
+        self.eta = [float(e) for e in prob.eta]
+        self.S = torch.from_numpy(prob.S).to(device)
+        self.zeta = torch.from_numpy(prob.zeta).to(device)
+        self.p_hist = torch.from_numpy(prob.p_hist).to(device)
+        self.m_hist = torch.from_numpy(prob.m_hist).to(device)
+        self.state_s = H.hero_state(self.S.data_ptr(), self.zeta.data_ptr(), self.p_hist.data_ptr(),
+                                    self.m_hist.data_ptr())
+        self.beta = torch.from_numpy(prob.beta).to(device) if prob.beta is not None else None
+        mode = H.HERO_MODE_BUDGET if w.mode == "budget" else H.HERO_MODE_THRESHOLD
+        self.routing_s = H.hero_routing(mode, w.tau, w.budget,
+                                        self.beta.data_ptr() if self.beta is not None else None)
+        n_layers = len(prob.ffn)
+        if for_stack is None:
+            for_stack = n_layers > 1
+        self.for_stack = for_stack
+        self.stats = [LayerStats(T, device) for _ in range(w.L_R if for_stack else 1)] if stats else None
+        self.ws_bytes = H.hero_workspace_size(self.dims, T, for_stack)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+
+    def stream(self):
+        return torch.cuda.current_stream(torch.device(self.device)).cuda_stream
+
+    def run_layer(self, j: int, layer: int = 0, check: bool = True) -> int:
+        st = H.hero_routed_layer(self.dims, j, self.T, self.hbar, self.prev1, self.prev2, self.h_out,
+                                 self.state_s, self.ffn_s[layer], self.router_s, self.adapter_s[layer],
+                                 self.eta[j - 1], self.routing_s,
+                                 self.stats[0].struct if self.stats else None,
+                                 self.ws, self.ws_bytes, self.stream())
+        if check:
+            H.check(st, "hero_routed_layer")
+        return st
+
+    def run_stack(self, check: bool = True) -> int:
+        st = H.hero_routed_stack(self.dims, self.T, self.hbar, self.h_out, self.state_s, self.ffn_s,
+                                 self.router_s, self.adapter_s, self.eta, self.routing_s,
+                                 [s.struct for s in self.stats] if self.stats else None,
+                                 self.ws, self.ws_bytes, self.stream())
+        if check:
+            H.check(st, "hero_routed_stack")
+        return st
+
+    def results(self) -> Dict[str, object]:
+        torch.cuda.synchronize()
+        out = dict(h=download_f64(self.h_out), S=self.S.cpu().numpy().astype(np.float64),
+                   zeta=self.zeta.cpu().numpy().astype(np.float64),
+                   p_hist=self.p_hist.cpu().numpy().astype(np.float64),
+                   m_hist=self.m_hist.cpu().numpy().astype(np.float64))
+        if self.stats:
+            out["layers"] = [s.host() for s in self.stats]
+        return out

@@ -1,0 +1,171 @@
+"""Python binding of libhero.so: the C ABI of include/hero.h, argument marshalling only.
+
+Every function here has the name of the C entry point it calls.  Pointer
+arguments accept a torch tensor (its data_ptr is passed), an int address, or
+None.  Nothing here computes any part of the routed layer; if the library has
+not been built, loading fails with an error instead of falling back to
+anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhero.so")
+
+HERO_OK = 0
+HERO_E_NULL = 1
+HERO_E_DIM = 2
+HERO_E_RANGE = 3
+HERO_E_DTYPE = 4
+HERO_E_ALIGN = 5
+HERO_E_ALIAS = 6
+HERO_E_WORKSPACE = 7
+HERO_E_UNSUPPORTED = 8
+HERO_E_LAUNCH = 9
+HERO_E_DEVICE = 10
+
+HERO_F32 = 0
+HERO_BF16 = 1
+HERO_MODE_THRESHOLD = 0
+HERO_MODE_BUDGET = 1
+
+_vp = ctypes.c_void_p
+
+
+class hero_dims(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int), ("d_ff", ctypes.c_int), ("d_r", ctypes.c_int), ("L_R", ctypes.c_int),
+                ("d_m", ctypes.c_int), ("d_s", ctypes.c_int), ("d_h", ctypes.c_int), ("d_a", ctypes.c_int),
+                ("d_e", ctypes.c_int), ("d_p", ctypes.c_int), ("d_head", ctypes.c_int),
+                ("dtype", ctypes.c_int),
+                ("eps_norm", ctypes.c_float), ("eps", ctypes.c_float), ("T_hist", ctypes.c_float)]
+
+
+class hero_ffn_weights(ctypes.Structure):
+    _fields_ = [("norm_w", _vp), ("w_gate", _vp), ("w_up", _vp), ("w_down", _vp)]
+
+
+class hero_adapter_weights(ctypes.Structure):
+    _fields_ = [("w1", _vp), ("w2", _vp)]
+
+
+ROUTER_FIELDS = ("w_hd", "w_hu", "w_p1", "w_p2", "w_q", "w_k", "w_v", "w_n", "w_c",
+                 "th1", "th2", "ps1", "ps2")
+
+
+class hero_router_weights(ctypes.Structure):
+    _fields_ = [(n, _vp) for n in ROUTER_FIELDS]
+
+
+class hero_state(ctypes.Structure):
+    _fields_ = [("S", _vp), ("zeta", _vp), ("p_hist", _vp), ("m_hist", _vp)]
+
+
+class hero_routing(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int), ("tau", ctypes.c_float), ("budget", ctypes.c_double),
+                ("logit_bias", _vp)]
+
+
+class hero_layer_stats(ctypes.Structure):
+    _fields_ = [("mask", _vp), ("idx_ffn", _vp), ("idx_ad", _vp), ("counts", _vp),
+                ("logit", _vp), ("gate", _vp), ("lambda_", _vp)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libhero.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.hero_status_string.restype = ctypes.c_char_p
+        L.hero_status_string.argtypes = [ctypes.c_int]
+        L.hero_abi_version.restype = ctypes.c_int
+        L.hero_abi_version.argtypes = []
+        L.hero_workspace_size.restype = ctypes.c_int
+        L.hero_workspace_size.argtypes = [P(hero_dims), ctypes.c_int, ctypes.c_int, P(ctypes.c_size_t)]
+        L.hero_routed_layer.restype = ctypes.c_int
+        L.hero_routed_layer.argtypes = [P(hero_dims), ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp,
+                                        P(hero_state), P(hero_ffn_weights), P(hero_router_weights),
+                                        P(hero_adapter_weights), ctypes.c_float, P(hero_routing),
+                                        P(hero_layer_stats), _vp, ctypes.c_size_t, _vp]
+        L.hero_routed_stack.restype = ctypes.c_int
+        L.hero_routed_stack.argtypes = [P(hero_dims), ctypes.c_int, _vp, _vp, P(hero_state),
+                                        P(hero_ffn_weights), P(hero_router_weights),
+                                        P(hero_adapter_weights), P(ctypes.c_float), P(hero_routing),
+                                        P(hero_layer_stats), _vp, ctypes.c_size_t, _vp]
+        _lib = L
+    return _lib
+
+
+def ptr(x) -> Optional[int]:
+    """Device address of a tensor, an int address, or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+class HeroError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {hero_status_string(status)} (status {status})")
+
+
+def check(status: int, where: str) -> None:
+    if status != HERO_OK:
+        raise HeroError(status, where)
+
+
+def hero_status_string(status: int) -> str:
+    return lib().hero_status_string(status).decode()
+
+
+def hero_abi_version() -> int:
+    return lib().hero_abi_version()
+
+
+def hero_workspace_size(dims: hero_dims, T: int, for_stack: bool) -> int:
+    out = ctypes.c_size_t(0)
+    check(lib().hero_workspace_size(ctypes.byref(dims), T, int(bool(for_stack)), ctypes.byref(out)),
+          "hero_workspace_size")
+    return out.value
+
+
+def _byref(s):
+    return None if s is None else ctypes.byref(s)
+
+
+def hero_routed_layer(dims: hero_dims, j: int, T: int, hbar, hbar_prev1, hbar_prev2, h_out,
+                      state: hero_state, ffn: hero_ffn_weights, router: hero_router_weights,
+                      adapter: hero_adapter_weights, eta: float, routing: hero_routing,
+                      stats: Optional[hero_layer_stats], workspace, workspace_bytes: int,
+                      stream=None) -> int:
+    """Enqueue one routed layer; returns the hero_status code."""
+    return lib().hero_routed_layer(ctypes.byref(dims), j, T, ptr(hbar), ptr(hbar_prev1), ptr(hbar_prev2),
+                                   ptr(h_out), _byref(state), _byref(ffn), _byref(router), _byref(adapter),
+                                   float(eta), _byref(routing), _byref(stats), ptr(workspace),
+                                   int(workspace_bytes), stream)
+
+
+def hero_routed_stack(dims: hero_dims, T: int, h_in, h_out, state: hero_state,
+                      ffn: Sequence[hero_ffn_weights], router: hero_router_weights,
+                      adapter: Sequence[hero_adapter_weights], eta: Sequence[float],
+                      routing: hero_routing, stats: Optional[Sequence[hero_layer_stats]],
+                      workspace, workspace_bytes: int, stream=None) -> int:
+    """Enqueue the whole routed stack; returns the hero_status code."""
+    L = len(ffn)
+    ffn_arr = (hero_ffn_weights * L)(*ffn)
+    ad_arr = (hero_adapter_weights * L)(*adapter)
+    eta_arr = (ctypes.c_float * L)(*[float(e) for e in eta])
+    st_arr = None if stats is None else (hero_layer_stats * L)(*stats)
+    return lib().hero_routed_stack(ctypes.byref(dims), T, ptr(h_in), ptr(h_out), _byref(state), ffn_arr,
+                                   _byref(router), ad_arr, eta_arr, _byref(routing), st_arr,
+                                   ptr(workspace), int(workspace_bytes), stream)
