@@ -1,0 +1,294 @@
+#!/usr/bin/env python3
+"""Throughput of the HeRo routed FFN hot path on one MI355X.
+
+A step is one hero_routed_layer call (router pre-pass, fused router tail with
+the memory read-modify-write, branch decision and compaction, gathered SwiGLU
+FFN, adapter, scatter) over the whole token batch of the workload, with every
+input already resident in HBM.  Default workload: Llama-3.1-8B shape, one
+routed layer (j = 17 of 32, synthesized incoming router state), bf16, 4096
+prefill tokens, skip budget 26.87 %.
+
+Prints one JSON line.  The dominant kernel (the FFN gate/up GEMM) is timed live
+inside the timed region with HIP events recorded around its launches; a second,
+untimed pass instruments every kernel for the per-kernel table.  The CPU
+baseline times the float64 oracle on a bounded token sample of the same inputs.
+"""
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector / MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+class HipEvents:
+    """hipEvent_t handles through the HIP runtime already loaded by torch."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+
+    def create(self, n):
+        out = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            assert self.hip.hipEventCreate(ctypes.byref(e)) == 0
+            out.append(e.value)
+        return out
+
+    def record(self, ev, stream):
+        assert self.hip.hipEventRecord(ev, stream) == 0
+
+    def elapsed_ms(self, a, b):
+        f = ctypes.c_float()
+        assert self.hip.hipEventSynchronize(b) == 0
+        assert self.hip.hipEventElapsedTime(ctypes.byref(f), a, b) == 0
+        return f.value
+
+    def destroy(self, evs):
+        for e in evs:
+            self.hip.hipEventDestroy(e)
+
+
+def kernel_work(w, n_f, n_a, T, j):
+    """Algorithmic FLOPs and HBM bytes per launch of each kernel (bf16 I/O, fp32 state)."""
+    es = 2 if w.dtype == "bf16" else 4
+    d, dff, r, dm = w.d, w.d_ff, w.d_r, w.d_m
+    npre = w.d_e + w.d_head
+    hid_reads = 1 + (j >= 2) + (j >= 3)
+    state_rw = (2 if j > 1 else 1) * 4 * (dm * dm + dm)
+    return {
+        "rowstats": dict(flops=0, bytes=T * (hid_reads * d * es + d * es + 16)),
+        "router_gemm": dict(flops=2 * d * npre * T, bytes=T * (d * es + 4 * npre)),
+        "router_tail": dict(flops=0, bytes=T * (state_rw + 4 * npre + 16 + 8 * 2 + 8)),
+        "select": dict(flops=0, bytes=T * (4 + 1 + 4)),
+        "ffn_gate_up": dict(flops=4 * d * dff * n_f, bytes=n_f * (d * es + dff * es) + 2 * d * dff * es),
+        "ffn_down": dict(flops=2 * d * dff * n_f, bytes=n_f * (dff * es + 2 * d * es) + d * dff * es),
+        "adapter_down": dict(flops=2 * d * r * n_a, bytes=n_a * d * es + r * d * es),
+        "adapter_up": dict(flops=2 * d * r * n_a, bytes=n_a * 2 * d * es + r * d * es),
+    }
+
+
+def describe(w, j):
+    return (f"{w.name}: d={w.d}, d_ff={w.d_ff}, adapter rank {w.d_r}, memory dim {w.d_m}, "
+            f"T={w.T} tokens ({w.batch}x{w.seq}), routed layer j={j} of {w.L_R}, "
+            + (f"skip budget {w.budget}" if w.mode == "budget" else f"threshold tau={w.tau}"))
+
+
+def cpu_baseline(prob, gpu_stats, j, target_s=12.0, max_tokens=None):
+    """Time the float64 oracle on a growing token sample until it runs >= target_s."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import hero_oracle as O
+    from tests.oracle_inputs import adapter_of, dims_of, ffn_of, router_of
+
+    w = prob.w
+    T = prob.hbar.shape[0]
+    max_tokens = T if max_tokens is None else min(T, max_tokens)
+    dims, R = dims_of(w), router_of(prob)
+    F, A = ffn_of(prob.ffn[0]), adapter_of(prob.adapter[0])
+    hb = prob.hbar.f64
+    hp1 = prob.hbar_prev1.f64 if prob.hbar_prev1 is not None else None
+    hp2 = prob.hbar_prev2.f64 if prob.hbar_prev2 is not None else None
+    n = 64
+    while True:
+        rows = np.linspace(0, T - 1, n).astype(np.int64)
+        st = O.State(prob.S[rows].astype("f8"), prob.zeta[rows].astype("f8"),
+                     prob.p_hist[rows].astype("f8"), prob.m_hist[rows].astype("f8"))
+        beta = None if prob.beta is None else prob.beta[rows].astype("f8")
+        lam = gpu_stats["lam"] if w.mode == "budget" else None
+        t0 = time.perf_counter()
+        O.routed_layer(j, dims, hb[rows], None if hp1 is None else hp1[rows],
+                       None if hp2 is None else hp2[rows], st, F, R, A, float(prob.eta[j - 1]),
+                       mode=w.mode, budget=w.budget, tau=w.tau, beta=beta,
+                       forced_ffn=gpu_stats["mask"][rows], lam_given=lam)
+        dt = time.perf_counter() - t0
+        if dt >= target_s or n >= max_tokens:
+            break
+        n = min(max_tokens, max(2 * n, int(n * target_s / max(dt, 1e-3) * 1.1)))
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": n / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} of {T} tokens of the same layer call (router, memory, branch; float64 numpy, "
+                      f"branch decisions teacher-forced to the GPU's), {dt:.1f} s"}
+
+
+def _short(name):
+    return name.replace("hero::(anonymous namespace)::", "").replace("void ", "")[:150].replace("|", "/")
+
+
+def summarize_rocprof(root):
+    """Markdown summary of rocprofv3 CSV files (kernel stats and/or counter collection) under root.
+
+    Counter tables give the mean per dispatch of each kernel; for the plain device
+    copy (the runtime's copyBuffer kernel) the largest dispatch is shown, which is
+    the calibration copy of known size.
+    """
+    import csv
+    import glob
+    stats = sorted(glob.glob(os.path.join(root, "**", "*kernel_stats.csv"), recursive=True))
+    for path in stats:
+        print(f"### kernel stats ({os.path.relpath(path, root)})\n")
+        print("| kernel | calls | total ms | avg us | min us | max us | % |")
+        print("|---|---|---|---|---|---|---|")
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                print(f"| {_short(r['Name'])} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
+                      f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                      f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+        print()
+    counters = sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True))
+    for path in counters:
+        agg = {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                key = (r["Kernel_Name"], r["Counter_Name"])
+                agg.setdefault(key, []).append(float(r["Counter_Value"]))
+        print(f"### counters ({os.path.relpath(path, root)}), KiB per dispatch as reported\n")
+        print("| kernel | counter | dispatches | mean | max |")
+        print("|---|---|---|---|---|")
+        for (k, c), v in sorted(agg.items()):
+            print(f"| {_short(k)} | {c} | {len(v)} | {sum(v) / len(v):.1f} | {max(v):.1f} |")
+        print()
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama31_8b_layer")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-target-s", type=float, default=12.0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run a plain device-to-device copy of this many MiB (HBM counter calibration)")
+    ap.add_argument("--summarize", metavar="DIR",
+                    help="print a summary of rocprofv3 CSV output found under DIR and exit (no GPU)")
+    args = ap.parse_args()
+    if args.summarize:
+        summarize_rocprof(args.summarize)
+        return
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the routed FFN path shards over tokens with no "
+              f"communication in threshold mode, and multi-GPU runs are not part of this build "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2609_08189_amd import hero as H
+    from paper_2609_08189_amd import synth
+    from paper_2609_08189_amd.device import DeviceProblem
+
+    w = synth.WORKLOADS[args.workload]
+    if w.layer_j <= 0:
+        raise SystemExit(f"{args.workload} is a stack workload; this bench times single layer calls")
+    j = w.layer_j
+    print(f"# preparing {describe(w, j)}", file=sys.stderr, flush=True)
+    prob = synth.make_problem(w, seed=args.seed)
+    dp = DeviceProblem(prob, device="cuda:0", stats=True)
+    stream = dp.stream()
+    ev = HipEvents()
+
+    # one checked call with stats for the realized branch sizes (and the CPU baseline)
+    dp.run_layer(j)
+    torch.cuda.synchronize()
+    st0 = dp.stats[0].host()
+    n_f, n_a = st0["n_ffn"], st0["n_ad"]
+    # the timed steps run without the optional stats outputs
+    stats_saved, dp.stats = dp.stats, None
+
+    for _ in range(args.warmup):
+        dp.run_layer(j)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    dom = "ffn_gate_up"
+    ks, ke = ev.create(K), ev.create(K)
+    H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
+    t_start, t_stop = ev.create(2)
+    torch.cuda.synchronize()
+    ev.record(t_start, stream)
+    for _ in range(K):
+        dp.run_layer(j)
+    ev.record(t_stop, stream)
+    torch.cuda.synchronize()
+    H.hero_kernel_timer(H.HERO_K[dom], [], [])
+    total_ms = ev.elapsed_ms(t_start, t_stop)
+    dom_ms = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
+    ms_step = total_ms / K
+    print(f"# timed {K} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
+
+    # per-kernel breakdown (untimed pass, every kernel instrumented)
+    per = {}
+    handles = {}
+    for name in H.KERNELS:
+        a, b = ev.create(K), ev.create(K)
+        handles[name] = (a, b)
+        H.hero_kernel_timer(H.HERO_K[name], a, b)
+    for _ in range(K):
+        dp.run_layer(j)
+    torch.cuda.synchronize()
+    work = kernel_work(w, n_f, n_a, w.T, j)
+    for name in H.KERNELS:
+        H.hero_kernel_timer(H.HERO_K[name], [], [])
+        a, b = handles[name]
+        launched = (name.startswith("ffn") and n_f > 0) or (name.startswith("adapter") and n_a > 0) or \
+            not (name.startswith("ffn") or name.startswith("adapter"))
+        if launched:
+            us = 1000.0 * sum(ev.elapsed_ms(x, y) for x, y in zip(a, b)) / K
+            wk = work[name]
+            per[name] = {"us": round(us, 2),
+                         "tflops": round(wk["flops"] / us * 1e-6, 1) if wk["flops"] else None,
+                         "gbs": round(wk["bytes"] / us * 1e-3, 1)}
+        ev.destroy(a + b)
+
+    tokens_per_s = w.T / (ms_step * 1e-3)
+    dflops = work[dom]["flops"]
+    achieved = dflops / (dom_ms * 1e-3) * 1e-12
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": None, "kernel": dom,
+            "avg_launch_us": round(dom_ms * 1e3, 2),
+            "work_per_launch": f"4*d*d_ff FLOP per FFN token x {n_f} FFN tokens = {dflops / 1e9:.1f} GFLOP"}
+
+    result = {
+        "metric": "routed-FFN-stack tokens/sec at Llama-3.1-8B shape; % MFMA/HBM roofline",
+        "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": describe(w, j), "global_batch": w.batch, "seq_len": w.seq,
+                   "tokens": w.T, "parallelism": "none", "n_ffn": n_f, "n_adapter": n_a},
+        "roofline": roof,
+        "kernels": per,
+    }
+    if not args.no_cpu_baseline:
+        dp.stats = stats_saved
+        print("# timing the CPU oracle on a token sample", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(prob, st0, j, target_s=args.cpu_target_s)
+    print(json.dumps(result), flush=True)
+    ev.destroy(ks + ke + [t_start, t_stop])
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"# calibration copy: {n} bytes read, {n} bytes written", file=sys.stderr, flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -142,6 +142,28 @@ typedef struct hero_layer_stats {
   float *logit, *gate, *lambda;
 } hero_layer_stats;
 
+/* Kernels of one routed layer, in launch order (for hero_kernel_timer). */
+typedef enum hero_kernel {
+  HERO_K_ROWSTATS = 0,      /* inv_rms, residual-transition sums, u = RMSNorm_w(hbar)        */
+  HERO_K_ROUTER_GEMM = 1,   /* [W_hd; psi_1] hbar                                             */
+  HERO_K_ROUTER_TAIL = 2,   /* router state, memory read-modify-write, heads, gate           */
+  HERO_K_SELECT = 3,        /* branch decision and ordered compaction                         */
+  HERO_K_FFN_GATE_UP = 4,   /* SiLU(W_g u) * (W_u u) over the FFN tokens                      */
+  HERO_K_FFN_DOWN = 5,      /* W_d act, scattered as hbar + g y                               */
+  HERO_K_ADAPTER_DOWN = 6,  /* W_1 u over the adapter tokens (partial sums)                   */
+  HERO_K_ADAPTER_UP = 7,    /* W_2 SiLU(.), scattered as hbar + (1 - g) y                     */
+  HERO_K_COUNT = 8
+} hero_kernel;
+
+/*
+ * Measurement hook.  While attached, every launch of `kernel` is bracketed by
+ * hipEventRecord(start_events[i]) and hipEventRecord(stop_events[i]) on the
+ * call's stream, with i cycling over the n_slots caller-created hipEvent_t
+ * handles (passed as void*).  n_slots = 0 detaches.  The registry is process
+ * global and must not be changed while routed calls are being enqueued.
+ */
+int hero_kernel_timer(int kernel, void *const *start_events, void *const *stop_events, int n_slots);
+
 /* Static string for a status code (host). */
 const char *hero_status_string(int status);
 

@@ -131,6 +131,29 @@ int check_device() {
   return ok ? HERO_OK : HERO_E_DEVICE;
 }
 
+// Measurement hook: caller-created events recorded around the launches of one kernel.
+struct KernelTimer {
+  hipEvent_t* start = nullptr;
+  hipEvent_t* stop = nullptr;
+  int n = 0;
+  int next = 0;
+};
+KernelTimer g_timer[HERO_K_COUNT];
+
+template <class F>
+hipError_t timed(int which, hipStream_t s, F&& launch) {
+  KernelTimer& k = g_timer[which];
+  if (k.n == 0) return launch();
+  const int i = k.next;
+  hipError_t e = hipEventRecord(k.start[i], s);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(k.stop[i], s);
+  k.next = (i + 1) % k.n;
+  return e;
+}
+
 struct LayerCall {
   const hero_dims* dims;
   int j, T;
@@ -166,11 +189,15 @@ int run_layer(const LayerCall& c) {
   float* P = reinterpret_cast<float*>(ws + L.P);
   float* rowstat = reinterpret_cast<float*>(ws + L.rowstat);
 
-  hipError_t e = launch_rowstats(D.dtype, c.hbar, c.j >= 2 ? c.prev1 : nullptr,
-                                 c.j >= 3 ? c.prev2 : nullptr, c.ffn->norm_w, T, D.d, c.j,
-                                 D.eps_norm, rowstat, u, c.stream);
+  const hipStream_t st = c.stream;
+  hipError_t e = timed(HERO_K_ROWSTATS, st, [&] {
+    return launch_rowstats(D.dtype, c.hbar, c.j >= 2 ? c.prev1 : nullptr, c.j >= 3 ? c.prev2 : nullptr,
+                           c.ffn->norm_w, T, D.d, c.j, D.eps_norm, rowstat, u, st);
+  });
   if (e != hipSuccess) return HERO_E_LAUNCH;
-  e = launch_router_gemm(D.dtype, c.hbar, c.rt->w_hd, c.rt->ps1, T, D.d, D.d_e, D.d_head, P, c.stream);
+  e = timed(HERO_K_ROUTER_GEMM, st, [&] {
+    return launch_router_gemm(D.dtype, c.hbar, c.rt->w_hd, c.rt->ps1, T, D.d, D.d_e, D.d_head, P, st);
+  });
   if (e != hipSuccess) return HERO_E_LAUNCH;
 
   RouterTailArgs ra{};
@@ -208,7 +235,7 @@ int run_layer(const LayerCall& c) {
   ra.m_hist = c.st->m_hist;
   ra.logit = logit;
   ra.gate = gate;
-  e = launch_router_tail(ra, c.stream);
+  e = timed(HERO_K_ROUTER_TAIL, st, [&] { return launch_router_tail(ra, st); });
   if (e != hipSuccess) return HERO_E_LAUNCH;
 
   SelectArgs sa{};
@@ -225,19 +252,38 @@ int run_layer(const LayerCall& c) {
   sa.idx_ad = idx_ad;
   sa.counts = counts;
   sa.lambda = lambda;
-  e = launch_select(sa, c.stream);
+  e = timed(HERO_K_SELECT, st, [&] { return launch_select(sa, st); });
   if (e != hipSuccess) return HERO_E_LAUNCH;
 
   // grid sizes: exact in budget mode, T in threshold mode (tiles past the device count exit)
   const int n_ffn_max = c.rc->mode == HERO_MODE_BUDGET ? T - n_skip : T;
   const int n_ad_max = c.rc->mode == HERO_MODE_BUDGET ? n_skip : T;
-  e = launch_ffn(D.dtype, u, idx_ffn, counts, n_ffn_max, c.ffn->w_gate, c.ffn->w_up, c.ffn->w_down,
-                 ws + L.act, c.hbar, gate, c.h_out, D.d, D.d_ff, c.stream);
-  if (e != hipSuccess) return HERO_E_LAUNCH;
-  e = launch_adapter(D.dtype, u, idx_ad, counts + 1, n_ad_max, c.ad->w1, c.ad->w2,
-                     reinterpret_cast<float*>(ws + L.part), c.hbar, gate, c.h_out, D.d, D.d_r,
-                     c.stream);
-  if (e != hipSuccess) return HERO_E_LAUNCH;
+  void* act = ws + L.act;
+  float* part = reinterpret_cast<float*>(ws + L.part);
+  if (n_ffn_max > 0) {
+    e = timed(HERO_K_FFN_GATE_UP, st, [&] {
+      return launch_ffn_gateup(D.dtype, u, idx_ffn, counts, n_ffn_max, c.ffn->w_gate, c.ffn->w_up,
+                               act, D.d, D.d_ff, st);
+    });
+    if (e != hipSuccess) return HERO_E_LAUNCH;
+    e = timed(HERO_K_FFN_DOWN, st, [&] {
+      return launch_ffn_down(D.dtype, act, idx_ffn, counts, n_ffn_max, c.ffn->w_down, c.hbar, gate,
+                             c.h_out, D.d, D.d_ff, st);
+    });
+    if (e != hipSuccess) return HERO_E_LAUNCH;
+  }
+  if (n_ad_max > 0) {
+    e = timed(HERO_K_ADAPTER_DOWN, st, [&] {
+      return launch_adapter_down(D.dtype, u, idx_ad, counts + 1, n_ad_max, c.ad->w1, part, D.d,
+                                 D.d_r, st);
+    });
+    if (e != hipSuccess) return HERO_E_LAUNCH;
+    e = timed(HERO_K_ADAPTER_UP, st, [&] {
+      return launch_adapter_up(D.dtype, part, idx_ad, counts + 1, n_ad_max, c.ad->w2, c.hbar, gate,
+                               c.h_out, D.d, D.d_r, st);
+    });
+    if (e != hipSuccess) return HERO_E_LAUNCH;
+  }
   return HERO_OK;
 }
 
@@ -263,6 +309,25 @@ const char* hero_status_string(int status) {
 }
 
 int hero_abi_version(void) { return HERO_ABI_VERSION; }
+
+int hero_kernel_timer(int kernel, void* const* start_events, void* const* stop_events, int n_slots) {
+  if (kernel < 0 || kernel >= HERO_K_COUNT || n_slots < 0) return HERO_E_RANGE;
+  if (n_slots > 0 && (!start_events || !stop_events)) return HERO_E_NULL;
+  KernelTimer& k = g_timer[kernel];
+  delete[] k.start;
+  delete[] k.stop;
+  k.start = k.stop = nullptr;
+  k.n = k.next = 0;
+  if (n_slots == 0) return HERO_OK;
+  k.start = new hipEvent_t[n_slots];
+  k.stop = new hipEvent_t[n_slots];
+  for (int i = 0; i < n_slots; ++i) {
+    k.start[i] = static_cast<hipEvent_t>(start_events[i]);
+    k.stop[i] = static_cast<hipEvent_t>(stop_events[i]);
+  }
+  k.n = n_slots;
+  return HERO_OK;
+}
 
 int hero_workspace_size(const hero_dims* dims, int T, int for_stack, size_t* bytes) {
   if (!bytes) return HERO_E_NULL;

@@ -50,18 +50,23 @@ struct SelectArgs {
 };
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 
-// FFN branch: act = SiLU(W_g u) * (W_u u) over gathered rows, then
-// h_out[t] = hbar[t] + g[t] * (W_d act) for t in idx_ffn.
-hipError_t launch_ffn(int dtype, const void* u, const int* idx_ffn, const int* counts, int n_max,
-                      const void* w_gate, const void* w_up, const void* w_down, void* act,
-                      const void* hbar, const float* gate, void* h_out, int d, int d_ff,
-                      hipStream_t s);
+// FFN branch, gate/up: act[m] = SiLU(W_g u_t) * (W_u u_t), t = idx_ffn[m], m < counts[0].
+hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const int* counts,
+                             int n_max, const void* w_gate, const void* w_up, void* act, int d,
+                             int d_ff, hipStream_t s);
+// FFN branch, down + scatter: h_out[t] = hbar[t] + g[t] * (W_d act[m]), t = idx_ffn[m].
+hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const int* counts,
+                           int n_max, const void* w_down, const void* hbar, const float* gate,
+                           void* h_out, int d, int d_ff, hipStream_t s);
 
-// Adapter branch: h_out[t] = hbar[t] + (1 - g[t]) * W_2 SiLU(W_1 u) for t in idx_ad.
-// part: fp32 scratch of adapter_part_floats(d, d_r, T).
+// Adapter branch: h_out[t] = hbar[t] + (1 - g[t]) * W_2 SiLU(W_1 u_t) for t = idx_ad[m].
+// part: fp32 scratch of adapter_part_floats(dtype, d, d_r, T) floats.
 size_t adapter_part_floats(int dtype, int d, int d_r, int T);
-hipError_t launch_adapter(int dtype, const void* u, const int* idx_ad, const int* counts, int n_max,
-                          const void* w1, const void* w2, float* part, const void* hbar,
-                          const float* gate, void* h_out, int d, int d_r, hipStream_t s);
+hipError_t launch_adapter_down(int dtype, const void* u, const int* idx_ad, const int* counts,
+                               int n_max, const void* w1, float* part, int d, int d_r,
+                               hipStream_t s);
+hipError_t launch_adapter_up(int dtype, const float* part, const int* idx_ad, const int* counts,
+                             int n_max, const void* w2, const void* hbar, const float* gate,
+                             void* h_out, int d, int d_r, hipStream_t s);
 
 }  // namespace hero

@@ -478,33 +478,38 @@ hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, con
   return run_f32<false>(A, B, epi, nullptr, T, N, d, s);
 }
 
-hipError_t launch_ffn(int dtype, const void* u, const int* idx_ffn, const int* counts, int n_max,
-                      const void* w_gate, const void* w_up, const void* w_down, void* act,
-                      const void* hbar, const float* gate, void* h_out, int d, int d_ff,
-                      hipStream_t s) {
+hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const int* counts,
+                             int n_max, const void* w_gate, const void* w_up, void* act, int d,
+                             int d_ff, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
-  hipError_t e;
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(u), idx_ffn, d};
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), INT_MAX, d};
-    e = run_mfma<TileGateUp>(A, B, EpiSwiGLU<bf16_t>{static_cast<bf16_t*>(act), d_ff}, counts,
-                             n_max, d_ff, d, s);
-    if (e != hipSuccess) return e;
-    ARows<bf16_t> A2{static_cast<const bf16_t*>(act), nullptr, d_ff};
-    BRows<bf16_t> B2{static_cast<const bf16_t*>(w_down), nullptr, INT_MAX, d_ff};
-    EpiScatter<bf16_t, false> epi{idx_ffn, static_cast<const bf16_t*>(hbar), gate,
-                                  static_cast<bf16_t*>(h_out), d};
-    return run_mfma<TileDown>(A2, B2, epi, counts, n_max, d, d_ff, s);
+    return run_mfma<TileGateUp>(A, B, EpiSwiGLU<bf16_t>{static_cast<bf16_t*>(act), d_ff}, counts,
+                                n_max, d_ff, d, s);
   }
   ARows<float> A{static_cast<const float*>(u), idx_ffn, d};
   BRows<float> B{static_cast<const float*>(w_gate), static_cast<const float*>(w_up), INT_MAX, d};
-  e = run_f32<true>(A, B, EpiSwiGLU<float>{static_cast<float*>(act), d_ff}, counts, n_max, d_ff, d, s);
-  if (e != hipSuccess) return e;
-  ARows<float> A2{static_cast<const float*>(act), nullptr, d_ff};
-  BRows<float> B2{static_cast<const float*>(w_down), nullptr, INT_MAX, d_ff};
+  return run_f32<true>(A, B, EpiSwiGLU<float>{static_cast<float*>(act), d_ff}, counts, n_max, d_ff,
+                       d, s);
+}
+
+hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const int* counts,
+                           int n_max, const void* w_down, const void* hbar, const float* gate,
+                           void* h_out, int d, int d_ff, hipStream_t s) {
+  if (n_max <= 0) return hipSuccess;
+  if (dtype == 1) {
+    ARows<bf16_t> A{static_cast<const bf16_t*>(act), nullptr, d_ff};
+    BRows<bf16_t> B{static_cast<const bf16_t*>(w_down), nullptr, INT_MAX, d_ff};
+    EpiScatter<bf16_t, false> epi{idx_ffn, static_cast<const bf16_t*>(hbar), gate,
+                                  static_cast<bf16_t*>(h_out), d};
+    return run_mfma<TileDown>(A, B, epi, counts, n_max, d, d_ff, s);
+  }
+  ARows<float> A{static_cast<const float*>(act), nullptr, d_ff};
+  BRows<float> B{static_cast<const float*>(w_down), nullptr, INT_MAX, d_ff};
   EpiScatter<float, false> epi{idx_ffn, static_cast<const float*>(hbar), gate,
                                static_cast<float*>(h_out), d};
-  return run_f32<false>(A2, B2, epi, counts, n_max, d, d_ff, s);
+  return run_f32<false>(A, B, epi, counts, n_max, d, d_ff, s);
 }
 
 size_t adapter_part_floats(int dtype, int d, int d_r, int T) {
@@ -512,49 +517,55 @@ size_t adapter_part_floats(int dtype, int d, int d_r, int T) {
   return static_cast<size_t>(G) * T * d_r;
 }
 
-hipError_t launch_adapter(int dtype, const void* u, const int* idx_ad, const int* counts, int n_max,
-                          const void* w1, const void* w2, float* part, const void* hbar,
-                          const float* gate, void* h_out, int d, int d_r, hipStream_t s) {
+hipError_t launch_adapter_down(int dtype, const void* u, const int* idx_ad, const int* counts,
+                               int n_max, const void* w1, float* part, int d, int d_r,
+                               hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
   if (dtype == 1) {
     const int G = adapter_groups(d);
-    const int K = d;
     dim3 g1((n_max + 31) / 32, G);
     const bf16_t* uu = static_cast<const bf16_t*>(u);
-    const bf16_t* ww1 = static_cast<const bf16_t*>(w1);
-    // the adapter rank is a compile-time tile count (32-column MFMA tiles)
+    const bf16_t* ww = static_cast<const bf16_t*>(w1);
+    // the adapter rank is a compile-time count of 32-column MFMA tiles
     switch (d_r) {
-      case 32: adapter_down_bf16<1><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww1, part, n_max, K, K / G); break;
-      case 64: adapter_down_bf16<2><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww1, part, n_max, K, K / G); break;
-      case 96: adapter_down_bf16<3><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww1, part, n_max, K, K / G); break;
-      case 128: adapter_down_bf16<4><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww1, part, n_max, K, K / G); break;
-      default: return hipErrorInvalidValue;
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    dim3 g2((n_max + 31) / 32, d / 256);
-    const bf16_t* ww2 = static_cast<const bf16_t*>(w2);
-    const bf16_t* hb = static_cast<const bf16_t*>(hbar);
-    bf16_t* ho = static_cast<bf16_t*>(h_out);
-    switch (d_r) {
-      case 32: adapter_up_bf16<32><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww2, hb, gate, ho, n_max, d); break;
-      case 64: adapter_up_bf16<64><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww2, hb, gate, ho, n_max, d); break;
-      case 96: adapter_up_bf16<96><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww2, hb, gate, ho, n_max, d); break;
-      case 128: adapter_up_bf16<128><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww2, hb, gate, ho, n_max, d); break;
+      case 32: adapter_down_bf16<1><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G); break;
+      case 64: adapter_down_bf16<2><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G); break;
+      case 96: adapter_down_bf16<3><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G); break;
+      case 128: adapter_down_bf16<4><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G); break;
       default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
   }
-  // fp32: hid = SiLU(u W_1^T) into part[m][n], then the up-projection with scatter
+  // fp32: hid = SiLU(u W_1^T) into part[m][n]
   ARows<float> A{static_cast<const float*>(u), idx_ad, d};
   BRows<float> B{static_cast<const float*>(w1), nullptr, INT_MAX, d};
-  hipError_t e = run_f32<false>(A, B, EpiSiLU<float>{part, d_r}, counts, n_max, d_r, d, s);
-  if (e != hipSuccess) return e;
-  ARows<float> A2{part, nullptr, d_r};
-  BRows<float> B2{static_cast<const float*>(w2), nullptr, INT_MAX, d_r};
+  return run_f32<false>(A, B, EpiSiLU<float>{part, d_r}, counts, n_max, d_r, d, s);
+}
+
+hipError_t launch_adapter_up(int dtype, const float* part, const int* idx_ad, const int* counts,
+                             int n_max, const void* w2, const void* hbar, const float* gate,
+                             void* h_out, int d, int d_r, hipStream_t s) {
+  if (n_max <= 0) return hipSuccess;
+  if (dtype == 1) {
+    const int G = adapter_groups(d);
+    dim3 g2((n_max + 31) / 32, d / 256);
+    const bf16_t* ww = static_cast<const bf16_t*>(w2);
+    const bf16_t* hb = static_cast<const bf16_t*>(hbar);
+    bf16_t* ho = static_cast<bf16_t*>(h_out);
+    switch (d_r) {
+      case 32: adapter_up_bf16<32><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
+      case 64: adapter_up_bf16<64><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
+      case 96: adapter_up_bf16<96><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
+      case 128: adapter_up_bf16<128><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
+  ARows<float> A{part, nullptr, d_r};
+  BRows<float> B{static_cast<const float*>(w2), nullptr, INT_MAX, d_r};
   EpiScatter<float, true> epi{idx_ad, static_cast<const float*>(hbar), gate,
                               static_cast<float*>(h_out), d};
-  return run_f32<false>(A2, B2, epi, counts, n_max, d, d_r, s);
+  return run_f32<false>(A, B, epi, counts, n_max, d, d_r, s);
 }
 
 }  // namespace hero

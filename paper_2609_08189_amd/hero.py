@@ -32,6 +32,10 @@ HERO_BF16 = 1
 HERO_MODE_THRESHOLD = 0
 HERO_MODE_BUDGET = 1
 
+KERNELS = ("rowstats", "router_gemm", "router_tail", "select", "ffn_gate_up", "ffn_down",
+           "adapter_down", "adapter_up")
+HERO_K = {name: i for i, name in enumerate(KERNELS)}
+
 _vp = ctypes.c_void_p
 
 
@@ -88,6 +92,8 @@ def lib() -> ctypes.CDLL:
         L.hero_status_string.argtypes = [ctypes.c_int]
         L.hero_abi_version.restype = ctypes.c_int
         L.hero_abi_version.argtypes = []
+        L.hero_kernel_timer.restype = ctypes.c_int
+        L.hero_kernel_timer.argtypes = [ctypes.c_int, P(_vp), P(_vp), ctypes.c_int]
         L.hero_workspace_size.restype = ctypes.c_int
         L.hero_workspace_size.argtypes = [P(hero_dims), ctypes.c_int, ctypes.c_int, P(ctypes.c_size_t)]
         L.hero_routed_layer.restype = ctypes.c_int
@@ -130,6 +136,14 @@ def hero_status_string(status: int) -> str:
 
 def hero_abi_version() -> int:
     return lib().hero_abi_version()
+
+
+def hero_kernel_timer(kernel: int, start_events: Sequence[int], stop_events: Sequence[int]) -> None:
+    """Attach caller-created hipEvent_t handles around every launch of one kernel (empty: detach)."""
+    n = len(start_events)
+    a = (_vp * max(n, 1))(*start_events)
+    b = (_vp * max(n, 1))(*stop_events)
+    check(lib().hero_kernel_timer(kernel, a, b, n), "hero_kernel_timer")
 
 
 def hero_workspace_size(dims: hero_dims, T: int, for_stack: bool) -> int:

@@ -258,12 +258,13 @@ def incoming_state(w: Workload, j: int, T: int, seed: int = 0, decay: float = 0.
         return S, zeta, np.ones(T, np.float32), np.ones(T, np.float32)
     ga = _rng(seed, "state_a")
     gb = _rng(seed, "state_b")
-    for i in range(1, j):
-        wgt = np.float32(decay ** (j - 1 - i))
-        a = np.exp(np.float32(0.5) * ga.standard_normal((T, dm), dtype=np.float32))
-        b = gb.standard_normal((T, dm), dtype=np.float32)
-        S += wgt * (a[:, :, None] * b[:, None, :])
-        zeta += wgt * a
+    n = j - 1
+    wgt = np.array([decay ** (j - 1 - i) for i in range(1, j)], dtype=np.float32)
+    a = np.exp(np.float32(0.5) * ga.standard_normal((T, n, dm), dtype=np.float32))
+    b = gb.standard_normal((T, n, dm), dtype=np.float32)
+    aw = a * wgt[None, :, None]
+    S = np.matmul(aw.transpose(0, 2, 1), b)          # [T, dm, dm] = sum_i w_i a_i b_i^T
+    zeta = aw.sum(axis=1)
     gp = _rng(seed, "p_hist")
     p = gp.uniform(0.2, 0.8, size=T).astype(np.float32)
     gm = _rng(seed, "m_hist")

@@ -63,3 +63,28 @@ def test_budget_extremes(budget):
 def test_tiny_token_counts(T):
     _run(BF16_SMALL.replace(T=T), 3, seed=7)
     _run(BF16_SMALL.replace(T=T, mode="threshold"), 1, seed=7)
+
+
+def test_llama31_8b_layer_full_shape():
+    """Llama-3.1-8B shape, j = 17 of 32, T = 4096, budget 26.87 %, in the launch configuration the
+    benchmark times.  Router, memory, decisions and index lists are checked for every token; the
+    branch outputs on a sample of 48 FFN and 24 adapter rows (the oracle's FFN is costly)."""
+    import torch
+    from paper_2609_08189_amd.device import DeviceProblem
+    w = synth.WORKLOADS["llama31_8b_layer"]
+    print(f"case {w.name} T={w.T} j={w.layer_j}", flush=True)
+    prob = synth.make_problem(w, seed=0)
+    dp = DeviceProblem(prob)
+    dp.run_layer(w.layer_j)
+    res = dp.results()
+    mask = res["layers"][0]["mask"]
+    rng = np.random.default_rng(0)
+    rows = np.zeros(w.T, bool)
+    rows[rng.choice(np.nonzero(mask)[0], 48, replace=False)] = True
+    rows[rng.choice(np.nonzero(~mask)[0], 24, replace=False)] = True
+    report = {}
+    check_layer(prob, res, w.layer_j, rows=rows, report=report)
+    print("  errors:", report, flush=True)
+    assert res["layers"][0]["n_ad"] == 1101
+    del dp
+    torch.cuda.empty_cache()
