@@ -74,10 +74,12 @@ class DeviceProblem:
         self.h_out = torch.empty_like(self.hbar)
         self.router = {k: upload(v, device) for k, v in prob.router.items()}
         self.router_s = H.hero_router_weights(**{k: self.router[k].data_ptr() for k in H.ROUTER_FIELDS})
-        self.ffn = [{k: upload(v, device) for k, v in layer.items()} for layer in prob.ffn]
+        # weights are drawn and uploaded one layer at a time
+        self.ffn = [{k: upload(v, device) for k, v in prob.ffn[i].items()} for i in range(len(prob.ffn))]
         self.ffn_s = [H.hero_ffn_weights(f["norm_w"].data_ptr(), f["w_gate"].data_ptr(),
                                          f["w_up"].data_ptr(), f["w_down"].data_ptr()) for f in self.ffn]
-        self.adapter = [{k: upload(v, device) for k, v in layer.items()} for layer in prob.adapter]
+        self.adapter = [{k: upload(v, device) for k, v in prob.adapter[i].items()}
+                        for i in range(len(prob.adapter))]
         self.adapter_s = [H.hero_adapter_weights(a["w1"].data_ptr(), a["w2"].data_ptr()) for a in self.adapter]
         self.eta = [float(e) for e in prob.eta]
         self.S = torch.from_numpy(prob.S).to(device)
@@ -90,9 +92,8 @@ class DeviceProblem:
         mode = H.HERO_MODE_BUDGET if w.mode == "budget" else H.HERO_MODE_THRESHOLD
         self.routing_s = H.hero_routing(mode, w.tau, w.budget,
                                         self.beta.data_ptr() if self.beta is not None else None)
-        n_layers = len(prob.ffn)
         if for_stack is None:
-            for_stack = n_layers > 1
+            for_stack = w.layer_j <= 0      # a stack workload (a layer workload names its j)
         self.for_stack = for_stack
         self.stats = [LayerStats(T, device) for _ in range(w.L_R if for_stack else 1)] if stats else None
         self.ws_bytes = H.hero_workspace_size(self.dims, T, for_stack)
@@ -129,3 +130,39 @@ class DeviceProblem:
         if self.stats:
             out["layers"] = [s.host() for s in self.stats]
         return out
+
+    def run_chained(self, rows=None) -> List[Dict[str, object]]:
+        """Run the routed stack as chained hero_routed_layer calls and capture, for the
+        selected token rows, every layer's post-attention input, the router state before and
+        after it, its stats and its output (host float64).  The final output is left in
+        h_out and the final state in the state buffers, as hero_routed_stack leaves them."""
+        T = self.T
+        idx = None if rows is None else torch.as_tensor(np.asarray(rows), device=self.device)
+        pick = (lambda x: x) if idx is None else (lambda x: x.index_select(0, idx))
+        ws_bytes = H.hero_workspace_size(self.dims, T, False)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=self.device)
+        stats = LayerStats(T, self.device)
+        hs = [self.hbar]
+        n_sel = T if idx is None else len(idx)
+        prev_state = (np.zeros((n_sel, self.w.d_m, self.w.d_m)), np.zeros((n_sel, self.w.d_m)),
+                      np.ones(n_sel), np.ones(n_sel))
+        io = []
+        for j in range(1, self.w.L_R + 1):
+            out = self.h_out if j == self.w.L_R else torch.empty_like(self.hbar)
+            H.check(H.hero_routed_layer(self.dims, j, T, hs[-1], hs[-2] if j >= 2 else None,
+                                        hs[-3] if j >= 3 else None, out, self.state_s, self.ffn_s[j - 1],
+                                        self.router_s, self.adapter_s[j - 1], self.eta[j - 1],
+                                        self.routing_s, stats.struct, ws, ws_bytes, self.stream()),
+                    "hero_routed_layer")
+            torch.cuda.synchronize()
+            after = (pick(self.S).cpu().numpy().astype(np.float64), pick(self.zeta).cpu().numpy().astype(np.float64),
+                     pick(self.p_hist).cpu().numpy().astype(np.float64),
+                     pick(self.m_hist).cpu().numpy().astype(np.float64))
+            io.append(dict(hbar=download_f64(pick(hs[-1])), S=prev_state[0], zeta=prev_state[1],
+                           p=prev_state[2], m=prev_state[3], stats=stats.host(), h=download_f64(pick(out)),
+                           S1=after[0], zeta1=after[1], p1=after[2], m1=after[3]))
+            prev_state = after
+            hs.append(out)
+            if len(hs) > 3:
+                hs.pop(0)
+        return io

@@ -119,7 +119,17 @@ def to_store(x32: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "f32":
         return np.ascontiguousarray(x32, dtype=np.float32)
     if dtype == "bf16":
-        return f32_to_bf16_bits(x32)
+        flat = np.ascontiguousarray(x32, dtype=np.float32).reshape(-1)
+        if flat.size <= 4 * _CHUNK:
+            return f32_to_bf16_bits(flat).reshape(x32.shape)
+        out = np.empty(flat.size, dtype=np.uint16)
+
+        def conv(c):
+            lo, hi = c * _CHUNK, min(flat.size, (c + 1) * _CHUNK)
+            out[lo:hi] = f32_to_bf16_bits(flat[lo:hi])
+
+        list(_pool().map(conv, range((flat.size + _CHUNK - 1) // _CHUNK)))
+        return out.reshape(x32.shape)
     raise ValueError(dtype)
 
 
@@ -151,15 +161,43 @@ def _rng(seed: int, name: str, layer: int = 0) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64([seed, _TID[name], layer]))
 
 
+_CHUNK = 1 << 20   # elements per independent stream of a large tensor
+_POOL = None
+
+
+def _pool():
+    global _POOL
+    if _POOL is None:
+        import concurrent.futures
+        import os
+        n = min(16, os.cpu_count() or 1)
+        _POOL = concurrent.futures.ThreadPoolExecutor(max_workers=n)
+    return _POOL
+
+
 def normal32(seed: int, name: str, shape, std: float = 1.0, mean: float = 0.0,
              layer: int = 0) -> np.ndarray:
-    g = _rng(seed, name, layer)
-    x = g.standard_normal(size=shape, dtype=np.float32)
-    if std != 1.0:
-        x *= np.float32(std)
-    if mean != 0.0:
-        x += np.float32(mean)
-    return x
+    """N(mean, std^2) in float32.  Chunk c of 2^20 elements comes from PCG64 keyed by
+    (seed, tensor id, layer, c), so large tensors are drawn in parallel."""
+    n = int(np.prod(shape))
+    x = np.empty(n, dtype=np.float32)
+
+    def fill(c):
+        lo, hi = c * _CHUNK, min(n, (c + 1) * _CHUNK)
+        g = np.random.Generator(np.random.PCG64([seed, _TID[name], layer, c]))
+        g.standard_normal(size=hi - lo, dtype=np.float32, out=x[lo:hi])
+        if std != 1.0:
+            x[lo:hi] *= np.float32(std)
+        if mean != 0.0:
+            x[lo:hi] += np.float32(mean)
+
+    nch = (n + _CHUNK - 1) // _CHUNK
+    if nch <= 2:
+        for c in range(nch):
+            fill(c)
+    else:
+        list(_pool().map(fill, range(nch)))
+    return x.reshape(shape)
 
 
 class Tensor:
@@ -294,6 +332,32 @@ def logit_bias(w: Workload, seed: int = 0, T: Optional[int] = None) -> Optional[
 # ---------------------------------------------------------------------------
 
 
+class LazyLayers:
+    """Per-layer weights drawn on first access (the most recent layers are cached)."""
+
+    def __init__(self, make, layers, keep: int = 2):
+        self._make = make
+        self._layers = list(layers)
+        self._keep = keep
+        self._cache: Dict[int, Dict[str, Tensor]] = {}
+
+    def __len__(self):
+        return len(self._layers)
+
+    def __getitem__(self, i):
+        if i < 0:
+            i += len(self._layers)
+        if i not in self._cache:
+            while len(self._cache) >= self._keep:
+                self._cache.pop(next(iter(self._cache)))
+            self._cache[i] = self._make(self._layers[i])
+        return self._cache[i]
+
+    def __iter__(self):
+        for i in range(len(self._layers)):
+            yield self[i]
+
+
 @dataclasses.dataclass
 class Problem:
     w: Workload
@@ -305,8 +369,8 @@ class Problem:
     p_hist: np.ndarray                # [T] f32
     m_hist: np.ndarray                # [T] f32
     router: Dict[str, Tensor]
-    ffn: List[Dict[str, Tensor]]      # one per routed layer (a layer call: one entry)
-    adapter: List[Dict[str, Tensor]]
+    ffn: "LazyLayers"                 # one per routed layer (a layer call: one entry)
+    adapter: "LazyLayers"
     eta: np.ndarray                   # [L_R] f32 (a layer call uses eta[j-1])
     beta: Optional[np.ndarray]        # [T] f32 or None
 
@@ -336,8 +400,8 @@ def make_problem(w: Workload, seed: int = 0, T: Optional[int] = None,
         w=w, hbar=hb, hbar_prev1=prev1, hbar_prev2=prev2,
         S=S, zeta=zeta, p_hist=p, m_hist=m,
         router=router_weights(w, seed),
-        ffn=[ffn_layer(w, l, seed) for l in layers],
-        adapter=[adapter_layer(w, l, seed) for l in layers],
+        ffn=LazyLayers(lambda l: ffn_layer(w, l, seed), layers),
+        adapter=LazyLayers(lambda l: adapter_layer(w, l, seed), layers, keep=4),
         eta=eta_values(w),
         beta=logit_bias(w, seed, T),
     )

@@ -114,3 +114,120 @@ def check_layer(prob, gpu_res, j, rows=None, report=None):
     for k in ("logit", "gate", "h", "S", "zeta", "p", "m"):
         assert errs[k] <= tol, f"{k}: max rel err {errs[k]:.3e} > {tol:.0e} ({errs})"
     return errs
+
+
+class _LazyMap:
+    """Sequence view applying f to the items of a lazily generated sequence."""
+
+    def __init__(self, seq, f):
+        self.seq, self.f = seq, f
+
+    def __len__(self):
+        return len(self.seq)
+
+    def __getitem__(self, i):
+        return self.f(self.seq[i])
+
+
+def check_stack(prob, gpu_res, rows=None, report=None):
+    """Routed stack: per-layer decisions, logits and gates, and the final hidden state and
+    router state, against the oracle stack teacher-forced to the GPU's decisions.  With
+    ``rows`` (a token subset) the oracle's own budget decisions use the GPU's per-layer
+    lambda, since the quantile is over the whole batch."""
+    w = prob.w
+    T = prob.hbar.shape[0]
+    tol = TOL[w.dtype]
+    layers = gpu_res["layers"]
+    sel = np.arange(T) if rows is None else np.asarray(rows)
+    for L in layers:
+        check_compaction(L, T)
+        if w.mode == "budget":
+            check_budget_selection(L, w.budget, T)
+    forced = [L["mask"][sel] for L in layers]
+    lam_given = [L["lam"] for L in layers] if (rows is not None and w.mode == "budget") else None
+    beta = None if prob.beta is None else prob.beta[sel].astype(np.float64)
+    ref = O.routed_stack(dims_of(w), prob.hbar.f64[sel], _LazyMap(prob.ffn, ffn_of), router_of(prob),
+                         _LazyMap(prob.adapter, adapter_of), prob.eta.astype(np.float64),
+                         mode=w.mode, budget=w.budget, tau=w.tau, beta=beta,
+                         forced_ffn=forced, lam_given=lam_given)
+    n_band = 0
+    errs = dict(logit=0.0, gate=0.0)
+    for L, R in zip(layers, ref.layers):
+        if w.mode == "budget" and rows is None:
+            _, lam_ref = O.decide_budget(R.logit, w.budget)
+        else:
+            lam_ref = R.lam
+        mism = L["mask"][sel] != R.own_ffn
+        thr = band_threshold(w, lam_ref)
+        far = mism & (np.abs(R.gate - thr) >= BAND)
+        assert not far.any(), (f"{int(far.sum())} decisions differ outside the band at layer "
+                               f"{len(errs) and layers.index(L) + 1}: gates {R.gate[far][:4]}, thr {thr}, "
+                               f"logit err so far {errs['logit']:.2e}")
+        n_band += int(mism.sum())
+        errs["logit"] = max(errs["logit"], scalar_err(L["logit"][sel], R.logit))
+        errs["gate"] = max(errs["gate"], scalar_err(L["gate"][sel], R.gate))
+    errs.update(h=row_rel_err(gpu_res["h"][sel], ref.h), S=row_rel_err(gpu_res["S"][sel], ref.state.S),
+                zeta=row_rel_err(gpu_res["zeta"][sel], ref.state.zeta),
+                p=scalar_err(gpu_res["p_hist"][sel], ref.state.p_hist),
+                m=scalar_err(gpu_res["m_hist"][sel], ref.state.m_hist), band_flips=n_band)
+    if report is not None:
+        report.update(errs)
+    for k in ("logit", "gate", "h", "S", "zeta", "p", "m"):
+        assert errs[k] <= tol, f"{k}: max rel err {errs[k]:.3e} > {tol:.0e} ({errs})"
+    return errs
+
+
+def check_stack_layerwise(prob, layer_io, rows=None, report=None):
+    """Deep stacks: every routed layer checked on the GPU's own inputs.
+
+    ``layer_io[j-1]`` holds, for the selected token rows, what the GPU fed into and got out
+    of routed layer j: ``hbar`` (its post-attention input), ``S``/``zeta``/``p``/``m``
+    before the layer, the layer's stats, and ``h``/``S1``/``zeta1``/``p1``/``m1`` after it.
+    The oracle runs each layer from the GPU's inputs with the GPU's decisions (so errors
+    cannot compound over depth) and each layer is held to the single-layer tolerance.
+    """
+    w = prob.w
+    tol = TOL[w.dtype]
+    T = prob.hbar.shape[0]
+    sel = np.arange(T) if rows is None else np.asarray(rows)
+    worst = dict(logit=0.0, gate=0.0, h=0.0, S=0.0, zeta=0.0, p=0.0, m=0.0)
+    n_band = 0
+    far_info = []
+    for j in range(1, w.L_R + 1):
+        io = layer_io[j - 1]
+        L = io["stats"]
+        check_compaction(L, T)
+        if w.mode == "budget":
+            check_budget_selection(L, w.budget, T)
+        prev1 = layer_io[j - 2]["hbar"] if j >= 2 else None
+        prev2 = layer_io[j - 3]["hbar"] if j >= 3 else None
+        st = O.State(io["S"], io["zeta"], io["p"], io["m"])
+        beta = None if prob.beta is None else prob.beta[sel].astype(np.float64)
+        lam_given = L["lam"] if (rows is not None and w.mode == "budget") else None
+        R = O.routed_layer(j, dims_of(w), io["hbar"], prev1, prev2, st, ffn_of(prob.ffn[j - 1]), router_of(prob),
+                           adapter_of(prob.adapter[j - 1]), float(prob.eta[j - 1]), mode=w.mode,
+                           budget=w.budget, tau=w.tau, beta=beta, forced_ffn=L["mask"][sel],
+                           lam_given=lam_given)
+        if w.mode == "budget" and rows is None:
+            _, lam_ref = O.decide_budget(R.logit, w.budget)
+        else:
+            lam_ref = R.lam
+        mism = L["mask"][sel] != R.own_ffn
+        thr = band_threshold(w, lam_ref)
+        far = mism & (np.abs(R.gate - thr) >= BAND)
+        if far.any():
+            far_info.append((j, R.gate[far][:4].tolist(), thr))
+        n_band += int(mism.sum())
+        e = dict(logit=scalar_err(L["logit"][sel], R.logit), gate=scalar_err(L["gate"][sel], R.gate),
+                 h=row_rel_err(io["h"], R.h), S=row_rel_err(io["S1"], R.state.S),
+                 zeta=row_rel_err(io["zeta1"], R.state.zeta), p=scalar_err(io["p1"], R.state.p_hist),
+                 m=scalar_err(io["m1"], R.state.m_hist))
+        for k in worst:
+            worst[k] = max(worst[k], e[k])
+    worst["band_flips"] = n_band
+    if report is not None:
+        report.update(worst)
+    assert not far_info, f"decisions outside the band (layer, gates, threshold): {far_info}"
+    for k in ("logit", "gate", "h", "S", "zeta", "p", "m"):
+        assert worst[k] <= tol, f"{k}: max rel err {worst[k]:.3e} > {tol:.0e} ({worst})"
+    return worst

@@ -1,0 +1,184 @@
+"""Host-side checks of libhero.so that need no GPU.
+
+The library must load and export every function include/hero.h declares, and
+every argument check must return its documented status before any HIP call.
+Device pointers here are fake aligned addresses: each call is invalid in exactly
+one way, so validation rejects it before the device check and nothing is ever
+launched, on a machine with or without a GPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_08189_amd import hero as H
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x7F0000000000   # aligned, never dereferenced
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "hero.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hero_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert {"hero_routed_layer", "hero_routed_stack", "hero_workspace_size"} <= set(names)
+    lib = H.lib()
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in include/hero.h but not exported"
+    assert H.hero_abi_version() == 1
+
+
+def test_status_strings():
+    for code in range(11):
+        assert H.hero_status_string(code) != "unknown status"
+    assert H.hero_status_string(99) == "unknown status"
+
+
+def good_dims(dtype=H.HERO_BF16, **kw):
+    d = dict(d=512, d_ff=1408, d_r=64, L_R=8, d_m=128, d_s=64, d_h=48, d_a=16, d_e=256, d_p=64,
+             d_head=256, dtype=dtype, eps_norm=1e-5, eps=1e-6, T_hist=0.9)
+    d.update(kw)
+    return H.hero_dims(**d)
+
+
+def fake_structs(L=1):
+    a = iter(range(1, 1000))
+    nxt = lambda: FAKE + 4096 * next(a)
+    ffn = [H.hero_ffn_weights(nxt(), nxt(), nxt(), nxt()) for _ in range(L)]
+    ad = [H.hero_adapter_weights(nxt(), nxt()) for _ in range(L)]
+    rt = H.hero_router_weights(**{k: nxt() for k in H.ROUTER_FIELDS})
+    st = H.hero_state(nxt(), nxt(), nxt(), nxt())
+    return ffn, ad, rt, st
+
+
+def call_layer(dims=None, j=3, T=100, routing=None, ws_bytes=None, **over):
+    dims = dims or good_dims()
+    ffn, ad, rt, st = fake_structs()
+    routing = routing or H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.27, None)
+    need = ctypes.c_size_t(0)
+    if H.lib().hero_workspace_size(ctypes.byref(dims), max(T, 1), 0, ctypes.byref(need)) != H.HERO_OK:
+        need.value = 1 << 20
+    args = dict(hbar=FAKE + (1 << 30), prev1=FAKE + (2 << 30), prev2=FAKE + (3 << 30),
+                h_out=FAKE + (4 << 30), state=st, ffn=ffn[0], router=rt, adapter=ad[0], eta=3.89,
+                routing=routing, stats=None, ws=FAKE + (8 << 30),
+                ws_bytes=need.value if ws_bytes is None else ws_bytes)
+    args.update(over)
+    return H.hero_routed_layer(dims, j, T, args["hbar"], args["prev1"], args["prev2"], args["h_out"],
+                               args["state"], args["ffn"], args["router"], args["adapter"], args["eta"],
+                               args["routing"], args["stats"], args["ws"], args["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("dtype", 7, H.HERO_E_DTYPE),
+    ("d", 0, H.HERO_E_DIM),
+    ("d_ff", -1, H.HERO_E_DIM),
+    ("d_s", 63, H.HERO_E_DIM),          # d_s != d_h + d_a
+    ("eps", 0.0, H.HERO_E_RANGE),
+    ("T_hist", -1.0, H.HERO_E_RANGE),
+    ("d_m", 48, H.HERO_E_UNSUPPORTED),
+    ("d", 640, H.HERO_E_UNSUPPORTED),    # bf16 needs d % 256 == 0
+    ("d_ff", 688, H.HERO_E_UNSUPPORTED),  # bf16 needs d_ff % 128 == 0
+    ("d_r", 16, H.HERO_E_UNSUPPORTED),
+    ("d_e", 1024, H.HERO_E_UNSUPPORTED),
+])
+def test_dims_validation(field, value, status):
+    assert call_layer(good_dims(**{field: value})) == status
+
+
+def test_f32_accepts_ragged_widths_bf16_does_not():
+    need = ctypes.c_size_t(0)
+    dims = good_dims(H.HERO_F32, d=256, d_ff=688, d_r=16, d_m=32)
+    assert H.lib().hero_workspace_size(ctypes.byref(dims), 64, 1, ctypes.byref(need)) == H.HERO_OK
+    dims = good_dims(H.HERO_BF16, d=256, d_ff=688, d_r=16, d_m=32)
+    assert H.lib().hero_workspace_size(ctypes.byref(dims), 64, 1, ctypes.byref(need)) == H.HERO_E_UNSUPPORTED
+
+
+def test_argument_validation():
+    assert call_layer(T=0) == H.HERO_E_DIM
+    assert call_layer(j=0) == H.HERO_E_RANGE
+    assert call_layer(j=9) == H.HERO_E_RANGE
+    assert call_layer(hbar=None) == H.HERO_E_NULL
+    assert call_layer(h_out=None) == H.HERO_E_NULL
+    assert call_layer(j=2, prev1=None) == H.HERO_E_NULL
+    assert call_layer(j=3, prev2=None) == H.HERO_E_NULL
+    assert call_layer(hbar=FAKE + 8) == H.HERO_E_ALIGN
+    assert call_layer(h_out=FAKE + (1 << 30) + 512) == H.HERO_E_ALIAS       # overlaps hbar
+    assert call_layer(h_out=FAKE + (2 << 30)) == H.HERO_E_ALIAS              # is hbar_prev1
+    assert call_layer(state=None) == H.HERO_E_NULL
+    ffn, ad, rt, st = fake_structs()
+    st.S = None
+    assert call_layer(state=st) == H.HERO_E_NULL
+    ffn[0].w_down = None
+    assert call_layer(ffn=ffn[0]) == H.HERO_E_NULL
+    rt.th1 = FAKE + 2
+    assert call_layer(router=rt) == H.HERO_E_ALIGN
+    assert call_layer(eta=float("nan")) == H.HERO_E_RANGE
+    assert call_layer(ws=None) == H.HERO_E_WORKSPACE
+    assert call_layer(ws_bytes=1024) == H.HERO_E_WORKSPACE
+    stats = H.hero_layer_stats(FAKE + 4, None, None, None, None, None, None)
+    assert call_layer(stats=stats) == H.HERO_E_ALIGN
+
+
+@pytest.mark.parametrize("routing,status", [
+    (H.hero_routing(H.HERO_MODE_THRESHOLD, 0.0, 0.0, None), H.HERO_E_RANGE),
+    (H.hero_routing(H.HERO_MODE_THRESHOLD, 1.0, 0.0, None), H.HERO_E_RANGE),
+    (H.hero_routing(H.HERO_MODE_BUDGET, 0.5, -0.1, None), H.HERO_E_RANGE),
+    (H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 1.5, None), H.HERO_E_RANGE),
+    (H.hero_routing(5, 0.5, 0.5, None), H.HERO_E_RANGE),
+    (H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.5, FAKE + 6), H.HERO_E_ALIGN),
+])
+def test_routing_validation(routing, status):
+    assert call_layer(routing=routing) == status
+
+
+def test_j1_and_j2_do_not_need_history():
+    # with prev pointers absent, j = 1 and j = 2 pass the NULL checks and stop at the workspace
+    assert call_layer(j=1, prev1=None, prev2=None, ws=None) == H.HERO_E_WORKSPACE
+    assert call_layer(j=2, prev2=None, ws=None) == H.HERO_E_WORKSPACE
+
+
+def test_stack_validation():
+    L = 4
+    dims = good_dims(L_R=L)
+    ffn, ad, rt, st = fake_structs(L)
+    rc = H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.3, None)
+    need = H.hero_workspace_size(dims, 100, True)
+
+    def call(**kw):
+        a = dict(h_in=FAKE + (1 << 30), h_out=FAKE + (4 << 30), ffn=ffn, ad=ad, eta=[3.9] * L,
+                 ws=FAKE + (8 << 30), ws_bytes=need, st=st, rc=rc)
+        a.update(kw)
+        return H.hero_routed_stack(dims, 100, a["h_in"], a["h_out"], a["st"], a["ffn"], rt, a["ad"], a["eta"],
+                                   a["rc"], None, a["ws"], a["ws_bytes"], None)
+
+    assert call(h_out=FAKE + (1 << 30)) == H.HERO_E_ALIAS
+    assert call(ws_bytes=need - 1) == H.HERO_E_WORKSPACE
+    assert call(eta=[3.9, float("nan"), 3.9, 3.9]) == H.HERO_E_RANGE
+    bad = list(ffn)
+    bad[2] = H.hero_ffn_weights(FAKE, FAKE, None, FAKE)
+    assert call(ffn=bad) == H.HERO_E_NULL
+    # the output may not sit inside the workspace (its ring holds the layer-to-layer states)
+    assert call(h_out=FAKE + (8 << 30) + 4096) == H.HERO_E_ALIAS
+
+
+def test_workspace_size_monotone_and_stack_larger():
+    dims = good_dims()
+    a = H.hero_workspace_size(dims, 100, False)
+    b = H.hero_workspace_size(dims, 1000, False)
+    c = H.hero_workspace_size(dims, 1000, True)
+    assert 0 < a < b < c
+    # the stack adds a three-deep ring of [T][d] post-attention states
+    assert c - b >= 3 * 1000 * 512 * 2
+
+
+def test_no_device_means_device_error():
+    """All arguments valid: without a usable gfx950 device the call stops at the device check."""
+    import torch
+    if torch.cuda.device_count() > 0:
+        pytest.skip("a GPU is visible; this test covers hosts without one")
+    assert call_layer() == H.HERO_E_DEVICE
