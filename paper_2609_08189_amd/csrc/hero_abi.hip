@@ -67,7 +67,7 @@ int check_dims(const hero_dims* d) {
   if (d->d_m != 32 && d->d_m != 64 && d->d_m != 128 && d->d_m != 256) return HERO_E_UNSUPPORTED;
   if (d->d_s > 128 || d->d_e > 512 || d->d_head > 512 || d->d_p > 128) return HERO_E_UNSUPPORTED;
   if (d->dtype == HERO_BF16) {
-    if (d->d % 256 || d->d_ff % 128 || (d->d_e + d->d_head) % 128) return HERO_E_UNSUPPORTED;
+    if (d->d % 256 || d->d_ff % 128 || d->d_e % 64 || (d->d_e + d->d_head) % 128) return HERO_E_UNSUPPORTED;
     if (d->d_r % 32 || d->d_r > 128) return HERO_E_UNSUPPORTED;
   } else {
     if (d->d % 128) return HERO_E_UNSUPPORTED;

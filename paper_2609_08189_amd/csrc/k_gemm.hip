@@ -27,23 +27,6 @@ namespace {
 constexpr int BK = 64;     // k elements per tile
 constexpr int ROWB = 128;  // bytes of one row of a bf16 k-tile
 
-__device__ __forceinline__ int swz(int row, int ch) { return row * ROWB + ((ch ^ (row & 7)) << 4); }
-
-template <int BM_, int BN_, int WM_, int WN_, bool DUAL_>
-struct Tile {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
-  static constexpr bool DUAL = DUAL_;
-  static constexpr int NT = 64 * WM * WN;
-  static constexpr int WTM = BM / WM, WTN = BN / WN;
-  static constexpr int TM = WTM / 32, TN = WTN / 32;
-  static constexpr int A_CH = BM * 8 / NT, B_CH = BN * 8 / NT;
-  static constexpr int STAGE = (BM + BN) * ROWB;
-  static constexpr int OUT_N = DUAL ? BN / 2 : BN;  // output columns per tile
-  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole MFMA tiles");
-  static_assert(!DUAL || TN % 2 == 0, "gate/up tiles come in pairs");
-  static_assert((BM * 8) % NT == 0 && (BN * 8) % NT == 0, "loader split");
-};
-
 template <typename T>
 struct ARows {
   const T* base;
@@ -79,6 +62,11 @@ struct EpiStoreF32 {  // P[m][n] = acc
   __device__ __forceinline__ void store(int m, int n, float v) const {
     out[static_cast<size_t>(m) * ld + n] = v;
   }
+  __device__ __forceinline__ void emit8(int m, int n, const float* v) const {
+    float* o = out + static_cast<size_t>(m) * ld + n;
+    *reinterpret_cast<f32x4*>(o) = *reinterpret_cast<const f32x4*>(v);
+    *reinterpret_cast<f32x4*>(o + 4) = *reinterpret_cast<const f32x4*>(v + 4);
+  }
 };
 
 template <typename T>
@@ -87,6 +75,13 @@ struct EpiSwiGLU {  // act[m][c] = SiLU(gate) * up
   int ld;
   __device__ __forceinline__ void store2(int m, int c, float g, float u) const {
     stf(act + static_cast<size_t>(m) * ld + c, siluf_(g) * u);
+  }
+  // v holds SiLU(gate) * up already (the MFMA path forms it while staging)
+  __device__ __forceinline__ void emit8(int m, int c, const float* v) const {
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = v[e];
+    st8(act + static_cast<size_t>(m) * ld + c, x);
   }
 };
 
@@ -114,17 +109,75 @@ struct EpiScatter {
     const size_t o = static_cast<size_t>(t) * ld + n;
     stf(out + o, ldf(hbar + o) + sc * v);
   }
+  __device__ __forceinline__ void emit8(int m, int n, const float* v) const {
+    const int t = idx[m];
+    const float g = gate[t];
+    const float sc = ADAPTER ? 1.0f - g : g;
+    const size_t o = static_cast<size_t>(t) * ld + n;
+    float h[8];
+    ld8(hbar + o, h);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = h[e] + sc * v[e];
+    st8(out + o, h);
+  }
 };
 
 // ---------------------------------------------------------------------------
 // bf16 MFMA GEMM
+//
+// One workgroup of WM x WN waves computes a BM x BN tile; each wave owns a
+// (BM/WM) x (BN/WN) block of 32 x 32 MFMA tiles with fp32 accumulators in AGPRs.
+// K advances in 64-deep tiles through two LDS stages:
+//   * each stage is filled by wave-wide global_load_lds_dwordx4: one instruction
+//     moves 64 x 16 bytes into a contiguous 1 KiB of LDS, i.e. eight 128-byte
+//     tile rows; lane L lands in row 8b + L/8 at physical chunk L%8 and so loads
+//     logical chunk (L%8) ^ ((row/2)%8) of that row.  The fragment reads undo the
+//     XOR; with it, the 16 lanes of one LDS read phase (16 consecutive rows, one
+//     logical chunk) hit 16 distinct 16-byte slots of the 256-byte bank window;
+//   * within a k-tile the fragments of the next 16-deep k-step are read while the
+//     MFMAs of the current one run (two register sets, fenced by sched_barrier);
+//   * the workgroup barrier sits before the last k-step: by then every wave has
+//     read the whole stage, so the loads of tile k+2 can be issued into it and the
+//     first fragments of tile k+1 read while the last MFMAs of tile k run.
+// The epilogue stages each wave's results through LDS in 32-row blocks so that
+// every lane then handles 8 consecutive columns with 16-byte accesses.
 // ---------------------------------------------------------------------------
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ void load_lds16(const void* g, unsigned char* l) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void*)(l), 16, 0, 0);
+}
+
+__device__ __forceinline__ int swz(int row, int ch) { return row * ROWB + ((ch ^ ((row >> 1) & 7)) << 4); }
+
+template <int BM_, int BN_, int WM_, int WN_, bool DUAL_>
+struct Tile {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+  static constexpr bool DUAL = DUAL_;
+  static constexpr int NT = 64 * WM * WN;
+  static constexpr int NW = WM * WN;
+  static constexpr int WTM = BM / WM, WTN = BN / WN;
+  static constexpr int TM = WTM / 32, TN = WTN / 32;
+  static constexpr int STAGE = (BM + BN) * ROWB;
+  static constexpr int OUT_N = DUAL ? BN / 2 : BN;   // output columns per tile
+  static constexpr int ON = DUAL ? WTN / 2 : WTN;     // output columns per wave
+  static constexpr int OPAD = ON + 4;                 // staged row pitch (floats)
+  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole MFMA tiles");
+  static_assert(!DUAL || TN % 2 == 0, "gate/up tiles come in pairs");
+  static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "loader split");
+  static_assert(NW * 32 * OPAD * 4 <= 2 * STAGE, "epilogue staging must fit in the stages");
+};
 
 template <class C, class Epi>
 __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi,
                                                   const int* __restrict__ m_count, int M_fixed,
                                                   int K, int mt_max, int n_tiles) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE];
+  constexpr int NW = C::NW;
+  constexpr int A_LD = C::BM / 8 / NW;  // wave-wide loads per k-tile, A
+  constexpr int B_LD = C::BN / 8 / NW;
+  constexpr int KS = BK / 16;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * C::STAGE];
   const int per = gridDim.x >> 3;
   const int tile = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
   if (tile >= mt_max * n_tiles) return;
@@ -133,37 +186,54 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   const int m0 = mt * C::BM;
   if (m0 >= M) return;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int wm = wave / C::WN, wn = wave % C::WN;
+  const int rsub = lane >> 3;
 
-  // per-thread global sources and LDS destinations of the 16-byte chunks it moves
-  const bf16_t* a_src[C::A_CH];
-  int a_dst[C::A_CH];
+  const unsigned char* a_base = reinterpret_cast<const unsigned char*>(A.base);
+  uint32_t a_off[A_LD];
 #pragma unroll
-  for (int i = 0; i < C::A_CH; ++i) {
-    const int c = tid + i * C::NT, row = c >> 3, ch = c & 7;
-    const int m = min(m0 + row, M - 1);
-    a_src[i] = A.row(m) + ch * 8;
-    a_dst[i] = swz(row, ch);
+  for (int i = 0; i < A_LD; ++i) {
+    const int r = 8 * (i * NW + wave) + rsub;
+    const int ch = (lane & 7) ^ ((r >> 1) & 7);
+    const int m = min(m0 + r, M - 1);
+    const int row = A.idx ? A.idx[m] : m;
+    a_off[i] = static_cast<uint32_t>(row) * static_cast<uint32_t>(A.ld * 2) + ch * 16;
   }
-  const bf16_t* b_src[C::B_CH];
-  int b_dst[C::B_CH];
+  const unsigned char* b_base[B_LD];
+  uint32_t b_off[B_LD];
 #pragma unroll
-  for (int i = 0; i < C::B_CH; ++i) {
-    const int c = tid + i * C::NT, row = c >> 3, ch = c & 7;
-    const bf16_t* p;
-    if (C::DUAL) {
-      const int wb = row / C::WTN, q = row % C::WTN, h = C::WTN / 2;
-      const int col = nt * C::OUT_N + wb * h + (q % h);
-      p = (q < h) ? B.gate_row(col) : B.up_row(col);
+  for (int i = 0; i < B_LD; ++i) {
+    const int blk = i * NW + wave;  // 8-row block, wave-uniform
+    const int r = 8 * blk + rsub;
+    const int ch = (lane & 7) ^ ((r >> 1) & 7);
+    const bf16_t* base;
+    int row;
+    if constexpr (C::DUAL) {
+      const int wb = (8 * blk) / C::WTN, q0 = (8 * blk) % C::WTN, h = C::WTN / 2;
+      const bool up = q0 >= h;
+      base = up ? B.b1 : B.b0;
+      row = nt * C::OUT_N + wb * h + (r % C::WTN) - (up ? h : 0);
     } else {
-      p = B.row(nt * C::BN + row);
+      const bool second = nt * C::BN + 8 * blk >= B.split;
+      base = second ? B.b1 : B.b0;
+      row = nt * C::BN + r - (second ? B.split : 0);
     }
-    b_src[i] = p + ch * 8;
-    b_dst[i] = C::BM * ROWB + swz(row, ch);
+    b_base[i] = reinterpret_cast<const unsigned char*>(base);
+    b_off[i] = static_cast<uint32_t>(row) * static_cast<uint32_t>(B.ld * 2) + ch * 16;
   }
 
-  u32x4 ra[C::A_CH], rb[C::B_CH];
+  auto issue = [&](int stage, int k0) {
+    unsigned char* sa = smem + stage * C::STAGE;
+    const uint32_t kb = static_cast<uint32_t>(k0) * 2;
+#pragma unroll
+    for (int i = 0; i < A_LD; ++i) load_lds16(a_base + a_off[i] + kb, sa + (i * NW + wave) * 1024);
+#pragma unroll
+    for (int i = 0; i < B_LD; ++i)
+      load_lds16(b_base[i] + b_off[i] + kb, sa + C::BM * ROWB + (i * NW + wave) * 1024);
+  };
+
   f32x16 acc[C::TM][C::TN];
 #pragma unroll
   for (int a = 0; a < C::TM; ++a)
@@ -172,85 +242,88 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  const int nk = K / BK;
+  int fa_row[C::TM], fb_row[C::TN];
 #pragma unroll
-  for (int i = 0; i < C::A_CH; ++i) ra[i] = *reinterpret_cast<const u32x4*>(a_src[i]);
+  for (int a = 0; a < C::TM; ++a) fa_row[a] = wm * C::WTM + a * 32 + (lane & 31);
 #pragma unroll
-  for (int i = 0; i < C::B_CH; ++i) rb[i] = *reinterpret_cast<const u32x4*>(b_src[i]);
+  for (int b = 0; b < C::TN; ++b) fb_row[b] = C::BM + wn * C::WTN + b * 32 + (lane & 31);
+  const int khalf = lane >> 5;
+  bf16x8 fa[2][C::TM], fb[2][C::TN];
+  auto read_frags = [&](int buf, const unsigned char* st, int ks) {
+    const int c = 2 * ks + khalf;
 #pragma unroll
-  for (int i = 0; i < C::A_CH; ++i) *reinterpret_cast<u32x4*>(smem + a_dst[i]) = ra[i];
+    for (int a = 0; a < C::TM; ++a) fa[buf][a] = *reinterpret_cast<const bf16x8*>(st + swz(fa_row[a], c));
 #pragma unroll
-  for (int i = 0; i < C::B_CH; ++i) *reinterpret_cast<u32x4*>(smem + b_dst[i]) = rb[i];
-  __syncthreads();
+    for (int b = 0; b < C::TN; ++b) fb[buf][b] = *reinterpret_cast<const bf16x8*>(st + swz(fb_row[b], c));
+  };
+  auto mfmas = [&](int buf) {
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+      for (int b = 0; b < C::TN; ++b)
+        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][a], fb[buf][b], acc[a][b], 0, 0, 0);
+  };
 
+  const int nk = K / BK;
+  issue(0, 0);
+  if (nk > 1) issue(1, BK);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  read_frags(0, smem, 0);
   for (int kt = 0; kt < nk; ++kt) {
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int k1 = (kt + 1) * BK;
+    const unsigned char* st = smem + (kt & 1) * C::STAGE;
 #pragma unroll
-      for (int i = 0; i < C::A_CH; ++i) ra[i] = *reinterpret_cast<const u32x4*>(a_src[i] + k1);
-#pragma unroll
-      for (int i = 0; i < C::B_CH; ++i) rb[i] = *reinterpret_cast<const u32x4*>(b_src[i] + k1);
+    for (int ks = 0; ks < KS - 1; ++ks) {
+      read_frags((ks + 1) & 1, st, ks + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      mfmas(ks & 1);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    const unsigned char* sa = smem + (kt & 1) * C::STAGE;
-    const unsigned char* sb = sa + C::BM * ROWB;
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int ch = 2 * ks + (lane >> 5);
-      bf16x8 fa[C::TM], fb[C::TN];
-#pragma unroll
-      for (int a = 0; a < C::TM; ++a) {
-        const int row = wm * C::WTM + a * 32 + (lane & 31);
-        fa[a] = *reinterpret_cast<const bf16x8*>(sa + swz(row, ch));
-      }
-#pragma unroll
-      for (int b = 0; b < C::TN; ++b) {
-        const int row = wn * C::WTN + b * 32 + (lane & 31);
-        fb[b] = *reinterpret_cast<const bf16x8*>(sb + swz(row, ch));
-      }
-#pragma unroll
-      for (int a = 0; a < C::TM; ++a)
-#pragma unroll
-        for (int b = 0; b < C::TN; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
-    }
-    if (more) {
-      unsigned char* nxt = smem + ((kt + 1) & 1) * C::STAGE;
-#pragma unroll
-      for (int i = 0; i < C::A_CH; ++i) *reinterpret_cast<u32x4*>(nxt + a_dst[i]) = ra[i];
-#pragma unroll
-      for (int i = 0; i < C::B_CH; ++i) *reinterpret_cast<u32x4*>(nxt + b_dst[i]) = rb[i];
-    }
+    // every wave has read all of stage kt and the loads of tile kt+1 have landed
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __syncthreads();
+    if (kt + 2 < nk) issue(kt & 1, (kt + 2) * BK);
+    if (kt + 1 < nk) read_frags(KS & 1, smem + ((kt + 1) & 1) * C::STAGE, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas((KS - 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);
   }
 
-  // epilogue: D[i][j] of an MFMA tile sits in lane j + 32*((i/4)&1), register 4*(i/8) + i%4
+  // epilogue: 32-row blocks of each wave's results go through LDS (fp32, padded rows),
+  // then each lane emits 8 consecutive columns
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  float* stg = reinterpret_cast<float*>(smem) + wave * (32 * C::OPAD);
 #pragma unroll
   for (int a = 0; a < C::TM; ++a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int i = wm * C::WTM + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      const int m = m0 + i;
-      if (m >= M) continue;
+      const int i = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       if constexpr (C::DUAL) {
 #pragma unroll
         for (int b = 0; b < C::TN / 2; ++b) {
-          const int c = nt * C::OUT_N + wn * (C::WTN / 2) + b * 32 + (lane & 31);
-          epi.store2(m, c, acc[a][b][r], acc[a][b + C::TN / 2][r]);
+          const float g = acc[a][b][r], u = acc[a][b + C::TN / 2][r];
+          stg[i * C::OPAD + b * 32 + (lane & 31)] = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
         }
       } else {
 #pragma unroll
-        for (int b = 0; b < C::TN; ++b) {
-          const int n = nt * C::BN + wn * C::WTN + b * 32 + (lane & 31);
-          epi.store(m, n, acc[a][b][r]);
-        }
+        for (int b = 0; b < C::TN; ++b) stg[i * C::OPAD + b * 32 + (lane & 31)] = acc[a][b][r];
+      }
+    }
+    constexpr int CPR = C::ON / 8;   // 8-column pieces per staged row
+    for (int e = lane; e < 32 * CPR; e += 64) {
+      const int i = e / CPR, c8 = (e % CPR) * 8;
+      const int m = m0 + wm * C::WTM + a * 32 + i;
+      if (m < M) {
+        const float* v = stg + i * C::OPAD + c8;
+        epi.emit8(m, nt * C::OUT_N + wn * C::ON + c8, v);
       }
     }
   }
 }
 
 template <class C, class Epi>
-hipError_t run_mfma(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_count, int M_max,
+hipError_t run_tile(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_count, int M_max,
                     int N_out, int K, hipStream_t s) {
   const int mt_max = (M_max + C::BM - 1) / C::BM;
   const int n_tiles = N_out / C::OUT_N;
@@ -259,6 +332,25 @@ hipError_t run_mfma(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_coun
   const int grid = (total + 7) / 8 * 8;
   mfma_gemm<C, Epi><<<grid, C::NT, 0, s>>>(A, B, epi, m_count, M_max, K, mt_max, n_tiles);
   return hipGetLastError();
+}
+
+// Number of 256-CU rounds times the tile height: proportional to the time of a
+// launch whose tiles all cost the same per row.
+int tile_cost(int M, int BM, int n_tiles) {
+  const int tiles = (M + BM - 1) / BM * n_tiles;
+  return (tiles + 255) / 256 * BM;
+}
+
+// Big-tile launch: 256 or 192 rows per tile, whichever finishes in fewer CU-rounds.
+template <int BN, bool DUAL, class Epi>
+hipError_t run_big(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_count, int M_max,
+                   int N_out, int K, hipStream_t s) {
+  using T256 = Tile<256, BN, 2, 2, DUAL>;
+  using T192 = Tile<192, BN, 2, 2, DUAL>;
+  const int n_tiles = N_out / T256::OUT_N;
+  if (tile_cost(M_max, 192, n_tiles) < tile_cost(M_max, 256, n_tiles))
+    return run_tile<T192>(A, B, epi, m_count, M_max, N_out, K, s);
+  return run_tile<T256>(A, B, epi, m_count, M_max, N_out, K, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -457,10 +549,7 @@ int adapter_groups(int K) {
   return G;
 }
 
-// tile shapes
 using TileRouter = Tile<64, 128, 2, 2, false>;
-using TileGateUp = Tile<256, 256, 2, 2, true>;
-using TileDown = Tile<256, 256, 2, 2, false>;
 
 }  // namespace
 
@@ -471,7 +560,7 @@ hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, con
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(hbar), nullptr, d};
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_hd), static_cast<const bf16_t*>(ps1), d_e, d};
-    return run_mfma<TileRouter>(A, B, epi, nullptr, T, N, d, s);
+    return run_tile<TileRouter>(A, B, epi, nullptr, T, N, d, s);
   }
   ARows<float> A{static_cast<const float*>(hbar), nullptr, d};
   BRows<float> B{static_cast<const float*>(w_hd), static_cast<const float*>(ps1), d_e, d};
@@ -485,8 +574,8 @@ hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(u), idx_ffn, d};
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), INT_MAX, d};
-    return run_mfma<TileGateUp>(A, B, EpiSwiGLU<bf16_t>{static_cast<bf16_t*>(act), d_ff}, counts,
-                                n_max, d_ff, d, s);
+    return run_big<256, true>(A, B, EpiSwiGLU<bf16_t>{static_cast<bf16_t*>(act), d_ff}, counts,
+                              n_max, d_ff, d, s);
   }
   ARows<float> A{static_cast<const float*>(u), idx_ffn, d};
   BRows<float> B{static_cast<const float*>(w_gate), static_cast<const float*>(w_up), INT_MAX, d};
@@ -503,7 +592,7 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_down), nullptr, INT_MAX, d_ff};
     EpiScatter<bf16_t, false> epi{idx_ffn, static_cast<const bf16_t*>(hbar), gate,
                                   static_cast<bf16_t*>(h_out), d};
-    return run_mfma<TileDown>(A, B, epi, counts, n_max, d, d_ff, s);
+    return run_big<256, false>(A, B, epi, counts, n_max, d, d_ff, s);
   }
   ARows<float> A{static_cast<const float*>(act), nullptr, d_ff};
   BRows<float> B{static_cast<const float*>(w_down), nullptr, INT_MAX, d_ff};
