@@ -72,7 +72,9 @@ def kernel_work(w, n_f, n_a, T, j):
     return {
         "rowstats": dict(flops=0, bytes=T * (hid_reads * d * es + d * es + 16)),
         "router_gemm": dict(flops=2 * d * npre * T, bytes=T * (d * es + 4 * npre)),
-        "router_tail": dict(flops=0, bytes=T * (state_rw + 4 * npre + 16 + 8 * 2 + 8)),
+        "router_pre": dict(flops=0, bytes=T * (4 * npre + 16 + 8 + 4 * (4 * dm + w.d_head + 1))),
+        "router_mem": dict(flops=0, bytes=T * (state_rw + 4 * 3 * dm + 4 * dm)),
+        "router_post": dict(flops=0, bytes=T * (4 * (dm + dm + w.d_head + 1) + 8 * 2 + 8)),
         "select": dict(flops=0, bytes=T * (4 + 1 + 4)),
         "ffn_gate_up": dict(flops=4 * d * dff * n_f, bytes=n_f * (d * es + dff * es) + 2 * d * dff * es),
         "ffn_down": dict(flops=2 * d * dff * n_f, bytes=n_f * (dff * es + 2 * d * es) + d * dff * es),

@@ -72,8 +72,9 @@ typedef enum hero_mode {
  * encoder's, d_head the history/local heads' hidden width (Sec. 4.1: 256); the
  * comparison space of W_n, W_c has width d_m.
  * Supported: d % 256 == 0 (bf16) or d % 128 == 0 (f32); bf16 also needs
- * d_ff % 128 == 0, d_r % 64 == 0 and (d_e + d_head) % 128 == 0; d_m in
- * {32, 64, 128, 256}; d_s <= 128; d_e, d_head <= 512; d_p <= 128.
+ * d_ff % 128 == 0, d_r in {32, 64, 96, 128}, d_s % 8 == 0, d_e % 64 == 0 and
+ * (d_e + d_head) % 128 == 0; d_m in
+ * {32, 64, 128, 256}; d_s <= 128; d_e, d_head <= 256; d_p <= 128.
  */
 typedef struct hero_dims {
   int d, d_ff, d_r, L_R;
@@ -101,9 +102,15 @@ typedef struct hero_adapter_weights {
  *   w_p1 [d_p][6], w_p2 [d_a][d_p]         path encoder z_a = FFN_path(x_path)
  *   w_q, w_k, w_v [d_m][d_s]               memory projections
  *   w_n [d_m][d_s], w_c [d_m][d_m]         comparison projections of nu
- *   th1 [d_head][d_s + d_m + 1], th2 [d_head]   history head f_theta([s; c; nu])
+ *   th1 [d_head][HERO_TH1_PITCH(d_s, d_m)], th2 [d_head]
+ *                                          history head f_theta([s; c; nu]): row o holds the
+ *                                          d_s + d_m + 1 input weights, then zero padding to a
+ *                                          multiple of 8 elements (16-byte rows in bf16); the
+ *                                          padding is never read
  *   ps1 [d_head][d], ps2 [d_head]          local head f_psi(hbar)
  */
+#define HERO_TH1_PITCH(d_s, d_m) ((((d_s) + (d_m) + 1) + 7) / 8 * 8)
+
 typedef struct hero_router_weights {
   const void *w_hd, *w_hu, *w_p1, *w_p2, *w_q, *w_k, *w_v, *w_n, *w_c;
   const void *th1, *th2, *ps1, *ps2;
@@ -144,15 +151,17 @@ typedef struct hero_layer_stats {
 
 /* Kernels of one routed layer, in launch order (for hero_kernel_timer). */
 typedef enum hero_kernel {
-  HERO_K_ROWSTATS = 0,      /* inv_rms, residual-transition sums, u = RMSNorm_w(hbar)        */
-  HERO_K_ROUTER_GEMM = 1,   /* [W_hd; psi_1] hbar                                             */
-  HERO_K_ROUTER_TAIL = 2,   /* router state, memory read-modify-write, heads, gate           */
-  HERO_K_SELECT = 3,        /* branch decision and ordered compaction                         */
-  HERO_K_FFN_GATE_UP = 4,   /* SiLU(W_g u) * (W_u u) over the FFN tokens                      */
-  HERO_K_FFN_DOWN = 5,      /* W_d act, scattered as hbar + g y                               */
-  HERO_K_ADAPTER_DOWN = 6,  /* W_1 u over the adapter tokens (partial sums)                   */
-  HERO_K_ADAPTER_UP = 7,    /* W_2 SiLU(.), scattered as hbar + (1 - g) y                     */
-  HERO_K_COUNT = 8
+  HERO_K_ROWSTATS = 0,      /* inv_rms, residual-transition sums, u = RMSNorm_w(hbar)          */
+  HERO_K_ROUTER_GEMM = 1,   /* [W_hd; psi_1] hbar                                               */
+  HERO_K_ROUTER_PRE = 2,    /* router state s, phi(q), phi(k), v, W_n s, local head            */
+  HERO_K_ROUTER_MEM = 3,    /* memory read c and write S, zeta (one pass over the state)       */
+  HERO_K_ROUTER_POST = 4,   /* nu, history head, p, m, logit, gate                             */
+  HERO_K_SELECT = 5,        /* branch decision and ordered compaction                           */
+  HERO_K_FFN_GATE_UP = 6,   /* SiLU(W_g u) * (W_u u) over the FFN tokens                        */
+  HERO_K_FFN_DOWN = 7,      /* W_d act, scattered as hbar + g y                                 */
+  HERO_K_ADAPTER_DOWN = 8,  /* W_1 u over the adapter tokens (partial sums)                     */
+  HERO_K_ADAPTER_UP = 9,    /* W_2 SiLU(.), scattered as hbar + (1 - g) y                       */
+  HERO_K_COUNT = 10
 } hero_kernel;
 
 /*

@@ -26,7 +26,7 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
 }
 
 struct Layout {
-  size_t u, P, rowstat, logit, gate, mask, idx_ffn, idx_ad, counts, lambda, act, part, ring, total;
+  size_t u, P, rowstat, logit, gate, mask, idx_ffn, idx_ad, counts, lambda, act, part, rscr, ring, total;
 };
 
 Layout layout_of(const hero_dims& d, int T, bool stack) {
@@ -50,6 +50,7 @@ Layout layout_of(const hero_dims& d, int T, bool stack) {
   L.lambda = take(16);
   L.act = take(t * d.d_ff * es);
   L.part = take(hero::adapter_part_floats(d.dtype, d.d, d.d_r, T) * 4);
+  L.rscr = take(hero::router_scratch_floats(d.d_m, d.d_head, T) * 4);
   L.ring = stack ? take(3 * t * d.d * es) : 0;
   L.total = off;
   return L;
@@ -65,10 +66,10 @@ int check_dims(const hero_dims* d) {
   if (!(d->eps_norm >= 0.f) || !(d->eps > 0.f) || !(d->T_hist > 0.f)) return HERO_E_RANGE;
   // kernel support
   if (d->d_m != 32 && d->d_m != 64 && d->d_m != 128 && d->d_m != 256) return HERO_E_UNSUPPORTED;
-  if (d->d_s > 128 || d->d_e > 512 || d->d_head > 512 || d->d_p > 128) return HERO_E_UNSUPPORTED;
+  if (d->d_s > 128 || d->d_e > 256 || d->d_head > 256 || d->d_p > 128) return HERO_E_UNSUPPORTED;
   if (d->dtype == HERO_BF16) {
     if (d->d % 256 || d->d_ff % 128 || d->d_e % 64 || (d->d_e + d->d_head) % 128) return HERO_E_UNSUPPORTED;
-    if (d->d_r % 32 || d->d_r > 128) return HERO_E_UNSUPPORTED;
+    if (d->d_r % 32 || d->d_r > 128 || d->d_s % 8) return HERO_E_UNSUPPORTED;
   } else {
     if (d->d % 128) return HERO_E_UNSUPPORTED;
   }
@@ -226,6 +227,7 @@ int run_layer(const LayerCall& c) {
   ra.w_n = c.rt->w_n;
   ra.w_c = c.rt->w_c;
   ra.th1 = c.rt->th1;
+  ra.ld_th1 = HERO_TH1_PITCH(D.d_s, D.d_m);
   ra.th2 = c.rt->th2;
   ra.ps2 = c.rt->ps2;
   ra.beta = c.rc->logit_bias;
@@ -235,7 +237,19 @@ int run_layer(const LayerCall& c) {
   ra.m_hist = c.st->m_hist;
   ra.logit = logit;
   ra.gate = gate;
-  e = timed(HERO_K_ROUTER_TAIL, st, [&] { return launch_router_tail(ra, st); });
+  {
+    float* r = reinterpret_cast<float*>(ws + L.rscr);
+    const size_t t = static_cast<size_t>(T);
+    ra.qkvn = r;
+    ra.hs = r + t * 4 * D.d_m;
+    ra.cvec = ra.hs + t * D.d_head;
+    ra.bvec = ra.cvec + t * D.d_m;
+  }
+  e = timed(HERO_K_ROUTER_PRE, st, [&] { return launch_router_pre(ra, st); });
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = timed(HERO_K_ROUTER_MEM, st, [&] { return launch_router_mem(ra, st); });
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = timed(HERO_K_ROUTER_POST, st, [&] { return launch_router_post(ra, st); });
   if (e != hipSuccess) return HERO_E_LAUNCH;
 
   SelectArgs sa{};

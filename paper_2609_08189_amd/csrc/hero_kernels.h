@@ -25,6 +25,7 @@ struct RouterTailArgs {
   const float* P;         // [T][d_e + d_head]
   const float* rowstat;   // [T][4]
   const void *w_hu, *w_p1, *w_p2, *w_q, *w_k, *w_v, *w_n, *w_c, *th1, *th2, *ps2;
+  int ld_th1;             // row pitch of th1 (elements)
   const float* beta;      // [T] or null
   float* S;               // [T][d_m][d_m]   in/out
   float* zeta;            // [T][d_m]        in/out
@@ -32,8 +33,19 @@ struct RouterTailArgs {
   float* m_hist;          // [T]             in/out
   float* logit;           // [T]
   float* gate;            // [T]
+  // intermediates between the three router kernels (router_scratch_floats(d_m, d_head, T))
+  float* qkvn;            // [T][4][d_m]  phi(q), phi(k), v, W_n s
+  float* hs;              // [T][d_head]  th1[:, :d_s] s
+  float* cvec;            // [T][d_m]     memory read c
+  float* bvec;            // [T]          local-head logit b
 };
-hipError_t launch_router_tail(const RouterTailArgs& a, hipStream_t s);
+size_t router_scratch_floats(int d_m, int d_head, int T);
+// router state, q/k/v, W_n s, the s part of the history head, local head
+hipError_t launch_router_pre(const RouterTailArgs& a, hipStream_t s);
+// streaming memory read-modify-write (one token per workgroup)
+hipError_t launch_router_mem(const RouterTailArgs& a, hipStream_t s);
+// nu, history head, p, m, logit and gate
+hipError_t launch_router_post(const RouterTailArgs& a, hipStream_t s);
 
 // Branch decision and ordered compaction (one workgroup).
 struct SelectArgs {

@@ -1,33 +1,37 @@
-// Fused router tail with the depth-memory read-modify-write (Sec. 3.2).
+// Router of one routed layer after the two large projections (Sec. 3.2), as three kernels:
 //
-// One workgroup of 256 threads takes TB consecutive tokens.  From the router
-// pre-activations P = [W_hd hbar; psi_1 hbar] and the row statistics it forms,
-// per token and in the paper's order:
-//   z^h = W_hu SiLU(inv_rms * W_hd hbar)                         (hidden encoder, unit-gain RMSNorm)
-//   x^path = [j/L_R, (L_R-j)/L_R, |delta_j|, gamma_j, p_{j-1}, m_{j-1}]   (eq:path_vector)
-//   z^a = W_p2 SiLU(W_p1 x^path),  s = [z^h; z^a]                (eq:router_state)
-//   q, k, v = W_q s, W_k s, W_v s
-//   one streaming pass over S (fp32, d_m x d_m per token):
-//     c = phi(q)^T S / (phi(q)^T zeta + eps)                     (eq:memory_read, read first)
-//     S <- rho S + phi(k) v^T,  zeta <- rho zeta + phi(k)         (eq:memory_update, same pass)
-//   nu = 1 - cos(W_n s, W_c c) (0 at j = 1)
-//   a = th2 . SiLU(th1 [s; c; nu]),  p = sigma(a / T_hist),  m = m_{j-1} p
-//   b = ps2 . SiLU(psi_1 hbar),  logit = a + b (+ bias),  g = sigma(logit)   (eq:final_gate)
-// At j = 1 the state is the paper's initial value: S and zeta are not read (taken
-// as zero) and p_{0} = m_{0} = 1.
-// The S pass is the HBM-bound part (2 * 4 * d_m^2 bytes per token); the small
-// matrix-vector products reuse each weight element across the TB tokens.
+//   router_pre   (8 tokens per workgroup, reuses each weight across them)
+//     z^h = W_hu SiLU(inv_rms * W_hd hbar)                       hidden encoder (unit-gain RMSNorm)
+//     x^path = [j/L_R, (L_R-j)/L_R, |delta_j|, gamma_j, p_{j-1}, m_{j-1}]   (eq:path_vector,
+//                                                                 eq:transition_features)
+//     z^a = W_p2 SiLU(W_p1 x^path),  s = [z^h; z^a]              (eq:router_state)
+//     phi(q), phi(k), v, W_n s;  th1[:, :d_s] s (the s part of the history head's input layer)
+//     b = ps2 . SiLU(psi_1 hbar)                                  local head (eq:final_gate)
+//   router_mem   (one token per workgroup: a streaming read-modify-write of the memory)
+//     c = phi(q)^T S / (phi(q)^T zeta + eps)                      (eq:memory_read, read first)
+//     S <- rho S + phi(k) v^T,  zeta <- rho zeta + phi(k)          (eq:memory_update, same pass)
+//   router_post  (8 tokens per workgroup)
+//     nu = 1 - cos(W_n s, W_c c)  (0 at j = 1)
+//     a = th2 . SiLU(th1 [s; c; nu]),  p = sigma(a / T_hist),  m = m_{j-1} p
+//     logit = a + b (+ bias),  g = sigma(logit)
+// At j = 1 the incoming state is the paper's initial value: S and zeta are not read
+// (taken as zero) and p_0 = m_0 = 1.
+// The memory kernel moves 2 * 4 * (d_m^2 + d_m) bytes of state per token and is the
+// HBM-bound part; keeping it free of the matrix-vector work lets many workgroups per
+// CU keep HBM busy.  All arithmetic is fp32.
 #include "hero_device.h"
 #include "hero_kernels.h"
 
 namespace hero {
 namespace {
 
-constexpr int TB = 8;     // tokens per workgroup
+constexpr int TB = 16;    // tokens per workgroup (pre / post)
 constexpr int NT = 256;   // threads per workgroup
-constexpr int MAXE = 512; // max(d_e, d_head)
+constexpr int MAXE = 256; // max(d_e, d_head)
+constexpr int KC = 32;    // weight columns staged per step of block_matmul
 constexpr int MAXS = 128; // max d_s
 constexpr int MAXP = 128; // max d_p
+constexpr int MAXM = 256; // max d_m
 
 struct Ident {
   __device__ __forceinline__ float operator()(float x) const { return x; }
@@ -35,16 +39,24 @@ struct Ident {
 struct SiLU {
   __device__ __forceinline__ float operator()(float x) const { return siluf_(x); }
 };
+struct Phi {
+  __device__ __forceinline__ float operator()(float x) const { return phif_(x); }
+};
 
-// out[t*os + o] = act(sum_i W[o*ldw + i] * in[t*is + i]) for o < O and all TB tokens.
-// P lanes share one output row (power of two, within a wave) and reduce by shuffles.
+// out[t*os + o] = act(sum_i W[o*ldw + i] * in[t*is + i]) for o < O and tokens t < nvalid.
+// P lanes share one output row (power of two, within a wave) and reduce by shuffles;
+// each lane takes 8 consecutive inputs per step, loaded as one 16-byte vector when
+// the row pitch allows it and as 8 independent loads otherwise.
 template <typename W, class Act>
 __device__ __forceinline__ void matvec(const W* __restrict__ w, int ldw, int O, int I,
-                                       const float* in, int is, float* out, int os, Act act) {
+                                       const float* in, int is, float* out, int os, Act act,
+                                       int nvalid = TB) {
   int P = 64;
   while (P > 1 && P * O > NT) P >>= 1;
+  while (P > 1 && 8 * (P >> 1) >= I) P >>= 1;   // no lane without work
   const int rows_per_pass = NT / P;
   const int slice = threadIdx.x % P;
+  const bool vec = (ldw % 8 == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
   for (int o0 = 0; o0 < O; o0 += rows_per_pass) {
     const int o = o0 + static_cast<int>(threadIdx.x) / P;
     float acc[TB];
@@ -52,10 +64,21 @@ __device__ __forceinline__ void matvec(const W* __restrict__ w, int ldw, int O, 
     for (int t = 0; t < TB; ++t) acc[t] = 0.f;
     if (o < O) {
       const W* wr = w + static_cast<size_t>(o) * ldw;
-      for (int i = slice; i < I; i += P) {
-        const float wv = ldf(wr + i);
+      for (int i = 8 * slice; i < I; i += 8 * P) {
+        float wv[8];
+        if (vec && i + 8 <= I) {
+          ld8(wr + i, wv);
+        } else {
 #pragma unroll
-        for (int t = 0; t < TB; ++t) acc[t] = fmaf(wv, in[t * is + i], acc[t]);
+          for (int e = 0; e < 8; ++e) wv[e] = (i + e < I) ? ldf(wr + i + e) : 0.f;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if (i + e < I) {
+#pragma unroll
+            for (int t = 0; t < TB; ++t) acc[t] = fmaf(wv[e], in[t * is + i + e], acc[t]);
+          }
+        }
       }
     }
     for (int off = P >> 1; off > 0; off >>= 1)
@@ -63,39 +86,132 @@ __device__ __forceinline__ void matvec(const W* __restrict__ w, int ldw, int O, 
       for (int t = 0; t < TB; ++t) acc[t] += __shfl_xor(acc[t], off, kWave);
     if (o < O && slice == 0)
 #pragma unroll
-      for (int t = 0; t < TB; ++t) out[t * os + o] = act(acc[t]);
+      for (int t = 0; t < TB; ++t)
+        if (t < nvalid) out[t * os + o] = act(acc[t]);
   }
 }
 
-template <typename W, int DM>
-__global__ __launch_bounds__(NT) void router_tail_kernel(RouterTailArgs a) {
-  constexpr int C4 = DM / 4;        // float4 columns of one S row
-  constexpr int RP = NT / C4;       // S rows per pass
-  constexpr int NR = DM / RP;       // S rows per thread
-  constexpr int XIN = MAXS + DM + 1;
+// out[t*os + o] = act(bias[t*bs + o] + sum_i W[o*ldw + i] * X[t*ldx + i]) for o < O (<= 256) and
+// tokens t < nvalid, all TB tokens computed.  Weight columns are staged KC at a time into LDS,
+// transposed to [k][o] and converted to fp32, with loads that are contiguous along each
+// row; each thread then accumulates a tile of RO rows x 4 tokens, reading one RO-wide weight
+// vector and four broadcast inputs per k.
+template <int RO, typename W, class Act>
+__device__ __forceinline__ void block_matmul_ro(const W* __restrict__ w, int ldw, int O, int I,
+                                                const float* X, int ldx, const float* bias, int bs,
+                                                float* out, int os, Act act, float* wst, int nvalid) {
+  constexpr int OPAD = 4 * 64 + 4;   // staged row pitch (floats)
+  const int tid = threadIdx.x;
+  const int og = tid >> 2, tg = tid & 3;   // rows og*RO.., tokens 4*tg..
+  float acc[RO][4];
+#pragma unroll
+  for (int r = 0; r < RO; ++r)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[r][q] = 0.f;
+  constexpr int U = 4 * 64 * KC / NT;   // staged elements per thread (rows <= 256)
+  for (int i0 = 0; i0 < I; i0 += KC) {
+    // all of this thread's loads are issued before any is used
+    float tmp[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int e = tid + NT * u;
+      const int o = e / KC, k = e % KC;
+      tmp[u] = (o < O && i0 + k < I) ? ldf(w + static_cast<size_t>(o) * ldw + i0 + k) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int e = tid + NT * u;
+      const int o = e / KC, k = e % KC;
+      if (o < O) wst[k * OPAD + o] = tmp[u];
+    }
+    __syncthreads();
+    if (og * RO < O) {
+      const int kn = min(KC, I - i0);
+      for (int k = 0; k < kn; ++k) {
+        float wv[RO];
+#pragma unroll
+        for (int r = 0; r < RO; ++r) wv[r] = wst[k * OPAD + og * RO + r];
+        float xv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) xv[q] = X[(4 * tg + q) * ldx + i0 + k];
+#pragma unroll
+        for (int r = 0; r < RO; ++r)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[r][q] = fmaf(wv[r], xv[q], acc[r][q]);
+      }
+    }
+  }
+  if (og * RO < O) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int t = 4 * tg + q;
+      if (t >= nvalid) continue;
+#pragma unroll
+      for (int r = 0; r < RO; ++r) {
+        const int o = og * RO + r;
+        if (o < O) out[t * os + o] = act(acc[r][q] + (bias ? bias[t * bs + o] : 0.f));
+      }
+    }
+  }
+}
+
+template <typename W, class Act>
+__device__ __forceinline__ void block_matmul(const W* w, int ldw, int O, int I, const float* X, int ldx,
+                                             const float* bias, int bs, float* out, int os, Act act,
+                                             float* wst, int nvalid = TB) {
+  if (O > 128)
+    block_matmul_ro<4>(w, ldw, O, I, X, ldx, bias, bs, out, os, act, wst, nvalid);
+  else if (O > 64)
+    block_matmul_ro<2>(w, ldw, O, I, X, ldx, bias, bs, out, os, act, wst, nvalid);
+  else
+    block_matmul_ro<1>(w, ldw, O, I, X, ldx, bias, bs, out, os, act, wst, nvalid);
+  __syncthreads();
+}
+
+// for (e = tid; e < n; e += NT) f(e, src(e)), with eight loads in flight per thread
+template <class Src, class F>
+__device__ __forceinline__ void batched(int n, Src src, F f) {
+  for (int e0 = threadIdx.x; e0 < n; e0 += 8 * NT) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + NT * u;
+      v[u] = e < n ? src(e) : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + NT * u;
+      if (e < n) f(e, v[u]);
+    }
+  }
+}
+
 #define LDS16 __shared__ __attribute__((aligned(16)))
-  LDS16 float bufA[TB][MAXE];       // SiLU(inv_rms W_hd hbar), later the f_theta hidden
-  LDS16 float bufB[TB][MAXE];       // SiLU(psi_1 hbar)
-  LDS16 float x[TB][XIN];           // [s; c; nu]
-  LDS16 float xp[TB][8];            // path vector
-  LDS16 float zp[TB][MAXP];         // path-encoder hidden
-  LDS16 float qkvn[4][TB][DM];      // phi(q), phi(k), v, W_n s
-  LDS16 float wc[TB][DM];           // W_c c
-  LDS16 f32x4 red[RP][C4];          // partial memory reads
-  LDS16 float sc[8][TB];            // per-token scalars
-#undef LDS16
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// ---------------------------------------------------------------------------
+// router_pre
+// ---------------------------------------------------------------------------
+template <typename W>
+__global__ __launch_bounds__(NT) void router_pre_kernel(RouterTailArgs a) {
+  constexpr int EP = MAXE + 4;
+  LDS16 float bufA[TB][EP];     // SiLU(inv_rms W_hd hbar)
+  LDS16 float bufB[TB][EP];     // SiLU(psi_1 hbar)
+  LDS16 float s[TB][MAXS + 4];  // router state
+  LDS16 float xp[TB][8];        // path vector
+  LDS16 float zp[TB][MAXP];     // path-encoder hidden
+  LDS16 float wst[KC * (4 * 64 + 4)];
+  LDS16 float sc[TB];
+
+  const int tid = threadIdx.x;
   const int t0 = blockIdx.x * TB;
+  const int nvalid = min(TB, a.T - t0);
   const int j = a.j;
-  const int d_s = a.d_s, d_e = a.d_e, d_head = a.d_head, NP = a.d_e + a.d_head;
-  const float rho = 1.0f / (1.0f + expf(-a.eta));
-  const W* w_hu = static_cast<const W*>(a.w_hu);
+  const int d_e = a.d_e, d_head = a.d_head, NP = a.d_e + a.d_head, DM = a.d_m;
 
-  // per-token scalars and the path vector
   if (tid < TB) {
     const int t = t0 + tid;
-    float inv_rms = 0.f, dd = 0.f, dp = 0.f, pp = 0.f, pprev = 1.f, mprev = 1.f, beta = 0.f;
+    float inv_rms = 0.f, dd = 0.f, dp = 0.f, pp = 0.f, pprev = 1.f, mprev = 1.f;
     if (t < a.T) {
       const f32x4 rs = *reinterpret_cast<const f32x4*>(a.rowstat + 4 * static_cast<size_t>(t));
       inv_rms = rs[0];
@@ -106,7 +222,6 @@ __global__ __launch_bounds__(NT) void router_tail_kernel(RouterTailArgs a) {
         pprev = a.p_hist[t];
         mprev = a.m_hist[t];
       }
-      if (a.beta) beta = a.beta[t];
     }
     const float dj = j >= 2 ? sqrtf(dd) : 0.f;
     const float gam = j >= 3 ? dp / (dj * sqrtf(pp) + a.eps) : 0.f;
@@ -116,112 +231,158 @@ __global__ __launch_bounds__(NT) void router_tail_kernel(RouterTailArgs a) {
     xp[tid][3] = gam;
     xp[tid][4] = pprev;
     xp[tid][5] = mprev;
-    sc[0][tid] = inv_rms;
-    sc[1][tid] = mprev;
-    sc[2][tid] = beta;
+    sc[tid] = inv_rms;
   }
   __syncthreads();
-
-  // SiLU of the encoder and local-head pre-activations
-  for (int e = tid; e < TB * NP; e += NT) {
-    const int tt = e / NP, i = e % NP;
-    const int t = min(t0 + tt, a.T - 1);
-    const float pv = a.P[static_cast<size_t>(t) * NP + i];
-    if (i < d_e)
-      bufA[tt][i] = siluf_(sc[0][tt] * pv);
-    else
-      bufB[tt][i - d_e] = siluf_(pv);
-  }
+  batched(
+      TB * NP,
+      [&](int e) { return a.P[static_cast<size_t>(min(t0 + e / NP, a.T - 1)) * NP + e % NP]; },
+      [&](int e, float pv) {
+        const int tt = e / NP, i = e % NP;
+        if (i < d_e)
+          bufA[tt][i] = siluf_(sc[tt] * pv);
+        else
+          bufB[tt][i - d_e] = siluf_(pv);
+      });
   __syncthreads();
-
-  // z^h into s[0:d_h), path-encoder hidden, local head b
-  matvec(w_hu, d_e, a.d_h, d_e, &bufA[0][0], MAXE, &x[0][0], XIN, Ident());
+  block_matmul(static_cast<const W*>(a.w_hu), d_e, a.d_h, d_e, &bufA[0][0], EP, nullptr, 0, &s[0][0],
+               MAXS + 4, Ident(), wst);
   matvec(static_cast<const W*>(a.w_p1), 6, a.d_p, 6, &xp[0][0], 8, &zp[0][0], MAXP, SiLU());
-  matvec(static_cast<const W*>(a.ps2), d_head, 1, d_head, &bufB[0][0], MAXE, &sc[3][0], 1, Ident());
+  matvec(static_cast<const W*>(a.ps2), d_head, 1, d_head, &bufB[0][0], EP, a.bvec + t0, 1, Ident(),
+         nvalid);
   __syncthreads();
-  // z^a into s[d_h:d_s)
-  matvec(static_cast<const W*>(a.w_p2), a.d_p, a.d_a, a.d_p, &zp[0][0], MAXP, &x[0][a.d_h], XIN, Ident());
+  matvec(static_cast<const W*>(a.w_p2), a.d_p, a.d_a, a.d_p, &zp[0][0], MAXP, &s[0][a.d_h], MAXS + 4,
+         Ident());
   __syncthreads();
-  // q, k, v, W_n s
-  matvec(static_cast<const W*>(a.w_q), d_s, DM, d_s, &x[0][0], XIN, &qkvn[0][0][0], DM, Ident());
-  matvec(static_cast<const W*>(a.w_k), d_s, DM, d_s, &x[0][0], XIN, &qkvn[1][0][0], DM, Ident());
-  matvec(static_cast<const W*>(a.w_v), d_s, DM, d_s, &x[0][0], XIN, &qkvn[2][0][0], DM, Ident());
-  matvec(static_cast<const W*>(a.w_n), d_s, DM, d_s, &x[0][0], XIN, &qkvn[3][0][0], DM, Ident());
-  __syncthreads();
-  for (int e = tid; e < 2 * TB * DM; e += NT) {
-    float* p = &qkvn[0][0][0] + e;
-    *p = phif_(*p);
+  const int d_s = a.d_s;
+  float* qkvn = a.qkvn + static_cast<size_t>(t0) * 4 * DM;
+  const float* S0 = &s[0][0];
+  block_matmul(static_cast<const W*>(a.w_q), d_s, DM, d_s, S0, MAXS + 4, nullptr, 0, qkvn, 4 * DM, Phi(),
+               wst, nvalid);
+  block_matmul(static_cast<const W*>(a.w_k), d_s, DM, d_s, S0, MAXS + 4, nullptr, 0, qkvn + DM, 4 * DM,
+               Phi(), wst, nvalid);
+  block_matmul(static_cast<const W*>(a.w_v), d_s, DM, d_s, S0, MAXS + 4, nullptr, 0, qkvn + 2 * DM, 4 * DM,
+               Ident(), wst, nvalid);
+  block_matmul(static_cast<const W*>(a.w_n), d_s, DM, d_s, S0, MAXS + 4, nullptr, 0, qkvn + 3 * DM, 4 * DM,
+               Ident(), wst, nvalid);
+  // the s columns of the history head's input layer
+  block_matmul(static_cast<const W*>(a.th1), a.ld_th1, d_head, d_s, S0, MAXS + 4, nullptr, 0,
+               a.hs + static_cast<size_t>(t0) * d_head, d_head, Ident(), wst, nvalid);
+}
+
+// ---------------------------------------------------------------------------
+// router_mem: one token per workgroup
+// ---------------------------------------------------------------------------
+template <int DM>
+__global__ __launch_bounds__(NT) void router_mem_kernel(RouterTailArgs a) {
+  constexpr int C4 = DM / 4;   // float4 columns of one S row
+  constexpr int RP = NT / C4;  // S rows per pass
+  constexpr int NR = DM / RP;  // S rows per thread
+  LDS16 float fq[DM];
+  LDS16 float fk[DM];
+  LDS16 float vv[DM];
+  LDS16 f32x4 red[RP][C4];
+  __shared__ float sden;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t = blockIdx.x;
+  const int j = a.j;
+  const float rho = 1.0f / (1.0f + expf(-a.eta));
+  const float* q = a.qkvn + static_cast<size_t>(t) * 4 * DM;
+  for (int i = tid; i < 3 * DM; i += NT) {
+    const float x = q[i];
+    if (i < DM)
+      fq[i] = x;
+    else if (i < 2 * DM)
+      fk[i - DM] = x;
+    else
+      vv[i - 2 * DM] = x;
   }
   __syncthreads();
-
-  // normaliser: den = phi(q).zeta (before the update), zeta <- rho zeta + phi(k)
-  for (int tt = wave; tt < TB; tt += NT / 64) {
-    const int t = t0 + tt;
+  if (wave == 0) {
     float part = 0.f;
-    if (t < a.T) {
-      float* z = a.zeta + static_cast<size_t>(t) * DM;
-      for (int k = lane; k < DM; k += 64) {
-        const float zv = j > 1 ? z[k] : 0.f;
-        part = fmaf(qkvn[0][tt][k], zv, part);
-        z[k] = fmaf(rho, zv, qkvn[1][tt][k]);
-      }
+    float* z = a.zeta + static_cast<size_t>(t) * DM;
+    for (int k = lane; k < DM; k += 64) {
+      const float zv = j > 1 ? z[k] : 0.f;
+      part = fmaf(fq[k], zv, part);
+      z[k] = fmaf(rho, zv, fk[k]);
     }
     part = wave_sum(part);
-    if (lane == 0) sc[4][tt] = part;
+    if (lane == 0) sden = part;
   }
-
-  // memory read-modify-write, one token at a time, all threads streaming its S
   const int cq = tid % C4, rg = tid / C4;
-  for (int tt = 0; tt < TB; ++tt) {
-    const int t = t0 + tt;
-    f32x4 cacc = {0.f, 0.f, 0.f, 0.f};
-    if (t < a.T) {
-      float* Sp = a.S + static_cast<size_t>(t) * DM * DM + 4 * cq;
-      const f32x4 v4 = *reinterpret_cast<const f32x4*>(&qkvn[2][tt][4 * cq]);
-      if (j == 1) {
+  float* Sp = a.S + static_cast<size_t>(t) * DM * DM + 4 * cq;
+  const f32x4 v4 = *reinterpret_cast<const f32x4*>(&vv[4 * cq]);
+  f32x4 cacc = {0.f, 0.f, 0.f, 0.f};
+  if (j == 1) {
 #pragma unroll 16
-        for (int i = 0; i < NR; ++i) {
-          const int r = rg + RP * i;
-          *reinterpret_cast<f32x4*>(Sp + r * DM) = qkvn[1][tt][r] * v4;
+    for (int i = 0; i < NR; ++i) {
+      const int r = rg + RP * i;
+      *reinterpret_cast<f32x4*>(Sp + r * DM) = fk[r] * v4;
+    }
+  } else {
+    constexpr int CH = NR < 16 ? NR : 16;
+    for (int i0 = 0; i0 < NR; i0 += CH) {
+      f32x4 sv[CH];
+#pragma unroll
+      for (int c = 0; c < CH; ++c) sv[c] = *reinterpret_cast<const f32x4*>(Sp + (rg + RP * (i0 + c)) * DM);
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        const int r = rg + RP * (i0 + c);
+        const float qv = fq[r], kv = fk[r];
+        f32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          cacc[e] = fmaf(qv, sv[c][e], cacc[e]);
+          o[e] = fmaf(rho, sv[c][e], kv * v4[e]);
         }
-      } else {
-        constexpr int CH = NR < 16 ? NR : 16;
-        for (int i0 = 0; i0 < NR; i0 += CH) {
-          f32x4 sv[CH];
-#pragma unroll
-          for (int c = 0; c < CH; ++c) sv[c] = *reinterpret_cast<const f32x4*>(Sp + (rg + RP * (i0 + c)) * DM);
-#pragma unroll
-          for (int c = 0; c < CH; ++c) {
-            const int r = rg + RP * (i0 + c);
-            const float fq = qkvn[0][tt][r], fk = qkvn[1][tt][r];
-            f32x4 o;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              cacc[e] = fmaf(fq, sv[c][e], cacc[e]);
-              o[e] = fmaf(rho, sv[c][e], fk * v4[e]);
-            }
-            *reinterpret_cast<f32x4*>(Sp + r * DM) = o;
-          }
-        }
+        *reinterpret_cast<f32x4*>(Sp + r * DM) = o;
       }
     }
-    red[rg][cq] = cacc;
-    __syncthreads();
-    if (tid < DM) {
-      float cs = 0.f;
-      for (int g = 0; g < RP; ++g) cs += red[g][tid >> 2][tid & 3];
-      x[tt][d_s + tid] = j > 1 ? cs / (sc[4][tt] + a.eps) : 0.f;
-    }
-    __syncthreads();
   }
-
-  // nu = 1 - cos(W_n s, W_c c)
-  matvec(static_cast<const W*>(a.w_c), DM, DM, DM, &x[0][d_s], XIN, &wc[0][0], DM, Ident());
+  red[rg][cq] = cacc;
   __syncthreads();
+  if (tid < DM) {
+    float cs = 0.f;
+    for (int g = 0; g < RP; ++g) cs += red[g][tid >> 2][tid & 3];
+    a.cvec[static_cast<size_t>(t) * DM + tid] = j > 1 ? cs / (sden + a.eps) : 0.f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// router_post
+// ---------------------------------------------------------------------------
+template <typename W>
+__global__ __launch_bounds__(NT) void router_post_kernel(RouterTailArgs a) {
+  constexpr int CX = MAXM + 4;
+  constexpr int HP = MAXE + 4;
+  LDS16 float cx[TB][CX];         // [c; nu]
+  LDS16 float ns[TB][MAXM];       // W_n s
+  LDS16 float wc[TB][MAXM];       // W_c c
+  LDS16 float hh[TB][HP];         // s part of the f_theta pre-activation, then its hidden
+  LDS16 float wst[KC * (4 * 64 + 4)];
+  LDS16 float sc[TB];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t0 = blockIdx.x * TB;
+  const int nvalid = min(TB, a.T - t0);
+  const int j = a.j;
+  const int DM = a.d_m, d_head = a.d_head, d_s = a.d_s;
+  auto tok = [&](int tt) { return static_cast<size_t>(min(t0 + tt, a.T - 1)); };
+  batched(
+      TB * DM, [&](int e) { return a.cvec[tok(e / DM) * DM + e % DM]; },
+      [&](int e, float v) { cx[e / DM][e % DM] = v; });
+  batched(
+      TB * DM, [&](int e) { return a.qkvn[tok(e / DM) * 4 * DM + 3 * DM + e % DM]; },
+      [&](int e, float v) { ns[e / DM][e % DM] = v; });
+  batched(
+      TB * d_head, [&](int e) { return a.hs[tok(e / d_head) * d_head + e % d_head]; },
+      [&](int e, float v) { hh[e / d_head][e % d_head] = v; });
+  __syncthreads();
+  block_matmul(static_cast<const W*>(a.w_c), DM, DM, DM, &cx[0][0], CX, nullptr, 0, &wc[0][0], MAXM,
+               Ident(), wst);
   for (int tt = wave; tt < TB; tt += NT / 64) {
     float nn = 0.f, cc = 0.f, nc = 0.f;
     for (int k = lane; k < DM; k += 64) {
-      const float n = qkvn[3][tt][k], c = wc[tt][k];
+      const float n = ns[tt][k], c = wc[tt][k];
       nn = fmaf(n, n, nn);
       cc = fmaf(c, c, cc);
       nc = fmaf(n, c, nc);
@@ -229,49 +390,440 @@ __global__ __launch_bounds__(NT) void router_tail_kernel(RouterTailArgs a) {
     nn = wave_sum(nn);
     cc = wave_sum(cc);
     nc = wave_sum(nc);
-    if (lane == 0) x[tt][d_s + DM] = j > 1 ? 1.0f - nc / (sqrtf(nn) * sqrtf(cc) + a.eps) : 0.f;
+    if (lane == 0) cx[tt][DM] = j > 1 ? 1.0f - nc / (sqrtf(nn) * sqrtf(cc) + a.eps) : 0.f;
+  }
+  __syncthreads();
+  // the [c; nu] columns of the history head's input layer on top of its s part, then SiLU
+  block_matmul(static_cast<const W*>(a.th1) + d_s, a.ld_th1, d_head, DM + 1, &cx[0][0], CX, &hh[0][0], HP,
+               &hh[0][0], HP, SiLU(), wst);
+  matvec(static_cast<const W*>(a.th2), d_head, 1, d_head, &hh[0][0], HP, &sc[0], 1, Ident());
+  __syncthreads();
+  if (tid < nvalid) {
+    const int t = t0 + tid;
+    const float av = sc[tid];
+    const float mprev = j > 1 ? a.m_hist[t] : 1.0f;
+    const float p = sigmoidf_(av / a.T_hist);
+    a.p_hist[t] = p;
+    a.m_hist[t] = mprev * p;
+    const float l = av + a.bvec[t] + (a.beta ? a.beta[t] : 0.f);
+    a.logit[t] = l;
+    a.gate[t] = sigmoidf_(l);
+  }
+}
+
+
+// ---------------------------------------------------------------------------
+// bf16 weights: matrix cores.  Every product above is a contraction over a batch of
+// tokens, run here on v_mfma_f32_16x16x32_bf16 with one 16-token row block per
+// workgroup.  The fp32 activations are split as x = hi + lo into two bf16 values
+// (|x - hi - lo| <= 2^-18 |x|) and the bf16 weights are exact, so each product
+// hi*w and lo*w is exact in fp32 and only the fp32 accumulation rounds.
+// A fragments live in LDS in MFMA order: entry [k-step s][lane], lane = i + 16 g,
+// holds row i at k = 32 s + 8 g .. + 7.  B fragments are 16-byte loads of eight
+// consecutive weights of one output row (L2-resident: every workgroup reads the
+// same router weights).  Output lane i + 16 g holds rows 4 g .. 4 g + 3 of column i.
+// ---------------------------------------------------------------------------
+constexpr int MT = 16;            // tokens per workgroup
+constexpr int KS_E = MAXE / 32;   // k-steps over d_e
+constexpr int KS_S = MAXS / 32;   // k-steps over d_s
+constexpr int KS_M = MAXM / 32;   // k-steps over d_m
+
+__device__ __forceinline__ void split8(const float* x, bf16x8& hi, bf16x8& lo) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const __bf16 h = static_cast<__bf16>(x[e]);
+    hi[e] = h;
+    lo[e] = static_cast<__bf16>(x[e] - static_cast<float>(h));
+  }
+}
+
+__device__ __forceinline__ f32x4 mfma_split(const bf16x8& ahi, const bf16x8& alo, const bf16x8& b,
+                                            f32x4 acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, b, acc, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, b, acc, 0, 0, 0);
+}
+
+// Weights w[r][k0 + 8 g .. + 7] of row r = r0 + (lane & 15), g = lane >> 4, of a [nrows][ld]
+// matrix (ld % 8 == 0, 16-byte aligned base); zero past nrows or past kmax (kmax % 8 == 0).
+__device__ __forceinline__ bf16x8 bfrag(const bf16_t* __restrict__ w, int ld, int nrows, int r0,
+                                        int k0, int kmax, int lane) {
+  const int r = r0 + (lane & 15), k = k0 + 8 * (lane >> 4);
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (r < nrows && k < kmax) v = *reinterpret_cast<const u32x4*>(w + static_cast<size_t>(r) * ld + k);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// One 16-column output tile of the s-projections: which matrix, its row offset, destination.
+struct SProj {
+  const bf16_t* w;
+  int ld, nrows, r0, os;
+  float* out;
+  bool phi;
+};
+
+__global__ __launch_bounds__(NT) void router_pre_mfma(RouterTailArgs a) {
+  LDS16 bf16x8 ax[2][KS_E][kWave];   // SiLU(inv_rms W_hd hbar): hi, lo
+  LDS16 bf16x8 as[2][KS_S][kWave];   // s: hi, lo
+  LDS16 float s[MT][MAXS + 4];
+  LDS16 float hp[MT][MAXP + 1];      // path-encoder hidden
+  __shared__ float xp[MT][8];
+  __shared__ float sc[MT];
+  __shared__ float bpart[MT][16];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t0 = blockIdx.x * MT;
+  const int nvalid = min(MT, a.T - t0);
+  const int j = a.j;
+  const int d_e = a.d_e, d_head = a.d_head, NP = d_e + d_head, DM = a.d_m, d_s = a.d_s;
+  const int d_h = a.d_h, d_a = a.d_a, d_p = a.d_p;
+
+  // P segment of 32 values: token tt, segment sg (NP % 32 == 0, NP <= 512)
+  const int tt = tid >> 4, sg = tid & 15;
+  const bool has_seg = 32 * sg < NP;
+  f32x4 pv[8];
+  if (has_seg) {
+    const float* src = a.P + static_cast<size_t>(min(t0 + tt, a.T - 1)) * NP + 32 * sg;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) pv[q] = *reinterpret_cast<const f32x4*>(src + 4 * q);
+  }
+  if (tid < MT) {
+    const int t = t0 + tid;
+    float inv_rms = 0.f, dd = 0.f, dp = 0.f, pp = 0.f, pprev = 1.f, mprev = 1.f;
+    if (t < a.T) {
+      const f32x4 rs = *reinterpret_cast<const f32x4*>(a.rowstat + 4 * static_cast<size_t>(t));
+      inv_rms = rs[0];
+      dd = rs[1];
+      dp = rs[2];
+      pp = rs[3];
+      if (j > 1) {
+        pprev = a.p_hist[t];
+        mprev = a.m_hist[t];
+      }
+    }
+    const float dj = j >= 2 ? sqrtf(dd) : 0.f;
+    const float gam = j >= 3 ? dp / (dj * sqrtf(pp) + a.eps) : 0.f;
+    xp[tid][0] = static_cast<float>(j) / static_cast<float>(a.L_R);
+    xp[tid][1] = static_cast<float>(a.L_R - j) / static_cast<float>(a.L_R);
+    xp[tid][2] = dj;
+    xp[tid][3] = gam;
+    xp[tid][4] = pprev;
+    xp[tid][5] = mprev;
+    sc[tid] = inv_rms;
   }
   __syncthreads();
 
-  // history head
-  const int XI = d_s + DM + 1;
-  matvec(static_cast<const W*>(a.th1), XI, d_head, XI, &x[0][0], XIN, &bufA[0][0], MAXE, SiLU());
-  __syncthreads();
-  matvec(static_cast<const W*>(a.th2), d_head, 1, d_head, &bufA[0][0], MAXE, &sc[5][0], 1, Ident());
+  // hidden-encoder A fragments, local-head partial dot products, path-encoder hidden layer
+  if (has_seg) {
+    float x[32];
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[4 * q + e] = pv[q][e];
+    if (32 * sg < d_e) {
+      const float ir = sc[tt];
+#pragma unroll
+      for (int e = 0; e < 32; ++e) x[e] = siluf_(ir * x[e]);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bf16x8 hi, lo;
+        split8(x + 8 * g, hi, lo);
+        ax[0][sg][tt + 16 * g] = hi;
+        ax[1][sg][tt + 16 * g] = lo;
+      }
+    } else {
+      const bf16_t* w = static_cast<const bf16_t*>(a.ps2) + 32 * sg - d_e;
+      float acc = 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float wv[8];
+        ld8(w + 8 * q, wv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = fmaf(wv[e], siluf_(x[8 * q + e]), acc);
+      }
+      bpart[tt][sg - d_e / 32] = acc;
+    }
+  }
+  {
+    const bf16_t* w1 = static_cast<const bf16_t*>(a.w_p1);
+    for (int e = tid; e < MT * d_p; e += NT) {
+      const int t = e / d_p, o = e % d_p;
+      float acc = 0.f;
+#pragma unroll
+      for (int k = 0; k < 6; ++k) acc = fmaf(ldf(w1 + o * 6 + k), xp[t][k], acc);
+      hp[t][o] = siluf_(acc);
+    }
+  }
   __syncthreads();
 
-  if (tid < TB) {
-    const int t = t0 + tid;
-    if (t < a.T) {
-      const float av = sc[5][tid], bv = sc[3][tid];
-      const float p = sigmoidf_(av / a.T_hist);
-      a.p_hist[t] = p;
-      a.m_hist[t] = sc[1][tid] * p;
-      const float l = av + bv + sc[2][tid];
-      a.logit[t] = l;
-      a.gate[t] = sigmoidf_(l);
+  // z_h = W_hu x on matrix cores (16-column tiles over the waves), z_a = W_p2 hp
+  {
+    const bf16_t* w = static_cast<const bf16_t*>(a.w_hu);
+    const int ks = d_e / 32;
+    for (int ct = wave; 16 * ct < d_h; ct += NT / kWave) {
+      bf16x8 b[KS_E];
+#pragma unroll
+      for (int st = 0; st < KS_E; ++st)
+        if (st < ks) b[st] = bfrag(w, d_e, d_h, 16 * ct, 32 * st, d_e, lane);
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < KS_E; ++st)
+        if (st < ks) acc = mfma_split(ax[0][st][lane], ax[1][st][lane], b[st], acc);
+      const int o = 16 * ct + (lane & 15);
+      if (o < d_h)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s[4 * (lane >> 4) + r][o] = acc[r];
+    }
+    const bf16_t* w2 = static_cast<const bf16_t*>(a.w_p2);
+    for (int e = tid; e < MT * d_a; e += NT) {
+      const int t = e / d_a, o = e % d_a;
+      float acc = 0.f;
+      for (int k = 0; k < d_p; ++k) acc = fmaf(ldf(w2 + o * d_p + k), hp[t][k], acc);
+      s[t][d_h + o] = acc;
+    }
+  }
+  __syncthreads();
+
+  // s as A fragments (zero past d_s); the local-head logit b
+  const int ks2 = (d_s + 31) / 32;
+  for (int e = tid; e < MT * 4 * ks2; e += NT) {
+    const int i = e & 15, g = (e >> 4) & 3, st = e >> 6;
+    const int k0 = 32 * st + 8 * g;
+    float x[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) x[q] = k0 + q < d_s ? s[i][k0 + q] : 0.f;
+    split8(x, as[0][st][i + 16 * g], as[1][st][i + 16 * g]);
+  }
+  if (tid < nvalid) {
+    float b = 0.f;
+    for (int q = 0; q < d_head / 32; ++q) b += bpart[tid][q];
+    a.bvec[t0 + tid] = b;
+  }
+  __syncthreads();
+
+  // [phi(q); phi(k); v; W_n s; th1[:, :d_s] s], G tiles of 16 columns per wave in flight
+  constexpr int G = 4;
+  const int nq = DM / 16, nct = 4 * nq + d_head / 16;
+  auto proj = [&](int ct) {
+    const int m = ct / nq;
+    SProj p;
+    if (m < 4) {
+      const void* ws[4] = {a.w_q, a.w_k, a.w_v, a.w_n};
+      p = SProj{static_cast<const bf16_t*>(ws[m]), d_s, DM, 16 * (ct - m * nq), 4 * DM, a.qkvn + m * DM,
+                m < 2};
+    } else {
+      p = SProj{static_cast<const bf16_t*>(a.th1), a.ld_th1, d_head, 16 * (ct - 4 * nq), d_head, a.hs,
+                false};
+    }
+    return p;
+  };
+  for (int c0 = wave; c0 < nct; c0 += G * (NT / kWave)) {
+    bf16x8 b[G][KS_S];
+#pragma unroll
+    for (int c = 0; c < G; ++c) {
+      const int ct = c0 + c * (NT / kWave);
+      if (ct < nct) {
+        const SProj p = proj(ct);
+#pragma unroll
+        for (int st = 0; st < KS_S; ++st)
+          if (st < ks2) b[c][st] = bfrag(p.w, p.ld, p.nrows, p.r0, 32 * st, d_s, lane);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < G; ++c) {
+      const int ct = c0 + c * (NT / kWave);
+      if (ct >= nct) break;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < KS_S; ++st)
+        if (st < ks2) acc = mfma_split(as[0][st][lane], as[1][st][lane], b[c][st], acc);
+      const SProj p = proj(ct);
+      const int o = p.r0 + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = t0 + 4 * (lane >> 4) + r;
+        if (t < a.T) p.out[static_cast<size_t>(t) * p.os + o] = p.phi ? phif_(acc[r]) : acc[r];
+      }
     }
   }
 }
 
-template <typename W>
-hipError_t launch_dm(const RouterTailArgs& a, hipStream_t s) {
-  dim3 grid((a.T + TB - 1) / TB), block(NT);
-  switch (a.d_m) {
-    case 32: router_tail_kernel<W, 32><<<grid, block, 0, s>>>(a); break;
-    case 64: router_tail_kernel<W, 64><<<grid, block, 0, s>>>(a); break;
-    case 128: router_tail_kernel<W, 128><<<grid, block, 0, s>>>(a); break;
-    case 256: router_tail_kernel<W, 256><<<grid, block, 0, s>>>(a); break;
-    default: return hipErrorInvalidValue;
+__global__ __launch_bounds__(NT) void router_post_mfma(RouterTailArgs a) {
+  LDS16 bf16x8 ac[2][KS_M][kWave];   // c: hi, lo
+  LDS16 float ns[MT][MAXM + 4];      // W_n s
+  LDS16 float wc[MT][MAXM + 4];      // W_c c
+  __shared__ float nu[MT];
+  __shared__ float apart[NT / kWave][MT];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t0 = blockIdx.x * MT;
+  const int nvalid = min(MT, a.T - t0);
+  const int j = a.j;
+  const int DM = a.d_m, d_head = a.d_head, d_s = a.d_s;
+  auto tok = [&](int i) { return static_cast<size_t>(min(t0 + i, a.T - 1)); };
+
+  const int ks = DM / 32;   // d_m in {32, 64, 128, 256}
+  for (int e = tid; e < MT * 4 * ks; e += NT) {
+    const int i = e & 15, g = (e >> 4) & 3, st = e >> 6;
+    const float* src = a.cvec + tok(i) * DM + 32 * st + 8 * g;
+    const f32x4 lo4 = *reinterpret_cast<const f32x4*>(src);
+    const f32x4 hi4 = *reinterpret_cast<const f32x4*>(src + 4);
+    float x[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      x[q] = lo4[q];
+      x[4 + q] = hi4[q];
+    }
+    split8(x, ac[0][st][i + 16 * g], ac[1][st][i + 16 * g]);
+  }
+  for (int e = tid; e < MT * DM / 4; e += NT) {
+    const int i = e / (DM / 4), c4 = e % (DM / 4);
+    *reinterpret_cast<f32x4*>(&ns[i][4 * c4]) =
+        *reinterpret_cast<const f32x4*>(a.qkvn + tok(i) * 4 * DM + 3 * DM + 4 * c4);
+  }
+  __syncthreads();
+
+  // W_c c
+  {
+    const bf16_t* w = static_cast<const bf16_t*>(a.w_c);
+    for (int ct = wave; 16 * ct < DM; ct += NT / kWave) {
+      bf16x8 b[KS_M];
+#pragma unroll
+      for (int st = 0; st < KS_M; ++st)
+        if (st < ks) b[st] = bfrag(w, DM, DM, 16 * ct, 32 * st, DM, lane);
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < KS_M; ++st)
+        if (st < ks) acc = mfma_split(ac[0][st][lane], ac[1][st][lane], b[st], acc);
+      const int o = 16 * ct + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) wc[4 * (lane >> 4) + r][o] = acc[r];
+    }
+  }
+  __syncthreads();
+
+  // nu = 1 - cos(W_n s, W_c c); 0 at j = 1
+  for (int i = wave; i < MT; i += NT / kWave) {
+    float nn = 0.f, cc = 0.f, nc = 0.f;
+    for (int k = lane; k < DM; k += kWave) {
+      const float n = ns[i][k], c = wc[i][k];
+      nn = fmaf(n, n, nn);
+      cc = fmaf(c, c, cc);
+      nc = fmaf(n, c, nc);
+    }
+    nn = wave_sum(nn);
+    cc = wave_sum(cc);
+    nc = wave_sum(nc);
+    if (lane == 0) nu[i] = j > 1 ? 1.0f - nc / (sqrtf(nn) * sqrtf(cc) + a.eps) : 0.f;
+  }
+  __syncthreads();
+
+  // a = th2 . SiLU(th1 [s; c; nu]): the s part (hs) and the nu column are added in the epilogue
+  constexpr int G = 4;
+  const bf16_t* th1 = static_cast<const bf16_t*>(a.th1);
+  const bf16_t* th2 = static_cast<const bf16_t*>(a.th2);
+  const int ld = a.ld_th1, nct = d_head / 16, g4 = 4 * (lane >> 4);
+  float ap[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int c0 = wave; c0 < nct; c0 += G * (NT / kWave)) {
+    bf16x8 b[G][KS_M];
+    float hsv[G][4], wnu[G], w2[G];
+#pragma unroll
+    for (int c = 0; c < G; ++c) {
+      const int ct = c0 + c * (NT / kWave);
+      if (ct < nct) {
+        const int o = 16 * ct + (lane & 15);
+#pragma unroll
+        for (int st = 0; st < KS_M; ++st)
+          if (st < ks) b[c][st] = bfrag(th1 + d_s, ld, d_head, 16 * ct, 32 * st, DM, lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) hsv[c][r] = a.hs[tok(g4 + r) * d_head + o];
+        wnu[c] = bf16_to_f32(th1[static_cast<size_t>(o) * ld + d_s + DM]);
+        w2[c] = bf16_to_f32(th2[o]);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < G; ++c) {
+      const int ct = c0 + c * (NT / kWave);
+      if (ct >= nct) break;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < KS_M; ++st)
+        if (st < ks) acc = mfma_split(ac[0][st][lane], ac[1][st][lane], b[c][st], acc);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float pre = acc[r] + hsv[c][r] + wnu[c] * nu[g4 + r];
+        ap[r] = fmaf(w2[c], siluf_(pre), ap[r]);
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) ap[r] += __shfl_xor(ap[r], off, kWave);
+  if ((lane & 15) == 0)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) apart[wave][g4 + r] = ap[r];
+  __syncthreads();
+  if (tid < nvalid) {
+    const int t = t0 + tid;
+    float av = 0.f;
+#pragma unroll
+    for (int w = 0; w < NT / kWave; ++w) av += apart[w][tid];
+    const float mprev = j > 1 ? a.m_hist[t] : 1.0f;
+    const float p = sigmoidf_(av / a.T_hist);
+    a.p_hist[t] = p;
+    a.m_hist[t] = mprev * p;
+    const float l = av + a.bvec[t] + (a.beta ? a.beta[t] : 0.f);
+    a.logit[t] = l;
+    a.gate[t] = sigmoidf_(l);
+  }
+}
+
+#undef LDS16
+
+hipError_t launch_pre_post(const RouterTailArgs& a, bool post, hipStream_t s) {
+  if (a.dtype == 1) {
+    dim3 grid((a.T + MT - 1) / MT), block(NT);
+    if (post)
+      router_post_mfma<<<grid, block, 0, s>>>(a);
+    else
+      router_pre_mfma<<<grid, block, 0, s>>>(a);
+  } else {
+    dim3 grid((a.T + TB - 1) / TB), block(NT);
+    if (post)
+      router_post_kernel<float><<<grid, block, 0, s>>>(a);
+    else
+      router_pre_kernel<float><<<grid, block, 0, s>>>(a);
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_router_tail(const RouterTailArgs& a, hipStream_t s) {
+size_t router_scratch_floats(int d_m, int d_head, int T) {
+  return static_cast<size_t>(T) * (4 * d_m + d_head + d_m + 1);
+}
+
+hipError_t launch_router_pre(const RouterTailArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
-  return a.dtype == 1 ? launch_dm<bf16_t>(a, s) : launch_dm<float>(a, s);
+  return launch_pre_post(a, false, s);
+}
+
+hipError_t launch_router_mem(const RouterTailArgs& a, hipStream_t s) {
+  if (a.T <= 0) return hipSuccess;
+  dim3 grid(a.T), block(NT);
+  switch (a.d_m) {
+    case 32: router_mem_kernel<32><<<grid, block, 0, s>>>(a); break;
+    case 64: router_mem_kernel<64><<<grid, block, 0, s>>>(a); break;
+    case 128: router_mem_kernel<128><<<grid, block, 0, s>>>(a); break;
+    case 256: router_mem_kernel<256><<<grid, block, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_router_post(const RouterTailArgs& a, hipStream_t s) {
+  if (a.T <= 0) return hipSuccess;
+  return launch_pre_post(a, true, s);
 }
 
 }  // namespace hero

@@ -28,6 +28,17 @@ def download_f64(x: torch.Tensor) -> np.ndarray:
     return x.float().cpu().numpy().astype(np.float64)
 
 
+def th1_pitch(w: synth.Workload) -> int:
+    """Row pitch of the history head's input layer in the ABI layout (a multiple of 8)."""
+    return (w.d_s + w.d_m + 1 + 7) // 8 * 8
+
+
+def pad_th1(t: synth.Tensor, w: synth.Workload) -> synth.Tensor:
+    """th1 [d_head][d_s + d_m + 1] with zero columns appended up to the ABI row pitch."""
+    pad = th1_pitch(w) - t.store.shape[1]
+    return synth.Tensor(np.pad(t.store, ((0, 0), (0, pad))), t.dtype)
+
+
 def dims_struct(w: synth.Workload) -> H.hero_dims:
     return H.hero_dims(d=w.d, d_ff=w.d_ff, d_r=w.d_r, L_R=w.L_R, d_m=w.d_m, d_s=w.d_s, d_h=w.d_h,
                        d_a=w.d_a, d_e=w.d_e, d_p=w.d_p, d_head=w.d_head,
@@ -72,7 +83,7 @@ class DeviceProblem:
         self.prev1 = upload(prob.hbar_prev1, device) if prob.hbar_prev1 is not None else None
         self.prev2 = upload(prob.hbar_prev2, device) if prob.hbar_prev2 is not None else None
         self.h_out = torch.empty_like(self.hbar)
-        self.router = {k: upload(v, device) for k, v in prob.router.items()}
+        self.router = {k: upload(v if k != "th1" else pad_th1(v, w), device) for k, v in prob.router.items()}
         self.router_s = H.hero_router_weights(**{k: self.router[k].data_ptr() for k in H.ROUTER_FIELDS})
         # weights are drawn and uploaded one layer at a time
         self.ffn = [{k: upload(v, device) for k, v in prob.ffn[i].items()} for i in range(len(prob.ffn))]

@@ -32,8 +32,8 @@ HERO_BF16 = 1
 HERO_MODE_THRESHOLD = 0
 HERO_MODE_BUDGET = 1
 
-KERNELS = ("rowstats", "router_gemm", "router_tail", "select", "ffn_gate_up", "ffn_down",
-           "adapter_down", "adapter_up")
+KERNELS = ("rowstats", "router_gemm", "router_pre", "router_mem", "router_post", "select",
+           "ffn_gate_up", "ffn_down", "adapter_down", "adapter_up")
 HERO_K = {name: i for i, name in enumerate(KERNELS)}
 
 _vp = ctypes.c_void_p

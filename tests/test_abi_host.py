@@ -84,7 +84,7 @@ def call_layer(dims=None, j=3, T=100, routing=None, ws_bytes=None, **over):
     ("d", 640, H.HERO_E_UNSUPPORTED),    # bf16 needs d % 256 == 0
     ("d_ff", 688, H.HERO_E_UNSUPPORTED),  # bf16 needs d_ff % 128 == 0
     ("d_r", 16, H.HERO_E_UNSUPPORTED),
-    ("d_e", 1024, H.HERO_E_UNSUPPORTED),
+    ("d_e", 512, H.HERO_E_UNSUPPORTED),
 ])
 def test_dims_validation(field, value, status):
     assert call_layer(good_dims(**{field: value})) == status
@@ -96,6 +96,20 @@ def test_f32_accepts_ragged_widths_bf16_does_not():
     assert H.lib().hero_workspace_size(ctypes.byref(dims), 64, 1, ctypes.byref(need)) == H.HERO_OK
     dims = good_dims(H.HERO_BF16, d=256, d_ff=688, d_r=16, d_m=32)
     assert H.lib().hero_workspace_size(ctypes.byref(dims), 64, 1, ctypes.byref(need)) == H.HERO_E_UNSUPPORTED
+    # bf16 router weights are read as 16-byte rows: d_s must be a multiple of 8
+    dims = good_dims(H.HERO_BF16, d_s=66, d_h=50)
+    assert H.lib().hero_workspace_size(ctypes.byref(dims), 64, 1, ctypes.byref(need)) == H.HERO_E_UNSUPPORTED
+    dims = good_dims(H.HERO_F32, d_s=66, d_h=50)
+    assert H.lib().hero_workspace_size(ctypes.byref(dims), 64, 1, ctypes.byref(need)) == H.HERO_OK
+
+
+def test_th1_pitch_macro_matches_harness():
+    from paper_2609_08189_amd import device, synth
+    w = synth.WORKLOADS["llama31_8b_layer"]
+    assert device.th1_pitch(w) == 200 and device.th1_pitch(w) % 8 == 0
+    assert device.th1_pitch(w.replace(d_s=64, d_m=32)) == 104
+    text = open(os.path.join(ROOT, "include", "hero.h")).read()
+    assert "#define HERO_TH1_PITCH(d_s, d_m) ((((d_s) + (d_m) + 1) + 7) / 8 * 8)" in text
 
 
 def test_argument_validation():
