@@ -18,6 +18,8 @@
 // f32 path: a plain LDS-tiled VALU GEMM with full bounds checks (small shapes).
 #include <limits.h>
 
+#include <type_traits>
+
 #include "hero_device.h"
 #include "hero_kernels.h"
 
@@ -59,10 +61,12 @@ struct BRows {
 struct EpiStoreF32 {  // P[m][n] = acc
   float* out;
   int ld;
+  struct Pre {};
+  __device__ __forceinline__ Pre prep(int, int) const { return {}; }
   __device__ __forceinline__ void store(int m, int n, float v) const {
     out[static_cast<size_t>(m) * ld + n] = v;
   }
-  __device__ __forceinline__ void emit8(int m, int n, const float* v) const {
+  __device__ __forceinline__ void emit8(const Pre&, int m, int n, const float* v) const {
     float* o = out + static_cast<size_t>(m) * ld + n;
     *reinterpret_cast<f32x4*>(o) = *reinterpret_cast<const f32x4*>(v);
     *reinterpret_cast<f32x4*>(o + 4) = *reinterpret_cast<const f32x4*>(v + 4);
@@ -76,12 +80,9 @@ struct EpiSwiGLU {  // act[m][c] = SiLU(gate) * up
   __device__ __forceinline__ void store2(int m, int c, float g, float u) const {
     stf(act + static_cast<size_t>(m) * ld + c, siluf_(g) * u);
   }
-  // v holds SiLU(gate) * up already (the MFMA path forms it while staging)
-  __device__ __forceinline__ void emit8(int m, int c, const float* v) const {
-    float x[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = v[e];
-    st8(act + static_cast<size_t>(m) * ld + c, x);
+  // eight finished bf16 values (the MFMA path forms SiLU(gate) * up while staging)
+  __device__ __forceinline__ void emit_packed(int m, int c, u32x4 v) const {
+    *reinterpret_cast<u32x4*>(act + static_cast<size_t>(m) * ld + c) = v;
   }
 };
 
@@ -95,6 +96,8 @@ struct EpiSiLU {  // hid[m][n] = SiLU(acc)
 };
 
 // h_out[t][n] = hbar[t][n] + scale(g_t) * acc, t = idx[m]; FFN scales by g, adapter by 1 - g.
+// The MFMA path fetches each 8-column piece of hbar (prep) before it stages the accumulators,
+// so that the loads of a whole wave tile are in flight together.
 template <typename T, bool ADAPTER>
 struct EpiScatter {
   const int* idx;
@@ -109,16 +112,29 @@ struct EpiScatter {
     const size_t o = static_cast<size_t>(t) * ld + n;
     stf(out + o, ldf(hbar + o) + sc * v);
   }
-  __device__ __forceinline__ void emit8(int m, int n, const float* v) const {
+  struct Pre {
+    u32x4 h;
+    uint32_t row;
+    float sc;
+  };
+  __device__ __forceinline__ Pre prep(int m, int n) const {
     const int t = idx[m];
     const float g = gate[t];
-    const float sc = ADAPTER ? 1.0f - g : g;
-    const size_t o = static_cast<size_t>(t) * ld + n;
-    float h[8];
-    ld8(hbar + o, h);
+    Pre p;
+    p.row = static_cast<uint32_t>(t);
+    p.sc = ADAPTER ? 1.0f - g : g;
+    p.h = *reinterpret_cast<const u32x4*>(hbar + static_cast<size_t>(t) * ld + n);
+    return p;
+  }
+  __device__ __forceinline__ void emit8(const Pre& p, int, int n, const float* v) const {
+    u32x4 w;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) h[e] = h[e] + sc * v[e];
-    st8(out + o, h);
+    for (int i = 0; i < 4; ++i) {
+      const float lo = __uint_as_float(p.h[i] << 16) + p.sc * v[2 * i];
+      const float hi = __uint_as_float(p.h[i] & 0xffff0000u) + p.sc * v[2 * i + 1];
+      w[i] = static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+    }
+    *reinterpret_cast<u32x4*>(out + static_cast<size_t>(p.row) * ld + n) = w;
   }
 };
 
@@ -126,8 +142,10 @@ struct EpiScatter {
 // bf16 MFMA GEMM
 //
 // One workgroup of WM x WN waves computes a BM x BN tile; each wave owns a
-// (BM/WM) x (BN/WN) block of 32 x 32 MFMA tiles with fp32 accumulators in AGPRs.
-// K advances in 64-deep tiles through two LDS stages:
+// (BM/WM) x (BN/WN) block of 32 x 32 MFMA tiles with fp32 accumulators.  The big
+// products run 8 waves (two per SIMD) on a 256 x 256 (or 192 x 256) tile, so that one
+// wave's MFMAs cover the other's waits.  K advances in 64-deep tiles through two
+// LDS stages:
 //   * each stage is filled by wave-wide global_load_lds_dwordx4: one instruction
 //     moves 64 x 16 bytes into a contiguous 1 KiB of LDS, i.e. eight 128-byte
 //     tile rows; lane L lands in row 8b + L/8 at physical chunk L%8 and so loads
@@ -135,12 +153,14 @@ struct EpiScatter {
 //     XOR; with it, the 16 lanes of one LDS read phase (16 consecutive rows, one
 //     logical chunk) hit 16 distinct 16-byte slots of the 256-byte bank window;
 //   * within a k-tile the fragments of the next 16-deep k-step are read while the
-//     MFMAs of the current one run (two register sets, fenced by sched_barrier);
+//     MFMAs of the current one run (two register sets), the reads interleaved one
+//     by one with the MFMAs;
 //   * the workgroup barrier sits before the last k-step: by then every wave has
-//     read the whole stage, so the loads of tile k+2 can be issued into it and the
-//     first fragments of tile k+1 read while the last MFMAs of tile k run.
-// The epilogue stages each wave's results through LDS in 32-row blocks so that
-// every lane then handles 8 consecutive columns with 16-byte accesses.
+//     read the whole stage, so the loads of tile k+2 are issued into it, one per
+//     MFMA of that last k-step, together with the first fragment reads of tile k+1.
+// Epilogues: the gate/up product stages its finished bf16 tile in LDS at once and
+// writes 16-byte row pieces; the others first fetch what they combine with (hbar
+// rows) for the whole wave tile, then stage fp32 results in 32-row blocks.
 // ---------------------------------------------------------------------------
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -150,6 +170,9 @@ __device__ __forceinline__ void load_lds16(const void* g, unsigned char* l) {
 }
 
 __device__ __forceinline__ int swz(int row, int ch) { return row * ROWB + ((ch ^ ((row >> 1) & 7)) << 4); }
+
+// instruction classes of __builtin_amdgcn_sched_group_barrier
+constexpr int SG_MFMA = 0x008, SG_VMEM_READ = 0x020, SG_DS_READ = 0x100;
 
 template <int BM_, int BN_, int WM_, int WN_, bool DUAL_>
 struct Tile {
@@ -162,11 +185,14 @@ struct Tile {
   static constexpr int STAGE = (BM + BN) * ROWB;
   static constexpr int OUT_N = DUAL ? BN / 2 : BN;   // output columns per tile
   static constexpr int ON = DUAL ? WTN / 2 : WTN;     // output columns per wave
-  static constexpr int OPAD = ON + 4;                 // staged row pitch (floats)
+  static constexpr int OPAD = ON + 4;                 // fp32 staging row pitch (floats)
+  static constexpr int SPAD = ON + 8;                 // bf16 staging row pitch (elements)
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole MFMA tiles");
   static_assert(!DUAL || TN % 2 == 0, "gate/up tiles come in pairs");
   static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "loader split");
-  static_assert(NW * 32 * OPAD * 4 <= 2 * STAGE, "epilogue staging must fit in the stages");
+  static_assert(DUAL ? NW * WTM * SPAD * 2 <= 2 * STAGE : NW * 32 * OPAD * 4 <= 2 * STAGE,
+                "epilogue staging must fit in the stages");
+  static_assert((32 * (ON / 8)) % 64 == 0, "epilogue pieces split evenly over the lanes");
 };
 
 template <class C, class Epi>
@@ -177,6 +203,9 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   constexpr int A_LD = C::BM / 8 / NW;  // wave-wide loads per k-tile, A
   constexpr int B_LD = C::BN / 8 / NW;
   constexpr int KS = BK / 16;
+  constexpr int NM = C::TM * C::TN;     // MFMAs per k-step
+  constexpr int NR = C::TM + C::TN;     // fragment reads per k-step
+  constexpr int NL = A_LD + B_LD;       // stage loads per k-tile
   __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * C::STAGE];
   const int per = gridDim.x >> 3;
   const int tile = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
@@ -263,6 +292,19 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
       for (int b = 0; b < C::TN; ++b)
         acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][a], fb[buf][b], acc[a][b], 0, 0, 0);
   };
+  // order within the current scheduling region: MFMA, then (while any remain) one stage load
+  // and one fragment read after each
+  auto interleave = [&](auto nl_) {
+    constexpr int nl = decltype(nl_)::value;
+#pragma unroll
+    for (int i = 0; i < NM; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+      if (i < nl) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, 1, 0);
+      if (i < NR) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+    }
+    if constexpr (nl > NM) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, nl - NM, 0);
+    if constexpr (NR > NM) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, NR - NM, 0);
+  };
 
   const int nk = K / BK;
   issue(0, 0);
@@ -275,8 +317,8 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
 #pragma unroll
     for (int ks = 0; ks < KS - 1; ++ks) {
       read_frags((ks + 1) & 1, st, ks + 1);
-      __builtin_amdgcn_sched_barrier(0);
       mfmas(ks & 1);
+      interleave(std::integral_constant<int, 0>());
       __builtin_amdgcn_sched_barrier(0);
     }
     // every wave has read all of stage kt and the loads of tile kt+1 have landed
@@ -284,39 +326,65 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
     __syncthreads();
     if (kt + 2 < nk) issue(kt & 1, (kt + 2) * BK);
     if (kt + 1 < nk) read_frags(KS & 1, smem + ((kt + 1) & 1) * C::STAGE, 0);
-    __builtin_amdgcn_sched_barrier(0);
     mfmas((KS - 1) & 1);
+    interleave(std::integral_constant<int, NL>());
     __builtin_amdgcn_sched_barrier(0);
   }
 
-  // epilogue: 32-row blocks of each wave's results go through LDS (fp32, padded rows),
-  // then each lane emits 8 consecutive columns
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  float* stg = reinterpret_cast<float*>(smem) + wave * (32 * C::OPAD);
+  if constexpr (C::DUAL) {
+    // the wave's finished tile, SiLU(gate) * up in bf16, staged at once
+    bf16_t* stg = reinterpret_cast<bf16_t*>(smem) + wave * (C::WTM * C::SPAD);
 #pragma unroll
-  for (int a = 0; a < C::TM; ++a) {
+    for (int a = 0; a < C::TM; ++a)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int i = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      if constexpr (C::DUAL) {
+      for (int r = 0; r < 16; ++r) {
+        const int i = a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 #pragma unroll
         for (int b = 0; b < C::TN / 2; ++b) {
           const float g = acc[a][b][r], u = acc[a][b + C::TN / 2][r];
-          stg[i * C::OPAD + b * 32 + (lane & 31)] = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+          stg[i * C::SPAD + b * 32 + (lane & 31)] =
+              f32_to_bf16(g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u);
         }
-      } else {
+      }
+    constexpr int CPR = C::ON / 8;                 // 8-column pieces per row
+    constexpr int PPL = C::WTM * CPR / kWave;      // pieces per lane
+#pragma unroll
+    for (int q = 0; q < PPL; ++q) {
+      const int e = lane + kWave * q;
+      const int i = e / CPR, c8 = (e % CPR) * 8;
+      const int m = m0 + wm * C::WTM + i;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(stg + i * C::SPAD + c8);
+      if (m < M) epi.emit_packed(m, nt * C::OUT_N + wn * C::ON + c8, v);
+    }
+  } else {
+    constexpr int CPR = C::ON / 8;                 // 8-column pieces per staged row
+    constexpr int PPB = 32 * CPR / kWave;          // pieces per lane per 32-row block
+    typename Epi::Pre pre[C::TM][PPB];
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+      for (int q = 0; q < PPB; ++q) {
+        const int e = lane + kWave * q;
+        const int m = m0 + wm * C::WTM + a * 32 + e / CPR;
+        pre[a][q] = epi.prep(min(m, M - 1), nt * C::OUT_N + wn * C::ON + (e % CPR) * 8);
+      }
+    float* stg = reinterpret_cast<float*>(smem) + wave * (32 * C::OPAD);
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 #pragma unroll
         for (int b = 0; b < C::TN; ++b) stg[i * C::OPAD + b * 32 + (lane & 31)] = acc[a][b][r];
       }
-    }
-    constexpr int CPR = C::ON / 8;   // 8-column pieces per staged row
-    for (int e = lane; e < 32 * CPR; e += 64) {
-      const int i = e / CPR, c8 = (e % CPR) * 8;
-      const int m = m0 + wm * C::WTM + a * 32 + i;
-      if (m < M) {
-        const float* v = stg + i * C::OPAD + c8;
-        epi.emit8(m, nt * C::OUT_N + wn * C::ON + c8, v);
+#pragma unroll
+      for (int q = 0; q < PPB; ++q) {
+        const int e = lane + kWave * q;
+        const int i = e / CPR, c8 = (e % CPR) * 8;
+        const int m = m0 + wm * C::WTM + a * 32 + i;
+        if (m < M) epi.emit8(pre[a][q], m, nt * C::OUT_N + wn * C::ON + c8, stg + i * C::OPAD + c8);
       }
     }
   }
@@ -345,8 +413,8 @@ int tile_cost(int M, int BM, int n_tiles) {
 template <int BN, bool DUAL, class Epi>
 hipError_t run_big(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_count, int M_max,
                    int N_out, int K, hipStream_t s) {
-  using T256 = Tile<256, BN, 2, 2, DUAL>;
-  using T192 = Tile<192, BN, 2, 2, DUAL>;
+  using T256 = Tile<256, BN, 2, 4, DUAL>;
+  using T192 = Tile<192, BN, 2, 4, DUAL>;
   const int n_tiles = N_out / T256::OUT_N;
   if (tile_cost(M_max, 192, n_tiles) < tile_cost(M_max, 256, n_tiles))
     return run_tile<T192>(A, B, epi, m_count, M_max, N_out, K, s);
