@@ -39,7 +39,7 @@ Layout layout_of(const hero_dims& d, int T, bool stack) {
     return o;
   };
   L.u = take(t * d.d * es);
-  L.P = take(t * (d.d_e + d.d_head) * 4);
+  L.P = take(t * (d.d_e + d.d_head) * 4 * hero::router_gemm_splits(d.dtype, d.d));
   L.rowstat = take(t * 16);
   L.logit = take(t * 4);
   L.gate = take(t * 4);
@@ -217,6 +217,7 @@ int run_layer(const LayerCall& c) {
   ra.T_hist = D.T_hist;
   ra.eta = c.eta;
   ra.P = P;
+  ra.p_splits = router_gemm_splits(D.dtype, D.d);
   ra.rowstat = rowstat;
   ra.w_hu = c.rt->w_hu;
   ra.w_p1 = c.rt->w_p1;

@@ -13,7 +13,9 @@ hipError_t launch_rowstats(int dtype, const void* hbar, const void* prev1, const
                            const void* norm_w, int T, int d, int j, float eps_norm,
                            float* rowstat, void* u, hipStream_t s);
 
-// Router pre-activations P[t] = [W_hd hbar_t ; psi_1 hbar_t] (fp32, [T][d_e + d_head]).
+// Router pre-activations P[t] = [W_hd hbar_t ; psi_1 hbar_t] (fp32, [T][d_e + d_head]),
+// written as router_gemm_splits(dtype, d) partial sums over K slices, slice z at P + z T (d_e + d_head).
+int router_gemm_splits(int dtype, int d);
 hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, const void* ps1,
                               int T, int d, int d_e, int d_head, float* P, hipStream_t s);
 
@@ -22,7 +24,8 @@ struct RouterTailArgs {
   int T, j, L_R;
   int d_m, d_s, d_h, d_a, d_e, d_p, d_head;
   float eps, T_hist, eta;
-  const float* P;         // [T][d_e + d_head]
+  const float* P;         // [p_splits][T][d_e + d_head] partial sums
+  int p_splits;
   const float* rowstat;   // [T][4]
   const void *w_hu, *w_p1, *w_p2, *w_q, *w_k, *w_v, *w_n, *w_c, *th1, *th2, *ps2;
   int ld_th1;             // row pitch of th1 (elements)

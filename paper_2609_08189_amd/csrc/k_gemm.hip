@@ -58,16 +58,17 @@ struct BRows {
 // epilogues
 // ---------------------------------------------------------------------------
 
-struct EpiStoreF32 {  // P[m][n] = acc
+struct EpiStoreF32 {  // P[m][n] = acc; the MFMA path's K-slice z writes out + z * split_stride
   float* out;
   int ld;
+  size_t split_stride;
   struct Pre {};
   __device__ __forceinline__ Pre prep(int, int) const { return {}; }
   __device__ __forceinline__ void store(int m, int n, float v) const {
     out[static_cast<size_t>(m) * ld + n] = v;
   }
   __device__ __forceinline__ void emit8(const Pre&, int m, int n, const float* v) const {
-    float* o = out + static_cast<size_t>(m) * ld + n;
+    float* o = out + blockIdx.y * split_stride + static_cast<size_t>(m) * ld + n;
     *reinterpret_cast<f32x4*>(o) = *reinterpret_cast<const f32x4*>(v);
     *reinterpret_cast<f32x4*>(o + 4) = *reinterpret_cast<const f32x4*>(v + 4);
   }
@@ -158,6 +159,8 @@ struct EpiScatter {
 //   * the workgroup barrier sits before the last k-step: by then every wave has
 //     read the whole stage, so the loads of tile k+2 are issued into it, one per
 //     MFMA of that last k-step, together with the first fragment reads of tile k+1.
+// A grid with gridDim.y > 1 splits K: workgroup y covers k in [y K, (y + 1) K) and its
+// epilogue writes partial sums to a slice of its own (the router pre-activations).
 // Epilogues: the gate/up product stages its finished bf16 tile in LDS at once and
 // writes 16-byte row pieces; the others first fetch what they combine with (hbar
 // rows) for the whole wave tile, then stage fp32 results in 32-row blocks.
@@ -255,7 +258,7 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
 
   auto issue = [&](int stage, int k0) {
     unsigned char* sa = smem + stage * C::STAGE;
-    const uint32_t kb = static_cast<uint32_t>(k0) * 2;
+    const uint32_t kb = static_cast<uint32_t>(k0 + blockIdx.y * K) * 2;
 #pragma unroll
     for (int i = 0; i < A_LD; ++i) load_lds16(a_base + a_off[i] + kb, sa + (i * NW + wave) * 1024);
 #pragma unroll
@@ -392,13 +395,13 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
 
 template <class C, class Epi>
 hipError_t run_tile(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_count, int M_max,
-                    int N_out, int K, hipStream_t s) {
+                    int N_out, int K, hipStream_t s, int splits = 1) {
   const int mt_max = (M_max + C::BM - 1) / C::BM;
   const int n_tiles = N_out / C::OUT_N;
   const int total = mt_max * n_tiles;
   if (total == 0) return hipSuccess;
-  const int grid = (total + 7) / 8 * 8;
-  mfma_gemm<C, Epi><<<grid, C::NT, 0, s>>>(A, B, epi, m_count, M_max, K, mt_max, n_tiles);
+  const dim3 grid((total + 7) / 8 * 8, splits);
+  mfma_gemm<C, Epi><<<grid, C::NT, 0, s>>>(A, B, epi, m_count, M_max, K / splits, mt_max, n_tiles);
   return hipGetLastError();
 }
 
@@ -617,18 +620,24 @@ int adapter_groups(int K) {
   return G;
 }
 
-using TileRouter = Tile<64, 128, 2, 2, false>;
+// router pre-activations: 128-row tiles over all 8 waves, K split four ways
+using TileRouter = Tile<128, 256, 2, 4, false>;
+using TileRouterNarrow = Tile<128, 128, 2, 4, false>;
 
 }  // namespace
+
+int router_gemm_splits(int dtype, int d) { return dtype == 1 && d % (4 * 64) == 0 ? 4 : 1; }
 
 hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, const void* ps1, int T,
                               int d, int d_e, int d_head, float* P, hipStream_t s) {
   const int N = d_e + d_head;
-  EpiStoreF32 epi{P, N};
+  EpiStoreF32 epi{P, N, static_cast<size_t>(T) * N};
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(hbar), nullptr, d};
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_hd), static_cast<const bf16_t*>(ps1), d_e, d};
-    return run_tile<TileRouter>(A, B, epi, nullptr, T, N, d, s);
+    const int splits = router_gemm_splits(dtype, d);
+    if (N % TileRouter::OUT_N == 0) return run_tile<TileRouter>(A, B, epi, nullptr, T, N, d, s, splits);
+    return run_tile<TileRouterNarrow>(A, B, epi, nullptr, T, N, d, s, splits);
   }
   ARows<float> A{static_cast<const float*>(hbar), nullptr, d};
   BRows<float> B{static_cast<const float*>(w_hd), static_cast<const float*>(ps1), d_e, d};

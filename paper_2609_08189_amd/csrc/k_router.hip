@@ -424,6 +424,7 @@ __global__ __launch_bounds__(NT) void router_post_kernel(RouterTailArgs a) {
 // same router weights).  Output lane i + 16 g holds rows 4 g .. 4 g + 3 of column i.
 // ---------------------------------------------------------------------------
 constexpr int MT = 16;            // tokens per workgroup
+constexpr int MAXSPLIT = 4;       // K-slice partials of P
 constexpr int KS_E = MAXE / 32;   // k-steps over d_e
 constexpr int KS_S = MAXS / 32;   // k-steps over d_s
 constexpr int KS_M = MAXM / 32;   // k-steps over d_m
@@ -477,14 +478,27 @@ __global__ __launch_bounds__(NT) void router_pre_mfma(RouterTailArgs a) {
   const int d_e = a.d_e, d_head = a.d_head, NP = d_e + d_head, DM = a.d_m, d_s = a.d_s;
   const int d_h = a.d_h, d_a = a.d_a, d_p = a.d_p;
 
-  // P segment of 32 values: token tt, segment sg (NP % 32 == 0, NP <= 512)
+  // P segment of 32 values: token tt, segment sg (NP % 32 == 0, NP <= 512), summed over the
+  // K-slice partials in slice order (all loads issued first)
   const int tt = tid >> 4, sg = tid & 15;
   const bool has_seg = 32 * sg < NP;
   f32x4 pv[8];
   if (has_seg) {
     const float* src = a.P + static_cast<size_t>(min(t0 + tt, a.T - 1)) * NP + 32 * sg;
+    const size_t zs = static_cast<size_t>(a.T) * NP;
+    f32x4 pz[MAXSPLIT][8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) pv[q] = *reinterpret_cast<const f32x4*>(src + 4 * q);
+    for (int z = 0; z < MAXSPLIT; ++z)
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        pz[z][q] = *reinterpret_cast<const f32x4*>(src + (z < a.p_splits ? z : 0) * zs + 4 * q);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      pv[q] = pz[0][q];
+#pragma unroll
+      for (int z = 1; z < MAXSPLIT; ++z)
+        if (z < a.p_splits) pv[q] += pz[z][q];
+    }
   }
   if (tid < MT) {
     const int t = t0 + tid;
@@ -805,6 +819,7 @@ size_t router_scratch_floats(int d_m, int d_head, int T) {
 
 hipError_t launch_router_pre(const RouterTailArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
+  if (a.p_splits < 1 || a.p_splits > (a.dtype == 1 ? MAXSPLIT : 1)) return hipErrorInvalidValue;
   return launch_pre_post(a, false, s);
 }
 
