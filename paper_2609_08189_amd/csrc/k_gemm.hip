@@ -13,7 +13,8 @@
 // fragment reads of one MFMA hit distinct banks.  A rows may be gathered through
 // an index list whose length lives on the device (tiles past it exit at once).
 // Workgroups are mapped to tiles so that each XCD (8 per MI355X, round-robin
-// dispatch) owns a contiguous run of tiles that share weight panels in its L2.
+// dispatch) owns a contiguous run of a grouped tile order: the tiles it runs at
+// once share a few row panels and a few weight panels in its L2.
 //
 // f32 path: a plain LDS-tiled VALU GEMM with full bounds checks (small shapes).
 #include <limits.h>
@@ -174,6 +175,8 @@ __device__ __forceinline__ void load_lds16(const void* g, unsigned char* l) {
 
 __device__ __forceinline__ int swz(int row, int ch) { return row * ROWB + ((ch ^ ((row >> 1) & 7)) << 4); }
 
+constexpr int GROUP_M = 8;   // row tiles per group of the tile order
+
 // instruction classes of __builtin_amdgcn_sched_group_barrier
 constexpr int SG_MFMA = 0x008, SG_VMEM_READ = 0x020, SG_DS_READ = 0x100;
 
@@ -210,10 +213,16 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   constexpr int NR = C::TM + C::TN;     // fragment reads per k-step
   constexpr int NL = A_LD + B_LD;       // stage loads per k-tile
   __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * C::STAGE];
+  // Workgroups go to the 8 XCDs round-robin; XCD x takes the contiguous range
+  // [x per, (x+1) per) of a grouped tile order (GROUP_M row tiles by every column tile),
+  // so that the 32 tiles one XCD runs at a time share 8 row panels and 4 column panels
+  // in its L2.
   const int per = gridDim.x >> 3;
   const int tile = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
   if (tile >= mt_max * n_tiles) return;
-  const int mt = tile % mt_max, nt = tile / mt_max;
+  const int grp = tile / (GROUP_M * n_tiles), rem = tile % (GROUP_M * n_tiles);
+  const int gsz = min(GROUP_M, mt_max - grp * GROUP_M);
+  const int mt = grp * GROUP_M + rem % gsz, nt = rem / gsz;
   const int M = m_count ? *m_count : M_fixed;
   const int m0 = mt * C::BM;
   if (m0 >= M) return;
