@@ -518,7 +518,7 @@ hipError_t run_f32(ARows<float> A, BRows<float> B, Epi epi, const int* m_count, 
 // Adapter down-projection partial sums.  Workgroup (row tile of 32, k-group g) has
 // 4 waves, each over a quarter of the group's k range; the 4 partial 32 x d_r
 // tiles are summed in LDS and written to part[g][m][n] (fp32).
-template <int TN>
+template <int TN, int SB>
 __global__ __launch_bounds__(256) void adapter_down_bf16(const bf16_t* __restrict__ u,
                                                          const int* __restrict__ idx,
                                                          const int* __restrict__ m_count,
@@ -541,14 +541,23 @@ __global__ __launch_bounds__(256) void adapter_down_bf16(const bf16_t* __restric
   for (int b = 0; b < TN; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
-  for (int k = kbeg; k < kbeg + kw; k += 16) {
-    const bf16x8 fa = *reinterpret_cast<const bf16x8*>(arow + k);
+  // SB 16-deep k-steps per batch, all of a batch's loads issued first (kw % (16 SB) == 0)
+  for (int k = kbeg; k < kbeg + kw; k += 16 * SB) {
+    bf16x8 fa[SB], fb[SB][TN];
 #pragma unroll
-    for (int b = 0; b < TN; ++b) {
-      const bf16x8 fb = *reinterpret_cast<const bf16x8*>(
-          w1 + static_cast<size_t>(b * 32 + (lane & 31)) * K + 8 * (lane >> 5) + k);
-      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, acc[b], 0, 0, 0);
+    for (int st = 0; st < SB; ++st) {
+      fa[st] = *reinterpret_cast<const bf16x8*>(arow + k + 16 * st);
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+        fb[st][b] = *reinterpret_cast<const bf16x8*>(
+            w1 + static_cast<size_t>(b * 32 + (lane & 31)) * K + 8 * (lane >> 5) + k + 16 * st);
     }
+    __builtin_amdgcn_sched_barrier(0);   // keep the whole batch of loads ahead of the MFMAs
+#pragma unroll
+    for (int st = 0; st < SB; ++st)
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[st], fb[st][b], acc[b], 0, 0, 0);
   }
 #pragma unroll
   for (int b = 0; b < TN; ++b)
@@ -566,68 +575,113 @@ __global__ __launch_bounds__(256) void adapter_down_bf16(const bf16_t* __restric
   }
 }
 
-// Adapter up-projection with scatter: hid = SiLU(sum_g part[g]) rounded to bf16 as the
-// MFMA A operand; workgroup (row tile of 32, column tile of 256), wave = 64 columns.
-template <int KR>
-__global__ __launch_bounds__(256) void adapter_up_bf16(const float* __restrict__ part, int G,
+// Adapter up-projection with scatter, one workgroup per (32 rows, 256 columns):
+//   hid = SiLU(sum_g part[g]) for the 32 rows, rounded to bf16 (the MFMA A operand), in LDS;
+//   each wave computes 64 columns; results are staged in LDS and every thread then writes
+//   8-column pieces h_out[t] = hbar[t] + (1 - g_t) acc with hbar fetched at the start.
+template <int KR, int G>
+__global__ __launch_bounds__(256) void adapter_up_bf16(const float* __restrict__ part,
                                                        const int* __restrict__ idx,
                                                        const int* __restrict__ m_count,
                                                        const bf16_t* __restrict__ w2,
                                                        const bf16_t* __restrict__ hbar,
                                                        const float* __restrict__ gate,
                                                        bf16_t* __restrict__ out, int T, int d) {
+  constexpr int NC = 256;
+  constexpr int HP = KR + 8;     // hid row pitch (bf16)
+  constexpr int SP = NC + 4;     // staged row pitch (fp32)
+  constexpr int PPT = 32 * NC / 8 / 256;   // 8-column output pieces per thread
+  __shared__ __attribute__((aligned(16))) bf16_t hid[32 * HP];
+  __shared__ __attribute__((aligned(16))) float stg[32 * SP];
   const int M = *m_count;
   const int m0 = blockIdx.x * 32;
   if (m0 >= M) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n0 = blockIdx.y * 256 + wave * 64;
-  const int mr = min(m0 + (lane & 31), M - 1);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n0 = blockIdx.y * NC;
+  EpiScatter<bf16_t, true> epi{idx, hbar, gate, out, d};
+  typename EpiScatter<bf16_t, true>::Pre pre[PPT];
+#pragma unroll
+  for (int q = 0; q < PPT; ++q) {
+    const int e = tid + 256 * q;
+    pre[q] = epi.prep(min(m0 + (e >> 5), M - 1), n0 + (e & 31) * 8);
+  }
+  for (int e = tid; e < 32 * KR / 8; e += 256) {
+    const int i = e / (KR / 8), k8 = (e % (KR / 8)) * 8;
+    const int mr = min(m0 + i, M - 1);
+    f32x4 x[G][2];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float* p = part + (static_cast<size_t>(g) * T + mr) * KR + k8;
+      x[g][0] = *reinterpret_cast<const f32x4*>(p);
+      x[g][1] = *reinterpret_cast<const f32x4*>(p + 4);
+    }
+    bf16x8 v;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      float h = 0.f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) h += x[g][c >> 2][c & 3];
+      v[c] = static_cast<__bf16>(siluf_(h));
+    }
+    *reinterpret_cast<bf16x8*>(hid + i * HP + k8) = v;
+  }
+  bf16x8 fb[KR / 16][2];
+#pragma unroll
+  for (int st = 0; st < KR / 16; ++st)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+      fb[st][b] = *reinterpret_cast<const bf16x8*>(
+          w2 + static_cast<size_t>(n0 + wave * 64 + b * 32 + (lane & 31)) * KR + 16 * st + 8 * (lane >> 5));
+  __syncthreads();
   f32x16 acc[2];
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
 #pragma unroll
-  for (int k = 0; k < KR; k += 16) {
-    const int kk = k + 8 * (lane >> 5);
-    float h[8];
+  for (int st = 0; st < KR / 16; ++st) {
+    const bf16x8 fa = *reinterpret_cast<const bf16x8*>(hid + (lane & 31) * HP + 16 * st + 8 * (lane >> 5));
 #pragma unroll
-    for (int e = 0; e < 8; ++e) h[e] = 0.f;
-    for (int g = 0; g < G; ++g) {
-      const float* p = part + (static_cast<size_t>(g) * T + mr) * KR + kk;
-      const f32x4 x0 = *reinterpret_cast<const f32x4*>(p);
-      const f32x4 x1 = *reinterpret_cast<const f32x4*>(p + 4);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        h[e] += x0[e];
-        h[4 + e] += x1[e];
-      }
-    }
-    bf16x8 fa;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) fa[e] = static_cast<__bf16>(siluf_(h[e]));
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const bf16x8 fb = *reinterpret_cast<const bf16x8*>(
-          w2 + static_cast<size_t>(n0 + b * 32 + (lane & 31)) * KR + kk);
-      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, acc[b], 0, 0, 0);
-    }
+    for (int b = 0; b < 2; ++b) acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb[st][b], acc[b], 0, 0, 0);
   }
-  EpiScatter<bf16_t, true> epi{idx, hbar, gate, out, d};
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    const int m = m0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    if (m >= M) continue;
+    const int i = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 #pragma unroll
-    for (int b = 0; b < 2; ++b) epi.store(m, n0 + b * 32 + (lane & 31), acc[b][r]);
+    for (int b = 0; b < 2; ++b) stg[i * SP + wave * 64 + b * 32 + (lane & 31)] = acc[b][r];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < PPT; ++q) {
+    const int e = tid + 256 * q;
+    const int i = e >> 5, c8 = (e & 31) * 8;
+    if (m0 + i < M) epi.emit8(pre[q], m0 + i, n0 + c8, stg + i * SP + c8);
   }
 }
 
+template <int KR>
+void adapter_up_launch(dim3 g2, hipStream_t s, int G, const float* part, const int* idx, const int* counts,
+                       const bf16_t* w2, const bf16_t* hb, const float* gate, bf16_t* ho, int T, int d) {
+  switch (G) {
+    case 1: adapter_up_bf16<KR, 1><<<g2, 256, 0, s>>>(part, idx, counts, w2, hb, gate, ho, T, d); break;
+    case 2: adapter_up_bf16<KR, 2><<<g2, 256, 0, s>>>(part, idx, counts, w2, hb, gate, ho, T, d); break;
+    case 4: adapter_up_bf16<KR, 4><<<g2, 256, 0, s>>>(part, idx, counts, w2, hb, gate, ho, T, d); break;
+    default: adapter_up_bf16<KR, 8><<<g2, 256, 0, s>>>(part, idx, counts, w2, hb, gate, ho, T, d); break;
+  }
+}
+
+// K-slices of the adapter down-projection: up to 8, each deep enough for whole batches
+// (four waves times SB 16-deep k-steps); eight-step batches where the depth allows.
 int adapter_groups(int K) {
-  int G = 1;
-  while (K % (2 * G * 64) == 0 && K / (2 * G) >= 1024) G *= 2;
+  int G = 8;
+  while (G > 1 && K % (G * 512) != 0) G >>= 1;
+  if (K % (G * 512) != 0) {
+    G = 8;
+    while (G > 1 && K % (G * 256) != 0) G >>= 1;
+  }
   return G;
 }
+int adapter_batch(int K, int G) { return (K / G) % 512 == 0 ? 8 : 4; }
 
 // router pre-activations: 128-row tiles over all 8 waves, K split four ways
 using TileRouter = Tile<128, 256, 2, 4, false>;
@@ -702,13 +756,18 @@ hipError_t launch_adapter_down(int dtype, const void* u, const int* idx_ad, cons
     const bf16_t* uu = static_cast<const bf16_t*>(u);
     const bf16_t* ww = static_cast<const bf16_t*>(w1);
     // the adapter rank is a compile-time count of 32-column MFMA tiles
+    const bool b8 = adapter_batch(d, G) == 8;
+#define HERO_ADAPTER_DOWN(TN_)                                                                       \
+  (b8 ? adapter_down_bf16<TN_, 8><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G)  \
+      : adapter_down_bf16<TN_, 4><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G))
     switch (d_r) {
-      case 32: adapter_down_bf16<1><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G); break;
-      case 64: adapter_down_bf16<2><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G); break;
-      case 96: adapter_down_bf16<3><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G); break;
-      case 128: adapter_down_bf16<4><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G); break;
+      case 32: HERO_ADAPTER_DOWN(1); break;
+      case 64: HERO_ADAPTER_DOWN(2); break;
+      case 96: HERO_ADAPTER_DOWN(3); break;
+      case 128: HERO_ADAPTER_DOWN(4); break;
       default: return hipErrorInvalidValue;
     }
+#undef HERO_ADAPTER_DOWN
     return hipGetLastError();
   }
   // fp32: hid = SiLU(u W_1^T) into part[m][n]
@@ -728,10 +787,10 @@ hipError_t launch_adapter_up(int dtype, const float* part, const int* idx_ad, co
     const bf16_t* hb = static_cast<const bf16_t*>(hbar);
     bf16_t* ho = static_cast<bf16_t*>(h_out);
     switch (d_r) {
-      case 32: adapter_up_bf16<32><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
-      case 64: adapter_up_bf16<64><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
-      case 96: adapter_up_bf16<96><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
-      case 128: adapter_up_bf16<128><<<g2, 256, 0, s>>>(part, G, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
+      case 32: adapter_up_launch<32>(g2, s, G, part, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
+      case 64: adapter_up_launch<64>(g2, s, G, part, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
+      case 96: adapter_up_launch<96>(g2, s, G, part, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
+      case 128: adapter_up_launch<128>(g2, s, G, part, idx_ad, counts, ww, hb, gate, ho, n_max, d); break;
       default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -13,6 +13,30 @@
 
 namespace hero {
 
+// Eight consecutive elements as loaded (bf16 stays packed: 4 registers per chunk).
+template <typename T> struct Raw8;
+template <> struct Raw8<bf16_t> {
+  u32x4 v;
+  __device__ __forceinline__ void load(const bf16_t* p) { v = *reinterpret_cast<const u32x4*>(p); }
+  __device__ __forceinline__ float operator[](int i) const {
+    const uint32_t w = v[i >> 1];
+    return __uint_as_float((i & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+};
+template <> struct Raw8<float> {
+  f32x4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = *reinterpret_cast<const f32x4*>(p);
+    b = *reinterpret_cast<const f32x4*>(p + 4);
+  }
+  __device__ __forceinline__ float operator[](int i) const { return i < 4 ? a[i] : b[i - 4]; }
+};
+
+// Each lane owns CH 8-element chunks of a row per batch (chunk c at column 8 (lane + 64 c));
+// all loads of a batch are issued before any is used, and when the row fits in one batch
+// hbar stays in registers for the normalisation pass.
+constexpr int CH = 8;
+
 template <typename T>
 __global__ __launch_bounds__(256) void rowstats_kernel(const T* __restrict__ hbar,
                                                        const T* __restrict__ prev1,
@@ -25,29 +49,38 @@ __global__ __launch_bounds__(256) void rowstats_kernel(const T* __restrict__ hba
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= ntok) return;
   const size_t row = static_cast<size_t>(t) * d;
+  constexpr int W = 8 * kWave;   // columns per chunk step of the wave
   float ss = 0.f, dd = 0.f, dp = 0.f, pp = 0.f;
-  for (int c = lane * 8; c < d; c += 64 * 8) {
-    float h[8];
-    ld8(hbar + row + c, h);
+  Raw8<T> h[CH];
+  const bool resident = d <= CH * W;
+  for (int c0 = 0; c0 < d; c0 += CH * W) {
+    Raw8<T> a[CH], b[CH];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) ss += h[i] * h[i];
-    if (j >= 2) {
-      float a[8];
-      ld8(prev1 + row + c, a);
+    for (int c = 0; c < CH; ++c) {
+      const int col = c0 + c * W + 8 * lane;
+      if (col < d) {
+        h[c].load(hbar + row + col);
+        if (j >= 2) a[c].load(prev1 + row + col);
+        if (j >= 3) b[c].load(prev2 + row + col);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int col = c0 + c * W + 8 * lane;
+      if (col >= d) continue;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float dj = h[i] - a[i];
-        dd += dj * dj;
-      }
-      if (j >= 3) {
-        float b[8];
-        ld8(prev2 + row + c, b);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const float dj = h[i] - a[i];
-          const float dq = a[i] - b[i];
-          dp += dj * dq;
-          pp += dq * dq;
+        const float hv = h[c][i];
+        ss += hv * hv;
+        if (j >= 2) {
+          const float av = a[c][i];
+          const float dj = hv - av;
+          dd += dj * dj;
+          if (j >= 3) {
+            const float dq = av - b[c][i];
+            dp += dj * dq;
+            pp += dq * dq;
+          }
         }
       }
     }
@@ -61,13 +94,25 @@ __global__ __launch_bounds__(256) void rowstats_kernel(const T* __restrict__ hba
     f32x4 r = {inv_rms, dd, dp, pp};
     *reinterpret_cast<f32x4*>(rowstat + 4 * static_cast<size_t>(t)) = r;
   }
-  for (int c = lane * 8; c < d; c += 64 * 8) {
-    float h[8], w[8], o[8];
-    ld8(hbar + row + c, h);
-    ld8(norm_w + c, w);
+  for (int c0 = 0; c0 < d; c0 += CH * W) {
+    Raw8<T> w[CH];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) o[i] = h[i] * inv_rms * w[i];
-    st8(u + row + c, o);
+    for (int c = 0; c < CH; ++c) {
+      const int col = c0 + c * W + 8 * lane;
+      if (col < d) {
+        if (!resident) h[c].load(hbar + row + col);
+        w[c].load(norm_w + col);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int col = c0 + c * W + 8 * lane;
+      if (col >= d) continue;
+      float o[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = h[c][i] * inv_rms * w[c][i];
+      st8(u + row + col, o);
+    }
   }
 }
 
