@@ -126,6 +126,35 @@ def cpu_baseline(prob, gpu_stats, j, target_s=12.0, max_tokens=None):
                       f"branch decisions teacher-forced to the GPU's), {dt:.1f} s"}
 
 
+COUNTERS_MD = os.path.join(ROOT, "profiles", "routed_layer_llama31_8b_hbm_counters.md")
+GEMM_SOURCES = ("paper_2609_08189_amd/csrc/k_gemm.hip", "paper_2609_08189_amd/csrc/hero_device.h")
+
+
+def gemm_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def counted_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary
+    (scaled by the copy calibration there), or None when the GEMM sources changed since."""
+    try:
+        text = open(COUNTERS_MD).read()
+    except OSError:
+        return None
+    if f"`{gemm_source_hash()}`" not in text:
+        return None
+    for line in text.splitlines():
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) == 5 and cells[0] == kernel:
+            return int(round((float(cells[3]) + float(cells[4])) * 1e6))
+    return None
+
+
 def _short(name):
     return name.replace("hero::(anonymous namespace)::", "").replace("void ", "")[:150].replace("|", "/")
 
@@ -262,9 +291,11 @@ def main():
     achieved = dflops / (dom_ms * 1e-3) * 1e-12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": None, "kernel": dom,
+            "frac": round(achieved / peak, 4), "traffic": counted_traffic(dom), "kernel": dom,
             "avg_launch_us": round(dom_ms * 1e3, 2),
-            "work_per_launch": f"4*d*d_ff FLOP per FFN token x {n_f} FFN tokens = {dflops / 1e9:.1f} GFLOP"}
+            "work_per_launch": f"4*d*d_ff FLOP per FFN token x {n_f} FFN tokens = {dflops / 1e9:.1f} GFLOP",
+            "traffic_note": "HBM bytes read + written per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1, "
+                            "calibrated on a 1 GiB copy) from profiles/, null if the GEMM changed since"}
 
     result = {
         "metric": "routed-FFN-stack tokens/sec at Llama-3.1-8B shape; % MFMA/HBM roofline",

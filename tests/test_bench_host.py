@@ -1,0 +1,39 @@
+"""Host-side checks of bench.py that need no GPU: the --gpus contract, the rocprofv3 summary
+parser, and the rule that roofline.traffic comes from committed counters only while the GEMM
+sources they were taken with are unchanged."""
+import os
+import subprocess
+import sys
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_exits_with_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_traffic_from_committed_counters(monkeypatch):
+    t = bench.counted_traffic("ffn_gate_up")
+    assert t is not None and t > 260e6       # at least the algorithmic bytes of the launch
+    assert bench.counted_traffic("no_such_kernel") is None
+    # any change to the hashed sources makes the committed counters stale
+    monkeypatch.setattr(bench, "GEMM_SOURCES", ("paper_2609_08189_amd/csrc/k_select.hip",))
+    assert bench.counted_traffic("ffn_gate_up") is None
+
+
+def test_summarize_reads_rocprof_csv(tmp_path, capsys):
+    d = tmp_path / "prof"
+    d.mkdir()
+    (d / "x_kernel_stats.csv").write_text(
+        '"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs","StdDev"\n'
+        '"void hero::(anonymous namespace)::k(int)",3,3000,1000,100.0,900,1100,0\n')
+    (d / "x_counter_collection.csv").write_text(
+        '"Kernel_Name","Counter_Name","Counter_Value"\n"k(int)","FETCH_SIZE",10\n"k(int)","FETCH_SIZE",30\n')
+    bench.summarize_rocprof(str(d))
+    out = capsys.readouterr().out
+    assert "| k(int) | 3 | 0.003 | 1.00 | 0.90 | 1.10 | 100.00 |" in out
+    assert "| k(int) | FETCH_SIZE | 2 | 20.0 | 30.0 |" in out
