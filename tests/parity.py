@@ -177,7 +177,7 @@ def check_stack(prob, gpu_res, rows=None, report=None):
     return errs
 
 
-def check_stack_layerwise(prob, layer_io, rows=None, report=None):
+def check_stack_layerwise(prob, layer_io, rows=None, report=None, verbose=False):
     """Deep stacks: every routed layer checked on the GPU's own inputs.
 
     ``layer_io[j-1]`` holds, for the selected token rows, what the GPU fed into and got out
@@ -218,6 +218,9 @@ def check_stack_layerwise(prob, layer_io, rows=None, report=None):
         if far.any():
             far_info.append((j, R.gate[far][:4].tolist(), thr))
         n_band += int(mism.sum())
+        if verbose:
+            print(f"  layer {j}: n_ffn {L['n_ffn']}, logit err {scalar_err(L['logit'][sel], R.logit):.2e}, "
+                  f"{int(mism.sum())} band flips", flush=True)
         e = dict(logit=scalar_err(L["logit"][sel], R.logit), gate=scalar_err(L["gate"][sel], R.gate),
                  h=row_rel_err(io["h"], R.h), S=row_rel_err(io["S1"], R.state.S),
                  zeta=row_rel_err(io["zeta1"], R.state.zeta), p=scalar_err(io["p1"], R.state.p_hist),

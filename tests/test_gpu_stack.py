@@ -108,3 +108,47 @@ def test_llama2_7b_decode_stack_full_shape():
           flush=True)
     del dp
     torch.cuda.empty_cache()
+
+
+def _full_stack_sampled(name, n_rows=48, seed=0):
+    """A full-size stack workload: the stack is run once, then rerun as chained layer calls,
+    which must reproduce it bit for bit (output and final state, compared on the device);
+    the chained run captures a seeded sample of token rows per layer, and every layer is
+    checked on those rows against the oracle on the GPU's own inputs."""
+    import torch
+    from paper_2609_08189_amd.device import DeviceProblem
+    from tests.parity import check_stack_layerwise
+    w = synth.WORKLOADS[name]
+    print(f"case {w.name} L_R={w.L_R} T={w.T} d={w.d} d_ff={w.d_ff} d_m={w.d_m} mode={w.mode} "
+          f"sampled rows={n_rows}", flush=True)
+    prob = synth.make_problem(w, seed=seed)
+    dp = DeviceProblem(prob)
+    print("  inputs on the device", flush=True)
+    dp.run_stack()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (dp.h_out, dp.S, dp.zeta, dp.p_hist, dp.m_hist)]
+    rows = np.sort(np.random.default_rng(1234 + seed).choice(w.T, size=n_rows, replace=False))
+    io = dp.run_chained(rows=rows)
+    torch.cuda.synchronize()
+    for a, b in zip((dp.h_out, dp.S, dp.zeta, dp.p_hist, dp.m_hist), ref):
+        assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
+                           b.view(torch.int16) if b.dtype == torch.bfloat16 else b)
+    print("  stack == chained layer calls (bit-exact)", flush=True)
+    del ref
+    report = {}
+    check_stack_layerwise(prob, io, rows=rows, report=report, verbose=True)
+    print("  per-layer errors:", {k: (f"{v:.2e}" if isinstance(v, float) else v) for k, v in report.items()},
+          flush=True)
+    del dp
+    torch.cuda.empty_cache()
+
+
+def test_llama31_8b_stack_full_shape():
+    """Llama-3.1-8B shape, 32 routed layers, 16 x 2048 tokens, skip budget 38.82 %."""
+    _full_stack_sampled("llama31_8b_stack")
+
+
+def test_llama2_13b_prefill_full_shape():
+    """Llama-2-13B shape, 40 routed layers, 8 x 4096 tokens, threshold rule with the
+    position-clustered bimodal logit bias."""
+    _full_stack_sampled("llama2_13b_prefill")
