@@ -62,13 +62,18 @@ class HipEvents:
             self.hip.hipEventDestroy(e)
 
 
-def kernel_work(w, n_f, n_a, T, j):
-    """Algorithmic FLOPs and HBM bytes per launch of each kernel (bf16 I/O, fp32 state)."""
+def kernel_work(w, n_f, n_a, T, j, memory="matrix"):
+    """Algorithmic FLOPs and HBM bytes per launch of each kernel (bf16 I/O, fp32 state).
+    The memory pass moves S and zeta (read unless j = 1, written) in matrix form, or reads the
+    j-1 stored (phi(k), v) pairs and writes one in depth-history form."""
     es = 2 if w.dtype == "bf16" else 4
     d, dff, r, dm = w.d, w.d_ff, w.d_r, w.d_m
     npre = w.d_e + w.d_head
     hid_reads = 1 + (j >= 2) + (j >= 3)
-    state_rw = (2 if j > 1 else 1) * 4 * (dm * dm + dm)
+    if memory == "history":
+        state_rw = 4 * 2 * dm * ((j - 1) + 1)
+    else:
+        state_rw = (2 if j > 1 else 1) * 4 * (dm * dm + dm)
     return {
         "rowstats": dict(flops=0, bytes=T * (hid_reads * d * es + d * es + 16)),
         "router_gemm": dict(flops=2 * d * npre * T, bytes=T * (d * es + 4 * npre)),
@@ -203,6 +208,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-target-s", type=float, default=12.0)
+    ap.add_argument("--memory", choices=("matrix", "history"), default="matrix",
+                    help="router memory as the matrix S (the paper's form) or in depth-history form")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device-to-device copy of this many MiB (HBM counter calibration)")
     ap.add_argument("--summarize", metavar="DIR",
@@ -229,7 +236,7 @@ def main():
     j = w.layer_j
     print(f"# preparing {describe(w, j)}", file=sys.stderr, flush=True)
     prob = synth.make_problem(w, seed=args.seed)
-    dp = DeviceProblem(prob, device="cuda:0", stats=True)
+    dp = DeviceProblem(prob, device="cuda:0", stats=True, history=args.memory == "history")
     stream = dp.stream()
     ev = HipEvents()
 
@@ -272,7 +279,7 @@ def main():
     for _ in range(K):
         dp.run_layer(j)
     torch.cuda.synchronize()
-    work = kernel_work(w, n_f, n_a, w.T, j)
+    work = kernel_work(w, n_f, n_a, w.T, j, args.memory)
     for name in H.KERNELS:
         H.hero_kernel_timer(H.HERO_K[name], [], [])
         a, b = handles[name]
@@ -302,7 +309,9 @@ def main():
         "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
-        "config": {"workload": describe(w, j), "global_batch": w.batch, "seq_len": w.seq,
+        "config": {"workload": describe(w, j) + ("" if args.memory == "matrix" else
+                                                 ", router memory in depth-history form"),
+                   "memory": args.memory, "global_batch": w.batch, "seq_len": w.seq,
                    "tokens": w.T, "parallelism": "none", "n_ffn": n_f, "n_adapter": n_a},
         "roofline": roof,
         "kernels": per,

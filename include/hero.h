@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define HERO_ABI_VERSION 1
+#define HERO_ABI_VERSION 2
 
 typedef enum hero_status {
   HERO_OK = 0,
@@ -226,6 +226,60 @@ int hero_routed_stack(const hero_dims *dims, int T, const void *h_in, void *h_ou
                       const float *eta, const hero_routing *routing,
                       const hero_layer_stats *stats,
                       void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Depth-history form of the router memory.  The memory recursion of Sec. 3.2
+ * (eq:memory_update) starts from S_0 = 0, zeta_0 = 0, so it unrolls to
+ *   S_{j-1} = sum_{i<j} w_{j,i} phi(k_i) v_i^T,  zeta_{j-1} = sum_{i<j} w_{j,i} phi(k_i),
+ *   w_{j,i} = prod_{l=i+1}^{j-1} rho_l,  rho_l = sigma(eta_l),
+ * and the read of layer j (eq:memory_read) becomes attention over depth,
+ *   c_j = sum_i a_i v_i / (sum_i a_i + eps),  a_i = w_{j,i} phi(q_j) . phi(k_i).
+ * This form keeps the pairs (phi(k_i), v_i) instead of S and zeta: 2 d_m floats
+ * per token per layer, read j-1 times at layer j, instead of d_m^2 + d_m floats
+ * read and written at every layer.  The results equal those of the matrix form
+ * up to fp32 rounding order.  Supported for L_R <= 64.
+ */
+typedef struct hero_history {
+  float *kv;      /* [T][L_R][2][d_m] fp32: entry i-1 holds phi(k_i), then v_i, of routed layer i;
+                     layer j reads entries 0..j-2 and writes entry j-1 */
+  float *p_hist;  /* [T] fp32, in/out (as in hero_state) */
+  float *m_hist;  /* [T] fp32, in/out                    */
+} hero_history;
+
+/*
+ * hero_routed_layer with the memory in depth-history form.  eta is a HOST array
+ * of the j values eta_1 .. eta_j (the decays of the earlier layers weight the
+ * stored pairs).  Entries j .. L_R-1 of the history are neither read nor written.
+ * Everything else, including the workspace, is as for hero_routed_layer.
+ */
+int hero_routed_layer_hist(const hero_dims *dims, int j, int T,
+                           const void *hbar, const void *hbar_prev1, const void *hbar_prev2,
+                           void *h_out, const hero_history *history,
+                           const hero_ffn_weights *ffn, const hero_router_weights *router,
+                           const hero_adapter_weights *adapter, const float *eta,
+                           const hero_routing *routing, const hero_layer_stats *stats,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * hero_routed_stack with the memory in depth-history form: on return
+ * history->kv holds all L_R entries.  The result equals L_R chained
+ * hero_routed_layer_hist calls bit for bit.
+ */
+int hero_routed_stack_hist(const hero_dims *dims, int T, const void *h_in, void *h_out,
+                           const hero_history *history, const hero_ffn_weights *ffn,
+                           const hero_router_weights *router, const hero_adapter_weights *adapter,
+                           const float *eta, const hero_routing *routing,
+                           const hero_layer_stats *stats,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * The matrix-form state after routed layer n (0 <= n <= L_R) from a history:
+ * S[t] = sum_{i<=n} w_{n+1,i} phi(k_i) v_i^T and zeta[t] likewise (see above);
+ * n = 0 gives zeros.  eta: HOST array of n values.  S [T][d_m][d_m] and
+ * zeta [T][d_m] fp32 must not overlap kv.  Asynchronous on `stream`.
+ */
+int hero_history_state(const hero_dims *dims, int n, int T, const float *kv, const float *eta,
+                       float *S, float *zeta, void *stream);
 
 #ifdef __cplusplus
 }

@@ -291,6 +291,26 @@ def memory_write(k, v, S_prev, zeta_prev, rho):
     return S, zeta
 
 
+def memory_from_pairs(phik, v, rho):
+    """The memory after n routed layers, from their key/value pairs (eq:memory_update unrolled).
+
+    With the zero initial state of Sec. 3.2, n applications of memory_write give
+        S_n = sum_{i=1..n} (prod_{l=i+1..n} rho_l) phi(k_i) v_i^T,   zeta_n likewise with phi(k_i),
+    phik, v: [T, n, d_m] (phi(k_i) and v_i of layers 1..n), rho: [n] (rho_l of layers 1..n).
+    This is the state behind the depth-history form of the memory.
+    """
+    T, n, dm = phik.shape
+    S = np.zeros((T, dm, dm))
+    zeta = np.zeros((T, dm))
+    for i in range(n):
+        w = 1.0
+        for l in range(i + 1, n):
+            w *= rho[l]
+        S += w * phik[:, i, :, None] * v[:, i, None, :]
+        zeta += w * phik[:, i, :]
+    return S, zeta
+
+
 # ---------------------------------------------------------------------------
 # Sec. 3.2  HeRo router: gate computation
 # ---------------------------------------------------------------------------

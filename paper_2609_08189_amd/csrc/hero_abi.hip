@@ -108,6 +108,12 @@ int check_state(const hero_state* s) {
   return HERO_OK;
 }
 
+int check_history(const hero_history* h) {
+  if (!h || !h->kv || !h->p_hist || !h->m_hist) return HERO_E_NULL;
+  if (!aligned16(h->kv) || !aligned16(h->p_hist) || !aligned16(h->m_hist)) return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
 int check_stats(const hero_layer_stats* s) {
   if (!s) return HERO_OK;
   const void* ptrs[] = {s->mask, s->idx_ffn, s->idx_ad, s->counts, s->logit, s->gate, s->lambda};
@@ -170,7 +176,21 @@ struct LayerCall {
   unsigned char* ws;
   const Layout* L;
   hipStream_t stream;
+  // depth-history form of the memory: the pairs and the weights of the j-1 stored ones
+  const hero_history* hist = nullptr;
+  const float* hw = nullptr;
 };
+
+// rho_l = sigma(eta_l); w[i] = prod_{l=i+2}^{j-1} rho_l is the weight of entry i (routed layer
+// i+1) in the read of layer j, i < j-1 (eta: host, eta_1 .. eta_{j-1} at least)
+void history_weights(const float* eta, int j, float* w) {
+  double acc = 1.0;
+  for (int i = j - 2; i >= 0; --i) {
+    w[i] = static_cast<float>(acc);
+    const double rho = 1.0 / (1.0 + exp(-static_cast<double>(eta[i])));   // layer i+1
+    acc *= rho;
+  }
+}
 
 int run_layer(const LayerCall& c) {
   using namespace hero;
@@ -232,10 +252,17 @@ int run_layer(const LayerCall& c) {
   ra.th2 = c.rt->th2;
   ra.ps2 = c.rt->ps2;
   ra.beta = c.rc->logit_bias;
-  ra.S = c.st->S;
-  ra.zeta = c.st->zeta;
-  ra.p_hist = c.st->p_hist;
-  ra.m_hist = c.st->m_hist;
+  if (c.hist) {
+    ra.kv = c.hist->kv;
+    ra.p_hist = c.hist->p_hist;
+    ra.m_hist = c.hist->m_hist;
+    for (int i = 0; i < c.j - 1; ++i) ra.hw[i] = c.hw[i];
+  } else {
+    ra.S = c.st->S;
+    ra.zeta = c.st->zeta;
+    ra.p_hist = c.st->p_hist;
+    ra.m_hist = c.st->m_hist;
+  }
   ra.logit = logit;
   ra.gate = gate;
   {
@@ -248,7 +275,9 @@ int run_layer(const LayerCall& c) {
   }
   e = timed(HERO_K_ROUTER_PRE, st, [&] { return launch_router_pre(ra, st); });
   if (e != hipSuccess) return HERO_E_LAUNCH;
-  e = timed(HERO_K_ROUTER_MEM, st, [&] { return launch_router_mem(ra, st); });
+  e = timed(HERO_K_ROUTER_MEM, st, [&] {
+    return c.hist ? launch_router_mem_hist(ra, st) : launch_router_mem(ra, st);
+  });
   if (e != hipSuccess) return HERO_E_LAUNCH;
   e = timed(HERO_K_ROUTER_POST, st, [&] { return launch_router_post(ra, st); });
   if (e != hipSuccess) return HERO_E_LAUNCH;
@@ -353,12 +382,14 @@ int hero_workspace_size(const hero_dims* dims, int T, int for_stack, size_t* byt
   return HERO_OK;
 }
 
-int hero_routed_layer(const hero_dims* dims, int j, int T, const void* hbar, const void* hbar_prev1,
-                      const void* hbar_prev2, void* h_out, const hero_state* state,
-                      const hero_ffn_weights* ffn, const hero_router_weights* router,
-                      const hero_adapter_weights* adapter, float eta, const hero_routing* routing,
-                      const hero_layer_stats* stats, void* workspace, size_t workspace_bytes,
-                      void* stream) {
+namespace {
+
+// Checks shared by both forms of the layer call; state or history is checked by the caller.
+int check_layer_call(const hero_dims* dims, int j, int T, const void* hbar, const void* hbar_prev1,
+                     const void* hbar_prev2, const void* h_out, const hero_ffn_weights* ffn,
+                     const hero_router_weights* router, const hero_adapter_weights* adapter,
+                     const hero_routing* routing, const hero_layer_stats* stats, const void* workspace,
+                     size_t workspace_bytes, Layout* L) {
   int st = check_dims(dims);
   if (st != HERO_OK) return st;
   if (T <= 0) return HERO_E_DIM;
@@ -369,19 +400,34 @@ int hero_routed_layer(const hero_dims* dims, int j, int T, const void* hbar, con
   if (!aligned16(hbar) || !aligned16(h_out) || (j >= 2 && !aligned16(hbar_prev1)) ||
       (j >= 3 && !aligned16(hbar_prev2)))
     return HERO_E_ALIGN;
-  if ((st = check_state(state)) != HERO_OK) return st;
   if ((st = check_weights(ffn, router, adapter)) != HERO_OK) return st;
   if ((st = check_routing(routing)) != HERO_OK) return st;
   if ((st = check_stats(stats)) != HERO_OK) return st;
-  if (!(eta == eta)) return HERO_E_RANGE;
   const size_t hb = static_cast<size_t>(T) * dims->d * esize(dims->dtype);
   if (overlap(h_out, hb, hbar, hb) || (j >= 2 && overlap(h_out, hb, hbar_prev1, hb)) ||
       (j >= 3 && overlap(h_out, hb, hbar_prev2, hb)))
     return HERO_E_ALIAS;
-  const Layout L = layout_of(*dims, T, false);
+  *L = layout_of(*dims, T, false);
   if (!workspace) return HERO_E_WORKSPACE;
-  if (workspace_bytes < L.total) return HERO_E_WORKSPACE;
+  if (workspace_bytes < L->total) return HERO_E_WORKSPACE;
   if (!aligned16(workspace)) return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+}  // namespace
+
+int hero_routed_layer(const hero_dims* dims, int j, int T, const void* hbar, const void* hbar_prev1,
+                      const void* hbar_prev2, void* h_out, const hero_state* state,
+                      const hero_ffn_weights* ffn, const hero_router_weights* router,
+                      const hero_adapter_weights* adapter, float eta, const hero_routing* routing,
+                      const hero_layer_stats* stats, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  Layout L;
+  int st = check_layer_call(dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, ffn, router, adapter, routing,
+                            stats, workspace, workspace_bytes, &L);
+  if (st != HERO_OK) return st;
+  if ((st = check_state(state)) != HERO_OK) return st;
+  if (!(eta == eta)) return HERO_E_RANGE;
   if ((st = check_device()) != HERO_OK) return st;
   LayerCall c{dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, state, ffn, router, adapter, eta,
               routing, stats, static_cast<unsigned char*>(workspace), &L,
@@ -389,17 +435,48 @@ int hero_routed_layer(const hero_dims* dims, int j, int T, const void* hbar, con
   return run_layer(c);
 }
 
-int hero_routed_stack(const hero_dims* dims, int T, const void* h_in, void* h_out,
-                      const hero_state* state, const hero_ffn_weights* ffn,
-                      const hero_router_weights* router, const hero_adapter_weights* adapter,
-                      const float* eta, const hero_routing* routing, const hero_layer_stats* stats,
-                      void* workspace, size_t workspace_bytes, void* stream) {
+int hero_routed_layer_hist(const hero_dims* dims, int j, int T, const void* hbar, const void* hbar_prev1,
+                           const void* hbar_prev2, void* h_out, const hero_history* history,
+                           const hero_ffn_weights* ffn, const hero_router_weights* router,
+                           const hero_adapter_weights* adapter, const float* eta,
+                           const hero_routing* routing, const hero_layer_stats* stats, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  Layout L;
+  int st = check_layer_call(dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, ffn, router, adapter, routing,
+                            stats, workspace, workspace_bytes, &L);
+  if (st != HERO_OK) return st;
+  if (dims->L_R > 64) return HERO_E_UNSUPPORTED;
+  if ((st = check_history(history)) != HERO_OK) return st;
+  if (!eta) return HERO_E_NULL;
+  for (int l = 0; l < j; ++l)
+    if (!(eta[l] == eta[l])) return HERO_E_RANGE;
+  if ((st = check_device()) != HERO_OK) return st;
+  float hw[64];
+  history_weights(eta, j, hw);
+  LayerCall c{dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, nullptr, ffn, router, adapter, eta[j - 1],
+              routing, stats, static_cast<unsigned char*>(workspace), &L,
+              static_cast<hipStream_t>(stream), history, hw};
+  return run_layer(c);
+}
+
+namespace {
+
+// hero_routed_stack and hero_routed_stack_hist: exactly one of state / history is set.
+int routed_stack(const hero_dims* dims, int T, const void* h_in, void* h_out, const hero_state* state,
+                 const hero_history* history, const hero_ffn_weights* ffn, const hero_router_weights* router,
+                 const hero_adapter_weights* adapter, const float* eta, const hero_routing* routing,
+                 const hero_layer_stats* stats, void* workspace, size_t workspace_bytes, void* stream) {
   int st = check_dims(dims);
   if (st != HERO_OK) return st;
   if (T <= 0) return HERO_E_DIM;
   if (!h_in || !h_out || !ffn || !adapter || !eta) return HERO_E_NULL;
   if (!aligned16(h_in) || !aligned16(h_out)) return HERO_E_ALIGN;
-  if ((st = check_state(state)) != HERO_OK) return st;
+  if (history) {
+    if (dims->L_R > 64) return HERO_E_UNSUPPORTED;
+    if ((st = check_history(history)) != HERO_OK) return st;
+  } else if ((st = check_state(state)) != HERO_OK) {
+    return st;
+  }
   if ((st = check_routing(routing)) != HERO_OK) return st;
   for (int l = 0; l < dims->L_R; ++l) {
     if ((st = check_weights(&ffn[l], router, &adapter[l])) != HERO_OK) return st;
@@ -420,15 +497,63 @@ int hero_routed_stack(const hero_dims* dims, int T, const void* h_in, void* h_ou
   auto hbar_of = [&](int jj) -> const void* {  // post-attention state entering routed layer jj
     return jj == 1 ? h_in : ring[(jj - 2) % 3];
   };
+  float hw[64];
   for (int j = 1; j <= dims->L_R; ++j) {
     void* out = j == dims->L_R ? h_out : const_cast<void*>(ring[(j - 1) % 3]);
+    if (history) history_weights(eta, j, hw);
     LayerCall c{dims, j, T, hbar_of(j), j >= 2 ? hbar_of(j - 1) : nullptr,
                 j >= 3 ? hbar_of(j - 2) : nullptr, out, state, &ffn[j - 1], router,
                 &adapter[j - 1], eta[j - 1], routing, stats ? &stats[j - 1] : nullptr, ws, &L,
-                static_cast<hipStream_t>(stream)};
+                static_cast<hipStream_t>(stream), history, history ? hw : nullptr};
     if ((st = run_layer(c)) != HERO_OK) return st;
   }
   return HERO_OK;
+}
+
+}  // namespace
+
+int hero_routed_stack(const hero_dims* dims, int T, const void* h_in, void* h_out,
+                      const hero_state* state, const hero_ffn_weights* ffn,
+                      const hero_router_weights* router, const hero_adapter_weights* adapter,
+                      const float* eta, const hero_routing* routing, const hero_layer_stats* stats,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  return routed_stack(dims, T, h_in, h_out, state, nullptr, ffn, router, adapter, eta, routing, stats,
+                      workspace, workspace_bytes, stream);
+}
+
+int hero_routed_stack_hist(const hero_dims* dims, int T, const void* h_in, void* h_out,
+                           const hero_history* history, const hero_ffn_weights* ffn,
+                           const hero_router_weights* router, const hero_adapter_weights* adapter,
+                           const float* eta, const hero_routing* routing, const hero_layer_stats* stats,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  if (!history) return HERO_E_NULL;
+  return routed_stack(dims, T, h_in, h_out, nullptr, history, ffn, router, adapter, eta, routing, stats,
+                      workspace, workspace_bytes, stream);
+}
+
+int hero_history_state(const hero_dims* dims, int n, int T, const float* kv, const float* eta, float* S,
+                       float* zeta, void* stream) {
+  int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if (T <= 0) return HERO_E_DIM;
+  if (dims->L_R > 64) return HERO_E_UNSUPPORTED;
+  if (n < 0 || n > dims->L_R) return HERO_E_RANGE;
+  if (!kv || !S || !zeta || (n > 0 && !eta)) return HERO_E_NULL;
+  if (!aligned16(kv) || !aligned16(S) || !aligned16(zeta)) return HERO_E_ALIGN;
+  for (int l = 0; l < n; ++l)
+    if (!(eta[l] == eta[l])) return HERO_E_RANGE;
+  const size_t dm = static_cast<size_t>(dims->d_m), t = static_cast<size_t>(T);
+  const size_t kvb = t * dims->L_R * 2 * dm * 4;
+  if (overlap(S, t * dm * dm * 4, kv, kvb) || overlap(zeta, t * dm * 4, kv, kvb) ||
+      overlap(S, t * dm * dm * 4, zeta, t * dm * 4))
+    return HERO_E_ALIAS;
+  if ((st = check_device()) != HERO_OK) return st;
+  hero::HistWeights w{};
+  history_weights(eta, n + 1, w.w);   // the weights of a read at layer n + 1
+  return hero::launch_history_state(dims->d_m, dims->L_R, n, T, kv, w, S, zeta,
+                                    static_cast<hipStream_t>(stream)) == hipSuccess
+             ? HERO_OK
+             : HERO_E_LAUNCH;
 }
 
 }  // extern "C"

@@ -41,6 +41,10 @@ struct RouterTailArgs {
   float* hs;              // [T][d_head]  th1[:, :d_s] s
   float* cvec;            // [T][d_m]     memory read c
   float* bvec;            // [T]          local-head logit b
+  // depth-history form of the memory (router_mem_hist): kv [T][L_R][2][d_m], and the weights
+  // w_{j,i} of the j-1 stored pairs (hw[i] for entry i, i.e. routed layer i+1)
+  float* kv;
+  float hw[64];
 };
 size_t router_scratch_floats(int d_m, int d_head, int T);
 // router state, q/k/v, W_n s, the s part of the history head, local head
@@ -49,6 +53,14 @@ hipError_t launch_router_pre(const RouterTailArgs& a, hipStream_t s);
 hipError_t launch_router_mem(const RouterTailArgs& a, hipStream_t s);
 // nu, history head, p, m, logit and gate
 hipError_t launch_router_post(const RouterTailArgs& a, hipStream_t s);
+// memory read as attention over the stored pairs, then the layer's own pair appended
+hipError_t launch_router_mem_hist(const RouterTailArgs& a, hipStream_t s);
+// matrix-form state S, zeta after n layers from a history (weights w[i] for entry i)
+struct HistWeights {
+  float w[64];
+};
+hipError_t launch_history_state(int d_m, int L_R, int n, int T, const float* kv, const HistWeights& w,
+                                float* S, float* zeta, hipStream_t s);
 
 // Branch decision and ordered compaction (one workgroup).
 struct SelectArgs {

@@ -792,6 +792,101 @@ __global__ __launch_bounds__(NT) void router_post_mfma(RouterTailArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// router_mem_hist: the memory read in depth-history form, one wave per token.
+//   a_i = w_i phi(q) . phi(k_i),  c = sum_i a_i v_i / (sum_i a_i + eps)  over the stored
+//   pairs i < j-1 (oldest first), then the layer's own (phi(k), v) stored as entry j-1.
+// Each lane owns EPL consecutive elements of the d_m-vectors; the pairs are read in
+// batches of HB with all of a batch's loads issued first.
+// ---------------------------------------------------------------------------
+template <int DM>
+__global__ __launch_bounds__(NT) void router_mem_hist_kernel(RouterTailArgs a) {
+  constexpr int EPL = DM >= kWave ? DM / kWave : 1;   // elements per lane
+  constexpr int LANES = DM >= kWave ? kWave : DM;     // lanes holding elements
+  constexpr int HB = 8;
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * (NT / kWave) + (threadIdx.x >> 6);
+  if (t >= a.T) return;
+  const int n = a.j - 1;
+  const bool on = lane < LANES;
+  const int e0 = lane * EPL;
+  const float* q = a.qkvn + static_cast<size_t>(t) * 4 * DM;
+  float fq[EPL], fk[EPL], vv[EPL];
+#pragma unroll
+  for (int x = 0; x < EPL; ++x) {
+    fq[x] = on ? q[e0 + x] : 0.f;
+    fk[x] = on ? q[DM + e0 + x] : 0.f;
+    vv[x] = on ? q[2 * DM + e0 + x] : 0.f;
+  }
+  float* H = a.kv + static_cast<size_t>(t) * a.L_R * 2 * DM;
+  float c[EPL];
+#pragma unroll
+  for (int x = 0; x < EPL; ++x) c[x] = 0.f;
+  float den = 0.f;
+  for (int i0 = 0; i0 < n; i0 += HB) {
+    float kk[HB][EPL], vh[HB][EPL];
+#pragma unroll
+    for (int u = 0; u < HB; ++u) {
+      const int i = i0 + u;
+      const float* hk = H + static_cast<size_t>(min(i, n - 1)) * 2 * DM + e0;
+#pragma unroll
+      for (int x = 0; x < EPL; ++x) {
+        kk[u][x] = on ? hk[x] : 0.f;
+        vh[u][x] = on ? hk[DM + x] : 0.f;
+      }
+    }
+    float dots[HB];
+#pragma unroll
+    for (int u = 0; u < HB; ++u) {
+      float s = 0.f;
+#pragma unroll
+      for (int x = 0; x < EPL; ++x) s = fmaf(fq[x], kk[u][x], s);
+      dots[u] = wave_sum(s);
+    }
+#pragma unroll
+    for (int u = 0; u < HB; ++u) {
+      if (i0 + u < n) {
+        const float al = a.hw[i0 + u] * dots[u];
+        den += al;
+#pragma unroll
+        for (int x = 0; x < EPL; ++x) c[x] = fmaf(al, vh[u][x], c[x]);
+      }
+    }
+  }
+  if (on) {
+    float* cv = a.cvec + static_cast<size_t>(t) * DM + e0;
+    float* hn = H + static_cast<size_t>(n) * 2 * DM + e0;
+#pragma unroll
+    for (int x = 0; x < EPL; ++x) {
+      cv[x] = n > 0 ? c[x] / (den + a.eps) : 0.f;
+      hn[x] = fk[x];
+      hn[DM + x] = vv[x];
+    }
+  }
+}
+
+// S[t][k][v] = sum_{i<n} w_i phi(k_i)[k] v_i[v], zeta[t][k] = sum_{i<n} w_i phi(k_i)[k];
+// one workgroup per token, oldest pair first.
+template <int DM>
+__global__ __launch_bounds__(NT) void history_state_kernel(const float* __restrict__ kv, int L_R, int n,
+                                                           HistWeights hw, float* __restrict__ S,
+                                                           float* __restrict__ zeta) {
+  const int t = blockIdx.x;
+  const float* H = kv + static_cast<size_t>(t) * L_R * 2 * DM;
+  float* St = S + static_cast<size_t>(t) * DM * DM;
+  for (int e = threadIdx.x; e < DM * DM; e += NT) {
+    const int k = e / DM, v = e % DM;
+    float acc = 0.f;
+    for (int i = 0; i < n; ++i) acc = fmaf(hw.w[i] * H[i * 2 * DM + k], H[i * 2 * DM + DM + v], acc);
+    St[e] = acc;
+  }
+  for (int k = threadIdx.x; k < DM; k += NT) {
+    float z = 0.f;
+    for (int i = 0; i < n; ++i) z = fmaf(hw.w[i], H[i * 2 * DM + k], z);
+    zeta[static_cast<size_t>(t) * DM + k] = z;
+  }
+}
+
 #undef LDS16
 
 hipError_t launch_pre_post(const RouterTailArgs& a, bool post, hipStream_t s) {
@@ -831,6 +926,35 @@ hipError_t launch_router_mem(const RouterTailArgs& a, hipStream_t s) {
     case 64: router_mem_kernel<64><<<grid, block, 0, s>>>(a); break;
     case 128: router_mem_kernel<128><<<grid, block, 0, s>>>(a); break;
     case 256: router_mem_kernel<256><<<grid, block, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_router_mem_hist(const RouterTailArgs& a, hipStream_t s) {
+  if (a.T <= 0) return hipSuccess;
+  if (a.j < 1 || a.j > a.L_R || a.L_R > 64) return hipErrorInvalidValue;
+  dim3 grid((a.T + NT / kWave - 1) / (NT / kWave)), block(NT);
+  switch (a.d_m) {
+    case 32: router_mem_hist_kernel<32><<<grid, block, 0, s>>>(a); break;
+    case 64: router_mem_hist_kernel<64><<<grid, block, 0, s>>>(a); break;
+    case 128: router_mem_hist_kernel<128><<<grid, block, 0, s>>>(a); break;
+    case 256: router_mem_hist_kernel<256><<<grid, block, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_history_state(int d_m, int L_R, int n, int T, const float* kv, const HistWeights& w,
+                                float* S, float* zeta, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  if (n < 0 || n > L_R || L_R > 64) return hipErrorInvalidValue;
+  dim3 grid(T), block(NT);
+  switch (d_m) {
+    case 32: history_state_kernel<32><<<grid, block, 0, s>>>(kv, L_R, n, w, S, zeta); break;
+    case 64: history_state_kernel<64><<<grid, block, 0, s>>>(kv, L_R, n, w, S, zeta); break;
+    case 128: history_state_kernel<128><<<grid, block, 0, s>>>(kv, L_R, n, w, S, zeta); break;
+    case 256: history_state_kernel<256><<<grid, block, 0, s>>>(kv, L_R, n, w, S, zeta); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

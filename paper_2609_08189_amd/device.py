@@ -73,7 +73,7 @@ class DeviceProblem:
     """A synth.Problem resident on the GPU with the ABI structs that point at it."""
 
     def __init__(self, prob: synth.Problem, device: str = "cuda:0", stats: bool = True,
-                 for_stack: Optional[bool] = None):
+                 for_stack: Optional[bool] = None, history: bool = False):
         w = prob.w
         self.w = w
         self.device = device
@@ -99,6 +99,17 @@ class DeviceProblem:
         self.m_hist = torch.from_numpy(prob.m_hist).to(device)
         self.state_s = H.hero_state(self.S.data_ptr(), self.zeta.data_ptr(), self.p_hist.data_ptr(),
                                     self.m_hist.data_ptr())
+        # depth-history form of the memory: the pairs of the earlier layers instead of S, zeta
+        self.history = history
+        self.n_entries = 0
+        if history:
+            self.kv = torch.full((T, w.L_R, 2, w.d_m), float("nan"), dtype=torch.float32, device=device)
+            if prob.mem_k is not None:
+                n = prob.mem_k.shape[1]
+                self.kv[:, :n, 0] = torch.from_numpy(prob.mem_k).to(device)
+                self.kv[:, :n, 1] = torch.from_numpy(prob.mem_v).to(device)
+                self.n_entries = n
+            self.hist_s = H.hero_history(self.kv.data_ptr(), self.p_hist.data_ptr(), self.m_hist.data_ptr())
         self.beta = torch.from_numpy(prob.beta).to(device) if prob.beta is not None else None
         mode = H.HERO_MODE_BUDGET if w.mode == "budget" else H.HERO_MODE_THRESHOLD
         self.routing_s = H.hero_routing(mode, w.tau, w.budget,
@@ -114,28 +125,52 @@ class DeviceProblem:
         return torch.cuda.current_stream(torch.device(self.device)).cuda_stream
 
     def run_layer(self, j: int, layer: int = 0, check: bool = True) -> int:
-        st = H.hero_routed_layer(self.dims, j, self.T, self.hbar, self.prev1, self.prev2, self.h_out,
-                                 self.state_s, self.ffn_s[layer], self.router_s, self.adapter_s[layer],
-                                 self.eta[j - 1], self.routing_s,
-                                 self.stats[0].struct if self.stats else None,
-                                 self.ws, self.ws_bytes, self.stream())
+        stats = self.stats[0].struct if self.stats else None
+        if self.history:
+            st = H.hero_routed_layer_hist(self.dims, j, self.T, self.hbar, self.prev1, self.prev2, self.h_out,
+                                          self.hist_s, self.ffn_s[layer], self.router_s, self.adapter_s[layer],
+                                          self.eta[:j], self.routing_s, stats, self.ws, self.ws_bytes,
+                                          self.stream())
+            self.n_entries = j
+        else:
+            st = H.hero_routed_layer(self.dims, j, self.T, self.hbar, self.prev1, self.prev2, self.h_out,
+                                     self.state_s, self.ffn_s[layer], self.router_s, self.adapter_s[layer],
+                                     self.eta[j - 1], self.routing_s, stats, self.ws, self.ws_bytes,
+                                     self.stream())
         if check:
-            H.check(st, "hero_routed_layer")
+            H.check(st, "hero_routed_layer_hist" if self.history else "hero_routed_layer")
         return st
 
     def run_stack(self, check: bool = True) -> int:
-        st = H.hero_routed_stack(self.dims, self.T, self.hbar, self.h_out, self.state_s, self.ffn_s,
-                                 self.router_s, self.adapter_s, self.eta, self.routing_s,
-                                 [s.struct for s in self.stats] if self.stats else None,
-                                 self.ws, self.ws_bytes, self.stream())
+        stats = [s.struct for s in self.stats] if self.stats else None
+        if self.history:
+            st = H.hero_routed_stack_hist(self.dims, self.T, self.hbar, self.h_out, self.hist_s, self.ffn_s,
+                                          self.router_s, self.adapter_s, self.eta, self.routing_s, stats,
+                                          self.ws, self.ws_bytes, self.stream())
+            self.n_entries = self.w.L_R
+        else:
+            st = H.hero_routed_stack(self.dims, self.T, self.hbar, self.h_out, self.state_s, self.ffn_s,
+                                     self.router_s, self.adapter_s, self.eta, self.routing_s, stats,
+                                     self.ws, self.ws_bytes, self.stream())
         if check:
-            H.check(st, "hero_routed_stack")
+            H.check(st, "hero_routed_stack_hist" if self.history else "hero_routed_stack")
         return st
+
+    def history_state(self, n: int, kv=None):
+        """Matrix-form S, zeta after n layers from (a row subset of) the history, on the device."""
+        kv = self.kv if kv is None else kv
+        T = kv.shape[0]
+        S = torch.empty((T, self.w.d_m, self.w.d_m), dtype=torch.float32, device=self.device)
+        zeta = torch.empty((T, self.w.d_m), dtype=torch.float32, device=self.device)
+        H.check(H.hero_history_state(self.dims, n, T, kv, self.eta[:n], S, zeta, self.stream()),
+                "hero_history_state")
+        return S, zeta
 
     def results(self) -> Dict[str, object]:
         torch.cuda.synchronize()
-        out = dict(h=download_f64(self.h_out), S=self.S.cpu().numpy().astype(np.float64),
-                   zeta=self.zeta.cpu().numpy().astype(np.float64),
+        S, zeta = self.history_state(self.n_entries) if self.history else (self.S, self.zeta)
+        out = dict(h=download_f64(self.h_out), S=S.cpu().numpy().astype(np.float64),
+                   zeta=zeta.cpu().numpy().astype(np.float64),
                    p_hist=self.p_hist.cpu().numpy().astype(np.float64),
                    m_hist=self.m_hist.cpu().numpy().astype(np.float64))
         if self.stats:
@@ -160,13 +195,22 @@ class DeviceProblem:
         io = []
         for j in range(1, self.w.L_R + 1):
             out = self.h_out if j == self.w.L_R else torch.empty_like(self.hbar)
-            H.check(H.hero_routed_layer(self.dims, j, T, hs[-1], hs[-2] if j >= 2 else None,
-                                        hs[-3] if j >= 3 else None, out, self.state_s, self.ffn_s[j - 1],
-                                        self.router_s, self.adapter_s[j - 1], self.eta[j - 1],
-                                        self.routing_s, stats.struct, ws, ws_bytes, self.stream()),
-                    "hero_routed_layer")
+            args = (hs[-1], hs[-2] if j >= 2 else None, hs[-3] if j >= 3 else None, out)
+            if self.history:
+                H.check(H.hero_routed_layer_hist(self.dims, j, T, *args, self.hist_s, self.ffn_s[j - 1],
+                                                 self.router_s, self.adapter_s[j - 1], self.eta[:j],
+                                                 self.routing_s, stats.struct, ws, ws_bytes, self.stream()),
+                        "hero_routed_layer_hist")
+                self.n_entries = j
+                S_sel, z_sel = self.history_state(j, kv=pick(self.kv).contiguous())
+            else:
+                H.check(H.hero_routed_layer(self.dims, j, T, *args, self.state_s, self.ffn_s[j - 1],
+                                            self.router_s, self.adapter_s[j - 1], self.eta[j - 1],
+                                            self.routing_s, stats.struct, ws, ws_bytes, self.stream()),
+                        "hero_routed_layer")
+                S_sel, z_sel = pick(self.S), pick(self.zeta)
             torch.cuda.synchronize()
-            after = (pick(self.S).cpu().numpy().astype(np.float64), pick(self.zeta).cpu().numpy().astype(np.float64),
+            after = (S_sel.cpu().numpy().astype(np.float64), z_sel.cpu().numpy().astype(np.float64),
                      pick(self.p_hist).cpu().numpy().astype(np.float64),
                      pick(self.m_hist).cpu().numpy().astype(np.float64))
             io.append(dict(hbar=download_f64(pick(hs[-1])), S=prev_state[0], zeta=prev_state[1],

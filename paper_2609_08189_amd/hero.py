@@ -67,6 +67,10 @@ class hero_state(ctypes.Structure):
     _fields_ = [("S", _vp), ("zeta", _vp), ("p_hist", _vp), ("m_hist", _vp)]
 
 
+class hero_history(ctypes.Structure):
+    _fields_ = [("kv", _vp), ("p_hist", _vp), ("m_hist", _vp)]
+
+
 class hero_routing(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int), ("tau", ctypes.c_float), ("budget", ctypes.c_double),
                 ("logit_bias", _vp)]
@@ -106,6 +110,19 @@ def lib() -> ctypes.CDLL:
                                         P(hero_ffn_weights), P(hero_router_weights),
                                         P(hero_adapter_weights), P(ctypes.c_float), P(hero_routing),
                                         P(hero_layer_stats), _vp, ctypes.c_size_t, _vp]
+        L.hero_routed_layer_hist.restype = ctypes.c_int
+        L.hero_routed_layer_hist.argtypes = [P(hero_dims), ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp,
+                                             P(hero_history), P(hero_ffn_weights), P(hero_router_weights),
+                                             P(hero_adapter_weights), P(ctypes.c_float), P(hero_routing),
+                                             P(hero_layer_stats), _vp, ctypes.c_size_t, _vp]
+        L.hero_routed_stack_hist.restype = ctypes.c_int
+        L.hero_routed_stack_hist.argtypes = [P(hero_dims), ctypes.c_int, _vp, _vp, P(hero_history),
+                                             P(hero_ffn_weights), P(hero_router_weights),
+                                             P(hero_adapter_weights), P(ctypes.c_float), P(hero_routing),
+                                             P(hero_layer_stats), _vp, ctypes.c_size_t, _vp]
+        L.hero_history_state.restype = ctypes.c_int
+        L.hero_history_state.argtypes = [P(hero_dims), ctypes.c_int, ctypes.c_int, _vp, P(ctypes.c_float),
+                                         _vp, _vp, _vp]
         _lib = L
     return _lib
 
@@ -183,3 +200,40 @@ def hero_routed_stack(dims: hero_dims, T: int, h_in, h_out, state: hero_state,
     return lib().hero_routed_stack(ctypes.byref(dims), T, ptr(h_in), ptr(h_out), _byref(state), ffn_arr,
                                    _byref(router), ad_arr, eta_arr, _byref(routing), st_arr,
                                    ptr(workspace), int(workspace_bytes), stream)
+
+
+def _floats(xs):
+    xs = [float(x) for x in xs]
+    return (ctypes.c_float * max(len(xs), 1))(*xs)
+
+
+def hero_routed_layer_hist(dims: hero_dims, j: int, T: int, hbar, hbar_prev1, hbar_prev2, h_out,
+                           history: hero_history, ffn: hero_ffn_weights, router: hero_router_weights,
+                           adapter: hero_adapter_weights, eta: Sequence[float], routing: hero_routing,
+                           stats: Optional[hero_layer_stats], workspace, workspace_bytes: int,
+                           stream=None) -> int:
+    """One routed layer with the memory in depth-history form; eta holds eta_1 .. eta_j."""
+    return lib().hero_routed_layer_hist(ctypes.byref(dims), j, T, ptr(hbar), ptr(hbar_prev1), ptr(hbar_prev2),
+                                        ptr(h_out), _byref(history), _byref(ffn), _byref(router),
+                                        _byref(adapter), _floats(eta), _byref(routing), _byref(stats),
+                                        ptr(workspace), int(workspace_bytes), stream)
+
+
+def hero_routed_stack_hist(dims: hero_dims, T: int, h_in, h_out, history: hero_history,
+                           ffn: Sequence[hero_ffn_weights], router: hero_router_weights,
+                           adapter: Sequence[hero_adapter_weights], eta: Sequence[float],
+                           routing: hero_routing, stats: Optional[Sequence[hero_layer_stats]],
+                           workspace, workspace_bytes: int, stream=None) -> int:
+    """The routed stack with the memory in depth-history form."""
+    L = len(ffn)
+    ffn_arr = (hero_ffn_weights * L)(*ffn)
+    ad_arr = (hero_adapter_weights * L)(*adapter)
+    st_arr = None if stats is None else (hero_layer_stats * L)(*stats)
+    return lib().hero_routed_stack_hist(ctypes.byref(dims), T, ptr(h_in), ptr(h_out), _byref(history), ffn_arr,
+                                        _byref(router), ad_arr, _floats(eta), _byref(routing), st_arr,
+                                        ptr(workspace), int(workspace_bytes), stream)
+
+
+def hero_history_state(dims: hero_dims, n: int, T: int, kv, eta: Sequence[float], S, zeta, stream=None) -> int:
+    """Matrix-form state after n layers from a history (eta: eta_1 .. eta_n)."""
+    return lib().hero_history_state(ctypes.byref(dims), n, T, ptr(kv), _floats(eta), ptr(S), ptr(zeta), stream)

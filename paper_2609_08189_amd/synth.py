@@ -282,11 +282,23 @@ def incoming_history(w: Workload, hbar: Tensor, seed: int = 0):
     return prev1, prev2
 
 
+def incoming_memory_pairs(w: Workload, j: int, T: int, seed: int = 0):
+    """The key/value pairs of the j-1 routed layers before layer j behind a synthesized state:
+    log-normal (strictly positive) a_i in the role of phi(k_i) and Gaussian b_i in the role of
+    v_i, each [T, j-1, d_m] float32 (None, None for j == 1)."""
+    if j <= 1:
+        return None, None
+    n, dm = j - 1, w.d_m
+    a = np.exp(np.float32(0.5) * _rng(seed, "state_a").standard_normal((T, n, dm), dtype=np.float32))
+    b = _rng(seed, "state_b").standard_normal((T, n, dm), dtype=np.float32)
+    return a, b
+
+
 def incoming_state(w: Workload, j: int, T: int, seed: int = 0, decay: float = 0.98):
     """A plausible router state as it stands before routed layer j (fp32 storage).
 
-    S = sum_{i<j} decay^(j-1-i) a_i b_i^T and zeta = sum_{i<j} decay^(j-1-i) a_i with
-    log-normal (strictly positive) a_i and Gaussian b_i; p ~ U(0.2, 0.8), m ~ U(0, p).
+    S = sum_{i<j} decay^(j-1-i) a_i b_i^T and zeta = sum_{i<j} decay^(j-1-i) a_i over the pairs
+    of incoming_memory_pairs; p ~ U(0.2, 0.8), m ~ U(0, p).
     For j == 1 the state is the all-zero matrix/normaliser with p = m = 1.
     """
     dm = w.d_m
@@ -294,12 +306,8 @@ def incoming_state(w: Workload, j: int, T: int, seed: int = 0, decay: float = 0.
     zeta = np.zeros((T, dm), dtype=np.float32)
     if j <= 1:
         return S, zeta, np.ones(T, np.float32), np.ones(T, np.float32)
-    ga = _rng(seed, "state_a")
-    gb = _rng(seed, "state_b")
-    n = j - 1
+    a, b = incoming_memory_pairs(w, j, T, seed)
     wgt = np.array([decay ** (j - 1 - i) for i in range(1, j)], dtype=np.float32)
-    a = np.exp(np.float32(0.5) * ga.standard_normal((T, n, dm), dtype=np.float32))
-    b = gb.standard_normal((T, n, dm), dtype=np.float32)
     aw = a * wgt[None, :, None]
     S = np.matmul(aw.transpose(0, 2, 1), b)          # [T, dm, dm] = sum_i w_i a_i b_i^T
     zeta = aw.sum(axis=1)
@@ -373,6 +381,10 @@ class Problem:
     adapter: "LazyLayers"
     eta: np.ndarray                   # [L_R] f32 (a layer call uses eta[j-1])
     beta: Optional[np.ndarray]        # [T] f32 or None
+    # a layer call at j > 1: the pairs of layers 1..j-1 ([T, j-1, d_m] f32), for the depth-history
+    # form of the memory; S and zeta above are their decayed sums with decay 0.98
+    mem_k: Optional[np.ndarray] = None
+    mem_v: Optional[np.ndarray] = None
 
 
 def make_problem(w: Workload, seed: int = 0, T: Optional[int] = None,
@@ -389,12 +401,14 @@ def make_problem(w: Workload, seed: int = 0, T: Optional[int] = None,
             if j == 2:
                 prev2 = None
         S, zeta, p, m = incoming_state(w, j, T, seed)
+        mem_k, mem_v = incoming_memory_pairs(w, j, T, seed)
         layers = [j - 1]
     else:
         S = np.zeros((T, w.d_m, w.d_m), np.float32)
         zeta = np.zeros((T, w.d_m), np.float32)
         p = np.ones(T, np.float32)
         m = np.ones(T, np.float32)
+        mem_k = mem_v = None
         layers = list(range(w.L_R))
     return Problem(
         w=w, hbar=hb, hbar_prev1=prev1, hbar_prev2=prev2,
@@ -404,4 +418,5 @@ def make_problem(w: Workload, seed: int = 0, T: Optional[int] = None,
         adapter=LazyLayers(lambda l: adapter_layer(w, l, seed), layers, keep=4),
         eta=eta_values(w),
         beta=logit_bias(w, seed, T),
+        mem_k=mem_k, mem_v=mem_v,
     )

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_function():
     lib = H.lib()
     for n in names:
         assert hasattr(lib, n), f"{n} declared in include/hero.h but not exported"
-    assert H.hero_abi_version() == 1
+    assert H.hero_abi_version() == 2
 
 
 def test_status_strings():
@@ -196,3 +196,28 @@ def test_no_device_means_device_error():
     if torch.cuda.device_count() > 0:
         pytest.skip("a GPU is visible; this test covers hosts without one")
     assert call_layer() == H.HERO_E_DEVICE
+
+
+def test_history_entry_points_validate():
+    dims = good_dims()
+    ffn, ad, rt, st = fake_structs()
+    hist = H.hero_history(FAKE + (5 << 30), FAKE + (6 << 30), FAKE + (7 << 30))
+    rc = H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.27, None)
+    need = H.hero_workspace_size(dims, 100, False)
+
+    def layer(j=3, eta=(3.9, 3.9, 3.9), hs=hist, d=dims, ws=FAKE + (8 << 30)):
+        return H.hero_routed_layer_hist(d, j, 100, FAKE + (1 << 30), FAKE + (2 << 30), FAKE + (3 << 30),
+                                        FAKE + (4 << 30), hs, ffn[0], rt, ad[0], eta, rc, None, ws, need, None)
+
+    assert layer(hs=None) == H.HERO_E_NULL
+    assert layer(hs=H.hero_history(FAKE + (5 << 30), None, FAKE)) == H.HERO_E_NULL
+    assert layer(hs=H.hero_history(FAKE + 4, FAKE, FAKE)) == H.HERO_E_ALIGN
+    assert layer(eta=(3.9, float("nan"), 3.9)) == H.HERO_E_RANGE
+    assert layer(d=good_dims(L_R=65), j=3) == H.HERO_E_UNSUPPORTED
+    assert layer(ws=None) == H.HERO_E_WORKSPACE
+    S, z = FAKE + (9 << 30), FAKE + (10 << 30)
+    kv = FAKE + (5 << 30)
+    assert H.hero_history_state(dims, 9, 10, kv, [3.9] * 9, S, z) == H.HERO_E_RANGE      # n > L_R
+    assert H.hero_history_state(dims, 2, 10, kv, [3.9] * 2, kv, z) == H.HERO_E_ALIAS     # S overlaps kv
+    assert H.hero_history_state(dims, 2, 0, kv, [3.9] * 2, S, z) == H.HERO_E_DIM
+    assert H.hero_history_state(dims, 2, 10, None, [3.9] * 2, S, z) == H.HERO_E_NULL

@@ -149,6 +149,29 @@ def _brute_phi(x):
     return (F.elu(_t(x)) + 1.0).numpy()
 
 
+@pytest.mark.parametrize("L_R", [1, 2, 5])
+def test_memory_from_pairs_equals_the_recurrence(L_R):
+    """The depth-history state (the pairs of layers 1..n, weighted by decay products) equals
+    the stack's memory after n layers of the recurrence, for every n."""
+    w = SMALL.replace(L_R=L_R, T=4)
+    prob = _problem(w, router_std=0.3)
+    etas = np.linspace(-1.5, 2.5, L_R)
+    res = _stack(prob, w, etas=etas)
+    rhos = O.sigmoid(etas)
+    phik = np.stack([_brute_phi(L.debug["k"]) for L in res.layers], axis=1)
+    v = np.stack([L.debug["v"] for L in res.layers], axis=1)
+    S, zeta = O.memory_from_pairs(phik, v, rhos)
+    np.testing.assert_allclose(S, res.state.S, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(zeta, res.state.zeta, rtol=1e-12, atol=1e-14)
+    # and for a prefix of n < L_R layers, against the state the next layer reads (its c)
+    for n in range(1, L_R):
+        Sn, zn = O.memory_from_pairs(phik[:, :n], v[:, :n], rhos[:n])
+        c = O.memory_read(res.layers[n].debug["q"], Sn, zn, w.eps)
+        np.testing.assert_allclose(c, res.layers[n].debug["c"], rtol=1e-10, atol=1e-12)
+    S0, z0 = O.memory_from_pairs(phik[:, :0], v[:, :0], rhos[:0])
+    assert not S0.any() and not z0.any()
+
+
 @pytest.mark.parametrize("L_R", [1, 2, 3, 4, 8])
 @pytest.mark.parametrize("rho_one", [False, True])
 def test_memory_equals_explicit_decayed_sum(L_R, rho_one):
