@@ -72,7 +72,8 @@ typedef enum hero_mode {
  * encoder's, d_head the history/local heads' hidden width (Sec. 4.1: 256); the
  * comparison space of W_n, W_c has width d_m.
  * Supported: d % 256 == 0 (bf16) or d % 128 == 0 (f32); bf16 also needs
- * d_ff % 128 == 0, d_r in {32, 64, 96, 128}, d_s % 8 == 0, d_e % 64 == 0 and
+ * d_ff % 128 == 0, d_r in {32, 64, 96, 128} or a multiple of 128 up to 8192
+ * (the paper's 896), d_s % 8 == 0, d_e % 64 == 0 and
  * (d_e + d_head) % 128 == 0; d_m in
  * {32, 64, 128, 256}; d_s <= 128; d_e, d_head <= 256; d_p <= 128.
  */

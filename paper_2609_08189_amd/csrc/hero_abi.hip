@@ -69,7 +69,11 @@ int check_dims(const hero_dims* d) {
   if (d->d_s > 128 || d->d_e > 256 || d->d_head > 256 || d->d_p > 128) return HERO_E_UNSUPPORTED;
   if (d->dtype == HERO_BF16) {
     if (d->d % 256 || d->d_ff % 128 || d->d_e % 64 || (d->d_e + d->d_head) % 128) return HERO_E_UNSUPPORTED;
-    if (d->d_r % 32 || d->d_r > 128 || d->d_s % 8) return HERO_E_UNSUPPORTED;
+    // adapter ranks: 32..128 in steps of 32 (register-tiled kernels) or wider in steps of 128
+    // (GEMM path, e.g. the paper's 896)
+    const bool small_r = d->d_r % 32 == 0 && d->d_r <= 128;
+    const bool wide_r = d->d_r % 128 == 0 && d->d_r > 128 && d->d_r <= 8192;
+    if (!(small_r || wide_r) || d->d_s % 8) return HERO_E_UNSUPPORTED;
   } else {
     if (d->d % 128) return HERO_E_UNSUPPORTED;
   }

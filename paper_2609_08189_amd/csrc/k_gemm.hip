@@ -19,6 +19,8 @@
 // f32 path: a plain LDS-tiled VALU GEMM with full bounds checks (small shapes).
 #include <limits.h>
 
+#include <algorithm>
+
 #include <type_traits>
 
 #include "hero_device.h"
@@ -741,15 +743,67 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
   return run_f32<false>(A, B, epi, counts, n_max, d, d_ff, s);
 }
 
+// Wide adapters (ranks above 128, in steps of 128: the paper's d_r = 896).  The down-projection
+// runs on the MFMA GEMM core with K split WIDE_SPLIT ways into fp32 partials, a reduction pass forms
+// hid = bf16(SiLU(sum of the partials)), and the up-projection is a GEMM whose epilogue scatters
+// hbar + (1 - g) (W_2 hid) into the adapter rows.
+constexpr int WIDE_SPLIT = 4;
+using TileWide = Tile<128, 128, 2, 4, false>;
+
+bool adapter_wide(int d_r) { return d_r > 128; }
+
 size_t adapter_part_floats(int dtype, int d, int d_r, int T) {
+  if (dtype == 1 && adapter_wide(d_r))   // partials, then hid (bf16, half a float per element)
+    return static_cast<size_t>(WIDE_SPLIT) * T * d_r + static_cast<size_t>(T) * d_r / 2;
   const int G = dtype == 1 ? adapter_groups(d) : 1;
   return static_cast<size_t>(G) * T * d_r;
 }
+
+namespace {
+
+// hid[m][n] = bf16(SiLU(sum_z part[z][m][n])) for m < *m_count, eight columns per thread
+__global__ __launch_bounds__(256) void adapter_hidden_wide(const float* __restrict__ part, size_t split_stride,
+                                                           const int* __restrict__ m_count, int d_r,
+                                                           bf16_t* __restrict__ hid) {
+  const size_t n8 = static_cast<size_t>(*m_count) * d_r / 8;
+  for (size_t e = blockIdx.x * static_cast<size_t>(256) + threadIdx.x; e < n8;
+       e += static_cast<size_t>(gridDim.x) * 256) {
+    f32x4 x[WIDE_SPLIT][2];
+#pragma unroll
+    for (int z = 0; z < WIDE_SPLIT; ++z) {
+      const float* p = part + z * split_stride + 8 * e;
+      x[z][0] = *reinterpret_cast<const f32x4*>(p);
+      x[z][1] = *reinterpret_cast<const f32x4*>(p + 4);
+    }
+    float h[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      float v = 0.f;
+#pragma unroll
+      for (int z = 0; z < WIDE_SPLIT; ++z) v += x[z][c >> 2][c & 3];
+      h[c] = siluf_(v);
+    }
+    st8(hid + 8 * e, h);
+  }
+}
+
+}  // namespace
 
 hipError_t launch_adapter_down(int dtype, const void* u, const int* idx_ad, const int* counts,
                                int n_max, const void* w1, float* part, int d, int d_r,
                                hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
+  if (dtype == 1 && adapter_wide(d_r)) {
+    ARows<bf16_t> A{static_cast<const bf16_t*>(u), idx_ad, d};
+    BRows<bf16_t> B{static_cast<const bf16_t*>(w1), nullptr, INT_MAX, d};
+    const size_t stride = static_cast<size_t>(n_max) * d_r;
+    hipError_t e = run_tile<TileWide>(A, B, EpiStoreF32{part, d_r, stride}, counts, n_max, d_r, d, s, WIDE_SPLIT);
+    if (e != hipSuccess) return e;
+    bf16_t* hid = reinterpret_cast<bf16_t*>(part + WIDE_SPLIT * stride);
+    const int blocks = static_cast<int>(std::min<size_t>((stride / 8 + 255) / 256, 2048));
+    adapter_hidden_wide<<<blocks, 256, 0, s>>>(part, stride, counts, d_r, hid);
+    return hipGetLastError();
+  }
   if (dtype == 1) {
     const int G = adapter_groups(d);
     dim3 g1((n_max + 31) / 32, G);
@@ -780,6 +834,14 @@ hipError_t launch_adapter_up(int dtype, const float* part, const int* idx_ad, co
                              int n_max, const void* w2, const void* hbar, const float* gate,
                              void* h_out, int d, int d_r, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
+  if (dtype == 1 && adapter_wide(d_r)) {
+    const bf16_t* hid =
+        reinterpret_cast<const bf16_t*>(part + static_cast<size_t>(WIDE_SPLIT) * n_max * d_r);
+    ARows<bf16_t> A{hid, nullptr, d_r};
+    BRows<bf16_t> B{static_cast<const bf16_t*>(w2), nullptr, INT_MAX, d_r};
+    EpiScatter<bf16_t, true> epi{idx_ad, static_cast<const bf16_t*>(hbar), gate, static_cast<bf16_t*>(h_out), d};
+    return run_tile<TileWide>(A, B, epi, counts, n_max, d, d_r, s);
+  }
   if (dtype == 1) {
     const int G = adapter_groups(d);
     dim3 g2((n_max + 31) / 32, d / 256);

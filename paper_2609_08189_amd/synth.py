@@ -92,6 +92,10 @@ WORKLOADS: Dict[str, Workload] = {
     # Llama-2-7B shape, 32-layer decode step, 256 sequences x 1 token
     "llama2_7b_decode": Workload("llama2_7b_decode", "bf16", 4096, 11008, 64, 32, 128,
                                  256, "budget", budget=0.27, batch=256, seq=1),
+    # the paper's operating point on the Llama-3.1-8B shape: adapter rank 896, memory dim 64
+    # (Sec. 4.1), one routed layer (j=17 of 32), 25 % skip, T=4096 prefill tokens
+    "llama31_8b_paper": Workload("llama31_8b_paper", "bf16", 4096, 14336, 896, 32, 64,
+                                 4096, "budget", budget=0.25, layer_j=17, batch=1, seq=4096),
     # Llama-2-13B shape, 40-layer prefill, 8 x 4096 tokens, bimodal position-clustered bias
     "llama2_13b_prefill": Workload("llama2_13b_prefill", "bf16", 5120, 13824, 64, 40, 128,
                                    32768, "threshold", tau=0.5, bias="bimodal_runs",

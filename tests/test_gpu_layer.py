@@ -88,3 +88,34 @@ def test_llama31_8b_layer_full_shape():
     assert res["layers"][0]["n_ad"] == 1101
     del dp
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("d_r,mode", [(256, "budget"), (896, "budget"), (896, "threshold")])
+def test_wide_adapter(d_r, mode):
+    """Adapter ranks above 128 (the paper's 896) on the GEMM path, with ragged token counts."""
+    w = BF16_SMALL.replace(d_r=d_r, mode=mode, T=613, bias="bimodal_runs" if mode == "threshold" else "none")
+    _run(w, 3)
+
+
+def test_llama31_8b_paper_operating_point_full_shape():
+    """Llama-3.1-8B shape at the paper's operating point: adapter rank 896, memory dim 64, j = 17,
+    T = 4096, 25 % skip; branch outputs on 48 FFN and 48 adapter rows, the rest for every token."""
+    import torch
+    from paper_2609_08189_amd.device import DeviceProblem
+    w = synth.WORKLOADS["llama31_8b_paper"]
+    print(f"case {w.name} T={w.T} j={w.layer_j} d_r={w.d_r} d_m={w.d_m}", flush=True)
+    prob = synth.make_problem(w, seed=0)
+    dp = DeviceProblem(prob)
+    dp.run_layer(w.layer_j)
+    res = dp.results()
+    mask = res["layers"][0]["mask"]
+    rng = np.random.default_rng(1)
+    rows = np.zeros(w.T, bool)
+    rows[rng.choice(np.nonzero(mask)[0], 48, replace=False)] = True
+    rows[rng.choice(np.nonzero(~mask)[0], 48, replace=False)] = True
+    report = {}
+    check_layer(prob, res, w.layer_j, rows=rows, report=report)
+    print("  errors:", report, flush=True)
+    assert res["layers"][0]["n_ad"] == 1024
+    del dp
+    torch.cuda.empty_cache()
