@@ -10,7 +10,8 @@
 // 16-wave scan its rank within a 1024-token chunk, and a running count across
 // chunks keeps both index lists in ascending token order.
 // One workgroup of 1024 threads does the whole layer: the work is ~10 bytes per
-// token and the cost is a few microseconds of latency.
+// token and the cost is latency, so each thread keeps its tokens' logits in registers
+// (up to 32 chunks of 1024 tokens) for the six passes instead of reading them again.
 #include "hero_device.h"
 #include "hero_kernels.h"
 
@@ -31,6 +32,40 @@ __device__ __forceinline__ int lane_prefix(unsigned long long bal, int lane) {
   return __popcll(bal & ((1ull << lane) - 1ull));
 }
 
+// R > 0: token t = tid + NT r (r < R) keeps its logit in a register for all passes (T <= NT R);
+// R == 0: every pass reads the logits again (any T).
+template <int R>
+struct Logits {
+  float v[R > 0 ? R : 1];
+  __device__ __forceinline__ void load(const float* lg, int T) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int t = static_cast<int>(threadIdx.x) + NT * r;
+      v[r] = t < T ? lg[t] : 0.f;
+    }
+  }
+  __device__ __forceinline__ float at(const float* lg, int r, int t) const {
+    if constexpr (R > 0) {
+      return v[r];
+    } else {
+      return lg[t];
+    }
+  }
+};
+
+// for (r = 0; NT r < T; ++r) f(r, t = tid + NT r), unrolled when the chunk count is static
+template <int R, class F>
+__device__ __forceinline__ void for_chunks(int T, F&& f) {
+  if constexpr (R > 0) {
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (NT * r < T) f(r, static_cast<int>(threadIdx.x) + NT * r);
+  } else {
+    for (int r = 0; NT * r < T; ++r) f(r, static_cast<int>(threadIdx.x) + NT * r);
+  }
+}
+
+template <int R>
 __global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
   __shared__ uint32_t hist[256];
   __shared__ int wcount[NW];
@@ -42,6 +77,8 @@ __global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = a.T;
   const bool budget = a.mode == 1;
+  Logits<R> lg;
+  lg.load(a.logit, T);
 
   // adapter iff key < vstar, or key == vstar and t <= tstar
   uint32_t vstar = 0u;
@@ -55,11 +92,13 @@ __global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
       for (int i = tid; i < 256; i += NT) hist[i] = 0u;
       __syncthreads();
       const uint32_t prefix = s_prefix;
-      for (int t = tid; t < T; t += NT) {
-        const uint32_t key = okey(a.logit[t]);
-        if (shift == 24 || (key >> (shift + 8)) == (prefix >> (shift + 8)))
-          atomicAdd(&hist[(key >> shift) & 255u], 1u);
-      }
+      for_chunks<R>(T, [&](int r, int t) {
+        if (t < T) {
+          const uint32_t key = okey(lg.at(a.logit, r, t));
+          if (shift == 24 || (key >> (shift + 8)) == (prefix >> (shift + 8)))
+            atomicAdd(&hist[(key >> shift) & 255u], 1u);
+        }
+      });
       __syncthreads();
       if (wave == 0) {
         // lane l owns bins [4l, 4l+4); inclusive scan of their sums across the wave
@@ -96,9 +135,9 @@ __global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
     const int k = s_k;
     if (tid == 0) s_tstar = -1;
     int run = 0;
-    for (int base = 0; base < T; base += NT) {
-      const int t = base + tid;
-      const bool pred = t < T && okey(a.logit[t]) == vstar;
+    for_chunks<R>(T, [&](int r, int t) {
+      if (run >= k) return;   // uniform: every thread holds the same run
+      const bool pred = t < T && okey(lg.at(a.logit, r, t)) == vstar;
       const unsigned long long bal = __ballot(pred);
       if (lane == 0) wcount[wave] = __popcll(bal);
       __syncthreads();
@@ -111,8 +150,7 @@ __global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
       if (pred && run + wpre + lane_prefix(bal, lane) + 1 == k) s_tstar = t;
       run += tot;
       __syncthreads();
-      if (run >= k) break;
-    }
+    });
     __syncthreads();
     tstar = s_tstar;
   }
@@ -120,13 +158,11 @@ __global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
   // decision and compaction
   int nf = 0, na = 0;
   float lmin = __builtin_inff();
-  for (int base = 0; base < T; base += NT) {
-    const int t = base + tid;
+  for_chunks<R>(T, [&](int r, int t) {
     const bool valid = t < T;
     bool ffn = false;
-    float l = 0.f;
     if (valid) {
-      l = a.logit[t];
+      const float l = lg.at(a.logit, r, t);
       if (budget) {
         const uint32_t key = okey(l);
         const bool skip = a.n_skip > 0 && (key < vstar || (key == vstar && t <= tstar));
@@ -153,11 +189,11 @@ __global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
       else
         a.idx_ad[na + (tid - fpos)] = t;
     }
-    const int nvalid = min(NT, T - base);
+    const int nvalid = min(NT, T - NT * r);
     nf += tot;
     na += nvalid - tot;
     __syncthreads();
-  }
+  });
 
   // smallest FFN logit
 #pragma unroll
@@ -177,7 +213,17 @@ __global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
-  select_kernel<<<1, NT, 0, s>>>(a);
+  const int chunks = (a.T + NT - 1) / NT;
+  if (chunks <= 1)
+    select_kernel<1><<<1, NT, 0, s>>>(a);
+  else if (chunks <= 4)
+    select_kernel<4><<<1, NT, 0, s>>>(a);
+  else if (chunks <= 8)
+    select_kernel<8><<<1, NT, 0, s>>>(a);
+  else if (chunks <= 32)
+    select_kernel<32><<<1, NT, 0, s>>>(a);
+  else
+    select_kernel<0><<<1, NT, 0, s>>>(a);
   return hipGetLastError();
 }
 
