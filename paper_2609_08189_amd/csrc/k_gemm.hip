@@ -178,6 +178,7 @@ __device__ __forceinline__ void load_lds16(const void* g, unsigned char* l) {
 __device__ __forceinline__ int swz(int row, int ch) { return row * ROWB + ((ch ^ ((row >> 1) & 7)) << 4); }
 
 constexpr int GROUP_M = 8;   // row tiles per group of the tile order
+constexpr int kCUs = 256;    // compute units of an MI355X
 
 // instruction classes of __builtin_amdgcn_sched_group_barrier
 constexpr int SG_MFMA = 0x008, SG_VMEM_READ = 0x020, SG_DS_READ = 0x100;
@@ -404,6 +405,196 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   }
 }
 
+// ---------------------------------------------------------------------------
+// Persistent gate/up product.  The plain kernel ends every tile with an epilogue during
+// which the CU does no MFMA work, and all CUs reach it together, once per round of tiles.
+// Here one workgroup per CU walks the tiles its XCD owns (the same grouped order and
+// XCD ranges as mfma_gemm, workgroup q of an XCD taking every nq-th tile of the range);
+// a finished tile is staged as bf16 SiLU(gate) * up in a third LDS region and written
+// out at the start of the next tile's first k-tile, after its loads are in flight, so the
+// stores overlap that tile's MFMAs.  Each wave stages and stores only its own block, so the
+// staging region needs no barrier.  Results are identical to mfma_gemm's.
+// ---------------------------------------------------------------------------
+template <class C>
+__global__ __launch_bounds__(C::NT) void gateup_persist(ARows<bf16_t> A, BRows<bf16_t> B,
+                                                       EpiSwiGLU<bf16_t> epi,
+                                                       const int* __restrict__ m_count, int M_fixed,
+                                                       int K, int mt_max, int n_tiles, int per) {
+  static_assert(C::DUAL, "gate/up only");
+  constexpr int NW = C::NW;
+  constexpr int A_LD = C::BM / 8 / NW;
+  constexpr int B_LD = C::BN / 8 / NW;
+  constexpr int KS = BK / 16;
+  constexpr int NM = C::TM * C::TN;
+  constexpr int NR = C::TM + C::TN;
+  constexpr int NL = A_LD + B_LD;
+  constexpr int OUT_W = C::WTM * C::ON;            // staged bf16 elements per wave
+  constexpr int CPR = C::ON / 8;                   // 16-byte pieces per staged row
+  constexpr int PPL = C::WTM * CPR / kWave;        // pieces per lane
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * C::STAGE + NW * OUT_W * 2];
+  const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3, nq = gridDim.x >> 3;
+  const int total = mt_max * n_tiles;
+  const int M = m_count ? *m_count : M_fixed;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int wm = wave / C::WN, wn = wave % C::WN;
+  const int rsub = lane >> 3;
+  const int khalf = lane >> 5;
+  bf16_t* ostg = reinterpret_cast<bf16_t*>(smem + 2 * C::STAGE) + wave * OUT_W;
+  const int nk = K / BK;
+
+  int fa_row[C::TM], fb_row[C::TN];
+#pragma unroll
+  for (int a = 0; a < C::TM; ++a) fa_row[a] = wm * C::WTM + a * 32 + (lane & 31);
+#pragma unroll
+  for (int b = 0; b < C::TN; ++b) fb_row[b] = C::BM + wn * C::WTN + b * 32 + (lane & 31);
+  bf16x8 fa[2][C::TM], fb[2][C::TN];
+  f32x16 acc[C::TM][C::TN];
+  auto read_frags = [&](int buf, const unsigned char* st, int ks) {
+    const int c = 2 * ks + khalf;
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a) fa[buf][a] = *reinterpret_cast<const bf16x8*>(st + swz(fa_row[a], c));
+#pragma unroll
+    for (int b = 0; b < C::TN; ++b) fb[buf][b] = *reinterpret_cast<const bf16x8*>(st + swz(fb_row[b], c));
+  };
+  auto mfmas = [&](int buf) {
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+      for (int b = 0; b < C::TN; ++b)
+        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][a], fb[buf][b], acc[a][b], 0, 0, 0);
+  };
+  auto interleave = [&](auto nl_) {
+    constexpr int nl = decltype(nl_)::value;
+#pragma unroll
+    for (int i = 0; i < NM; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+      if (i < nl) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, 1, 0);
+      if (i < NR) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+    }
+    if constexpr (nl > NM) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, nl - NM, 0);
+    if constexpr (NR > NM) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, NR - NM, 0);
+  };
+  // write this wave's staged block of the tile at (m0, nt) to act
+  auto store_staged = [&](int m0, int nt) {
+#pragma unroll
+    for (int p = 0; p < PPL; ++p) {
+      const int e = lane + kWave * p;
+      const int i = e / CPR, c8 = (e % CPR) * 8;
+      const int m = m0 + wm * C::WTM + i;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(ostg + i * C::ON + c8);
+      if (m < M) epi.emit_packed(m, nt * C::OUT_N + wn * C::ON + c8, v);
+    }
+  };
+
+  int prev_m0 = -1, prev_nt = 0;
+  for (int li = q; li < per; li += nq) {
+    const int tile = xcd * per + li;
+    if (tile >= total) break;
+    const int grp = tile / (GROUP_M * n_tiles), rem = tile % (GROUP_M * n_tiles);
+    const int gsz = min(GROUP_M, mt_max - grp * GROUP_M);
+    const int mt = grp * GROUP_M + rem % gsz, nt = rem / gsz;
+    const int m0 = mt * C::BM;
+    if (m0 >= M) continue;
+
+    const unsigned char* a_base = reinterpret_cast<const unsigned char*>(A.base);
+    uint32_t a_off[A_LD];
+#pragma unroll
+    for (int i = 0; i < A_LD; ++i) {
+      const int r = 8 * (i * NW + wave) + rsub;
+      const int ch = (lane & 7) ^ ((r >> 1) & 7);
+      const int m = min(m0 + r, M - 1);
+      const int row = A.idx ? A.idx[m] : m;
+      a_off[i] = static_cast<uint32_t>(row) * static_cast<uint32_t>(A.ld * 2) + ch * 16;
+    }
+    const unsigned char* b_base[B_LD];
+    uint32_t b_off[B_LD];
+#pragma unroll
+    for (int i = 0; i < B_LD; ++i) {
+      const int blk = i * NW + wave;
+      const int r = 8 * blk + rsub;
+      const int ch = (lane & 7) ^ ((r >> 1) & 7);
+      const int wb = (8 * blk) / C::WTN, q0 = (8 * blk) % C::WTN, h = C::WTN / 2;
+      const bool up = q0 >= h;
+      b_base[i] = reinterpret_cast<const unsigned char*>(up ? B.b1 : B.b0);
+      const int row = nt * C::OUT_N + wb * h + (r % C::WTN) - (up ? h : 0);
+      b_off[i] = static_cast<uint32_t>(row) * static_cast<uint32_t>(B.ld * 2) + ch * 16;
+    }
+    auto issue = [&](int stage, int k0) {
+      unsigned char* sa = smem + stage * C::STAGE;
+      const uint32_t kb = static_cast<uint32_t>(k0) * 2;
+#pragma unroll
+      for (int i = 0; i < A_LD; ++i) load_lds16(a_base + a_off[i] + kb, sa + (i * NW + wave) * 1024);
+#pragma unroll
+      for (int i = 0; i < B_LD; ++i)
+        load_lds16(b_base[i] + b_off[i] + kb, sa + C::BM * ROWB + (i * NW + wave) * 1024);
+    };
+
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+      for (int b = 0; b < C::TN; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+    // every wave is past the previous tile's last barrier: the stages are free
+    issue(0, 0);
+    if (nk > 1) issue(1, BK);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    // the previous tile's results leave while this tile computes
+    if (prev_m0 >= 0) store_staged(prev_m0, prev_nt);
+    read_frags(0, smem, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+      const unsigned char* st = smem + (kt & 1) * C::STAGE;
+#pragma unroll
+      for (int ks = 0; ks < KS - 1; ++ks) {
+        read_frags((ks + 1) & 1, st, ks + 1);
+        mfmas(ks & 1);
+        interleave(std::integral_constant<int, 0>());
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (kt + 2 < nk) issue(kt & 1, (kt + 2) * BK);
+      if (kt + 1 < nk) read_frags(KS & 1, smem + ((kt + 1) & 1) * C::STAGE, 0);
+      mfmas((KS - 1) & 1);
+      interleave(std::integral_constant<int, NL>());
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // stage SiLU(gate) * up of this wave's block (its previous contents were stored above)
+#pragma unroll
+    for (int a = 0; a < C::TM; ++a)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+#pragma unroll
+        for (int b = 0; b < C::TN / 2; ++b) {
+          const float g = acc[a][b][r], u = acc[a][b + C::TN / 2][r];
+          ostg[i * C::ON + b * 32 + (lane & 31)] = f32_to_bf16(g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u);
+        }
+      }
+    prev_m0 = m0;
+    prev_nt = nt;
+  }
+  if (prev_m0 >= 0) store_staged(prev_m0, prev_nt);
+}
+
+// Persistent launch: one workgroup per CU (a multiple of 8 workgroups so that each XCD holds
+// the same number), each XCD owning a contiguous range of the grouped tile order.
+template <class C>
+hipError_t run_persist(ARows<bf16_t> A, BRows<bf16_t> B, EpiSwiGLU<bf16_t> epi, const int* m_count,
+                       int M_max, int N_out, int K, hipStream_t s) {
+  const int mt_max = (M_max + C::BM - 1) / C::BM;
+  const int n_tiles = N_out / C::OUT_N;
+  const int total = mt_max * n_tiles;
+  if (total == 0) return hipSuccess;
+  const int per = (total + 7) / 8;                 // tiles per XCD
+  const int nq = std::min(per, kCUs / 8);          // workgroups per XCD
+  gateup_persist<C><<<8 * nq, C::NT, 0, s>>>(A, B, epi, m_count, M_max, K, mt_max, n_tiles, per);
+  return hipGetLastError();
+}
+
 template <class C, class Epi>
 hipError_t run_tile(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_count, int M_max,
                     int N_out, int K, hipStream_t s, int splits = 1) {
@@ -430,8 +621,13 @@ hipError_t run_big(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_count
   using T256 = Tile<256, BN, 2, 4, DUAL>;
   using T192 = Tile<192, BN, 2, 4, DUAL>;
   const int n_tiles = N_out / T256::OUT_N;
-  if (tile_cost(M_max, 192, n_tiles) < tile_cost(M_max, 256, n_tiles))
+  if (tile_cost(M_max, 192, n_tiles) < tile_cost(M_max, 256, n_tiles)) {
+    if constexpr (DUAL) {
+      // more tiles than CUs: the persistent kernel hides each tile's epilogue behind the next
+      if ((M_max + 191) / 192 * n_tiles > kCUs) return run_persist<T192>(A, B, epi, m_count, M_max, N_out, K, s);
+    }
     return run_tile<T192>(A, B, epi, m_count, M_max, N_out, K, s);
+  }
   return run_tile<T256>(A, B, epi, m_count, M_max, N_out, K, s);
 }
 

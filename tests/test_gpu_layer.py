@@ -119,3 +119,10 @@ def test_llama31_8b_paper_operating_point_full_shape():
     assert res["layers"][0]["n_ad"] == 1024
     del dp
     torch.cuda.empty_cache()
+
+
+def test_persistent_gate_up_ragged():
+    """More FFN tiles than CUs (the persistent gate/up kernel: each tile's results leave during
+    the next tile) with a row count that is not a multiple of the tile height."""
+    w = BF16_SMALL.replace(d_ff=5120, T=2001, budget=0.27)
+    _run(w, 3)
