@@ -462,7 +462,16 @@ struct SProj {
   bool phi;
 };
 
-__global__ __launch_bounds__(NT) void router_pre_mfma(RouterTailArgs a) {
+// router_pre on 8 waves (16 tokens per workgroup).  Every global load of the kernel is issued
+// first: the P partials, the hidden encoder's and the s-projections' weight fragments (up to
+// PF2 output tiles per wave), the local head's weights and the path-vector inputs; what follows
+// works from registers and LDS between four barriers.
+constexpr int NTP = 512;
+constexpr int NWP = NTP / kWave;
+constexpr int PF2 = 6;
+
+template <int KSS>   // k-steps over d_s (ceil(d_s / 32))
+__global__ __launch_bounds__(NTP) void router_pre_mfma(RouterTailArgs a) {
   LDS16 bf16x8 ax[2][KS_E][kWave];   // SiLU(inv_rms W_hd hbar): hi, lo
   LDS16 bf16x8 as[2][KS_S][kWave];   // s: hi, lo
   LDS16 float s[MT][MAXS + 4];
@@ -477,29 +486,59 @@ __global__ __launch_bounds__(NT) void router_pre_mfma(RouterTailArgs a) {
   const int j = a.j;
   const int d_e = a.d_e, d_head = a.d_head, NP = d_e + d_head, DM = a.d_m, d_s = a.d_s;
   const int d_h = a.d_h, d_a = a.d_a, d_p = a.d_p;
+  const int nq = DM / 16, nct = 4 * nq + d_head / 16;
+  auto proj = [&](int ct) {
+    const int m = ct / nq;
+    if (m < 4) {
+      const void* ws[4] = {a.w_q, a.w_k, a.w_v, a.w_n};
+      return SProj{static_cast<const bf16_t*>(ws[m]), d_s, DM, 16 * (ct - m * nq), 4 * DM, a.qkvn + m * DM,
+                   m < 2};
+    }
+    return SProj{static_cast<const bf16_t*>(a.th1), a.ld_th1, d_head, 16 * (ct - 4 * nq), d_head, a.hs, false};
+  };
 
-  // P segment of 32 values: token tt, segment sg (NP % 32 == 0, NP <= 512), summed over the
-  // K-slice partials in slice order (all loads issued first)
-  const int tt = tid >> 4, sg = tid & 15;
-  const bool has_seg = 32 * sg < NP;
-  f32x4 pv[8];
-  if (has_seg) {
-    const float* src = a.P + static_cast<size_t>(min(t0 + tt, a.T - 1)) * NP + 32 * sg;
+  // (1) P: token tt, columns [16 pc, 16 pc + 16) (NP <= 512), the K-slice partials
+  const int tt = tid >> 5, pc = tid & 31;
+  const bool has_p = 16 * pc < NP;
+  const bool head = has_p && 16 * pc >= d_e;
+  f32x4 pz[MAXSPLIT][4];
+  if (has_p) {
+    const float* src = a.P + static_cast<size_t>(min(t0 + tt, a.T - 1)) * NP + 16 * pc;
     const size_t zs = static_cast<size_t>(a.T) * NP;
-    f32x4 pz[MAXSPLIT][8];
 #pragma unroll
     for (int z = 0; z < MAXSPLIT; ++z)
 #pragma unroll
-      for (int q = 0; q < 8; ++q)
+      for (int q = 0; q < 4; ++q)
         pz[z][q] = *reinterpret_cast<const f32x4*>(src + (z < a.p_splits ? z : 0) * zs + 4 * q);
+  }
+  // (2) the local head's output weights for head columns
+  u32x4 wps2[2] = {{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}};
+  if (head) {
+    const bf16_t* w = static_cast<const bf16_t*>(a.ps2) + 16 * pc - d_e;
+    wps2[0] = *reinterpret_cast<const u32x4*>(w);
+    wps2[1] = *reinterpret_cast<const u32x4*>(w + 8);
+  }
+  // (3) hidden encoder: wave w computes z_h columns [16 w, 16 w + 16)
+  const int ks1 = d_e / 32;
+  const bool st1 = 16 * wave < d_h;
+  bf16x8 b1[KS_E];
+  if (st1) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      pv[q] = pz[0][q];
+    for (int st = 0; st < KS_E; ++st)
+      if (st < ks1) b1[st] = bfrag(static_cast<const bf16_t*>(a.w_hu), d_e, d_h, 16 * wave, 32 * st, d_e, lane);
+  }
+  // (4) s-projections: this wave's first PF2 output tiles ct = wave + NWP c
+  bf16x8 b2[PF2][KSS];
 #pragma unroll
-      for (int z = 1; z < MAXSPLIT; ++z)
-        if (z < a.p_splits) pv[q] += pz[z][q];
+  for (int c = 0; c < PF2; ++c) {
+    const int ct = wave + NWP * c;
+    if (ct < nct) {
+      const SProj p = proj(ct);
+#pragma unroll
+      for (int st = 0; st < KSS; ++st) b2[c][st] = bfrag(p.w, p.ld, p.nrows, p.r0, 32 * st, d_s, lane);
     }
   }
+  // (5) path vector
   if (tid < MT) {
     const int t = t0 + tid;
     float inv_rms = 0.f, dd = 0.f, dp = 0.f, pp = 0.f, pprev = 1.f, mprev = 1.f;
@@ -526,40 +565,48 @@ __global__ __launch_bounds__(NT) void router_pre_mfma(RouterTailArgs a) {
   }
   __syncthreads();
 
-  // hidden-encoder A fragments, local-head partial dot products, path-encoder hidden layer
-  if (has_seg) {
-    float x[32];
+  // hidden-encoder A fragments (columns k = 16 pc + e: k-step pc/2, groups 2 (pc&1), +1),
+  // local-head partial dot products, path-encoder hidden layer
+  if (has_p) {
+    float x[16];
 #pragma unroll
-    for (int q = 0; q < 8; ++q)
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) x[4 * q + e] = pv[q][e];
-    if (32 * sg < d_e) {
+      for (int e = 0; e < 4; ++e) {
+        float v = pz[0][q][e];
+#pragma unroll
+        for (int z = 1; z < MAXSPLIT; ++z)
+          if (z < a.p_splits) v += pz[z][q][e];
+        x[4 * q + e] = v;
+      }
+    if (!head) {
       const float ir = sc[tt];
 #pragma unroll
-      for (int e = 0; e < 32; ++e) x[e] = siluf_(ir * x[e]);
+      for (int e = 0; e < 16; ++e) x[e] = siluf_(ir * x[e]);
+      const int st = pc >> 1, g0 = 2 * (pc & 1);
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
+      for (int h = 0; h < 2; ++h) {
         bf16x8 hi, lo;
-        split8(x + 8 * g, hi, lo);
-        ax[0][sg][tt + 16 * g] = hi;
-        ax[1][sg][tt + 16 * g] = lo;
+        split8(x + 8 * h, hi, lo);
+        ax[0][st][tt + 16 * (g0 + h)] = hi;
+        ax[1][st][tt + 16 * (g0 + h)] = lo;
       }
     } else {
-      const bf16_t* w = static_cast<const bf16_t*>(a.ps2) + 32 * sg - d_e;
       float acc = 0.f;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float wv[8];
-        ld8(w + 8 * q, wv);
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc = fmaf(wv[e], siluf_(x[8 * q + e]), acc);
-      }
-      bpart[tt][sg - d_e / 32] = acc;
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t w = wps2[h][i];
+          acc = fmaf(__uint_as_float(w << 16), siluf_(x[8 * h + 2 * i]), acc);
+          acc = fmaf(__uint_as_float(w & 0xffff0000u), siluf_(x[8 * h + 2 * i + 1]), acc);
+        }
+      bpart[tt][pc - d_e / 16] = acc;
     }
   }
   {
     const bf16_t* w1 = static_cast<const bf16_t*>(a.w_p1);
-    for (int e = tid; e < MT * d_p; e += NT) {
+    for (int e = tid; e < MT * d_p; e += NTP) {
       const int t = e / d_p, o = e % d_p;
       float acc = 0.f;
 #pragma unroll
@@ -569,26 +616,20 @@ __global__ __launch_bounds__(NT) void router_pre_mfma(RouterTailArgs a) {
   }
   __syncthreads();
 
-  // z_h = W_hu x on matrix cores (16-column tiles over the waves), z_a = W_p2 hp
+  // z_h = W_hu x on matrix cores, z_a = W_p2 hp
+  if (st1) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < KS_E; ++st)
+      if (st < ks1) acc = mfma_split(ax[0][st][lane], ax[1][st][lane], b1[st], acc);
+    const int o = 16 * wave + (lane & 15);
+    if (o < d_h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) s[4 * (lane >> 4) + r][o] = acc[r];
+  }
   {
-    const bf16_t* w = static_cast<const bf16_t*>(a.w_hu);
-    const int ks = d_e / 32;
-    for (int ct = wave; 16 * ct < d_h; ct += NT / kWave) {
-      bf16x8 b[KS_E];
-#pragma unroll
-      for (int st = 0; st < KS_E; ++st)
-        if (st < ks) b[st] = bfrag(w, d_e, d_h, 16 * ct, 32 * st, d_e, lane);
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int st = 0; st < KS_E; ++st)
-        if (st < ks) acc = mfma_split(ax[0][st][lane], ax[1][st][lane], b[st], acc);
-      const int o = 16 * ct + (lane & 15);
-      if (o < d_h)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) s[4 * (lane >> 4) + r][o] = acc[r];
-    }
     const bf16_t* w2 = static_cast<const bf16_t*>(a.w_p2);
-    for (int e = tid; e < MT * d_a; e += NT) {
+    for (int e = tid; e < MT * d_a; e += NTP) {
       const int t = e / d_a, o = e % d_a;
       float acc = 0.f;
       for (int k = 0; k < d_p; ++k) acc = fmaf(ldf(w2 + o * d_p + k), hp[t][k], acc);
@@ -598,8 +639,7 @@ __global__ __launch_bounds__(NT) void router_pre_mfma(RouterTailArgs a) {
   __syncthreads();
 
   // s as A fragments (zero past d_s); the local-head logit b
-  const int ks2 = (d_s + 31) / 32;
-  for (int e = tid; e < MT * 4 * ks2; e += NT) {
+  for (int e = tid; e < MT * 4 * KSS; e += NTP) {
     const int i = e & 15, g = (e >> 4) & 3, st = e >> 6;
     const int k0 = 32 * st + 8 * g;
     float x[8];
@@ -609,55 +649,33 @@ __global__ __launch_bounds__(NT) void router_pre_mfma(RouterTailArgs a) {
   }
   if (tid < nvalid) {
     float b = 0.f;
-    for (int q = 0; q < d_head / 32; ++q) b += bpart[tid][q];
+    for (int q = 0; q < d_head / 16; ++q) b += bpart[tid][q];
     a.bvec[t0 + tid] = b;
   }
   __syncthreads();
 
-  // [phi(q); phi(k); v; W_n s; th1[:, :d_s] s], G tiles of 16 columns per wave in flight
-  constexpr int G = 4;
-  const int nq = DM / 16, nct = 4 * nq + d_head / 16;
-  auto proj = [&](int ct) {
-    const int m = ct / nq;
-    SProj p;
-    if (m < 4) {
-      const void* ws[4] = {a.w_q, a.w_k, a.w_v, a.w_n};
-      p = SProj{static_cast<const bf16_t*>(ws[m]), d_s, DM, 16 * (ct - m * nq), 4 * DM, a.qkvn + m * DM,
-                m < 2};
-    } else {
-      p = SProj{static_cast<const bf16_t*>(a.th1), a.ld_th1, d_head, 16 * (ct - 4 * nq), d_head, a.hs,
-                false};
+  // [phi(q); phi(k); v; W_n s; th1[:, :d_s] s]
+  auto finish = [&](int ct, const bf16x8* bw) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < KSS; ++st) acc = mfma_split(as[0][st][lane], as[1][st][lane], bw[st], acc);
+    const SProj p = proj(ct);
+    const int o = p.r0 + (lane & 15);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = t0 + 4 * (lane >> 4) + r;
+      if (t < a.T) p.out[static_cast<size_t>(t) * p.os + o] = p.phi ? phif_(acc[r]) : acc[r];
     }
-    return p;
   };
-  for (int c0 = wave; c0 < nct; c0 += G * (NT / kWave)) {
-    bf16x8 b[G][KS_S];
 #pragma unroll
-    for (int c = 0; c < G; ++c) {
-      const int ct = c0 + c * (NT / kWave);
-      if (ct < nct) {
-        const SProj p = proj(ct);
+  for (int c = 0; c < PF2; ++c)
+    if (wave + NWP * c < nct) finish(wave + NWP * c, b2[c]);
+  for (int ct = wave + NWP * PF2; ct < nct; ct += NWP) {
+    const SProj p = proj(ct);
+    bf16x8 bw[KSS];
 #pragma unroll
-        for (int st = 0; st < KS_S; ++st)
-          if (st < ks2) b[c][st] = bfrag(p.w, p.ld, p.nrows, p.r0, 32 * st, d_s, lane);
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < G; ++c) {
-      const int ct = c0 + c * (NT / kWave);
-      if (ct >= nct) break;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int st = 0; st < KS_S; ++st)
-        if (st < ks2) acc = mfma_split(as[0][st][lane], as[1][st][lane], b[c][st], acc);
-      const SProj p = proj(ct);
-      const int o = p.r0 + (lane & 15);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = t0 + 4 * (lane >> 4) + r;
-        if (t < a.T) p.out[static_cast<size_t>(t) * p.os + o] = p.phi ? phif_(acc[r]) : acc[r];
-      }
-    }
+    for (int st = 0; st < KSS; ++st) bw[st] = bfrag(p.w, p.ld, p.nrows, p.r0, 32 * st, d_s, lane);
+    finish(ct, bw);
   }
 }
 
@@ -891,11 +909,18 @@ __global__ __launch_bounds__(NT) void history_state_kernel(const float* __restri
 
 hipError_t launch_pre_post(const RouterTailArgs& a, bool post, hipStream_t s) {
   if (a.dtype == 1) {
-    dim3 grid((a.T + MT - 1) / MT), block(NT);
-    if (post)
-      router_post_mfma<<<grid, block, 0, s>>>(a);
-    else
-      router_pre_mfma<<<grid, block, 0, s>>>(a);
+    dim3 grid((a.T + MT - 1) / MT);
+    if (post) {
+      router_post_mfma<<<grid, NT, 0, s>>>(a);
+    } else {
+      switch ((a.d_s + 31) / 32) {
+        case 1: router_pre_mfma<1><<<grid, NTP, 0, s>>>(a); break;
+        case 2: router_pre_mfma<2><<<grid, NTP, 0, s>>>(a); break;
+        case 3: router_pre_mfma<3><<<grid, NTP, 0, s>>>(a); break;
+        case 4: router_pre_mfma<4><<<grid, NTP, 0, s>>>(a); break;
+        default: return hipErrorInvalidValue;
+      }
+    }
   } else {
     dim3 grid((a.T + TB - 1) / TB), block(NT);
     if (post)
