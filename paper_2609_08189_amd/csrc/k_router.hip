@@ -679,22 +679,34 @@ __global__ __launch_bounds__(NTP) void router_pre_mfma(RouterTailArgs a) {
   }
 }
 
-__global__ __launch_bounds__(NT) void router_post_mfma(RouterTailArgs a) {
-  LDS16 bf16x8 ac[2][KS_M][kWave];   // c: hi, lo
-  LDS16 float ns[MT][MAXM + 4];      // W_n s
-  LDS16 float wc[MT][MAXM + 4];      // W_c c
+// router_post on 8 waves (16 tokens per workgroup), every global load issued first:
+// c (as split A fragments), W_n s, the s part of f_theta's first layer, and the weight
+// fragments of W_c and of f_theta's c columns for this wave's output tiles.
+template <int KSM>   // k-steps over d_m (d_m / 32)
+__global__ __launch_bounds__(NTP) void router_post_mfma(RouterTailArgs a) {
+  constexpr int DM = 32 * KSM;
+  constexpr int TWC = (DM / 16 + NWP - 1) / NWP;      // W_c output tiles per wave
+  constexpr int TWH = (MAXE / 16 + NWP - 1) / NWP;    // f_theta output tiles per wave (d_head <= 256)
+  LDS16 bf16x8 ac[2][KSM][kWave];   // c: hi, lo
+  LDS16 float ns[MT][DM + 4];       // W_n s
+  LDS16 float wc[MT][DM + 4];       // W_c c
   __shared__ float nu[MT];
-  __shared__ float apart[NT / kWave][MT];
+  __shared__ float apart[NWP][MT];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int t0 = blockIdx.x * MT;
   const int nvalid = min(MT, a.T - t0);
   const int j = a.j;
-  const int DM = a.d_m, d_head = a.d_head, d_s = a.d_s;
+  const int d_head = a.d_head, d_s = a.d_s;
+  const int g4 = 4 * (lane >> 4);
   auto tok = [&](int i) { return static_cast<size_t>(min(t0 + i, a.T - 1)); };
+  const bf16_t* th1 = static_cast<const bf16_t*>(a.th1);
+  const bf16_t* th2 = static_cast<const bf16_t*>(a.th2);
+  const bf16_t* w_c = static_cast<const bf16_t*>(a.w_c);
+  const int ld = a.ld_th1, nct_h = d_head / 16;
 
-  const int ks = DM / 32;   // d_m in {32, 64, 128, 256}
-  for (int e = tid; e < MT * 4 * ks; e += NT) {
+  // c rows as split fragments, and W_n s
+  for (int e = tid; e < MT * 4 * KSM; e += NTP) {
     const int i = e & 15, g = (e >> 4) & 3, st = e >> 6;
     const float* src = a.cvec + tok(i) * DM + 32 * st + 8 * g;
     const f32x4 lo4 = *reinterpret_cast<const f32x4*>(src);
@@ -707,34 +719,53 @@ __global__ __launch_bounds__(NT) void router_post_mfma(RouterTailArgs a) {
     }
     split8(x, ac[0][st][i + 16 * g], ac[1][st][i + 16 * g]);
   }
-  for (int e = tid; e < MT * DM / 4; e += NT) {
+  for (int e = tid; e < MT * DM / 4; e += NTP) {
     const int i = e / (DM / 4), c4 = e % (DM / 4);
     *reinterpret_cast<f32x4*>(&ns[i][4 * c4]) =
         *reinterpret_cast<const f32x4*>(a.qkvn + tok(i) * 4 * DM + 3 * DM + 4 * c4);
   }
+  // weight fragments of this wave's tiles, the s part of the pre-activation, nu and th2 weights
+  bf16x8 bc[TWC][KSM], bh[TWH][KSM];
+  float hsv[TWH][4], wnu[TWH], w2[TWH];
+#pragma unroll
+  for (int c = 0; c < TWC; ++c) {
+    const int ct = wave + NWP * c;
+    if (16 * ct < DM)
+#pragma unroll
+      for (int st = 0; st < KSM; ++st) bc[c][st] = bfrag(w_c, DM, DM, 16 * ct, 32 * st, DM, lane);
+  }
+#pragma unroll
+  for (int c = 0; c < TWH; ++c) {
+    const int ct = wave + NWP * c;
+    if (ct < nct_h) {
+      const int o = 16 * ct + (lane & 15);
+#pragma unroll
+      for (int st = 0; st < KSM; ++st) bh[c][st] = bfrag(th1 + d_s, ld, d_head, 16 * ct, 32 * st, DM, lane);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) hsv[c][r] = a.hs[tok(g4 + r) * d_head + o];
+      wnu[c] = bf16_to_f32(th1[static_cast<size_t>(o) * ld + d_s + DM]);
+      w2[c] = bf16_to_f32(th2[o]);
+    }
+  }
   __syncthreads();
 
   // W_c c
-  {
-    const bf16_t* w = static_cast<const bf16_t*>(a.w_c);
-    for (int ct = wave; 16 * ct < DM; ct += NT / kWave) {
-      bf16x8 b[KS_M];
 #pragma unroll
-      for (int st = 0; st < KS_M; ++st)
-        if (st < ks) b[st] = bfrag(w, DM, DM, 16 * ct, 32 * st, DM, lane);
+  for (int c = 0; c < TWC; ++c) {
+    const int ct = wave + NWP * c;
+    if (16 * ct < DM) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int st = 0; st < KS_M; ++st)
-        if (st < ks) acc = mfma_split(ac[0][st][lane], ac[1][st][lane], b[st], acc);
+      for (int st = 0; st < KSM; ++st) acc = mfma_split(ac[0][st][lane], ac[1][st][lane], bc[c][st], acc);
       const int o = 16 * ct + (lane & 15);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) wc[4 * (lane >> 4) + r][o] = acc[r];
+      for (int r = 0; r < 4; ++r) wc[g4 + r][o] = acc[r];
     }
   }
   __syncthreads();
 
   // nu = 1 - cos(W_n s, W_c c); 0 at j = 1
-  for (int i = wave; i < MT; i += NT / kWave) {
+  for (int i = wave; i < MT; i += NWP) {
     float nn = 0.f, cc = 0.f, nc = 0.f;
     for (int k = lane; k < DM; k += kWave) {
       const float n = ns[i][k], c = wc[i][k];
@@ -749,37 +780,15 @@ __global__ __launch_bounds__(NT) void router_post_mfma(RouterTailArgs a) {
   }
   __syncthreads();
 
-  // a = th2 . SiLU(th1 [s; c; nu]): the s part (hs) and the nu column are added in the epilogue
-  constexpr int G = 4;
-  const bf16_t* th1 = static_cast<const bf16_t*>(a.th1);
-  const bf16_t* th2 = static_cast<const bf16_t*>(a.th2);
-  const int ld = a.ld_th1, nct = d_head / 16, g4 = 4 * (lane >> 4);
+  // a = th2 . SiLU(th1 [s; c; nu])
   float ap[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int c0 = wave; c0 < nct; c0 += G * (NT / kWave)) {
-    bf16x8 b[G][KS_M];
-    float hsv[G][4], wnu[G], w2[G];
 #pragma unroll
-    for (int c = 0; c < G; ++c) {
-      const int ct = c0 + c * (NT / kWave);
-      if (ct < nct) {
-        const int o = 16 * ct + (lane & 15);
-#pragma unroll
-        for (int st = 0; st < KS_M; ++st)
-          if (st < ks) b[c][st] = bfrag(th1 + d_s, ld, d_head, 16 * ct, 32 * st, DM, lane);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) hsv[c][r] = a.hs[tok(g4 + r) * d_head + o];
-        wnu[c] = bf16_to_f32(th1[static_cast<size_t>(o) * ld + d_s + DM]);
-        w2[c] = bf16_to_f32(th2[o]);
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < G; ++c) {
-      const int ct = c0 + c * (NT / kWave);
-      if (ct >= nct) break;
+  for (int c = 0; c < TWH; ++c) {
+    const int ct = wave + NWP * c;
+    if (ct < nct_h) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int st = 0; st < KS_M; ++st)
-        if (st < ks) acc = mfma_split(ac[0][st][lane], ac[1][st][lane], b[c][st], acc);
+      for (int st = 0; st < KSM; ++st) acc = mfma_split(ac[0][st][lane], ac[1][st][lane], bh[c][st], acc);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const float pre = acc[r] + hsv[c][r] + wnu[c] * nu[g4 + r];
@@ -799,7 +808,7 @@ __global__ __launch_bounds__(NT) void router_post_mfma(RouterTailArgs a) {
     const int t = t0 + tid;
     float av = 0.f;
 #pragma unroll
-    for (int w = 0; w < NT / kWave; ++w) av += apart[w][tid];
+    for (int w = 0; w < NWP; ++w) av += apart[w][tid];
     const float mprev = j > 1 ? a.m_hist[t] : 1.0f;
     const float p = sigmoidf_(av / a.T_hist);
     a.p_hist[t] = p;
@@ -911,7 +920,13 @@ hipError_t launch_pre_post(const RouterTailArgs& a, bool post, hipStream_t s) {
   if (a.dtype == 1) {
     dim3 grid((a.T + MT - 1) / MT);
     if (post) {
-      router_post_mfma<<<grid, NT, 0, s>>>(a);
+      switch (a.d_m) {
+        case 32: router_post_mfma<1><<<grid, NTP, 0, s>>>(a); break;
+        case 64: router_post_mfma<2><<<grid, NTP, 0, s>>>(a); break;
+        case 128: router_post_mfma<4><<<grid, NTP, 0, s>>>(a); break;
+        case 256: router_post_mfma<8><<<grid, NTP, 0, s>>>(a); break;
+        default: return hipErrorInvalidValue;
+      }
     } else {
       switch ((a.d_s + 31) / 32) {
         case 1: router_pre_mfma<1><<<grid, NTP, 0, s>>>(a); break;
