@@ -164,12 +164,15 @@ def _short(name):
     return name.replace("hero::(anonymous namespace)::", "").replace("void ", "")[:150].replace("|", "/")
 
 
-def summarize_rocprof(root):
+def summarize_rocprof(root, window=None):
     """Markdown summary of rocprofv3 CSV files (kernel stats and/or counter collection) under root.
 
     Counter tables give the mean per dispatch of each kernel; for the plain device
     copy (the runtime's copyBuffer kernel) the largest dispatch is shown, which is
-    the calibration copy of known size.
+    the calibration copy of known size.  With window = (skip, count), the kernel trace
+    also gives each kernel's mean duration over its dispatches skip .. skip+count-1 (in
+    dispatch order): for a bench run with W warmup steps, (1 + W, K) selects exactly the
+    K timed steps (one checked call precedes the warmup).
     """
     import csv
     import glob
@@ -184,6 +187,24 @@ def summarize_rocprof(root):
                       f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
                       f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
         print()
+    traces = sorted(glob.glob(os.path.join(root, "**", "*kernel_trace.csv"), recursive=True))
+    if window is not None:
+        skip, count = window
+        for path in traces:
+            per = {}
+            with open(path) as f:
+                for r in csv.DictReader(f):
+                    per.setdefault(r["Kernel_Name"], []).append(
+                        (int(r["Dispatch_Id"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
+            print(f"### dispatches {skip}..{skip + count - 1} of each kernel ({os.path.relpath(path, root)})\n")
+            print("| kernel | dispatches | mean us | min us | max us |")
+            print("|---|---|---|---|---|")
+            for name, v in sorted(per.items(), key=lambda kv: -sum(d for _, d in kv[1])):
+                sel = [d for _, d in sorted(v)][skip:skip + count]
+                if sel:
+                    print(f"| {_short(name)} | {len(sel)} | {sum(sel) / len(sel):.2f} | {min(sel):.2f} | "
+                          f"{max(sel):.2f} |")
+            print()
     counters = sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True))
     for path in counters:
         agg = {}
@@ -214,9 +235,11 @@ def main():
                     help="also run a plain device-to-device copy of this many MiB (HBM counter calibration)")
     ap.add_argument("--summarize", metavar="DIR",
                     help="print a summary of rocprofv3 CSV output found under DIR and exit (no GPU)")
+    ap.add_argument("--window", type=int, nargs=2, metavar=("SKIP", "COUNT"),
+                    help="with --summarize: per-kernel mean over dispatches SKIP..SKIP+COUNT-1")
     args = ap.parse_args()
     if args.summarize:
-        summarize_rocprof(args.summarize)
+        summarize_rocprof(args.summarize, window=args.window)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the routed FFN path shards over tokens with no "

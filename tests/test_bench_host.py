@@ -38,7 +38,12 @@ def test_summarize_reads_rocprof_csv(tmp_path, capsys):
         '"void hero::(anonymous namespace)::k(int)",3,3000,1000,100.0,900,1100,0\n')
     (d / "x_counter_collection.csv").write_text(
         '"Kernel_Name","Counter_Name","Counter_Value"\n"k(int)","FETCH_SIZE",10\n"k(int)","FETCH_SIZE",30\n')
-    bench.summarize_rocprof(str(d))
+    (d / "x_kernel_trace.csv").write_text(
+        '"Kernel_Name","Dispatch_Id","Start_Timestamp","End_Timestamp"\n'
+        '"k(int)",1,0,1000\n"k(int)",2,5000,7000\n"k(int)",3,9000,12000\n"j(int)",4,0,500\n')
+    bench.summarize_rocprof(str(d), window=(1, 2))
     out = capsys.readouterr().out
     assert "| k(int) | 3 | 0.003 | 1.00 | 0.90 | 1.10 | 100.00 |" in out
     assert "| k(int) | FETCH_SIZE | 2 | 20.0 | 30.0 |" in out
+    assert "| k(int) | 2 | 2.50 | 2.00 | 3.00 |" in out      # dispatches 2 and 3 of k
+    assert "| j(int) |" not in out.split("dispatches 1..2")[1].split("###")[0]   # j has one dispatch
