@@ -89,8 +89,9 @@ def kernel_work(w, n_f, n_a, T, j, memory="matrix"):
 
 
 def describe(w, j):
+    where = f"routed layer j={j} of {w.L_R}" if j > 0 else f"routed stack of {w.L_R} layers"
     return (f"{w.name}: d={w.d}, d_ff={w.d_ff}, adapter rank {w.d_r}, memory dim {w.d_m}, "
-            f"T={w.T} tokens ({w.batch}x{w.seq}), routed layer j={j} of {w.L_R}, "
+            f"T={w.T} tokens ({w.batch}x{w.seq}), {where}, "
             + (f"skip budget {w.budget}" if w.mode == "budget" else f"threshold tau={w.tau}"))
 
 
@@ -254,78 +255,92 @@ def main():
     from paper_2609_08189_amd.device import DeviceProblem
 
     w = synth.WORKLOADS[args.workload]
-    if w.layer_j <= 0:
-        raise SystemExit(f"{args.workload} is a stack workload; this bench times single layer calls")
+    stack = w.layer_j <= 0          # a stack workload: a step is one hero_routed_stack call
     j = w.layer_j
+    L = w.L_R if stack else 1       # routed layers per step
     print(f"# preparing {describe(w, j)}", file=sys.stderr, flush=True)
     prob = synth.make_problem(w, seed=args.seed)
     dp = DeviceProblem(prob, device="cuda:0", stats=True, history=args.memory == "history")
     stream = dp.stream()
     ev = HipEvents()
+    step = dp.run_stack if stack else (lambda: dp.run_layer(j))
 
     # one checked call with stats for the realized branch sizes (and the CPU baseline)
-    dp.run_layer(j)
+    step()
     torch.cuda.synchronize()
-    st0 = dp.stats[0].host()
+    layer_stats = [s.host() for s in dp.stats]
+    st0 = layer_stats[0]
+    nfs = [ls["n_ffn"] for ls in layer_stats]
+    nas = [ls["n_ad"] for ls in layer_stats]
     n_f, n_a = st0["n_ffn"], st0["n_ad"]
     # the timed steps run without the optional stats outputs
     stats_saved, dp.stats = dp.stats, None
 
     for _ in range(args.warmup):
-        dp.run_layer(j)
+        step()
     torch.cuda.synchronize()
 
     K = args.steps
     dom = "ffn_gate_up"
-    ks, ke = ev.create(K), ev.create(K)
+    n_dom = K * sum(1 for x in nfs if x > 0)   # launches of the dominant kernel in the timed steps
+    ks, ke = ev.create(n_dom), ev.create(n_dom)
     H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
     t_start, t_stop = ev.create(2)
     torch.cuda.synchronize()
     ev.record(t_start, stream)
     for _ in range(K):
-        dp.run_layer(j)
+        step()
     ev.record(t_stop, stream)
     torch.cuda.synchronize()
     H.hero_kernel_timer(H.HERO_K[dom], [], [])
     total_ms = ev.elapsed_ms(t_start, t_stop)
-    dom_ms = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
+    dom_ms_step = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K     # per step, all layers
     ms_step = total_ms / K
     print(f"# timed {K} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
 
-    # per-kernel breakdown (untimed pass, every kernel instrumented)
+    # per-kernel breakdown (untimed pass, every kernel instrumented): mean per launch, with the
+    # algorithmic work of the mean layer
+    layers = list(range(1, L + 1)) if stack else [j]
+    works = [kernel_work(w, nf, na, w.T, jj, args.memory) for nf, na, jj in zip(nfs, nas, layers)]
     per = {}
     handles = {}
     for name in H.KERNELS:
-        a, b = ev.create(K), ev.create(K)
+        a, b = ev.create(K * L), ev.create(K * L)
         handles[name] = (a, b)
         H.hero_kernel_timer(H.HERO_K[name], a, b)
     for _ in range(K):
-        dp.run_layer(j)
+        step()
     torch.cuda.synchronize()
-    work = kernel_work(w, n_f, n_a, w.T, j, args.memory)
     for name in H.KERNELS:
         H.hero_kernel_timer(H.HERO_K[name], [], [])
         a, b = handles[name]
-        launched = (name.startswith("ffn") and n_f > 0) or (name.startswith("adapter") and n_a > 0) or \
-            not (name.startswith("ffn") or name.startswith("adapter"))
-        if launched:
-            us = 1000.0 * sum(ev.elapsed_ms(x, y) for x, y in zip(a, b)) / K
-            wk = work[name]
-            per[name] = {"us": round(us, 2),
-                         "tflops": round(wk["flops"] / us * 1e-6, 1) if wk["flops"] else None,
-                         "gbs": round(wk["bytes"] / us * 1e-3, 1)}
+        active = [i for i in range(L) if not ((name.startswith("ffn") and nfs[i] == 0) or
+                                               (name.startswith("adapter") and nas[i] == 0))]
+        if active:
+            n_launch = K * len(active)
+            us = 1000.0 * sum(ev.elapsed_ms(x, y) for x, y in zip(a[:n_launch], b[:n_launch])) / n_launch
+            fl = sum(works[i][name]["flops"] for i in active) / len(active)
+            by = sum(works[i][name]["bytes"] for i in active) / len(active)
+            per[name] = {"us": round(us, 2), "tflops": round(fl / us * 1e-6, 1) if fl else None,
+                         "gbs": round(by / us * 1e-3, 1)}
         ev.destroy(a + b)
 
     tokens_per_s = w.T / (ms_step * 1e-3)
-    dflops = work[dom]["flops"]
-    achieved = dflops / (dom_ms * 1e-3) * 1e-12
+    dflops = sum(wk[dom]["flops"] for wk in works)          # per step
+    achieved = dflops / (dom_ms_step * 1e-3) * 1e-12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    n_launch_step = max(1, n_dom // K)
     roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": counted_traffic(dom), "kernel": dom,
-            "avg_launch_us": round(dom_ms * 1e3, 2),
-            "work_per_launch": f"4*d*d_ff FLOP per FFN token x {n_f} FFN tokens = {dflops / 1e9:.1f} GFLOP",
+            "frac": round(achieved / peak, 4),
+            "traffic": counted_traffic(dom) if args.workload == "llama31_8b_layer" and args.memory == "matrix" else None,
+            "kernel": dom, "avg_launch_us": round(dom_ms_step * 1e3 / n_launch_step, 2),
+            "work_per_launch": (f"4*d*d_ff FLOP per FFN token x {n_f} FFN tokens = {dflops / 1e9:.1f} GFLOP"
+                                if not stack else
+                                f"4*d*d_ff FLOP per FFN token x {sum(nfs)} FFN tokens over {L} layers = "
+                                f"{dflops / 1e9:.1f} GFLOP per step, {n_launch_step} launches"),
             "traffic_note": "HBM bytes read + written per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1, "
-                            "calibrated on a 1 GiB copy) from profiles/, null if the GEMM changed since"}
+                            "calibrated on a 1 GiB copy) from profiles/, null if the GEMM changed since or "
+                            "for workloads the counters were not taken on"}
 
     result = {
         "metric": "routed-FFN-stack tokens/sec at Llama-3.1-8B shape; % MFMA/HBM roofline",
@@ -335,11 +350,12 @@ def main():
         "config": {"workload": describe(w, j) + ("" if args.memory == "matrix" else
                                                  ", router memory in depth-history form"),
                    "memory": args.memory, "global_batch": w.batch, "seq_len": w.seq,
-                   "tokens": w.T, "parallelism": "none", "n_ffn": n_f, "n_adapter": n_a},
+                   "tokens": w.T, "layers_per_step": L, "parallelism": "none",
+                   "n_ffn": n_f if not stack else sum(nfs), "n_adapter": n_a if not stack else sum(nas)},
         "roofline": roof,
         "kernels": per,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not stack:
         dp.stats = stats_saved
         print("# timing the CPU oracle on a token sample", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(prob, st0, j, target_s=args.cpu_target_s)

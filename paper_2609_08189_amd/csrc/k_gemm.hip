@@ -220,15 +220,19 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   // [x per, (x+1) per) of a grouped tile order (GROUP_M row tiles by every column tile),
   // so that the 32 tiles one XCD runs at a time share 8 row panels and 4 column panels
   // in its L2.
-  const int per = gridDim.x >> 3;
-  const int tile = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
-  if (tile >= mt_max * n_tiles) return;
-  const int grp = tile / (GROUP_M * n_tiles), rem = tile % (GROUP_M * n_tiles);
-  const int gsz = min(GROUP_M, mt_max - grp * GROUP_M);
-  const int mt = grp * GROUP_M + rem % gsz, nt = rem / gsz;
+  // The grid is sized for M_fixed rows; the order is laid over the rows that exist (the device
+  // count), so that every XCD gets an equal share however few rows there are.
   const int M = m_count ? *m_count : M_fixed;
+  const int mt_act = min(mt_max, (M + C::BM - 1) / C::BM);
+  const int per = (mt_act * n_tiles + 7) >> 3;
+  const int q = blockIdx.x >> 3;
+  if (q >= per) return;
+  const int tile = (blockIdx.x & 7) * per + q;
+  if (tile >= mt_act * n_tiles) return;
+  const int grp = tile / (GROUP_M * n_tiles), rem = tile % (GROUP_M * n_tiles);
+  const int gsz = min(GROUP_M, mt_act - grp * GROUP_M);
+  const int mt = grp * GROUP_M + rem % gsz, nt = rem / gsz;
   const int m0 = mt * C::BM;
-  if (m0 >= M) return;
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
@@ -419,7 +423,7 @@ template <class C>
 __global__ __launch_bounds__(C::NT) void gateup_persist(ARows<bf16_t> A, BRows<bf16_t> B,
                                                        EpiSwiGLU<bf16_t> epi,
                                                        const int* __restrict__ m_count, int M_fixed,
-                                                       int K, int mt_max, int n_tiles, int per) {
+                                                       int K, int mt_max, int n_tiles) {
   static_assert(C::DUAL, "gate/up only");
   constexpr int NW = C::NW;
   constexpr int A_LD = C::BM / 8 / NW;
@@ -433,8 +437,10 @@ __global__ __launch_bounds__(C::NT) void gateup_persist(ARows<bf16_t> A, BRows<b
   constexpr int PPL = C::WTM * CPR / kWave;        // pieces per lane
   __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * C::STAGE + NW * OUT_W * 2];
   const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3, nq = gridDim.x >> 3;
-  const int total = mt_max * n_tiles;
   const int M = m_count ? *m_count : M_fixed;
+  const int mt_act = min(mt_max, (M + C::BM - 1) / C::BM);   // row tiles that exist
+  const int total = mt_act * n_tiles;
+  const int per = (total + 7) >> 3;                           // tiles per XCD
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int wm = wave / C::WN, wn = wave % C::WN;
@@ -492,10 +498,9 @@ __global__ __launch_bounds__(C::NT) void gateup_persist(ARows<bf16_t> A, BRows<b
     const int tile = xcd * per + li;
     if (tile >= total) break;
     const int grp = tile / (GROUP_M * n_tiles), rem = tile % (GROUP_M * n_tiles);
-    const int gsz = min(GROUP_M, mt_max - grp * GROUP_M);
+    const int gsz = min(GROUP_M, mt_act - grp * GROUP_M);
     const int mt = grp * GROUP_M + rem % gsz, nt = rem / gsz;
     const int m0 = mt * C::BM;
-    if (m0 >= M) continue;
 
     const unsigned char* a_base = reinterpret_cast<const unsigned char*>(A.base);
     uint32_t a_off[A_LD];
@@ -589,9 +594,8 @@ hipError_t run_persist(ARows<bf16_t> A, BRows<bf16_t> B, EpiSwiGLU<bf16_t> epi, 
   const int n_tiles = N_out / C::OUT_N;
   const int total = mt_max * n_tiles;
   if (total == 0) return hipSuccess;
-  const int per = (total + 7) / 8;                 // tiles per XCD
-  const int nq = std::min(per, kCUs / 8);          // workgroups per XCD
-  gateup_persist<C><<<8 * nq, C::NT, 0, s>>>(A, B, epi, m_count, M_max, K, mt_max, n_tiles, per);
+  const int nq = std::min((total + 7) / 8, kCUs / 8);   // workgroups per XCD
+  gateup_persist<C><<<8 * nq, C::NT, 0, s>>>(A, B, epi, m_count, M_max, K, mt_max, n_tiles);
   return hipGetLastError();
 }
 
