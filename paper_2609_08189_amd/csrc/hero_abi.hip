@@ -5,6 +5,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 
 #include "../../include/hero.h"
@@ -49,7 +50,9 @@ Layout layout_of(const hero_dims& d, int T, bool stack) {
   L.counts = take(16);
   L.lambda = take(16);
   L.act = take(t * d.d_ff * es);
-  L.part = take(hero::adapter_part_floats(d.dtype, d.d, d.d_r, T) * 4);
+  // the FFN's split-K partials and the adapter's hidden rows share one region (run in turn)
+  L.part = take(std::max(hero::adapter_part_floats(d.dtype, d.d, d.d_r, T),
+                         hero::ffn_part_floats(d.dtype, d.d, d.d_ff, T)) * 4);
   L.rscr = take(hero::router_scratch_floats(d.d_m, d.d_head, T) * 4);
   L.ring = stack ? take(3 * t * d.d * es) : 0;
   L.total = off;
@@ -311,12 +314,12 @@ int run_layer(const LayerCall& c) {
   if (n_ffn_max > 0) {
     e = timed(HERO_K_FFN_GATE_UP, st, [&] {
       return launch_ffn_gateup(D.dtype, u, idx_ffn, counts, n_ffn_max, c.ffn->w_gate, c.ffn->w_up,
-                               act, D.d, D.d_ff, st);
+                               act, part, D.d, D.d_ff, st);
     });
     if (e != hipSuccess) return HERO_E_LAUNCH;
     e = timed(HERO_K_FFN_DOWN, st, [&] {
       return launch_ffn_down(D.dtype, act, idx_ffn, counts, n_ffn_max, c.ffn->w_down, c.hbar, gate,
-                             c.h_out, D.d, D.d_ff, st);
+                             c.h_out, part, D.d, D.d_ff, st);
     });
     if (e != hipSuccess) return HERO_E_LAUNCH;
   }

@@ -78,13 +78,16 @@ struct SelectArgs {
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 
 // FFN branch, gate/up: act[m] = SiLU(W_g u_t) * (W_u u_t), t = idx_ffn[m], m < counts[0].
+// part: fp32 scratch of ffn_part_floats(dtype, d, d_ff, T) floats for any n_max <= T (used
+// when few rows split K).
+size_t ffn_part_floats(int dtype, int d, int d_ff, int T);
 hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const int* counts,
-                             int n_max, const void* w_gate, const void* w_up, void* act, int d,
-                             int d_ff, hipStream_t s);
+                             int n_max, const void* w_gate, const void* w_up, void* act,
+                             float* part, int d, int d_ff, hipStream_t s);
 // FFN branch, down + scatter: h_out[t] = hbar[t] + g[t] * (W_d act[m]), t = idx_ffn[m].
 hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const int* counts,
                            int n_max, const void* w_down, const void* hbar, const float* gate,
-                           void* h_out, int d, int d_ff, hipStream_t s);
+                           void* h_out, float* part, int d, int d_ff, hipStream_t s);
 
 // Adapter branch: h_out[t] = hbar[t] + (1 - g[t]) * W_2 SiLU(W_1 u_t) for t = idx_ad[m].
 // part: fp32 scratch of adapter_part_floats(dtype, d, d_r, T) floats.

@@ -162,8 +162,9 @@ struct EpiScatter {
 //   * the workgroup barrier sits before the last k-step: by then every wave has
 //     read the whole stage, so the loads of tile k+2 are issued into it, one per
 //     MFMA of that last k-step, together with the first fragment reads of tile k+1.
-// A grid with gridDim.y > 1 splits K: workgroup y covers k in [y K, (y + 1) K) and its
-// epilogue writes partial sums to a slice of its own (the router pre-activations).
+// A grid with gridDim.y = S > 1 splits K: workgroup y covers k-tiles [y n / S, (y + 1) n / S)
+// of the n = K / 64 and its epilogue writes partial sums to a slice of its own (router
+// pre-activations; FFN products with few rows).
 // Epilogues: the gate/up product stages its finished bf16 tile in LDS at once and
 // writes 16-byte row pieces; the others first fetch what they combine with (hbar
 // rows) for the whole wave tile, then stage fp32 results in 32-row blocks.
@@ -233,6 +234,10 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   const int gsz = min(GROUP_M, mt_act - grp * GROUP_M);
   const int mt = grp * GROUP_M + rem % gsz, nt = rem / gsz;
   const int m0 = mt * C::BM;
+  // split K: workgroup y covers k-tiles [y nkt / S, (y+1) nkt / S) (S = gridDim.y <= nkt)
+  const int nkt = K / BK;
+  const int kt0 = static_cast<int>(blockIdx.y) * nkt / static_cast<int>(gridDim.y);
+  const int kt1 = (static_cast<int>(blockIdx.y) + 1) * nkt / static_cast<int>(gridDim.y);
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
@@ -274,7 +279,7 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
 
   auto issue = [&](int stage, int k0) {
     unsigned char* sa = smem + stage * C::STAGE;
-    const uint32_t kb = static_cast<uint32_t>(k0 + blockIdx.y * K) * 2;
+    const uint32_t kb = static_cast<uint32_t>(k0 + kt0 * BK) * 2;
 #pragma unroll
     for (int i = 0; i < A_LD; ++i) load_lds16(a_base + a_off[i] + kb, sa + (i * NW + wave) * 1024);
 #pragma unroll
@@ -325,7 +330,7 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
     if constexpr (NR > NM) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, NR - NM, 0);
   };
 
-  const int nk = K / BK;
+  const int nk = kt1 - kt0;
   issue(0, 0);
   if (nk > 1) issue(1, BK);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -607,7 +612,7 @@ hipError_t run_tile(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_coun
   const int total = mt_max * n_tiles;
   if (total == 0) return hipSuccess;
   const dim3 grid((total + 7) / 8 * 8, splits);
-  mfma_gemm<C, Epi><<<grid, C::NT, 0, s>>>(A, B, epi, m_count, M_max, K / splits, mt_max, n_tiles);
+  mfma_gemm<C, Epi><<<grid, C::NT, 0, s>>>(A, B, epi, m_count, M_max, K, mt_max, n_tiles);
   return hipGetLastError();
 }
 
@@ -909,12 +914,131 @@ hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, con
   return run_f32<false>(A, B, epi, nullptr, T, N, d, s);
 }
 
+namespace {
+
+// ---------------------------------------------------------------------------
+// FFN products with few rows (a decode batch): the plain launch has fewer output tiles than
+// half the CUs, each streaming the whole of K.  K is then split S ways (the most that keeps
+// the launch within one round of workgroups), the slices write fp32 partial sums, and a pass
+// over them adds the S slices in a fixed order and finishes the epilogue.
+// ---------------------------------------------------------------------------
+using TileSplitGU = Tile<192, 256, 2, 4, false>;    // [W_g; W_u] as one 2 d_ff-row operand
+using TileSplitDown = Tile<192, 128, 2, 4, false>;
+constexpr int kMaxSplitGU = 8, kMaxSplitDown = 16;
+
+int split_ways(int tiles, int nkt, int cap) {
+  if (tiles <= 0 || 2 * tiles > kCUs) return 1;
+  return std::max(1, std::min({cap, kCUs / tiles, nkt}));
+}
+int gateup_split(int n, int d, int d_ff) {
+  return split_ways((n + TileSplitGU::BM - 1) / TileSplitGU::BM * (2 * d_ff / TileSplitGU::OUT_N),
+                    d / BK, kMaxSplitGU);
+}
+int down_split(int n, int d, int d_ff) {
+  return split_ways((n + TileSplitDown::BM - 1) / TileSplitDown::BM * (d / TileSplitDown::OUT_N),
+                    d_ff / BK, kMaxSplitDown);
+}
+
+// act[m][c] = bf16(SiLU(g) u) with g, u the sums over z < S of P[z][m][c] and P[z][m][d_ff + c];
+// one thread per 8 columns of a row, rows m < *m_count
+__global__ __launch_bounds__(256) void swiglu_reduce(const float* __restrict__ P, int S,
+                                                    size_t stride, const int* __restrict__ m_count,
+                                                    int n_max, int d_ff, bf16_t* __restrict__ act) {
+  const int M = min(*m_count, n_max);
+  const int q = d_ff / 8;
+  const size_t e = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int m = static_cast<int>(e / q), c = static_cast<int>(e % q) * 8;
+  if (m >= M) return;
+  const float* p = P + static_cast<size_t>(m) * 2 * d_ff + c;
+  f32x4 g0 = *reinterpret_cast<const f32x4*>(p), g1 = *reinterpret_cast<const f32x4*>(p + 4);
+  f32x4 u0 = *reinterpret_cast<const f32x4*>(p + d_ff), u1 = *reinterpret_cast<const f32x4*>(p + d_ff + 4);
+  for (int z = 1; z < S; ++z) {
+    const float* pz = p + z * stride;
+    g0 += *reinterpret_cast<const f32x4*>(pz);
+    g1 += *reinterpret_cast<const f32x4*>(pz + 4);
+    u0 += *reinterpret_cast<const f32x4*>(pz + d_ff);
+    u1 += *reinterpret_cast<const f32x4*>(pz + d_ff + 4);
+  }
+  u32x4 w;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float ga = i < 2 ? g0[2 * i] : g1[2 * i - 4], gb = i < 2 ? g0[2 * i + 1] : g1[2 * i - 3];
+    const float ua = i < 2 ? u0[2 * i] : u1[2 * i - 4], ub = i < 2 ? u0[2 * i + 1] : u1[2 * i - 3];
+    const float lo = ga * __builtin_amdgcn_rcpf(1.0f + __expf(-ga)) * ua;
+    const float hi = gb * __builtin_amdgcn_rcpf(1.0f + __expf(-gb)) * ub;
+    w[i] = static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+  }
+  *reinterpret_cast<u32x4*>(act + static_cast<size_t>(m) * d_ff + c) = w;
+}
+
+// h_out[t][n] = bf16(hbar[t][n] + g_t y) with y the sum over z < S of P[z][m][n], t = idx[m];
+// one thread per 8 columns of a row, rows m < *m_count
+__global__ __launch_bounds__(256) void scatter_reduce(const float* __restrict__ P, int S, size_t stride,
+                                                     const int* __restrict__ m_count, int n_max,
+                                                     const int* __restrict__ idx,
+                                                     const bf16_t* __restrict__ hbar,
+                                                     const float* __restrict__ gate,
+                                                     bf16_t* __restrict__ out, int d) {
+  const int M = min(*m_count, n_max);
+  const int q = d / 8;
+  const size_t e = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int m = static_cast<int>(e / q), n = static_cast<int>(e % q) * 8;
+  if (m >= M) return;
+  const float* p = P + static_cast<size_t>(m) * d + n;
+  f32x4 y0 = *reinterpret_cast<const f32x4*>(p), y1 = *reinterpret_cast<const f32x4*>(p + 4);
+  for (int z = 1; z < S; ++z) {
+    y0 += *reinterpret_cast<const f32x4*>(p + z * stride);
+    y1 += *reinterpret_cast<const f32x4*>(p + z * stride + 4);
+  }
+  const int t = idx[m];
+  const float sc = gate[t];
+  const size_t o = static_cast<size_t>(t) * d + n;
+  const u32x4 h = *reinterpret_cast<const u32x4*>(hbar + o);
+  u32x4 w;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float ya = i < 2 ? y0[2 * i] : y1[2 * i - 4], yb = i < 2 ? y0[2 * i + 1] : y1[2 * i - 3];
+    const float lo = __uint_as_float(h[i] << 16) + sc * ya;
+    const float hi = __uint_as_float(h[i] & 0xffff0000u) + sc * yb;
+    w[i] = static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+  }
+  *reinterpret_cast<u32x4*>(out + o) = w;
+}
+
+}  // namespace
+
+size_t ffn_part_floats(int dtype, int d, int d_ff, int T) {
+  if (dtype != 1 || T <= 0) return 0;
+  // S is fixed per row-tile count and the slices hold n rows: the largest n of each count
+  size_t most = 0;
+  for (int mt = 1; (mt - 1) * TileSplitGU::BM < T; ++mt) {
+    const int n = std::min(mt * TileSplitGU::BM, T);
+    const int sg = gateup_split(n, d, d_ff), sd = down_split(n, d, d_ff);
+    if (sg > 1) most = std::max(most, static_cast<size_t>(sg) * n * 2 * d_ff);
+    if (sd > 1) most = std::max(most, static_cast<size_t>(sd) * n * d);
+    if (sg == 1 && sd == 1) break;   // both counts only grow from here
+  }
+  return most;
+}
+
 hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const int* counts,
-                             int n_max, const void* w_gate, const void* w_up, void* act, int d,
-                             int d_ff, hipStream_t s) {
+                             int n_max, const void* w_gate, const void* w_up, void* act,
+                             float* part, int d, int d_ff, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(u), idx_ffn, d};
+    const int S = gateup_split(n_max, d, d_ff);
+    if (S > 1) {
+      BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), d_ff, d};
+      const size_t stride = static_cast<size_t>(n_max) * 2 * d_ff;
+      hipError_t e = run_tile<TileSplitGU>(A, B, EpiStoreF32{part, 2 * d_ff, stride}, counts, n_max,
+                                           2 * d_ff, d, s, S);
+      if (e != hipSuccess) return e;
+      const size_t n8 = static_cast<size_t>(n_max) * (d_ff / 8);
+      swiglu_reduce<<<static_cast<unsigned>((n8 + 255) / 256), 256, 0, s>>>(
+          part, S, stride, counts, n_max, d_ff, static_cast<bf16_t*>(act));
+      return hipGetLastError();
+    }
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), INT_MAX, d};
     return run_big<256, true>(A, B, EpiSwiGLU<bf16_t>{static_cast<bf16_t*>(act), d_ff}, counts,
                               n_max, d_ff, d, s);
@@ -927,11 +1051,23 @@ hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const
 
 hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const int* counts,
                            int n_max, const void* w_down, const void* hbar, const float* gate,
-                           void* h_out, int d, int d_ff, hipStream_t s) {
+                           void* h_out, float* part, int d, int d_ff, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(act), nullptr, d_ff};
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_down), nullptr, INT_MAX, d_ff};
+    const int S = down_split(n_max, d, d_ff);
+    if (S > 1) {
+      const size_t stride = static_cast<size_t>(n_max) * d;
+      hipError_t e = run_tile<TileSplitDown>(A, B, EpiStoreF32{part, d, stride}, counts, n_max, d,
+                                             d_ff, s, S);
+      if (e != hipSuccess) return e;
+      const size_t n8 = static_cast<size_t>(n_max) * (d / 8);
+      scatter_reduce<<<static_cast<unsigned>((n8 + 255) / 256), 256, 0, s>>>(
+          part, S, stride, counts, n_max, idx_ffn, static_cast<const bf16_t*>(hbar), gate,
+          static_cast<bf16_t*>(h_out), d);
+      return hipGetLastError();
+    }
     EpiScatter<bf16_t, false> epi{idx_ffn, static_cast<const bf16_t*>(hbar), gate,
                                   static_cast<bf16_t*>(h_out), d};
     return run_big<256, false>(A, B, epi, counts, n_max, d, d_ff, s);

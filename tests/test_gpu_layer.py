@@ -126,3 +126,17 @@ def test_persistent_gate_up_ragged():
     the next tile) with a row count that is not a multiple of the tile height."""
     w = BF16_SMALL.replace(d_ff=5120, T=2001, budget=0.27)
     _run(w, 3)
+
+
+def test_ffn_single_pass_tiles_ragged():
+    """Enough FFN rows that both products run K in one pass (more than half the CUs' worth of
+    output tiles), with a ragged row count; smaller cases split K and reduce partial sums."""
+    w = BF16_SMALL.replace(d=2048, d_ff=2816, T=2201, budget=0.27)
+    _run(w, 2, seed=7)
+
+
+def test_ffn_split_k_decode_rows():
+    """A decode-sized batch (one row tile): both FFN products split K into fp32 slices; the
+    row count is ragged and K splits unevenly (d_ff / 64 = 42 k-tiles over 16 slices)."""
+    w = BF16_SMALL.replace(d=1024, d_ff=2688, T=256, budget=0.27)
+    _run(w, 5, seed=8)
