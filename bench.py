@@ -327,17 +327,28 @@ def main():
 
     tokens_per_s = w.T / (ms_step * 1e-3)
     dflops = sum(wk[dom]["flops"] for wk in works)          # per step
-    achieved = dflops / (dom_ms_step * 1e-3) * 1e-12
-    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    dbytes = sum(wk[dom]["bytes"] for wk in works)
+    peak_f = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     n_launch_step = max(1, n_dom // K)
-    roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4),
+    # the tighter roof for this row count: MFMA for prefill-sized products, HBM for decode
+    # batches, whose weight bytes take longer at 8 TB/s than their FLOPs at the MFMA peak
+    hbm_bound = dbytes / (PEAK_HBM_GBS * 1e9) > dflops / (peak_f * 1e12)
+    if hbm_bound:
+        achieved, peak, unit = dbytes / (dom_ms_step * 1e-3) * 1e-9, PEAK_HBM_GBS, "GB/s"
+        per_unit = "weights 2*d*d_ff*2 B per launch + (d + d_ff)*2 B per FFN token"
+        total = f"{dbytes / 1e6:.1f} MB"
+    else:
+        achieved, peak, unit = dflops / (dom_ms_step * 1e-3) * 1e-12, peak_f, "TFLOP/s"
+        per_unit = "4*d*d_ff FLOP per FFN token"
+        total = f"{dflops / 1e9:.1f} GFLOP"
+    roof = {"bound": "hbm" if hbm_bound else "mfma", "achieved": round(achieved, 1), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 4),
             "traffic": counted_traffic(dom) if args.workload == "llama31_8b_layer" and args.memory == "matrix" else None,
             "kernel": dom, "avg_launch_us": round(dom_ms_step * 1e3 / n_launch_step, 2),
-            "work_per_launch": (f"4*d*d_ff FLOP per FFN token x {n_f} FFN tokens = {dflops / 1e9:.1f} GFLOP"
+            "work_per_launch": (f"{per_unit} x {n_f} FFN tokens = {total}"
                                 if not stack else
-                                f"4*d*d_ff FLOP per FFN token x {sum(nfs)} FFN tokens over {L} layers = "
-                                f"{dflops / 1e9:.1f} GFLOP per step, {n_launch_step} launches"),
+                                f"{per_unit} x {sum(nfs)} FFN tokens over {L} layers = "
+                                f"{total} per step, {n_launch_step} launches"),
             "traffic_note": "HBM bytes read + written per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1, "
                             "calibrated on a 1 GiB copy) from profiles/, null if the GEMM changed since or "
                             "for workloads the counters were not taken on"}

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define HERO_ABI_VERSION 2
+#define HERO_ABI_VERSION 3
 
 typedef enum hero_status {
   HERO_OK = 0,
@@ -125,12 +125,36 @@ typedef struct hero_state {
   float *m_hist;  /* [T]           */
 } hero_state;
 
+/*
+ * Router ablations (Table 3, Sec. 4.3), a bit set in
+ * hero_routing.ablation; 0 is the full router.  Readings of the paper's one-line
+ * descriptions:
+ *   NO_POS_STATE  the path vector loses the routing-progress and residual-transition
+ *                 features: r = q_rem = d = gamma = 0, p and m stay;
+ *   NO_AUX_STATE  no auxiliary path encoder: z_a = 0, so s = [z_h; 0];
+ *   NO_MEMREAD    the history head keeps its inputs but not the memory: c = 0 and
+ *                 nu = 0 (as at the first routed block) at every layer; S and zeta are
+ *                 neither read nor written (their buffers are left as passed);
+ *   NO_HISTORY    no history branch: logit = b (+ bias), a is not formed, p = m = 1 are
+ *                 written (the initial scores); S and zeta are left as passed.
+ * Bits combine; NO_HISTORY implies NO_MEMREAD's treatment of the memory.
+ */
+typedef enum hero_ablation {
+  HERO_ABL_NO_POS_STATE = 1,
+  HERO_ABL_NO_AUX_STATE = 2,
+  HERO_ABL_NO_MEMREAD = 4,
+  HERO_ABL_NO_HISTORY = 8,
+  HERO_ABL_ALL = 15
+} hero_ablation;
+
 typedef struct hero_routing {
   int mode;                 /* hero_mode                                                */
   float tau;                /* threshold mode: tau_exec in (0,1)                        */
   double budget;            /* budget mode: skip fraction in [0,1]                      */
   const float *logit_bias;  /* optional device [T] fp32 added to the gate logit only;
                                NULL = none                                               */
+  int ablation;             /* hero_ablation bits, 0 = full router; other bits are
+                               rejected with HERO_E_RANGE                                */
 } hero_routing;
 
 /*

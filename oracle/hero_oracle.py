@@ -35,7 +35,14 @@ constant here):
   * at layer j = 1 the state is the paper's initial value (S = 0, zeta = 0,
     p = m = 1) whatever the incoming buffers hold;
   * hidden-state outputs are rounded to the storage dtype (bfloat16 nearest-even
-    for bf16 workloads) at every layer boundary; nothing else is rounded.
+    for bf16 workloads) at every layer boundary; nothing else is rounded;
+  * the component ablations of Table 3 (Sec. 4.3) are a bit set ``ablation``:
+    w/o Pos State zeroes the routing-progress and residual-transition features
+    (r, q_rem, d, gamma) of the path vector; w/o Aux State drops the path
+    encoder (z_a = 0); w/o MemRead keeps the history head but gives it no memory
+    (c = 0 and nu = 0 at every layer, as at the first routed block) and leaves S,
+    zeta as they came in; w/o History removes the history branch (a = 0, so the
+    logit is the local one), writes p = m = 1 and leaves S, zeta as they came in.
 """
 from __future__ import annotations
 
@@ -315,6 +322,9 @@ def memory_from_pairs(phik, v, rho):
 # Sec. 3.2  HeRo router: gate computation
 # ---------------------------------------------------------------------------
 
+# Component ablations of Table 3 (bits of ``ablation``)
+NO_POS_STATE, NO_AUX_STATE, NO_MEMREAD, NO_HISTORY = 1, 2, 4, 8
+
 
 def history_dissimilarity(j, s, c, R: RouterParams, eps):
     """nu = 1 - cos(W_n s, W_c c) for j > 1, nu = 0 at the first routed layer."""
@@ -404,7 +414,8 @@ class LayerResult:
 def routed_layer(j, dims: Dims, hbar, hbar_prev1, hbar_prev2, state: State,
                  ffn: FFNParams, R: RouterParams, ad: AdapterParams, eta,
                  mode="budget", budget=0.0, tau=0.5, beta=None,
-                 forced_ffn=None, round_output=True, compute_rows=None, lam_given=None):
+                 forced_ffn=None, round_output=True, compute_rows=None, lam_given=None,
+                 ablation=0):
     """Routed layer l_j for a batch of tokens, in the order of Sec. 3 (overview paragraph).
 
     ``forced_ffn`` (bool [T]) makes the branch follow a given decision (teacher
@@ -412,7 +423,8 @@ def routed_layer(j, dims: Dims, hbar, hbar_prev1, hbar_prev2, state: State,
     (bool [T]) restricts the expensive branch evaluation to those rows; other
     rows of ``h`` are left as NaN.  ``lam_given`` (budget mode on a subset of a
     larger batch) replaces the subset's own quantile: a token's own decision is
-    then FFN iff its float32 logit >= lam_given.
+    then FFN iff its float32 logit >= lam_given.  ``ablation`` selects a Table 3
+    router variant (bits NO_POS_STATE, NO_AUX_STATE, NO_MEMREAD, NO_HISTORY).
     """
     hbar = np.asarray(hbar, dtype=f64)
     T = hbar.shape[0]
@@ -422,17 +434,30 @@ def routed_layer(j, dims: Dims, hbar, hbar_prev1, hbar_prev2, state: State,
     z_h = hidden_encoder(hbar, R, dims)
     d_j, gamma_j = residual_transitions(j, hbar, hbar_prev1, hbar_prev2, dims.eps)
     x_path = path_vector(j, dims.L_R, d_j, gamma_j, state.p_hist, state.m_hist)
+    if ablation & NO_POS_STATE:
+        x_path = x_path.copy()
+        x_path[:, :4] = 0.0
     z_a = path_encoder(x_path, R)
+    if ablation & NO_AUX_STATE:
+        z_a = np.zeros_like(z_a)
     s = router_state(z_h, z_a)
     # memory: read before write
     q, k, v = memory_projections(s, R)
-    c = memory_read(q, state.S, state.zeta, dims.eps)
     rho = float(sigmoid(np.array([eta]))[0])
-    S_new, zeta_new = memory_write(k, v, state.S, state.zeta, rho)
+    if ablation & (NO_MEMREAD | NO_HISTORY):
+        c = np.zeros_like(q)
+        S_new, zeta_new = state.S.copy(), state.zeta.copy()
+        nu = np.zeros(T)
+    else:
+        c = memory_read(q, state.S, state.zeta, dims.eps)
+        S_new, zeta_new = memory_write(k, v, state.S, state.zeta, rho)
+        nu = history_dissimilarity(j, s, c, R, dims.eps)
     # gate
-    nu = history_dissimilarity(j, s, c, R, dims.eps)
-    a, p = history_head(s, c, nu, R, dims.T_hist)
-    m = cumulative_history(state.m_hist, p)
+    if ablation & NO_HISTORY:
+        a, p, m = np.zeros(T), np.ones(T), np.ones(T)
+    else:
+        a, p = history_head(s, c, nu, R, dims.T_hist)
+        m = cumulative_history(state.m_hist, p)
     b = local_head(hbar, R)
     ell, g = execution_gate(a, b, beta)
     # decision
@@ -473,7 +498,7 @@ class StackResult:
 
 def routed_stack(dims: Dims, h_in, ffns: List[FFNParams], R: RouterParams,
                  adapters: List[AdapterParams], etas, mode="budget", budget=0.0, tau=0.5,
-                 beta=None, forced_ffn=None, lam_given=None):
+                 beta=None, forced_ffn=None, lam_given=None, ablation=0):
     """L_R routed layers with zero initial state; hbar_{j+1} = h_j between them.
 
     ``forced_ffn`` is an optional list (one bool [T] per layer) for teacher
@@ -490,7 +515,7 @@ def routed_stack(dims: Dims, h_in, ffns: List[FFNParams], R: RouterParams,
         lg = None if lam_given is None else lam_given[j - 1]
         res = routed_layer(j, dims, hbar, hist[0], hist[1], state, ffns[j - 1], R,
                            adapters[j - 1], etas[j - 1], mode, budget, tau, beta, ff,
-                           lam_given=lg)
+                           lam_given=lg, ablation=ablation)
         layers.append(res)
         state = res.state
         hist = [hbar, hist[0]]

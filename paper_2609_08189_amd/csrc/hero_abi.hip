@@ -11,6 +11,10 @@
 #include "../../include/hero.h"
 #include "hero_kernels.h"
 
+static_assert(HERO_ABL_NO_POS_STATE == hero::ABL_NO_POS && HERO_ABL_NO_AUX_STATE == hero::ABL_NO_AUX &&
+                  HERO_ABL_NO_MEMREAD == hero::ABL_NO_MEMREAD && HERO_ABL_NO_HISTORY == hero::ABL_NO_HISTORY,
+              "ablation bits of the ABI and the kernels agree");
+
 namespace {
 
 constexpr size_t kAlign = 256;
@@ -92,6 +96,7 @@ int check_routing(const hero_routing* r) {
   } else {
     return HERO_E_RANGE;
   }
+  if (r->ablation & ~HERO_ABL_ALL) return HERO_E_RANGE;
   if (r->logit_bias && !aligned16(r->logit_bias)) return HERO_E_ALIGN;
   return HERO_OK;
 }
@@ -259,6 +264,7 @@ int run_layer(const LayerCall& c) {
   ra.th2 = c.rt->th2;
   ra.ps2 = c.rt->ps2;
   ra.beta = c.rc->logit_bias;
+  ra.abl = c.rc->ablation;
   if (c.hist) {
     ra.kv = c.hist->kv;
     ra.p_hist = c.hist->p_hist;
@@ -282,10 +288,13 @@ int run_layer(const LayerCall& c) {
   }
   e = timed(HERO_K_ROUTER_PRE, st, [&] { return launch_router_pre(ra, st); });
   if (e != hipSuccess) return HERO_E_LAUNCH;
-  e = timed(HERO_K_ROUTER_MEM, st, [&] {
-    return c.hist ? launch_router_mem_hist(ra, st) : launch_router_mem(ra, st);
-  });
-  if (e != hipSuccess) return HERO_E_LAUNCH;
+  // the ablations without memory access leave S, zeta (or the stored pairs) untouched
+  if (!(ra.abl & (HERO_ABL_NO_MEMREAD | HERO_ABL_NO_HISTORY))) {
+    e = timed(HERO_K_ROUTER_MEM, st, [&] {
+      return c.hist ? launch_router_mem_hist(ra, st) : launch_router_mem(ra, st);
+    });
+    if (e != hipSuccess) return HERO_E_LAUNCH;
+  }
   e = timed(HERO_K_ROUTER_POST, st, [&] { return launch_router_post(ra, st); });
   if (e != hipSuccess) return HERO_E_LAUNCH;
 

@@ -6,6 +6,9 @@
 
 namespace hero {
 
+// router ablation bits (the values of the C ABI's hero_ablation)
+constexpr int ABL_NO_POS = 1, ABL_NO_AUX = 2, ABL_NO_MEMREAD = 4, ABL_NO_HISTORY = 8;
+
 // Row statistics of the post-attention states and the FFN input:
 //   rowstat[t] = {1/rms(hbar_t), |delta_j|^2, <delta_j, delta_{j-1}>, |delta_{j-1}|^2}
 //   u[t] = RMSNorm_w(hbar_t) in the storage dtype.
@@ -30,6 +33,7 @@ struct RouterTailArgs {
   const void *w_hu, *w_p1, *w_p2, *w_q, *w_k, *w_v, *w_n, *w_c, *th1, *th2, *ps2;
   int ld_th1;             // row pitch of th1 (elements)
   const float* beta;      // [T] or null
+  int abl;                // router ablation bits (ABL_*)
   float* S;               // [T][d_m][d_m]   in/out
   float* zeta;            // [T][d_m]        in/out
   float* p_hist;          // [T]             in/out

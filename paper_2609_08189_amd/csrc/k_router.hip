@@ -16,6 +16,10 @@
 //     logit = a + b (+ bias),  g = sigma(logit)
 // At j = 1 the incoming state is the paper's initial value: S and zeta are not read
 // (taken as zero) and p_0 = m_0 = 1.
+// Router ablations (Table 3): without the position state the first four path features are
+// zero; without the auxiliary state z^a = 0; without the memory read (or the whole history
+// branch) router_mem is not launched, c = 0 and nu = 0 at every layer; without the history
+// branch a = 0, so logit = b (+ bias), and p = m = 1 are written.
 // The memory kernel moves 2 * 4 * (d_m^2 + d_m) bytes of state per token and is the
 // HBM-bound part; keeping it free of the matrix-vector work lets many workgroups per
 // CU keep HBM busy.  All arithmetic is fp32.
@@ -225,10 +229,11 @@ __global__ __launch_bounds__(NT) void router_pre_kernel(RouterTailArgs a) {
     }
     const float dj = j >= 2 ? sqrtf(dd) : 0.f;
     const float gam = j >= 3 ? dp / (dj * sqrtf(pp) + a.eps) : 0.f;
-    xp[tid][0] = static_cast<float>(j) / static_cast<float>(a.L_R);
-    xp[tid][1] = static_cast<float>(a.L_R - j) / static_cast<float>(a.L_R);
-    xp[tid][2] = dj;
-    xp[tid][3] = gam;
+    const bool pos = !(a.abl & ABL_NO_POS);
+    xp[tid][0] = pos ? static_cast<float>(j) / static_cast<float>(a.L_R) : 0.f;
+    xp[tid][1] = pos ? static_cast<float>(a.L_R - j) / static_cast<float>(a.L_R) : 0.f;
+    xp[tid][2] = pos ? dj : 0.f;
+    xp[tid][3] = pos ? gam : 0.f;
     xp[tid][4] = pprev;
     xp[tid][5] = mprev;
     sc[tid] = inv_rms;
@@ -251,8 +256,12 @@ __global__ __launch_bounds__(NT) void router_pre_kernel(RouterTailArgs a) {
   matvec(static_cast<const W*>(a.ps2), d_head, 1, d_head, &bufB[0][0], EP, a.bvec + t0, 1, Ident(),
          nvalid);
   __syncthreads();
-  matvec(static_cast<const W*>(a.w_p2), a.d_p, a.d_a, a.d_p, &zp[0][0], MAXP, &s[0][a.d_h], MAXS + 4,
-         Ident());
+  if (a.abl & ABL_NO_AUX) {
+    for (int e = tid; e < TB * a.d_a; e += NT) s[e / a.d_a][a.d_h + e % a.d_a] = 0.f;
+  } else {
+    matvec(static_cast<const W*>(a.w_p2), a.d_p, a.d_a, a.d_p, &zp[0][0], MAXP, &s[0][a.d_h], MAXS + 4,
+           Ident());
+  }
   __syncthreads();
   const int d_s = a.d_s;
   float* qkvn = a.qkvn + static_cast<size_t>(t0) * 4 * DM;
@@ -367,8 +376,10 @@ __global__ __launch_bounds__(NT) void router_post_kernel(RouterTailArgs a) {
   const int j = a.j;
   const int DM = a.d_m, d_head = a.d_head, d_s = a.d_s;
   auto tok = [&](int tt) { return static_cast<size_t>(min(t0 + tt, a.T - 1)); };
+  // a memory context exists after the first layer unless an ablation removes the memory
+  const bool ctx = j > 1 && !(a.abl & (ABL_NO_MEMREAD | ABL_NO_HISTORY));
   batched(
-      TB * DM, [&](int e) { return a.cvec[tok(e / DM) * DM + e % DM]; },
+      TB * DM, [&](int e) { return ctx ? a.cvec[tok(e / DM) * DM + e % DM] : 0.f; },
       [&](int e, float v) { cx[e / DM][e % DM] = v; });
   batched(
       TB * DM, [&](int e) { return a.qkvn[tok(e / DM) * 4 * DM + 3 * DM + e % DM]; },
@@ -390,7 +401,7 @@ __global__ __launch_bounds__(NT) void router_post_kernel(RouterTailArgs a) {
     nn = wave_sum(nn);
     cc = wave_sum(cc);
     nc = wave_sum(nc);
-    if (lane == 0) cx[tt][DM] = j > 1 ? 1.0f - nc / (sqrtf(nn) * sqrtf(cc) + a.eps) : 0.f;
+    if (lane == 0) cx[tt][DM] = ctx ? 1.0f - nc / (sqrtf(nn) * sqrtf(cc) + a.eps) : 0.f;
   }
   __syncthreads();
   // the [c; nu] columns of the history head's input layer on top of its s part, then SiLU
@@ -400,11 +411,12 @@ __global__ __launch_bounds__(NT) void router_post_kernel(RouterTailArgs a) {
   __syncthreads();
   if (tid < nvalid) {
     const int t = t0 + tid;
-    const float av = sc[tid];
+    const bool hist = !(a.abl & ABL_NO_HISTORY);
+    const float av = hist ? sc[tid] : 0.f;
     const float mprev = j > 1 ? a.m_hist[t] : 1.0f;
     const float p = sigmoidf_(av / a.T_hist);
-    a.p_hist[t] = p;
-    a.m_hist[t] = mprev * p;
+    a.p_hist[t] = hist ? p : 1.0f;
+    a.m_hist[t] = hist ? mprev * p : 1.0f;
     const float l = av + a.bvec[t] + (a.beta ? a.beta[t] : 0.f);
     a.logit[t] = l;
     a.gate[t] = sigmoidf_(l);
@@ -555,10 +567,11 @@ __global__ __launch_bounds__(NTP) void router_pre_mfma(RouterTailArgs a) {
     }
     const float dj = j >= 2 ? sqrtf(dd) : 0.f;
     const float gam = j >= 3 ? dp / (dj * sqrtf(pp) + a.eps) : 0.f;
-    xp[tid][0] = static_cast<float>(j) / static_cast<float>(a.L_R);
-    xp[tid][1] = static_cast<float>(a.L_R - j) / static_cast<float>(a.L_R);
-    xp[tid][2] = dj;
-    xp[tid][3] = gam;
+    const bool pos = !(a.abl & ABL_NO_POS);
+    xp[tid][0] = pos ? static_cast<float>(j) / static_cast<float>(a.L_R) : 0.f;
+    xp[tid][1] = pos ? static_cast<float>(a.L_R - j) / static_cast<float>(a.L_R) : 0.f;
+    xp[tid][2] = pos ? dj : 0.f;
+    xp[tid][3] = pos ? gam : 0.f;
     xp[tid][4] = pprev;
     xp[tid][5] = mprev;
     sc[tid] = inv_rms;
@@ -632,7 +645,8 @@ __global__ __launch_bounds__(NTP) void router_pre_mfma(RouterTailArgs a) {
     for (int e = tid; e < MT * d_a; e += NTP) {
       const int t = e / d_a, o = e % d_a;
       float acc = 0.f;
-      for (int k = 0; k < d_p; ++k) acc = fmaf(ldf(w2 + o * d_p + k), hp[t][k], acc);
+      if (!(a.abl & ABL_NO_AUX))
+        for (int k = 0; k < d_p; ++k) acc = fmaf(ldf(w2 + o * d_p + k), hp[t][k], acc);
       s[t][d_h + o] = acc;
     }
   }
@@ -705,12 +719,15 @@ __global__ __launch_bounds__(NTP) void router_post_mfma(RouterTailArgs a) {
   const bf16_t* w_c = static_cast<const bf16_t*>(a.w_c);
   const int ld = a.ld_th1, nct_h = d_head / 16;
 
+  // a memory context exists after the first layer unless an ablation removes the memory
+  const bool ctx = j > 1 && !(a.abl & (ABL_NO_MEMREAD | ABL_NO_HISTORY));
   // c rows as split fragments, and W_n s
   for (int e = tid; e < MT * 4 * KSM; e += NTP) {
     const int i = e & 15, g = (e >> 4) & 3, st = e >> 6;
     const float* src = a.cvec + tok(i) * DM + 32 * st + 8 * g;
-    const f32x4 lo4 = *reinterpret_cast<const f32x4*>(src);
-    const f32x4 hi4 = *reinterpret_cast<const f32x4*>(src + 4);
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    const f32x4 lo4 = ctx ? *reinterpret_cast<const f32x4*>(src) : zero;
+    const f32x4 hi4 = ctx ? *reinterpret_cast<const f32x4*>(src + 4) : zero;
     float x[8];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -776,7 +793,7 @@ __global__ __launch_bounds__(NTP) void router_post_mfma(RouterTailArgs a) {
     nn = wave_sum(nn);
     cc = wave_sum(cc);
     nc = wave_sum(nc);
-    if (lane == 0) nu[i] = j > 1 ? 1.0f - nc / (sqrtf(nn) * sqrtf(cc) + a.eps) : 0.f;
+    if (lane == 0) nu[i] = ctx ? 1.0f - nc / (sqrtf(nn) * sqrtf(cc) + a.eps) : 0.f;
   }
   __syncthreads();
 
@@ -806,13 +823,15 @@ __global__ __launch_bounds__(NTP) void router_post_mfma(RouterTailArgs a) {
   __syncthreads();
   if (tid < nvalid) {
     const int t = t0 + tid;
+    const bool hist = !(a.abl & ABL_NO_HISTORY);
     float av = 0.f;
 #pragma unroll
     for (int w = 0; w < NWP; ++w) av += apart[w][tid];
+    if (!hist) av = 0.f;
     const float mprev = j > 1 ? a.m_hist[t] : 1.0f;
     const float p = sigmoidf_(av / a.T_hist);
-    a.p_hist[t] = p;
-    a.m_hist[t] = mprev * p;
+    a.p_hist[t] = hist ? p : 1.0f;
+    a.m_hist[t] = hist ? mprev * p : 1.0f;
     const float l = av + a.bvec[t] + (a.beta ? a.beta[t] : 0.f);
     a.logit[t] = l;
     a.gate[t] = sigmoidf_(l);

@@ -113,7 +113,8 @@ class DeviceProblem:
         self.beta = torch.from_numpy(prob.beta).to(device) if prob.beta is not None else None
         mode = H.HERO_MODE_BUDGET if w.mode == "budget" else H.HERO_MODE_THRESHOLD
         self.routing_s = H.hero_routing(mode, w.tau, w.budget,
-                                        self.beta.data_ptr() if self.beta is not None else None)
+                                        self.beta.data_ptr() if self.beta is not None else None,
+                                        w.ablation)
         if for_stack is None:
             for_stack = w.layer_j <= 0      # a stack workload (a layer workload names its j)
         self.for_stack = for_stack

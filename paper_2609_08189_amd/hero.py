@@ -14,6 +14,7 @@ from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhero.so")
+ABI_VERSION = 3          # the struct layouts below follow include/hero.h of this version
 
 HERO_OK = 0
 HERO_E_NULL = 1
@@ -31,6 +32,10 @@ HERO_F32 = 0
 HERO_BF16 = 1
 HERO_MODE_THRESHOLD = 0
 HERO_MODE_BUDGET = 1
+HERO_ABL_NO_POS_STATE = 1
+HERO_ABL_NO_AUX_STATE = 2
+HERO_ABL_NO_MEMREAD = 4
+HERO_ABL_NO_HISTORY = 8
 
 KERNELS = ("rowstats", "router_gemm", "router_pre", "router_mem", "router_post", "select",
            "ffn_gate_up", "ffn_down", "adapter_down", "adapter_up")
@@ -73,7 +78,7 @@ class hero_history(ctypes.Structure):
 
 class hero_routing(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int), ("tau", ctypes.c_float), ("budget", ctypes.c_double),
-                ("logit_bias", _vp)]
+                ("logit_bias", _vp), ("ablation", ctypes.c_int)]
 
 
 class hero_layer_stats(ctypes.Structure):
@@ -96,6 +101,9 @@ def lib() -> ctypes.CDLL:
         L.hero_status_string.argtypes = [ctypes.c_int]
         L.hero_abi_version.restype = ctypes.c_int
         L.hero_abi_version.argtypes = []
+        if L.hero_abi_version() != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI version {L.hero_abi_version()}, the binding "
+                               f"expects {ABI_VERSION}: rebuild it with __graft_entry__.build()")
         L.hero_kernel_timer.restype = ctypes.c_int
         L.hero_kernel_timer.argtypes = [ctypes.c_int, P(_vp), P(_vp), ctypes.c_int]
         L.hero_workspace_size.restype = ctypes.c_int

@@ -69,6 +69,9 @@ class Workload:
     eps_norm: float = 1e-5
     eps: float = 1e-6
     T_hist: float = 0.9
+    # router variant of Table 3: bits 1 w/o Pos State, 2 w/o Aux State, 4 w/o MemRead,
+    # 8 w/o History (0 = the full router)
+    ablation: int = 0
 
     @property
     def d_c(self) -> int:

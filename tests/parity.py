@@ -79,7 +79,8 @@ def oracle_layer(prob, j, forced_ffn=None, rows=None, lam_given=None):
                           router_of(prob), adapter_of(prob.adapter[0]), float(prob.eta[j - 1]),
                           mode=w.mode, budget=w.budget, tau=w.tau,
                           beta=None if prob.beta is None else prob.beta.astype(np.float64),
-                          forced_ffn=forced_ffn, compute_rows=rows, lam_given=lam_given)
+                          forced_ffn=forced_ffn, compute_rows=rows, lam_given=lam_given,
+                          ablation=w.ablation)
 
 
 def check_layer(prob, gpu_res, j, rows=None, report=None):
@@ -99,12 +100,20 @@ def check_layer(prob, gpu_res, j, rows=None, report=None):
         lam_ref = ref.lam
     n_band = compare_decisions(w, L, ref, lam_ref)
     sel = np.arange(T) if rows is None else np.nonzero(rows)[0]
+    if w.ablation & (O.NO_MEMREAD | O.NO_HISTORY):
+        # no memory access: the buffers must come back exactly as they went in
+        # (the oracle's own S, zeta are its initial zeros at j = 1)
+        assert np.array_equal(gpu_res["S"], prob.S), "S was written"
+        assert np.array_equal(gpu_res["zeta"], prob.zeta), "zeta was written"
+        S_ref, zeta_ref = prob.S.astype(np.float64), prob.zeta.astype(np.float64)
+    else:
+        S_ref, zeta_ref = ref.state.S, ref.state.zeta
     errs = dict(
         logit=scalar_err(L["logit"], ref.logit),
         gate=scalar_err(L["gate"], ref.gate),
         h=row_rel_err(gpu_res["h"][sel], ref.h[sel]),
-        S=row_rel_err(gpu_res["S"], ref.state.S),
-        zeta=row_rel_err(gpu_res["zeta"], ref.state.zeta),
+        S=row_rel_err(gpu_res["S"], S_ref),
+        zeta=row_rel_err(gpu_res["zeta"], zeta_ref),
         p=scalar_err(gpu_res["p_hist"], ref.state.p_hist),
         m=scalar_err(gpu_res["m_hist"], ref.state.m_hist),
         band_flips=n_band, n_ffn=L["n_ffn"],
@@ -149,7 +158,13 @@ def check_stack(prob, gpu_res, rows=None, report=None):
     ref = O.routed_stack(dims_of(w), prob.hbar.f64[sel], _LazyMap(prob.ffn, ffn_of), router_of(prob),
                          _LazyMap(prob.adapter, adapter_of), prob.eta.astype(np.float64),
                          mode=w.mode, budget=w.budget, tau=w.tau, beta=beta,
-                         forced_ffn=forced, lam_given=lam_given)
+                         forced_ffn=forced, lam_given=lam_given, ablation=w.ablation)
+    if w.ablation & (O.NO_MEMREAD | O.NO_HISTORY):
+        # no memory access: the caller's buffers come back exactly as they went in
+        assert np.array_equal(gpu_res["S"], prob.S) and np.array_equal(gpu_res["zeta"], prob.zeta)
+        S_ref, zeta_ref = prob.S[sel].astype(np.float64), prob.zeta[sel].astype(np.float64)
+    else:
+        S_ref, zeta_ref = ref.state.S, ref.state.zeta
     n_band = 0
     errs = dict(logit=0.0, gate=0.0)
     for L, R in zip(layers, ref.layers):
@@ -166,8 +181,8 @@ def check_stack(prob, gpu_res, rows=None, report=None):
         n_band += int(mism.sum())
         errs["logit"] = max(errs["logit"], scalar_err(L["logit"][sel], R.logit))
         errs["gate"] = max(errs["gate"], scalar_err(L["gate"][sel], R.gate))
-    errs.update(h=row_rel_err(gpu_res["h"][sel], ref.h), S=row_rel_err(gpu_res["S"][sel], ref.state.S),
-                zeta=row_rel_err(gpu_res["zeta"][sel], ref.state.zeta),
+    errs.update(h=row_rel_err(gpu_res["h"][sel], ref.h), S=row_rel_err(gpu_res["S"][sel], S_ref),
+                zeta=row_rel_err(gpu_res["zeta"][sel], zeta_ref),
                 p=scalar_err(gpu_res["p_hist"][sel], ref.state.p_hist),
                 m=scalar_err(gpu_res["m_hist"][sel], ref.state.m_hist), band_flips=n_band)
     if report is not None:

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_function():
     lib = H.lib()
     for n in names:
         assert hasattr(lib, n), f"{n} declared in include/hero.h but not exported"
-    assert H.hero_abi_version() == 2
+    assert H.hero_abi_version() == H.ABI_VERSION == 3
 
 
 def test_status_strings():
@@ -145,6 +145,8 @@ def test_argument_validation():
     (H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 1.5, None), H.HERO_E_RANGE),
     (H.hero_routing(5, 0.5, 0.5, None), H.HERO_E_RANGE),
     (H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.5, FAKE + 6), H.HERO_E_ALIGN),
+    (H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.5, None, 16), H.HERO_E_RANGE),     # unknown ablation bit
+    (H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.5, None, -1), H.HERO_E_RANGE),
 ])
 def test_routing_validation(routing, status):
     assert call_layer(routing=routing) == status
