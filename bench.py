@@ -228,6 +228,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama31_8b_layer")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--budget", type=float, default=None,
+                    help="skip budget in place of the workload's own (budget-mode workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-target-s", type=float, default=12.0)
     ap.add_argument("--memory", choices=("matrix", "history"), default="matrix",
@@ -255,6 +257,10 @@ def main():
     from paper_2609_08189_amd.device import DeviceProblem
 
     w = synth.WORKLOADS[args.workload]
+    if args.budget is not None:
+        if w.mode != "budget" or not 0.0 <= args.budget <= 1.0:
+            sys.exit("--budget needs a budget-mode workload and a fraction in [0, 1]")
+        w = w.replace(budget=args.budget)
     stack = w.layer_j <= 0          # a stack workload: a step is one hero_routed_stack call
     j = w.layer_j
     L = w.L_R if stack else 1       # routed layers per step
@@ -343,7 +349,8 @@ def main():
         total = f"{dflops / 1e9:.1f} GFLOP"
     roof = {"bound": "hbm" if hbm_bound else "mfma", "achieved": round(achieved, 1), "peak": peak,
             "unit": unit, "frac": round(achieved / peak, 4),
-            "traffic": counted_traffic(dom) if args.workload == "llama31_8b_layer" and args.memory == "matrix" else None,
+            "traffic": counted_traffic(dom) if (args.workload == "llama31_8b_layer" and args.memory == "matrix"
+                                                  and args.budget is None) else None,
             "kernel": dom, "avg_launch_us": round(dom_ms_step * 1e3 / n_launch_step, 2),
             "work_per_launch": (f"{per_unit} x {n_f} FFN tokens = {total}"
                                 if not stack else

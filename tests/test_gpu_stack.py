@@ -85,15 +85,17 @@ def test_stack_equals_chained_layer_calls():
         assert h["lam"] == b["lam"] and h["n_ffn"] == b["n_ffn"]
 
 
-def test_llama2_7b_decode_stack_full_shape():
-    """Llama-2-7B shape, 32 routed layers, 256 sequences x 1 token, 27 % skip; every token.
-    The stack is rerun as chained layer calls (bit-identical to it, captured per layer) and
-    each layer is checked on the GPU's own inputs, so bf16 rounding cannot compound."""
+@pytest.mark.parametrize("budget", [0.0, 0.27, 0.39])
+def test_llama2_7b_decode_stack_full_shape(budget):
+    """Llama-2-7B shape, 32 routed layers, 256 sequences x 1 token, skip swept over 0, 27 and
+    39 %; every token.  The stack is rerun as chained layer calls (bit-identical to it,
+    captured per layer) and each layer is checked on the GPU's own inputs, so bf16 rounding
+    cannot compound."""
     import torch
     from paper_2609_08189_amd.device import DeviceProblem
     from tests.parity import check_stack_layerwise
-    w = synth.WORKLOADS["llama2_7b_decode"]
-    print(f"case {w.name} L_R={w.L_R} T={w.T}", flush=True)
+    w = synth.WORKLOADS["llama2_7b_decode"].replace(budget=budget)
+    print(f"case {w.name} L_R={w.L_R} T={w.T} budget={budget}", flush=True)
     prob = synth.make_problem(w, seed=0)
     dp = DeviceProblem(prob)
     dp.run_stack()
