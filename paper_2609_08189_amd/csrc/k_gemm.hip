@@ -616,11 +616,13 @@ hipError_t run_tile(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_coun
   return hipGetLastError();
 }
 
-// Number of 256-CU rounds times the tile height: proportional to the time of a
-// launch whose tiles all cost the same per row.
-int tile_cost(int M, int BM, int n_tiles) {
+// Time of a launch in units of one round of 192-row tiles: CU rounds times the relative
+// duration of a round.  A 256-row tile moves fewer bytes through L2 per FLOP, so its round
+// takes ~1.23x (not 256/192 = 1.33x) a 192-row round on the FFN products (measured on the
+// Llama-3.1-8B gate/up and down shapes at 3k-20k rows).
+double tile_cost(int M, int BM, int n_tiles) {
   const int tiles = (M + BM - 1) / BM * n_tiles;
-  return (tiles + 255) / 256 * BM;
+  return static_cast<double>((tiles + kCUs - 1) / kCUs) * (BM == 256 ? 1.23 : 1.0);
 }
 
 // Big-tile launch: 256 or 192 rows per tile, whichever finishes in fewer CU-rounds.
