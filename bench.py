@@ -63,17 +63,18 @@ class HipEvents:
 
 
 def kernel_work(w, n_f, n_a, T, j, memory="matrix"):
-    """Algorithmic FLOPs and HBM bytes per launch of each kernel (bf16 I/O, fp32 state).
+    """Algorithmic FLOPs and HBM bytes per launch of each kernel (bf16 I/O, fp32 or bf16 S).
     The memory pass moves S and zeta (read unless j = 1, written) in matrix form, or reads the
     j-1 stored (phi(k), v) pairs and writes one in depth-history form."""
     es = 2 if w.dtype == "bf16" else 4
+    ss = 2 if w.state_dtype == "bf16" else 4
     d, dff, r, dm = w.d, w.d_ff, w.d_r, w.d_m
     npre = w.d_e + w.d_head
     hid_reads = 1 + (j >= 2) + (j >= 3)
     if memory == "history":
         state_rw = 4 * 2 * dm * ((j - 1) + 1)
     else:
-        state_rw = (2 if j > 1 else 1) * 4 * (dm * dm + dm)
+        state_rw = (2 if j > 1 else 1) * (ss * dm * dm + 4 * dm)
     return {
         "rowstats": dict(flops=0, bytes=T * (hid_reads * d * es + d * es + 16)),
         "router_gemm": dict(flops=2 * d * npre * T, bytes=T * (d * es + 4 * npre)),
@@ -228,6 +229,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama31_8b_layer")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--state", choices=("f32", "bf16"), default="f32",
+                    help="storage of the router memory S between layers")
     ap.add_argument("--budget", type=float, default=None,
                     help="skip budget in place of the workload's own (budget-mode workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -261,6 +264,10 @@ def main():
         if w.mode != "budget" or not 0.0 <= args.budget <= 1.0:
             sys.exit("--budget needs a budget-mode workload and a fraction in [0, 1]")
         w = w.replace(budget=args.budget)
+    if args.state == "bf16":
+        if args.memory != "matrix":
+            sys.exit("--state bf16 needs the matrix-form memory")
+        w = w.replace(state_dtype="bf16")
     stack = w.layer_j <= 0          # a stack workload: a step is one hero_routed_stack call
     j = w.layer_j
     L = w.L_R if stack else 1       # routed layers per step
@@ -350,7 +357,7 @@ def main():
     roof = {"bound": "hbm" if hbm_bound else "mfma", "achieved": round(achieved, 1), "peak": peak,
             "unit": unit, "frac": round(achieved / peak, 4),
             "traffic": counted_traffic(dom) if (args.workload == "llama31_8b_layer" and args.memory == "matrix"
-                                                  and args.budget is None) else None,
+                                                  and args.budget is None and args.state == "f32") else None,
             "kernel": dom, "avg_launch_us": round(dom_ms_step * 1e3 / n_launch_step, 2),
             "work_per_launch": (f"{per_unit} x {n_f} FFN tokens = {total}"
                                 if not stack else
@@ -365,9 +372,10 @@ def main():
         "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
-        "config": {"workload": describe(w, j) + ("" if args.memory == "matrix" else
+        "config": {"workload": describe(w, j) + ("" if args.state == "f32" else ", S stored in bf16") +
+                               ("" if args.memory == "matrix" else
                                                  ", router memory in depth-history form"),
-                   "memory": args.memory, "global_batch": w.batch, "seq_len": w.seq,
+                   "memory": args.memory, "state": args.state, "global_batch": w.batch, "seq_len": w.seq,
                    "tokens": w.T, "layers_per_step": L, "parallelism": "none",
                    "n_ffn": n_f if not stack else sum(nfs), "n_adapter": n_a if not stack else sum(nas)},
         "roofline": roof,

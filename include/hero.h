@@ -76,6 +76,11 @@ typedef enum hero_mode {
  * (the paper's 896), d_s % 8 == 0, d_e % 64 == 0 and
  * (d_e + d_head) % 128 == 0; d_m in
  * {32, 64, 128, 256}; d_s <= 128; d_e, d_head <= 256; d_p <= 128.
+ * state_dtype selects how the memory matrix S is stored between layers: HERO_F32 (0, the
+ * default of a zeroed struct) or HERO_BF16, which halves the memory pass's traffic; every
+ * element written is rounded to the nearest bf16 (ties to even) and all arithmetic stays
+ * fp32.  zeta, p and m are fp32 either way.  A bf16 S needs d_m >= 64 and the matrix form
+ * (the depth-history entry points reject it).
  */
 typedef struct hero_dims {
   int d, d_ff, d_r, L_R;
@@ -85,6 +90,7 @@ typedef struct hero_dims {
   float eps_norm;     /* RMSNorm epsilon (1e-5)                                   */
   float eps;          /* epsilon of the two cosines and the memory read (1e-6)   */
   float T_hist;       /* history temperature (Sec. 4.1: 0.9)                      */
+  int state_dtype;    /* hero_dtype of S                                          */
 } hero_dims;
 
 /* Frozen backbone FFN of one routed layer: LN^ffn gain [d], W_g, W_u [d_ff][d], W_d [d][d_ff]. */
@@ -119,7 +125,7 @@ typedef struct hero_router_weights {
 
 /* Per-token router state (fp32), read and written in place. */
 typedef struct hero_state {
-  float *S;       /* [T][d_m][d_m] */
+  void *S;        /* [T][d_m][d_m], fp32 or bf16 (dims.state_dtype) */
   float *zeta;    /* [T][d_m]      */
   float *p_hist;  /* [T]           */
   float *m_hist;  /* [T]           */

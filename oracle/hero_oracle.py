@@ -35,7 +35,9 @@ constant here):
   * at layer j = 1 the state is the paper's initial value (S = 0, zeta = 0,
     p = m = 1) whatever the incoming buffers hold;
   * hidden-state outputs are rounded to the storage dtype (bfloat16 nearest-even
-    for bf16 workloads) at every layer boundary; nothing else is rounded;
+    for bf16 workloads) at every layer boundary; with ``state_dtype = "bf16"`` (an
+    option of this implementation, not of the paper) the memory matrix S is also
+    rounded to bfloat16 where it is written; nothing else is rounded;
   * the component ablations of Table 3 (Sec. 4.3) are a bit set ``ablation``:
     w/o Pos State zeroes the routing-progress and residual-transition features
     (r, q_rem, d, gamma) of the path vector; w/o Aux State drops the path
@@ -132,6 +134,7 @@ class Dims:
     eps: float = 1e-6
     T_hist: float = 0.9
     io_dtype: str = "f32"
+    state_dtype: str = "f32"   # storage of S between layers: "f32" (exact) or "bf16"
 
 
 @dataclasses.dataclass
@@ -451,6 +454,8 @@ def routed_layer(j, dims: Dims, hbar, hbar_prev1, hbar_prev2, state: State,
     else:
         c = memory_read(q, state.S, state.zeta, dims.eps)
         S_new, zeta_new = memory_write(k, v, state.S, state.zeta, rho)
+        if dims.state_dtype == "bf16":
+            S_new = round_bf16(S_new)       # the memory matrix as stored for the next layer
         nu = history_dissimilarity(j, s, c, R, dims.eps)
     # gate
     if ablation & NO_HISTORY:

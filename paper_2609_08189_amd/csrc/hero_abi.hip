@@ -71,6 +71,8 @@ int check_dims(const hero_dims* d) {
     return HERO_E_DIM;
   if (d->d_s != d->d_h + d->d_a) return HERO_E_DIM;
   if (!(d->eps_norm >= 0.f) || !(d->eps > 0.f) || !(d->T_hist > 0.f)) return HERO_E_RANGE;
+  if (d->state_dtype != HERO_F32 && d->state_dtype != HERO_BF16) return HERO_E_DTYPE;
+  if (d->state_dtype == HERO_BF16 && d->d_m < 64) return HERO_E_UNSUPPORTED;
   // kernel support
   if (d->d_m != 32 && d->d_m != 64 && d->d_m != 128 && d->d_m != 256) return HERO_E_UNSUPPORTED;
   if (d->d_s > 128 || d->d_e > 256 || d->d_head > 256 || d->d_p > 128) return HERO_E_UNSUPPORTED;
@@ -272,6 +274,7 @@ int run_layer(const LayerCall& c) {
     for (int i = 0; i < c.j - 1; ++i) ra.hw[i] = c.hw[i];
   } else {
     ra.S = c.st->S;
+    ra.state_bf16 = D.state_dtype == HERO_BF16;
     ra.zeta = c.st->zeta;
     ra.p_hist = c.st->p_hist;
     ra.m_hist = c.st->m_hist;
@@ -461,7 +464,7 @@ int hero_routed_layer_hist(const hero_dims* dims, int j, int T, const void* hbar
   int st = check_layer_call(dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, ffn, router, adapter, routing,
                             stats, workspace, workspace_bytes, &L);
   if (st != HERO_OK) return st;
-  if (dims->L_R > 64) return HERO_E_UNSUPPORTED;
+  if (dims->L_R > 64 || dims->state_dtype != HERO_F32) return HERO_E_UNSUPPORTED;
   if ((st = check_history(history)) != HERO_OK) return st;
   if (!eta) return HERO_E_NULL;
   for (int l = 0; l < j; ++l)
@@ -488,7 +491,7 @@ int routed_stack(const hero_dims* dims, int T, const void* h_in, void* h_out, co
   if (!h_in || !h_out || !ffn || !adapter || !eta) return HERO_E_NULL;
   if (!aligned16(h_in) || !aligned16(h_out)) return HERO_E_ALIGN;
   if (history) {
-    if (dims->L_R > 64) return HERO_E_UNSUPPORTED;
+    if (dims->L_R > 64 || dims->state_dtype != HERO_F32) return HERO_E_UNSUPPORTED;
     if ((st = check_history(history)) != HERO_OK) return st;
   } else if ((st = check_state(state)) != HERO_OK) {
     return st;
@@ -552,7 +555,7 @@ int hero_history_state(const hero_dims* dims, int n, int T, const float* kv, con
   int st = check_dims(dims);
   if (st != HERO_OK) return st;
   if (T <= 0) return HERO_E_DIM;
-  if (dims->L_R > 64) return HERO_E_UNSUPPORTED;
+  if (dims->L_R > 64 || dims->state_dtype != HERO_F32) return HERO_E_UNSUPPORTED;
   if (n < 0 || n > dims->L_R) return HERO_E_RANGE;
   if (!kv || !S || !zeta || (n > 0 && !eta)) return HERO_E_NULL;
   if (!aligned16(kv) || !aligned16(S) || !aligned16(zeta)) return HERO_E_ALIGN;

@@ -34,7 +34,8 @@ struct RouterTailArgs {
   int ld_th1;             // row pitch of th1 (elements)
   const float* beta;      // [T] or null
   int abl;                // router ablation bits (ABL_*)
-  float* S;               // [T][d_m][d_m]   in/out
+  void* S;                // [T][d_m][d_m]   in/out, fp32 or (state_bf16) bf16
+  int state_bf16;
   float* zeta;            // [T][d_m]        in/out
   float* p_hist;          // [T]             in/out
   float* m_hist;          // [T]             in/out

@@ -20,8 +20,8 @@
 // zero; without the auxiliary state z^a = 0; without the memory read (or the whole history
 // branch) router_mem is not launched, c = 0 and nu = 0 at every layer; without the history
 // branch a = 0, so logit = b (+ bias), and p = m = 1 are written.
-// The memory kernel moves 2 * 4 * (d_m^2 + d_m) bytes of state per token and is the
-// HBM-bound part; keeping it free of the matrix-vector work lets many workgroups per
+// The memory kernel moves 2 * 4 * (d_m^2 + d_m) bytes of state per token (2 * (2 d_m^2 + 4 d_m)
+// with S stored in bf16) and is the HBM-bound part; keeping it free of the matrix-vector work lets many workgroups per
 // CU keep HBM busy.  All arithmetic is fp32.
 #include "hero_device.h"
 #include "hero_kernels.h"
@@ -282,15 +282,54 @@ __global__ __launch_bounds__(NT) void router_pre_kernel(RouterTailArgs a) {
 // ---------------------------------------------------------------------------
 // router_mem: one token per workgroup
 // ---------------------------------------------------------------------------
-template <int DM>
+// 16 bytes of the state as fp32 values: four fp32, or eight bf16
+template <typename ST>
+struct SVec {
+  static constexpr int N = 16 / static_cast<int>(sizeof(ST));
+  float v[N];
+  __device__ __forceinline__ void load(const ST* p) {
+    if constexpr (sizeof(ST) == 4) {
+      const f32x4 x = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = x[e];
+    } else {
+      const u32x4 x = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] = __uint_as_float(x[e] << 16);
+        v[2 * e + 1] = __uint_as_float(x[e] & 0xffff0000u);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(ST* p) const {
+    if constexpr (sizeof(ST) == 4) {
+      f32x4 x;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = v[e];
+      *reinterpret_cast<f32x4*>(p) = x;
+    } else {
+      u32x4 x;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        x[e] = static_cast<uint32_t>(f32_to_bf16(v[2 * e])) |
+               (static_cast<uint32_t>(f32_to_bf16(v[2 * e + 1])) << 16);
+      *reinterpret_cast<u32x4*>(p) = x;
+    }
+  }
+};
+
+// ST: storage type of S (float, or bf16_t: every written element rounded to nearest even)
+template <int DM, typename ST>
 __global__ __launch_bounds__(NT) void router_mem_kernel(RouterTailArgs a) {
-  constexpr int C4 = DM / 4;   // float4 columns of one S row
-  constexpr int RP = NT / C4;  // S rows per pass
-  constexpr int NR = DM / RP;  // S rows per thread
+  constexpr int VE = SVec<ST>::N;  // state elements per 16-byte vector
+  constexpr int CV = DM / VE;      // vectors per S row
+  constexpr int RP = NT / CV;      // S rows per pass
+  constexpr int NR = DM / RP;      // S rows per thread
+  static_assert(NR >= 1 && NT % CV == 0, "state layout");
   LDS16 float fq[DM];
   LDS16 float fk[DM];
   LDS16 float vv[DM];
-  LDS16 f32x4 red[RP][C4];
+  LDS16 float red[RP][DM];
   __shared__ float sden;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int t = blockIdx.x;
@@ -318,41 +357,49 @@ __global__ __launch_bounds__(NT) void router_mem_kernel(RouterTailArgs a) {
     part = wave_sum(part);
     if (lane == 0) sden = part;
   }
-  const int cq = tid % C4, rg = tid / C4;
-  float* Sp = a.S + static_cast<size_t>(t) * DM * DM + 4 * cq;
-  const f32x4 v4 = *reinterpret_cast<const f32x4*>(&vv[4 * cq]);
-  f32x4 cacc = {0.f, 0.f, 0.f, 0.f};
+  const int cq = tid % CV, rg = tid / CV;
+  ST* Sp = static_cast<ST*>(a.S) + static_cast<size_t>(t) * DM * DM + VE * cq;
+  float vr[VE], cacc[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) {
+    vr[e] = vv[VE * cq + e];
+    cacc[e] = 0.f;
+  }
   if (j == 1) {
 #pragma unroll 16
     for (int i = 0; i < NR; ++i) {
       const int r = rg + RP * i;
-      *reinterpret_cast<f32x4*>(Sp + r * DM) = fk[r] * v4;
+      SVec<ST> o;
+#pragma unroll
+      for (int e = 0; e < VE; ++e) o.v[e] = fk[r] * vr[e];
+      o.store(Sp + r * DM);
     }
   } else {
     constexpr int CH = NR < 16 ? NR : 16;
     for (int i0 = 0; i0 < NR; i0 += CH) {
-      f32x4 sv[CH];
+      SVec<ST> sv[CH];
 #pragma unroll
-      for (int c = 0; c < CH; ++c) sv[c] = *reinterpret_cast<const f32x4*>(Sp + (rg + RP * (i0 + c)) * DM);
+      for (int c = 0; c < CH; ++c) sv[c].load(Sp + (rg + RP * (i0 + c)) * DM);
 #pragma unroll
       for (int c = 0; c < CH; ++c) {
         const int r = rg + RP * (i0 + c);
         const float qv = fq[r], kv = fk[r];
-        f32x4 o;
+        SVec<ST> o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          cacc[e] = fmaf(qv, sv[c][e], cacc[e]);
-          o[e] = fmaf(rho, sv[c][e], kv * v4[e]);
+        for (int e = 0; e < VE; ++e) {
+          cacc[e] = fmaf(qv, sv[c].v[e], cacc[e]);
+          o.v[e] = fmaf(rho, sv[c].v[e], kv * vr[e]);
         }
-        *reinterpret_cast<f32x4*>(Sp + r * DM) = o;
+        o.store(Sp + r * DM);
       }
     }
   }
-  red[rg][cq] = cacc;
+#pragma unroll
+  for (int e = 0; e < VE; ++e) red[rg][VE * cq + e] = cacc[e];
   __syncthreads();
   if (tid < DM) {
     float cs = 0.f;
-    for (int g = 0; g < RP; ++g) cs += red[g][tid >> 2][tid & 3];
+    for (int g = 0; g < RP; ++g) cs += red[g][tid];
     a.cvec[static_cast<size_t>(t) * DM + tid] = j > 1 ? cs / (sden + a.eps) : 0.f;
   }
 }
@@ -980,12 +1027,21 @@ hipError_t launch_router_pre(const RouterTailArgs& a, hipStream_t s) {
 hipError_t launch_router_mem(const RouterTailArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
   dim3 grid(a.T), block(NT);
-  switch (a.d_m) {
-    case 32: router_mem_kernel<32><<<grid, block, 0, s>>>(a); break;
-    case 64: router_mem_kernel<64><<<grid, block, 0, s>>>(a); break;
-    case 128: router_mem_kernel<128><<<grid, block, 0, s>>>(a); break;
-    case 256: router_mem_kernel<256><<<grid, block, 0, s>>>(a); break;
-    default: return hipErrorInvalidValue;
+  if (a.state_bf16) {
+    switch (a.d_m) {
+      case 64: router_mem_kernel<64, bf16_t><<<grid, block, 0, s>>>(a); break;
+      case 128: router_mem_kernel<128, bf16_t><<<grid, block, 0, s>>>(a); break;
+      case 256: router_mem_kernel<256, bf16_t><<<grid, block, 0, s>>>(a); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    switch (a.d_m) {
+      case 32: router_mem_kernel<32, float><<<grid, block, 0, s>>>(a); break;
+      case 64: router_mem_kernel<64, float><<<grid, block, 0, s>>>(a); break;
+      case 128: router_mem_kernel<128, float><<<grid, block, 0, s>>>(a); break;
+      case 256: router_mem_kernel<256, float><<<grid, block, 0, s>>>(a); break;
+      default: return hipErrorInvalidValue;
+    }
   }
   return hipGetLastError();
 }

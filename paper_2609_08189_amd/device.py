@@ -43,7 +43,8 @@ def dims_struct(w: synth.Workload) -> H.hero_dims:
     return H.hero_dims(d=w.d, d_ff=w.d_ff, d_r=w.d_r, L_R=w.L_R, d_m=w.d_m, d_s=w.d_s, d_h=w.d_h,
                        d_a=w.d_a, d_e=w.d_e, d_p=w.d_p, d_head=w.d_head,
                        dtype=H.HERO_BF16 if w.dtype == "bf16" else H.HERO_F32,
-                       eps_norm=w.eps_norm, eps=w.eps, T_hist=w.T_hist)
+                       eps_norm=w.eps_norm, eps=w.eps, T_hist=w.T_hist,
+                       state_dtype=H.HERO_BF16 if w.state_dtype == "bf16" else H.HERO_F32)
 
 
 class LayerStats:
@@ -93,7 +94,10 @@ class DeviceProblem:
                         for i in range(len(prob.adapter))]
         self.adapter_s = [H.hero_adapter_weights(a["w1"].data_ptr(), a["w2"].data_ptr()) for a in self.adapter]
         self.eta = [float(e) for e in prob.eta]
+        # S in its storage dtype (the synthetic bf16 state is bf16-exact, so the cast is exact)
         self.S = torch.from_numpy(prob.S).to(device)
+        if w.state_dtype == "bf16":
+            self.S = self.S.to(torch.bfloat16)
         self.zeta = torch.from_numpy(prob.zeta).to(device)
         self.p_hist = torch.from_numpy(prob.p_hist).to(device)
         self.m_hist = torch.from_numpy(prob.m_hist).to(device)
@@ -170,7 +174,7 @@ class DeviceProblem:
     def results(self) -> Dict[str, object]:
         torch.cuda.synchronize()
         S, zeta = self.history_state(self.n_entries) if self.history else (self.S, self.zeta)
-        out = dict(h=download_f64(self.h_out), S=S.cpu().numpy().astype(np.float64),
+        out = dict(h=download_f64(self.h_out), S=S.float().cpu().numpy().astype(np.float64),
                    zeta=zeta.cpu().numpy().astype(np.float64),
                    p_hist=self.p_hist.cpu().numpy().astype(np.float64),
                    m_hist=self.m_hist.cpu().numpy().astype(np.float64))
@@ -211,7 +215,7 @@ class DeviceProblem:
                         "hero_routed_layer")
                 S_sel, z_sel = pick(self.S), pick(self.zeta)
             torch.cuda.synchronize()
-            after = (S_sel.cpu().numpy().astype(np.float64), z_sel.cpu().numpy().astype(np.float64),
+            after = (S_sel.float().cpu().numpy().astype(np.float64), z_sel.cpu().numpy().astype(np.float64),
                      pick(self.p_hist).cpu().numpy().astype(np.float64),
                      pick(self.m_hist).cpu().numpy().astype(np.float64))
             io.append(dict(hbar=download_f64(pick(hs[-1])), S=prev_state[0], zeta=prev_state[1],

@@ -49,7 +49,8 @@ class hero_dims(ctypes.Structure):
                 ("d_m", ctypes.c_int), ("d_s", ctypes.c_int), ("d_h", ctypes.c_int), ("d_a", ctypes.c_int),
                 ("d_e", ctypes.c_int), ("d_p", ctypes.c_int), ("d_head", ctypes.c_int),
                 ("dtype", ctypes.c_int),
-                ("eps_norm", ctypes.c_float), ("eps", ctypes.c_float), ("T_hist", ctypes.c_float)]
+                ("eps_norm", ctypes.c_float), ("eps", ctypes.c_float), ("T_hist", ctypes.c_float),
+                ("state_dtype", ctypes.c_int)]
 
 
 class hero_ffn_weights(ctypes.Structure):

@@ -72,6 +72,8 @@ class Workload:
     # router variant of Table 3: bits 1 w/o Pos State, 2 w/o Aux State, 4 w/o MemRead,
     # 8 w/o History (0 = the full router)
     ablation: int = 0
+    # storage of the router memory S between layers: "f32" or "bf16" (zeta, p, m stay fp32)
+    state_dtype: str = "f32"
 
     @property
     def d_c(self) -> int:
@@ -417,6 +419,9 @@ def make_problem(w: Workload, seed: int = 0, T: Optional[int] = None,
         m = np.ones(T, np.float32)
         mem_k = mem_v = None
         layers = list(range(w.L_R))
+    if w.state_dtype == "bf16":
+        # the incoming memory as the caller stores it
+        S = bf16_bits_to_f64(f32_to_bf16_bits(S)).astype(np.float32)
     return Problem(
         w=w, hbar=hb, hbar_prev1=prev1, hbar_prev2=prev2,
         S=S, zeta=zeta, p_hist=p, m_hist=m,

@@ -5,7 +5,7 @@ from oracle import hero_oracle as O
 def dims_of(w):
     return O.Dims(d=w.d, d_ff=w.d_ff, d_r=w.d_r, L_R=w.L_R, d_m=w.d_m, d_s=w.d_s, d_h=w.d_h,
                   d_a=w.d_a, d_e=w.d_e, d_p=w.d_p, d_head=w.d_head, eps_norm=w.eps_norm,
-                  eps=w.eps, T_hist=w.T_hist, io_dtype=w.dtype)
+                  eps=w.eps, T_hist=w.T_hist, io_dtype=w.dtype, state_dtype=w.state_dtype)
 
 
 def router_of(prob):

@@ -85,6 +85,7 @@ def call_layer(dims=None, j=3, T=100, routing=None, ws_bytes=None, **over):
     ("d_ff", 688, H.HERO_E_UNSUPPORTED),  # bf16 needs d_ff % 128 == 0
     ("d_r", 16, H.HERO_E_UNSUPPORTED),
     ("d_e", 512, H.HERO_E_UNSUPPORTED),
+    ("state_dtype", 5, H.HERO_E_DTYPE),
 ])
 def test_dims_validation(field, value, status):
     assert call_layer(good_dims(**{field: value})) == status
@@ -216,6 +217,7 @@ def test_history_entry_points_validate():
     assert layer(hs=H.hero_history(FAKE + 4, FAKE, FAKE)) == H.HERO_E_ALIGN
     assert layer(eta=(3.9, float("nan"), 3.9)) == H.HERO_E_RANGE
     assert layer(d=good_dims(L_R=65), j=3) == H.HERO_E_UNSUPPORTED
+    assert layer(d=good_dims(state_dtype=H.HERO_BF16)) == H.HERO_E_UNSUPPORTED   # matrix form only
     assert layer(ws=None) == H.HERO_E_WORKSPACE
     S, z = FAKE + (9 << 30), FAKE + (10 << 30)
     kv = FAKE + (5 << 30)
@@ -223,3 +225,11 @@ def test_history_entry_points_validate():
     assert H.hero_history_state(dims, 2, 10, kv, [3.9] * 2, kv, z) == H.HERO_E_ALIAS     # S overlaps kv
     assert H.hero_history_state(dims, 2, 0, kv, [3.9] * 2, S, z) == H.HERO_E_DIM
     assert H.hero_history_state(dims, 2, 10, None, [3.9] * 2, S, z) == H.HERO_E_NULL
+    assert H.hero_history_state(good_dims(state_dtype=H.HERO_BF16), 2, 10, kv, [3.9] * 2, S, z) == \
+        H.HERO_E_UNSUPPORTED
+
+
+def test_bf16_state_needs_a_wide_memory():
+    assert call_layer(good_dims(state_dtype=H.HERO_BF16, d_m=32)) == H.HERO_E_UNSUPPORTED
+    # a valid bf16-state call gets past validation to the device check
+    assert call_layer(good_dims(state_dtype=H.HERO_BF16, d_m=64)) == H.HERO_E_DEVICE

@@ -65,14 +65,16 @@ def test_tiny_token_counts(T):
     _run(BF16_SMALL.replace(T=T, mode="threshold"), 1, seed=7)
 
 
-def test_llama31_8b_layer_full_shape():
+@pytest.mark.parametrize("state_dtype", ["f32", "bf16"])
+def test_llama31_8b_layer_full_shape(state_dtype):
     """Llama-3.1-8B shape, j = 17 of 32, T = 4096, budget 26.87 %, in the launch configuration the
-    benchmark times.  Router, memory, decisions and index lists are checked for every token; the
-    branch outputs on a sample of 48 FFN and 24 adapter rows (the oracle's FFN is costly)."""
+    benchmark times (S stored in fp32, or in bf16).  Router, memory, decisions and index lists
+    are checked for every token; the branch outputs on a sample of 48 FFN and 24 adapter rows
+    (the oracle's FFN is costly)."""
     import torch
     from paper_2609_08189_amd.device import DeviceProblem
-    w = synth.WORKLOADS["llama31_8b_layer"]
-    print(f"case {w.name} T={w.T} j={w.layer_j}", flush=True)
+    w = synth.WORKLOADS["llama31_8b_layer"].replace(state_dtype=state_dtype)
+    print(f"case {w.name} T={w.T} j={w.layer_j} state={state_dtype}", flush=True)
     prob = synth.make_problem(w, seed=0)
     dp = DeviceProblem(prob)
     dp.run_layer(w.layer_j)
@@ -140,3 +142,14 @@ def test_ffn_split_k_decode_rows():
     row count is ragged and K splits unevenly (d_ff / 64 = 42 k-tiles over 16 slices)."""
     w = BF16_SMALL.replace(d=1024, d_ff=2688, T=256, budget=0.27)
     _run(w, 5, seed=8)
+
+
+@pytest.mark.parametrize("j", [1, 3])
+def test_bf16_state(j):
+    """S stored in bf16 between layers (every element written is rounded to nearest even)."""
+    _run(BF16_SMALL.replace(state_dtype="bf16"), j, seed=9)
+
+
+@pytest.mark.parametrize("d_m", [64, 256])
+def test_bf16_state_widths_f32_weights(d_m):
+    _run(F32_SMALL.replace(d_m=d_m, state_dtype="bf16"), 2, seed=10)

@@ -28,6 +28,11 @@ def _run_stack(w, seed=0, rows=None):
     return prob, res
 
 
+def test_bf16_stack_bf16_state():
+    """A 6-layer bf16 stack with S stored in bf16 across depth."""
+    _run_stack(BF16_STACK.replace(state_dtype="bf16"), seed=4)
+
+
 def test_tiny_f32_stack():
     """4 routed layers, d=256, d_ff=688 (ragged for any 64-wide tile), r=16, d_m=32, T=64, 27 % skip."""
     prob, res = _run_stack(synth.WORKLOADS["tiny_f32_stack"], seed=0)

@@ -456,3 +456,26 @@ def test_logit_bias_enters_the_gate_only():
         np.testing.assert_allclose(L1.gate, scipy.special.expit(L0.logit + beta), rtol=1e-12, atol=1e-300)
     a = base.layers[0].debug["a"]
     np.testing.assert_allclose(base.layers[0].state.p_hist, scipy.special.expit(a / SMALL.T_hist), rtol=1e-13)
+
+
+def test_bf16_state_is_the_rounded_memory():
+    """S stored in bf16: every stored element is a bf16 value; at the first layer it is exactly
+    torch's bf16 rounding of the exact outer product; over the stack it stays within the rounding
+    error accumulated by one half-ulp per layer, and the logits barely move."""
+    w16 = SMALL.replace(state_dtype="bf16")
+    prob = _problem(router_std=0.3)
+    exact = _stack(prob, SMALL)
+    rounded = _stack(prob, w16)
+    for L in rounded.layers:
+        S = L.state.S
+        np.testing.assert_array_equal(_t(S).to(torch.bfloat16).double().numpy(), S)
+    np.testing.assert_array_equal(rounded.layers[0].state.S,
+                                  _t(exact.layers[0].state.S).to(torch.bfloat16).double().numpy())
+    for j, (Le, Lr) in enumerate(zip(exact.layers, rounded.layers), start=1):
+        scale = np.abs(Le.state.S).max()
+        assert np.abs(Lr.state.S - Le.state.S).max() <= j * 2.0 ** -8 * scale
+        assert Lr.state.S is not Le.state.S and not np.array_equal(Lr.state.S, Le.state.S)
+        if j == 1:   # the first layer reads no memory: same zeta and logits
+            np.testing.assert_array_equal(Lr.state.zeta, Le.state.zeta)
+            np.testing.assert_array_equal(Lr.logit, Le.logit)
+        assert np.abs(Lr.logit - Le.logit).max() < 5e-3 * np.abs(Le.logit).max()
