@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define HERO_ABI_VERSION 3
+#define HERO_ABI_VERSION 4
 
 typedef enum hero_status {
   HERO_OK = 0,

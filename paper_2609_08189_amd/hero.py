@@ -14,7 +14,7 @@ from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhero.so")
-ABI_VERSION = 3          # the struct layouts below follow include/hero.h of this version
+ABI_VERSION = 4          # the struct layouts below follow include/hero.h of this version
 
 HERO_OK = 0
 HERO_E_NULL = 1

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_function():
     lib = H.lib()
     for n in names:
         assert hasattr(lib, n), f"{n} declared in include/hero.h but not exported"
-    assert H.hero_abi_version() == H.ABI_VERSION == 3
+    assert H.hero_abi_version() == H.ABI_VERSION == 4
 
 
 def test_status_strings():
