@@ -526,3 +526,124 @@ def routed_stack(dims: Dims, h_in, ffns: List[FFNParams], R: RouterParams,
         hist = [hbar, hist[0]]
         hbar = res.h
     return StackResult(hbar, state, layers)
+
+
+# ---------------------------------------------------------------------------
+# The full decoder: dense attention before every FFN (Sec. 3.1, eq:dense_attention, first
+# line) and routing at the last L_R blocks ("latter half" placement, Sec. 4.1)
+#
+# Readings: Attn is Llama's bias-free grouped-query self-attention.  LN^attn is RMSNorm
+# with gain; q = W_q x, k = W_k x, v = W_v x per head of width hd; the rotary position
+# embedding turns each interleaved pair (x_{2i}, x_{2i+1}) of q and k by the angle
+# pos * inv_freq[i] (the frequency table is an input, so plain and rescaled variants are
+# both expressible); attention is causal within each sequence, softmax(q k^T / sqrt(hd)) v,
+# query head h reading key/value head floor(h / (n_heads / n_kv_heads)); the heads are
+# concatenated and projected by W_o.  Tokens are laid out as [batch][seq], position = index
+# in the sequence.  Non-routed blocks keep their pretrained FFN: h = hbar + FFN(LN^ffn(hbar)).
+# ---------------------------------------------------------------------------
+
+
+@dataclasses.dataclass
+class AttnDims:
+    n_heads: int
+    n_kv_heads: int
+    head_dim: int
+
+
+@dataclasses.dataclass
+class AttnParams:
+    norm_w: np.ndarray    # [d]                               LN^attn gain
+    w_q: np.ndarray       # [n_heads * hd, d]
+    w_k: np.ndarray       # [n_kv_heads * hd, d]
+    w_v: np.ndarray       # [n_kv_heads * hd, d]
+    w_o: np.ndarray       # [d, n_heads * hd]
+    inv_freq: np.ndarray  # [hd / 2]                          rotary frequencies
+
+
+def rope(x, pos, inv_freq):
+    """Rotary embedding of the rows of x [n, hd]: pair (x_{2i}, x_{2i+1}) turned by
+    pos * inv_freq[i] (pos [n])."""
+    x = np.asarray(x, dtype=f64)
+    ang = np.asarray(pos, dtype=f64)[:, None] * np.asarray(inv_freq, dtype=f64)[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    a, b = x[:, 0::2], x[:, 1::2]
+    out = np.empty_like(x)
+    out[:, 0::2] = a * c - b * s
+    out[:, 1::2] = a * s + b * c
+    return out
+
+
+def causal_attention(q, k, v):
+    """One head of one sequence: softmax(q k^T / sqrt(hd)) v with key i visible to query t iff
+    i <= t.  q, k, v: [seq, hd]."""
+    S = q.shape[0]
+    scores = (q @ k.T) / math.sqrt(q.shape[1])
+    scores = np.where(np.tril(np.ones((S, S), dtype=bool)), scores, -np.inf)
+    scores = scores - scores.max(axis=1, keepdims=True)
+    p = np.exp(scores)
+    p = p / p.sum(axis=1, keepdims=True)
+    return p @ v
+
+
+def attention_block(h, attn: AttnParams, adims: AttnDims, batch, seq, dims: Dims):
+    """hbar = h + Attn(LN^attn(h)) for tokens laid out as [batch][seq] (eq:dense_attention)."""
+    h = np.asarray(h, dtype=f64)
+    hd, nh, nkv = adims.head_dim, adims.n_heads, adims.n_kv_heads
+    x = rmsnorm(h, attn.norm_w, dims.eps_norm)
+    q, k, v = x @ attn.w_q.T, x @ attn.w_k.T, x @ attn.w_v.T
+    pos = np.tile(np.arange(seq), batch)
+    o = np.empty_like(q)
+    group = nh // nkv
+    for hh in range(nh):
+        g = hh // group
+        qh = rope(q[:, hh * hd:(hh + 1) * hd], pos, attn.inv_freq)
+        kh = rope(k[:, g * hd:(g + 1) * hd], pos, attn.inv_freq)
+        vh = v[:, g * hd:(g + 1) * hd]
+        for b in range(batch):
+            rows = slice(b * seq, (b + 1) * seq)
+            o[rows, hh * hd:(hh + 1) * hd] = causal_attention(qh[rows], kh[rows], vh[rows])
+    return h + o @ attn.w_o.T
+
+
+def dense_ffn_block(hbar, ffn: FFNParams, dims: Dims):
+    """A non-routed block's pretrained FFN: h = hbar + FFN(LN^ffn(hbar))."""
+    return hbar + frozen_ffn(ffn_input(hbar, ffn, dims), ffn)
+
+
+@dataclasses.dataclass
+class DecoderResult:
+    h: np.ndarray
+    state: State
+    hbars: List[np.ndarray]        # post-attention state of every block
+    routed: List[LayerResult]      # the routed blocks, in order
+
+
+def decoder_stack(dims: Dims, adims: AttnDims, n_layers, batch, seq, h_in,
+                  attns: List[AttnParams], ffns: List[FFNParams], R: RouterParams,
+                  adapters: List[AdapterParams], etas, mode="budget", budget=0.0, tau=0.5,
+                  beta=None, forced_ffn=None, ablation=0):
+    """n_layers decoder blocks; blocks n_layers - L_R + 1 .. n_layers are routed (j = 1..L_R,
+    adapters[j-1], etas[j-1]), the others keep their FFN.  Every block starts with dense
+    attention.  Hidden states are rounded to the storage dtype after every sub-block."""
+    L_R = dims.L_R
+    first = n_layers - L_R
+    T = h_in.shape[0]
+    state = State.initial(T, dims.d_m)
+    hist = [None, None]
+    h = np.asarray(h_in, dtype=f64)
+    hbars, routed = [], []
+    for l in range(n_layers):
+        hbar = round_io(attention_block(h, attns[l], adims, batch, seq, dims), dims.io_dtype)
+        hbars.append(hbar)
+        if l < first:
+            h = round_io(dense_ffn_block(hbar, ffns[l], dims), dims.io_dtype)
+            continue
+        j = l - first + 1
+        ff = None if forced_ffn is None else forced_ffn[j - 1]
+        res = routed_layer(j, dims, hbar, hist[0], hist[1], state, ffns[l], R, adapters[j - 1],
+                           etas[j - 1], mode, budget, tau, beta, ff, ablation=ablation)
+        routed.append(res)
+        state = res.state
+        hist = [hbar, hist[0]]
+        h = res.h
+    return DecoderResult(h, state, hbars, routed)

@@ -25,7 +25,10 @@ are used):
     differ from the current one by N(0, 0.5^2) steps;
   * the 13B prefill workload adds a per-token logit bias that is constant over
     runs of 64 positions: a seeded 29 % of the runs draw N(-2, 1), the rest
-    N(2, 1), so that skip decisions cluster by position.
+    N(2, 1), so that skip decisions cluster by position;
+  * a full-decoder workload adds per block an attention-input RMSNorm gain
+    ~ 1 + N(0, 0.02), a fused [W_q; W_k; W_v] and W_o ~ N(0, 0.02), and the
+    standard rotary frequency table theta^(-2i/hd) of the model.
 Every draw comes from numpy's PCG64 keyed by (seed, tensor id, layer), drawn in
 float32 and rounded once, round-to-nearest-even, to the storage dtype.
 """
@@ -74,6 +77,12 @@ class Workload:
     ablation: int = 0
     # storage of the router memory S between layers: "f32" or "bf16" (zeta, p, m stay fp32)
     state_dtype: str = "f32"
+    # full decoder (n_layers > 0): every block has dense attention, the last L_R are routed
+    n_layers: int = 0
+    n_heads: int = 32
+    n_kv_heads: int = 8
+    head_dim: int = 128
+    rope_theta: float = 500000.0
 
     @property
     def d_c(self) -> int:
@@ -105,6 +114,13 @@ WORKLOADS: Dict[str, Workload] = {
     "llama2_13b_prefill": Workload("llama2_13b_prefill", "bf16", 5120, 13824, 64, 40, 128,
                                    32768, "threshold", tau=0.5, bias="bimodal_runs",
                                    batch=8, seq=4096),
+    # the whole Llama-3.1-8B decoder (32 blocks, GQA 32/8 heads of 128, rotary base 5e5) with
+    # the latter half routed (Sec. 4.1), 2 x 2048 prefill tokens, 75 % of routed FFN calls
+    # skipped (the rate the paper's 25 % parameter budget implies)
+    "llama31_8b_decoder": Workload("llama31_8b_decoder", "bf16", 4096, 14336, 64, 16, 128,
+                                   4096, "budget", budget=0.75, batch=2, seq=2048,
+                                   n_layers=32, n_heads=32, n_kv_heads=8, head_dim=128,
+                                   rope_theta=500000.0),
 }
 
 # ---------------------------------------------------------------------------
@@ -163,6 +179,7 @@ _TID = {
     "w_n": 37, "w_c": 38, "th1": 39, "th2": 40, "ps1": 41, "ps2": 42,
     "state_a": 50, "state_b": 51, "p_hist": 52, "m_hist": 53,
     "bias_runs": 60, "bias_vals": 61,
+    "attn_norm": 70, "w_qkv": 71, "w_o": 72,
 }
 
 
@@ -269,6 +286,21 @@ def adapter_layer(w: Workload, layer: int, seed: int = 0) -> Dict[str, Tensor]:
         "w1": _t(normal32(seed, "w1", (w.d_r, w.d), 0.02, layer=layer), w.dtype),
         "w2": _t(normal32(seed, "w2", (w.d, w.d_r), 0.02, layer=layer), w.dtype),
     }
+
+
+def attn_layer(w: Workload, layer: int, seed: int = 0) -> Dict[str, Tensor]:
+    n_qkv = (w.n_heads + 2 * w.n_kv_heads) * w.head_dim
+    return {
+        "norm_w": _t(normal32(seed, "attn_norm", (w.d,), 0.02, 1.0, layer), w.dtype),
+        "w_qkv": _t(normal32(seed, "w_qkv", (n_qkv, w.d), 0.02, layer=layer), w.dtype),
+        "w_o": _t(normal32(seed, "w_o", (w.d, w.n_heads * w.head_dim), 0.02, layer=layer), w.dtype),
+    }
+
+
+def rope_inv_freq(w: Workload) -> np.ndarray:
+    """The model's rotary frequency table theta^(-2i/hd), i < hd/2, as float32."""
+    i = np.arange(w.head_dim // 2, dtype=np.float64)
+    return (w.rope_theta ** (-2.0 * i / w.head_dim)).astype(np.float32)
 
 
 def eta_values(w: Workload) -> np.ndarray:
@@ -393,6 +425,9 @@ class Problem:
     # a layer call at j > 1: the pairs of layers 1..j-1 ([T, j-1, d_m] f32), for the depth-history
     # form of the memory; S and zeta above are their decayed sums with decay 0.98
     mem_k: Optional[np.ndarray] = None
+    # full decoder: attention weights of every block, and the rotary frequency table
+    attn: Optional["LazyLayers"] = None
+    inv_freq: Optional[np.ndarray] = None
     mem_v: Optional[np.ndarray] = None
 
 
@@ -422,6 +457,18 @@ def make_problem(w: Workload, seed: int = 0, T: Optional[int] = None,
     if w.state_dtype == "bf16":
         # the incoming memory as the caller stores it
         S = bf16_bits_to_f64(f32_to_bf16_bits(S)).astype(np.float32)
+    if w.n_layers > 0:
+        # full decoder: a frozen FFN and attention in every block, adapters in the routed ones
+        return Problem(
+            w=w, hbar=hb, hbar_prev1=None, hbar_prev2=None,
+            S=S, zeta=zeta, p_hist=p, m_hist=m,
+            router=router_weights(w, seed),
+            ffn=LazyLayers(lambda l: ffn_layer(w, l, seed), range(w.n_layers)),
+            adapter=LazyLayers(lambda l: adapter_layer(w, l, seed), range(w.L_R), keep=4),
+            eta=eta_values(w), beta=logit_bias(w, seed, T),
+            attn=LazyLayers(lambda l: attn_layer(w, l, seed), range(w.n_layers)),
+            inv_freq=rope_inv_freq(w),
+        )
     return Problem(
         w=w, hbar=hb, hbar_prev1=prev1, hbar_prev2=prev2,
         S=S, zeta=zeta, p_hist=p, m_hist=m,

@@ -1,4 +1,6 @@
 """Convert a seeded synthetic problem into the CPU oracle's float64 parameters (test helper)."""
+import numpy as np
+
 from oracle import hero_oracle as O
 
 
@@ -26,3 +28,16 @@ def state_of(prob, rows=None):
     sl = slice(None) if rows is None else rows
     return O.State(prob.S[sl].astype("f8"), prob.zeta[sl].astype("f8"),
                    prob.p_hist[sl].astype("f8"), prob.m_hist[sl].astype("f8"))
+
+
+def adims_of(w):
+    return O.AttnDims(n_heads=w.n_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim)
+
+
+def attn_of(layer, w, inv_freq):
+    """Split the stored fused [W_q; W_k; W_v] into the oracle's three projections."""
+    qkv = layer["w_qkv"].f64
+    nq, nkv = w.n_heads * w.head_dim, w.n_kv_heads * w.head_dim
+    return O.AttnParams(norm_w=layer["norm_w"].f64, w_q=qkv[:nq], w_k=qkv[nq:nq + nkv],
+                        w_v=qkv[nq + nkv:], w_o=layer["w_o"].f64,
+                        inv_freq=np.asarray(inv_freq, dtype=np.float64))

@@ -1,0 +1,145 @@
+"""Pins for the oracle's full decoder (dense attention before every FFN, routing at the last
+L_R blocks; Sec. 3.1 eq:dense_attention and the placement of Sec. 4.1).
+
+The rotary embedding is checked against its complex-number form, causal attention against
+torch's scaled_dot_product_attention, the attention block against a torch module stack built
+independently (library RMSNorm, Linear, complex rotation, SDPA with repeated KV heads), and the
+decoder against the routed stack it must reduce to when attention contributes nothing.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import hero_oracle as O
+from paper_2609_08189_amd import synth
+from tests.oracle_inputs import adapter_of, adims_of, attn_of, dims_of, ffn_of, router_of
+
+W = synth.Workload("dec_small", "f32", d=64, d_ff=96, d_r=8, L_R=3, d_m=8, T=2 * 9, mode="threshold",
+                   d_s=16, d_h=12, d_a=4, d_e=32, d_p=16, d_head=32, batch=2, seq=9,
+                   n_layers=5, n_heads=4, n_kv_heads=2, head_dim=16, rope_theta=10000.0)
+
+
+def _t(x):
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64))
+
+
+def test_rope_is_a_complex_rotation():
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((7, 16))
+    pos = np.array([0, 1, 2, 5, 100, 2047, 4095])
+    inv = synth.rope_inv_freq(W).astype(np.float64)
+    z = x[:, 0::2] + 1j * x[:, 1::2]
+    rot = z * np.exp(1j * pos[:, None] * inv[None, :])
+    ref = np.empty_like(x)
+    ref[:, 0::2], ref[:, 1::2] = rot.real, rot.imag
+    np.testing.assert_allclose(O.rope(x, pos, inv), ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_array_equal(O.rope(x[:1], [0], inv), x[:1])
+    # scores depend on the relative position only
+    q, k = rng.standard_normal((1, 16)), rng.standard_normal((1, 16))
+    s1 = O.rope(q, [9], inv) @ O.rope(k, [4], inv).T
+    s2 = O.rope(q, [1009], inv) @ O.rope(k, [1004], inv).T
+    np.testing.assert_allclose(s1, s2, rtol=1e-9)
+
+
+def test_causal_attention_matches_torch_sdpa():
+    rng = np.random.default_rng(1)
+    q, k, v = (rng.standard_normal((11, 16)) for _ in range(3))
+    ref = F.scaled_dot_product_attention(_t(q)[None], _t(k)[None], _t(v)[None], is_causal=True)[0]
+    np.testing.assert_allclose(O.causal_attention(q, k, v), ref.numpy(), rtol=1e-12, atol=1e-13)
+
+
+def _torch_attention_block(h, A, w):
+    """Llama attention built from torch library pieces, independently of the oracle."""
+    hd, nh, nkv = w.head_dim, w.n_heads, w.n_kv_heads
+    x = torch.nn.functional.rms_norm(_t(h), (w.d,), weight=_t(A.norm_w), eps=w.eps_norm)
+    q = (x @ _t(A.w_q).T).view(w.batch, w.seq, nh, hd)
+    k = (x @ _t(A.w_k).T).view(w.batch, w.seq, nkv, hd)
+    v = (x @ _t(A.w_v).T).view(w.batch, w.seq, nkv, hd)
+    ang = torch.arange(w.seq, dtype=torch.float64)[:, None] * _t(A.inv_freq)[None, :]
+    rot = torch.polar(torch.ones_like(ang), ang)[None, :, None, :]
+
+    def turn(x4):
+        z = torch.view_as_complex(x4.reshape(*x4.shape[:-1], hd // 2, 2).contiguous())
+        return torch.view_as_real(z * rot).reshape(x4.shape)
+
+    q, k = turn(q), turn(k)
+    k = k.repeat_interleave(nh // nkv, dim=2)
+    v = v.repeat_interleave(nh // nkv, dim=2)
+    o = F.scaled_dot_product_attention(q.transpose(1, 2), k.transpose(1, 2), v.transpose(1, 2), is_causal=True)
+    o = o.transpose(1, 2).reshape(w.batch * w.seq, nh * hd)
+    return (_t(h) + o @ _t(A.w_o).T).numpy()
+
+
+def _prob(seed=2, std=None):
+    prob = synth.make_problem(W, seed=seed)
+    return prob
+
+
+def test_attention_block_matches_torch_modules():
+    prob = _prob()
+    A = attn_of(prob.attn[0], W, prob.inv_freq)
+    h = prob.hbar.f64
+    got = O.attention_block(h, A, adims_of(W), W.batch, W.seq, dims_of(W))
+    np.testing.assert_allclose(got, _torch_attention_block(h, A, W), rtol=1e-10, atol=1e-12)
+    assert np.abs(got - h).max() > 1e-3
+
+
+def test_attention_is_causal_within_each_sequence():
+    prob = _prob()
+    A = attn_of(prob.attn[0], W, prob.inv_freq)
+    h = prob.hbar.f64
+    base = O.attention_block(h, A, adims_of(W), W.batch, W.seq, dims_of(W))
+    h2 = h.copy()
+    h2[W.seq + 5] += 1.0                       # sequence 1, position 5
+    moved = O.attention_block(h2, A, adims_of(W), W.batch, W.seq, dims_of(W))
+    np.testing.assert_array_equal(moved[:W.seq + 5], base[:W.seq + 5])
+    assert np.abs(moved[W.seq + 6:] - base[W.seq + 6:]).max() > 1e-6
+
+
+def _decoder(prob, w=W, w_o_zero=False):
+    attns = [attn_of(prob.attn[l], w, prob.inv_freq) for l in range(w.n_layers)]
+    if w_o_zero:
+        attns = [dataclasses.replace(a, w_o=np.zeros_like(a.w_o)) for a in attns]
+    return O.decoder_stack(dims_of(w), adims_of(w), w.n_layers, w.batch, w.seq, prob.hbar.f64, attns,
+                           [ffn_of(prob.ffn[l]) for l in range(w.n_layers)], router_of(prob),
+                           [adapter_of(prob.adapter[j]) for j in range(w.L_R)], prob.eta.astype("f8"),
+                           mode="threshold", tau=0.5)
+
+
+def test_decoder_without_attention_is_dense_blocks_then_the_routed_stack():
+    prob = _prob()
+    dec = _decoder(prob, w_o_zero=True)
+    # the two non-routed blocks: the Llama MLP on the residual, through torch modules
+    h = _t(prob.hbar.f64)
+    for l in range(W.n_layers - W.L_R):
+        F_ = ffn_of(prob.ffn[l])
+        x = torch.nn.functional.rms_norm(h, (W.d,), weight=_t(F_.norm_w), eps=W.eps_norm)
+        h = h + (F.silu(x @ _t(F_.w_gate).T) * (x @ _t(F_.w_up).T)) @ _t(F_.w_down).T
+    h = h.numpy()
+    # (the decoder stores every hidden state in the workload's float32, so one rounding per block)
+    np.testing.assert_allclose(dec.hbars[W.n_layers - W.L_R], h, rtol=3e-7, atol=1e-12)
+    # then exactly the routed stack over the last L_R blocks' FFNs
+    first = W.n_layers - W.L_R
+    ref = O.routed_stack(dims_of(W), dec.hbars[first], [ffn_of(prob.ffn[l]) for l in range(first, W.n_layers)],
+                         router_of(prob), [adapter_of(prob.adapter[j]) for j in range(W.L_R)],
+                         prob.eta.astype("f8"), mode="threshold", tau=0.5)
+    np.testing.assert_array_equal(dec.h, ref.h)
+    np.testing.assert_array_equal(dec.state.S, ref.state.S)
+    for a, b in zip(dec.routed, ref.layers):
+        np.testing.assert_array_equal(a.logit, b.logit)
+
+
+def test_decoder_routes_only_the_latter_blocks():
+    prob = _prob()
+    dec = _decoder(prob)
+    assert len(dec.hbars) == W.n_layers and len(dec.routed) == W.L_R
+    # the residual transition of the first routed block is zero (no earlier decision point)
+    assert np.all(dec.routed[0].debug["d"] == 0.0)
+    # the second routed block sees the transition between the post-attention states of the
+    # first two routed blocks
+    first = W.n_layers - W.L_R
+    np.testing.assert_allclose(dec.routed[1].debug["d"],
+                               np.linalg.norm(dec.hbars[first + 1] - dec.hbars[first], axis=1), rtol=1e-12)
