@@ -180,7 +180,9 @@ typedef struct hero_layer_stats {
   float *logit, *gate, *lambda;
 } hero_layer_stats;
 
-/* Kernels of one routed layer, in launch order (for hero_kernel_timer). */
+/* Kernels of one routed layer, in launch order, then those of the attention sub-block (for
+ * hero_kernel_timer).  The pretrained FFN of a non-routed decoder block is timed as
+ * HERO_K_ROWSTATS, HERO_K_FFN_GATE_UP and HERO_K_FFN_DOWN. */
 typedef enum hero_kernel {
   HERO_K_ROWSTATS = 0,      /* inv_rms, residual-transition sums, u = RMSNorm_w(hbar)          */
   HERO_K_ROUTER_GEMM = 1,   /* [W_hd; psi_1] hbar                                               */
@@ -192,7 +194,12 @@ typedef enum hero_kernel {
   HERO_K_FFN_DOWN = 7,      /* W_d act, scattered as hbar + g y                                 */
   HERO_K_ADAPTER_DOWN = 8,  /* W_1 u over the adapter tokens (partial sums)                     */
   HERO_K_ADAPTER_UP = 9,    /* W_2 SiLU(.), scattered as hbar + (1 - g) y                       */
-  HERO_K_COUNT = 10
+  /* attention sub-block of a decoder block (hero_attention_block, hero_decoder_stack) */
+  HERO_K_ATTN_NORM = 10,    /* x = RMSNorm(h) * norm_w                                          */
+  HERO_K_ATTN_QKV = 11,     /* [q; k; v] = x W_qkv^T with the rotary embedding                  */
+  HERO_K_ATTN_CORE = 12,    /* causal grouped-query softmax attention                           */
+  HERO_K_ATTN_OUT = 13,     /* hbar = h + o W_o^T                                               */
+  HERO_K_COUNT = 14
 } hero_kernel;
 
 /*
@@ -311,6 +318,66 @@ int hero_routed_stack_hist(const hero_dims *dims, int T, const void *h_in, void 
  */
 int hero_history_state(const hero_dims *dims, int n, int T, const float *kv, const float *eta,
                        float *S, float *zeta, void *stream);
+
+/*
+ * The full decoder (Sec. 3.1): dense attention at every block,
+ *   hbar = h + Attn(LN^attn(h))                                        (eq:dense_attention)
+ * then the block's FFN: the pretrained one, h = hbar + FFN(LN^ffn(hbar)), at non-routed
+ * blocks, and the routed layer at routed blocks.  The routed blocks are the last L_R of the
+ * n_layers (the paper routes the latter half, Sec. 4.1).
+ *
+ * Attn is bias-free grouped-query self-attention of Llama form, causal within each sequence:
+ * x = RMSNorm(h) * norm_w; q, k, v = x W_{q,k,v}^T per head of width head_dim; the rotary
+ * embedding turns each pair (x_{2i}, x_{2i+1}) of q and k by pos * inv_freq[i], pos the
+ * token's index in its sequence; o_h = softmax(q_h k_g^T / sqrt(head_dim)) v_g with
+ * g = h / (n_heads / n_kv_heads); hbar = h + [o_1 .. o_{n_heads}] W_o^T.  Tokens are laid out
+ * [batch][seq].  bf16 only; supported: head_dim == 128, n_heads % n_kv_heads == 0,
+ * n_heads even.  q, k, v and the attention output are rounded to bf16 on their way through
+ * HBM; softmax and every sum are fp32.
+ */
+typedef struct hero_attn_dims {
+  int n_heads, n_kv_heads, head_dim;
+} hero_attn_dims;
+
+/* One block's attention weights: LN^attn gain [d]; W_q, W_k, W_v stacked as one
+ * [(n_heads + 2 n_kv_heads) head_dim][d] matrix (rows: the q heads, then k, then v);
+ * W_o [d][n_heads head_dim]. */
+typedef struct hero_attn_weights {
+  const void *norm_w, *w_qkv, *w_o;
+} hero_attn_weights;
+
+/*
+ * Workspace bytes for hero_attention_block (n_layers = 0) or hero_decoder_stack with
+ * batch x seq tokens.  Host-only; validates both dims structs.
+ */
+int hero_decoder_workspace_size(const hero_dims *dims, const hero_attn_dims *adims, int n_layers,
+                                int batch, int seq, size_t *bytes);
+
+/*
+ * The attention sub-block of one decoder block: hbar = h + Attn(LN^attn(h)).  inv_freq is a
+ * HOST array of head_dim / 2 rotary frequencies.  hbar must not overlap h.
+ */
+int hero_attention_block(const hero_dims *dims, const hero_attn_dims *adims, int batch, int seq,
+                         const void *h, void *hbar, const hero_attn_weights *attn,
+                         const float *inv_freq, void *workspace, size_t workspace_bytes,
+                         void *stream);
+
+/*
+ * n_layers decoder blocks (L_R <= n_layers): attention at every block; the pretrained FFN at
+ * blocks 1 .. n_layers - L_R; routed layers j = 1 .. L_R at the rest, with the router state
+ * starting from its initial value at routed layer 1 and left in `state` (as in
+ * hero_routed_stack; the residual transitions of the path vector are taken between the
+ * post-attention states of consecutive routed blocks).  attn and ffn are HOST arrays of
+ * n_layers entries; adapter, eta and stats (or NULL) of L_R entries.  The routing rule
+ * applies at every routed block.  h_out must not overlap h_in.
+ */
+int hero_decoder_stack(const hero_dims *dims, const hero_attn_dims *adims, int n_layers, int batch,
+                       int seq, const void *h_in, void *h_out, const hero_state *state,
+                       const hero_attn_weights *attn, const hero_ffn_weights *ffn,
+                       const hero_router_weights *router, const hero_adapter_weights *adapter,
+                       const float *eta, const float *inv_freq, const hero_routing *routing,
+                       const hero_layer_stats *stats, void *workspace, size_t workspace_bytes,
+                       void *stream);
 
 #ifdef __cplusplus
 }

@@ -585,24 +585,44 @@ def causal_attention(q, k, v):
     return p @ v
 
 
-def attention_block(h, attn: AttnParams, adims: AttnDims, batch, seq, dims: Dims):
-    """hbar = h + Attn(LN^attn(h)) for tokens laid out as [batch][seq] (eq:dense_attention)."""
+def attention_block(h, attn: AttnParams, adims: AttnDims, batch, seq, dims: Dims, rows=None):
+    """hbar = h + Attn(LN^attn(h)) for tokens laid out as [batch][seq] (eq:dense_attention).
+
+    ``rows`` (token indices) restricts the output to those rows, each computed from its own
+    query and all keys up to it; other rows are NaN."""
     h = np.asarray(h, dtype=f64)
     hd, nh, nkv = adims.head_dim, adims.n_heads, adims.n_kv_heads
     x = rmsnorm(h, attn.norm_w, dims.eps_norm)
-    q, k, v = x @ attn.w_q.T, x @ attn.w_k.T, x @ attn.w_v.T
+    k, v = x @ attn.w_k.T, x @ attn.w_v.T
     pos = np.tile(np.arange(seq), batch)
-    o = np.empty_like(q)
     group = nh // nkv
-    for hh in range(nh):
-        g = hh // group
-        qh = rope(q[:, hh * hd:(hh + 1) * hd], pos, attn.inv_freq)
-        kh = rope(k[:, g * hd:(g + 1) * hd], pos, attn.inv_freq)
-        vh = v[:, g * hd:(g + 1) * hd]
-        for b in range(batch):
-            rows = slice(b * seq, (b + 1) * seq)
-            o[rows, hh * hd:(hh + 1) * hd] = causal_attention(qh[rows], kh[rows], vh[rows])
-    return h + o @ attn.w_o.T
+    k_rot = [rope(k[:, g * hd:(g + 1) * hd], pos, attn.inv_freq) for g in range(nkv)]
+    if rows is None:
+        q = x @ attn.w_q.T
+        o = np.empty_like(q)
+        for hh in range(nh):
+            g = hh // group
+            qh = rope(q[:, hh * hd:(hh + 1) * hd], pos, attn.inv_freq)
+            vh = v[:, g * hd:(g + 1) * hd]
+            for b in range(batch):
+                sl = slice(b * seq, (b + 1) * seq)
+                o[sl, hh * hd:(hh + 1) * hd] = causal_attention(qh[sl], k_rot[g][sl], vh[sl])
+        return h + o @ attn.w_o.T
+    rows = np.asarray(rows)
+    out = np.full(h.shape, np.nan)
+    q = x[rows] @ attn.w_q.T
+    o = np.empty((len(rows), nh * hd))
+    for i, t in enumerate(rows):
+        b, s_ = divmod(int(t), seq)
+        keys = slice(b * seq, b * seq + s_ + 1)          # the token itself and the ones before it
+        for hh in range(nh):
+            g = hh // group
+            qh = rope(q[i:i + 1, hh * hd:(hh + 1) * hd], [s_], attn.inv_freq)[0]
+            sc = k_rot[g][keys] @ qh / math.sqrt(hd)
+            p = np.exp(sc - sc.max())
+            o[i, hh * hd:(hh + 1) * hd] = (p / p.sum()) @ v[keys, g * hd:(g + 1) * hd]
+    out[rows] = h[rows] + o @ attn.w_o.T
+    return out
 
 
 def dense_ffn_block(hbar, ffn: FFNParams, dims: Dims):

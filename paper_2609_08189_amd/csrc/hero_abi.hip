@@ -1,6 +1,7 @@
 // C ABI of the HeRo routed FFN stack: argument validation, workspace layout and
 // the per-layer kernel sequence.  Every argument check runs on the host before
 // any HIP call, so invalid calls never reach the GPU.
+#include <limits.h>
 #include <math.h>
 #include <stdint.h>
 #include <string.h>
@@ -576,3 +577,224 @@ int hero_history_state(const hero_dims* dims, int n, int T, const float* kv, con
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The full decoder: attention sub-block, pretrained FFN of non-routed blocks, decoder stack
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr int kAttnHeadDim = 128;
+constexpr int kAttnQTile = 128;   // queries per attention workgroup: the q/k/v row padding
+
+int check_attn_dims(const hero_dims* d, const hero_attn_dims* a) {
+  if (!a) return HERO_E_NULL;
+  if (a->n_heads <= 0 || a->n_kv_heads <= 0 || a->head_dim <= 0) return HERO_E_DIM;
+  if (a->n_heads % a->n_kv_heads) return HERO_E_DIM;
+  if (d->dtype != HERO_BF16 || a->head_dim != kAttnHeadDim || a->n_heads % 2) return HERO_E_UNSUPPORTED;
+  return HERO_OK;
+}
+
+int check_attn_weights(const hero_attn_weights* w) {
+  if (!w || !w->norm_w || !w->w_qkv || !w->w_o) return HERO_E_NULL;
+  if (!aligned16(w->norm_w) || !aligned16(w->w_qkv) || !aligned16(w->w_o)) return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+int check_rope(const float* inv_freq, int head_dim, hero::RopeTable* t) {
+  if (!inv_freq) return HERO_E_NULL;
+  for (int i = 0; i < head_dim / 2; ++i) {
+    if (!(inv_freq[i] == inv_freq[i]) || inv_freq[i] - inv_freq[i] != 0.f) return HERO_E_RANGE;
+    t->inv_freq[i] = inv_freq[i];
+  }
+  return HERO_OK;
+}
+
+struct DecLayout {
+  Layout L;            // the routed layer's workspace (its u region holds LN^attn(h) too)
+  int seq_pad;
+  size_t q, k, vt, o;  // attention intermediates
+  size_t ring, hA, hB, hbar_tmp;
+  size_t total;
+};
+
+DecLayout dec_layout_of(const hero_dims& d, const hero_attn_dims& a, int n_layers, int batch, int seq) {
+  DecLayout D{};
+  const size_t T = static_cast<size_t>(batch) * seq;
+  D.L = layout_of(d, static_cast<int>(T), false);
+  D.seq_pad = (seq + kAttnQTile - 1) / kAttnQTile * kAttnQTile;
+  size_t off = D.L.total;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  const size_t hd = a.head_dim, sp = D.seq_pad, B = batch;
+  D.q = take(B * a.n_heads * sp * hd * 2);
+  D.k = take(B * a.n_kv_heads * sp * hd * 2);
+  D.vt = take(B * a.n_kv_heads * hd * sp * 2);
+  D.o = take(T * a.n_heads * hd * 2);
+  if (n_layers > 0) {
+    const size_t hb = T * d.d * 2;
+    D.ring = take(3 * hb);
+    D.hA = take(hb);
+    D.hB = take(hb);
+    D.hbar_tmp = take(hb);
+  }
+  D.total = off;
+  return D;
+}
+
+// hbar = h + Attn(LN^attn(h)) over batch x seq tokens
+int run_attention(const hero_dims& dm, const hero_attn_dims& a, int batch, int seq, const void* h, void* hbar,
+                  const hero_attn_weights& w, const hero::RopeTable& rope, unsigned char* ws,
+                  const DecLayout& DL, hipStream_t st) {
+  using namespace hero;
+  const int T = batch * seq;
+  void* x = ws + DL.L.u;
+  float* rowstat = reinterpret_cast<float*>(ws + DL.L.rowstat);
+  void *q = ws + DL.q, *k = ws + DL.k, *vt = ws + DL.vt, *o = ws + DL.o;
+  hipError_t e = timed(HERO_K_ATTN_NORM, st, [&] {
+    return launch_rowstats(dm.dtype, h, nullptr, nullptr, w.norm_w, T, dm.d, 1, dm.eps_norm, rowstat, x, st);
+  });
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = timed(HERO_K_ATTN_QKV, st, [&] {
+    return launch_attn_qkv(x, w.w_qkv, T, dm.d, seq, DL.seq_pad, a.n_heads, a.n_kv_heads, rope, q, k, vt, st);
+  });
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = timed(HERO_K_ATTN_CORE, st, [&] {
+    return launch_attn_core(q, k, vt, o, batch, seq, DL.seq_pad, a.n_heads, a.n_kv_heads, st);
+  });
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = timed(HERO_K_ATTN_OUT, st, [&] {
+    return launch_attn_out(o, w.w_o, h, hbar, T, dm.d, a.n_heads, st);
+  });
+  return e == hipSuccess ? HERO_OK : HERO_E_LAUNCH;
+}
+
+// The pretrained FFN of a non-routed block: h = hbar + FFN(LN^ffn(hbar)), every token
+int run_dense_ffn(const hero_dims& dm, int T, const void* hbar, void* h, const hero_ffn_weights& f,
+                  unsigned char* ws, const Layout& L, hipStream_t st) {
+  using namespace hero;
+  void* u = ws + L.u;
+  void* act = ws + L.act;
+  float* part = reinterpret_cast<float*>(ws + L.part);
+  float* rowstat = reinterpret_cast<float*>(ws + L.rowstat);
+  hipError_t e = timed(HERO_K_ROWSTATS, st, [&] {
+    return launch_rowstats(dm.dtype, hbar, nullptr, nullptr, f.norm_w, T, dm.d, 1, dm.eps_norm, rowstat, u, st);
+  });
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = timed(HERO_K_FFN_GATE_UP, st, [&] {
+    return launch_ffn_gateup(dm.dtype, u, nullptr, nullptr, T, f.w_gate, f.w_up, act, part, dm.d, dm.d_ff, st);
+  });
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = timed(HERO_K_FFN_DOWN, st, [&] {
+    return launch_ffn_down(dm.dtype, act, nullptr, nullptr, T, f.w_down, hbar, nullptr, h, part, dm.d,
+                           dm.d_ff, st);
+  });
+  return e == hipSuccess ? HERO_OK : HERO_E_LAUNCH;
+}
+
+}  // namespace
+
+int hero_decoder_workspace_size(const hero_dims* dims, const hero_attn_dims* adims, int n_layers, int batch,
+                                int seq, size_t* bytes) {
+  if (!bytes) return HERO_E_NULL;
+  int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if ((st = check_attn_dims(dims, adims)) != HERO_OK) return st;
+  if (batch <= 0 || seq <= 0 || n_layers < 0) return HERO_E_DIM;
+  if (static_cast<long long>(batch) * seq > INT_MAX / 2) return HERO_E_DIM;
+  *bytes = dec_layout_of(*dims, *adims, n_layers, batch, seq).total;
+  return HERO_OK;
+}
+
+int hero_attention_block(const hero_dims* dims, const hero_attn_dims* adims, int batch, int seq, const void* h,
+                         void* hbar, const hero_attn_weights* attn, const float* inv_freq, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if ((st = check_attn_dims(dims, adims)) != HERO_OK) return st;
+  if (batch <= 0 || seq <= 0) return HERO_E_DIM;
+  if (static_cast<long long>(batch) * seq > INT_MAX / 2) return HERO_E_DIM;
+  if (!h || !hbar) return HERO_E_NULL;
+  if (!aligned16(h) || !aligned16(hbar)) return HERO_E_ALIGN;
+  if ((st = check_attn_weights(attn)) != HERO_OK) return st;
+  hero::RopeTable rope{};
+  if ((st = check_rope(inv_freq, adims->head_dim, &rope)) != HERO_OK) return st;
+  const size_t hb = static_cast<size_t>(batch) * seq * dims->d * 2;
+  if (overlap(h, hb, hbar, hb)) return HERO_E_ALIAS;
+  const DecLayout DL = dec_layout_of(*dims, *adims, 0, batch, seq);
+  if (!workspace || workspace_bytes < DL.total) return HERO_E_WORKSPACE;
+  if (!aligned16(workspace)) return HERO_E_ALIGN;
+  if (overlap(hbar, hb, workspace, DL.total) || overlap(h, hb, workspace, DL.total)) return HERO_E_ALIAS;
+  if ((st = check_device()) != HERO_OK) return st;
+  return run_attention(*dims, *adims, batch, seq, h, hbar, *attn, rope, static_cast<unsigned char*>(workspace),
+                       DL, static_cast<hipStream_t>(stream));
+}
+
+int hero_decoder_stack(const hero_dims* dims, const hero_attn_dims* adims, int n_layers, int batch, int seq,
+                       const void* h_in, void* h_out, const hero_state* state, const hero_attn_weights* attn,
+                       const hero_ffn_weights* ffn, const hero_router_weights* router,
+                       const hero_adapter_weights* adapter, const float* eta, const float* inv_freq,
+                       const hero_routing* routing, const hero_layer_stats* stats, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if ((st = check_attn_dims(dims, adims)) != HERO_OK) return st;
+  if (batch <= 0 || seq <= 0) return HERO_E_DIM;
+  if (static_cast<long long>(batch) * seq > INT_MAX / 2) return HERO_E_DIM;
+  if (n_layers < dims->L_R) return HERO_E_RANGE;
+  if (!h_in || !h_out || !attn || !ffn || !adapter || !eta || !router) return HERO_E_NULL;
+  if (!aligned16(h_in) || !aligned16(h_out)) return HERO_E_ALIGN;
+  if ((st = check_state(state)) != HERO_OK) return st;
+  if ((st = check_routing(routing)) != HERO_OK) return st;
+  hero::RopeTable rope{};
+  if ((st = check_rope(inv_freq, adims->head_dim, &rope)) != HERO_OK) return st;
+  const int first = n_layers - dims->L_R;   // index of the first routed block
+  for (int l = 0; l < n_layers; ++l) {
+    if ((st = check_attn_weights(&attn[l])) != HERO_OK) return st;
+    if (l < first) {
+      if (!ffn[l].norm_w || !ffn[l].w_gate || !ffn[l].w_up || !ffn[l].w_down) return HERO_E_NULL;
+      if (!aligned16(ffn[l].norm_w) || !aligned16(ffn[l].w_gate) || !aligned16(ffn[l].w_up) ||
+          !aligned16(ffn[l].w_down))
+        return HERO_E_ALIGN;
+    } else {
+      const int j = l - first;
+      if ((st = check_weights(&ffn[l], router, &adapter[j])) != HERO_OK) return st;
+      if (!(eta[j] == eta[j])) return HERO_E_RANGE;
+      if (stats && (st = check_stats(&stats[j])) != HERO_OK) return st;
+    }
+  }
+  const int T = batch * seq;
+  const size_t hb = static_cast<size_t>(T) * dims->d * 2;
+  if (overlap(h_out, hb, h_in, hb)) return HERO_E_ALIAS;
+  const DecLayout DL = dec_layout_of(*dims, *adims, n_layers, batch, seq);
+  if (!workspace || workspace_bytes < DL.total) return HERO_E_WORKSPACE;
+  if (!aligned16(workspace)) return HERO_E_ALIGN;
+  if (overlap(h_out, hb, workspace, DL.total) || overlap(h_in, hb, workspace, DL.total)) return HERO_E_ALIAS;
+  if ((st = check_device()) != HERO_OK) return st;
+
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char* ring[3] = {ws + DL.ring, ws + DL.ring + hb, ws + DL.ring + 2 * hb};
+  unsigned char* hbuf[2] = {ws + DL.hA, ws + DL.hB};
+  const void* h = h_in;
+  for (int l = 0; l < n_layers; ++l) {
+    void* out = l == n_layers - 1 ? h_out : static_cast<void*>(hbuf[l & 1]);
+    if (l < first) {
+      void* hbar = ws + DL.hbar_tmp;
+      if ((st = run_attention(*dims, *adims, batch, seq, h, hbar, attn[l], rope, ws, DL, s)) != HERO_OK) return st;
+      if ((st = run_dense_ffn(*dims, T, hbar, out, ffn[l], ws, DL.L, s)) != HERO_OK) return st;
+    } else {
+      const int j = l - first + 1;
+      void* hbar = ring[(j - 1) % 3];
+      if ((st = run_attention(*dims, *adims, batch, seq, h, hbar, attn[l], rope, ws, DL, s)) != HERO_OK) return st;
+      LayerCall c{dims, j, T, hbar, j >= 2 ? ring[(j - 2) % 3] : nullptr, j >= 3 ? ring[(j - 3) % 3] : nullptr,
+                  out, state, &ffn[l], router, &adapter[j - 1], eta[j - 1], routing,
+                  stats ? &stats[j - 1] : nullptr, ws, &DL.L, s};
+      if ((st = run_layer(c)) != HERO_OK) return st;
+    }
+    h = out;
+  }
+  return HERO_OK;
+}

@@ -94,6 +94,24 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
                            int n_max, const void* w_down, const void* hbar, const float* gate,
                            void* h_out, float* part, int d, int d_ff, hipStream_t s);
 
+// FFN of a non-routed block: the two launchers above with idx_ffn = counts = gate = null
+// (every row, t = m, g = 1).
+
+// Attention sub-block of a decoder block (bf16, head width 128).  Token t = b seq + pos.
+struct RopeTable {
+  float inv_freq[64];   // [head_dim / 2] rotary frequencies
+};
+// [q; k; v] = x [W_q; W_k; W_v]^T with the rotary embedding on q, k; q [B][nh][seq_pad][128],
+// k [B][nkv][seq_pad][128], vt [B][nkv][128][seq_pad] (rows past seq are not written)
+hipError_t launch_attn_qkv(const void* x, const void* w_qkv, int T, int d, int seq, int seq_pad, int nh,
+                           int nkv, const RopeTable& rope, void* q, void* k, void* vt, hipStream_t s);
+// o[t][h 128 + c] = causal softmax(q k^T / sqrt(128)) v, head h reading kv head h / (nh / nkv)
+hipError_t launch_attn_core(const void* q, const void* k, const void* vt, void* o, int batch, int seq,
+                            int seq_pad, int nh, int nkv, hipStream_t s);
+// hbar = h + o W_o^T
+hipError_t launch_attn_out(const void* o, const void* w_o, const void* h, void* hbar, int T, int d, int nh,
+                           hipStream_t s);
+
 // Adapter branch: h_out[t] = hbar[t] + (1 - g[t]) * W_2 SiLU(W_1 u_t) for t = idx_ad[m].
 // part: fp32 scratch of adapter_part_floats(dtype, d, d_r, T) floats.
 size_t adapter_part_floats(int dtype, int d, int d_r, int T);

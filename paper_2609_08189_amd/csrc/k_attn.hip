@@ -1,0 +1,252 @@
+// Causal grouped-query attention of a decoder block (Sec. 3.1, eq:dense_attention): for every
+// sequence, query head h and position t, o_t = sum_{i <= t} softmax_i(q_t . k_i / sqrt(128)) v_i
+// with key/value head h / (n_h / n_kv).  Head width 128, bf16 operands, fp32 softmax.
+//
+// One workgroup (4 waves) takes 128 consecutive queries of one head; wave w owns 32 of them.
+// Keys stream through LDS in tiles of 64 (K [64][128] and V^T [128][64], double-buffered,
+// filled by global_load_lds_dwordx4), with an online softmax, so the scores never leave
+// registers:
+//   * scores are formed transposed, S^T = K Q^T, on v_mfma_f32_32x32x16_bf16; in the
+//     accumulator layout lane l then holds query l % 32, so a query's running max and sum are
+//     lane-local (plus one exchange with lane l ^ 32, which holds the other 16 keys);
+//   * the output is also formed transposed, O^T = V^T P^T, so the rescaling of a query's
+//     partial output by exp(m_old - m_new) is lane-local too;
+//   * P^T goes from the score accumulators straight into the B operand of the second product:
+//     the contraction over keys takes the keys in the order the accumulator holds them (four
+//     consecutive, then four 8 further on), and the V^T fragments are read in that same order.
+// The LDS rows are XOR-swizzled in 16-byte chunks: K rows (256 B) by row % 16, which makes the
+// 32-row fragment reads conflict free; V^T rows (128 B) by (row / 2) % 8 (two-way at most).
+#include "hero_device.h"
+#include "hero_kernels.h"
+
+namespace hero {
+namespace {
+
+constexpr int HD = 128;                  // head width
+constexpr int QT = 128;                  // queries per workgroup
+constexpr int KT = 64;                   // keys per tile
+constexpr int NTA = 256;                 // 4 waves
+constexpr int K_BYTES = KT * HD * 2;     // K tile [64][128] bf16
+constexpr int V_BYTES = HD * KT * 2;     // V^T tile [128][64] bf16
+constexpr int STG = K_BYTES + V_BYTES;
+constexpr int OPITCH = HD + 8;           // output staging row pitch (bf16 elements)
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void load_lds16(const void* g, unsigned char* l) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void*)(l), 16, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 pack8(const float* x) {
+  bf16x8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = __builtin_bit_cast(__bf16, f32_to_bf16(x[e]));
+  return r;
+}
+
+__global__ __launch_bounds__(NTA) void attn_fwd_kernel(const bf16_t* __restrict__ q,
+                                                      const bf16_t* __restrict__ k,
+                                                      const bf16_t* __restrict__ vt,
+                                                      bf16_t* __restrict__ o, int seq, int seq_pad,
+                                                      int nh, int nkv, float scale_log2) {
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STG];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int hl = lane >> 5, col = lane & 31;
+  const int n_qt = gridDim.x;
+  const int qt = n_qt - 1 - static_cast<int>(blockIdx.x);   // the longest rows first
+  const int head = blockIdx.y, b = blockIdx.z;
+  const int kvh = head / (nh / nkv);
+  const int q0 = qt * QT;
+  const int wq0 = q0 + 32 * wave;                 // this wave's first query
+  const int my_q = wq0 + col;                     // the query this lane's columns hold
+
+  const bf16_t* qb = q + (static_cast<size_t>(b) * nh + head) * seq_pad * HD;
+  const bf16_t* kb = k + (static_cast<size_t>(b) * nkv + kvh) * seq_pad * HD;
+  const bf16_t* vb = vt + (static_cast<size_t>(b) * nkv + kvh) * HD * seq_pad;
+
+  // keys needed by this workgroup: 0 .. min(q0 + 127, seq - 1)
+  const int n_kt = (min(q0 + QT, seq) + KT - 1) / KT;
+
+  auto issue = [&](int stage, int k0) {
+    unsigned char* st = smem + stage * STG;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int blk = 4 * wave + i;
+      const int r = 4 * blk + (lane >> 4), p = lane & 15;
+      const int c = p ^ (r & 15);
+      load_lds16(kb + static_cast<size_t>(k0 + r) * HD + 8 * c, st + blk * 1024);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int blk = 4 * wave + i;
+      const int r = 8 * blk + (lane >> 3), p = lane & 7;
+      const int c = p ^ ((r >> 1) & 7);
+      load_lds16(vb + static_cast<size_t>(r) * seq_pad + k0 + 8 * c, st + K_BYTES + blk * 1024);
+    }
+  };
+
+  issue(0, 0);
+
+  // this lane's query as the B operand of S^T = K Q^T: hd 16 s + 8 hl .. + 8, s = 0..7
+  bf16x8 qf[8];
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+    qf[s] = *reinterpret_cast<const bf16x8*>(qb + static_cast<size_t>(my_q) * HD + 16 * s + 8 * hl);
+
+  f32x16 acc_o[4];
+#pragma unroll
+  for (int t4 = 0; t4 < 4; ++t4)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc_o[t4][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  for (int kt = 0; kt < n_kt; ++kt) {
+    const int k0 = kt * KT;
+    if (kt + 1 < n_kt) issue((kt + 1) & 1, k0 + KT);
+    const unsigned char* st = smem + (kt & 1) * STG;
+    // keys past this wave's last query are all masked: nothing to add
+    if (k0 <= wq0 + 31) {
+      f32x16 sacc[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sacc[t][r] = 0.f;
+        const int r = 32 * t + col;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const int c = 2 * s + hl;
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(st + 256 * r + 16 * (c ^ (r & 15)));
+          sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[t], 0, 0, 0);
+        }
+      }
+      // scale (to base 2), causal / length mask, running max
+      const bool edge = k0 + KT - 1 > wq0 || k0 + KT > seq;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float x = sacc[t][r] * scale_log2;
+          if (edge) {
+            const int key = k0 + 32 * t + 8 * (r >> 2) + 4 * hl + (r & 3);
+            if (key > my_q || key >= seq) x = -INFINITY;
+          }
+          sacc[t][r] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = exp2f(m_run - m_new);
+      float ps = 0.f;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = exp2f(sacc[t][r] - m_new);
+          sacc[t][r] = p;
+          ps += p;
+        }
+      ps += __shfl_xor(ps, 32, 64);
+      l_run = l_run * alpha + ps;
+      m_run = m_new;
+#pragma unroll
+      for (int t4 = 0; t4 < 4; ++t4)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc_o[t4][r] *= alpha;
+      // P^T as B operands: k-step (t, u) takes accumulator registers 8u .. 8u + 7 of tile t
+      bf16x8 pf[2][2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          float x[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[e] = sacc[t][8 * u + e];
+          pf[t][u] = pack8(x);
+        }
+      // O^T += V^T P^T; the V^T fragment of k-step (t, u) holds keys 32t + 16u + 4hl + {0..3}
+      // and the same + 8
+#pragma unroll
+      for (int t4 = 0; t4 < 4; ++t4) {
+        const int r = 32 * t4 + col;
+        const unsigned char* vrow = st + K_BYTES + 128 * r;
+        const int sw = (r >> 1) & 7;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const int c1 = 4 * t + 2 * u;
+            const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow + 16 * (c1 ^ sw) + 8 * hl);
+            const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16 * ((c1 + 1) ^ sw) + 8 * hl);
+            bf16x8 vf;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              vf[e] = lo[e];
+              vf[4 + e] = hi[e];
+            }
+            if (k0 + KT > seq) {
+              // V^T columns past the sequence hold whatever the buffer held: zero them, so that
+              // their zero probabilities cannot meet a NaN
+#pragma unroll
+              for (int e = 0; e < 8; ++e)
+                if (k0 + 32 * t + 16 * u + 4 * hl + (e & 3) + 8 * (e >> 2) >= seq) vf[e] = 0;
+            }
+            acc_o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t][u], acc_o[t4], 0, 0, 0);
+          }
+      }
+    }
+    // every wave is done with this stage and the next tile has landed
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  }
+
+  // normalise and stage the wave's [32 queries][128] block, then write 16-byte row pieces
+  const float inv_l = 1.0f / l_run;
+  bf16_t* stg = reinterpret_cast<bf16_t*>(smem) + wave * 32 * OPITCH;
+#pragma unroll
+  for (int t4 = 0; t4 < 4; ++t4)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int c = 32 * t4 + 8 * g + 4 * hl;
+      uint32_t w0 = static_cast<uint32_t>(f32_to_bf16(acc_o[t4][4 * g + 0] * inv_l)) |
+                    (static_cast<uint32_t>(f32_to_bf16(acc_o[t4][4 * g + 1] * inv_l)) << 16);
+      uint32_t w1 = static_cast<uint32_t>(f32_to_bf16(acc_o[t4][4 * g + 2] * inv_l)) |
+                    (static_cast<uint32_t>(f32_to_bf16(acc_o[t4][4 * g + 3] * inv_l)) << 16);
+      uint32_t* dst = reinterpret_cast<uint32_t*>(stg + col * OPITCH + c);
+      dst[0] = w0;
+      dst[1] = w1;
+    }
+  __syncthreads();
+  const size_t ld_o = static_cast<size_t>(nh) * HD;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int e = lane + 64 * i;
+    const int row = e >> 4, piece = e & 15;
+    const int tq = wq0 + row;
+    if (tq < seq) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(stg + row * OPITCH + 8 * piece);
+      *reinterpret_cast<u32x4*>(o + (static_cast<size_t>(b) * seq + tq) * ld_o + head * HD + 8 * piece) = v;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attn_core(const void* q, const void* k, const void* vt, void* o, int batch, int seq,
+                            int seq_pad, int nh, int nkv, hipStream_t s) {
+  if (batch <= 0 || seq <= 0) return hipSuccess;
+  if (seq_pad % QT != 0 || seq_pad < seq || nkv <= 0 || nh % nkv != 0) return hipErrorInvalidValue;
+  const dim3 grid(seq_pad / QT, nh, batch);
+  const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(HD));
+  attn_fwd_kernel<<<grid, NTA, 0, s>>>(static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
+                                       static_cast<const bf16_t*>(vt), static_cast<bf16_t*>(o), seq,
+                                       seq_pad, nh, nkv, scale_log2);
+  return hipGetLastError();
+}
+
+}  // namespace hero

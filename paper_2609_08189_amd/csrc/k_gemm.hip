@@ -100,6 +100,8 @@ struct EpiSiLU {  // hid[m][n] = SiLU(acc)
 };
 
 // h_out[t][n] = hbar[t][n] + scale(g_t) * acc, t = idx[m]; FFN scales by g, adapter by 1 - g.
+// Without an index list t = m, and without gates the scale is 1 (a plain residual add: the
+// dense FFN of a non-routed block, the attention output projection).
 // The MFMA path fetches each 8-column piece of hbar (prep) before it stages the accumulators,
 // so that the loads of a whole wave tile are in flight together.
 template <typename T, bool ADAPTER>
@@ -110,8 +112,8 @@ struct EpiScatter {
   T* out;
   int ld;
   __device__ __forceinline__ void store(int m, int n, float v) const {
-    const int t = idx[m];
-    const float g = gate[t];
+    const int t = idx ? idx[m] : m;
+    const float g = gate ? gate[t] : (ADAPTER ? 0.0f : 1.0f);
     const float sc = ADAPTER ? 1.0f - g : g;
     const size_t o = static_cast<size_t>(t) * ld + n;
     stf(out + o, ldf(hbar + o) + sc * v);
@@ -122,8 +124,8 @@ struct EpiScatter {
     float sc;
   };
   __device__ __forceinline__ Pre prep(int m, int n) const {
-    const int t = idx[m];
-    const float g = gate[t];
+    const int t = idx ? idx[m] : m;
+    const float g = gate ? gate[t] : (ADAPTER ? 0.0f : 1.0f);
     Pre p;
     p.row = static_cast<uint32_t>(t);
     p.sc = ADAPTER ? 1.0f - g : g;
@@ -946,7 +948,7 @@ int down_split(int n, int d, int d_ff) {
 __global__ __launch_bounds__(256) void swiglu_reduce(const float* __restrict__ P, int S,
                                                     size_t stride, const int* __restrict__ m_count,
                                                     int n_max, int d_ff, bf16_t* __restrict__ act) {
-  const int M = min(*m_count, n_max);
+  const int M = m_count ? min(*m_count, n_max) : n_max;
   const int q = d_ff / 8;
   const size_t e = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
   const int m = static_cast<int>(e / q), c = static_cast<int>(e % q) * 8;
@@ -981,7 +983,7 @@ __global__ __launch_bounds__(256) void scatter_reduce(const float* __restrict__ 
                                                      const bf16_t* __restrict__ hbar,
                                                      const float* __restrict__ gate,
                                                      bf16_t* __restrict__ out, int d) {
-  const int M = min(*m_count, n_max);
+  const int M = m_count ? min(*m_count, n_max) : n_max;
   const int q = d / 8;
   const size_t e = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
   const int m = static_cast<int>(e / q), n = static_cast<int>(e % q) * 8;
@@ -992,8 +994,8 @@ __global__ __launch_bounds__(256) void scatter_reduce(const float* __restrict__ 
     y0 += *reinterpret_cast<const f32x4*>(p + z * stride);
     y1 += *reinterpret_cast<const f32x4*>(p + z * stride + 4);
   }
-  const int t = idx[m];
-  const float sc = gate[t];
+  const int t = idx ? idx[m] : m;
+  const float sc = gate ? gate[t] : 1.0f;
   const size_t o = static_cast<size_t>(t) * d + n;
   const u32x4 h = *reinterpret_cast<const u32x4*>(hbar + o);
   u32x4 w;
@@ -1079,6 +1081,74 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
   EpiScatter<float, false> epi{idx_ffn, static_cast<const float*>(hbar), gate,
                                static_cast<float*>(h_out), d};
   return run_f32<false>(A, B, epi, counts, n_max, d, d_ff, s);
+}
+
+// ---------------------------------------------------------------------------
+// Attention projections of a decoder block (Sec. 3.1, eq:dense_attention).
+// [q; k; v] = x [W_q; W_k; W_v]^T runs on the GEMM core with an epilogue that applies the
+// rotary embedding to q and k (pair (2i, 2i+1) of a head turned by pos * inv_freq[i], in
+// fp32) and writes each head where the attention kernel reads it: q [B][n_h][S_pad][128],
+// k [B][n_kv][S_pad][128] and v transposed, [B][n_kv][128][S_pad].  The output projection
+// adds its product to the block input: hbar = h + o W_o^T.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr int kHeadDim = 128;
+
+struct EpiQKV {
+  bf16_t* q;
+  bf16_t* k;
+  bf16_t* vt;
+  int seq, seq_pad, nh, nkv;
+  RopeTable rope;
+  struct Pre {};
+  __device__ __forceinline__ Pre prep(int, int) const { return {}; }
+  __device__ __forceinline__ void store(int, int, float) const {}
+  __device__ __forceinline__ void emit8(const Pre&, int m, int n, const float* v) const {
+    const int b = m / seq, pos = m - b * seq;
+    const int head = n / kHeadDim, c = n % kHeadDim;
+    if (head < nh + nkv) {
+      u32x4 w;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float sn, cs;
+        sincosf(static_cast<float>(pos) * rope.inv_freq[c / 2 + i], &sn, &cs);
+        const float a = v[2 * i], bb = v[2 * i + 1];
+        w[i] = static_cast<uint32_t>(f32_to_bf16(a * cs - bb * sn)) |
+               (static_cast<uint32_t>(f32_to_bf16(a * sn + bb * cs)) << 16);
+      }
+      bf16_t* dst = head < nh
+          ? q + ((static_cast<size_t>(b) * nh + head) * seq_pad + pos) * kHeadDim + c
+          : k + ((static_cast<size_t>(b) * nkv + (head - nh)) * seq_pad + pos) * kHeadDim + c;
+      *reinterpret_cast<u32x4*>(dst) = w;
+    } else {
+      bf16_t* dst = vt + ((static_cast<size_t>(b) * nkv + (head - nh - nkv)) * kHeadDim + c) * seq_pad + pos;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dst[static_cast<size_t>(e) * seq_pad] = f32_to_bf16(v[e]);
+    }
+  }
+};
+
+}  // namespace
+
+hipError_t launch_attn_qkv(const void* x, const void* w_qkv, int T, int d, int seq, int seq_pad, int nh,
+                           int nkv, const RopeTable& rope, void* q, void* k, void* vt, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  ARows<bf16_t> A{static_cast<const bf16_t*>(x), nullptr, d};
+  BRows<bf16_t> B{static_cast<const bf16_t*>(w_qkv), nullptr, INT_MAX, d};
+  EpiQKV epi{static_cast<bf16_t*>(q), static_cast<bf16_t*>(k), static_cast<bf16_t*>(vt), seq, seq_pad,
+             nh, nkv, rope};
+  return run_big<256, false>(A, B, epi, nullptr, T, (nh + 2 * nkv) * kHeadDim, d, s);
+}
+
+hipError_t launch_attn_out(const void* o, const void* w_o, const void* h, void* hbar, int T, int d, int nh,
+                           hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  const int K = nh * kHeadDim;
+  ARows<bf16_t> A{static_cast<const bf16_t*>(o), nullptr, K};
+  BRows<bf16_t> B{static_cast<const bf16_t*>(w_o), nullptr, INT_MAX, K};
+  EpiScatter<bf16_t, false> epi{nullptr, static_cast<const bf16_t*>(h), nullptr, static_cast<bf16_t*>(hbar), d};
+  return run_big<256, false>(A, B, epi, nullptr, T, d, K, s);
 }
 
 // Wide adapters (ranks above 128, in steps of 128: the paper's d_r = 896).  The down-projection

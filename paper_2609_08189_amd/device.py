@@ -226,3 +226,82 @@ class DeviceProblem:
             if len(hs) > 3:
                 hs.pop(0)
         return io
+
+
+class DeviceDecoder:
+    """A full-decoder problem (synth workload with n_layers > 0) on the GPU: attention and FFN
+    weights of every block, adapters of the routed ones, the router state and the ABI structs."""
+
+    def __init__(self, prob: synth.Problem, device: str = "cuda:0", stats: bool = True):
+        w = prob.w
+        assert w.n_layers > 0 and w.dtype == "bf16"
+        self.w = w
+        self.device = device
+        self.T = T = prob.hbar.shape[0]
+        self.dims = dims_struct(w)
+        self.adims = H.hero_attn_dims(w.n_heads, w.n_kv_heads, w.head_dim)
+        self.h_in = upload(prob.hbar, device)
+        self.h_out = torch.empty_like(self.h_in)
+        self.router = {k: upload(v if k != "th1" else pad_th1(v, w), device) for k, v in prob.router.items()}
+        self.router_s = H.hero_router_weights(**{k: self.router[k].data_ptr() for k in H.ROUTER_FIELDS})
+        self.attn, self.attn_s, self.ffn, self.ffn_s = [], [], [], []
+        for l in range(w.n_layers):
+            a = {k: upload(v, device) for k, v in prob.attn[l].items()}
+            self.attn.append(a)
+            self.attn_s.append(H.hero_attn_weights(a["norm_w"].data_ptr(), a["w_qkv"].data_ptr(),
+                                                   a["w_o"].data_ptr()))
+            f = {k: upload(v, device) for k, v in prob.ffn[l].items()}
+            self.ffn.append(f)
+            self.ffn_s.append(H.hero_ffn_weights(f["norm_w"].data_ptr(), f["w_gate"].data_ptr(),
+                                                 f["w_up"].data_ptr(), f["w_down"].data_ptr()))
+        self.adapter = [{k: upload(v, device) for k, v in prob.adapter[j].items()} for j in range(w.L_R)]
+        self.adapter_s = [H.hero_adapter_weights(a["w1"].data_ptr(), a["w2"].data_ptr()) for a in self.adapter]
+        self.eta = [float(e) for e in prob.eta]
+        self.inv_freq = [float(x) for x in prob.inv_freq]
+        self.S = torch.zeros((T, w.d_m, w.d_m), dtype=torch.bfloat16 if w.state_dtype == "bf16" else torch.float32,
+                             device=device)
+        self.zeta = torch.zeros((T, w.d_m), dtype=torch.float32, device=device)
+        self.p_hist = torch.ones(T, dtype=torch.float32, device=device)
+        self.m_hist = torch.ones(T, dtype=torch.float32, device=device)
+        self.state_s = H.hero_state(self.S.data_ptr(), self.zeta.data_ptr(), self.p_hist.data_ptr(),
+                                    self.m_hist.data_ptr())
+        self.beta = torch.from_numpy(prob.beta).to(device) if prob.beta is not None else None
+        mode = H.HERO_MODE_BUDGET if w.mode == "budget" else H.HERO_MODE_THRESHOLD
+        self.routing_s = H.hero_routing(mode, w.tau, w.budget,
+                                        self.beta.data_ptr() if self.beta is not None else None, w.ablation)
+        self.stats = [LayerStats(T, device) for _ in range(w.L_R)] if stats else None
+        self.ws_bytes = H.hero_decoder_workspace_size(self.dims, self.adims, w.n_layers, w.batch, w.seq)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+
+    def stream(self):
+        return torch.cuda.current_stream(torch.device(self.device)).cuda_stream
+
+    def run(self, check: bool = True) -> int:
+        w = self.w
+        st = H.hero_decoder_stack(self.dims, self.adims, w.n_layers, w.batch, w.seq, self.h_in, self.h_out,
+                                  self.state_s, self.attn_s, self.ffn_s, self.router_s, self.adapter_s, self.eta,
+                                  self.inv_freq, self.routing_s, [s.struct for s in self.stats] if self.stats else None,
+                                  self.ws, self.ws_bytes, self.stream())
+        if check:
+            H.check(st, "hero_decoder_stack")
+        return st
+
+    def attention(self, layer: int, h=None, hbar=None) -> torch.Tensor:
+        """One attention sub-block on h (default: the decoder input); returns hbar."""
+        w = self.w
+        h = self.h_in if h is None else h
+        hbar = torch.empty_like(h) if hbar is None else hbar
+        H.check(H.hero_attention_block(self.dims, self.adims, w.batch, w.seq, h, hbar, self.attn_s[layer],
+                                       self.inv_freq, self.ws, self.ws_bytes, self.stream()),
+                "hero_attention_block")
+        return hbar
+
+    def results(self) -> Dict[str, object]:
+        torch.cuda.synchronize()
+        out = dict(h=download_f64(self.h_out), S=self.S.float().cpu().numpy().astype(np.float64),
+                   zeta=self.zeta.cpu().numpy().astype(np.float64),
+                   p_hist=self.p_hist.cpu().numpy().astype(np.float64),
+                   m_hist=self.m_hist.cpu().numpy().astype(np.float64))
+        if self.stats:
+            out["layers"] = [s.host() for s in self.stats]
+        return out

@@ -38,7 +38,8 @@ HERO_ABL_NO_MEMREAD = 4
 HERO_ABL_NO_HISTORY = 8
 
 KERNELS = ("rowstats", "router_gemm", "router_pre", "router_mem", "router_post", "select",
-           "ffn_gate_up", "ffn_down", "adapter_down", "adapter_up")
+           "ffn_gate_up", "ffn_down", "adapter_down", "adapter_up",
+           "attn_norm", "attn_qkv", "attn_core", "attn_out")
 HERO_K = {name: i for i, name in enumerate(KERNELS)}
 
 _vp = ctypes.c_void_p
@@ -80,6 +81,14 @@ class hero_history(ctypes.Structure):
 class hero_routing(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int), ("tau", ctypes.c_float), ("budget", ctypes.c_double),
                 ("logit_bias", _vp), ("ablation", ctypes.c_int)]
+
+
+class hero_attn_dims(ctypes.Structure):
+    _fields_ = [("n_heads", ctypes.c_int), ("n_kv_heads", ctypes.c_int), ("head_dim", ctypes.c_int)]
+
+
+class hero_attn_weights(ctypes.Structure):
+    _fields_ = [("norm_w", _vp), ("w_qkv", _vp), ("w_o", _vp)]
 
 
 class hero_layer_stats(ctypes.Structure):
@@ -132,6 +141,18 @@ def lib() -> ctypes.CDLL:
         L.hero_history_state.restype = ctypes.c_int
         L.hero_history_state.argtypes = [P(hero_dims), ctypes.c_int, ctypes.c_int, _vp, P(ctypes.c_float),
                                          _vp, _vp, _vp]
+        L.hero_decoder_workspace_size.restype = ctypes.c_int
+        L.hero_decoder_workspace_size.argtypes = [P(hero_dims), P(hero_attn_dims), ctypes.c_int, ctypes.c_int,
+                                                  ctypes.c_int, P(ctypes.c_size_t)]
+        L.hero_attention_block.restype = ctypes.c_int
+        L.hero_attention_block.argtypes = [P(hero_dims), P(hero_attn_dims), ctypes.c_int, ctypes.c_int, _vp, _vp,
+                                           P(hero_attn_weights), P(ctypes.c_float), _vp, ctypes.c_size_t, _vp]
+        L.hero_decoder_stack.restype = ctypes.c_int
+        L.hero_decoder_stack.argtypes = [P(hero_dims), P(hero_attn_dims), ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                         _vp, _vp, P(hero_state), P(hero_attn_weights), P(hero_ffn_weights),
+                                         P(hero_router_weights), P(hero_adapter_weights), P(ctypes.c_float),
+                                         P(ctypes.c_float), P(hero_routing), P(hero_layer_stats), _vp,
+                                         ctypes.c_size_t, _vp]
         _lib = L
     return _lib
 
@@ -246,3 +267,38 @@ def hero_routed_stack_hist(dims: hero_dims, T: int, h_in, h_out, history: hero_h
 def hero_history_state(dims: hero_dims, n: int, T: int, kv, eta: Sequence[float], S, zeta, stream=None) -> int:
     """Matrix-form state after n layers from a history (eta: eta_1 .. eta_n)."""
     return lib().hero_history_state(ctypes.byref(dims), n, T, ptr(kv), _floats(eta), ptr(S), ptr(zeta), stream)
+
+
+def hero_decoder_workspace_size(dims: hero_dims, adims: hero_attn_dims, n_layers: int, batch: int,
+                                seq: int) -> int:
+    out = ctypes.c_size_t(0)
+    check(lib().hero_decoder_workspace_size(ctypes.byref(dims), ctypes.byref(adims), n_layers, batch, seq,
+                                            ctypes.byref(out)), "hero_decoder_workspace_size")
+    return out.value
+
+
+def hero_attention_block(dims: hero_dims, adims: hero_attn_dims, batch: int, seq: int, h, hbar,
+                         attn: hero_attn_weights, inv_freq: Sequence[float], workspace, workspace_bytes: int,
+                         stream=None) -> int:
+    """hbar = h + Attn(LN^attn(h)) for batch x seq tokens; inv_freq: head_dim / 2 host floats."""
+    return lib().hero_attention_block(ctypes.byref(dims), _byref(adims), batch, seq, ptr(h), ptr(hbar),
+                                      _byref(attn), None if inv_freq is None else _floats(inv_freq),
+                                      ptr(workspace), int(workspace_bytes), stream)
+
+
+def hero_decoder_stack(dims: hero_dims, adims: hero_attn_dims, n_layers: int, batch: int, seq: int, h_in, h_out,
+                       state: hero_state, attn: Sequence[hero_attn_weights], ffn: Sequence[hero_ffn_weights],
+                       router: hero_router_weights, adapter: Sequence[hero_adapter_weights],
+                       eta: Sequence[float], inv_freq: Sequence[float], routing: hero_routing,
+                       stats: Optional[Sequence[hero_layer_stats]], workspace, workspace_bytes: int,
+                       stream=None) -> int:
+    """n_layers decoder blocks, the last len(adapter) of them routed."""
+    n, L = len(attn), len(adapter)
+    at_arr = (hero_attn_weights * n)(*attn)
+    ffn_arr = (hero_ffn_weights * n)(*ffn)
+    ad_arr = (hero_adapter_weights * max(L, 1))(*adapter)
+    st_arr = None if stats is None else (hero_layer_stats * max(L, 1))(*stats)
+    return lib().hero_decoder_stack(ctypes.byref(dims), _byref(adims), n_layers, batch, seq, ptr(h_in), ptr(h_out),
+                                    _byref(state), at_arr, ffn_arr, _byref(router), ad_arr, _floats(eta),
+                                    _floats(inv_freq), _byref(routing), st_arr, ptr(workspace),
+                                    int(workspace_bytes), stream)

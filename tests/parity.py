@@ -261,3 +261,45 @@ def check_stack_layerwise(prob, layer_io, rows=None, report=None, verbose=False)
         t = tol_of(w, k)
         assert worst[k] <= t, f"{k}: max rel err {worst[k]:.3e} > {t:.0e} ({worst})"
     return worst
+
+
+def check_decoder(prob, gpu_res, report=None):
+    """Full decoder (attention at every block, routing at the last L_R): per routed block the
+    decisions, logits and gates, then the output and the router state, against the oracle
+    decoder teacher-forced to the GPU's decisions."""
+    from tests.oracle_inputs import adims_of, attn_of
+    w = prob.w
+    T = prob.hbar.shape[0]
+    layers = gpu_res["layers"]
+    for L in layers:
+        check_compaction(L, T)
+        if w.mode == "budget":
+            check_budget_selection(L, w.budget, T)
+    beta = None if prob.beta is None else prob.beta.astype(np.float64)
+    ref = O.decoder_stack(dims_of(w), adims_of(w), w.n_layers, w.batch, w.seq, prob.hbar.f64,
+                          _LazyMap(prob.attn, lambda a: attn_of(a, w, prob.inv_freq)),
+                          _LazyMap(prob.ffn, ffn_of), router_of(prob), _LazyMap(prob.adapter, adapter_of),
+                          prob.eta.astype(np.float64), mode=w.mode, budget=w.budget, tau=w.tau, beta=beta,
+                          forced_ffn=[L["mask"] for L in layers], ablation=w.ablation)
+    n_band = 0
+    errs = dict(logit=0.0, gate=0.0)
+    for jj, (L, R) in enumerate(zip(layers, ref.routed), start=1):
+        lam_ref = O.decide_budget(R.logit, w.budget)[1] if w.mode == "budget" else R.lam
+        mism = L["mask"] != R.own_ffn
+        thr = band_threshold(w, lam_ref)
+        far = mism & (np.abs(R.gate - thr) >= BAND)
+        assert not far.any(), (f"{int(far.sum())} decisions differ outside the band at routed block {jj}: "
+                               f"gates {R.gate[far][:4]}, thr {thr}")
+        n_band += int(mism.sum())
+        errs["logit"] = max(errs["logit"], scalar_err(L["logit"], R.logit))
+        errs["gate"] = max(errs["gate"], scalar_err(L["gate"], R.gate))
+    errs.update(h=row_rel_err(gpu_res["h"], ref.h), S=row_rel_err(gpu_res["S"], ref.state.S),
+                zeta=row_rel_err(gpu_res["zeta"], ref.state.zeta),
+                p=scalar_err(gpu_res["p_hist"], ref.state.p_hist),
+                m=scalar_err(gpu_res["m_hist"], ref.state.m_hist), band_flips=n_band)
+    if report is not None:
+        report.update(errs)
+    for k in ("logit", "gate", "h", "S", "zeta", "p", "m"):
+        t = tol_of(w, k)
+        assert errs[k] <= t, f"{k}: max rel err {errs[k]:.3e} > {t:.0e} ({errs})"
+    return errs

@@ -233,3 +233,56 @@ def test_bf16_state_needs_a_wide_memory():
     assert call_layer(good_dims(state_dtype=H.HERO_BF16, d_m=32)) == H.HERO_E_UNSUPPORTED
     # a valid bf16-state call gets past validation to the device check
     assert call_layer(good_dims(state_dtype=H.HERO_BF16, d_m=64)) == H.HERO_E_DEVICE
+
+
+def test_decoder_entry_points_validate():
+    dims = good_dims(L_R=2)
+    ad = H.hero_attn_dims(4, 2, 128)
+    need = H.hero_decoder_workspace_size(dims, ad, 4, 2, 300)
+    assert need > H.hero_decoder_workspace_size(dims, ad, 0, 2, 300) > H.hero_workspace_size(dims, 600, False)
+    out = ctypes.c_size_t(0)
+    ws_call = lambda d, a, n=4, b=2, s=300: H.lib().hero_decoder_workspace_size(
+        ctypes.byref(d), None if a is None else ctypes.byref(a), n, b, s, ctypes.byref(out))
+    assert ws_call(dims, None) == H.HERO_E_NULL
+    assert ws_call(dims, H.hero_attn_dims(4, 3, 128)) == H.HERO_E_DIM          # heads % kv heads
+    assert ws_call(dims, H.hero_attn_dims(4, 2, 64)) == H.HERO_E_UNSUPPORTED   # head width 128 only
+    assert ws_call(dims, H.hero_attn_dims(3, 3, 128)) == H.HERO_E_UNSUPPORTED  # odd head count
+    assert ws_call(good_dims(H.HERO_F32, d=256, d_ff=688, d_r=16, d_m=32), ad) == H.HERO_E_UNSUPPORTED
+    assert ws_call(dims, ad, b=0) == H.HERO_E_DIM
+
+    aw = H.hero_attn_weights(FAKE + 4096, FAKE + 8192, FAKE + 12288)
+    freq = [1.0] * 64
+    h, hb, ws = FAKE + (1 << 30), FAKE + (2 << 30), FAKE + (8 << 30)
+
+    need_attn = H.hero_decoder_workspace_size(dims, ad, 0, 2, 300)
+
+    def attn(**kw):
+        a = dict(d=dims, ad=ad, b=2, s=300, h=h, hb=hb, w=aw, f=freq, ws=ws, n=need_attn)
+        a.update(kw)
+        return H.hero_attention_block(a["d"], a["ad"], a["b"], a["s"], a["h"], a["hb"], a["w"], a["f"],
+                                      a["ws"], a["n"])
+
+    assert attn(h=None) == H.HERO_E_NULL
+    assert attn(hb=h) == H.HERO_E_ALIAS
+    assert attn(hb=hb + 2) == H.HERO_E_ALIGN
+    assert attn(w=H.hero_attn_weights(FAKE, None, FAKE)) == H.HERO_E_NULL
+    assert attn(f=None) == H.HERO_E_NULL
+    assert attn(f=[1.0] * 63 + [float("inf")]) == H.HERO_E_RANGE
+    assert attn(n=need_attn - 1) == H.HERO_E_WORKSPACE
+    assert attn(ws=hb) == H.HERO_E_ALIAS
+    assert attn() == H.HERO_E_DEVICE
+
+    ffn, adp, rt, st = fake_structs(4)
+    rc = H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.3, None)
+
+    def dec(n_layers=4, eta=(3.9, 3.9), adapters=adp[:2], **kw):
+        a = dict(h_in=h, h_out=hb, ws=ws)
+        a.update(kw)
+        return H.hero_decoder_stack(dims, ad, n_layers, 2, 300, a["h_in"], a["h_out"], st, [aw] * n_layers,
+                                    ffn[:n_layers] + ffn[:max(0, n_layers - 4)], rt, adapters, eta, freq, rc,
+                                    None, a["ws"], need)
+
+    assert dec(n_layers=1) == H.HERO_E_RANGE           # fewer blocks than routed layers
+    assert dec(h_out=h) == H.HERO_E_ALIAS
+    assert dec(eta=(3.9, float("nan"))) == H.HERO_E_RANGE
+    assert dec() == H.HERO_E_DEVICE

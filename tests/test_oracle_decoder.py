@@ -87,6 +87,17 @@ def test_attention_block_matches_torch_modules():
     assert np.abs(got - h).max() > 1e-3
 
 
+def test_attention_on_selected_rows_equals_the_full_block():
+    prob = _prob()
+    A = attn_of(prob.attn[1], W, prob.inv_freq)
+    h = prob.hbar.f64
+    full = O.attention_block(h, A, adims_of(W), W.batch, W.seq, dims_of(W))
+    rows = np.array([0, 3, W.seq - 1, W.seq, W.seq + 7])
+    part = O.attention_block(h, A, adims_of(W), W.batch, W.seq, dims_of(W), rows=rows)
+    np.testing.assert_allclose(part[rows], full[rows], rtol=1e-12, atol=1e-13)
+    assert np.isnan(part[1]).all()
+
+
 def test_attention_is_causal_within_each_sequence():
     prob = _prob()
     A = attn_of(prob.attn[0], W, prob.inv_freq)
