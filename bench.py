@@ -222,6 +222,119 @@ def summarize_rocprof(root, window=None):
         print()
 
 
+def decoder_work(w, nfs, nas):
+    """Algorithmic FLOPs / HBM bytes per step of each kernel of a full-decoder call."""
+    T, d, dff, hd, B, S = w.T, w.d, w.d_ff, w.head_dim, w.batch, w.seq
+    nh, nkv, r = w.n_heads, w.n_kv_heads, w.d_r
+    n_dense = w.n_layers - w.L_R
+    rows_ffn = n_dense * T + sum(nfs)
+    rows_ad = sum(nas)
+    pairs = B * nh * S * (S + 1) // 2                 # (query, visible key) pairs
+    wk = {
+        "attn_norm": dict(flops=0, bytes=w.n_layers * T * 4 * d),
+        "attn_qkv": dict(flops=w.n_layers * 2 * T * d * (nh + 2 * nkv) * hd,
+                         bytes=w.n_layers * 2 * ((nh + 2 * nkv) * hd * (d + T) + T * d)),
+        "attn_core": dict(flops=w.n_layers * 4 * hd * pairs,
+                          bytes=w.n_layers * 2 * B * S * hd * (2 * nh + 2 * nkv)),
+        "attn_out": dict(flops=w.n_layers * 2 * T * nh * hd * d,
+                         bytes=w.n_layers * 2 * (d * nh * hd + T * nh * hd + 2 * T * d)),
+        "ffn_gate_up": dict(flops=4 * d * dff * rows_ffn,
+                            bytes=sum(2 * (2 * d * dff + n * (d + dff)) for n in [T] * n_dense + nfs if n)),
+        "ffn_down": dict(flops=2 * d * dff * rows_ffn,
+                         bytes=sum(2 * (d * dff + n * (dff + 2 * d)) for n in [T] * n_dense + nfs if n)),
+        "adapter_down": dict(flops=2 * d * r * rows_ad, bytes=2 * (rows_ad * d + sum(1 for n in nas if n) * r * d)),
+        "adapter_up": dict(flops=2 * d * r * rows_ad, bytes=2 * (2 * rows_ad * d + sum(1 for n in nas if n) * r * d)),
+    }
+    return wk
+
+
+def bench_decoder(args, w):
+    """A step is one hero_decoder_stack call: every block's attention, the pretrained FFN of the
+    first n_layers - L_R blocks and the routed layers of the rest, over all T tokens."""
+    import torch
+    from paper_2609_08189_amd import hero as H
+    from paper_2609_08189_amd import synth
+    from paper_2609_08189_amd.device import DeviceDecoder
+
+    print(f"# preparing {w.name}: {w.n_layers} blocks, last {w.L_R} routed", file=sys.stderr, flush=True)
+    prob = synth.make_problem(w, seed=args.seed)
+    dd = DeviceDecoder(prob, device="cuda:0", stats=True)
+    stream = dd.stream()
+    ev = HipEvents()
+    dd.run()
+    torch.cuda.synchronize()
+    layer_stats = [s.host() for s in dd.stats]
+    nfs = [ls["n_ffn"] for ls in layer_stats]
+    nas = [ls["n_ad"] for ls in layer_stats]
+    dd.stats = None
+    for _ in range(args.warmup):
+        dd.run()
+    torch.cuda.synchronize()
+    K = args.steps
+    n_dense = w.n_layers - w.L_R
+    # launches per step of every kernel
+    launches = {k: w.n_layers for k in ("attn_norm", "attn_qkv", "attn_core", "attn_out")}
+    launches.update({k: w.L_R for k in ("router_gemm", "router_pre", "router_post", "select")})
+    launches["router_mem"] = w.L_R if not (w.ablation & 12) else 0
+    launches["rowstats"] = w.n_layers
+    launches["ffn_gate_up"] = launches["ffn_down"] = n_dense + sum(1 for n in nfs if n)
+    launches["adapter_down"] = launches["adapter_up"] = sum(1 for n in nas if n)
+    # instrumented pass: every kernel's time per step, which names the dominant one
+    per, handles = {}, {}
+    for name, n in launches.items():
+        if n:
+            handles[name] = (ev.create(K * n), ev.create(K * n))
+            H.hero_kernel_timer(H.HERO_K[name], *handles[name])
+    for _ in range(K):
+        dd.run()
+    torch.cuda.synchronize()
+    works = decoder_work(w, nfs, nas)
+    for name, (a, b) in handles.items():
+        H.hero_kernel_timer(H.HERO_K[name], [], [])
+        ms = sum(ev.elapsed_ms(x, y) for x, y in zip(a, b)) / K         # per step
+        n = launches[name]
+        wk = works.get(name)
+        per[name] = {"ms_per_step": round(ms, 3), "launches": n, "us": round(1000 * ms / n, 2),
+                     "tflops": round(wk["flops"] / (ms * 1e-3) * 1e-12, 1) if wk and wk["flops"] else None,
+                     "gbs": round(wk["bytes"] / (ms * 1e-3) * 1e-9, 1) if wk else None}
+        ev.destroy(a + b)
+    dom = max((k for k in per if k in works and works[k]["flops"]), key=lambda k: per[k]["ms_per_step"])
+    # timed region, with the dominant kernel's launches bracketed on the call's stream
+    n_dom = K * launches[dom]
+    ks, ke = ev.create(n_dom), ev.create(n_dom)
+    H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
+    t_start, t_stop = ev.create(2)
+    torch.cuda.synchronize()
+    ev.record(t_start, stream)
+    for _ in range(K):
+        dd.run()
+    ev.record(t_stop, stream)
+    torch.cuda.synchronize()
+    H.hero_kernel_timer(H.HERO_K[dom], [], [])
+    ms_step = ev.elapsed_ms(t_start, t_stop) / K
+    dom_ms = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
+    achieved = works[dom]["flops"] / (dom_ms * 1e-3) * 1e-12
+    result = {
+        "metric": "routed-FFN-stack tokens/sec at Llama-3.1-8B shape; % MFMA/HBM roofline",
+        "value": round(w.T / (ms_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": (f"{w.name}: full decoder, {w.n_layers} blocks of d={w.d}, d_ff={w.d_ff}, "
+                                f"{w.n_heads}/{w.n_kv_heads} heads of {w.head_dim}, attention at every block, "
+                                f"the last {w.L_R} routed (adapter rank {w.d_r}, memory dim {w.d_m}, "
+                                f"skip budget {w.budget}), T={w.T} tokens ({w.batch}x{w.seq})"),
+                   "global_batch": w.batch, "seq_len": w.seq, "tokens": w.T, "layers_per_step": w.n_layers,
+                   "parallelism": "none", "n_ffn_routed": sum(nfs), "n_adapter": sum(nas)},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "kernel": dom, "avg_launch_us": round(1000 * dom_ms / launches[dom], 2),
+                     "work_per_launch": f"{works[dom]['flops'] / 1e12:.2f} TFLOP per step over "
+                                        f"{launches[dom]} launches"},
+        "kernels": per,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -249,7 +362,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the routed FFN path shards over tokens with no "
-              f"communication in threshold mode, and multi-GPU runs are not part of this build "
+              f"communication in threshold mode, and runs on several GPUs are not implemented "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
 
@@ -268,6 +381,8 @@ def main():
         if args.memory != "matrix":
             sys.exit("--state bf16 needs the matrix-form memory")
         w = w.replace(state_dtype="bf16")
+    if w.n_layers > 0:
+        return bench_decoder(args, w)
     stack = w.layer_j <= 0          # a stack workload: a step is one hero_routed_stack call
     j = w.layer_j
     L = w.L_R if stack else 1       # routed layers per step

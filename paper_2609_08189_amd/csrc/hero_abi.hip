@@ -613,6 +613,7 @@ struct DecLayout {
   Layout L;            // the routed layer's workspace (its u region holds LN^attn(h) too)
   int seq_pad;
   size_t q, k, vt, o;  // attention intermediates
+  size_t rope;         // [seq][64] (cos, sin) of the rotary angles
   size_t ring, hA, hB, hbar_tmp;
   size_t total;
 };
@@ -633,6 +634,7 @@ DecLayout dec_layout_of(const hero_dims& d, const hero_attn_dims& a, int n_layer
   D.k = take(B * a.n_kv_heads * sp * hd * 2);
   D.vt = take(B * a.n_kv_heads * hd * sp * 2);
   D.o = take(T * a.n_heads * hd * 2);
+  D.rope = take(static_cast<size_t>(seq) * (hd / 2) * 8);
   if (n_layers > 0) {
     const size_t hb = T * d.d * 2;
     D.ring = take(3 * hb);
@@ -645,9 +647,15 @@ DecLayout dec_layout_of(const hero_dims& d, const hero_attn_dims& a, int n_layer
 }
 
 // hbar = h + Attn(LN^attn(h)) over batch x seq tokens
+// the rotary table of the call's positions, made once per call
+int make_rope_table(int seq, const hero::RopeTable& rope, unsigned char* ws, const DecLayout& DL, hipStream_t st) {
+  return hero::launch_rope_table(seq, rope, reinterpret_cast<float*>(ws + DL.rope), st) == hipSuccess
+             ? HERO_OK : HERO_E_LAUNCH;
+}
+
+// hbar = h + Attn(LN^attn(h)) over batch x seq tokens (the rotary table already made)
 int run_attention(const hero_dims& dm, const hero_attn_dims& a, int batch, int seq, const void* h, void* hbar,
-                  const hero_attn_weights& w, const hero::RopeTable& rope, unsigned char* ws,
-                  const DecLayout& DL, hipStream_t st) {
+                  const hero_attn_weights& w, unsigned char* ws, const DecLayout& DL, hipStream_t st) {
   using namespace hero;
   const int T = batch * seq;
   void* x = ws + DL.L.u;
@@ -658,7 +666,8 @@ int run_attention(const hero_dims& dm, const hero_attn_dims& a, int batch, int s
   });
   if (e != hipSuccess) return HERO_E_LAUNCH;
   e = timed(HERO_K_ATTN_QKV, st, [&] {
-    return launch_attn_qkv(x, w.w_qkv, T, dm.d, seq, DL.seq_pad, a.n_heads, a.n_kv_heads, rope, q, k, vt, st);
+    return launch_attn_qkv(x, w.w_qkv, T, dm.d, seq, DL.seq_pad, a.n_heads, a.n_kv_heads,
+                           reinterpret_cast<const float*>(ws + DL.rope), q, k, vt, st);
   });
   if (e != hipSuccess) return HERO_E_LAUNCH;
   e = timed(HERO_K_ATTN_CORE, st, [&] {
@@ -728,8 +737,10 @@ int hero_attention_block(const hero_dims* dims, const hero_attn_dims* adims, int
   if (!aligned16(workspace)) return HERO_E_ALIGN;
   if (overlap(hbar, hb, workspace, DL.total) || overlap(h, hb, workspace, DL.total)) return HERO_E_ALIAS;
   if ((st = check_device()) != HERO_OK) return st;
-  return run_attention(*dims, *adims, batch, seq, h, hbar, *attn, rope, static_cast<unsigned char*>(workspace),
-                       DL, static_cast<hipStream_t>(stream));
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = make_rope_table(seq, rope, ws, DL, s)) != HERO_OK) return st;
+  return run_attention(*dims, *adims, batch, seq, h, hbar, *attn, ws, DL, s);
 }
 
 int hero_decoder_stack(const hero_dims* dims, const hero_attn_dims* adims, int n_layers, int batch, int seq,
@@ -778,17 +789,18 @@ int hero_decoder_stack(const hero_dims* dims, const hero_attn_dims* adims, int n
   const hipStream_t s = static_cast<hipStream_t>(stream);
   unsigned char* ring[3] = {ws + DL.ring, ws + DL.ring + hb, ws + DL.ring + 2 * hb};
   unsigned char* hbuf[2] = {ws + DL.hA, ws + DL.hB};
+  if ((st = make_rope_table(seq, rope, ws, DL, s)) != HERO_OK) return st;
   const void* h = h_in;
   for (int l = 0; l < n_layers; ++l) {
     void* out = l == n_layers - 1 ? h_out : static_cast<void*>(hbuf[l & 1]);
     if (l < first) {
       void* hbar = ws + DL.hbar_tmp;
-      if ((st = run_attention(*dims, *adims, batch, seq, h, hbar, attn[l], rope, ws, DL, s)) != HERO_OK) return st;
+      if ((st = run_attention(*dims, *adims, batch, seq, h, hbar, attn[l], ws, DL, s)) != HERO_OK) return st;
       if ((st = run_dense_ffn(*dims, T, hbar, out, ffn[l], ws, DL.L, s)) != HERO_OK) return st;
     } else {
       const int j = l - first + 1;
       void* hbar = ring[(j - 1) % 3];
-      if ((st = run_attention(*dims, *adims, batch, seq, h, hbar, attn[l], rope, ws, DL, s)) != HERO_OK) return st;
+      if ((st = run_attention(*dims, *adims, batch, seq, h, hbar, attn[l], ws, DL, s)) != HERO_OK) return st;
       LayerCall c{dims, j, T, hbar, j >= 2 ? ring[(j - 2) % 3] : nullptr, j >= 3 ? ring[(j - 3) % 3] : nullptr,
                   out, state, &ffn[l], router, &adapter[j - 1], eta[j - 1], routing,
                   stats ? &stats[j - 1] : nullptr, ws, &DL.L, s};

@@ -101,10 +101,12 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
 struct RopeTable {
   float inv_freq[64];   // [head_dim / 2] rotary frequencies
 };
+// cs[pos][i] = (cos, sin)(pos * inv_freq[i]) in fp32, pos < seq, i < 64 (2 seq 64 floats)
+hipError_t launch_rope_table(int seq, const RopeTable& rope, float* cs, hipStream_t s);
 // [q; k; v] = x [W_q; W_k; W_v]^T with the rotary embedding on q, k; q [B][nh][seq_pad][128],
 // k [B][nkv][seq_pad][128], vt [B][nkv][128][seq_pad] (rows past seq are not written)
 hipError_t launch_attn_qkv(const void* x, const void* w_qkv, int T, int d, int seq, int seq_pad, int nh,
-                           int nkv, const RopeTable& rope, void* q, void* k, void* vt, hipStream_t s);
+                           int nkv, const float* rope_cs, void* q, void* k, void* vt, hipStream_t s);
 // o[t][h 128 + c] = causal softmax(q k^T / sqrt(128)) v, head h reading kv head h / (nh / nkv)
 hipError_t launch_attn_core(const void* q, const void* k, const void* vt, void* o, int batch, int seq,
                             int seq_pad, int nh, int nkv, hipStream_t s);

@@ -45,7 +45,7 @@ __device__ __forceinline__ bf16x8 pack8(const float* x) {
   return r;
 }
 
-__global__ __launch_bounds__(NTA) void attn_fwd_kernel(const bf16_t* __restrict__ q,
+__global__ __launch_bounds__(NTA, 2) void attn_fwd_kernel(const bf16_t* __restrict__ q,
                                                       const bf16_t* __restrict__ k,
                                                       const bf16_t* __restrict__ vt,
                                                       bf16_t* __restrict__ o, int seq, int seq_pad,

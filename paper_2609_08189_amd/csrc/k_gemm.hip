@@ -186,6 +186,13 @@ constexpr int kCUs = 256;    // compute units of an MI355X
 // instruction classes of __builtin_amdgcn_sched_group_barrier
 constexpr int SG_MFMA = 0x008, SG_VMEM_READ = 0x020, SG_DS_READ = 0x100;
 
+// An epilogue with a block() member takes each staged 32-row block of a wave tile whole,
+// instead of 8-column row pieces through emit8().
+template <class E, class = void>
+struct BlockEpilogue : std::false_type {};
+template <class E>
+struct BlockEpilogue<E, std::void_t<decltype(&E::block)>> : std::true_type {};
+
 template <int BM_, int BN_, int WM_, int WN_, bool DUAL_>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
@@ -405,12 +412,17 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
 #pragma unroll
         for (int b = 0; b < C::TN; ++b) stg[i * C::OPAD + b * 32 + (lane & 31)] = acc[a][b][r];
       }
+      if constexpr (BlockEpilogue<Epi>::value) {
+        // the epilogue takes the whole staged 32-row block (any lane may read any element)
+        epi.block(stg, C::OPAD, C::ON, m0 + wm * C::WTM + a * 32, nt * C::OUT_N + wn * C::ON, M, lane);
+      } else {
 #pragma unroll
-      for (int q = 0; q < PPB; ++q) {
-        const int e = lane + kWave * q;
-        const int i = e / CPR, c8 = (e % CPR) * 8;
-        const int m = m0 + wm * C::WTM + a * 32 + i;
-        if (m < M) epi.emit8(pre[a][q], m, nt * C::OUT_N + wn * C::ON + c8, stg + i * C::OPAD + c8);
+        for (int q = 0; q < PPB; ++q) {
+          const int e = lane + kWave * q;
+          const int i = e / CPR, c8 = (e % CPR) * 8;
+          const int m = m0 + wm * C::WTM + a * 32 + i;
+          if (m < M) epi.emit8(pre[a][q], m, nt * C::OUT_N + wn * C::ON + c8, stg + i * C::OPAD + c8);
+        }
       }
     }
   }
@@ -1086,9 +1098,10 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
 // ---------------------------------------------------------------------------
 // Attention projections of a decoder block (Sec. 3.1, eq:dense_attention).
 // [q; k; v] = x [W_q; W_k; W_v]^T runs on the GEMM core with an epilogue that applies the
-// rotary embedding to q and k (pair (2i, 2i+1) of a head turned by pos * inv_freq[i], in
-// fp32) and writes each head where the attention kernel reads it: q [B][n_h][S_pad][128],
-// k [B][n_kv][S_pad][128] and v transposed, [B][n_kv][128][S_pad].  The output projection
+// rotary embedding to q and k (pair (2i, 2i+1) of a head turned by pos * inv_freq[i]: a
+// table of cos and sin for the call's positions, made once in fp32) and writes each head
+// where the attention kernel reads it: q [B][n_h][S_pad][128], k [B][n_kv][S_pad][128] and
+// v transposed, [B][n_kv][128][S_pad], the latter as 16-byte runs of 8 positions.  The output projection
 // adds its product to the block input: hbar = h + o W_o^T.
 // ---------------------------------------------------------------------------
 namespace {
@@ -1099,45 +1112,94 @@ struct EpiQKV {
   bf16_t* q;
   bf16_t* k;
   bf16_t* vt;
+  const float2* cs;   // [seq][64] (cos, sin) of pos * inv_freq[i]
   int seq, seq_pad, nh, nkv;
-  RopeTable rope;
   struct Pre {};
   __device__ __forceinline__ Pre prep(int, int) const { return {}; }
   __device__ __forceinline__ void store(int, int, float) const {}
-  __device__ __forceinline__ void emit8(const Pre&, int m, int n, const float* v) const {
-    const int b = m / seq, pos = m - b * seq;
-    const int head = n / kHeadDim, c = n % kHeadDim;
+  __device__ __forceinline__ void emit8(const Pre&, int, int, const float*) const {}
+  // a staged block of 32 token rows x `on` columns (one head's half: 64 | 128) starting at
+  // row mb, column nb
+  __device__ __forceinline__ void block(const float* stg, int opad, int on, int mb, int nb, int M,
+                                        int lane) const {
+    const int head = nb / kHeadDim, c0 = nb % kHeadDim;
     if (head < nh + nkv) {
-      u32x4 w;
+      // q or k: 8-column row pieces, turned by the rotary table
+      const int cpr = on / 8;
+      for (int e = lane; e < 32 * cpr; e += kWave) {
+        const int i = e / cpr, c8 = (e % cpr) * 8;
+        const int m = mb + i;
+        if (m >= M) continue;
+        const int b = m / seq, pos = m - b * seq;
+        const int c = c0 + c8;
+        const float* v = stg + i * opad + c8;
+        const float2* t = cs + static_cast<size_t>(pos) * (kHeadDim / 2) + c / 2;
+        u32x4 w;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float sn, cs;
-        sincosf(static_cast<float>(pos) * rope.inv_freq[c / 2 + i], &sn, &cs);
-        const float a = v[2 * i], bb = v[2 * i + 1];
-        w[i] = static_cast<uint32_t>(f32_to_bf16(a * cs - bb * sn)) |
-               (static_cast<uint32_t>(f32_to_bf16(a * sn + bb * cs)) << 16);
+        for (int x = 0; x < 4; ++x) {
+          const float2 r = t[x];
+          const float a = v[2 * x], bb = v[2 * x + 1];
+          w[x] = static_cast<uint32_t>(f32_to_bf16(a * r.x - bb * r.y)) |
+                 (static_cast<uint32_t>(f32_to_bf16(a * r.y + bb * r.x)) << 16);
+        }
+        bf16_t* dst = head < nh
+            ? q + ((static_cast<size_t>(b) * nh + head) * seq_pad + pos) * kHeadDim + c
+            : k + ((static_cast<size_t>(b) * nkv + (head - nh)) * seq_pad + pos) * kHeadDim + c;
+        *reinterpret_cast<u32x4*>(dst) = w;
       }
-      bf16_t* dst = head < nh
-          ? q + ((static_cast<size_t>(b) * nh + head) * seq_pad + pos) * kHeadDim + c
-          : k + ((static_cast<size_t>(b) * nkv + (head - nh)) * seq_pad + pos) * kHeadDim + c;
-      *reinterpret_cast<u32x4*>(dst) = w;
     } else {
-      bf16_t* dst = vt + ((static_cast<size_t>(b) * nkv + (head - nh - nkv)) * kHeadDim + c) * seq_pad + pos;
+      // v, transposed: each piece is one column over 8 consecutive token rows
+      const int vh = head - nh - nkv;
+      for (int e = lane; e < 4 * on; e += kWave) {
+        const int col = e % on, rg = e / on;
+        const int m = mb + 8 * rg;
+        if (m >= M) continue;
+        const int b = m / seq, pos = m - b * seq;
+        bf16_t* dst = vt + ((static_cast<size_t>(b) * nkv + vh) * kHeadDim + c0 + col) * seq_pad + pos;
+        if (m + 7 < M && pos + 7 < seq && (pos & 7) == 0) {
+          u32x4 w;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) dst[static_cast<size_t>(e) * seq_pad] = f32_to_bf16(v[e]);
+          for (int x = 0; x < 4; ++x)
+            w[x] = static_cast<uint32_t>(f32_to_bf16(stg[(8 * rg + 2 * x) * opad + col])) |
+                   (static_cast<uint32_t>(f32_to_bf16(stg[(8 * rg + 2 * x + 1) * opad + col])) << 16);
+          *reinterpret_cast<u32x4*>(dst) = w;
+        } else {
+          for (int x = 0; x < 8 && m + x < M; ++x) {
+            const int mm = m + x, bx = mm / seq, px = mm - bx * seq;
+            vt[((static_cast<size_t>(bx) * nkv + vh) * kHeadDim + c0 + col) * seq_pad + px] =
+                f32_to_bf16(stg[(8 * rg + x) * opad + col]);
+          }
+        }
+      }
     }
   }
 };
 
+__global__ void rope_table_kernel(float2* __restrict__ cs, int seq, RopeTable rope) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= seq * (kHeadDim / 2)) return;
+  const int pos = e / (kHeadDim / 2), i = e % (kHeadDim / 2);
+  float sn, c;
+  sincosf(static_cast<float>(pos) * rope.inv_freq[i], &sn, &c);
+  cs[e] = make_float2(c, sn);
+}
+
 }  // namespace
 
+hipError_t launch_rope_table(int seq, const RopeTable& rope, float* cs, hipStream_t s) {
+  const int n = seq * (kHeadDim / 2);
+  if (n <= 0) return hipSuccess;
+  rope_table_kernel<<<(n + 255) / 256, 256, 0, s>>>(reinterpret_cast<float2*>(cs), seq, rope);
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_qkv(const void* x, const void* w_qkv, int T, int d, int seq, int seq_pad, int nh,
-                           int nkv, const RopeTable& rope, void* q, void* k, void* vt, hipStream_t s) {
+                           int nkv, const float* rope_cs, void* q, void* k, void* vt, hipStream_t s) {
   if (T <= 0) return hipSuccess;
   ARows<bf16_t> A{static_cast<const bf16_t*>(x), nullptr, d};
   BRows<bf16_t> B{static_cast<const bf16_t*>(w_qkv), nullptr, INT_MAX, d};
-  EpiQKV epi{static_cast<bf16_t*>(q), static_cast<bf16_t*>(k), static_cast<bf16_t*>(vt), seq, seq_pad,
-             nh, nkv, rope};
+  EpiQKV epi{static_cast<bf16_t*>(q), static_cast<bf16_t*>(k), static_cast<bf16_t*>(vt),
+             reinterpret_cast<const float2*>(rope_cs), seq, seq_pad, nh, nkv};
   return run_big<256, false>(A, B, epi, nullptr, T, (nh + 2 * nkv) * kHeadDim, d, s);
 }
 
