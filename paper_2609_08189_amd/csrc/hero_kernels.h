@@ -104,11 +104,13 @@ struct RopeTable {
 // cs[pos][i] = (cos, sin)(pos * inv_freq[i]) in fp32, pos < seq, i < 64 (2 seq 64 floats)
 hipError_t launch_rope_table(int seq, const RopeTable& rope, float* cs, hipStream_t s);
 // [q; k; v] = x [W_q; W_k; W_v]^T with the rotary embedding on q, k; q [B][nh][seq_pad][128],
-// k [B][nkv][seq_pad][128], vt [B][nkv][128][seq_pad] (rows past seq are not written)
+// k [B][nkv][seq_pad][128], vt [B][nkv][128][seq_pad] with position p of a row at slot p with
+// bits 2 and 3 swapped (rows past seq are not written)
 hipError_t launch_attn_qkv(const void* x, const void* w_qkv, int T, int d, int seq, int seq_pad, int nh,
                            int nkv, const float* rope_cs, void* q, void* k, void* vt, hipStream_t s);
 // o[t][h 128 + c] = causal softmax(q k^T / sqrt(128)) v, head h reading kv head h / (nh / nkv)
-hipError_t launch_attn_core(const void* q, const void* k, const void* vt, void* o, int batch, int seq,
+// (zeroes the V^T positions seq .. seq_pad - 1 first)
+hipError_t launch_attn_core(const void* q, const void* k, void* vt, void* o, int batch, int seq,
                             int seq_pad, int nh, int nkv, hipStream_t s);
 // hbar = h + o W_o^T
 hipError_t launch_attn_out(const void* o, const void* w_o, const void* h, void* hbar, int T, int d, int nh,

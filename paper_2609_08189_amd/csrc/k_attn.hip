@@ -5,7 +5,8 @@
 // One workgroup (4 waves) takes 128 consecutive queries of one head; wave w owns 32 of them.
 // Keys stream through LDS in tiles of 64 (K [64][128] and V^T [128][64], double-buffered,
 // filled by global_load_lds_dwordx4), with an online softmax, so the scores never leave
-// registers:
+// registers (the V^T positions past the sequence are zeroed first, since the workspace may hold
+// anything there):
 //   * scores are formed transposed, S^T = K Q^T, on v_mfma_f32_32x32x16_bf16; in the
 //     accumulator layout lane l then holds query l % 32, so a query's running max and sum are
 //     lane-local (plus one exchange with lane l ^ 32, which holds the other 16 keys);
@@ -13,9 +14,11 @@
 //     partial output by exp(m_old - m_new) is lane-local too;
 //   * P^T goes from the score accumulators straight into the B operand of the second product:
 //     the contraction over keys takes the keys in the order the accumulator holds them (four
-//     consecutive, then four 8 further on), and the V^T fragments are read in that same order.
-// The LDS rows are XOR-swizzled in 16-byte chunks: K rows (256 B) by row % 16, which makes the
-// 32-row fragment reads conflict free; V^T rows (128 B) by (row / 2) % 8 (two-way at most).
+//     consecutive, then four 8 further on), and V^T is stored with its positions in that
+//     order (within each group of 16, the blocks 4-7 and 8-11 swapped), so that a lane's 8
+//     keys are one 16-byte read.
+// The LDS rows are XOR-swizzled in 16-byte chunks, K rows (256 B) by row % 16 and V^T rows
+// (128 B) by (row / 2) % 8, which makes both kinds of 32-row fragment reads conflict free.
 #include "hero_device.h"
 #include "hero_kernels.h"
 
@@ -32,10 +35,24 @@ constexpr int STG = K_BYTES + V_BYTES;
 constexpr int OPITCH = HD + 8;           // output staging row pitch (bf16 elements)
 
 typedef __attribute__((address_space(3))) void lds_void;
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void load_lds16(const void* g, unsigned char* l) {
   __builtin_amdgcn_global_load_lds(g, (lds_void*)(l), 16, 0, 0);
+}
+
+// instruction classes of __builtin_amdgcn_sched_group_barrier
+constexpr int SG_MFMA = 0x008, SG_DS_READ = 0x100;
+
+// Order the 16 fragment reads and 16 MFMAs of a product phase as: 4 reads ahead, then one
+// MFMA and one read alternately, then the last 4 MFMAs (bounds the fragments in flight)
+__device__ __forceinline__ void pipeline_reads_with_mfmas() {
+  __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 4, 0);
+#pragma unroll
+  for (int i = 0; i < 12; ++i) {
+    __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(SG_MFMA, 4, 0);
 }
 
 __device__ __forceinline__ bf16x8 pack8(const float* x) {
@@ -48,16 +65,26 @@ __device__ __forceinline__ bf16x8 pack8(const float* x) {
 __global__ __launch_bounds__(NTA, 2) void attn_fwd_kernel(const bf16_t* __restrict__ q,
                                                       const bf16_t* __restrict__ k,
                                                       const bf16_t* __restrict__ vt,
-                                                      bf16_t* __restrict__ o, int seq, int seq_pad,
-                                                      int nh, int nkv, float scale_log2) {
+                                                      bf16_t* __restrict__ o, int batch, int seq,
+                                                      int seq_pad, int nh, int nkv, float scale_log2) {
   __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STG];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int hl = lane >> 5, col = lane & 31;
-  const int n_qt = gridDim.x;
-  const int qt = n_qt - 1 - static_cast<int>(blockIdx.x);   // the longest rows first
-  const int head = blockIdx.y, b = blockIdx.z;
-  const int kvh = head / (nh / nkv);
+  // Work items (sequence b, kv head, query head of its group, query tile) are laid over the 8
+  // XCDs (workgroups go to XCD blockIdx % 8) so that each XCD takes whole kv groups: the K and
+  // V^T of a group (2 x 128 x seq_pad bf16) then stay in that XCD's L2.  Within an XCD the
+  // longest query tiles come first.
+  const int n_qt = seq_pad / QT;
+  const int hpg = nh / nkv;                              // query heads per kv head
+  const int n_groups = batch * nkv;
+  const int gx = (n_groups + 7) / 8;                     // kv groups per XCD
+  const int xcd = blockIdx.x & 7, kq = blockIdx.x >> 3;
+  const int g = xcd + 8 * (kq % gx);
+  if (g >= n_groups) return;
+  const int rest = kq / gx;                              // < hpg * n_qt
+  const int qt = n_qt - 1 - rest / hpg;
+  const int b = g / nkv, kvh = g % nkv, head = kvh * hpg + rest % hpg;
   const int q0 = qt * QT;
   const int wq0 = q0 + 32 * wave;                 // this wave's first query
   const int my_q = wq0 + col;                     // the query this lane's columns hold
@@ -111,31 +138,32 @@ __global__ __launch_bounds__(NTA, 2) void attn_fwd_kernel(const bf16_t* __restri
     const unsigned char* st = smem + (kt & 1) * STG;
     // keys past this wave's last query are all masked: nothing to add
     if (k0 <= wq0 + 31) {
+      // the two 32-key halves are independent accumulation chains: alternate them
       f32x16 sacc[2];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[t][r] = 0.f;
-        const int r = 32 * t + col;
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          const int c = 2 * s + hl;
+      for (int s = 0; s < 8; ++s)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const int r = 32 * t + col, c = 2 * s + hl;
           const bf16x8 kf = *reinterpret_cast<const bf16x8*>(st + 256 * r + 16 * (c ^ (r & 15)));
           sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[t], 0, 0, 0);
         }
-      }
-      // scale (to base 2), causal / length mask, running max
+      pipeline_reads_with_mfmas();
+      // scale (to base 2), causal / length mask (keys past the query or the sequence; only
+      // tiles that reach the diagonal or the end can hold any), running max
       const bool edge = k0 + KT - 1 > wq0 || k0 + KT > seq;
+      const int lim = edge ? min(my_q, seq - 1) - k0 : KT;   // last visible key of the tile
       float mx = -INFINITY;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float x = sacc[t][r] * scale_log2;
-          if (edge) {
-            const int key = k0 + 32 * t + 8 * (r >> 2) + 4 * hl + (r & 3);
-            if (key > my_q || key >= seq) x = -INFINITY;
-          }
+          const int kr = 32 * t + 8 * (r >> 2) + 4 * hl + (r & 3);
+          const float x = kr > lim ? -INFINITY : sacc[t][r] * scale_log2;
           sacc[t][r] = x;
           mx = fmaxf(mx, x);
         }
@@ -170,35 +198,20 @@ __global__ __launch_bounds__(NTA, 2) void attn_fwd_kernel(const bf16_t* __restri
           pf[t][u] = pack8(x);
         }
       // O^T += V^T P^T; the V^T fragment of k-step (t, u) holds keys 32t + 16u + 4hl + {0..3}
-      // and the same + 8
+      // and the same + 8; the four 32-row output blocks are independent chains, alternated
 #pragma unroll
-      for (int t4 = 0; t4 < 4; ++t4) {
-        const int r = 32 * t4 + col;
-        const unsigned char* vrow = st + K_BYTES + 128 * r;
-        const int sw = (r >> 1) & 7;
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-          for (int u = 0; u < 2; ++u) {
-            const int c1 = 4 * t + 2 * u;
-            const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow + 16 * (c1 ^ sw) + 8 * hl);
-            const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16 * ((c1 + 1) ^ sw) + 8 * hl);
-            bf16x8 vf;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              vf[e] = lo[e];
-              vf[4 + e] = hi[e];
-            }
-            if (k0 + KT > seq) {
-              // V^T columns past the sequence hold whatever the buffer held: zero them, so that
-              // their zero probabilities cannot meet a NaN
-#pragma unroll
-              for (int e = 0; e < 8; ++e)
-                if (k0 + 32 * t + 16 * u + 4 * hl + (e & 3) + 8 * (e >> 2) >= seq) vf[e] = 0;
-            }
+          for (int t4 = 0; t4 < 4; ++t4) {
+            const int r = 32 * t4 + col;
+            const unsigned char* vrow = st + K_BYTES + 128 * r;
+            const int sw = (r >> 1) & 7;
+            const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vrow + 16 * ((4 * t + 2 * u + hl) ^ sw));
             acc_o[t4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t][u], acc_o[t4], 0, 0, 0);
           }
-      }
+      pipeline_reads_with_mfmas();
     }
     // every wave is done with this stage and the next tile has landed
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -235,17 +248,34 @@ __global__ __launch_bounds__(NTA, 2) void attn_fwd_kernel(const bf16_t* __restri
   }
 }
 
+// V^T positions seq .. seq_pad - 1 of every row set to zero: their probabilities are zero, and
+// a zero probability must not meet whatever the workspace held there (a NaN)
+__global__ void vt_pad_kernel(bf16_t* __restrict__ vt, int rows, int seq, int seq_pad) {
+  const int pad = seq_pad - seq;
+  const size_t e = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= static_cast<size_t>(rows) * pad) return;
+  const int row = static_cast<int>(e / pad), p = seq + static_cast<int>(e % pad);
+  const int slot = (p & ~15) | (p & 3) | ((p & 4) << 1) | ((p & 8) >> 1);
+  vt[static_cast<size_t>(row) * seq_pad + slot] = 0;
+}
+
 }  // namespace
 
-hipError_t launch_attn_core(const void* q, const void* k, const void* vt, void* o, int batch, int seq,
+hipError_t launch_attn_core(const void* q, const void* k, void* vt, void* o, int batch, int seq,
                             int seq_pad, int nh, int nkv, hipStream_t s) {
   if (batch <= 0 || seq <= 0) return hipSuccess;
   if (seq_pad % QT != 0 || seq_pad < seq || nkv <= 0 || nh % nkv != 0) return hipErrorInvalidValue;
-  const dim3 grid(seq_pad / QT, nh, batch);
+  if (seq_pad > seq) {
+    const size_t n = static_cast<size_t>(batch) * nkv * HD * (seq_pad - seq);
+    vt_pad_kernel<<<static_cast<unsigned>((n + 255) / 256), 256, 0, s>>>(static_cast<bf16_t*>(vt),
+                                                                      batch * nkv * HD, seq, seq_pad);
+  }
+  const int n_groups = batch * nkv, gx = (n_groups + 7) / 8;
+  const dim3 grid(8 * gx * (nh / nkv) * (seq_pad / QT));
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(HD));
   attn_fwd_kernel<<<grid, NTA, 0, s>>>(static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
-                                       static_cast<const bf16_t*>(vt), static_cast<bf16_t*>(o), seq,
-                                       seq_pad, nh, nkv, scale_log2);
+                                       static_cast<const bf16_t*>(vt), static_cast<bf16_t*>(o), batch,
+                                       seq, seq_pad, nh, nkv, scale_log2);
   return hipGetLastError();
 }
 

@@ -1101,7 +1101,8 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
 // rotary embedding to q and k (pair (2i, 2i+1) of a head turned by pos * inv_freq[i]: a
 // table of cos and sin for the call's positions, made once in fp32) and writes each head
 // where the attention kernel reads it: q [B][n_h][S_pad][128], k [B][n_kv][S_pad][128] and
-// v transposed, [B][n_kv][128][S_pad], the latter as 16-byte runs of 8 positions.  The output projection
+// v transposed, [B][n_kv][128][S_pad] with positions permuted within groups of 16 (the
+// attention kernel's key order), written as 16-byte runs.  The output projection
 // adds its product to the block input: hbar = h + o W_o^T.
 // ---------------------------------------------------------------------------
 namespace {
@@ -1148,26 +1149,35 @@ struct EpiQKV {
         *reinterpret_cast<u32x4*>(dst) = w;
       }
     } else {
-      // v, transposed: each piece is one column over 8 consecutive token rows
+      // v, transposed, positions permuted within each group of 16 (position p at slot
+      // p with bits 2 and 3 swapped: 0-3, 8-11, 4-7, 12-15): a piece is one column over the
+      // 8 positions 16G + 4X + {0..3} and 16G + 8 + 4X + {0..3} of the block, one 16-byte run
       const int vh = head - nh - nkv;
       for (int e = lane; e < 4 * on; e += kWave) {
         const int col = e % on, rg = e / on;
-        const int m = mb + 8 * rg;
-        if (m >= M) continue;
-        const int b = m / seq, pos = m - b * seq;
-        bf16_t* dst = vt + ((static_cast<size_t>(b) * nkv + vh) * kHeadDim + c0 + col) * seq_pad + pos;
-        if (m + 7 < M && pos + 7 < seq && (pos & 7) == 0) {
+        const int G = rg >> 1, X = rg & 1;
+        const int m16 = mb + 16 * G;
+        if (m16 >= M) continue;
+        const int b = m16 / seq, p16 = m16 - b * seq;
+        bf16_t* row = vt + ((static_cast<size_t>(b) * nkv + vh) * kHeadDim + c0 + col) * seq_pad;
+        if (m16 + 15 < M && p16 + 15 < seq && (p16 & 15) == 0) {
           u32x4 w;
 #pragma unroll
-          for (int x = 0; x < 4; ++x)
-            w[x] = static_cast<uint32_t>(f32_to_bf16(stg[(8 * rg + 2 * x) * opad + col])) |
-                   (static_cast<uint32_t>(f32_to_bf16(stg[(8 * rg + 2 * x + 1) * opad + col])) << 16);
-          *reinterpret_cast<u32x4*>(dst) = w;
+          for (int x = 0; x < 4; ++x) {
+            const int r0 = 16 * G + (x < 2 ? 4 * X + 2 * x : 8 + 4 * X + 2 * (x - 2));
+            w[x] = static_cast<uint32_t>(f32_to_bf16(stg[r0 * opad + col])) |
+                   (static_cast<uint32_t>(f32_to_bf16(stg[(r0 + 1) * opad + col])) << 16);
+          }
+          *reinterpret_cast<u32x4*>(row + p16 + 8 * X) = w;
         } else {
-          for (int x = 0; x < 8 && m + x < M; ++x) {
-            const int mm = m + x, bx = mm / seq, px = mm - bx * seq;
-            vt[((static_cast<size_t>(bx) * nkv + vh) * kHeadDim + c0 + col) * seq_pad + px] =
-                f32_to_bf16(stg[(8 * rg + x) * opad + col]);
+          for (int x = 0; x < 8; ++x) {
+            const int r = 16 * G + (x < 4 ? 4 * X + x : 8 + 4 * X + x - 4);
+            const int mm = mb + r;
+            if (mm >= M) continue;
+            const int bx = mm / seq, px = mm - bx * seq;
+            const int slot = (px & ~15) | (px & 3) | ((px & 4) << 1) | ((px & 8) >> 1);
+            vt[((static_cast<size_t>(bx) * nkv + vh) * kHeadDim + c0 + col) * seq_pad + slot] =
+                f32_to_bf16(stg[r * opad + col]);
           }
         }
       }
