@@ -55,11 +55,16 @@ __device__ __forceinline__ void pipeline_reads_with_mfmas() {
   __builtin_amdgcn_sched_group_barrier(SG_MFMA, 4, 0);
 }
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// eight fp32 values to bf16 (nearest even), two per v_cvt_pk_bf16_f32
 __device__ __forceinline__ bf16x8 pack8(const float* x) {
-  bf16x8 r;
+  u32x4 w;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) r[e] = __builtin_bit_cast(__bf16, f32_to_bf16(x[e]));
-  return r;
+  for (int i = 0; i < 4; ++i)
+    w[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x[2 * i], x[2 * i + 1]}, bf16x2));
+  return __builtin_bit_cast(bf16x8, w);
 }
 
 __global__ __launch_bounds__(NTA, 2) void attn_fwd_kernel(const bf16_t* __restrict__ q,
@@ -96,22 +101,23 @@ __global__ __launch_bounds__(NTA, 2) void attn_fwd_kernel(const bf16_t* __restri
   // keys needed by this workgroup: 0 .. min(q0 + 127, seq - 1)
   const int n_kt = (min(q0 + QT, seq) + KT - 1) / KT;
 
+  // per-lane element offsets of the stage loads (rows and swizzled 16-byte chunks)
+  int k_off[4], v_off[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int blk = 4 * wave + i;
+    const int rk = 4 * blk + (lane >> 4), rv = 8 * blk + (lane >> 3);
+    k_off[i] = rk * HD + 8 * ((lane & 15) ^ (rk & 15));
+    v_off[i] = rv * seq_pad + 8 * ((lane & 7) ^ ((rv >> 1) & 7));
+  }
   auto issue = [&](int stage, int k0) {
     unsigned char* st = smem + stage * STG;
+    const bf16_t* kt0 = kb + static_cast<size_t>(k0) * HD;
+    const bf16_t* vt0 = vb + k0;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int blk = 4 * wave + i;
-      const int r = 4 * blk + (lane >> 4), p = lane & 15;
-      const int c = p ^ (r & 15);
-      load_lds16(kb + static_cast<size_t>(k0 + r) * HD + 8 * c, st + blk * 1024);
-    }
+    for (int i = 0; i < 4; ++i) load_lds16(kt0 + k_off[i], st + (4 * wave + i) * 1024);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int blk = 4 * wave + i;
-      const int r = 8 * blk + (lane >> 3), p = lane & 7;
-      const int c = p ^ ((r >> 1) & 7);
-      load_lds16(vb + static_cast<size_t>(r) * seq_pad + k0 + 8 * c, st + K_BYTES + blk * 1024);
-    }
+    for (int i = 0; i < 4; ++i) load_lds16(vt0 + v_off[i], st + K_BYTES + (4 * wave + i) * 1024);
   };
 
   issue(0, 0);
@@ -153,39 +159,51 @@ __global__ __launch_bounds__(NTA, 2) void attn_fwd_kernel(const bf16_t* __restri
           sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[t], 0, 0, 0);
         }
       pipeline_reads_with_mfmas();
-      // scale (to base 2), causal / length mask (keys past the query or the sequence; only
-      // tiles that reach the diagonal or the end can hold any), running max
+      // causal / length mask (keys past the query or the sequence; only tiles that reach the
+      // diagonal or the end can hold any) and the running max, in raw score units; the base-2
+      // scale enters through the exponent's fma
       const bool edge = k0 + KT - 1 > wq0 || k0 + KT > seq;
-      const int lim = edge ? min(my_q, seq - 1) - k0 : KT;   // last visible key of the tile
       float mx = -INFINITY;
+      if (edge) {
+        const int lim = min(my_q, seq - 1) - k0;     // last visible key of the tile
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kr = 32 * t + 8 * (r >> 2) + 4 * hl + (r & 3);
-          const float x = kr > lim ? -INFINITY : sacc[t][r] * scale_log2;
-          sacc[t][r] = x;
-          mx = fmaxf(mx, x);
-        }
+          for (int r = 0; r < 16; ++r) {
+            const int kr = 32 * t + 8 * (r >> 2) + 4 * hl + (r & 3);
+            if (kr > lim) sacc[t][r] = -INFINITY;
+            mx = fmaxf(mx, sacc[t][r]);
+          }
+      } else {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[t][r]);
+      }
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float m_new = fmaxf(m_run, mx);
-      const float alpha = exp2f(m_run - m_new);
+      const float mc = m_new * scale_log2;
       float ps = 0.f;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = exp2f(sacc[t][r] - m_new);
+          const float p = __builtin_amdgcn_exp2f(fmaf(sacc[t][r], scale_log2, -mc));
           sacc[t][r] = p;
           ps += p;
         }
       ps += __shfl_xor(ps, 32, 64);
-      l_run = l_run * alpha + ps;
+      // rescale the partial output only when some query's max moved (exp2(0) = 1 otherwise)
+      if (__any(m_new > m_run)) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run * scale_log2 - mc);
+        l_run *= alpha;
+#pragma unroll
+        for (int t4 = 0; t4 < 4; ++t4)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc_o[t4][r] *= alpha;
+      }
+      l_run += ps;
       m_run = m_new;
-#pragma unroll
-      for (int t4 = 0; t4 < 4; ++t4)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc_o[t4][r] *= alpha;
       // P^T as B operands: k-step (t, u) takes accumulator registers 8u .. 8u + 7 of tile t
       bf16x8 pf[2][2];
 #pragma unroll
