@@ -128,7 +128,14 @@ def cpu_baseline(prob, gpu_stats, j, target_s=12.0, max_tokens=None):
             break
         n = min(max_tokens, max(2 * n, int(n * target_s / max(dt, 1e-3) * 1.1)))
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), cpu_model)
+    except OSError:
+        pass
     return {"value": n / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "nproc": os.cpu_count(), "omp_num_threads": os.environ.get("OMP_NUM_THREADS"), "cpu_model": cpu_model,
             "sample": f"{n} of {T} tokens of the same layer call (router, memory, branch; float64 numpy, "
                       f"branch decisions teacher-forced to the GPU's), {dt:.1f} s"}
 
@@ -222,6 +229,23 @@ def summarize_rocprof(root, window=None):
         print()
 
 
+def step_stats(step_ms):
+    """Median and 10th/90th percentiles of the per-step times inside the timed region."""
+    n = len(step_ms)
+    pick = lambda f: round(step_ms[min(n - 1, int(f * (n - 1) + 0.5))], 4)
+    return {"median": pick(0.5), "p10": pick(0.1), "p90": pick(0.9), "n": n}
+
+
+def ideal_fraction(works, ms_step, dtype, stack):
+    """Ideal time of one step (every kernel at its own roof: max(FLOP / MFMA peak, bytes / HBM
+    peak), summed) over the measured step time."""
+    peak_f = (PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS) * 1e12
+    ideal = sum(max(k["flops"] / peak_f, k["bytes"] / (PEAK_HBM_GBS * 1e9)) for wk in works for k in wk.values())
+    return {"ideal_ms": round(ideal * 1e3, 4), "measured_ms": round(ms_step, 4),
+            "frac": round(ideal * 1e3 / ms_step, 4),
+            "note": "sum over kernels of max(algorithmic FLOP / 2.5 PFLOP/s, algorithmic bytes / 8 TB/s)"}
+
+
 def decoder_work(w, nfs, nas):
     """Algorithmic FLOPs / HBM bytes per step of each kernel of a full-decoder call."""
     T, d, dff, hd, B, S = w.T, w.d, w.d_ff, w.head_dim, w.batch, w.seq
@@ -305,13 +329,18 @@ def bench_decoder(args, w):
     H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
     t_start, t_stop = ev.create(2)
     torch.cuda.synchronize()
+    marks = ev.create(K - 1)
     ev.record(t_start, stream)
-    for _ in range(K):
+    for i in range(K):
         dd.run()
+        if i < K - 1:
+            ev.record(marks[i], stream)
     ev.record(t_stop, stream)
     torch.cuda.synchronize()
     H.hero_kernel_timer(H.HERO_K[dom], [], [])
     ms_step = ev.elapsed_ms(t_start, t_stop) / K
+    bounds = [t_start] + marks + [t_stop]
+    step_ms = sorted(ev.elapsed_ms(a, b) for a, b in zip(bounds[:-1], bounds[1:]))
     dom_ms = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
     achieved = works[dom]["flops"] / (dom_ms * 1e-3) * 1e-12
     result = {
@@ -330,6 +359,7 @@ def bench_decoder(args, w):
                      "kernel": dom, "avg_launch_us": round(1000 * dom_ms / launches[dom], 2),
                      "work_per_launch": f"{works[dom]['flops'] / 1e12:.2f} TFLOP per step over "
                                         f"{launches[dom]} launches"},
+        "step_ms": step_stats(step_ms),
         "kernels": per,
     }
     print(json.dumps(result), flush=True)
@@ -415,13 +445,18 @@ def main():
     H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
     t_start, t_stop = ev.create(2)
     torch.cuda.synchronize()
+    marks = ev.create(K - 1)            # step boundaries inside the timed region
     ev.record(t_start, stream)
-    for _ in range(K):
+    for i in range(K):
         step()
+        if i < K - 1:
+            ev.record(marks[i], stream)
     ev.record(t_stop, stream)
     torch.cuda.synchronize()
     H.hero_kernel_timer(H.HERO_K[dom], [], [])
     total_ms = ev.elapsed_ms(t_start, t_stop)
+    bounds = [t_start] + marks + [t_stop]
+    step_ms = sorted(ev.elapsed_ms(a, b) for a, b in zip(bounds[:-1], bounds[1:]))
     dom_ms_step = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K     # per step, all layers
     ms_step = total_ms / K
     print(f"# timed {K} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
@@ -495,6 +530,8 @@ def main():
                    "tokens": w.T, "layers_per_step": L, "parallelism": "none",
                    "n_ffn": n_f if not stack else sum(nfs), "n_adapter": n_a if not stack else sum(nas)},
         "roofline": roof,
+        "step_ms": step_stats(step_ms),
+        "whole_call": ideal_fraction(works, ms_step, w.dtype, stack),
         "kernels": per,
     }
     if not args.no_cpu_baseline and not stack:
