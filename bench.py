@@ -372,6 +372,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama31_8b_layer")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--ablation", type=int, default=0,
+                    help="router ablation bits (1 w/o Pos State, 2 w/o Aux State, 4 w/o MemRead, 8 w/o History)")
     ap.add_argument("--state", choices=("f32", "bf16"), default="f32",
                     help="storage of the router memory S between layers")
     ap.add_argument("--budget", type=float, default=None,
@@ -407,6 +409,10 @@ def main():
         if w.mode != "budget" or not 0.0 <= args.budget <= 1.0:
             sys.exit("--budget needs a budget-mode workload and a fraction in [0, 1]")
         w = w.replace(budget=args.budget)
+    if args.ablation:
+        if not 0 < args.ablation <= 15:
+            sys.exit("--ablation takes bits 1, 2, 4, 8")
+        w = w.replace(ablation=args.ablation)
     if args.state == "bf16":
         if args.memory != "matrix":
             sys.exit("--state bf16 needs the matrix-form memory")
@@ -467,7 +473,10 @@ def main():
     works = [kernel_work(w, nf, na, w.T, jj, args.memory) for nf, na, jj in zip(nfs, nas, layers)]
     per = {}
     handles = {}
-    names = [k for k in H.KERNELS if not k.startswith("attn")]
+    names = [k for k in H.KERNELS if not k.startswith("attn") and not (k == "router_mem" and w.ablation & 12)]
+    if w.ablation & 12:            # no memory pass under the memory-less ablations
+        for wk in works:
+            wk["router_mem"] = dict(flops=0, bytes=0)
     for name in names:
         a, b = ev.create(K * L), ev.create(K * L)
         handles[name] = (a, b)
@@ -508,7 +517,8 @@ def main():
     roof = {"bound": "hbm" if hbm_bound else "mfma", "achieved": round(achieved, 1), "peak": peak,
             "unit": unit, "frac": round(achieved / peak, 4),
             "traffic": counted_traffic(dom) if (args.workload == "llama31_8b_layer" and args.memory == "matrix"
-                                                  and args.budget is None and args.state == "f32") else None,
+                                                  and args.budget is None and args.state == "f32"
+                                                  and not args.ablation) else None,
             "kernel": dom, "avg_launch_us": round(dom_ms_step * 1e3 / n_launch_step, 2),
             "work_per_launch": (f"{per_unit} x {n_f} FFN tokens = {total}"
                                 if not stack else
@@ -524,6 +534,7 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": describe(w, j) + ("" if args.state == "f32" else ", S stored in bf16") +
+                               ("" if not args.ablation else f", router ablation bits {args.ablation}") +
                                ("" if args.memory == "matrix" else
                                                  ", router memory in depth-history form"),
                    "memory": args.memory, "state": args.state, "global_batch": w.batch, "seq_len": w.seq,
