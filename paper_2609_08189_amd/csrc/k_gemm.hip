@@ -193,10 +193,14 @@ struct BlockEpilogue : std::false_type {};
 template <class E>
 struct BlockEpilogue<E, std::void_t<decltype(&E::block)>> : std::true_type {};
 
-template <int BM_, int BN_, int WM_, int WN_, bool DUAL_>
+// NS_: LDS stages of the k-loop; the loads of tile k + NS - 1 are in flight while tile k is
+// consumed (2 for the big products, more where streaming weights from HBM needs more bytes in
+// flight per CU)
+template <int BM_, int BN_, int WM_, int WN_, bool DUAL_, int NS_ = 2>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr bool DUAL = DUAL_;
+  static constexpr int NS = NS_;
   static constexpr int NT = 64 * WM * WN;
   static constexpr int NW = WM * WN;
   static constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -212,7 +216,15 @@ struct Tile {
   static_assert(DUAL ? NW * WTM * SPAD * 2 <= 2 * STAGE : NW * 32 * OPAD * 4 <= 2 * STAGE,
                 "epilogue staging must fit in the stages");
   static_assert((32 * (ON / 8)) % 64 == 0, "epilogue pieces split evenly over the lanes");
+  static_assert(NS >= 2 && NS * STAGE <= 160 * 1024, "stages fit in LDS");
 };
+
+// s_waitcnt vmcnt(N) lgkmcnt(0) for a compile-time N
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(N) : "memory");
+}
 
 template <class C, class Epi>
 __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi,
@@ -225,7 +237,7 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   constexpr int NM = C::TM * C::TN;     // MFMAs per k-step
   constexpr int NR = C::TM + C::TN;     // fragment reads per k-step
   constexpr int NL = A_LD + B_LD;       // stage loads per k-tile
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * C::STAGE];
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::NS * C::STAGE];
   // Workgroups go to the 8 XCDs round-robin; XCD x takes the contiguous range
   // [x per, (x+1) per) of a grouped tile order (GROUP_M row tiles by every column tile),
   // so that the 32 tiles one XCD runs at a time share 8 row panels and 4 column panels
@@ -340,13 +352,19 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   };
 
   const int nk = kt1 - kt0;
-  issue(0, 0);
-  if (nk > 1) issue(1, BK);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  constexpr int NS = C::NS;
+  // tiles 0 .. NS-1 into the NS stages; wait for tile 0 (the others may still be landing)
+#pragma unroll
+  for (int i = 0; i < NS; ++i)
+    if (i < nk) issue(i, i * BK);
+  if (nk >= NS)
+    wait_vm_lgkm<(NS - 1) * NL>();
+  else
+    wait_vm_lgkm<0>();
   __syncthreads();
   read_frags(0, smem, 0);
   for (int kt = 0; kt < nk; ++kt) {
-    const unsigned char* st = smem + (kt & 1) * C::STAGE;
+    const unsigned char* st = smem + (kt % NS) * C::STAGE;
 #pragma unroll
     for (int ks = 0; ks < KS - 1; ++ks) {
       read_frags((ks + 1) & 1, st, ks + 1);
@@ -354,11 +372,15 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
       interleave(std::integral_constant<int, 0>());
       __builtin_amdgcn_sched_barrier(0);
     }
-    // every wave has read all of stage kt and the loads of tile kt+1 have landed
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+    // every wave has read all of stage kt and the loads of tile kt+1 have landed (tiles
+    // kt+2 .. kt+NS-1 may still be in flight; near the end, fewer were issued)
+    if (kt + NS - 1 < nk)
+      wait_vm_lgkm<(NS - 2) * NL>();
+    else
+      wait_vm_lgkm<0>();
     __syncthreads();
-    if (kt + 2 < nk) issue(kt & 1, (kt + 2) * BK);
-    if (kt + 1 < nk) read_frags(KS & 1, smem + ((kt + 1) & 1) * C::STAGE, 0);
+    if (kt + NS < nk) issue(kt % NS, (kt + NS) * BK);
+    if (kt + 1 < nk) read_frags(KS & 1, smem + ((kt + 1) % NS) * C::STAGE, 0);
     mfmas((KS - 1) & 1);
     interleave(std::integral_constant<int, NL>());
     __builtin_amdgcn_sched_barrier(0);
@@ -939,7 +961,10 @@ namespace {
 // over them adds the S slices in a fixed order and finishes the epilogue.
 // ---------------------------------------------------------------------------
 using TileSplitGU = Tile<192, 256, 2, 4, false>;    // [W_g; W_u] as one 2 d_ff-row operand
-using TileSplitDown = Tile<192, 128, 2, 4, false>;
+using TileSplitDown = Tile<192, 128, 2, 4, false, 4>;
+// one row tile (a decode batch): gate/up on 4-wave 192 x 128 tiles (64 output columns each), so
+// that d_ff / 64 workgroups cover the CUs without splitting K, with four stages in flight
+using TileDecodeGU = Tile<192, 128, 2, 2, true, 4>;
 constexpr int kMaxSplitGU = 8, kMaxSplitDown = 16;
 
 int split_ways(int tiles, int nkt, int cap) {
@@ -1043,6 +1068,11 @@ hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const
   if (n_max <= 0) return hipSuccess;
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(u), idx_ffn, d};
+    if (n_max <= TileDecodeGU::BM && d_ff % TileDecodeGU::OUT_N == 0 && d_ff / TileDecodeGU::OUT_N <= kCUs) {
+      BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), INT_MAX, d};
+      return run_tile<TileDecodeGU>(A, B, EpiSwiGLU<bf16_t>{static_cast<bf16_t*>(act), d_ff}, counts,
+                                    n_max, d_ff, d, s);
+    }
     const int S = gateup_split(n_max, d, d_ff);
     if (S > 1) {
       BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), d_ff, d};
