@@ -44,7 +44,10 @@ constant here):
     encoder (z_a = 0); w/o MemRead keeps the history head but gives it no memory
     (c = 0 and nu = 0 at every layer, as at the first routed block) and leaves S,
     zeta as they came in; w/o History removes the history branch (a = 0, so the
-    logit is the local one), writes p = m = 1 and leaves S, zeta as they came in.
+    logit is the local one), writes p = m = 1 and leaves S, zeta as they came in;
+  * the training-side backward (last section) holds the branch decision fixed, gives the
+    frozen backbone no gradient, hands the router dL/dlogit = dL/dg g (1 - g), and takes
+    the utilisation penalty over the first T - 1 positions of each sequence.
 """
 from __future__ import annotations
 
@@ -667,3 +670,124 @@ def decoder_stack(dims: Dims, adims: AttnDims, n_layers, batch, seq, h_in,
         hist = [hbar, hist[0]]
         h = res.h
     return DecoderResult(h, state, hbars, routed)
+
+
+# ---------------------------------------------------------------------------
+# Training side: the backward of the routed block through the gate scaling (Sec. 3.1,
+# eq:ffn_route and the remark after it) and the gate-utilisation penalty (Sec. 3.3, Eq. 17-18)
+#
+# Readings: the branch decision is a constant of the backward (the threshold is not
+# differentiated); the backbone (LN^ffn gain and the FFN weights) is frozen, so it takes no
+# gradient but passes one on to hbar; the gradient leaves the block at hbar (the residual, and
+# LN^ffn through the branch taken) and at the gate g, and the router receives it as
+# dL/dlogit = dL/dg g (1 - g) (g = sigma(logit)).  Only the adapter weights of the block are
+# trained here.  The penalty's positions are the first T - 1 of every length-T sequence (those
+# with a next token; none when T = 1), tokens ordered sequence-major (t = b T + pos), and the
+# weight alpha_t is an input.  Everything is float64 with no rounding.
+# ---------------------------------------------------------------------------
+
+
+@dataclasses.dataclass
+class BlockGrad:
+    dhbar: np.ndarray   # [T, d]   dL/dhbar
+    dgate: np.ndarray   # [T]      dL/dg (including a gradient passed in for g)
+    dlogit: np.ndarray  # [T]      dL/dlogit
+    dw1: np.ndarray     # [d_r, d] dL/dW_1
+    dw2: np.ndarray     # [d, d_r] dL/dW_2
+
+
+def routed_block(hbar, gate, use_ffn, ffn: FFNParams, ad: AdapterParams, dims: Dims):
+    """The routed block's output (eq:ffn_route) for a given gate and branch decision, in float64
+    without rounding: the function whose gradient routed_block_backward forms."""
+    hbar = np.asarray(hbar, dtype=f64)
+    gate = np.asarray(gate, dtype=f64)
+    use_ffn = np.asarray(use_ffn, dtype=bool)
+    u = ffn_input(hbar, ffn, dims)
+    ffn_out = np.zeros_like(hbar)
+    ad_out = np.zeros_like(hbar)
+    if use_ffn.any():
+        ffn_out[use_ffn] = frozen_ffn(u[use_ffn], ffn)
+    if (~use_ffn).any():
+        ad_out[~use_ffn] = adapter(u[~use_ffn], ad)
+    return routed_output(hbar, gate, use_ffn, ffn_out, ad_out)
+
+
+def silu_grad(x):
+    """d SiLU(x) / dx = sigma(x) (1 + x (1 - sigma(x)))."""
+    s = sigmoid(x)
+    return s * (1.0 + x * (1.0 - s))
+
+
+def rmsnorm_backward(h, gain, eps_norm, du):
+    """dL/dh of u = h r gain with r = (mean(h^2) + eps)^(-1/2), given dL/du, per token row:
+    dh = r (gain du) - (r^3 / d) h <gain du, h>."""
+    h = np.asarray(h, dtype=f64)
+    d = h.shape[-1]
+    r = 1.0 / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + eps_norm)
+    gdu = du * gain
+    return r * gdu - (r ** 3 / d) * h * np.sum(gdu * h, axis=-1, keepdims=True)
+
+
+def routed_block_backward(hbar, gate, use_ffn, ffn: FFNParams, ad: AdapterParams, dims: Dims,
+                          dh_out, dgate_in=None) -> BlockGrad:
+    """Gradients of the routed block, given dL/dh_out (and optionally a further dL/dg, e.g. the
+    utilisation penalty's), by the chain rule through eq:ffn_route:
+      FFN token:     h = hbar + g y,       y = W_d (SiLU(G) * U), G = W_g u, U = W_u u
+      adapter token: h = hbar + (1 - g) y, y = W_2 SiLU(z),       z = W_1 u
+    with u = LN^ffn(hbar) and the branch fixed."""
+    hbar = np.asarray(hbar, dtype=f64)
+    gate = np.asarray(gate, dtype=f64)
+    use_ffn = np.asarray(use_ffn, dtype=bool)
+    dh = np.asarray(dh_out, dtype=f64)
+    T = hbar.shape[0]
+    u = ffn_input(hbar, ffn, dims)
+    du = np.zeros_like(u)
+    dgate = np.zeros(T)
+    f = use_ffn
+    if f.any():
+        uf = u[f]
+        G = uf @ ffn.w_gate.T
+        U = uf @ ffn.w_up.T
+        y = (silu(G) * U) @ ffn.w_down.T
+        dgate[f] = np.sum(dh[f] * y, axis=-1)
+        dact = (gate[f, None] * dh[f]) @ ffn.w_down
+        dG = dact * U * silu_grad(G)
+        dU = dact * silu(G)
+        du[f] = dG @ ffn.w_gate + dU @ ffn.w_up
+    a = ~use_ffn
+    dw1 = np.zeros_like(np.asarray(ad.w1, dtype=f64))
+    dw2 = np.zeros_like(np.asarray(ad.w2, dtype=f64))
+    if a.any():
+        ua = u[a]
+        z = ua @ ad.w1.T
+        hid = silu(z)
+        y = hid @ ad.w2.T
+        dgate[a] = -np.sum(dh[a] * y, axis=-1)
+        dy = (1.0 - gate[a, None]) * dh[a]
+        dw2 = dy.T @ hid
+        dz = (dy @ ad.w2) * silu_grad(z)
+        dw1 = dz.T @ ua
+        du[a] = dz @ ad.w1
+    dhbar = dh + rmsnorm_backward(hbar, ffn.norm_w, dims.eps_norm, du)
+    if dgate_in is not None:
+        dgate = dgate + np.asarray(dgate_in, dtype=f64)
+    dlogit = dgate * gate * (1.0 - gate)
+    return BlockGrad(dhbar, dgate, dlogit, dw1, dw2)
+
+
+def skip_penalty(gates, batch, seq, alpha=1.0):
+    """alpha L_skip of Eq. 18 and its gradient over the gates.
+
+    gates [L_R, batch * seq] (token t = b seq + pos).  L_skip is the mean over the
+    batch (seq - 1) positions with a next token of the squared sum of the token's gates over
+    the routed blocks; the gradient at such a position is 2 alpha (sum_j g) / (batch (seq - 1))
+    for every block, and 0 at each sequence's last position.  Returns (value, [L_R, batch*seq])."""
+    g = np.asarray(gates, dtype=f64).reshape(gates.shape[0], batch, seq)
+    grad = np.zeros_like(g)
+    if seq < 2:
+        return 0.0, grad.reshape(gates.shape)
+    n = batch * (seq - 1)
+    tot = g[:, :, : seq - 1].sum(axis=0)            # [batch, seq - 1]
+    value = alpha * float(np.sum(tot * tot)) / n
+    grad[:, :, : seq - 1] = (2.0 * alpha / n) * tot[None]
+    return value, grad.reshape(gates.shape)
