@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define HERO_ABI_VERSION 4
+#define HERO_ABI_VERSION 5
 
 typedef enum hero_status {
   HERO_OK = 0,
@@ -199,7 +199,16 @@ typedef enum hero_kernel {
   HERO_K_ATTN_QKV = 11,     /* [q; k; v] = x W_qkv^T with the rotary embedding                  */
   HERO_K_ATTN_CORE = 12,    /* causal grouped-query softmax attention                           */
   HERO_K_ATTN_OUT = 13,     /* hbar = h + o W_o^T                                               */
-  HERO_K_COUNT = 14
+  /* backward of the routed block (hero_routed_block_backward) and the penalty */
+  HERO_K_BWD_NORM = 14,     /* branch lists copied in range; u and 1/rms recomputed             */
+  HERO_K_BWD_FFN_E = 15,    /* e = dL/dh W_d over the FFN tokens                                */
+  HERO_K_BWD_FFN_GATE_UP = 16, /* G, U recomputed; dG, dU and the shares of dL/dg              */
+  HERO_K_BWD_FFN_DU = 17,   /* du = [dG dU] [W_g; W_u]                                          */
+  HERO_K_BWD_ADAPTER = 18,  /* W_1^T, W_2^T; z, e_a; a, dz, dL/dg; du = dz W_1                 */
+  HERO_K_BWD_ADAPTER_WGRAD = 19, /* dW_1, dW_2                                                  */
+  HERO_K_BWD_ROWS = 20,     /* dL/dhbar (RMSNorm backward + residual), dL/dg, dL/dlogit          */
+  HERO_K_SKIP_PENALTY = 21, /* alpha L_skip and its gradient                                    */
+  HERO_K_COUNT = 22
 } hero_kernel;
 
 /*
@@ -378,6 +387,74 @@ int hero_decoder_stack(const hero_dims *dims, const hero_attn_dims *adims, int n
                        const float *eta, const float *inv_freq, const hero_routing *routing,
                        const hero_layer_stats *stats, void *workspace, size_t workspace_bytes,
                        void *stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Training side: the backward of a routed block through the gate scaling (Sec. 3.1,
+ * eq:ffn_route and the remark after it) and the gate-utilisation penalty (Sec. 3.3,
+ * Eq. 17-18).  The backbone is frozen: its FFN and LN^ffn pass a gradient on to hbar but take
+ * none; the adapter's weights take theirs; the router receives dL/dlogit.  The branch
+ * decision is a constant of the backward (the threshold is not differentiated).
+ * ------------------------------------------------------------------------------------- */
+
+/* Transposed copies of one frozen FFN's weights, which the backward's products read
+ * (dims.dtype, caller-owned, made once per model by hero_ffn_backward_weights_make):
+ *   w_down_t    [d_ff][d]      W_d^T
+ *   w_gate_up_t [d][2 d_ff]    [W_g; W_u]^T: row i holds column i of W_g, then of W_u */
+typedef struct hero_ffn_backward_weights {
+  const void *w_down_t, *w_gate_up_t;
+} hero_ffn_backward_weights;
+
+/* Fill w_down_t and w_gate_up_t (device, dims.dtype, 16-byte aligned, not overlapping the
+ * weights or each other) from ffn.  Asynchronous on `stream`. */
+int hero_ffn_backward_weights_make(const hero_dims *dims, const hero_ffn_weights *ffn, void *w_down_t,
+                                   void *w_gate_up_t, void *stream);
+
+/* Outputs of hero_routed_block_backward (all required, device, overwritten):
+ *   dhbar  [T][d] dims.dtype   dL/dhbar: dL/dh plus LN^ffn's backward of the branch's du
+ *   dgate  [T] fp32            dL/dg (with dgate_in added)
+ *   dlogit [T] fp32            dL/dlogit = dL/dg g (1 - g), what the router's backward takes
+ *   dw1    [d_r][d] fp32       dL/dW_1
+ *   dw2    [d][d_r] fp32       dL/dW_2 */
+typedef struct hero_block_grads {
+  void *dhbar;
+  float *dgate, *dlogit, *dw1, *dw2;
+} hero_block_grads;
+
+/* Workspace bytes for hero_routed_block_backward with T tokens.  Host-only; validates dims. */
+int hero_backward_workspace_size(const hero_dims *dims, int T, size_t *bytes);
+
+/*
+ * Backward of one routed block (eq:ffn_route with u = RMSNorm_w(hbar)) given dL/dh_out:
+ *   FFN token t   (h = hbar + g y, y = W_d (SiLU(W_g u) * (W_u u))):
+ *     dL/dg = <dL/dh, y>; du from dL/dy = g dL/dh through the SwiGLU;
+ *   adapter token (h = hbar + (1 - g) y, y = W_2 SiLU(W_1 u)):
+ *     dL/dg = -<dL/dh, y>; dW_2 += ((1 - g) dL/dh) SiLU(z)^T, dW_1 += dz u^T, du = dz W_1;
+ *   dL/dhbar = dL/dh + RMSNorm_w backward of du;  dL/dg += dgate_in (may be NULL: e.g. the
+ *   penalty's gradient from hero_skip_penalty);  dL/dlogit = dL/dg g (1 - g).
+ * gate, idx_ffn, idx_ad, counts are the forward's (hero_layer_stats of the same layer: every
+ * token in exactly one list).  The lists are read through copies with counts clamped to
+ * [0, T] and indices to [0, T - 1], so malformed lists give wrong values, never an access out
+ * of bounds.  The FFN's gate/up products are recomputed from hbar (the forward's activations
+ * are not kept).  dhbar must not overlap hbar or dh_out.  All products are bf16 x bf16 with
+ * fp32 accumulation for a bf16 model (e and [dG dU] pass through HBM in bf16), fp32 otherwise;
+ * every reduction has a fixed order.
+ */
+int hero_routed_block_backward(const hero_dims *dims, int T, const void *hbar, const void *dh_out,
+                               const float *gate, const int32_t *idx_ffn, const int32_t *idx_ad,
+                               const int32_t *counts, const float *dgate_in, const hero_ffn_weights *ffn,
+                               const hero_ffn_backward_weights *ffn_t, const hero_adapter_weights *adapter,
+                               const hero_block_grads *grads, void *workspace, size_t workspace_bytes,
+                               void *stream);
+
+/*
+ * alpha L_skip (Eq. 18) and its gradient: gates [L_R][batch seq] fp32 (the routed blocks'
+ * g, token t = b seq + pos); L_skip is the mean, over the batch (seq - 1) positions that have
+ * a next token, of the square of the token's gate sum over the L_R blocks.  loss[0] = alpha
+ * L_skip; dgates [L_R][batch seq] = 2 alpha (sum_j g) / (batch (seq - 1)) at those positions
+ * and 0 at each sequence's last (everything 0 when seq = 1).  dgates must not overlap gates.
+ */
+int hero_skip_penalty(int L_R, int batch, int seq, const float *gates, float alpha, float *loss,
+                      float *dgates, void *stream);
 
 #ifdef __cplusplus
 }

@@ -810,3 +810,250 @@ int hero_decoder_stack(const hero_dims* dims, const hero_attn_dims* adims, int n
   }
   return HERO_OK;
 }
+
+// ---------------------------------------------------------------------------
+// Training side: backward of the routed block, the utilisation penalty
+// ---------------------------------------------------------------------------
+namespace {
+
+// adapter tokens per partial of the weight gradients: at most 16 partials, whole LDS batches
+int wgrad_chunk(int T) {
+  const int c = (T + 15) / 16;
+  return std::max(64, (c + 63) / 64 * 64);
+}
+
+// the adapter rank as the K of the du product: whole 64-deep k-tiles on the MFMA path
+int rank_pad(const hero_dims& d) { return d.dtype == HERO_BF16 ? (d.d_r + 63) / 64 * 64 : d.d_r; }
+
+struct BwdLayout {
+  size_t idx_f, idx_a, counts, rowstat, u, e, dgu, dgpart, du_f, du_a, part_z, part_e, dz32, a32, dzk, dg_ad,
+      w1t, w2t, pw1, pw2, total;
+  int n_parts, chunk, rpad;
+};
+
+BwdLayout bwd_layout_of(const hero_dims& d, int T) {
+  const size_t es = esize(d.dtype), t = static_cast<size_t>(T);
+  BwdLayout L{};
+  L.n_parts = hero::swiglu_bwd_parts(d.dtype, d.d_ff);
+  L.chunk = wgrad_chunk(T);
+  L.rpad = rank_pad(d);
+  const size_t n_chunks = (t + L.chunk - 1) / L.chunk;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.idx_f = take(t * 4);
+  L.idx_a = take(t * 4);
+  L.counts = take(16);
+  L.rowstat = take(t * 16);
+  L.u = take(t * d.d * es);
+  L.e = take(t * d.d_ff * es);
+  L.dgu = take(t * 2 * d.d_ff * es);
+  L.dgpart = take(t * L.n_parts * 4);
+  L.du_f = take(t * d.d * 4);
+  L.du_a = take(t * d.d * 4);
+  L.part_z = take(hero::adapter_part_floats(d.dtype, d.d, d.d_r, T) * 4);
+  L.part_e = take(hero::adapter_part_floats(d.dtype, d.d, d.d_r, T) * 4);
+  L.dz32 = take(t * d.d_r * 4);
+  L.a32 = take(t * d.d_r * 4);
+  L.dzk = take(t * L.rpad * es);
+  L.dg_ad = take(t * 4);
+  L.w1t = take(static_cast<size_t>(d.d) * L.rpad * es);
+  L.w2t = take(static_cast<size_t>(d.d_r) * d.d * es);
+  L.pw1 = take(n_chunks * d.d_r * d.d * 4);
+  L.pw2 = take(n_chunks * d.d_r * d.d * 4);
+  L.total = off;
+  return L;
+}
+
+// the GEMM core addresses operand rows with 32-bit byte offsets
+bool bwd_fits(const hero_dims& d, int T) {
+  const size_t es = esize(d.dtype);
+  return static_cast<size_t>(T) * 2 * d.d_ff * es < (static_cast<size_t>(1) << 32) &&
+         static_cast<size_t>(d.d_ff) * d.d * es < (static_cast<size_t>(1) << 32) &&
+         static_cast<size_t>(T) * d.d * es < (static_cast<size_t>(1) << 32);
+}
+
+int check_ffn(const hero_ffn_weights* f) {
+  if (!f || !f->norm_w || !f->w_gate || !f->w_up || !f->w_down) return HERO_E_NULL;
+  if (!aligned16(f->norm_w) || !aligned16(f->w_gate) || !aligned16(f->w_up) || !aligned16(f->w_down))
+    return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+int check_adapter(const hero_adapter_weights* a) {
+  if (!a || !a->w1 || !a->w2) return HERO_E_NULL;
+  if (!aligned16(a->w1) || !aligned16(a->w2)) return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+}  // namespace
+
+int hero_ffn_backward_weights_make(const hero_dims* dims, const hero_ffn_weights* ffn, void* w_down_t,
+                                   void* w_gate_up_t, void* stream) {
+  int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if ((st = check_ffn(ffn)) != HERO_OK) return st;
+  if (!w_down_t || !w_gate_up_t) return HERO_E_NULL;
+  if (!aligned16(w_down_t) || !aligned16(w_gate_up_t)) return HERO_E_ALIGN;
+  const size_t wb = static_cast<size_t>(dims->d) * dims->d_ff * esize(dims->dtype);
+  const void* in[] = {ffn->w_gate, ffn->w_up, ffn->w_down};
+  for (const void* p : in)
+    if (overlap(w_down_t, wb, p, wb) || overlap(w_gate_up_t, 2 * wb, p, wb)) return HERO_E_ALIAS;
+  if (overlap(w_down_t, wb, w_gate_up_t, 2 * wb)) return HERO_E_ALIAS;
+  if ((st = check_device()) != HERO_OK) return st;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int d = dims->d, f = dims->d_ff, dt = dims->dtype;
+  unsigned char* gu = static_cast<unsigned char*>(w_gate_up_t);
+  hipError_t e = hero::launch_transpose(dt, ffn->w_down, d, f, f, w_down_t, d, d, s);
+  if (e == hipSuccess) e = hero::launch_transpose(dt, ffn->w_gate, f, d, d, gu, 2 * f, f, s);
+  if (e == hipSuccess) e = hero::launch_transpose(dt, ffn->w_up, f, d, d, gu + f * esize(dt), 2 * f, f, s);
+  return e == hipSuccess ? HERO_OK : HERO_E_LAUNCH;
+}
+
+int hero_backward_workspace_size(const hero_dims* dims, int T, size_t* bytes) {
+  if (!bytes) return HERO_E_NULL;
+  const int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if (T <= 0) return HERO_E_DIM;
+  *bytes = bwd_layout_of(*dims, T).total;
+  return HERO_OK;
+}
+
+int hero_routed_block_backward(const hero_dims* dims, int T, const void* hbar, const void* dh_out,
+                               const float* gate, const int32_t* idx_ffn, const int32_t* idx_ad,
+                               const int32_t* counts, const float* dgate_in, const hero_ffn_weights* ffn,
+                               const hero_ffn_backward_weights* ffn_t, const hero_adapter_weights* adapter,
+                               const hero_block_grads* grads, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  using namespace hero;
+  int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if (T <= 0) return HERO_E_DIM;
+  if (!bwd_fits(*dims, T)) return HERO_E_UNSUPPORTED;
+  if (!hbar || !dh_out || !gate || !idx_ffn || !idx_ad || !counts || !ffn_t || !grads) return HERO_E_NULL;
+  if (!ffn_t->w_down_t || !ffn_t->w_gate_up_t || !grads->dhbar || !grads->dgate || !grads->dlogit ||
+      !grads->dw1 || !grads->dw2)
+    return HERO_E_NULL;
+  if ((st = check_ffn(ffn)) != HERO_OK) return st;
+  if ((st = check_adapter(adapter)) != HERO_OK) return st;
+  const void* al[] = {hbar, dh_out, gate, idx_ffn, idx_ad, counts, dgate_in, ffn_t->w_down_t, ffn_t->w_gate_up_t,
+                      grads->dhbar, grads->dgate, grads->dlogit, grads->dw1, grads->dw2, workspace};
+  for (const void* p : al)
+    if (p && !aligned16(p)) return HERO_E_ALIGN;
+  const size_t hb = static_cast<size_t>(T) * dims->d * esize(dims->dtype);
+  if (overlap(grads->dhbar, hb, hbar, hb) || overlap(grads->dhbar, hb, dh_out, hb)) return HERO_E_ALIAS;
+  const BwdLayout L = bwd_layout_of(*dims, T);
+  if (!workspace || workspace_bytes < L.total) return HERO_E_WORKSPACE;
+  if (overlap(workspace, L.total, hbar, hb) || overlap(workspace, L.total, dh_out, hb) ||
+      overlap(workspace, L.total, grads->dhbar, hb))
+    return HERO_E_ALIAS;
+  if ((st = check_device()) != HERO_OK) return st;
+
+  const hero_dims& D = *dims;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  BlockBwdArgs a{};
+  a.dtype = D.dtype;
+  a.T = T;
+  a.d = D.d;
+  a.d_r = D.d_r;
+  a.rpad = L.rpad;
+  a.dh = dh_out;
+  a.hbar = hbar;
+  a.norm_w = ffn->norm_w;
+  a.rowstat = reinterpret_cast<float*>(ws + L.rowstat);
+  int* idx_f = reinterpret_cast<int*>(ws + L.idx_f);
+  int* idx_a = reinterpret_cast<int*>(ws + L.idx_a);
+  int* cnt = reinterpret_cast<int*>(ws + L.counts);
+  a.idx_ffn = idx_f;
+  a.idx_ad = idx_a;
+  a.counts = cnt;
+  a.gate = gate;
+  a.dgate_in = dgate_in;
+  a.du_f = reinterpret_cast<float*>(ws + L.du_f);
+  a.du_a = reinterpret_cast<float*>(ws + L.du_a);
+  a.dgpart = reinterpret_cast<float*>(ws + L.dgpart);
+  a.n_parts = L.n_parts;
+  a.dg_ad = reinterpret_cast<float*>(ws + L.dg_ad);
+  a.part_z = reinterpret_cast<float*>(ws + L.part_z);
+  a.part_e = reinterpret_cast<float*>(ws + L.part_e);
+  a.splits = adapter_proj_splits(D.dtype, D.d, D.d_r);
+  a.dz32 = reinterpret_cast<float*>(ws + L.dz32);
+  a.a32 = reinterpret_cast<float*>(ws + L.a32);
+  a.dzk = ws + L.dzk;
+  a.u = ws + L.u;
+  a.chunk = L.chunk;
+  a.pw1 = reinterpret_cast<float*>(ws + L.pw1);
+  a.pw2 = reinterpret_cast<float*>(ws + L.pw2);
+  a.dhbar = grads->dhbar;
+  a.dgate = grads->dgate;
+  a.dlogit = grads->dlogit;
+  a.dw1 = grads->dw1;
+  a.dw2 = grads->dw2;
+  void* u = ws + L.u;
+  void* e = ws + L.e;
+  void* dgu = ws + L.dgu;
+  void* w1t = ws + L.w1t;
+  void* w2t = ws + L.w2t;
+
+  hipError_t err = timed(HERO_K_BWD_NORM, s, [&] {
+    hipError_t x = launch_bwd_lists(T, idx_ffn, idx_ad, counts, idx_f, idx_a, cnt, s);
+    if (x != hipSuccess) return x;
+    return launch_rowstats(D.dtype, hbar, nullptr, nullptr, ffn->norm_w, T, D.d, 1, D.eps_norm,
+                           const_cast<float*>(a.rowstat), u, s);
+  });
+  if (err != hipSuccess) return HERO_E_LAUNCH;
+  err = timed(HERO_K_BWD_FFN_E, s, [&] {
+    return launch_ffn_bwd_e(D.dtype, dh_out, idx_f, cnt, T, ffn_t->w_down_t, e, D.d, D.d_ff, s);
+  });
+  if (err != hipSuccess) return HERO_E_LAUNCH;
+  err = timed(HERO_K_BWD_FFN_GATE_UP, s, [&] {
+    return launch_ffn_bwd_gateup(D.dtype, u, idx_f, cnt, T, ffn->w_gate, ffn->w_up, e, gate, dgu,
+                                 const_cast<float*>(a.dgpart), D.d, D.d_ff, s);
+  });
+  if (err != hipSuccess) return HERO_E_LAUNCH;
+  err = timed(HERO_K_BWD_FFN_DU, s, [&] {
+    return launch_ffn_bwd_du(D.dtype, dgu, cnt, T, ffn_t->w_gate_up_t, const_cast<float*>(a.du_f), D.d, D.d_ff, s);
+  });
+  if (err != hipSuccess) return HERO_E_LAUNCH;
+  err = timed(HERO_K_BWD_ADAPTER, s, [&] {
+    hipError_t x = launch_transpose(D.dtype, adapter->w2, D.d, D.d_r, D.d_r, w2t, D.d, D.d, s);
+    if (x == hipSuccess) x = launch_transpose(D.dtype, adapter->w1, D.d_r, D.d, D.d, w1t, L.rpad, L.rpad, s);
+    if (x == hipSuccess)
+      x = launch_adapter_proj(D.dtype, u, idx_a, cnt + 1, T, adapter->w1, const_cast<float*>(a.part_z), D.d, D.d_r, s);
+    if (x == hipSuccess)
+      x = launch_adapter_proj(D.dtype, dh_out, idx_a, cnt + 1, T, w2t, const_cast<float*>(a.part_e), D.d, D.d_r, s);
+    if (x == hipSuccess) x = launch_adapter_bwd_mid(a, s);
+    if (x == hipSuccess)
+      x = launch_adapter_du(D.dtype, a.dzk, cnt + 1, T, w1t, const_cast<float*>(a.du_a), D.d, L.rpad, s);
+    return x;
+  });
+  if (err != hipSuccess) return HERO_E_LAUNCH;
+  err = timed(HERO_K_BWD_ADAPTER_WGRAD, s, [&] { return launch_adapter_wgrad(a, s); });
+  if (err != hipSuccess) return HERO_E_LAUNCH;
+  err = timed(HERO_K_BWD_ROWS, s, [&] { return launch_block_bwd_rows(a, s); });
+  return err == hipSuccess ? HERO_OK : HERO_E_LAUNCH;
+}
+
+int hero_skip_penalty(int L_R, int batch, int seq, const float* gates, float alpha, float* loss, float* dgates,
+                      void* stream) {
+  if (L_R <= 0 || batch <= 0 || seq <= 0) return HERO_E_DIM;
+  if (static_cast<long long>(batch) * seq > INT_MAX) return HERO_E_DIM;
+  if (!(alpha - alpha == 0.f)) return HERO_E_RANGE;
+  if (!gates || !loss || !dgates) return HERO_E_NULL;
+  if (!aligned16(gates) || !aligned16(loss) || !aligned16(dgates)) return HERO_E_ALIGN;
+  const size_t gb = static_cast<size_t>(L_R) * batch * seq * 4;
+  if (overlap(dgates, gb, gates, gb) || overlap(loss, 4, gates, gb) || overlap(loss, 4, dgates, gb))
+    return HERO_E_ALIAS;
+  int st = check_device();
+  if (st != HERO_OK) return st;
+  return timed(HERO_K_SKIP_PENALTY, static_cast<hipStream_t>(stream), [&] {
+           return hero::launch_skip_penalty(gates, L_R, batch, seq, alpha, loss, dgates,
+                                            static_cast<hipStream_t>(stream));
+         }) == hipSuccess
+             ? HERO_OK
+             : HERO_E_LAUNCH;
+}

@@ -126,4 +126,81 @@ hipError_t launch_adapter_up(int dtype, const float* part, const int* idx_ad, co
                              int n_max, const void* w2, const void* hbar, const float* gate,
                              void* h_out, int d, int d_r, hipStream_t s);
 
+// ---------------------------------------------------------------------------
+// Backward of the routed block (training side; frozen FFN, trained adapter)
+// ---------------------------------------------------------------------------
+// copies of the branch lists with counts clamped to [0, T] (n_ffn + n_ad <= T) and indices to
+// [0, T - 1]: f, ad [T], c [2]
+hipError_t launch_bwd_lists(int T, const int* idx_ffn, const int* idx_ad, const int* counts, int* f, int* ad,
+                            int* c, hipStream_t s);
+// out[c][r] = in[r][c] for r < R, c < C ([R][C] with row pitch ld_in into rows of pitch
+// ld_out); with R_pad > R the columns R .. R_pad - 1 of every output row are written as 0
+hipError_t launch_transpose(int dtype, const void* in, int R, int C, int ld_in, void* out, int ld_out,
+                            int R_pad, hipStream_t s);
+// e[m] = dL/dh[idx_ffn[m]] W_d (W_d^T given, [d_ff][d]), storage dtype, [n][d_ff]
+hipError_t launch_ffn_bwd_e(int dtype, const void* dh, const int* idx_ffn, const int* counts, int n_max,
+                            const void* w_down_t, void* e, int d, int d_ff, hipStream_t s);
+// G, U recomputed from u[idx_ffn[m]]; dgu[m] = [dG | dU] (storage dtype, [n][2 d_ff]) and
+// dgpart[m][p] = the p-th share of <e_m, act_m> (swiglu_bwd_parts(dtype, d_ff) per row)
+int swiglu_bwd_parts(int dtype, int d_ff);
+hipError_t launch_ffn_bwd_gateup(int dtype, const void* u, const int* idx_ffn, const int* counts, int n_max,
+                                 const void* w_gate, const void* w_up, const void* e, const float* gate,
+                                 void* dgu, float* dgpart, int d, int d_ff, hipStream_t s);
+// du[m] = dgu[m] [W_g; W_u] (([W_g; W_u])^T given, [d][2 d_ff]), fp32 [n][d]
+hipError_t launch_ffn_bwd_du(int dtype, const void* dgu, const int* counts, int n_max, const void* w_gate_up_t,
+                             float* du, int d, int d_ff, hipStream_t s);
+// part[z][m][n] (z < adapter_proj_splits, slices n_max d_r floats apart): K-slice partial sums
+// of rows[idx_ad[m]] W^T for W [d_r][d] (adapter_part_floats(dtype, d, d_r, n_max) floats)
+int adapter_proj_splits(int dtype, int d, int d_r);
+hipError_t launch_adapter_proj(int dtype, const void* rows, const int* idx_ad, const int* counts, int n_max,
+                               const void* w, float* part, int d, int d_r, hipStream_t s);
+// du[m] = dz[m] W_1 (W_1^T given, [d][k]); dz [n][k] in the storage dtype, k = the rank padded to
+// a multiple of 64 (bf16) or d_r (fp32)
+hipError_t launch_adapter_du(int dtype, const void* dz, const int* counts, int n_max, const void* w1t, float* du,
+                             int d, int k, hipStream_t s);
+
+struct BlockBwdArgs {
+  int dtype, T, d, d_r, rpad;
+  const void* dh;            // [T][d]    dL/dh_out
+  const void* hbar;          // [T][d]
+  const void* norm_w;        // [d]
+  const float* rowstat;      // [T][4]    1/rms in [0]
+  const int* idx_ffn;
+  const int* idx_ad;
+  const int* counts;         // [2]
+  const float* gate;         // [T]
+  const float* dgate_in;     // [T] or null
+  const float* du_f;         // [T][d]    FFN rows, in idx_ffn order
+  const float* du_a;         // [T][d]    adapter rows, in idx_ad order
+  const float* dgpart;       // [T][n_parts]
+  int n_parts;
+  float* dg_ad;              // [T]
+  // adapter
+  const float* part_z;       // [splits][T][d_r]
+  const float* part_e;
+  int splits;
+  float* dz32;               // [T][d_r]
+  float* a32;                // [T][d_r]
+  void* dzk;                 // [T][rpad] storage dtype (the du product's A operand)
+  const void* u;             // [T][d]
+  int chunk;                 // adapter tokens per weight-gradient partial
+  float* pw1;                // [n_chunks][d_r][d]
+  float* pw2;                // [n_chunks][d][d_r]
+  // outputs
+  void* dhbar;               // [T][d]
+  float* dgate;              // [T]
+  float* dlogit;             // [T]
+  float* dw1;                // [d_r][d]
+  float* dw2;                // [d][d_r]
+};
+// a = SiLU(z), dz = (1 - g) e_a SiLU'(z), dL/dg = -<e_a, a> for every adapter row
+hipError_t launch_adapter_bwd_mid(const BlockBwdArgs& a, hipStream_t s);
+// dW_1 = sum_m dz_m u_m^T, dW_2 = sum_m ((1 - g) dL/dh)_m a_m^T over the adapter rows
+hipError_t launch_adapter_wgrad(const BlockBwdArgs& a, hipStream_t s);
+// dL/dhbar = dL/dh + RMSNorm backward of du (every token once), dL/dg, dL/dlogit
+hipError_t launch_block_bwd_rows(const BlockBwdArgs& a, hipStream_t s);
+// alpha L_skip (Eq. 18) into loss[0] and its gradient over gates [L_R][batch seq]
+hipError_t launch_skip_penalty(const float* gates, int L_R, int batch, int seq, float alpha, float* loss,
+                               float* dgates, hipStream_t s);
+
 }  // namespace hero

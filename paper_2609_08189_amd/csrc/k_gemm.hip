@@ -99,6 +99,53 @@ struct EpiSiLU {  // hid[m][n] = SiLU(acc)
   }
 };
 
+template <typename T>
+struct EpiStore {  // out[m][n] = acc in the storage dtype
+  T* out;
+  int ld;
+  struct Pre {};
+  __device__ __forceinline__ Pre prep(int, int) const { return {}; }
+  __device__ __forceinline__ void store(int m, int n, float v) const {
+    stf(out + static_cast<size_t>(m) * ld + n, v);
+  }
+  __device__ __forceinline__ void emit8(const Pre&, int m, int n, const float* v) const {
+    st8(out + static_cast<size_t>(m) * ld + n, v);
+  }
+};
+
+// Backward of the gated SwiGLU branch, on the recomputed gate/up products G = u W_g^T,
+// U = u W_u^T of FFN row m (token t = idx[m]), given e = dL/dy W_d at the same (m, c) with
+// dL/dy = g_t dL/dh (e itself carries no g):
+//   act = SiLU(G) U,  dL/dact = g_t e,
+//   dG = g_t e U SiLU'(G),  dU = g_t e SiLU(G)   -> dgu[m][c], dgu[m][d_ff + c]
+//   the row's share of dL/dg_t = <dL/dh_t, y_t> = <e_m, act_m> over the tile's columns
+//                                                  -> dgpart[m][part]
+// The MFMA path hands this epilogue the accumulators of a finished wave tile (dual); the
+// fp32 path calls store2 per element with one partial per column.
+template <typename T>
+struct EpiSwiGLUBwd {
+  const T* e;
+  int ld_e;
+  const int* idx;
+  const float* gate;
+  T* dgu;
+  int ld_dgu;
+  int d_ff;
+  float* dgpart;
+  int n_parts;
+  static constexpr bool kDualHook = true;
+  __device__ __forceinline__ void store2(int m, int c, float g, float u) const {
+    const int t = idx ? idx[m] : m;
+    const float gt = gate ? gate[t] : 1.0f;
+    const float ev = ldf(e + static_cast<size_t>(m) * ld_e + c);
+    const float sg = 1.0f / (1.0f + expf(-g));
+    const float act = g * sg * u, dact = gt * ev;
+    stf(dgu + static_cast<size_t>(m) * ld_dgu + c, dact * u * sg * (1.0f + g * (1.0f - sg)));
+    stf(dgu + static_cast<size_t>(m) * ld_dgu + d_ff + c, dact * g * sg);
+    dgpart[static_cast<size_t>(m) * n_parts + c] = ev * act;
+  }
+};
+
 // h_out[t][n] = hbar[t][n] + scale(g_t) * acc, t = idx[m]; FFN scales by g, adapter by 1 - g.
 // Without an index list t = m, and without gates the scale is 1 (a plain residual add: the
 // dense FFN of a non-routed block, the attention output projection).
@@ -192,6 +239,16 @@ template <class E, class = void>
 struct BlockEpilogue : std::false_type {};
 template <class E>
 struct BlockEpilogue<E, std::void_t<decltype(&E::block)>> : std::true_type {};
+// A two-product epilogue with kDualHook takes the gate/up accumulators of a finished wave tile
+// itself (the backward of the gated SwiGLU) instead of the forward's SiLU(gate) * up staging.
+template <class E, class = void>
+struct DualHook : std::false_type {};
+template <class E>
+struct DualHook<E, std::void_t<decltype(E::kDualHook)>> : std::true_type {};
+
+template <class C, class Epi>
+__device__ __forceinline__ void swiglu_bwd_tile(const Epi& epi, f32x16 (&acc)[C::TM][C::TN], unsigned char* smem, int m0,
+                                int nt, int wave, int wm, int wn, int M, int lane);
 
 // NS_: LDS stages of the k-loop; the loads of tile k + NS - 1 are in flight while tile k is
 // consumed (2 for the big products, more where streaming weights from HBM needs more bytes in
@@ -388,7 +445,9 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  if constexpr (C::DUAL) {
+  if constexpr (DualHook<Epi>::value) {
+    swiglu_bwd_tile<C>(epi, acc, smem, m0, nt, wave, wm, wn, M, lane);
+  } else if constexpr (C::DUAL) {
     // the wave's finished tile, SiLU(gate) * up in bf16, staged at once
     bf16_t* stg = reinterpret_cast<bf16_t*>(smem) + wave * (C::WTM * C::SPAD);
 #pragma unroll
@@ -446,6 +505,91 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
           if (m < M) epi.emit8(pre[a][q], m, nt * C::OUT_N + wn * C::ON + c8, stg + i * C::OPAD + c8);
         }
       }
+    }
+  }
+}
+
+// Backward SwiGLU epilogue of one wave tile (EpiSwiGLUBwd on the MFMA path).  Lane (lane & 31)
+// holds column b 32 + (lane & 31) of gate tile b and of up tile b + TN/2, at rows
+// a 32 + 8 (r >> 2) + 4 (lane >> 5) + (r & 3) for accumulator element r.  The wave's own LDS
+// region (the stages are free once the k-loop has ended) holds in turn the rows' gates, the
+// per-lane shares of <e, act> (one lane then sums each row), and the bf16 staging of dG, then
+// dU, which leave as 16-byte row pieces.  A wave's LDS operations complete in order, so the
+// region needs no barrier between these uses.
+template <class C, class Epi>
+__device__ __forceinline__ void swiglu_bwd_tile(const Epi& epi, f32x16 (&acc)[C::TM][C::TN], unsigned char* smem, int m0,
+                                int nt, int wave, int wm, int wn, int M, int lane) {
+  static_assert(C::DUAL, "gate/up tiles");
+  constexpr int TM = C::TM, TH = C::TN / 2, WTM = C::WTM;
+  constexpr int PP = 33;   // row pitch of the per-lane shares (floats): rows hit distinct banks
+  constexpr int RP = (WTM + WTM * PP) * 4, RS = WTM * C::SPAD * 2;
+  constexpr int REG = ((RP > RS ? RP : RS) + 15) / 16 * 16;
+  static_assert(C::NW * REG <= C::NS * C::STAGE, "backward staging fits in the stages");
+  unsigned char* reg = smem + wave * REG;
+  float* gl = reinterpret_cast<float*>(reg);
+  float* pr = gl + WTM;
+  const int rw = m0 + wm * WTM;                   // first row of the wave tile
+  const int col0 = nt * C::OUT_N + wn * C::ON;    // first output column of the wave
+  for (int i = lane; i < WTM; i += kWave) {
+    const int m = min(rw + i, M - 1);
+    const int t = epi.idx ? epi.idx[m] : m;
+    gl[i] = epi.gate ? epi.gate[t] : 1.0f;
+  }
+#pragma unroll
+  for (int a = 0; a < TM; ++a) {
+    // e at this lane's elements of the 32-row block, the loads in flight together
+    float ev[16][TH];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = min(rw + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3), M - 1);
+#pragma unroll
+      for (int b = 0; b < TH; ++b)
+        ev[r][b] = bf16_to_f32(epi.e[static_cast<size_t>(m) * epi.ld_e + col0 + b * 32 + (lane & 31)]);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      const float gt = gl[i];
+      float sum = 0.f;
+#pragma unroll
+      for (int b = 0; b < TH; ++b) {
+        const float g = acc[a][b][r], u = acc[a][b + TH][r];
+        const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+        const float ee = ev[r][b];
+        const float dact = gt * ee;
+        sum += ee * (g * sg * u);
+        acc[a][b][r] = dact * u * sg * (1.0f + g * (1.0f - sg));   // dG
+        acc[a][b + TH][r] = dact * g * sg;                          // dU
+      }
+      pr[i * PP + (lane & 31)] = sum;
+    }
+  }
+  for (int i = lane; i < WTM; i += kWave) {
+    float v = 0.f;
+#pragma unroll 8
+    for (int c = 0; c < 32; ++c) v += pr[i * PP + c];
+    if (rw + i < M) epi.dgpart[static_cast<size_t>(rw + i) * epi.n_parts + col0 / C::ON] = v;
+  }
+  bf16_t* stg = reinterpret_cast<bf16_t*>(reg);
+  constexpr int CPR = C::ON / 8, PPL = WTM * CPR / kWave;
+  static_assert(WTM * CPR % kWave == 0, "pieces split evenly over the lanes");
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+#pragma unroll
+        for (int b = 0; b < TH; ++b) stg[i * C::SPAD + b * 32 + (lane & 31)] = f32_to_bf16(acc[a][b + h * TH][r]);
+      }
+#pragma unroll
+    for (int q = 0; q < PPL; ++q) {
+      const int e = lane + kWave * q;
+      const int i = e / CPR, c8 = (e % CPR) * 8;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(stg + i * C::SPAD + c8);
+      if (rw + i < M)
+        *reinterpret_cast<u32x4*>(epi.dgu + static_cast<size_t>(rw + i) * epi.ld_dgu + h * epi.d_ff + col0 + c8) = v;
     }
   }
 }
@@ -1372,6 +1516,94 @@ hipError_t launch_adapter_up(int dtype, const float* part, const int* idx_ad, co
   EpiScatter<float, true> epi{idx_ad, static_cast<const float*>(hbar), gate,
                               static_cast<float*>(h_out), d};
   return run_f32<false>(A, B, epi, counts, n_max, d, d_r, s);
+}
+
+// ---------------------------------------------------------------------------
+// Backward of the routed block (frozen FFN, trained adapter) on the same cores.  The frozen
+// weights enter through transposed copies, so every product keeps K contiguous:
+//   e    = dL/dh[idx] W_d         B = W_d^T [d_ff][d]          (FFN rows)
+//   G, U recomputed from u[idx]   B = W_g, W_u                 epilogue: EpiSwiGLUBwd
+//   du   = [dG dU] [W_g; W_u]     B = [W_g; W_u]^T [d][2 d_ff]
+// and the adapter's: z = u[idx] W_1^T, e_a = dL/dh[idx] W_2 (B = W_2^T), du = dz W_1 (B = W_1^T).
+// ---------------------------------------------------------------------------
+namespace {
+using TileBwdGU = Tile<192, 256, 2, 4, true>;
+}
+
+int swiglu_bwd_parts(int dtype, int d_ff) { return dtype == 1 ? d_ff / TileBwdGU::ON : d_ff; }
+
+hipError_t launch_ffn_bwd_e(int dtype, const void* dh, const int* idx_ffn, const int* counts, int n_max,
+                            const void* w_down_t, void* e, int d, int d_ff, hipStream_t s) {
+  if (n_max <= 0) return hipSuccess;
+  if (dtype == 1) {
+    ARows<bf16_t> A{static_cast<const bf16_t*>(dh), idx_ffn, d};
+    BRows<bf16_t> B{static_cast<const bf16_t*>(w_down_t), nullptr, INT_MAX, d};
+    EpiStore<bf16_t> epi{static_cast<bf16_t*>(e), d_ff};
+    return d_ff % 256 == 0 ? run_big<256, false>(A, B, epi, counts, n_max, d_ff, d, s)
+                           : run_big<128, false>(A, B, epi, counts, n_max, d_ff, d, s);
+  }
+  ARows<float> A{static_cast<const float*>(dh), idx_ffn, d};
+  BRows<float> B{static_cast<const float*>(w_down_t), nullptr, INT_MAX, d};
+  return run_f32<false>(A, B, EpiStore<float>{static_cast<float*>(e), d_ff}, counts, n_max, d_ff, d, s);
+}
+
+hipError_t launch_ffn_bwd_gateup(int dtype, const void* u, const int* idx_ffn, const int* counts, int n_max,
+                                 const void* w_gate, const void* w_up, const void* e, const float* gate,
+                                 void* dgu, float* dgpart, int d, int d_ff, hipStream_t s) {
+  if (n_max <= 0) return hipSuccess;
+  if (dtype == 1) {
+    ARows<bf16_t> A{static_cast<const bf16_t*>(u), idx_ffn, d};
+    BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), INT_MAX, d};
+    EpiSwiGLUBwd<bf16_t> epi{static_cast<const bf16_t*>(e), d_ff, idx_ffn, gate, static_cast<bf16_t*>(dgu),
+                             2 * d_ff, d_ff, dgpart, swiglu_bwd_parts(1, d_ff)};
+    return run_tile<TileBwdGU>(A, B, epi, counts, n_max, d_ff, d, s);
+  }
+  ARows<float> A{static_cast<const float*>(u), idx_ffn, d};
+  BRows<float> B{static_cast<const float*>(w_gate), static_cast<const float*>(w_up), INT_MAX, d};
+  EpiSwiGLUBwd<float> epi{static_cast<const float*>(e), d_ff, idx_ffn, gate, static_cast<float*>(dgu),
+                          2 * d_ff, d_ff, dgpart, d_ff};
+  return run_f32<true>(A, B, epi, counts, n_max, d_ff, d, s);
+}
+
+hipError_t launch_ffn_bwd_du(int dtype, const void* dgu, const int* counts, int n_max, const void* w_gate_up_t,
+                             float* du, int d, int d_ff, hipStream_t s) {
+  if (n_max <= 0) return hipSuccess;
+  const int K = 2 * d_ff;
+  if (dtype == 1) {
+    ARows<bf16_t> A{static_cast<const bf16_t*>(dgu), nullptr, K};
+    BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate_up_t), nullptr, INT_MAX, K};
+    return run_big<256, false>(A, B, EpiStoreF32{du, d, 0}, counts, n_max, d, K, s);
+  }
+  ARows<float> A{static_cast<const float*>(dgu), nullptr, K};
+  BRows<float> B{static_cast<const float*>(w_gate_up_t), nullptr, INT_MAX, K};
+  return run_f32<false>(A, B, EpiStoreF32{du, d, 0}, counts, n_max, d, K, s);
+}
+
+int adapter_proj_splits(int dtype, int d, int d_r) {
+  if (dtype != 1) return 1;
+  return adapter_wide(d_r) ? WIDE_SPLIT : adapter_groups(d);
+}
+
+hipError_t launch_adapter_proj(int dtype, const void* rows, const int* idx_ad, const int* counts, int n_max,
+                               const void* w, float* part, int d, int d_r, hipStream_t s) {
+  if (n_max <= 0) return hipSuccess;
+  if (dtype == 1) return launch_adapter_down(1, rows, idx_ad, counts, n_max, w, part, d, d_r, s);
+  ARows<float> A{static_cast<const float*>(rows), idx_ad, d};
+  BRows<float> B{static_cast<const float*>(w), nullptr, INT_MAX, d};
+  return run_f32<false>(A, B, EpiStoreF32{part, d_r, 0}, counts, n_max, d_r, d, s);
+}
+
+hipError_t launch_adapter_du(int dtype, const void* dz, const int* counts, int n_max, const void* w1t, float* du,
+                             int d, int k, hipStream_t s) {
+  if (n_max <= 0) return hipSuccess;
+  if (dtype == 1) {
+    ARows<bf16_t> A{static_cast<const bf16_t*>(dz), nullptr, k};
+    BRows<bf16_t> B{static_cast<const bf16_t*>(w1t), nullptr, INT_MAX, k};
+    return run_tile<TileWide>(A, B, EpiStoreF32{du, d, 0}, counts, n_max, d, k, s);
+  }
+  ARows<float> A{static_cast<const float*>(dz), nullptr, k};
+  BRows<float> B{static_cast<const float*>(w1t), nullptr, INT_MAX, k};
+  return run_f32<false>(A, B, EpiStoreF32{du, d, 0}, counts, n_max, d, k, s);
 }
 
 }  // namespace hero

@@ -305,3 +305,63 @@ class DeviceDecoder:
         if self.stats:
             out["layers"] = [s.host() for s in self.stats]
         return out
+
+
+class DeviceBackward:
+    """The backward of one routed block on the GPU: the layer's input hbar, its frozen FFN (with
+    the transposed copies the backward reads) and adapter, an upstream gradient, the gates and
+    the branch lists, and the gradient buffers the ABI call fills."""
+
+    def __init__(self, w: synth.Workload, hbar: synth.Tensor, ffn: Dict[str, synth.Tensor],
+                 adapter: Dict[str, synth.Tensor], dh: synth.Tensor, gate: np.ndarray, use_ffn: np.ndarray,
+                 dgate_in: Optional[np.ndarray] = None, device: str = "cuda:0", stream=None):
+        self.w = w
+        self.T = T = hbar.shape[0]
+        self.dims = dims_struct(w)
+        self.hbar = upload(hbar, device)
+        self.dh = upload(dh, device)
+        self.ffn = {k: upload(v, device) for k, v in ffn.items()}
+        self.ffn_s = H.hero_ffn_weights(self.ffn["norm_w"].data_ptr(), self.ffn["w_gate"].data_ptr(),
+                                        self.ffn["w_up"].data_ptr(), self.ffn["w_down"].data_ptr())
+        self.adapter = {k: upload(v, device) for k, v in adapter.items()}
+        self.adapter_s = H.hero_adapter_weights(self.adapter["w1"].data_ptr(), self.adapter["w2"].data_ptr())
+        wdt = self.ffn["w_down"].dtype
+        self.w_down_t = torch.empty((w.d_ff, w.d), dtype=wdt, device=device)
+        self.w_gate_up_t = torch.empty((w.d, 2 * w.d_ff), dtype=wdt, device=device)
+        self.ffn_t = H.hero_ffn_backward_weights(self.w_down_t.data_ptr(), self.w_gate_up_t.data_ptr())
+        self.stream = stream
+        H.check(H.hero_ffn_backward_weights_make(self.dims, self.ffn_s, self.w_down_t, self.w_gate_up_t, stream),
+                "hero_ffn_backward_weights_make")
+        self.gate = torch.from_numpy(np.ascontiguousarray(gate, dtype=np.float32)).to(device)
+        use_ffn = np.asarray(use_ffn, dtype=bool)
+        # the branch lists as the forward's stats hold them: ascending token indices
+        idx_f = np.nonzero(use_ffn)[0].astype(np.int32)
+        idx_a = np.nonzero(~use_ffn)[0].astype(np.int32)
+        self.idx_ffn = torch.zeros(T, dtype=torch.int32, device=device)
+        self.idx_ad = torch.zeros(T, dtype=torch.int32, device=device)
+        self.idx_ffn[:len(idx_f)] = torch.from_numpy(idx_f).to(device)
+        self.idx_ad[:len(idx_a)] = torch.from_numpy(idx_a).to(device)
+        self.counts = torch.tensor([len(idx_f), len(idx_a), 0, 0], dtype=torch.int32, device=device)
+        self.dgate_in = None if dgate_in is None else \
+            torch.from_numpy(np.ascontiguousarray(dgate_in, dtype=np.float32)).to(device)
+        self.dhbar = torch.empty_like(self.hbar)
+        self.dgate = torch.empty(T, dtype=torch.float32, device=device)
+        self.dlogit = torch.empty(T, dtype=torch.float32, device=device)
+        self.dw1 = torch.empty((w.d_r, w.d), dtype=torch.float32, device=device)
+        self.dw2 = torch.empty((w.d, w.d_r), dtype=torch.float32, device=device)
+        self.grads_s = H.hero_block_grads(self.dhbar.data_ptr(), self.dgate.data_ptr(), self.dlogit.data_ptr(),
+                                          self.dw1.data_ptr(), self.dw2.data_ptr())
+        self.ws_bytes = H.hero_backward_workspace_size(self.dims, T)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+
+    def run(self) -> None:
+        H.check(H.hero_routed_block_backward(self.dims, self.T, self.hbar, self.dh, self.gate, self.idx_ffn,
+                                             self.idx_ad, self.counts, self.dgate_in, self.ffn_s, self.ffn_t,
+                                             self.adapter_s, self.grads_s, self.ws, self.ws_bytes, self.stream),
+                "hero_routed_block_backward")
+
+    def results(self) -> Dict[str, np.ndarray]:
+        torch.cuda.synchronize()
+        return dict(dhbar=download_f64(self.dhbar), dgate=self.dgate.cpu().numpy().astype(np.float64),
+                    dlogit=self.dlogit.cpu().numpy().astype(np.float64),
+                    dw1=self.dw1.cpu().numpy().astype(np.float64), dw2=self.dw2.cpu().numpy().astype(np.float64))

@@ -14,7 +14,7 @@ from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhero.so")
-ABI_VERSION = 4          # the struct layouts below follow include/hero.h of this version
+ABI_VERSION = 5          # the struct layouts below follow include/hero.h of this version
 
 HERO_OK = 0
 HERO_E_NULL = 1
@@ -39,7 +39,9 @@ HERO_ABL_NO_HISTORY = 8
 
 KERNELS = ("rowstats", "router_gemm", "router_pre", "router_mem", "router_post", "select",
            "ffn_gate_up", "ffn_down", "adapter_down", "adapter_up",
-           "attn_norm", "attn_qkv", "attn_core", "attn_out")
+           "attn_norm", "attn_qkv", "attn_core", "attn_out",
+           "bwd_norm", "bwd_ffn_e", "bwd_ffn_gate_up", "bwd_ffn_du", "bwd_adapter", "bwd_adapter_wgrad",
+           "bwd_rows", "skip_penalty")
 HERO_K = {name: i for i, name in enumerate(KERNELS)}
 
 _vp = ctypes.c_void_p
@@ -89,6 +91,14 @@ class hero_attn_dims(ctypes.Structure):
 
 class hero_attn_weights(ctypes.Structure):
     _fields_ = [("norm_w", _vp), ("w_qkv", _vp), ("w_o", _vp)]
+
+
+class hero_ffn_backward_weights(ctypes.Structure):
+    _fields_ = [("w_down_t", _vp), ("w_gate_up_t", _vp)]
+
+
+class hero_block_grads(ctypes.Structure):
+    _fields_ = [("dhbar", _vp), ("dgate", _vp), ("dlogit", _vp), ("dw1", _vp), ("dw2", _vp)]
 
 
 class hero_layer_stats(ctypes.Structure):
@@ -153,6 +163,18 @@ def lib() -> ctypes.CDLL:
                                          P(hero_router_weights), P(hero_adapter_weights), P(ctypes.c_float),
                                          P(ctypes.c_float), P(hero_routing), P(hero_layer_stats), _vp,
                                          ctypes.c_size_t, _vp]
+        L.hero_ffn_backward_weights_make.restype = ctypes.c_int
+        L.hero_ffn_backward_weights_make.argtypes = [P(hero_dims), P(hero_ffn_weights), _vp, _vp, _vp]
+        L.hero_backward_workspace_size.restype = ctypes.c_int
+        L.hero_backward_workspace_size.argtypes = [P(hero_dims), ctypes.c_int, P(ctypes.c_size_t)]
+        L.hero_routed_block_backward.restype = ctypes.c_int
+        L.hero_routed_block_backward.argtypes = [P(hero_dims), ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                                 P(hero_ffn_weights), P(hero_ffn_backward_weights),
+                                                 P(hero_adapter_weights), P(hero_block_grads), _vp,
+                                                 ctypes.c_size_t, _vp]
+        L.hero_skip_penalty.restype = ctypes.c_int
+        L.hero_skip_penalty.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, ctypes.c_float, _vp, _vp,
+                                        _vp]
         _lib = L
     return _lib
 
@@ -302,3 +324,33 @@ def hero_decoder_stack(dims: hero_dims, adims: hero_attn_dims, n_layers: int, ba
                                     _byref(state), at_arr, ffn_arr, _byref(router), ad_arr, _floats(eta),
                                     _floats(inv_freq), _byref(routing), st_arr, ptr(workspace),
                                     int(workspace_bytes), stream)
+
+
+def hero_ffn_backward_weights_make(dims: hero_dims, ffn: hero_ffn_weights, w_down_t, w_gate_up_t,
+                                   stream=None) -> int:
+    """Fill the transposed copies W_d^T [d_ff][d] and [W_g; W_u]^T [d][2 d_ff] of a frozen FFN."""
+    return lib().hero_ffn_backward_weights_make(ctypes.byref(dims), _byref(ffn), ptr(w_down_t), ptr(w_gate_up_t),
+                                                stream)
+
+
+def hero_backward_workspace_size(dims: hero_dims, T: int) -> int:
+    out = ctypes.c_size_t(0)
+    check(lib().hero_backward_workspace_size(ctypes.byref(dims), T, ctypes.byref(out)),
+          "hero_backward_workspace_size")
+    return out.value
+
+
+def hero_routed_block_backward(dims: hero_dims, T: int, hbar, dh_out, gate, idx_ffn, idx_ad, counts, dgate_in,
+                               ffn: hero_ffn_weights, ffn_t: hero_ffn_backward_weights,
+                               adapter: hero_adapter_weights, grads: hero_block_grads, workspace,
+                               workspace_bytes: int, stream=None) -> int:
+    """Gradients of one routed block given dL/dh_out (the forward's gate and branch lists)."""
+    return lib().hero_routed_block_backward(ctypes.byref(dims), T, ptr(hbar), ptr(dh_out), ptr(gate), ptr(idx_ffn),
+                                            ptr(idx_ad), ptr(counts), ptr(dgate_in), _byref(ffn), _byref(ffn_t),
+                                            _byref(adapter), _byref(grads), ptr(workspace), int(workspace_bytes),
+                                            stream)
+
+
+def hero_skip_penalty(L_R: int, batch: int, seq: int, gates, alpha: float, loss, dgates, stream=None) -> int:
+    """alpha L_skip (Eq. 18) into loss[0] and its gradient over gates [L_R][batch seq]."""
+    return lib().hero_skip_penalty(L_R, batch, seq, ptr(gates), float(alpha), ptr(loss), ptr(dgates), stream)

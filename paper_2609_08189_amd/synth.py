@@ -28,7 +28,10 @@ are used):
     N(2, 1), so that skip decisions cluster by position;
   * a full-decoder workload adds per block an attention-input RMSNorm gain
     ~ 1 + N(0, 0.02), a fused [W_q; W_k; W_v] and W_o ~ N(0, 0.02), and the
-    standard rotary frequency table theta^(-2i/hd) of the model.
+    standard rotary frequency table theta^(-2i/hd) of the model;
+  * the backward of a routed block takes an upstream gradient dL/dh ~ N(0, 1), gates
+    g ~ U(0.02, 0.98) and a branch per token drawn apart from g (adapter with probability
+    equal to the workload's budget), so that both branches meet gates on either side of 1/2.
 Every draw comes from numpy's PCG64 keyed by (seed, tensor id, layer), drawn in
 float32 and rounded once, round-to-nearest-even, to the storage dtype.
 """
@@ -180,6 +183,7 @@ _TID = {
     "state_a": 50, "state_b": 51, "p_hist": 52, "m_hist": 53,
     "bias_runs": 60, "bias_vals": 61,
     "attn_norm": 70, "w_qkv": 71, "w_o": 72,
+    "dh_out": 80, "bwd_gate": 81, "bwd_branch": 82,
 }
 
 
@@ -374,6 +378,16 @@ def logit_bias(w: Workload, seed: int = 0, T: Optional[int] = None) -> Optional[
     run_of = np.arange(T) // run
     beta = np.where(neg[run_of], vals - np.float32(2.0), vals + np.float32(2.0)).astype(np.float32)
     return beta
+
+
+def backward_inputs(w: Workload, seed: int = 0, T: Optional[int] = None):
+    """Inputs of one routed block's backward besides the layer's own: dL/dh [T, d] in the storage
+    dtype, the gates [T] (float32) and the branch taken [T] (True = FFN)."""
+    T = w.T if T is None else T
+    dh = _t(normal32(seed, "dh_out", (T, w.d)), w.dtype)
+    gate = _rng(seed, "bwd_gate").uniform(0.02, 0.98, size=T).astype(np.float32)
+    use_ffn = _rng(seed, "bwd_branch").uniform(0.0, 1.0, size=T) >= w.budget
+    return dh, gate, use_ffn
 
 
 # ---------------------------------------------------------------------------

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_function():
     lib = H.lib()
     for n in names:
         assert hasattr(lib, n), f"{n} declared in include/hero.h but not exported"
-    assert H.hero_abi_version() == H.ABI_VERSION == 4
+    assert H.hero_abi_version() == H.ABI_VERSION == 5
 
 
 def test_status_strings():
@@ -286,3 +286,59 @@ def test_decoder_entry_points_validate():
     assert dec(h_out=h) == H.HERO_E_ALIAS
     assert dec(eta=(3.9, float("nan"))) == H.HERO_E_RANGE
     assert dec() == H.HERO_E_DEVICE
+
+
+def test_backward_entry_points_validate():
+    """The training-side calls check every argument before the device check."""
+    dims = good_dims()
+    T = 300
+    need = H.hero_backward_workspace_size(dims, T)
+    assert need > H.hero_backward_workspace_size(dims, T - 100) > 0
+    ffn, ad, rt, st = fake_structs()
+    hb, dh, gate = FAKE + (1 << 30), FAKE + (2 << 30), FAKE + (3 << 30)
+    fi, ai, cnt = FAKE + (3 << 30) + 4096, FAKE + (3 << 30) + 8192, FAKE + (3 << 30) + 12288
+    ft = H.hero_ffn_backward_weights(FAKE + (5 << 30), FAKE + (6 << 30))
+    g = H.hero_block_grads(FAKE + (4 << 30), FAKE + (7 << 30), FAKE + (7 << 30) + 4096,
+                           FAKE + (7 << 30) + 8192, FAKE + (7 << 30) + (1 << 20))
+    ws = FAKE + (8 << 30)
+
+    def bwd(d=dims, T=T, hbar=hb, dh_out=dh, gate=gate, lists=(fi, ai, cnt), dgate_in=None, ffn_t=ft,
+            grads=g, ws=ws, n=need, adapter=ad[0]):
+        return H.hero_routed_block_backward(d, T, hbar, dh_out, gate, *lists, dgate_in, ffn[0], ffn_t, adapter,
+                                            grads, ws, n)
+
+    assert bwd(T=0) == H.HERO_E_DIM
+    assert bwd(d=good_dims(dtype=9)) == H.HERO_E_DTYPE
+    assert bwd(hbar=None) == H.HERO_E_NULL
+    assert bwd(lists=(fi, None, cnt)) == H.HERO_E_NULL
+    assert bwd(ffn_t=H.hero_ffn_backward_weights(FAKE, None)) == H.HERO_E_NULL
+    assert bwd(grads=H.hero_block_grads(FAKE + (4 << 30), None, FAKE, FAKE, FAKE)) == H.HERO_E_NULL
+    assert bwd(adapter=H.hero_adapter_weights(FAKE, FAKE + 2)) == H.HERO_E_ALIGN
+    assert bwd(dgate_in=FAKE + 6) == H.HERO_E_ALIGN
+    assert bwd(grads=H.hero_block_grads(hb + 1024, FAKE, FAKE, FAKE, FAKE)) == H.HERO_E_ALIAS   # dhbar in hbar
+    assert bwd(grads=H.hero_block_grads(dh, FAKE, FAKE, FAKE, FAKE)) == H.HERO_E_ALIAS
+    assert bwd(ws=None) == H.HERO_E_WORKSPACE
+    assert bwd(n=need - 1) == H.HERO_E_WORKSPACE
+    assert bwd(ws=hb) == H.HERO_E_ALIAS
+    # operand rows the GEMM core addresses with 32-bit offsets: [dG dU] of 2^17 tokens is too big
+    assert bwd(d=good_dims(d_ff=8192), T=1 << 17, n=1 << 40) == H.HERO_E_UNSUPPORTED
+    assert bwd() == H.HERO_E_DEVICE
+    assert bwd(dgate_in=FAKE + (9 << 30)) == H.HERO_E_DEVICE
+
+    wd, wgu = FAKE + (5 << 30), FAKE + (6 << 30)
+    make = lambda f=ffn[0], a=wd, b=wgu, d=dims: H.hero_ffn_backward_weights_make(d, f, a, b)
+    assert make(a=None) == H.HERO_E_NULL
+    assert make(b=wgu + 8) == H.HERO_E_ALIGN
+    assert make(a=ffn[0].w_down) == H.HERO_E_ALIAS
+    assert make(b=wd) == H.HERO_E_ALIAS
+    assert make(f=H.hero_ffn_weights(FAKE, FAKE, None, FAKE)) == H.HERO_E_NULL
+    assert make() == H.HERO_E_DEVICE
+
+    gates, loss, dg = FAKE + (1 << 30), FAKE + (2 << 30), FAKE + (3 << 30)
+    assert H.hero_skip_penalty(0, 2, 5, gates, 1.0, loss, dg) == H.HERO_E_DIM
+    assert H.hero_skip_penalty(4, 2, 0, gates, 1.0, loss, dg) == H.HERO_E_DIM
+    assert H.hero_skip_penalty(4, 2, 5, None, 1.0, loss, dg) == H.HERO_E_NULL
+    assert H.hero_skip_penalty(4, 2, 5, gates, float("nan"), loss, dg) == H.HERO_E_RANGE
+    assert H.hero_skip_penalty(4, 2, 5, gates, 1.0, loss, gates + 16) == H.HERO_E_ALIAS
+    assert H.hero_skip_penalty(4, 2, 5, gates, 1.0, loss + 4, dg) == H.HERO_E_ALIGN
+    assert H.hero_skip_penalty(4, 2, 5, gates, 1.0, loss, dg) == H.HERO_E_DEVICE

@@ -1,0 +1,210 @@
+"""GPU parity of the training side against the oracle, through the C ABI: the backward of a
+routed block through the gate scaling (Sec. 3.1, eq:ffn_route and the remark after it) and
+the gate-utilisation penalty (Sec. 3.3, Eq. 18).
+
+Comparison rules: dL/dhbar per token row (max error over the row relative to the row's largest
+reference value); the weight gradients as one matrix each (relative to the largest entry);
+dL/dg of token t relative to |dL/dh_t| |y_t| / sqrt(d), y_t the branch output, which is the
+size of the inner product <dL/dh_t, y_t> of two unrelated vectors of those norms (the inner
+product itself can cancel to near zero, where its own size is no yardstick), and dL/dlogit
+relative to that scale times g (1 - g).  Tolerances are the dtype's (bf16 2e-2, fp32 1e-4)."""
+import numpy as np
+import pytest
+
+from oracle import hero_oracle as O
+from paper_2609_08189_amd import synth
+from tests.oracle_inputs import adapter_of, dims_of, ffn_of
+from tests.parity import TOL, row_rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _scaled_err(x, ref, scale):
+    if len(ref) == 0:
+        return 0.0
+    return float(np.max(np.abs(x - ref) / np.maximum(scale, 1e-30)))
+
+
+def _dg_scale(w, hb, dh, gate, use_ffn, F, A):
+    """|dL/dh_t| |y_t| / sqrt(d) per token, y_t = FFN(u_t) or Adapter(u_t) (the oracle's forward)."""
+    y = O.routed_block(hb, np.where(use_ffn, 1.0, 0.0), use_ffn, F, A, dims_of(w)) - hb
+    return np.linalg.norm(dh, axis=1) * np.linalg.norm(y, axis=1) / np.sqrt(w.d)
+
+
+def _mat_err(x, ref):
+    return float(np.max(np.abs(x - ref)) / max(np.max(np.abs(ref)), 1e-30))
+
+
+def _setup(w, seed, dgate_in=False):
+    import torch
+    from paper_2609_08189_amd.device import DeviceBackward
+    T = w.T
+    print(f"case {w.name} dtype={w.dtype} T={T} d={w.d} d_ff={w.d_ff} d_r={w.d_r} budget={w.budget} "
+          f"seed={seed} dgate_in={dgate_in}", flush=True)
+    hbar = synth.hidden(w, seed, T)
+    ffn = synth.ffn_layer(w, 0, seed)
+    ad = synth.adapter_layer(w, 0, seed)
+    dh, gate, use_ffn = synth.backward_inputs(w, seed, T)
+    gin = np.random.default_rng(seed + 100).standard_normal(T).astype(np.float32) * 10 if dgate_in else None
+    db = DeviceBackward(w, hbar, ffn, ad, dh, gate, use_ffn, gin)
+    return db, hbar, ffn, ad, dh, gate, use_ffn, gin
+
+
+def _check(w, res, ref, use_ffn, hbar, dh, gate, F, A, rows=None, report=None):
+    tol = TOL[w.dtype]
+    rows = np.arange(len(use_ffn)) if rows is None else rows
+    f = use_ffn[rows]
+    g = gate[rows].astype(np.float64)
+    sc = _dg_scale(w, hbar.f64[rows], dh.f64[rows], g, f, F, A)
+    errs = dict(dhbar=row_rel_err(res["dhbar"][rows], ref.dhbar))
+    for k, s_ in (("dgate", sc), ("dlogit", sc * g * (1 - g))):
+        x, r = res[k][rows], getattr(ref, k)
+        errs[k + "_ffn"] = _scaled_err(x[f], r[f], s_[f])
+        errs[k + "_ad"] = _scaled_err(x[~f], r[~f], s_[~f])
+    if report is not None:
+        report.update(errs)
+    print("  errors:", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for k, v in errs.items():
+        assert v <= tol, f"{k}: {v:.3e} > {tol:.0e}"
+
+
+def _check_wgrad(w, res, dw1, dw2, n_ad):
+    tol = TOL[w.dtype]
+    if n_ad == 0:
+        assert not res["dw1"].any() and not res["dw2"].any(), "no adapter token: zero weight gradients"
+        return
+    e1, e2 = _mat_err(res["dw1"], dw1), _mat_err(res["dw2"], dw2)
+    print(f"  dw1 {e1:.2e} dw2 {e2:.2e}", flush=True)
+    assert e1 <= tol and e2 <= tol
+
+
+def _run_small(w, seed, dgate_in=False):
+    import torch
+    db, hbar, ffn, ad, dh, gate, use_ffn, gin = _setup(w, seed, dgate_in)
+    db.run()
+    res = db.results()
+    F, A = ffn_of(ffn), adapter_of(ad)
+    ref = O.routed_block_backward(hbar.f64, gate.astype(np.float64), use_ffn, F, A, dims_of(w), dh.f64,
+                                  None if gin is None else gin.astype(np.float64))
+    _check(w, res, ref, use_ffn, hbar, dh, gate, F, A)
+    _check_wgrad(w, res, ref.dw1, ref.dw2, int((~use_ffn).sum()))
+    del db
+    torch.cuda.empty_cache()
+    return res
+
+
+BF16 = synth.Workload("bwd_bf16", "bf16", d=512, d_ff=1408, d_r=64, L_R=8, d_m=64, T=333,
+                      mode="budget", budget=0.27)
+F32 = synth.Workload("bwd_f32", "f32", d=256, d_ff=688, d_r=16, L_R=4, d_m=32, T=130,
+                     mode="budget", budget=0.27)
+
+
+@pytest.mark.parametrize("w,seed,gin", [
+    (BF16, 1, False),                                        # d_ff % 256 != 0: 128-wide e tiles
+    (BF16.replace(d_ff=1536, T=1000), 2, True),              # several row tiles, extra dL/dg
+    (BF16.replace(d_r=32, T=97), 3, False),                  # rank padded to 64 for du
+    (BF16.replace(d_r=96, d=768, d_ff=2048, T=450), 4, True),
+    (BF16.replace(d_r=256, d_ff=1024, T=200), 5, False),     # wide adapter path
+    (F32, 6, False),
+    (F32.replace(T=61, d_r=24), 7, True),
+])
+def test_block_backward_matches_oracle(w, seed, gin):
+    _run_small(w, seed, gin)
+
+
+@pytest.mark.parametrize("budget", [0.0, 1.0])
+def test_block_backward_single_branch(budget):
+    """Every token on one branch: the other branch's kernels see an empty list (and the
+    weight gradients are exactly zero without adapter tokens)."""
+    _run_small(BF16.replace(budget=budget, T=130), 8)
+
+
+@pytest.mark.parametrize("T", [1, 2])
+def test_block_backward_tiny_batches(T):
+    _run_small(BF16.replace(T=T, budget=0.5), 9 + T)
+    _run_small(F32.replace(T=T, budget=0.5), 9 + T)
+
+
+def test_block_backward_is_deterministic():
+    """Fixed-order reductions: two calls give the same bits."""
+    import torch
+    db, *_ = _setup(BF16.replace(T=700), 12)
+    db.run()
+    a = db.results()
+    db.run()
+    b = db.results()
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+    del db
+    torch.cuda.empty_cache()
+
+
+def test_block_backward_llama31_8b_shape():
+    """The Llama-3.1-8B layer shape (T = 4096, d = 4096, d_ff = 14336, r = 64, 26.87 % of the
+    tokens on the adapter), in the launch configuration the benchmark times: the adapter rows
+    and the weight gradients in full, the FFN rows on a sample the oracle computes row by row."""
+    import torch
+    w = synth.WORKLOADS["llama31_8b_layer"]
+    db, hbar, ffn, ad, dh, gate, use_ffn, _ = _setup(w, 0)
+    db.run()
+    res = db.results()
+    dims, F, A = dims_of(w), ffn_of(ffn), adapter_of(ad)
+    ad_rows = np.nonzero(~use_ffn)[0]
+    ref_a = O.routed_block_backward(hbar.f64[ad_rows], gate[ad_rows].astype(np.float64), use_ffn[ad_rows], F, A,
+                                    dims, dh.f64[ad_rows])
+    _check(w, res, ref_a, use_ffn, hbar, dh, gate, F, A, rows=ad_rows)
+    _check_wgrad(w, res, ref_a.dw1, ref_a.dw2, len(ad_rows))
+    ffn_rows = np.nonzero(use_ffn)[0]
+    rng = np.random.default_rng(5)
+    sample = np.sort(np.concatenate([ffn_rows[:2], ffn_rows[-2:], rng.choice(ffn_rows, 20, replace=False)]))
+    ref_f = O.routed_block_backward(hbar.f64[sample], gate[sample].astype(np.float64), use_ffn[sample], F, A,
+                                    dims, dh.f64[sample])
+    _check(w, res, ref_f, use_ffn, hbar, dh, gate, F, A, rows=sample)
+    del db
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("L_R,batch,seq", [(4, 3, 7), (32, 16, 2048), (5, 4, 1)])
+def test_skip_penalty_matches_oracle(L_R, batch, seq):
+    import torch
+    from paper_2609_08189_amd import hero as H
+    print(f"case skip penalty L_R={L_R} batch={batch} seq={seq}", flush=True)
+    g = np.random.default_rng(L_R + seq).uniform(0.02, 0.98, (L_R, batch * seq)).astype(np.float32)
+    gates = torch.from_numpy(g).cuda()
+    loss = torch.empty(4, dtype=torch.float32, device="cuda")
+    dg = torch.empty_like(gates)
+    H.check(H.hero_skip_penalty(L_R, batch, seq, gates, 0.3, loss, dg), "hero_skip_penalty")
+    torch.cuda.synchronize()
+    val, grad = O.skip_penalty(g.astype(np.float64), batch, seq, alpha=0.3)
+    got = float(loss.cpu()[0])
+    assert abs(got - val) <= 1e-5 * max(abs(val), 1e-30), (got, val)
+    assert _mat_err(dg.cpu().numpy().astype(np.float64), grad) <= 1e-5 if seq > 1 else not dg.cpu().numpy().any()
+
+
+def test_skip_penalty_gradient_feeds_the_block_backward():
+    """The penalty's gradient row of a block, passed as dgate_in, is added to dL/dg."""
+    import torch
+    from paper_2609_08189_amd import hero as H
+    from paper_2609_08189_amd.device import DeviceBackward
+    w = BF16.replace(T=256)
+    batch, seq, L_R = 2, 128, 3
+    seed = 21
+    hbar = synth.hidden(w, seed)
+    ffn, ad = synth.ffn_layer(w, 0, seed), synth.adapter_layer(w, 0, seed)
+    dh, gate, use_ffn = synth.backward_inputs(w, seed)
+    g_all = np.random.default_rng(3).uniform(0.02, 0.98, (L_R, w.T)).astype(np.float32)
+    g_all[1] = gate
+    gates = torch.from_numpy(g_all).cuda()
+    loss = torch.empty(4, dtype=torch.float32, device="cuda")
+    dgs = torch.empty_like(gates)
+    H.check(H.hero_skip_penalty(L_R, batch, seq, gates, 0.05, loss, dgs), "hero_skip_penalty")
+    db = DeviceBackward(w, hbar, ffn, ad, dh, gate, use_ffn)
+    db.dgate_in = dgs[1]
+    db.run()
+    res = db.results()
+    _, grad = O.skip_penalty(g_all.astype(np.float64), batch, seq, alpha=0.05)
+    F, A = ffn_of(ffn), adapter_of(ad)
+    ref = O.routed_block_backward(hbar.f64, gate.astype(np.float64), use_ffn, F, A, dims_of(w), dh.f64, grad[1])
+    _check(w, res, ref, use_ffn, hbar, dh, gate, F, A)
+    del db
+    torch.cuda.empty_cache()
