@@ -365,6 +365,144 @@ def bench_decoder(args, w):
     print(json.dumps(result), flush=True)
 
 
+BWD_KERNELS = ("bwd_norm", "bwd_ffn_e", "bwd_ffn_gate_up", "bwd_ffn_du", "bwd_adapter", "bwd_adapter_wgrad",
+               "bwd_rows")
+
+
+def backward_work(w, n_f, n_a):
+    """Algorithmic FLOPs / HBM bytes of each kernel group of one routed-block backward call
+    (storage dtype es; fp32 intermediates where the kernels keep them)."""
+    T, d, dff, r = w.T, w.d, w.d_ff, w.d_r
+    es = 2 if w.dtype == "bf16" else 4
+    n_parts = dff // 32 if w.dtype == "bf16" else dff
+    return {
+        "bwd_norm": dict(flops=0, bytes=es * 2 * T * d),
+        "bwd_ffn_e": dict(flops=2 * n_f * d * dff, bytes=es * (d * dff + n_f * d + n_f * dff)),
+        "bwd_ffn_gate_up": dict(flops=4 * n_f * d * dff,
+                                bytes=es * (2 * d * dff + n_f * d + n_f * dff + 2 * n_f * dff) + 4 * n_f * n_parts),
+        "bwd_ffn_du": dict(flops=4 * n_f * d * dff, bytes=es * (2 * d * dff + 2 * n_f * dff) + 4 * n_f * d),
+        "bwd_adapter": dict(flops=6 * n_a * d * r, bytes=es * (2 * n_a * d + 6 * d * r) + 4 * n_a * d),
+        "bwd_adapter_wgrad": dict(flops=4 * n_a * d * r, bytes=es * 2 * n_a * d + 4 * 2 * d * r),
+        "bwd_rows": dict(flops=0, bytes=es * (3 * T * d + d) + 4 * T * d),
+    }
+
+
+def cpu_baseline_backward(w, hbar, ffn, ad, dh, gate, use_ffn, target_s=12.0):
+    """The oracle's block backward on a token sample of the same inputs (rows in their order)."""
+    import numpy as np
+    from oracle import hero_oracle as O
+    from tests.oracle_inputs import adapter_of, dims_of, ffn_of
+    dims, F, A = dims_of(w), ffn_of(ffn), adapter_of(ad)
+    hb, dhf = hbar.f64, dh.f64
+    g64 = gate.astype(np.float64)
+
+    def run(n):
+        t0 = time.perf_counter()
+        O.routed_block_backward(hb[:n], g64[:n], use_ffn[:n], F, A, dims, dhf[:n])
+        return time.perf_counter() - t0
+
+    # grow the sample until it takes a quarter of the target; then repeat it up to the target
+    n, t = 8, run(8)
+    while t < target_s / 4 and n < w.T:
+        n = min(w.T, 4 * n)
+        t = run(n)
+    reps, total = 1, t
+    while total < target_s and reps < 8:
+        total += run(n)
+        reps += 1
+    return {"value": round(reps * n / total, 2), "unit": "tokens/s",
+            "cores": int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1)), "kind": "oracle",
+            "sample": f"first {n} of {w.T} tokens ({int(use_ffn[:n].sum())} FFN, {int((~use_ffn[:n]).sum())} "
+                      f"adapter), {reps} run(s), float64 numpy, {total:.1f} s; nproc {os.cpu_count()}"}
+
+
+def bench_backward(args, w):
+    """A step is one hero_routed_block_backward call over the workload's T tokens (frozen FFN with
+    its transposed copies made once beforehand, adapter, upstream gradient, gates and branch lists
+    resident in HBM)."""
+    import numpy as np
+    import torch
+    from paper_2609_08189_amd import hero as H
+    from paper_2609_08189_amd import synth
+    from paper_2609_08189_amd.device import DeviceBackward
+
+    if w.layer_j <= 0 or w.n_layers > 0:
+        sys.exit("--backward times one routed block: use a single-layer workload")
+    print(f"# preparing the backward of {describe(w, w.layer_j)}", file=sys.stderr, flush=True)
+    hbar = synth.hidden(w, args.seed)
+    ffn = synth.ffn_layer(w, w.layer_j - 1, args.seed)
+    ad = synth.adapter_layer(w, w.layer_j - 1, args.seed)
+    dh, gate, use_ffn = synth.backward_inputs(w, args.seed)
+    n_f, n_a = int(use_ffn.sum()), int((~use_ffn).sum())
+    db = DeviceBackward(w, hbar, ffn, ad, dh, gate, use_ffn)
+    stream = db.stream
+    ev = HipEvents()
+    db.run()
+    for _ in range(args.warmup):
+        db.run()
+    torch.cuda.synchronize()
+    K = args.steps
+    works = backward_work(w, n_f, n_a)
+    # instrumented pass: every kernel group's time per step
+    per, handles = {}, {}
+    for name in BWD_KERNELS:
+        handles[name] = (ev.create(K), ev.create(K))
+        H.hero_kernel_timer(H.HERO_K[name], *handles[name])
+    for _ in range(K):
+        db.run()
+    torch.cuda.synchronize()
+    for name, (a, b) in handles.items():
+        H.hero_kernel_timer(H.HERO_K[name], [], [])
+        us = 1000.0 * sum(ev.elapsed_ms(x, y) for x, y in zip(a, b)) / K
+        wk = works[name]
+        per[name] = {"us": round(us, 2), "tflops": round(wk["flops"] / us * 1e-6, 1) if wk["flops"] else None,
+                     "gbs": round(wk["bytes"] / us * 1e-3, 1)}
+        ev.destroy(a + b)
+    dom = max((k for k in per if works[k]["flops"]), key=lambda k: per[k]["us"])
+    ks, ke = ev.create(K), ev.create(K)
+    H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
+    t_start, t_stop = ev.create(2)
+    marks = ev.create(K - 1)
+    torch.cuda.synchronize()
+    ev.record(t_start, stream)
+    for i in range(K):
+        db.run()
+        if i < K - 1:
+            ev.record(marks[i], stream)
+    ev.record(t_stop, stream)
+    torch.cuda.synchronize()
+    H.hero_kernel_timer(H.HERO_K[dom], [], [])
+    ms_step = ev.elapsed_ms(t_start, t_stop) / K
+    bounds = [t_start] + marks + [t_stop]
+    step_ms = sorted(ev.elapsed_ms(a, b) for a, b in zip(bounds[:-1], bounds[1:]))
+    dom_ms = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
+    peak_f = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    achieved = works[dom]["flops"] / (dom_ms * 1e-3) * 1e-12
+    result = {
+        "metric": "routed-block backward tokens/sec at Llama-3.1-8B shape; % MFMA roofline",
+        "value": round(w.T / (ms_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": (f"backward of one routed block (eq:ffn_route through the gate scaling) at "
+                                f"{describe(w, w.layer_j)}; upstream gradient N(0,1), gates U(0.02,0.98), "
+                                f"branch drawn with the budget"),
+                   "global_batch": w.batch, "seq_len": w.seq, "tokens": w.T, "parallelism": "none",
+                   "n_ffn": n_f, "n_adapter": n_a},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak_f, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak_f, 4), "traffic": None, "kernel": dom,
+                     "avg_launch_us": round(1000 * dom_ms, 2),
+                     "work_per_launch": f"{works[dom]['flops'] // (n_f or 1) // (w.d * w.d_ff)}*d*d_ff FLOP per "
+                                        f"FFN token x {n_f} FFN tokens = {works[dom]['flops'] / 1e9:.1f} GFLOP"},
+        "step_ms": step_stats(step_ms),
+        "whole_call": ideal_fraction([works], ms_step, w.dtype, False),
+        "kernels": per,
+    }
+    if not args.no_cpu_baseline:
+        print("# timing the CPU oracle on a token sample", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline_backward(w, hbar, ffn, ad, dh, gate, use_ffn, args.cpu_target_s)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -378,6 +516,8 @@ def main():
                     help="storage of the router memory S between layers")
     ap.add_argument("--budget", type=float, default=None,
                     help="skip budget in place of the workload's own (budget-mode workloads)")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the backward of the routed block (training side) instead of the forward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-target-s", type=float, default=12.0)
     ap.add_argument("--memory", choices=("matrix", "history"), default="matrix",
@@ -417,6 +557,8 @@ def main():
         if args.memory != "matrix":
             sys.exit("--state bf16 needs the matrix-form memory")
         w = w.replace(state_dtype="bf16")
+    if args.backward:
+        return bench_backward(args, w)
     if w.n_layers > 0:
         return bench_decoder(args, w)
     stack = w.layer_j <= 0          # a stack workload: a step is one hero_routed_stack call
@@ -473,7 +615,7 @@ def main():
     works = [kernel_work(w, nf, na, w.T, jj, args.memory) for nf, na, jj in zip(nfs, nas, layers)]
     per = {}
     handles = {}
-    names = [k for k in H.KERNELS if not k.startswith("attn") and not (k == "router_mem" and w.ablation & 12)]
+    names = [k for k in H.KERNELS[:H.HERO_K["adapter_up"] + 1] if not (k == "router_mem" and w.ablation & 12)]
     if w.ablation & 12:            # no memory pass under the memory-less ablations
         for wk in works:
             wk["router_mem"] = dict(flops=0, bytes=0)

@@ -816,11 +816,9 @@ int hero_decoder_stack(const hero_dims* dims, const hero_attn_dims* adims, int n
 // ---------------------------------------------------------------------------
 namespace {
 
-// adapter tokens per partial of the weight gradients: at most 16 partials, whole LDS batches
-int wgrad_chunk(int T) {
-  const int c = (T + 15) / 16;
-  return std::max(64, (c + 63) / 64 * 64);
-}
+// partials of the adapter weight gradients: the adapter rows split up to 8 ways, in chunks of at
+// least 32 rows
+int wgrad_slices(int T) { return std::max(1, std::min(8, T / 32)); }
 
 // the adapter rank as the K of the du product: whole 64-deep k-tiles on the MFMA path
 int rank_pad(const hero_dims& d) { return d.dtype == HERO_BF16 ? (d.d_r + 63) / 64 * 64 : d.d_r; }
@@ -828,16 +826,16 @@ int rank_pad(const hero_dims& d) { return d.dtype == HERO_BF16 ? (d.d_r + 63) / 
 struct BwdLayout {
   size_t idx_f, idx_a, counts, rowstat, u, e, dgu, dgpart, du_f, du_a, part_z, part_e, dz32, a32, dzk, dg_ad,
       w1t, w2t, pw1, pw2, total;
-  int n_parts, chunk, rpad;
+  int n_parts, n_slices, rpad;
 };
 
 BwdLayout bwd_layout_of(const hero_dims& d, int T) {
   const size_t es = esize(d.dtype), t = static_cast<size_t>(T);
   BwdLayout L{};
   L.n_parts = hero::swiglu_bwd_parts(d.dtype, d.d_ff);
-  L.chunk = wgrad_chunk(T);
+  L.n_slices = wgrad_slices(T);
   L.rpad = rank_pad(d);
-  const size_t n_chunks = (t + L.chunk - 1) / L.chunk;
+  const size_t n_chunks = L.n_slices;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -985,7 +983,7 @@ int hero_routed_block_backward(const hero_dims* dims, int T, const void* hbar, c
   a.a32 = reinterpret_cast<float*>(ws + L.a32);
   a.dzk = ws + L.dzk;
   a.u = ws + L.u;
-  a.chunk = L.chunk;
+  a.n_slices = L.n_slices;
   a.pw1 = reinterpret_cast<float*>(ws + L.pw1);
   a.pw2 = reinterpret_cast<float*>(ws + L.pw2);
   a.dhbar = grads->dhbar;

@@ -183,9 +183,9 @@ struct BlockBwdArgs {
   float* a32;                // [T][d_r]
   void* dzk;                 // [T][rpad] storage dtype (the du product's A operand)
   const void* u;             // [T][d]
-  int chunk;                 // adapter tokens per weight-gradient partial
-  float* pw1;                // [n_chunks][d_r][d]
-  float* pw2;                // [n_chunks][d][d_r]
+  int n_slices;              // weight-gradient partials: the adapter rows split this many ways
+  float* pw1;                // [n_slices][d_r][d]
+  float* pw2;                // [n_slices][d][d_r]
   // outputs
   void* dhbar;               // [T][d]
   float* dgate;              // [T]

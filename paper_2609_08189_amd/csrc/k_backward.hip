@@ -73,71 +73,119 @@ __global__ __launch_bounds__(256) void adapter_bwd_mid_kernel(BlockBwdArgs a) {
   if (lane == 0) a.dg_ad[m] = -acc;
 }
 
-// Weight-gradient partials of one chunk of adapter rows: thread = one column i of d, RB ranks.
-//   pw1[c][r][i] = sum_m dz[m][r] u[t_m][i],  pw2[c][i][r] = sum_m a[m][r] (1 - g_t) dh[t_m][i]
-constexpr int WG_RB = 32, WG_TB = 64;
+// Weight-gradient partials of one chunk of adapter rows,
+//   pw1[c][r][i] = sum_m dz[m][r] u[t_m][i],  pw2[c][i][r] = sum_m a[m][r] (1 - g_t) dh[t_m][i].
+// A workgroup covers 128 columns i and 64 ranks r; a thread owns an 8-rank x 4-column block of
+// both (rank group tid % 8, column group tid / 8), so each staged
+// value read from LDS feeds 4 or 8 FMAs.  Rows are staged WG_TB at a time (u and
+// (1 - g) dh as fp32, dz, a), zero past the chunk's end.  The rows split into gridDim.z chunks
+// of equal size (whole batches) from the device count.
+constexpr int WG_TB = 32, WG_C = 128, WG_R = 64;
+
+__device__ __forceinline__ int wgrad_chunk(int n, int slices) {
+  return ((n + slices - 1) / slices + WG_TB - 1) / WG_TB * WG_TB;
+}
 
 template <typename T>
 __global__ __launch_bounds__(256) void adapter_wgrad_kernel(BlockBwdArgs a) {
-  __shared__ float sdz[WG_TB][WG_RB];
-  __shared__ float sa[WG_TB][WG_RB];
-  __shared__ int st[WG_TB];
-  __shared__ float sg[WG_TB];
+  __shared__ __attribute__((aligned(16))) float su[WG_TB][WG_C];
+  __shared__ __attribute__((aligned(16))) float sdy[WG_TB][WG_C];
+  __shared__ __attribute__((aligned(16))) float sdz[WG_TB][WG_R];
+  __shared__ __attribute__((aligned(16))) float sa[WG_TB][WG_R];
   const int n = a.counts[1];
-  const int mb = blockIdx.z * a.chunk;
+  const int chunk = wgrad_chunk(n, gridDim.z);
+  const int mb = blockIdx.z * chunk;
   if (mb >= n) return;
-  const int me = min(n, mb + a.chunk);
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  const int r0 = blockIdx.y * WG_RB;
-  const bool col_ok = i < a.d;
+  const int me = min(n, mb + chunk);
+  const int tid = threadIdx.x;
+  const int rg = tid & 7, cg = tid >> 3;            // 8 ranks, 4 columns
+  const int c0 = blockIdx.x * WG_C, r0 = blockIdx.y * WG_R;
   const T* U = static_cast<const T*>(a.u);
   const T* DH = static_cast<const T*>(a.dh);
-  float g1[WG_RB], g2[WG_RB];
+  float g1[8][4], g2[4][8];
 #pragma unroll
-  for (int rr = 0; rr < WG_RB; ++rr) g1[rr] = g2[rr] = 0.f;
+  for (int x = 0; x < 8; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) g1[x][y] = g2[y][x] = 0.f;
   for (int m0 = mb; m0 < me; m0 += WG_TB) {
     const int nb = min(WG_TB, me - m0);
     __syncthreads();
-    for (int e = threadIdx.x; e < WG_TB * WG_RB; e += 256) {
-      const int k = e / WG_RB, rr = e % WG_RB, r = r0 + rr;
+    // u and (1 - g) dh: WG_TB rows x 128 columns in 8-column pieces, two per thread
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int e = tid + 256 * q;
+      const int k = e >> 4, c8 = (e & 15) * 8;
+      float uv[8], dv[8];
+      if (k < nb && c0 + c8 < a.d) {
+        const int t = a.idx_ad[m0 + k];
+        const float om = 1.0f - a.gate[t];
+        const size_t row = static_cast<size_t>(t) * a.d + c0 + c8;
+        ld8(U + row, uv);
+        ld8(DH + row, dv);
+#pragma unroll
+        for (int x = 0; x < 8; ++x) dv[x] *= om;
+      } else {
+#pragma unroll
+        for (int x = 0; x < 8; ++x) uv[x] = dv[x] = 0.f;
+      }
+#pragma unroll
+      for (int x = 0; x < 8; ++x) {
+        su[k][c8 + x] = uv[x];
+        sdy[k][c8 + x] = dv[x];
+      }
+    }
+    for (int e = tid; e < WG_TB * WG_R; e += 256) {
+      const int k = e / WG_R, rr = e % WG_R, r = r0 + rr;
       const bool ok = k < nb && r < a.d_r;
       sdz[k][rr] = ok ? a.dz32[static_cast<size_t>(m0 + k) * a.d_r + r] : 0.f;
       sa[k][rr] = ok ? a.a32[static_cast<size_t>(m0 + k) * a.d_r + r] : 0.f;
     }
-    if (threadIdx.x < WG_TB) {
-      const int k = threadIdx.x;
-      const int t = k < nb ? a.idx_ad[m0 + k] : 0;
-      st[k] = t;
-      sg[k] = k < nb ? 1.0f - a.gate[t] : 0.f;
-    }
     __syncthreads();
-    if (!col_ok) continue;
 #pragma unroll 4
-    for (int k = 0; k < nb; ++k) {
-      const size_t row = static_cast<size_t>(st[k]) * a.d + i;
-      const float uu = ldf(U + row), dy = sg[k] * ldf(DH + row);
+    for (int k = 0; k < WG_TB; ++k) {
+      const f32x4 u4 = *reinterpret_cast<const f32x4*>(&su[k][cg * 4]);
+      const f32x4 y4 = *reinterpret_cast<const f32x4*>(&sdy[k][cg * 4]);
+      const f32x4 z0 = *reinterpret_cast<const f32x4*>(&sdz[k][rg * 8]);
+      const f32x4 z1 = *reinterpret_cast<const f32x4*>(&sdz[k][rg * 8 + 4]);
+      const f32x4 a0 = *reinterpret_cast<const f32x4*>(&sa[k][rg * 8]);
+      const f32x4 a1 = *reinterpret_cast<const f32x4*>(&sa[k][rg * 8 + 4]);
 #pragma unroll
-      for (int rr = 0; rr < WG_RB; ++rr) {
-        g1[rr] = fmaf(sdz[k][rr], uu, g1[rr]);
-        g2[rr] = fmaf(sa[k][rr], dy, g2[rr]);
+      for (int x = 0; x < 8; ++x) {
+        const float zv = x < 4 ? z0[x] : z1[x - 4];
+        const float av = x < 4 ? a0[x] : a1[x - 4];
+#pragma unroll
+        for (int y = 0; y < 4; ++y) {
+          g1[x][y] = fmaf(zv, u4[y], g1[x][y]);
+          g2[y][x] = fmaf(av, y4[y], g2[y][x]);
+        }
       }
     }
   }
-  if (!col_ok) return;
   const size_t c = blockIdx.z;
+  const int i = c0 + cg * 4;
+  if (i >= a.d) return;
 #pragma unroll
-  for (int rr = 0; rr < WG_RB; ++rr) {
-    const int r = r0 + rr;
-    if (r >= a.d_r) break;
-    a.pw1[(c * a.d_r + r) * a.d + i] = g1[rr];
-    a.pw2[(c * a.d + i) * a.d_r + r] = g2[rr];
+  for (int x = 0; x < 8; ++x) {
+    const int r = r0 + rg * 8 + x;
+    if (r < a.d_r) {
+      f32x4 v = {g1[x][0], g1[x][1], g1[x][2], g1[x][3]};
+      *reinterpret_cast<f32x4*>(a.pw1 + (c * a.d_r + r) * a.d + i) = v;
+    }
+  }
+#pragma unroll
+  for (int y = 0; y < 4; ++y) {
+    float* o = a.pw2 + (c * a.d + i + y) * a.d_r + r0 + rg * 8;
+#pragma unroll
+    for (int x = 0; x < 8; ++x)
+      if (r0 + rg * 8 + x < a.d_r) o[x] = g2[y][x];
   }
 }
 
 // dW = the sum of the chunks' partials, chunk 0 first (zero when no token took the adapter)
 __global__ __launch_bounds__(256) void adapter_wgrad_reduce(BlockBwdArgs a) {
   const int n = a.counts[1];
-  const int nc = (n + a.chunk - 1) / a.chunk;
+  const int chunk = wgrad_chunk(n, a.n_slices);
+  const int nc = n > 0 ? (n + chunk - 1) / chunk : 0;
   const size_t E = static_cast<size_t>(a.d_r) * a.d;
   for (size_t e = blockIdx.x * static_cast<size_t>(256) + threadIdx.x; e < E;
        e += static_cast<size_t>(gridDim.x) * 256) {
@@ -284,7 +332,7 @@ hipError_t launch_adapter_bwd_mid(const BlockBwdArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_adapter_wgrad(const BlockBwdArgs& a, hipStream_t s) {
-  const dim3 grid((a.d + 255) / 256, (a.d_r + WG_RB - 1) / WG_RB, (a.T + a.chunk - 1) / a.chunk);
+  const dim3 grid((a.d + WG_C - 1) / WG_C, (a.d_r + WG_R - 1) / WG_R, a.n_slices);
   if (a.dtype == 1)
     adapter_wgrad_kernel<bf16_t><<<grid, 256, 0, s>>>(a);
   else
