@@ -432,9 +432,11 @@ def bench_backward(args, w):
     hbar = synth.hidden(w, args.seed)
     ffn = synth.ffn_layer(w, w.layer_j - 1, args.seed)
     ad = synth.adapter_layer(w, w.layer_j - 1, args.seed)
-    dh, gate, use_ffn = synth.backward_inputs(w, args.seed)
+    # the budget rule's branch sizes (floor(budget T + 1/2) adapter tokens) at random positions
+    n_skip = int(math.floor(w.budget * w.T + 0.5)) if w.mode == "budget" else None
+    dh, gate, use_ffn = synth.backward_inputs(w, args.seed, n_adapter=n_skip)
     n_f, n_a = int(use_ffn.sum()), int((~use_ffn).sum())
-    db = DeviceBackward(w, hbar, ffn, ad, dh, gate, use_ffn)
+    db = DeviceBackward(w, hbar, ffn, ad, dh, gate, use_ffn, budget=w.budget if n_skip is not None else None)
     stream = db.stream
     ev = HipEvents()
     db.run()
@@ -485,7 +487,7 @@ def bench_backward(args, w):
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": (f"backward of one routed block (eq:ffn_route through the gate scaling) at "
                                 f"{describe(w, w.layer_j)}; upstream gradient N(0,1), gates U(0.02,0.98), "
-                                f"branch drawn with the budget"),
+                                f"the budget's adapter count at random positions"),
                    "global_batch": w.batch, "seq_len": w.seq, "tokens": w.T, "parallelism": "none",
                    "n_ffn": n_f, "n_adapter": n_a},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak_f, "unit": "TFLOP/s",

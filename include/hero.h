@@ -432,16 +432,19 @@ int hero_backward_workspace_size(const hero_dims *dims, int T, size_t *bytes);
  *   dL/dhbar = dL/dh + RMSNorm_w backward of du;  dL/dg += dgate_in (may be NULL: e.g. the
  *   penalty's gradient from hero_skip_penalty);  dL/dlogit = dL/dg g (1 - g).
  * gate, idx_ffn, idx_ad, counts are the forward's (hero_layer_stats of the same layer: every
- * token in exactly one list).  The lists are read through copies with counts clamped to
- * [0, T] and indices to [0, T - 1], so malformed lists give wrong values, never an access out
- * of bounds.  The FFN's gate/up products are recomputed from hbar (the forward's activations
+ * token in exactly one list), and routing is the forward's rule (NULL: taken as threshold mode):
+ * in budget mode the branch sizes are known on the host (T - n_skip FFN tokens, n_skip adapter
+ * tokens), which sizes the launches; counts are then clamped to those sizes.  The lists are read
+ * through copies with counts clamped to [0, T] and indices to [0, T - 1], so malformed lists
+ * give wrong values, never an access out of bounds.  The FFN's gate/up products are recomputed from hbar (the forward's activations
  * are not kept).  dhbar must not overlap hbar or dh_out.  All products are bf16 x bf16 with
  * fp32 accumulation for a bf16 model (e and [dG dU] pass through HBM in bf16), fp32 otherwise;
  * every reduction has a fixed order.
  */
 int hero_routed_block_backward(const hero_dims *dims, int T, const void *hbar, const void *dh_out,
                                const float *gate, const int32_t *idx_ffn, const int32_t *idx_ad,
-                               const int32_t *counts, const float *dgate_in, const hero_ffn_weights *ffn,
+                               const int32_t *counts, const hero_routing *routing, const float *dgate_in,
+                               const hero_ffn_weights *ffn,
                                const hero_ffn_backward_weights *ffn_t, const hero_adapter_weights *adapter,
                                const hero_block_grads *grads, void *workspace, size_t workspace_bytes,
                                void *stream);

@@ -922,10 +922,10 @@ int hero_backward_workspace_size(const hero_dims* dims, int T, size_t* bytes) {
 
 int hero_routed_block_backward(const hero_dims* dims, int T, const void* hbar, const void* dh_out,
                                const float* gate, const int32_t* idx_ffn, const int32_t* idx_ad,
-                               const int32_t* counts, const float* dgate_in, const hero_ffn_weights* ffn,
-                               const hero_ffn_backward_weights* ffn_t, const hero_adapter_weights* adapter,
-                               const hero_block_grads* grads, void* workspace, size_t workspace_bytes,
-                               void* stream) {
+                               const int32_t* counts, const hero_routing* routing, const float* dgate_in,
+                               const hero_ffn_weights* ffn, const hero_ffn_backward_weights* ffn_t,
+                               const hero_adapter_weights* adapter, const hero_block_grads* grads, void* workspace,
+                               size_t workspace_bytes, void* stream) {
   using namespace hero;
   int st = check_dims(dims);
   if (st != HERO_OK) return st;
@@ -937,6 +937,7 @@ int hero_routed_block_backward(const hero_dims* dims, int T, const void* hbar, c
     return HERO_E_NULL;
   if ((st = check_ffn(ffn)) != HERO_OK) return st;
   if ((st = check_adapter(adapter)) != HERO_OK) return st;
+  if (routing && (st = check_routing(routing)) != HERO_OK) return st;
   const void* al[] = {hbar, dh_out, gate, idx_ffn, idx_ad, counts, dgate_in, ffn_t->w_down_t, ffn_t->w_gate_up_t,
                       grads->dhbar, grads->dgate, grads->dlogit, grads->dw1, grads->dw2, workspace};
   for (const void* p : al)
@@ -997,36 +998,45 @@ int hero_routed_block_backward(const hero_dims* dims, int T, const void* hbar, c
   void* w1t = ws + L.w1t;
   void* w2t = ws + L.w2t;
 
+  // launch sizes: exact in budget mode, T otherwise (tiles past the device count exit)
+  const bool budget = routing && routing->mode == HERO_MODE_BUDGET;
+  const int n_skip = budget ? static_cast<int>(floor(routing->budget * static_cast<double>(T) + 0.5)) : 0;
+  const int nf_max = budget ? T - n_skip : T;
+  const int na_max = budget ? n_skip : T;
+  a.na_max = na_max;
   hipError_t err = timed(HERO_K_BWD_NORM, s, [&] {
-    hipError_t x = launch_bwd_lists(T, idx_ffn, idx_ad, counts, idx_f, idx_a, cnt, s);
+    hipError_t x = launch_bwd_lists(T, nf_max, na_max, idx_ffn, idx_ad, counts, idx_f, idx_a, cnt, s);
     if (x != hipSuccess) return x;
     return launch_rowstats(D.dtype, hbar, nullptr, nullptr, ffn->norm_w, T, D.d, 1, D.eps_norm,
                            const_cast<float*>(a.rowstat), u, s);
   });
   if (err != hipSuccess) return HERO_E_LAUNCH;
   err = timed(HERO_K_BWD_FFN_E, s, [&] {
-    return launch_ffn_bwd_e(D.dtype, dh_out, idx_f, cnt, T, ffn_t->w_down_t, e, D.d, D.d_ff, s);
+    return launch_ffn_bwd_e(D.dtype, dh_out, idx_f, cnt, nf_max, ffn_t->w_down_t, e, D.d, D.d_ff, s);
   });
   if (err != hipSuccess) return HERO_E_LAUNCH;
   err = timed(HERO_K_BWD_FFN_GATE_UP, s, [&] {
-    return launch_ffn_bwd_gateup(D.dtype, u, idx_f, cnt, T, ffn->w_gate, ffn->w_up, e, gate, dgu,
+    return launch_ffn_bwd_gateup(D.dtype, u, idx_f, cnt, nf_max, ffn->w_gate, ffn->w_up, e, gate, dgu,
                                  const_cast<float*>(a.dgpart), D.d, D.d_ff, s);
   });
   if (err != hipSuccess) return HERO_E_LAUNCH;
   err = timed(HERO_K_BWD_FFN_DU, s, [&] {
-    return launch_ffn_bwd_du(D.dtype, dgu, cnt, T, ffn_t->w_gate_up_t, const_cast<float*>(a.du_f), D.d, D.d_ff, s);
+    return launch_ffn_bwd_du(D.dtype, dgu, cnt, nf_max, ffn_t->w_gate_up_t, const_cast<float*>(a.du_f), D.d,
+                             D.d_ff, s);
   });
   if (err != hipSuccess) return HERO_E_LAUNCH;
   err = timed(HERO_K_BWD_ADAPTER, s, [&] {
     hipError_t x = launch_transpose(D.dtype, adapter->w2, D.d, D.d_r, D.d_r, w2t, D.d, D.d, s);
     if (x == hipSuccess) x = launch_transpose(D.dtype, adapter->w1, D.d_r, D.d, D.d, w1t, L.rpad, L.rpad, s);
     if (x == hipSuccess)
-      x = launch_adapter_proj(D.dtype, u, idx_a, cnt + 1, T, adapter->w1, const_cast<float*>(a.part_z), D.d, D.d_r, s);
+      x = launch_adapter_proj(D.dtype, u, idx_a, cnt + 1, na_max, adapter->w1, const_cast<float*>(a.part_z), D.d,
+                              D.d_r, s);
     if (x == hipSuccess)
-      x = launch_adapter_proj(D.dtype, dh_out, idx_a, cnt + 1, T, w2t, const_cast<float*>(a.part_e), D.d, D.d_r, s);
+      x = launch_adapter_proj(D.dtype, dh_out, idx_a, cnt + 1, na_max, w2t, const_cast<float*>(a.part_e), D.d,
+                              D.d_r, s);
     if (x == hipSuccess) x = launch_adapter_bwd_mid(a, s);
     if (x == hipSuccess)
-      x = launch_adapter_du(D.dtype, a.dzk, cnt + 1, T, w1t, const_cast<float*>(a.du_a), D.d, L.rpad, s);
+      x = launch_adapter_du(D.dtype, a.dzk, cnt + 1, na_max, w1t, const_cast<float*>(a.du_a), D.d, L.rpad, s);
     return x;
   });
   if (err != hipSuccess) return HERO_E_LAUNCH;

@@ -129,10 +129,10 @@ hipError_t launch_adapter_up(int dtype, const float* part, const int* idx_ad, co
 // ---------------------------------------------------------------------------
 // Backward of the routed block (training side; frozen FFN, trained adapter)
 // ---------------------------------------------------------------------------
-// copies of the branch lists with counts clamped to [0, T] (n_ffn + n_ad <= T) and indices to
-// [0, T - 1]: f, ad [T], c [2]
-hipError_t launch_bwd_lists(int T, const int* idx_ffn, const int* idx_ad, const int* counts, int* f, int* ad,
-                            int* c, hipStream_t s);
+// copies of the branch lists with counts clamped to [0, nf_max] and [0, na_max] (n_ffn + n_ad <= T)
+// and indices to [0, T - 1]: f, ad [T], c [2]
+hipError_t launch_bwd_lists(int T, int nf_max, int na_max, const int* idx_ffn, const int* idx_ad, const int* counts,
+                            int* f, int* ad, int* c, hipStream_t s);
 // out[c][r] = in[r][c] for r < R, c < C ([R][C] with row pitch ld_in into rows of pitch
 // ld_out); with R_pad > R the columns R .. R_pad - 1 of every output row are written as 0
 hipError_t launch_transpose(int dtype, const void* in, int R, int C, int ld_in, void* out, int ld_out,
@@ -176,7 +176,8 @@ struct BlockBwdArgs {
   int n_parts;
   float* dg_ad;              // [T]
   // adapter
-  const float* part_z;       // [splits][T][d_r]
+  int na_max;                // launch bound of the adapter rows (the partials' slice height)
+  const float* part_z;       // [splits][na_max][d_r]
   const float* part_e;
   int splits;
   float* dz32;               // [T][d_r]

@@ -47,7 +47,7 @@ __global__ __launch_bounds__(256) void adapter_bwd_mid_kernel(BlockBwdArgs a) {
   if (m >= a.counts[1]) return;
   const int t = a.idx_ad[m];
   const float om = 1.0f - a.gate[t];
-  const size_t slice = static_cast<size_t>(a.T) * a.d_r;
+  const size_t slice = static_cast<size_t>(a.na_max) * a.d_r;
   const size_t row = static_cast<size_t>(m) * a.d_r;
   T* dzk = static_cast<T*>(a.dzk) + static_cast<size_t>(m) * a.rpad;
   float acc = 0.f;
@@ -285,12 +285,13 @@ __global__ __launch_bounds__(1024) void skip_penalty_kernel(const float* __restr
 
 // The caller's branch lists, copied with every count and index clamped into range, so that a
 // malformed list gives wrong numbers but no access outside the buffers.
-__global__ __launch_bounds__(256) void bwd_lists_kernel(int T, const int* __restrict__ idx_ffn,
+__global__ __launch_bounds__(256) void bwd_lists_kernel(int T, int nf_max, int na_max,
+                                                        const int* __restrict__ idx_ffn,
                                                         const int* __restrict__ idx_ad,
                                                         const int* __restrict__ counts, int* __restrict__ f,
                                                         int* __restrict__ ad, int* __restrict__ c) {
-  const int nf = min(max(counts[0], 0), T);
-  const int na = min(max(counts[1], 0), T - nf);
+  const int nf = min(max(counts[0], 0), nf_max);
+  const int na = min(min(max(counts[1], 0), T - nf), na_max);
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i == 0) {
     c[0] = nf;
@@ -302,9 +303,9 @@ __global__ __launch_bounds__(256) void bwd_lists_kernel(int T, const int* __rest
 
 }  // namespace
 
-hipError_t launch_bwd_lists(int T, const int* idx_ffn, const int* idx_ad, const int* counts, int* f, int* ad,
-                            int* c, hipStream_t s) {
-  bwd_lists_kernel<<<(T + 255) / 256, 256, 0, s>>>(T, idx_ffn, idx_ad, counts, f, ad, c);
+hipError_t launch_bwd_lists(int T, int nf_max, int na_max, const int* idx_ffn, const int* idx_ad, const int* counts,
+                            int* f, int* ad, int* c, hipStream_t s) {
+  bwd_lists_kernel<<<(T + 255) / 256, 256, 0, s>>>(T, nf_max, na_max, idx_ffn, idx_ad, counts, f, ad, c);
   return hipGetLastError();
 }
 

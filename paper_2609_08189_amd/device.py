@@ -314,7 +314,8 @@ class DeviceBackward:
 
     def __init__(self, w: synth.Workload, hbar: synth.Tensor, ffn: Dict[str, synth.Tensor],
                  adapter: Dict[str, synth.Tensor], dh: synth.Tensor, gate: np.ndarray, use_ffn: np.ndarray,
-                 dgate_in: Optional[np.ndarray] = None, device: str = "cuda:0", stream=None):
+                 dgate_in: Optional[np.ndarray] = None, device: str = "cuda:0", stream=None,
+                 budget: Optional[float] = None):
         self.w = w
         self.T = T = hbar.shape[0]
         self.dims = dims_struct(w)
@@ -344,6 +345,8 @@ class DeviceBackward:
         self.counts = torch.tensor([len(idx_f), len(idx_a), 0, 0], dtype=torch.int32, device=device)
         self.dgate_in = None if dgate_in is None else \
             torch.from_numpy(np.ascontiguousarray(dgate_in, dtype=np.float32)).to(device)
+        # the forward's rule: in budget mode the branch sizes are known on the host
+        self.routing_s = None if budget is None else H.hero_routing(H.HERO_MODE_BUDGET, 0.5, budget, None)
         self.dhbar = torch.empty_like(self.hbar)
         self.dgate = torch.empty(T, dtype=torch.float32, device=device)
         self.dlogit = torch.empty(T, dtype=torch.float32, device=device)
@@ -356,7 +359,8 @@ class DeviceBackward:
 
     def run(self) -> None:
         H.check(H.hero_routed_block_backward(self.dims, self.T, self.hbar, self.dh, self.gate, self.idx_ffn,
-                                             self.idx_ad, self.counts, self.dgate_in, self.ffn_s, self.ffn_t,
+                                             self.idx_ad, self.counts, self.routing_s, self.dgate_in, self.ffn_s,
+                                             self.ffn_t,
                                              self.adapter_s, self.grads_s, self.ws, self.ws_bytes, self.stream),
                 "hero_routed_block_backward")
 

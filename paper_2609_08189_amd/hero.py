@@ -168,8 +168,8 @@ def lib() -> ctypes.CDLL:
         L.hero_backward_workspace_size.restype = ctypes.c_int
         L.hero_backward_workspace_size.argtypes = [P(hero_dims), ctypes.c_int, P(ctypes.c_size_t)]
         L.hero_routed_block_backward.restype = ctypes.c_int
-        L.hero_routed_block_backward.argtypes = [P(hero_dims), ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
-                                                 P(hero_ffn_weights), P(hero_ffn_backward_weights),
+        L.hero_routed_block_backward.argtypes = [P(hero_dims), ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp,
+                                                 P(hero_routing), _vp, P(hero_ffn_weights), P(hero_ffn_backward_weights),
                                                  P(hero_adapter_weights), P(hero_block_grads), _vp,
                                                  ctypes.c_size_t, _vp]
         L.hero_skip_penalty.restype = ctypes.c_int
@@ -340,13 +340,14 @@ def hero_backward_workspace_size(dims: hero_dims, T: int) -> int:
     return out.value
 
 
-def hero_routed_block_backward(dims: hero_dims, T: int, hbar, dh_out, gate, idx_ffn, idx_ad, counts, dgate_in,
-                               ffn: hero_ffn_weights, ffn_t: hero_ffn_backward_weights,
-                               adapter: hero_adapter_weights, grads: hero_block_grads, workspace,
-                               workspace_bytes: int, stream=None) -> int:
-    """Gradients of one routed block given dL/dh_out (the forward's gate and branch lists)."""
+def hero_routed_block_backward(dims: hero_dims, T: int, hbar, dh_out, gate, idx_ffn, idx_ad, counts,
+                               routing: Optional[hero_routing], dgate_in, ffn: hero_ffn_weights,
+                               ffn_t: hero_ffn_backward_weights, adapter: hero_adapter_weights,
+                               grads: hero_block_grads, workspace, workspace_bytes: int, stream=None) -> int:
+    """Gradients of one routed block given dL/dh_out (the forward's gate, branch lists and routing rule)."""
     return lib().hero_routed_block_backward(ctypes.byref(dims), T, ptr(hbar), ptr(dh_out), ptr(gate), ptr(idx_ffn),
-                                            ptr(idx_ad), ptr(counts), ptr(dgate_in), _byref(ffn), _byref(ffn_t),
+                                            ptr(idx_ad), ptr(counts), _byref(routing), ptr(dgate_in), _byref(ffn),
+                                            _byref(ffn_t),
                                             _byref(adapter), _byref(grads), ptr(workspace), int(workspace_bytes),
                                             stream)
 

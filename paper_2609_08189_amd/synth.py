@@ -380,13 +380,19 @@ def logit_bias(w: Workload, seed: int = 0, T: Optional[int] = None) -> Optional[
     return beta
 
 
-def backward_inputs(w: Workload, seed: int = 0, T: Optional[int] = None):
+def backward_inputs(w: Workload, seed: int = 0, T: Optional[int] = None, n_adapter: Optional[int] = None):
     """Inputs of one routed block's backward besides the layer's own: dL/dh [T, d] in the storage
-    dtype, the gates [T] (float32) and the branch taken [T] (True = FFN)."""
+    dtype, the gates [T] (float32) and the branch taken [T] (True = FFN).  The adapter tokens are
+    each token with probability w.budget, or exactly n_adapter tokens at random positions."""
     T = w.T if T is None else T
     dh = _t(normal32(seed, "dh_out", (T, w.d)), w.dtype)
     gate = _rng(seed, "bwd_gate").uniform(0.02, 0.98, size=T).astype(np.float32)
-    use_ffn = _rng(seed, "bwd_branch").uniform(0.0, 1.0, size=T) >= w.budget
+    draw = _rng(seed, "bwd_branch").uniform(0.0, 1.0, size=T)
+    if n_adapter is None:
+        use_ffn = draw >= w.budget
+    else:
+        use_ffn = np.ones(T, dtype=bool)
+        use_ffn[np.argsort(draw, kind="stable")[:n_adapter]] = False
     return dh, gate, use_ffn
 
 

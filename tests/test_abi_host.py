@@ -303,8 +303,8 @@ def test_backward_entry_points_validate():
     ws = FAKE + (8 << 30)
 
     def bwd(d=dims, T=T, hbar=hb, dh_out=dh, gate=gate, lists=(fi, ai, cnt), dgate_in=None, ffn_t=ft,
-            grads=g, ws=ws, n=need, adapter=ad[0]):
-        return H.hero_routed_block_backward(d, T, hbar, dh_out, gate, *lists, dgate_in, ffn[0], ffn_t, adapter,
+            grads=g, ws=ws, n=need, adapter=ad[0], routing=None):
+        return H.hero_routed_block_backward(d, T, hbar, dh_out, gate, *lists, routing, dgate_in, ffn[0], ffn_t, adapter,
                                             grads, ws, n)
 
     assert bwd(T=0) == H.HERO_E_DIM
@@ -322,8 +322,11 @@ def test_backward_entry_points_validate():
     assert bwd(ws=hb) == H.HERO_E_ALIAS
     # operand rows the GEMM core addresses with 32-bit offsets: [dG dU] of 2^17 tokens is too big
     assert bwd(d=good_dims(d_ff=8192), T=1 << 17, n=1 << 40) == H.HERO_E_UNSUPPORTED
+    assert bwd(routing=H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 1.5, None)) == H.HERO_E_RANGE
+    assert bwd(routing=H.hero_routing(7, 0.5, 0.5, None)) == H.HERO_E_RANGE
     assert bwd() == H.HERO_E_DEVICE
     assert bwd(dgate_in=FAKE + (9 << 30)) == H.HERO_E_DEVICE
+    assert bwd(routing=H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.27, None)) == H.HERO_E_DEVICE
 
     wd, wgu = FAKE + (5 << 30), FAKE + (6 << 30)
     make = lambda f=ffn[0], a=wd, b=wgu, d=dims: H.hero_ffn_backward_weights_make(d, f, a, b)

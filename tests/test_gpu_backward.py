@@ -35,18 +35,22 @@ def _mat_err(x, ref):
     return float(np.max(np.abs(x - ref)) / max(np.max(np.abs(ref)), 1e-30))
 
 
-def _setup(w, seed, dgate_in=False):
+def _setup(w, seed, dgate_in=False, budget_mode=False):
+    """budget_mode: exactly the budget rule's n_skip adapter tokens, and the call told the rule
+    (launches sized by the branch sizes); otherwise a per-token draw and no rule (launches sized
+    by T)."""
     import torch
     from paper_2609_08189_amd.device import DeviceBackward
     T = w.T
     print(f"case {w.name} dtype={w.dtype} T={T} d={w.d} d_ff={w.d_ff} d_r={w.d_r} budget={w.budget} "
-          f"seed={seed} dgate_in={dgate_in}", flush=True)
+          f"budget_mode={budget_mode} seed={seed} dgate_in={dgate_in}", flush=True)
     hbar = synth.hidden(w, seed, T)
     ffn = synth.ffn_layer(w, 0, seed)
     ad = synth.adapter_layer(w, 0, seed)
-    dh, gate, use_ffn = synth.backward_inputs(w, seed, T)
+    n_ad = O.n_skip_for(w.budget, T) if budget_mode else None
+    dh, gate, use_ffn = synth.backward_inputs(w, seed, T, n_adapter=n_ad)
     gin = np.random.default_rng(seed + 100).standard_normal(T).astype(np.float32) * 10 if dgate_in else None
-    db = DeviceBackward(w, hbar, ffn, ad, dh, gate, use_ffn, gin)
+    db = DeviceBackward(w, hbar, ffn, ad, dh, gate, use_ffn, gin, budget=w.budget if budget_mode else None)
     return db, hbar, ffn, ad, dh, gate, use_ffn, gin
 
 
@@ -78,9 +82,9 @@ def _check_wgrad(w, res, dw1, dw2, n_ad):
     assert e1 <= tol and e2 <= tol
 
 
-def _run_small(w, seed, dgate_in=False):
+def _run_small(w, seed, dgate_in=False, budget_mode=False):
     import torch
-    db, hbar, ffn, ad, dh, gate, use_ffn, gin = _setup(w, seed, dgate_in)
+    db, hbar, ffn, ad, dh, gate, use_ffn, gin = _setup(w, seed, dgate_in, budget_mode)
     db.run()
     res = db.results()
     F, A = ffn_of(ffn), adapter_of(ad)
@@ -99,24 +103,26 @@ F32 = synth.Workload("bwd_f32", "f32", d=256, d_ff=688, d_r=16, L_R=4, d_m=32, T
                      mode="budget", budget=0.27)
 
 
-@pytest.mark.parametrize("w,seed,gin", [
-    (BF16, 1, False),                                        # d_ff % 256 != 0: 128-wide e tiles
-    (BF16.replace(d_ff=1536, T=1000), 2, True),              # several row tiles, extra dL/dg
-    (BF16.replace(d_r=32, T=97), 3, False),                  # rank padded to 64 for du
-    (BF16.replace(d_r=96, d=768, d_ff=2048, T=450), 4, True),
-    (BF16.replace(d_r=256, d_ff=1024, T=200), 5, False),     # wide adapter path
-    (F32, 6, False),
-    (F32.replace(T=61, d_r=24), 7, True),
+@pytest.mark.parametrize("w,seed,gin,bm", [
+    (BF16, 1, False, False),                                 # d_ff % 256 != 0: 128-wide e tiles
+    (BF16, 1, False, True),
+    (BF16.replace(d_ff=1536, T=1000), 2, True, True),        # several row tiles, extra dL/dg
+    (BF16.replace(d_r=32, T=97), 3, False, False),           # rank padded to 64 for du
+    (BF16.replace(d_r=96, d=768, d_ff=2048, T=450), 4, True, True),
+    (BF16.replace(d_r=256, d_ff=1024, T=200), 5, False, True),   # wide adapter path
+    (F32, 6, False, False),
+    (F32.replace(T=61, d_r=24), 7, True, True),
 ])
-def test_block_backward_matches_oracle(w, seed, gin):
-    _run_small(w, seed, gin)
+def test_block_backward_matches_oracle(w, seed, gin, bm):
+    _run_small(w, seed, gin, bm)
 
 
-@pytest.mark.parametrize("budget", [0.0, 1.0])
-def test_block_backward_single_branch(budget):
-    """Every token on one branch: the other branch's kernels see an empty list (and the
-    weight gradients are exactly zero without adapter tokens)."""
-    _run_small(BF16.replace(budget=budget, T=130), 8)
+@pytest.mark.parametrize("budget,bm", [(0.0, False), (1.0, False), (0.0, True), (1.0, True)])
+def test_block_backward_single_branch(budget, bm):
+    """Every token on one branch: the other branch's kernels see an empty list, or with the
+    budget rule get no launch at all (and the weight gradients are exactly zero without adapter
+    tokens)."""
+    _run_small(BF16.replace(budget=budget, T=130), 8, budget_mode=bm)
 
 
 @pytest.mark.parametrize("T", [1, 2])
@@ -145,7 +151,7 @@ def test_block_backward_llama31_8b_shape():
     and the weight gradients in full, the FFN rows on a sample the oracle computes row by row."""
     import torch
     w = synth.WORKLOADS["llama31_8b_layer"]
-    db, hbar, ffn, ad, dh, gate, use_ffn, _ = _setup(w, 0)
+    db, hbar, ffn, ad, dh, gate, use_ffn, _ = _setup(w, 0, budget_mode=True)
     db.run()
     res = db.results()
     dims, F, A = dims_of(w), ffn_of(ffn), adapter_of(ad)
