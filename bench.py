@@ -229,6 +229,21 @@ def summarize_rocprof(root, window=None):
         print()
 
 
+_GRAPHS = []
+
+
+def graphed(step):
+    """The step captured once as a HIP graph (torch.cuda.graph around the library's launches, which
+    go to torch's current stream); replays launch the whole call at once."""
+    import torch
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    _GRAPHS.append(g)
+    return g.replay
+
+
 def step_stats(step_ms):
     """Median and 10th/90th percentiles of the per-step times inside the timed region."""
     n = len(step_ms)
@@ -323,16 +338,19 @@ def bench_decoder(args, w):
                      "gbs": round(wk["bytes"] / (ms * 1e-3) * 1e-9, 1) if wk else None}
         ev.destroy(a + b)
     dom = max((k for k in per if k in works and works[k]["flops"]), key=lambda k: per[k]["ms_per_step"])
-    # timed region, with the dominant kernel's launches bracketed on the call's stream
+    # timed region, with the dominant kernel's launches bracketed on the call's stream (graph mode:
+    # replays of the captured call; the kernel's time then comes from the instrumented pass)
+    run = graphed(dd.run) if args.graph else dd.run
     n_dom = K * launches[dom]
     ks, ke = ev.create(n_dom), ev.create(n_dom)
-    H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
+    if not args.graph:
+        H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
     t_start, t_stop = ev.create(2)
     torch.cuda.synchronize()
     marks = ev.create(K - 1)
     ev.record(t_start, stream)
     for i in range(K):
-        dd.run()
+        run()
         if i < K - 1:
             ev.record(marks[i], stream)
     ev.record(t_stop, stream)
@@ -341,7 +359,7 @@ def bench_decoder(args, w):
     ms_step = ev.elapsed_ms(t_start, t_stop) / K
     bounds = [t_start] + marks + [t_stop]
     step_ms = sorted(ev.elapsed_ms(a, b) for a, b in zip(bounds[:-1], bounds[1:]))
-    dom_ms = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
+    dom_ms = per[dom]["ms_per_step"] if args.graph else sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
     achieved = works[dom]["flops"] / (dom_ms * 1e-3) * 1e-12
     result = {
         "metric": "routed-FFN-stack tokens/sec at Llama-3.1-8B shape; % MFMA/HBM roofline",
@@ -353,7 +371,8 @@ def bench_decoder(args, w):
                                 f"the last {w.L_R} routed (adapter rank {w.d_r}, memory dim {w.d_m}, "
                                 f"skip budget {w.budget}), T={w.T} tokens ({w.batch}x{w.seq})"),
                    "global_batch": w.batch, "seq_len": w.seq, "tokens": w.T, "layers_per_step": w.n_layers,
-                   "parallelism": "none", "n_ffn_routed": sum(nfs), "n_adapter": sum(nas)},
+                   "parallelism": "none", "n_ffn_routed": sum(nfs), "n_adapter": sum(nas),
+                   "hip_graph": bool(args.graph)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
                      "kernel": dom, "avg_launch_us": round(1000 * dom_ms / launches[dom], 2),
@@ -437,7 +456,7 @@ def bench_backward(args, w):
     dh, gate, use_ffn = synth.backward_inputs(w, args.seed, n_adapter=n_skip)
     n_f, n_a = int(use_ffn.sum()), int((~use_ffn).sum())
     db = DeviceBackward(w, hbar, ffn, ad, dh, gate, use_ffn, budget=w.budget if n_skip is not None else None)
-    stream = db.stream
+    stream = db.stream()
     ev = HipEvents()
     db.run()
     for _ in range(args.warmup):
@@ -461,14 +480,16 @@ def bench_backward(args, w):
                      "gbs": round(wk["bytes"] / us * 1e-3, 1)}
         ev.destroy(a + b)
     dom = max((k for k in per if works[k]["flops"]), key=lambda k: per[k]["us"])
+    run = graphed(db.run) if args.graph else db.run
     ks, ke = ev.create(K), ev.create(K)
-    H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
+    if not args.graph:
+        H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
     t_start, t_stop = ev.create(2)
     marks = ev.create(K - 1)
     torch.cuda.synchronize()
     ev.record(t_start, stream)
     for i in range(K):
-        db.run()
+        run()
         if i < K - 1:
             ev.record(marks[i], stream)
     ev.record(t_stop, stream)
@@ -477,7 +498,7 @@ def bench_backward(args, w):
     ms_step = ev.elapsed_ms(t_start, t_stop) / K
     bounds = [t_start] + marks + [t_stop]
     step_ms = sorted(ev.elapsed_ms(a, b) for a, b in zip(bounds[:-1], bounds[1:]))
-    dom_ms = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
+    dom_ms = per[dom]["us"] / 1000 if args.graph else sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
     peak_f = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     achieved = works[dom]["flops"] / (dom_ms * 1e-3) * 1e-12
     result = {
@@ -489,7 +510,7 @@ def bench_backward(args, w):
                                 f"{describe(w, w.layer_j)}; upstream gradient N(0,1), gates U(0.02,0.98), "
                                 f"the budget's adapter count at random positions"),
                    "global_batch": w.batch, "seq_len": w.seq, "tokens": w.T, "parallelism": "none",
-                   "n_ffn": n_f, "n_adapter": n_a},
+                   "n_ffn": n_f, "n_adapter": n_a, "hip_graph": bool(args.graph)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak_f, "unit": "TFLOP/s",
                      "frac": round(achieved / peak_f, 4), "traffic": None, "kernel": dom,
                      "avg_launch_us": round(1000 * dom_ms, 2),
@@ -518,6 +539,9 @@ def main():
                     help="storage of the router memory S between layers")
     ap.add_argument("--budget", type=float, default=None,
                     help="skip budget in place of the workload's own (budget-mode workloads)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of the call captured once as a HIP graph (kernel times then come "
+                         "from the instrumented pass)")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward of the routed block (training side) instead of the forward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -591,14 +615,18 @@ def main():
     K = args.steps
     dom = "ffn_gate_up"
     n_dom = K * sum(1 for x in nfs if x > 0)   # launches of the dominant kernel in the timed steps
+    # graph mode: the timed steps replay the call captured once; the dominant kernel's time then
+    # comes from the instrumented pass below
+    run = graphed(step) if args.graph else step
     ks, ke = ev.create(n_dom), ev.create(n_dom)
-    H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
+    if not args.graph:
+        H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
     t_start, t_stop = ev.create(2)
     torch.cuda.synchronize()
     marks = ev.create(K - 1)            # step boundaries inside the timed region
     ev.record(t_start, stream)
     for i in range(K):
-        step()
+        run()
         if i < K - 1:
             ev.record(marks[i], stream)
     ev.record(t_stop, stream)
@@ -607,7 +635,7 @@ def main():
     total_ms = ev.elapsed_ms(t_start, t_stop)
     bounds = [t_start] + marks + [t_stop]
     step_ms = sorted(ev.elapsed_ms(a, b) for a, b in zip(bounds[:-1], bounds[1:]))
-    dom_ms_step = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K     # per step, all layers
+    dom_ms_step = 0.0 if args.graph else sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
     ms_step = total_ms / K
     print(f"# timed {K} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
 
@@ -642,6 +670,8 @@ def main():
                          "gbs": round(by / us * 1e-3, 1)}
         ev.destroy(a + b)
 
+    if args.graph:
+        dom_ms_step = per[dom]["us"] * sum(1 for x in nfs if x > 0) / 1000.0
     tokens_per_s = w.T / (ms_step * 1e-3)
     dflops = sum(wk[dom]["flops"] for wk in works)          # per step
     dbytes = sum(wk[dom]["bytes"] for wk in works)
@@ -682,7 +712,7 @@ def main():
                                ("" if args.memory == "matrix" else
                                                  ", router memory in depth-history form"),
                    "memory": args.memory, "state": args.state, "global_batch": w.batch, "seq_len": w.seq,
-                   "tokens": w.T, "layers_per_step": L, "parallelism": "none",
+                   "tokens": w.T, "layers_per_step": L, "parallelism": "none", "hip_graph": bool(args.graph),
                    "n_ffn": n_f if not stack else sum(nfs), "n_adapter": n_a if not stack else sum(nas)},
         "roofline": roof,
         "step_ms": step_stats(step_ms),

@@ -330,9 +330,10 @@ class DeviceBackward:
         self.w_down_t = torch.empty((w.d_ff, w.d), dtype=wdt, device=device)
         self.w_gate_up_t = torch.empty((w.d, 2 * w.d_ff), dtype=wdt, device=device)
         self.ffn_t = H.hero_ffn_backward_weights(self.w_down_t.data_ptr(), self.w_gate_up_t.data_ptr())
-        self.stream = stream
-        H.check(H.hero_ffn_backward_weights_make(self.dims, self.ffn_s, self.w_down_t, self.w_gate_up_t, stream),
-                "hero_ffn_backward_weights_make")
+        self.device = device
+        self._stream = stream
+        H.check(H.hero_ffn_backward_weights_make(self.dims, self.ffn_s, self.w_down_t, self.w_gate_up_t,
+                                                 self.stream()), "hero_ffn_backward_weights_make")
         self.gate = torch.from_numpy(np.ascontiguousarray(gate, dtype=np.float32)).to(device)
         use_ffn = np.asarray(use_ffn, dtype=bool)
         # the branch lists as the forward's stats hold them: ascending token indices
@@ -357,11 +358,17 @@ class DeviceBackward:
         self.ws_bytes = H.hero_backward_workspace_size(self.dims, T)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
 
+    def stream(self):
+        """The given stream, else torch's current one (so that graph capture sees the launches)."""
+        if self._stream is not None:
+            return self._stream
+        return torch.cuda.current_stream(torch.device(self.device)).cuda_stream
+
     def run(self) -> None:
         H.check(H.hero_routed_block_backward(self.dims, self.T, self.hbar, self.dh, self.gate, self.idx_ffn,
                                              self.idx_ad, self.counts, self.routing_s, self.dgate_in, self.ffn_s,
-                                             self.ffn_t,
-                                             self.adapter_s, self.grads_s, self.ws, self.ws_bytes, self.stream),
+                                             self.ffn_t, self.adapter_s, self.grads_s, self.ws, self.ws_bytes,
+                                             self.stream()),
                 "hero_routed_block_backward")
 
     def results(self) -> Dict[str, np.ndarray]:
