@@ -1026,14 +1026,10 @@ int hero_routed_block_backward(const hero_dims* dims, int T, const void* hbar, c
   });
   if (err != hipSuccess) return HERO_E_LAUNCH;
   err = timed(HERO_K_BWD_ADAPTER, s, [&] {
-    hipError_t x = launch_transpose(D.dtype, adapter->w2, D.d, D.d_r, D.d_r, w2t, D.d, D.d, s);
-    if (x == hipSuccess) x = launch_transpose(D.dtype, adapter->w1, D.d_r, D.d, D.d, w1t, L.rpad, L.rpad, s);
+    hipError_t x = launch_adapter_transpose(D.dtype, adapter->w1, adapter->w2, w1t, w2t, D.d, D.d_r, L.rpad, s);
     if (x == hipSuccess)
-      x = launch_adapter_proj(D.dtype, u, idx_a, cnt + 1, na_max, adapter->w1, const_cast<float*>(a.part_z), D.d,
-                              D.d_r, s);
-    if (x == hipSuccess)
-      x = launch_adapter_proj(D.dtype, dh_out, idx_a, cnt + 1, na_max, w2t, const_cast<float*>(a.part_e), D.d,
-                              D.d_r, s);
+      x = launch_adapter_proj2(D.dtype, u, adapter->w1, const_cast<float*>(a.part_z), dh_out, w2t,
+                               const_cast<float*>(a.part_e), idx_a, cnt + 1, na_max, D.d, D.d_r, s);
     if (x == hipSuccess) x = launch_adapter_bwd_mid(a, s);
     if (x == hipSuccess)
       x = launch_adapter_du(D.dtype, a.dzk, cnt + 1, na_max, w1t, const_cast<float*>(a.du_a), D.d, L.rpad, s);

@@ -137,6 +137,9 @@ hipError_t launch_bwd_lists(int T, int nf_max, int na_max, const int* idx_ffn, c
 // ld_out); with R_pad > R the columns R .. R_pad - 1 of every output row are written as 0
 hipError_t launch_transpose(int dtype, const void* in, int R, int C, int ld_in, void* out, int ld_out,
                             int R_pad, hipStream_t s);
+// W_2^T [d_r][d] and W_1^T [d][rpad] (columns d_r .. rpad - 1 zero) of an adapter, one launch
+hipError_t launch_adapter_transpose(int dtype, const void* w1, const void* w2, void* w1t, void* w2t, int d, int d_r,
+                                    int rpad, hipStream_t s);
 // e[m] = dL/dh[idx_ffn[m]] W_d (W_d^T given, [d_ff][d]), storage dtype, [n][d_ff]
 hipError_t launch_ffn_bwd_e(int dtype, const void* dh, const int* idx_ffn, const int* counts, int n_max,
                             const void* w_down_t, void* e, int d, int d_ff, hipStream_t s);
@@ -154,6 +157,10 @@ hipError_t launch_ffn_bwd_du(int dtype, const void* dgu, const int* counts, int 
 int adapter_proj_splits(int dtype, int d, int d_r);
 hipError_t launch_adapter_proj(int dtype, const void* rows, const int* idx_ad, const int* counts, int n_max,
                                const void* w, float* part, int d, int d_r, hipStream_t s);
+// two such products over the same rows (one launch where the ranks allow)
+hipError_t launch_adapter_proj2(int dtype, const void* rows0, const void* w0, float* part0, const void* rows1,
+                                const void* w1, float* part1, const int* idx_ad, const int* counts, int n_max, int d,
+                                int d_r, hipStream_t s);
 // du[m] = dz[m] W_1 (W_1^T given, [d][k]); dz [n][k] in the storage dtype, k = the rank padded to
 // a multiple of 64 (bf16) or d_r (fp32)
 hipError_t launch_adapter_du(int dtype, const void* dz, const int* counts, int n_max, const void* w1t, float* du,

@@ -23,10 +23,9 @@ namespace hero {
 namespace {
 
 template <typename T>
-__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in, int R, int C, int ld_in,
-                                                        T* __restrict__ out, int ld_out, int R_pad) {
+__device__ __forceinline__ void transpose_tile(const T* __restrict__ in, int R, int C, int ld_in,
+                                               T* __restrict__ out, int ld_out, int R_pad, int c0, int r0) {
   __shared__ T tile[64][65];
-  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   for (int i = ty; i < 64; i += 4) {
     const int r = r0 + i, c = c0 + tx;
@@ -36,6 +35,29 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in
   for (int i = ty; i < 64; i += 4) {
     const int c = c0 + i, r = r0 + tx;   // output row c, column r
     if (c < C && r < R_pad) out[static_cast<size_t>(c) * ld_out + r] = tile[tx][i];
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in, int R, int C, int ld_in,
+                                                        T* __restrict__ out, int ld_out, int R_pad) {
+  transpose_tile(in, R, C, ld_in, out, ld_out, R_pad, blockIdx.x * 64, blockIdx.y * 64);
+}
+
+// W_2^T [d_r][d] and W_1^T [d][rpad] (zero columns past d_r) in one launch: the first tiles of
+// the 1-D grid cover W_2, the rest W_1
+template <typename T>
+__global__ __launch_bounds__(256) void adapter_transpose_kernel(const T* __restrict__ w1, const T* __restrict__ w2,
+                                                                T* __restrict__ w1t, T* __restrict__ w2t, int d,
+                                                                int d_r, int rpad) {
+  const int tx2 = (d_r + 63) / 64;             // W_2 [d][d_r]: column tiles x row tiles
+  const int n2 = tx2 * ((d + 63) / 64);
+  const int b = blockIdx.x;
+  if (b < n2)
+    transpose_tile(w2, d, d_r, d_r, w2t, d, d, (b % tx2) * 64, (b / tx2) * 64);
+  else {
+    const int b1 = b - n2, tx1 = (d + 63) / 64;  // W_1 [d_r][d], rows padded to rpad
+    transpose_tile(w1, d_r, d, d, w1t, rpad, rpad, (b1 % tx1) * 64, (b1 / tx1) * 64);
   }
 }
 
@@ -181,6 +203,118 @@ __global__ __launch_bounds__(256) void adapter_wgrad_kernel(BlockBwdArgs a) {
   }
 }
 
+// The same partials on the matrix cores (bf16): the tokens are the K of two products,
+//   dW_1 block [64 r][128 i] = dz^T [r][m] (u [m][i]),  dW_2 block [128 i][64 r] = dy^T [i][m] (a [m][r]),
+// with dy = (1 - g) dh.  A batch of 32 rows is staged transposed in LDS as bf16 (K contiguous, row
+// pitch 40 elements, so the 16-byte fragment reads of 32 rows spread over the banks); the next
+// batch's global loads are in flight while the current one is multiplied.  Wave w owns column
+// block i = 32 w of both products: 2 + 2 tiles of v_mfma_f32_32x32x16_bf16 per 16 rows.
+constexpr int WM_TB = 32, WM_PT = 40;
+
+__global__ __launch_bounds__(256) void adapter_wgrad_mfma(BlockBwdArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t suT[WG_C][WM_PT];
+  __shared__ __attribute__((aligned(16))) bf16_t sdyT[WG_C][WM_PT];
+  __shared__ __attribute__((aligned(16))) bf16_t sdzT[WG_R][WM_PT];
+  __shared__ __attribute__((aligned(16))) bf16_t saT[WG_R][WM_PT];
+  const int n = a.counts[1];
+  const int chunk = wgrad_chunk(n, gridDim.z);
+  const int mb = blockIdx.z * chunk;
+  if (mb >= n) return;
+  const int me = min(n, mb + chunk);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c0 = blockIdx.x * WG_C, r0 = blockIdx.y * WG_R;
+  const bf16_t* U = static_cast<const bf16_t*>(a.u);
+  const bf16_t* DH = static_cast<const bf16_t*>(a.dh);
+  // this thread's staging work per batch: two 8-column pieces of u and dh (token k = e / 16),
+  // eight (token, rank) entries of dz and a; fetched into registers one batch ahead
+  u32x4 pu0, pu1, pd0, pd1;
+  float om0, om1, pz[8], pa[8];
+  const int k0 = tid >> 4, k1 = (tid + 256) >> 4, c8 = (tid & 15) * 8;
+#define HERO_WG_FETCH(m0_)                                                                          \
+  {                                                                                               \
+    const int nb_ = min(WM_TB, me - (m0_));                                                       \
+    om0 = om1 = 0.f;                                                                              \
+    pu0 = pu1 = pd0 = pd1 = u32x4{0, 0, 0, 0};                                                    \
+    if (k0 < nb_) {                                                                               \
+      const int t_ = a.idx_ad[(m0_) + k0];                                                        \
+      om0 = 1.0f - a.gate[t_];                                                                    \
+      const size_t row_ = static_cast<size_t>(t_) * a.d + c0 + c8;                                \
+      pu0 = *reinterpret_cast<const u32x4*>(U + row_);                                            \
+      pd0 = *reinterpret_cast<const u32x4*>(DH + row_);                                           \
+    }                                                                                             \
+    if (k1 < nb_) {                                                                               \
+      const int t_ = a.idx_ad[(m0_) + k1];                                                        \
+      om1 = 1.0f - a.gate[t_];                                                                    \
+      const size_t row_ = static_cast<size_t>(t_) * a.d + c0 + c8;                                \
+      pu1 = *reinterpret_cast<const u32x4*>(U + row_);                                            \
+      pd1 = *reinterpret_cast<const u32x4*>(DH + row_);                                           \
+    }                                                                                             \
+    _Pragma("unroll") for (int q = 0; q < 8; ++q) {                                               \
+      const int e_ = tid + 256 * q;                                                               \
+      const int k_ = e_ / WG_R, r_ = r0 + e_ % WG_R;                                              \
+      const bool ok_ = k_ < nb_ && r_ < a.d_r;                                                    \
+      pz[q] = ok_ ? a.dz32[static_cast<size_t>((m0_) + k_) * a.d_r + r_] : 0.f;                   \
+      pa[q] = ok_ ? a.a32[static_cast<size_t>((m0_) + k_) * a.d_r + r_] : 0.f;                    \
+    }                                                                                             \
+  }
+  auto put8 = [&](int k, u32x4 wu, u32x4 wd, float om) {
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      const uint32_t u2 = wu[x >> 1], d2 = wd[x >> 1];
+      suT[c8 + x][k] = static_cast<bf16_t>((x & 1) ? (u2 >> 16) : (u2 & 0xffffu));
+      sdyT[c8 + x][k] = f32_to_bf16(__uint_as_float((x & 1) ? (d2 & 0xffff0000u) : (d2 << 16)) * om);
+    }
+  };
+  f32x16 acc1[2], acc2[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc1[b][r] = acc2[b][r] = 0.f;
+  const int fr = lane & 31, kh = 8 * (lane >> 5);
+  HERO_WG_FETCH(mb)
+  for (int m0 = mb; m0 < me; m0 += WM_TB) {
+    __syncthreads();
+    put8(k0, pu0, pd0, om0);
+    put8(k1, pu1, pd1, om1);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int e = tid + 256 * q;
+      const int k = e / WG_R, rr = e % WG_R;
+      sdzT[rr][k] = f32_to_bf16(pz[q]);
+      saT[rr][k] = f32_to_bf16(pa[q]);
+    }
+    __syncthreads();
+    if (m0 + WM_TB < me) HERO_WG_FETCH(m0 + WM_TB)
+#pragma unroll
+    for (int ks = 0; ks < WM_TB / 16; ++ks) {
+      const int ko = 16 * ks + kh;
+      const bf16x8 fu = *reinterpret_cast<const bf16x8*>(&suT[32 * wave + fr][ko]);
+      const bf16x8 fy = *reinterpret_cast<const bf16x8*>(&sdyT[32 * wave + fr][ko]);
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const bf16x8 fz = *reinterpret_cast<const bf16x8*>(&sdzT[32 * b + fr][ko]);
+        const bf16x8 fa = *reinterpret_cast<const bf16x8*>(&saT[32 * b + fr][ko]);
+        acc1[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fz, fu, acc1[b], 0, 0, 0);
+        acc2[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fy, fa, acc2[b], 0, 0, 0);
+      }
+    }
+  }
+#undef HERO_WG_FETCH
+  const size_t c = blockIdx.z;
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      // dW_1: row = rank 32 b + row, column i = 32 wave + fr
+      const int rk = r0 + 32 * b + row;
+      if (rk < a.d_r) a.pw1[(c * a.d_r + rk) * a.d + c0 + 32 * wave + fr] = acc1[b][r];
+      // dW_2: row = column i = 32 wave + row, column = rank 32 b + fr
+      const int rk2 = r0 + 32 * b + fr;
+      if (rk2 < a.d_r) a.pw2[(c * a.d + c0 + 32 * wave + row) * a.d_r + rk2] = acc2[b][r];
+    }
+}
+
 // dW = the sum of the chunks' partials, chunk 0 first (zero when no token took the adapter)
 __global__ __launch_bounds__(256) void adapter_wgrad_reduce(BlockBwdArgs a) {
   const int n = a.counts[1];
@@ -323,6 +457,20 @@ hipError_t launch_transpose(int dtype, const void* in, int R, int C, int ld_in, 
   return hipGetLastError();
 }
 
+hipError_t launch_adapter_transpose(int dtype, const void* w1, const void* w2, void* w1t, void* w2t, int d, int d_r,
+                                    int rpad, hipStream_t s) {
+  const int blocks = (d_r + 63) / 64 * ((d + 63) / 64) + (d + 63) / 64 * ((rpad + 63) / 64);
+  if (dtype == 1)
+    adapter_transpose_kernel<bf16_t><<<blocks, 256, 0, s>>>(static_cast<const bf16_t*>(w1),
+                                                            static_cast<const bf16_t*>(w2), static_cast<bf16_t*>(w1t),
+                                                            static_cast<bf16_t*>(w2t), d, d_r, rpad);
+  else
+    adapter_transpose_kernel<float><<<blocks, 256, 0, s>>>(static_cast<const float*>(w1),
+                                                           static_cast<const float*>(w2), static_cast<float*>(w1t),
+                                                           static_cast<float*>(w2t), d, d_r, rpad);
+  return hipGetLastError();
+}
+
 hipError_t launch_adapter_bwd_mid(const BlockBwdArgs& a, hipStream_t s) {
   const dim3 grid((a.T + 3) / 4);
   if (a.dtype == 1)
@@ -335,7 +483,7 @@ hipError_t launch_adapter_bwd_mid(const BlockBwdArgs& a, hipStream_t s) {
 hipError_t launch_adapter_wgrad(const BlockBwdArgs& a, hipStream_t s) {
   const dim3 grid((a.d + WG_C - 1) / WG_C, (a.d_r + WG_R - 1) / WG_R, a.n_slices);
   if (a.dtype == 1)
-    adapter_wgrad_kernel<bf16_t><<<grid, 256, 0, s>>>(a);
+    adapter_wgrad_mfma<<<grid, 256, 0, s>>>(a);
   else
     adapter_wgrad_kernel<float><<<grid, 256, 0, s>>>(a);
   hipError_t e = hipGetLastError();

@@ -908,12 +908,18 @@ hipError_t run_f32(ARows<float> A, BRows<float> B, Epi epi, const int* m_count, 
 // 4 waves, each over a quarter of the group's k range; the 4 partial 32 x d_r
 // tiles are summed in LDS and written to part[g][m][n] (fp32).
 template <int TN, int SB>
-__global__ __launch_bounds__(256) void adapter_down_bf16(const bf16_t* __restrict__ u,
+__global__ __launch_bounds__(256) void adapter_down_bf16(const bf16_t* __restrict__ u0,
                                                          const int* __restrict__ idx,
                                                          const int* __restrict__ m_count,
-                                                         const bf16_t* __restrict__ w1,
-                                                         float* __restrict__ part, int T, int K,
-                                                         int k_group) {
+                                                         const bf16_t* __restrict__ w0,
+                                                         float* __restrict__ part0, int T, int K,
+                                                         int k_group, const bf16_t* __restrict__ u_z1,
+                                                         const bf16_t* __restrict__ w_z1,
+                                                         float* __restrict__ part_z1) {
+  // gridDim.z = 2 runs a second product over the same rows (the backward's z and e_a)
+  const bf16_t* __restrict__ u = blockIdx.z ? u_z1 : u0;
+  const bf16_t* __restrict__ w1 = blockIdx.z ? w_z1 : w0;
+  float* __restrict__ part = blockIdx.z ? part_z1 : part0;
   constexpr int R = TN * 32;
   __shared__ float red[4][32][R + 1];
   const int M = *m_count;
@@ -1443,6 +1449,33 @@ __global__ __launch_bounds__(256) void adapter_hidden_wide(const float* __restri
 
 }  // namespace
 
+namespace {
+
+// K-sliced partials of rows[idx[m]] W^T for the register-tiled ranks (32 .. 128); with u2 set, a
+// second product over the same rows in the same launch (gridDim.z = 2)
+hipError_t adapter_down_small(const bf16_t* uu, const int* idx_ad, const int* counts, int n_max, const bf16_t* ww,
+                              float* part, int d, int d_r, hipStream_t s, const bf16_t* u2, const bf16_t* w2_,
+                              float* p2) {
+  const int G = adapter_groups(d);
+  dim3 g1((n_max + 31) / 32, G, u2 ? 2 : 1);
+  // the adapter rank is a compile-time count of 32-column MFMA tiles
+  const bool b8 = adapter_batch(d, G) == 8;
+#define HERO_ADAPTER_DOWN(TN_)                                                                       \
+  (b8 ? adapter_down_bf16<TN_, 8><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G, u2, w2_, p2) \
+      : adapter_down_bf16<TN_, 4><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G, u2, w2_, p2))
+  switch (d_r) {
+    case 32: HERO_ADAPTER_DOWN(1); break;
+    case 64: HERO_ADAPTER_DOWN(2); break;
+    case 96: HERO_ADAPTER_DOWN(3); break;
+    case 128: HERO_ADAPTER_DOWN(4); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef HERO_ADAPTER_DOWN
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_adapter_down(int dtype, const void* u, const int* idx_ad, const int* counts,
                                int n_max, const void* w1, float* part, int d, int d_r,
                                hipStream_t s) {
@@ -1458,26 +1491,9 @@ hipError_t launch_adapter_down(int dtype, const void* u, const int* idx_ad, cons
     adapter_hidden_wide<<<blocks, 256, 0, s>>>(part, stride, counts, d_r, hid);
     return hipGetLastError();
   }
-  if (dtype == 1) {
-    const int G = adapter_groups(d);
-    dim3 g1((n_max + 31) / 32, G);
-    const bf16_t* uu = static_cast<const bf16_t*>(u);
-    const bf16_t* ww = static_cast<const bf16_t*>(w1);
-    // the adapter rank is a compile-time count of 32-column MFMA tiles
-    const bool b8 = adapter_batch(d, G) == 8;
-#define HERO_ADAPTER_DOWN(TN_)                                                                       \
-  (b8 ? adapter_down_bf16<TN_, 8><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G)  \
-      : adapter_down_bf16<TN_, 4><<<g1, 256, 0, s>>>(uu, idx_ad, counts, ww, part, n_max, d, d / G))
-    switch (d_r) {
-      case 32: HERO_ADAPTER_DOWN(1); break;
-      case 64: HERO_ADAPTER_DOWN(2); break;
-      case 96: HERO_ADAPTER_DOWN(3); break;
-      case 128: HERO_ADAPTER_DOWN(4); break;
-      default: return hipErrorInvalidValue;
-    }
-#undef HERO_ADAPTER_DOWN
-    return hipGetLastError();
-  }
+  if (dtype == 1)
+    return adapter_down_small(static_cast<const bf16_t*>(u), idx_ad, counts, n_max, static_cast<const bf16_t*>(w1),
+                              part, d, d_r, s, nullptr, nullptr, nullptr);
   // fp32: hid = SiLU(u W_1^T) into part[m][n]
   ARows<float> A{static_cast<const float*>(u), idx_ad, d};
   BRows<float> B{static_cast<const float*>(w1), nullptr, INT_MAX, d};
@@ -1582,6 +1598,19 @@ hipError_t launch_ffn_bwd_du(int dtype, const void* dgu, const int* counts, int 
 int adapter_proj_splits(int dtype, int d, int d_r) {
   if (dtype != 1) return 1;
   return adapter_wide(d_r) ? WIDE_SPLIT : adapter_groups(d);
+}
+
+hipError_t launch_adapter_proj2(int dtype, const void* rows0, const void* w0, float* part0, const void* rows1,
+                                const void* w1, float* part1, const int* idx_ad, const int* counts, int n_max, int d,
+                                int d_r, hipStream_t s) {
+  if (n_max <= 0) return hipSuccess;
+  if (dtype == 1 && !adapter_wide(d_r))
+    return adapter_down_small(static_cast<const bf16_t*>(rows0), idx_ad, counts, n_max, static_cast<const bf16_t*>(w0),
+                              part0, d, d_r, s, static_cast<const bf16_t*>(rows1), static_cast<const bf16_t*>(w1),
+                              part1);
+  hipError_t e = launch_adapter_proj(dtype, rows0, idx_ad, counts, n_max, w0, part0, d, d_r, s);
+  if (e != hipSuccess) return e;
+  return launch_adapter_proj(dtype, rows1, idx_ad, counts, n_max, w1, part1, d, d_r, s);
 }
 
 hipError_t launch_adapter_proj(int dtype, const void* rows, const int* idx_ad, const int* counts, int n_max,
