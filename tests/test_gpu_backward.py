@@ -214,3 +214,44 @@ def test_skip_penalty_gradient_feeds_the_block_backward():
     _check(w, res, ref, use_ffn, hbar, dh, gate, F, A)
     del db
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("w", [BF16.replace(d_ff=1408), F32])
+def test_frozen_weight_copies_are_exact_transposes(w):
+    """hero_ffn_backward_weights_make writes W_d^T and [W_g; W_u]^T bit for bit."""
+    import torch
+    from paper_2609_08189_amd import hero as H
+    from paper_2609_08189_amd.device import dims_struct, upload
+    print(f"case weight copies {w.name} d={w.d} d_ff={w.d_ff}", flush=True)
+    ffn = {k: upload(v, "cuda") for k, v in synth.ffn_layer(w, 0, 4).items()}
+    s = H.hero_ffn_weights(*(ffn[k].data_ptr() for k in ("norm_w", "w_gate", "w_up", "w_down")))
+    wd_t = torch.empty((w.d_ff, w.d), dtype=ffn["w_down"].dtype, device="cuda")
+    wgu_t = torch.empty((w.d, 2 * w.d_ff), dtype=ffn["w_down"].dtype, device="cuda")
+    H.check(H.hero_ffn_backward_weights_make(dims_struct(w), s, wd_t, wgu_t), "hero_ffn_backward_weights_make")
+    torch.cuda.synchronize()
+    bits = lambda t: t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
+    assert torch.equal(bits(wd_t), bits(ffn["w_down"].t().contiguous()))
+    assert torch.equal(bits(wgu_t), bits(torch.cat([ffn["w_gate"], ffn["w_up"]], 0).t().contiguous()))
+
+
+def test_block_backward_paper_operating_point():
+    """The paper's operating point on the Llama-3.1-8B shape (adapter rank 896 through the wide
+    path, 25 % of the tokens on the adapter), budget rule given: every adapter row and the weight
+    gradients in full, the FFN rows on a sample."""
+    import torch
+    w = synth.WORKLOADS["llama31_8b_paper"]
+    db, hbar, ffn, ad, dh, gate, use_ffn, _ = _setup(w, 1, budget_mode=True)
+    db.run()
+    res = db.results()
+    dims, F, A = dims_of(w), ffn_of(ffn), adapter_of(ad)
+    ad_rows = np.nonzero(~use_ffn)[0]
+    ref_a = O.routed_block_backward(hbar.f64[ad_rows], gate[ad_rows].astype(np.float64), use_ffn[ad_rows], F, A,
+                                    dims, dh.f64[ad_rows])
+    _check(w, res, ref_a, use_ffn, hbar, dh, gate, F, A, rows=ad_rows)
+    _check_wgrad(w, res, ref_a.dw1, ref_a.dw2, len(ad_rows))
+    sample = np.sort(np.random.default_rng(7).choice(np.nonzero(use_ffn)[0], 12, replace=False))
+    ref_f = O.routed_block_backward(hbar.f64[sample], gate[sample].astype(np.float64), use_ffn[sample], F, A,
+                                    dims, dh.f64[sample])
+    _check(w, res, ref_f, use_ffn, hbar, dh, gate, F, A, rows=sample)
+    del db
+    torch.cuda.empty_cache()
