@@ -209,26 +209,31 @@ __global__ __launch_bounds__(256) void adapter_wgrad_kernel(BlockBwdArgs a) {
 // pitch 40 elements, so the 16-byte fragment reads of 32 rows spread over the banks); the next
 // batch's global loads are in flight while the current one is multiplied.  Wave w owns column
 // block i = 32 w of both products: 2 + 2 tiles of v_mfma_f32_32x32x16_bf16 per 16 rows.
+// RT: 32-rank tiles per workgroup (2: 128-rank blocks at rank 896 measured no faster, the
+// kernel being bound by each batch's load latency rather than by re-staging u and dh).
 constexpr int WM_TB = 32, WM_PT = 40;
 
+template <int RT>
 __global__ __launch_bounds__(256) void adapter_wgrad_mfma(BlockBwdArgs a) {
+  constexpr int WR = 32 * RT;
   __shared__ __attribute__((aligned(16))) bf16_t suT[WG_C][WM_PT];
   __shared__ __attribute__((aligned(16))) bf16_t sdyT[WG_C][WM_PT];
-  __shared__ __attribute__((aligned(16))) bf16_t sdzT[WG_R][WM_PT];
-  __shared__ __attribute__((aligned(16))) bf16_t saT[WG_R][WM_PT];
+  __shared__ __attribute__((aligned(16))) bf16_t sdzT[WR][WM_PT];
+  __shared__ __attribute__((aligned(16))) bf16_t saT[WR][WM_PT];
   const int n = a.counts[1];
   const int chunk = wgrad_chunk(n, gridDim.z);
   const int mb = blockIdx.z * chunk;
   if (mb >= n) return;
   const int me = min(n, mb + chunk);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int c0 = blockIdx.x * WG_C, r0 = blockIdx.y * WG_R;
+  const int c0 = blockIdx.x * WG_C, r0 = blockIdx.y * WR;
   const bf16_t* U = static_cast<const bf16_t*>(a.u);
   const bf16_t* DH = static_cast<const bf16_t*>(a.dh);
   // this thread's staging work per batch: two 8-column pieces of u and dh (token k = e / 16),
-  // eight (token, rank) entries of dz and a; fetched into registers one batch ahead
+  // 4 RT (token, rank) entries of dz and a; fetched into registers one batch ahead
+  constexpr int NZ = WM_TB * WR / 256;
   u32x4 pu0, pu1, pd0, pd1;
-  float om0, om1, pz[8], pa[8];
+  float om0, om1, pz[NZ], pa[NZ];
   const int k0 = tid >> 4, k1 = (tid + 256) >> 4, c8 = (tid & 15) * 8;
 #define HERO_WG_FETCH(m0_)                                                                          \
   {                                                                                               \
@@ -249,9 +254,9 @@ __global__ __launch_bounds__(256) void adapter_wgrad_mfma(BlockBwdArgs a) {
       pu1 = *reinterpret_cast<const u32x4*>(U + row_);                                            \
       pd1 = *reinterpret_cast<const u32x4*>(DH + row_);                                           \
     }                                                                                             \
-    _Pragma("unroll") for (int q = 0; q < 8; ++q) {                                               \
+    _Pragma("unroll") for (int q = 0; q < NZ; ++q) {                                              \
       const int e_ = tid + 256 * q;                                                               \
-      const int k_ = e_ / WG_R, r_ = r0 + e_ % WG_R;                                              \
+      const int k_ = e_ / WR, r_ = r0 + e_ % WR;                                                  \
       const bool ok_ = k_ < nb_ && r_ < a.d_r;                                                    \
       pz[q] = ok_ ? a.dz32[static_cast<size_t>((m0_) + k_) * a.d_r + r_] : 0.f;                   \
       pa[q] = ok_ ? a.a32[static_cast<size_t>((m0_) + k_) * a.d_r + r_] : 0.f;                    \
@@ -265,9 +270,9 @@ __global__ __launch_bounds__(256) void adapter_wgrad_mfma(BlockBwdArgs a) {
       sdyT[c8 + x][k] = f32_to_bf16(__uint_as_float((x & 1) ? (d2 & 0xffff0000u) : (d2 << 16)) * om);
     }
   };
-  f32x16 acc1[2], acc2[2];
+  f32x16 acc1[RT], acc2[RT];
 #pragma unroll
-  for (int b = 0; b < 2; ++b)
+  for (int b = 0; b < RT; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc1[b][r] = acc2[b][r] = 0.f;
   const int fr = lane & 31, kh = 8 * (lane >> 5);
@@ -277,9 +282,9 @@ __global__ __launch_bounds__(256) void adapter_wgrad_mfma(BlockBwdArgs a) {
     put8(k0, pu0, pd0, om0);
     put8(k1, pu1, pd1, om1);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
+    for (int q = 0; q < NZ; ++q) {
       const int e = tid + 256 * q;
-      const int k = e / WG_R, rr = e % WG_R;
+      const int k = e / WR, rr = e % WR;
       sdzT[rr][k] = f32_to_bf16(pz[q]);
       saT[rr][k] = f32_to_bf16(pa[q]);
     }
@@ -291,7 +296,7 @@ __global__ __launch_bounds__(256) void adapter_wgrad_mfma(BlockBwdArgs a) {
       const bf16x8 fu = *reinterpret_cast<const bf16x8*>(&suT[32 * wave + fr][ko]);
       const bf16x8 fy = *reinterpret_cast<const bf16x8*>(&sdyT[32 * wave + fr][ko]);
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
+      for (int b = 0; b < RT; ++b) {
         const bf16x8 fz = *reinterpret_cast<const bf16x8*>(&sdzT[32 * b + fr][ko]);
         const bf16x8 fa = *reinterpret_cast<const bf16x8*>(&saT[32 * b + fr][ko]);
         acc1[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fz, fu, acc1[b], 0, 0, 0);
@@ -302,7 +307,7 @@ __global__ __launch_bounds__(256) void adapter_wgrad_mfma(BlockBwdArgs a) {
 #undef HERO_WG_FETCH
   const size_t c = blockIdx.z;
 #pragma unroll
-  for (int b = 0; b < 2; ++b)
+  for (int b = 0; b < RT; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
@@ -481,11 +486,11 @@ hipError_t launch_adapter_bwd_mid(const BlockBwdArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_adapter_wgrad(const BlockBwdArgs& a, hipStream_t s) {
-  const dim3 grid((a.d + WG_C - 1) / WG_C, (a.d_r + WG_R - 1) / WG_R, a.n_slices);
-  if (a.dtype == 1)
-    adapter_wgrad_mfma<<<grid, 256, 0, s>>>(a);
-  else
-    adapter_wgrad_kernel<float><<<grid, 256, 0, s>>>(a);
+  if (a.dtype == 1) {
+    adapter_wgrad_mfma<2><<<dim3((a.d + WG_C - 1) / WG_C, (a.d_r + 63) / 64, a.n_slices), 256, 0, s>>>(a);
+  } else {
+    adapter_wgrad_kernel<float><<<dim3((a.d + WG_C - 1) / WG_C, (a.d_r + WG_R - 1) / WG_R, a.n_slices), 256, 0, s>>>(a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t E = static_cast<size_t>(a.d_r) * a.d;
