@@ -110,6 +110,8 @@ F32 = synth.Workload("bwd_f32", "f32", d=256, d_ff=688, d_r=16, L_R=4, d_m=32, T
     (BF16.replace(d_r=32, T=97), 3, False, False),           # rank padded to 64 for du
     (BF16.replace(d_r=96, d=768, d_ff=2048, T=450), 4, True, True),
     (BF16.replace(d_r=256, d_ff=1024, T=200), 5, False, True),   # wide adapter path
+    (BF16.replace(d=256, d_ff=4096, T=2500), 13, True, True),    # more tiles than CUs: persistent gate/up
+    (BF16.replace(d=256, d_ff=4096, T=2500), 14, False, False),  # the same, launches sized by T
     (F32, 6, False, False),
     (F32.replace(T=61, d_r=24), 7, True, True),
 ])
