@@ -116,10 +116,99 @@ __global__ __launch_bounds__(256) void rowstats_kernel(const T* __restrict__ hba
   }
 }
 
+// Few tokens (a decode batch): one workgroup per token, its row split over the 4 waves (8
+// elements per lane per pass), the four sums reduced across the waves through LDS, so that
+// every CU takes part.
+template <typename T>
+__global__ __launch_bounds__(256) void rowstats_row_kernel(const T* __restrict__ hbar,
+                                                           const T* __restrict__ prev1,
+                                                           const T* __restrict__ prev2,
+                                                           const T* __restrict__ norm_w, int d, int j,
+                                                           float eps_norm, float* __restrict__ rowstat,
+                                                           T* __restrict__ u) {
+  __shared__ f32x4 part[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const size_t row = static_cast<size_t>(blockIdx.x) * d;
+  constexpr int RC = 4;   // 8-element chunks per thread kept in registers (rows up to 8192)
+  Raw8<T> h[RC];
+  float ss = 0.f, dd = 0.f, dp = 0.f, pp = 0.f;
+  const bool resident = d <= RC * 8 * 256;
+  for (int c0 = 0; c0 < d; c0 += RC * 8 * 256) {
+    Raw8<T> a[RC], b[RC];
+#pragma unroll
+    for (int c = 0; c < RC; ++c) {
+      const int col = c0 + 8 * (tid + 256 * c);
+      if (col < d) {
+        h[c].load(hbar + row + col);
+        if (j >= 2) a[c].load(prev1 + row + col);
+        if (j >= 3) b[c].load(prev2 + row + col);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < RC; ++c) {
+      const int col = c0 + 8 * (tid + 256 * c);
+      if (col >= d) continue;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float hv = h[c][i];
+        ss += hv * hv;
+        if (j >= 2) {
+          const float av = a[c][i];
+          const float dj = hv - av;
+          dd += dj * dj;
+          if (j >= 3) {
+            const float dq = av - b[c][i];
+            dp += dj * dq;
+            pp += dq * dq;
+          }
+        }
+      }
+    }
+  }
+  ss = wave_sum(ss);
+  dd = wave_sum(dd);
+  dp = wave_sum(dp);
+  pp = wave_sum(pp);
+  if (lane == 0) part[wave] = f32x4{ss, dd, dp, pp};
+  __syncthreads();
+  const f32x4 tot = part[0] + part[1] + part[2] + part[3];
+  const float inv_rms = 1.0f / sqrtf(tot[0] / static_cast<float>(d) + eps_norm);
+  if (tid == 0) {
+    f32x4 r = {inv_rms, tot[1], tot[2], tot[3]};
+    *reinterpret_cast<f32x4*>(rowstat + 4 * static_cast<size_t>(blockIdx.x)) = r;
+  }
+  for (int c0 = 0; c0 < d; c0 += RC * 8 * 256) {
+#pragma unroll
+    for (int c = 0; c < RC; ++c) {
+      const int col = c0 + 8 * (tid + 256 * c);
+      if (col >= d) continue;
+      if (!resident) h[c].load(hbar + row + col);
+      Raw8<T> w;
+      w.load(norm_w + col);
+      float o[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = h[c][i] * inv_rms * w[i];
+      st8(u + row + col, o);
+    }
+  }
+}
+
 hipError_t launch_rowstats(int dtype, const void* hbar, const void* prev1, const void* prev2,
                            const void* norm_w, int T, int d, int j, float eps_norm,
                            float* rowstat, void* u, hipStream_t s) {
   dim3 grid((T + 3) / 4), block(256);
+  if (T <= 1024) {
+    // fewer than 4 row-waves per CU: a workgroup per token
+    if (dtype == 1)
+      rowstats_row_kernel<bf16_t><<<T, 256, 0, s>>>(
+          static_cast<const bf16_t*>(hbar), static_cast<const bf16_t*>(prev1), static_cast<const bf16_t*>(prev2),
+          static_cast<const bf16_t*>(norm_w), d, j, eps_norm, rowstat, static_cast<bf16_t*>(u));
+    else
+      rowstats_row_kernel<float><<<T, 256, 0, s>>>(
+          static_cast<const float*>(hbar), static_cast<const float*>(prev1), static_cast<const float*>(prev2),
+          static_cast<const float*>(norm_w), d, j, eps_norm, rowstat, static_cast<float*>(u));
+    return hipGetLastError();
+  }
   if (dtype == 1) {
     rowstats_kernel<bf16_t><<<grid, block, 0, s>>>(
         static_cast<const bf16_t*>(hbar), static_cast<const bf16_t*>(prev1),
