@@ -1081,6 +1081,8 @@ int adapter_batch(int K, int G) { return (K / G) % 512 == 0 ? 8 : 4; }
 // router pre-activations: 128-row tiles over all 8 waves, K split four ways
 using TileRouter = Tile<128, 256, 2, 4, false>;
 using TileRouterNarrow = Tile<128, 128, 2, 4, false>;
+// few tokens (a decode batch): 64-row tiles of 4 waves, four times the workgroups
+using TileRouterSmall = Tile<64, 128, 1, 4, false>;
 
 }  // namespace
 
@@ -1094,6 +1096,8 @@ hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, con
     ARows<bf16_t> A{static_cast<const bf16_t*>(hbar), nullptr, d};
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_hd), static_cast<const bf16_t*>(ps1), d_e, d};
     const int splits = router_gemm_splits(dtype, d);
+    if (T <= 1024 && N % TileRouterSmall::OUT_N == 0)
+      return run_tile<TileRouterSmall>(A, B, epi, nullptr, T, N, d, s, splits);
     if (N % TileRouter::OUT_N == 0) return run_tile<TileRouter>(A, B, epi, nullptr, T, N, d, s, splits);
     return run_tile<TileRouterNarrow>(A, B, epi, nullptr, T, N, d, s, splits);
   }
