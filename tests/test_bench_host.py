@@ -47,3 +47,26 @@ def test_summarize_reads_rocprof_csv(tmp_path, capsys):
     assert "| k(int) | FETCH_SIZE | 2 | 20.0 | 30.0 |" in out
     assert "| k(int) | 2 | 2.50 | 2.00 | 3.00 |" in out      # dispatches 2 and 3 of k
     assert "| j(int) |" not in out.split("dispatches 1..2")[1].split("###")[0]   # j has one dispatch
+
+
+def test_backward_work_counts():
+    """The backward's algorithmic work: e (2 d d_ff), the gate/up recompute and du (4 d d_ff each)
+    per FFN token; 6 d r + 4 d r per adapter token; every kernel group has bytes."""
+    from paper_2609_08189_amd import synth
+    w = synth.WORKLOADS["llama31_8b_layer"]
+    n_f, n_a = 2995, 1101
+    wk = bench.backward_work(w, n_f, n_a)
+    assert set(wk) == set(bench.BWD_KERNELS)
+    dd = w.d * w.d_ff
+    assert wk["bwd_ffn_e"]["flops"] == 2 * dd * n_f
+    assert wk["bwd_ffn_gate_up"]["flops"] == wk["bwd_ffn_du"]["flops"] == 4 * dd * n_f
+    assert wk["bwd_adapter"]["flops"] + wk["bwd_adapter_wgrad"]["flops"] == 10 * w.d * w.d_r * n_a
+    # the weights dominate the FFN products' bytes: W_d^T once, W_g and W_u (or their transposes) twice
+    assert wk["bwd_ffn_e"]["bytes"] >= 2 * dd and wk["bwd_ffn_du"]["bytes"] >= 4 * dd
+    assert all(v["bytes"] > 0 for v in wk.values())
+
+
+def test_graph_flag_and_backward_flag_parse():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--help"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0 and "--graph" in r.stdout and "--backward" in r.stdout
