@@ -823,9 +823,14 @@ int wgrad_slices(int T) { return std::max(1, std::min(8, T / 32)); }
 // the adapter rank as the K of the du product: whole 64-deep k-tiles on the MFMA path
 int rank_pad(const hero_dims& d) { return d.dtype == HERO_BF16 ? (d.d_r + 63) / 64 * 64 : d.d_r; }
 
+// wide adapter ranks (bf16, above 128): the weight gradients run on the GEMM core over
+// tokens-contiguous copies of the adapter rows
+bool wgrad_wide(const hero_dims& d) { return d.dtype == HERO_BF16 && d.d_r > 128; }
+int wgrad_kp(int n) { return std::max(64, (n + 63) / 64 * 64); }
+
 struct BwdLayout {
   size_t idx_f, idx_a, counts, rowstat, u, e, dgu, dgpart, du_f, du_a, part_z, part_e, dz32, a32, dzk, dg_ad,
-      w1t, w2t, pw1, pw2, total;
+      w1t, w2t, pw1, pw2, uaT, dyT, dzT, aT, total;
   int n_parts, n_slices, rpad;
 };
 
@@ -860,8 +865,14 @@ BwdLayout bwd_layout_of(const hero_dims& d, int T) {
   L.dg_ad = take(t * 4);
   L.w1t = take(static_cast<size_t>(d.d) * L.rpad * es);
   L.w2t = take(static_cast<size_t>(d.d_r) * d.d * es);
-  L.pw1 = take(n_chunks * d.d_r * d.d * 4);
-  L.pw2 = take(n_chunks * d.d_r * d.d * 4);
+  const bool wide = wgrad_wide(d);
+  const size_t kp = static_cast<size_t>(wgrad_kp(T));
+  L.pw1 = take(wide ? 0 : n_chunks * d.d_r * d.d * 4);
+  L.pw2 = take(wide ? 0 : n_chunks * d.d_r * d.d * 4);
+  L.uaT = take(wide ? kp * d.d * 2 : 0);
+  L.dyT = take(wide ? kp * d.d * 2 : 0);
+  L.dzT = take(wide ? kp * d.d_r * 2 : 0);
+  L.aT = take(wide ? kp * d.d_r * 2 : 0);
   L.total = off;
   return L;
 }
@@ -1036,7 +1047,15 @@ int hero_routed_block_backward(const hero_dims* dims, int T, const void* hbar, c
     return x;
   });
   if (err != hipSuccess) return HERO_E_LAUNCH;
-  err = timed(HERO_K_BWD_ADAPTER_WGRAD, s, [&] { return launch_adapter_wgrad(a, s); });
+  err = timed(HERO_K_BWD_ADAPTER_WGRAD, s, [&] {
+    if (!wgrad_wide(D)) return launch_adapter_wgrad(a, s);
+    // dW_1 = dz^T u, dW_2 = dy^T a with the adapter tokens as K (zero columns pad it to kp)
+    const int kp = wgrad_kp(na_max);
+    hipError_t x = launch_adapter_wgrad_stage(a, kp, ws + L.uaT, ws + L.dyT, ws + L.dzT, ws + L.aT, s);
+    if (x == hipSuccess) x = launch_gemm_nt_f32(ws + L.dzT, D.d_r, ws + L.uaT, D.d, kp, grads->dw1, D.d, s);
+    if (x == hipSuccess) x = launch_gemm_nt_f32(ws + L.dyT, D.d, ws + L.aT, D.d_r, kp, grads->dw2, D.d_r, s);
+    return x;
+  });
   if (err != hipSuccess) return HERO_E_LAUNCH;
   err = timed(HERO_K_BWD_ROWS, s, [&] { return launch_block_bwd_rows(a, s); });
   return err == hipSuccess ? HERO_OK : HERO_E_LAUNCH;

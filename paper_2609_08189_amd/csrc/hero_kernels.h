@@ -207,6 +207,14 @@ hipError_t launch_adapter_bwd_mid(const BlockBwdArgs& a, hipStream_t s);
 hipError_t launch_adapter_wgrad(const BlockBwdArgs& a, hipStream_t s);
 // dL/dhbar = dL/dh + RMSNorm backward of du (every token once), dL/dg, dL/dlogit
 hipError_t launch_block_bwd_rows(const BlockBwdArgs& a, hipStream_t s);
+// Wide adapter ranks: the adapter rows staged transposed in bf16 with the tokens contiguous
+// (columns m >= counts[1] up to kp zero): uaT [d][kp] = u rows, dyT [d][kp] = (1 - g) dh rows,
+// dzT [d_r][kp], aT [d_r][kp]; then dW_1 = dzT uaT^T and dW_2 = dyT aT^T on the GEMM core.
+hipError_t launch_adapter_wgrad_stage(const BlockBwdArgs& a, int kp, void* uaT, void* dyT, void* dzT, void* aT,
+                                      hipStream_t s);
+// C[m][n] = sum_k A[m][k] B[n][k] (bf16 A [M][K], B [N][K]; fp32 C with row pitch ldc); N % 128 == 0,
+// K % 64 == 0
+hipError_t launch_gemm_nt_f32(const void* A, int M, const void* B, int N, int K, float* C, int ldc, hipStream_t s);
 // alpha L_skip (Eq. 18) into loss[0] and its gradient over gates [L_R][batch seq]
 hipError_t launch_skip_penalty(const float* gates, int L_R, int batch, int seq, float alpha, float* loss,
                                float* dgates, hipStream_t s);

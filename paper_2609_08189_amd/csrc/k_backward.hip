@@ -320,6 +320,44 @@ __global__ __launch_bounds__(256) void adapter_wgrad_mfma(BlockBwdArgs a) {
     }
 }
 
+// Tokens-contiguous copies of the adapter rows for the wide-rank weight gradients.  A workgroup
+// takes 64 tokens x 64 features of one of the four outputs (blockIdx.z): it reads the token-major
+// rows with loads contiguous along the features, and writes the transposed tile with stores
+// contiguous along the tokens; tokens past counts[1] (up to kp) are written as zero.
+__global__ __launch_bounds__(256) void adapter_wgrad_stage_kernel(BlockBwdArgs a, int kp, bf16_t* __restrict__ uaT,
+                                                                  bf16_t* __restrict__ dyT, bf16_t* __restrict__ dzT,
+                                                                  bf16_t* __restrict__ aT) {
+  __shared__ float tile[64][65];
+  const int n = a.counts[1];
+  const int which = blockIdx.z;                      // 0 u, 1 dy, 2 dz, 3 a
+  const int F = which < 2 ? a.d : a.d_r;             // features of this output
+  const int f0 = blockIdx.y * 64, m0 = blockIdx.x * 64;
+  if (f0 >= F) return;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const bf16_t* U = static_cast<const bf16_t*>(a.u);
+  const bf16_t* DH = static_cast<const bf16_t*>(a.dh);
+  for (int k = ty; k < 64; k += 4) {
+    const int m = m0 + k, f = f0 + tx;
+    float v = 0.f;
+    if (m < n && f < F) {
+      if (which < 2) {
+        const int t = a.idx_ad[m];
+        const size_t o = static_cast<size_t>(t) * a.d + f;
+        v = which == 0 ? bf16_to_f32(U[o]) : (1.0f - a.gate[t]) * bf16_to_f32(DH[o]);
+      } else {
+        v = (which == 2 ? a.dz32 : a.a32)[static_cast<size_t>(m) * a.d_r + f];
+      }
+    }
+    tile[k][tx] = v;
+  }
+  __syncthreads();
+  bf16_t* out = which == 0 ? uaT : which == 1 ? dyT : which == 2 ? dzT : aT;
+  for (int k = ty; k < 64; k += 4) {
+    const int f = f0 + k, m = m0 + tx;
+    if (f < F && m < kp) out[static_cast<size_t>(f) * kp + m] = f32_to_bf16(tile[tx][k]);
+  }
+}
+
 // dW = the sum of the chunks' partials, chunk 0 first (zero when no token took the adapter)
 __global__ __launch_bounds__(256) void adapter_wgrad_reduce(BlockBwdArgs a) {
   const int n = a.counts[1];
@@ -496,6 +534,15 @@ hipError_t launch_adapter_wgrad(const BlockBwdArgs& a, hipStream_t s) {
   const size_t E = static_cast<size_t>(a.d_r) * a.d;
   const int blocks = static_cast<int>(std::min<size_t>((E + 255) / 256, 4096));
   adapter_wgrad_reduce<<<blocks, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_adapter_wgrad_stage(const BlockBwdArgs& a, int kp, void* uaT, void* dyT, void* dzT, void* aT,
+                                      hipStream_t s) {
+  const int fmax = a.d > a.d_r ? a.d : a.d_r;
+  const dim3 grid((kp + 63) / 64, (fmax + 63) / 64, 4);
+  adapter_wgrad_stage_kernel<<<grid, 256, 0, s>>>(a, kp, static_cast<bf16_t*>(uaT), static_cast<bf16_t*>(dyT),
+                                                  static_cast<bf16_t*>(dzT), static_cast<bf16_t*>(aT));
   return hipGetLastError();
 }
 

@@ -1620,6 +1620,13 @@ hipError_t launch_adapter_proj2(int dtype, const void* rows0, const void* w0, fl
 hipError_t launch_adapter_proj(int dtype, const void* rows, const int* idx_ad, const int* counts, int n_max,
                                const void* w, float* part, int d, int d_r, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
+  if (dtype == 1 && adapter_wide(d_r)) {
+    // the K-sliced partials only (the forward's SiLU hidden rows are not needed here)
+    ARows<bf16_t> A{static_cast<const bf16_t*>(rows), idx_ad, d};
+    BRows<bf16_t> B{static_cast<const bf16_t*>(w), nullptr, INT_MAX, d};
+    const size_t stride = static_cast<size_t>(n_max) * d_r;
+    return run_tile<TileWide>(A, B, EpiStoreF32{part, d_r, stride}, counts, n_max, d_r, d, s, WIDE_SPLIT);
+  }
   if (dtype == 1) return launch_adapter_down(1, rows, idx_ad, counts, n_max, w, part, d, d_r, s);
   ARows<float> A{static_cast<const float*>(rows), idx_ad, d};
   BRows<float> B{static_cast<const float*>(w), nullptr, INT_MAX, d};
@@ -1637,6 +1644,13 @@ hipError_t launch_adapter_du(int dtype, const void* dz, const int* counts, int n
   ARows<float> A{static_cast<const float*>(dz), nullptr, k};
   BRows<float> B{static_cast<const float*>(w1t), nullptr, INT_MAX, k};
   return run_f32<false>(A, B, EpiStoreF32{du, d, 0}, counts, n_max, d, k, s);
+}
+
+hipError_t launch_gemm_nt_f32(const void* A, int M, const void* B, int N, int K, float* C, int ldc, hipStream_t s) {
+  if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
+  ARows<bf16_t> a{static_cast<const bf16_t*>(A), nullptr, K};
+  BRows<bf16_t> b{static_cast<const bf16_t*>(B), nullptr, INT_MAX, K};
+  return run_tile<TileWide>(a, b, EpiStoreF32{C, ldc, 0}, nullptr, M, N, K, s);
 }
 
 }  // namespace hero
