@@ -420,7 +420,8 @@ typedef struct hero_block_grads {
   float *dgate, *dlogit, *dw1, *dw2;
 } hero_block_grads;
 
-/* Workspace bytes for hero_routed_block_backward with T tokens.  Host-only; validates dims. */
+/* Workspace bytes for hero_routed_block_backward with T tokens.  Host-only; validates dims.
+ * The workspace must not overlap any argument of the call (HERO_E_ALIAS). */
 int hero_backward_workspace_size(const hero_dims *dims, int T, size_t *bytes);
 
 /*

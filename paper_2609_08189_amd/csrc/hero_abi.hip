@@ -957,8 +957,11 @@ int hero_routed_block_backward(const hero_dims* dims, int T, const void* hbar, c
   if (overlap(grads->dhbar, hb, hbar, hb) || overlap(grads->dhbar, hb, dh_out, hb)) return HERO_E_ALIAS;
   const BwdLayout L = bwd_layout_of(*dims, T);
   if (!workspace || workspace_bytes < L.total) return HERO_E_WORKSPACE;
+  const size_t tb = static_cast<size_t>(T) * 4, wb = static_cast<size_t>(dims->d) * dims->d_r * 4;
   if (overlap(workspace, L.total, hbar, hb) || overlap(workspace, L.total, dh_out, hb) ||
-      overlap(workspace, L.total, grads->dhbar, hb))
+      overlap(workspace, L.total, grads->dhbar, hb) || overlap(workspace, L.total, grads->dgate, tb) ||
+      overlap(workspace, L.total, grads->dlogit, tb) || overlap(workspace, L.total, grads->dw1, wb) ||
+      overlap(workspace, L.total, grads->dw2, wb) || overlap(grads->dw1, wb, grads->dw2, wb))
     return HERO_E_ALIAS;
   if ((st = check_device()) != HERO_OK) return st;
 

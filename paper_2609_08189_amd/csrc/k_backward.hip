@@ -9,7 +9,8 @@
 // take theirs here.  The products (FFN and adapter) run on the GEMM core; this file holds
 //   * a tiled transpose (the frozen weights' K-contiguous copies, the adapter's per call);
 //   * the adapter's middle step: a = SiLU(z), dz = (1 - g) e_a SiLU'(z), dL/dg = -<e_a, a>;
-//   * the adapter weight gradients, summed over token chunks in a fixed order;
+//   * the adapter weight gradients, summed over token chunks in a fixed order (for wide ranks,
+//     tokens-contiguous copies of the adapter rows, which the GEMM core then contracts);
 //   * the row pass: dL/dhbar = dL/dh + the RMSNorm backward of du, and dL/dg, dL/dlogit;
 //   * alpha L_skip (Sec. 3.3, Eq. 18): the squared per-token sum of the gates over the routed
 //     blocks, averaged over the positions with a next token, and its gradient.

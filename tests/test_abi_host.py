@@ -320,6 +320,10 @@ def test_backward_entry_points_validate():
     assert bwd(ws=None) == H.HERO_E_WORKSPACE
     assert bwd(n=need - 1) == H.HERO_E_WORKSPACE
     assert bwd(ws=hb) == H.HERO_E_ALIAS
+    assert bwd(grads=H.hero_block_grads(FAKE + (4 << 30), FAKE, FAKE, ws + 4096, FAKE + (7 << 30) + (1 << 20))) == \
+        H.HERO_E_ALIAS                                                       # dW_1 inside the workspace
+    assert bwd(grads=H.hero_block_grads(FAKE + (4 << 30), FAKE, FAKE, FAKE + (7 << 30) + 8192,
+                                        FAKE + (7 << 30) + 8192 + 4096)) == H.HERO_E_ALIAS   # dW_1, dW_2 overlap
     # operand rows the GEMM core addresses with 32-bit offsets: [dG dU] of 2^17 tokens is too big
     assert bwd(d=good_dims(d_ff=8192), T=1 << 17, n=1 << 40) == H.HERO_E_UNSUPPORTED
     assert bwd(routing=H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 1.5, None)) == H.HERO_E_RANGE
