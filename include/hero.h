@@ -30,6 +30,11 @@
  *   normaliser zeta         [T][d_m] fp32
  *   history scores p, m     [T] fp32
  * All device pointers must be 16-byte aligned.
+ * Size limit (bf16): the matrix products address operand rows with 32-bit byte
+ * offsets, so a call whose token rows (T x max(d, d_ff, d_r), or the attention
+ * width n_heads x head_dim in the decoder calls) or weight matrices (d_ff x d,
+ * d_r x d, the attention projections) would span 4 GiB or more returns
+ * HERO_E_UNSUPPORTED; split such a batch into smaller calls.
  */
 #ifndef HERO_H
 #define HERO_H

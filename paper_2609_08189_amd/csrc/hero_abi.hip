@@ -64,6 +64,17 @@ Layout layout_of(const hero_dims& d, int T, bool stack) {
   return L;
 }
 
+// The bf16 GEMM core addresses operand rows with 32-bit byte offsets, so every operand it reads
+// must span less than 4 GiB: T token rows of width d, d_ff or d_r (or of a given extra width),
+// and the d_ff x d and d_r x d weights (the fp32 path uses 64-bit offsets).
+constexpr long long kGemmSpan = 1LL << 32;
+bool fwd_fits(const hero_dims& d, long long T, long long extra_width = 0) {
+  if (d.dtype != HERO_BF16) return true;
+  const long long w = std::max({static_cast<long long>(d.d), static_cast<long long>(d.d_ff),
+                                static_cast<long long>(d.d_r), extra_width});
+  return T * w * 2 < kGemmSpan && 2LL * d.d_ff * d.d < kGemmSpan && 2LL * d.d_r * d.d < kGemmSpan;
+}
+
 int check_dims(const hero_dims* d) {
   if (!d) return HERO_E_NULL;
   if (d->dtype != HERO_F32 && d->dtype != HERO_BF16) return HERO_E_DTYPE;
@@ -413,6 +424,7 @@ int check_layer_call(const hero_dims* dims, int j, int T, const void* hbar, cons
   int st = check_dims(dims);
   if (st != HERO_OK) return st;
   if (T <= 0) return HERO_E_DIM;
+  if (!fwd_fits(*dims, T)) return HERO_E_UNSUPPORTED;
   if (j < 1 || j > dims->L_R) return HERO_E_RANGE;
   if (!hbar || !h_out) return HERO_E_NULL;
   if (j >= 2 && !hbar_prev1) return HERO_E_NULL;
@@ -489,6 +501,7 @@ int routed_stack(const hero_dims* dims, int T, const void* h_in, void* h_out, co
   int st = check_dims(dims);
   if (st != HERO_OK) return st;
   if (T <= 0) return HERO_E_DIM;
+  if (!fwd_fits(*dims, T)) return HERO_E_UNSUPPORTED;
   if (!h_in || !h_out || !ffn || !adapter || !eta) return HERO_E_NULL;
   if (!aligned16(h_in) || !aligned16(h_out)) return HERO_E_ALIGN;
   if (history) {
@@ -591,6 +604,19 @@ int check_attn_dims(const hero_dims* d, const hero_attn_dims* a) {
   if (a->n_heads <= 0 || a->n_kv_heads <= 0 || a->head_dim <= 0) return HERO_E_DIM;
   if (a->n_heads % a->n_kv_heads) return HERO_E_DIM;
   if (d->dtype != HERO_BF16 || a->head_dim != kAttnHeadDim || a->n_heads % 2) return HERO_E_UNSUPPORTED;
+  return HERO_OK;
+}
+
+// token count and the spans of the attention products' operands (x [T][d], o [T][n_h hd],
+// W_qkv [(n_h + 2 n_kv) hd][d], W_o [d][n_h hd]) on the GEMM core
+int check_dec_size(const hero_dims& d, const hero_attn_dims& a, int batch, int seq) {
+  if (batch <= 0 || seq <= 0) return HERO_E_DIM;
+  const long long T = static_cast<long long>(batch) * seq;
+  if (T > INT_MAX / 2) return HERO_E_DIM;
+  const long long q_width = static_cast<long long>(a.n_heads) * a.head_dim;
+  const long long qkv_rows = static_cast<long long>(a.n_heads + 2 * a.n_kv_heads) * a.head_dim;
+  if (!fwd_fits(d, T, q_width) || 2 * qkv_rows * d.d >= kGemmSpan || 2 * q_width * d.d >= kGemmSpan)
+    return HERO_E_UNSUPPORTED;
   return HERO_OK;
 }
 
@@ -711,8 +737,8 @@ int hero_decoder_workspace_size(const hero_dims* dims, const hero_attn_dims* adi
   int st = check_dims(dims);
   if (st != HERO_OK) return st;
   if ((st = check_attn_dims(dims, adims)) != HERO_OK) return st;
-  if (batch <= 0 || seq <= 0 || n_layers < 0) return HERO_E_DIM;
-  if (static_cast<long long>(batch) * seq > INT_MAX / 2) return HERO_E_DIM;
+  if (n_layers < 0) return HERO_E_DIM;
+  if ((st = check_dec_size(*dims, *adims, batch, seq)) != HERO_OK) return st;
   *bytes = dec_layout_of(*dims, *adims, n_layers, batch, seq).total;
   return HERO_OK;
 }
@@ -723,8 +749,7 @@ int hero_attention_block(const hero_dims* dims, const hero_attn_dims* adims, int
   int st = check_dims(dims);
   if (st != HERO_OK) return st;
   if ((st = check_attn_dims(dims, adims)) != HERO_OK) return st;
-  if (batch <= 0 || seq <= 0) return HERO_E_DIM;
-  if (static_cast<long long>(batch) * seq > INT_MAX / 2) return HERO_E_DIM;
+  if ((st = check_dec_size(*dims, *adims, batch, seq)) != HERO_OK) return st;
   if (!h || !hbar) return HERO_E_NULL;
   if (!aligned16(h) || !aligned16(hbar)) return HERO_E_ALIGN;
   if ((st = check_attn_weights(attn)) != HERO_OK) return st;
@@ -752,8 +777,7 @@ int hero_decoder_stack(const hero_dims* dims, const hero_attn_dims* adims, int n
   int st = check_dims(dims);
   if (st != HERO_OK) return st;
   if ((st = check_attn_dims(dims, adims)) != HERO_OK) return st;
-  if (batch <= 0 || seq <= 0) return HERO_E_DIM;
-  if (static_cast<long long>(batch) * seq > INT_MAX / 2) return HERO_E_DIM;
+  if ((st = check_dec_size(*dims, *adims, batch, seq)) != HERO_OK) return st;
   if (n_layers < dims->L_R) return HERO_E_RANGE;
   if (!h_in || !h_out || !attn || !ffn || !adapter || !eta || !router) return HERO_E_NULL;
   if (!aligned16(h_in) || !aligned16(h_out)) return HERO_E_ALIGN;

@@ -183,6 +183,30 @@ def test_stack_validation():
     assert call(h_out=FAKE + (8 << 30) + 4096) == H.HERO_E_ALIAS
 
 
+def test_operand_spans_past_32_bit_offsets_are_rejected():
+    """The bf16 GEMM core addresses operand rows with 32-bit byte offsets: the layer, the stack and
+    the decoder entry points reject shapes where an operand would span 4 GiB or more, before any
+    other use of their arguments."""
+    dims = good_dims(d=256, d_ff=1 << 16)          # act rows: T x 65536 x 2 B, 4 GiB at T = 32768
+    assert call_layer(dims, T=32768) == H.HERO_E_UNSUPPORTED
+    assert call_layer(dims, T=32767, ws=None) == H.HERO_E_WORKSPACE   # passes on to the next check
+    assert call_layer(good_dims(d=4096, d_ff=1 << 19), T=1) == H.HERO_E_UNSUPPORTED   # 4 GiB of W_g
+    # the fp32 path addresses rows with 64-bit offsets
+    d32 = good_dims(H.HERO_F32, d=256, d_ff=1 << 16)
+    assert call_layer(d32, T=32768, ws=None) == H.HERO_E_WORKSPACE
+    ffn, ad, rt, st = fake_structs(dims.L_R)
+    rc = H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.3, None)
+    assert H.hero_routed_stack(dims, 32768, FAKE, FAKE + (1 << 40), st, ffn, rt, ad, [3.9] * dims.L_R,
+                               rc, None, None, 0, None) == H.HERO_E_UNSUPPORTED
+    # decoder: the attention output [T][n_h x 128] of 64 heads spans 4 GiB at T = 262144
+    out = ctypes.c_size_t(0)
+    adims = H.hero_attn_dims(64, 8, 128)
+    ws = lambda b, s: H.lib().hero_decoder_workspace_size(ctypes.byref(good_dims(L_R=2)), ctypes.byref(adims),
+                                                          4, b, s, ctypes.byref(out))
+    assert ws(2, 131072) == H.HERO_E_UNSUPPORTED
+    assert ws(2, 131071) == H.HERO_OK
+
+
 def test_workspace_size_monotone_and_stack_larger():
     dims = good_dims()
     a = H.hero_workspace_size(dims, 100, False)
