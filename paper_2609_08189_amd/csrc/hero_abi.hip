@@ -8,6 +8,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <new>
 
 #include "../../include/hero.h"
 #include "hero_kernels.h"
@@ -394,8 +395,15 @@ int hero_kernel_timer(int kernel, void* const* start_events, void* const* stop_e
   k.start = k.stop = nullptr;
   k.n = k.next = 0;
   if (n_slots == 0) return HERO_OK;
-  k.start = new hipEvent_t[n_slots];
-  k.stop = new hipEvent_t[n_slots];
+  // no exception may leave the C interface: a registry too large to allocate is out of range
+  k.start = new (std::nothrow) hipEvent_t[n_slots];
+  k.stop = new (std::nothrow) hipEvent_t[n_slots];
+  if (!k.start || !k.stop) {
+    delete[] k.start;
+    delete[] k.stop;
+    k.start = k.stop = nullptr;
+    return HERO_E_RANGE;
+  }
   for (int i = 0; i < n_slots; ++i) {
     k.start[i] = static_cast<hipEvent_t>(start_events[i]);
     k.stop[i] = static_cast<hipEvent_t>(stop_events[i]);
