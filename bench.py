@@ -111,22 +111,31 @@ def cpu_baseline(prob, gpu_stats, j, target_s=12.0, max_tokens=None):
     hb = prob.hbar.f64
     hp1 = prob.hbar_prev1.f64 if prob.hbar_prev1 is not None else None
     hp2 = prob.hbar_prev2.f64 if prob.hbar_prev2 is not None else None
-    n = 64
-    while True:
-        rows = np.linspace(0, T - 1, n).astype(np.int64)
+    lam = gpu_stats["lam"] if w.mode == "budget" else None
+
+    def run(rows):
         st = O.State(prob.S[rows].astype("f8"), prob.zeta[rows].astype("f8"),
                      prob.p_hist[rows].astype("f8"), prob.m_hist[rows].astype("f8"))
         beta = None if prob.beta is None else prob.beta[rows].astype("f8")
-        lam = gpu_stats["lam"] if w.mode == "budget" else None
         t0 = time.perf_counter()
         O.routed_layer(j, dims, hb[rows], None if hp1 is None else hp1[rows],
                        None if hp2 is None else hp2[rows], st, F, R, A, float(prob.eta[j - 1]),
                        mode=w.mode, budget=w.budget, tau=w.tau, beta=beta,
                        forced_ffn=gpu_stats["mask"][rows], lam_given=lam)
-        dt = time.perf_counter() - t0
+        return time.perf_counter() - t0
+
+    n = 64
+    while True:
+        rows = np.linspace(0, T - 1, n).astype(np.int64)
+        dt = run(rows)
         if dt >= target_s or n >= max_tokens:
             break
         n = min(max_tokens, max(2 * n, int(n * target_s / max(dt, 1e-3) * 1.1)))
+    # the whole call took less than the target: repeat it (up to 8 runs in all) for a steadier rate
+    reps = 1
+    while dt < target_s and reps < 8:
+        dt += run(rows)
+        reps += 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     cpu_model = "unknown"
     try:
@@ -134,10 +143,11 @@ def cpu_baseline(prob, gpu_stats, j, target_s=12.0, max_tokens=None):
             cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), cpu_model)
     except OSError:
         pass
-    return {"value": n / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+    return {"value": n * reps / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "nproc": os.cpu_count(), "omp_num_threads": os.environ.get("OMP_NUM_THREADS"), "cpu_model": cpu_model,
             "sample": f"{n} of {T} tokens of the same layer call (router, memory, branch; float64 numpy, "
-                      f"branch decisions teacher-forced to the GPU's), {dt:.1f} s"}
+                      f"branch decisions teacher-forced to the GPU's)" +
+                      (f", run {reps} times" if reps > 1 else "") + f", {dt:.1f} s"}
 
 
 COUNTERS_MD = os.path.join(ROOT, "profiles", "routed_layer_llama31_8b_hbm_counters.md")
@@ -526,6 +536,53 @@ def bench_backward(args, w):
     print(json.dumps(result), flush=True)
 
 
+# the paper's two Llama-3.1-8B operating points (Table 1: 26.87 % and 38.82 % skip)
+PAPER_SKIPS = (0.2687, 0.3882)
+
+
+def other_skip_point(dp, stats, w, j, budget, K, warmup):
+    """One more layer measurement at another skip budget on the same device problem (the inputs
+    do not depend on the budget; only the call's routing argument changes): tokens/s, the step time
+    and the dominant kernel's roofline fraction (HIP events on the call's stream)."""
+    import torch
+    from paper_2609_08189_amd import hero as H
+    saved_budget, saved_stats = dp.routing_s.budget, dp.stats
+    dp.routing_s.budget = budget
+    try:
+        stream = dp.stream()
+        ev = HipEvents()
+        dp.stats = stats
+        dp.run_layer(j)
+        torch.cuda.synchronize()
+        st = dp.stats[0].host()
+        dp.stats = None
+        for _ in range(warmup):
+            dp.run_layer(j)
+        dom = "ffn_gate_up"
+        ks, ke = ev.create(K), ev.create(K)
+        t0, t1 = ev.create(2)
+        H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
+        torch.cuda.synchronize()
+        ev.record(t0, stream)
+        for _ in range(K):
+            dp.run_layer(j)
+        ev.record(t1, stream)
+        torch.cuda.synchronize()
+        H.hero_kernel_timer(H.HERO_K[dom], [], [])
+        ms = ev.elapsed_ms(t0, t1) / K
+        dom_us = 1000.0 * sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
+        ev.destroy(ks + ke + [t0, t1])
+    finally:
+        dp.routing_s.budget, dp.stats = saved_budget, saved_stats
+    wb = w.replace(budget=budget)
+    fl = kernel_work(wb, st["n_ffn"], st["n_ad"], wb.T, j)[dom]["flops"]
+    peak = PEAK_BF16_TFLOPS if wb.dtype == "bf16" else PEAK_F32_TFLOPS
+    return {"budget": budget, "value": round(wb.T / (ms * 1e-3), 1), "unit": "tokens/s",
+            "ms_per_step": round(ms, 4), "steps": K, "n_ffn": st["n_ffn"], "n_adapter": st["n_ad"],
+            "ffn_gate_up_us": round(dom_us, 2),
+            "ffn_gate_up_frac": round(fl / (dom_us * 1e-6) * 1e-12 / peak, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -719,6 +776,12 @@ def main():
         "whole_call": ideal_fraction(works, ms_step, w.dtype, stack),
         "kernels": per,
     }
+    # the paper's other operating point, when the default layer workload runs at one of them
+    others = [b for b in PAPER_SKIPS if abs(b - w.budget) > 1e-6]
+    if (not stack and w.mode == "budget" and args.budget is None and args.workload == "llama31_8b_layer"
+            and not args.graph and args.memory == "matrix" and others):
+        print(f"# timing the layer at skip budget {others[0]}", file=sys.stderr, flush=True)
+        result["other_skip"] = other_skip_point(dp, stats_saved, w, j, others[0], K, args.warmup)
     if not args.no_cpu_baseline and not stack:
         dp.stats = stats_saved
         print("# timing the CPU oracle on a token sample", file=sys.stderr, flush=True)

@@ -70,3 +70,31 @@ def test_graph_flag_and_backward_flag_parse():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--help"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 0 and "--graph" in r.stdout and "--backward" in r.stdout
+
+
+def test_both_paper_skip_points_are_reported():
+    """The default layer workload runs at one of the paper's two Llama-3.1-8B operating points
+    (Table 1: 26.87 % and 38.82 % skip); the bench line adds the other as `other_skip`."""
+    from paper_2609_08189_amd import synth
+    assert bench.PAPER_SKIPS == (0.2687, 0.3882)
+    w = synth.WORKLOADS["llama31_8b_layer"]
+    assert w.mode == "budget" and w.budget in bench.PAPER_SKIPS
+    assert [b for b in bench.PAPER_SKIPS if abs(b - w.budget) > 1e-6] == [0.3882]
+
+
+def test_cpu_baseline_repeats_a_short_whole_call():
+    """On a call shorter than the time target the oracle baseline covers every token and repeats
+    the whole call (at most 8 runs); the rate is tokens x runs over the summed time."""
+    from paper_2609_08189_amd import synth
+    from oracle import hero_oracle as O
+    from tests.oracle_inputs import adapter_of, dims_of, ffn_of, router_of
+    w = synth.WORKLOADS["tiny_f32_stack"].replace(layer_j=3)
+    prob = synth.make_problem(w, seed=1, layer_j=3)
+    st = O.State(prob.S.astype("f8"), prob.zeta.astype("f8"), prob.p_hist.astype("f8"),
+                 prob.m_hist.astype("f8"))
+    ref = O.routed_layer(3, dims_of(w), prob.hbar.f64, prob.hbar_prev1.f64, prob.hbar_prev2.f64, st,
+                         ffn_of(prob.ffn[0]), router_of(prob), adapter_of(prob.adapter[0]),
+                         float(prob.eta[2]), mode=w.mode, budget=w.budget)
+    r = bench.cpu_baseline(prob, {"mask": ref.use_ffn, "lam": ref.lam}, 3, target_s=30.0)
+    assert r["kind"] == "oracle" and r["value"] > 0
+    assert r["sample"].startswith(f"{w.T} of {w.T} tokens") and "run 8 times" in r["sample"]
