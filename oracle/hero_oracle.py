@@ -47,7 +47,11 @@ constant here):
     logit is the local one), writes p = m = 1 and leaves S, zeta as they came in;
   * the training-side backward (last section) holds the branch decision fixed, gives the
     frozen backbone no gradient, hands the router dL/dlogit = dL/dg g (1 - g), and takes
-    the utilisation penalty over the first T - 1 positions of each sequence.
+    the utilisation penalty over the first T - 1 positions of each sequence;
+  * the router's backward through the stack treats the initial state (S = 0, zeta = 0,
+    p = m = 1) and the depth features r, q_rem as constants, takes d_j = |delta_j| to have
+    zero gradient where delta_j = 0, and covers the full router with S in full precision
+    (no ablation bits, no bf16 S); the logit bias beta takes no gradient.
 """
 from __future__ import annotations
 
@@ -791,3 +795,232 @@ def skip_penalty(gates, batch, seq, alpha=1.0):
     value = alpha * float(np.sum(tot * tot)) / n
     grad[:, :, : seq - 1] = (2.0 * alpha / n) * tot[None]
     return value, grad.reshape(gates.shape)
+
+
+# ---------------------------------------------------------------------------
+# Training side, continued: gradients reach the router through the gate scaling
+# (Sec. 3.1, the remark after eq:ffn_route), and the router's encoders, depth memory and
+# heads are trained with the adapters (Sec. 3.3, training objective).  Below: the routed
+# stack's backward with every routed layer's branch held fixed, by the chain rule through the
+# router equations of Sec. 3.2 in reverse order (gate <- heads <- memory read/write <- router
+# state <- encoders and path features), the memory carried backwards across depth.  float64
+# throughout, no rounding; the full router (no ablation) and S kept in full precision.
+# ---------------------------------------------------------------------------
+
+
+@dataclasses.dataclass
+class StackTrace:
+    hbars: List[np.ndarray]        # post-attention state entering routed layer j (index j - 1)
+    states: List[State]            # router state entering layer j (index j - 1)
+    layers: List[LayerResult]
+    h_out: np.ndarray
+
+
+def routed_stack_f64(dims: Dims, h_in, ffns: List[FFNParams], R: RouterParams,
+                     adapters: List[AdapterParams], etas, use_ffn, beta=None) -> StackTrace:
+    """The routed stack in float64 with no rounding at layer boundaries and each layer's branch
+    given (use_ffn: one bool [T] per layer): the function whose gradient routed_stack_backward
+    forms.  Same equations as routed_stack otherwise."""
+    if dims.state_dtype != "f32":
+        raise ValueError("the backward keeps S in full precision")
+    T = np.asarray(h_in).shape[0]
+    state = State.initial(T, dims.d_m)
+    hbar = np.asarray(h_in, dtype=f64)
+    hbars, states, layers = [], [], []
+    prev = [None, None]
+    for j in range(1, dims.L_R + 1):
+        hbars.append(hbar)
+        states.append(state)
+        res = routed_layer(j, dims, hbar, prev[0], prev[1], state, ffns[j - 1], R, adapters[j - 1],
+                           etas[j - 1], mode="threshold", beta=beta, forced_ffn=use_ffn[j - 1],
+                           round_output=False)
+        layers.append(res)
+        prev = [hbar, prev[0]]
+        state = res.state
+        hbar = res.h
+    return StackTrace(hbars, states, layers, hbar)
+
+
+@dataclasses.dataclass
+class StackGrad:
+    dh_in: np.ndarray                 # [T, d]
+    router: RouterParams              # dL/d(router weights), summed over tokens and layers
+    deta: np.ndarray                  # [L_R] dL/d eta_j
+    dw1: List[np.ndarray]             # per layer, dL/dW_1
+    dw2: List[np.ndarray]             # per layer, dL/dW_2
+    dlogit: List[np.ndarray]          # per layer, dL/dlogit [T]
+
+
+def phi_grad(x):
+    """d phi / dx: 1 for x > 0, exp(x) otherwise."""
+    x = np.asarray(x, dtype=f64)
+    return np.where(x > 0, 1.0, np.exp(np.minimum(x, 0.0)))
+
+
+def cosine_eps_backward(a, b, eps, dcos):
+    """Gradients over a and b of cos = <a, b> / (|a| |b| + eps) (row-wise), given dL/dcos [T]:
+    with N = <a, b> and D = |a| |b| + eps,
+      dcos/da = b / D - (N / D^2) |b| a / |a|   (the last term taken as 0 where a = 0),
+    and symmetrically for b."""
+    na = np.linalg.norm(a, axis=-1)
+    nb = np.linalg.norm(b, axis=-1)
+    N = np.sum(a * b, axis=-1)
+    D = na * nb + eps
+    ua = np.divide(a, na[:, None], out=np.zeros_like(a), where=na[:, None] > 0)
+    ub = np.divide(b, nb[:, None], out=np.zeros_like(b), where=nb[:, None] > 0)
+    k = (N / (D * D))[:, None]
+    da = dcos[:, None] * (b / D[:, None] - k * nb[:, None] * ua)
+    db = dcos[:, None] * (a / D[:, None] - k * na[:, None] * ub)
+    return da, db
+
+
+def _zero_router(R: RouterParams) -> RouterParams:
+    return RouterParams(**{f.name: np.zeros_like(np.asarray(getattr(R, f.name), dtype=f64))
+                           for f in dataclasses.fields(RouterParams)})
+
+
+def router_layer_backward(j, dims: Dims, hbar, hbar_prev1, hbar_prev2, state_in: State,
+                          res: LayerResult, R: RouterParams, dl, dS, dzeta, dp, dm, G: RouterParams):
+    """Reverse of the router at routed layer j (Sec. 3.2), given dL/dlogit and the gradients
+    over the state it hands on (S_j, zeta_j, p_j, m_j).  Adds the weight gradients into G and
+    returns (dhbar_j, dhbar_{j-1}, dhbar_{j-2}, dL/drho_j, dS_{j-1}, dzeta_{j-1}, dp_{j-1},
+    dm_{j-1}); entries for absent predecessors are None."""
+    dbg = res.debug
+    s, q, k, v, c, nu = dbg["s"], dbg["q"], dbg["k"], dbg["v"], dbg["c"], dbg["nu"]
+    rho = dbg["rho"]
+    p, m_prev, p_prev = res.state.p_hist, state_in.m_hist, state_in.p_hist
+    T = s.shape[0]
+    dl = np.asarray(dl, dtype=f64)
+    # gate logit ell = a + b (+ beta)
+    da = dl.copy()
+    db = dl.copy()
+    # cumulative history m_j = m_{j-1} p_j and p_j = sigma(a / T_hist)
+    dp_tot = dp + dm * m_prev
+    dm_prev = dm * p
+    da = da + dp_tot * p * (1.0 - p) / dims.T_hist
+    # local head b = f_psi(hbar)
+    pre_b = hbar @ R.ps1.T
+    G.ps2 += silu(pre_b).T @ db
+    dpre_b = db[:, None] * R.ps2[None, :] * silu_grad(pre_b)
+    G.ps1 += dpre_b.T @ hbar
+    dhbar = dpre_b @ R.ps1
+    # history head a = f_theta([s; c; nu])
+    x_th = np.concatenate([s, c, nu[:, None]], axis=-1)
+    pre_a = x_th @ R.th1.T
+    G.th2 += silu(pre_a).T @ da
+    dpre_a = da[:, None] * R.th2[None, :] * silu_grad(pre_a)
+    G.th1 += dpre_a.T @ x_th
+    dx_th = dpre_a @ R.th1
+    ds = dx_th[:, :dims.d_s].copy()
+    dc = dx_th[:, dims.d_s:dims.d_s + dims.d_m].copy()
+    dnu = dx_th[:, -1]
+    # history dissimilarity nu = 1 - cos(W_n s, W_c c) (a constant 0 at j = 1)
+    if j > 1:
+        du1, du2 = cosine_eps_backward(s @ R.w_n.T, c @ R.w_c.T, dims.eps, -dnu)
+        G.w_n += du1.T @ s
+        ds += du1 @ R.w_n
+        G.w_c += du2.T @ c
+        dc += du2 @ R.w_c
+    # memory write S_j = rho S_{j-1} + phi(k) v^T, zeta_j = rho zeta_{j-1} + phi(k)
+    S_prev, z_prev = state_in.S, state_in.zeta
+    fk = phi(k)
+    drho = float(np.sum(dS * S_prev) + np.sum(dzeta * z_prev))
+    dS_prev = rho * dS
+    dz_prev = rho * dzeta
+    dfk = np.einsum("tkv,tv->tk", dS, v) + dzeta
+    dv = np.einsum("tkv,tk->tv", dS, fk)
+    dk = dfk * phi_grad(k)
+    # memory read c = phi(q)^T S_{j-1} / (phi(q)^T zeta_{j-1} + eps), before the write
+    fq = phi(q)
+    den = np.sum(fq * z_prev, axis=-1) + dims.eps
+    dnum = dc / den[:, None]
+    dden = -np.sum(dc * c, axis=-1) / den
+    dfq = np.einsum("tkv,tv->tk", S_prev, dnum) + z_prev * dden[:, None]
+    dS_prev += fq[:, :, None] * dnum[:, None, :]
+    dz_prev += fq * dden[:, None]
+    dq = dfq * phi_grad(q)
+    # projections q, k, v = W s
+    G.w_q += dq.T @ s
+    G.w_k += dk.T @ s
+    G.w_v += dv.T @ s
+    ds += dq @ R.w_q + dk @ R.w_k + dv @ R.w_v
+    # router state s = [z^h; z^a]
+    dzh = ds[:, :dims.d_h]
+    dza = ds[:, dims.d_h:]
+    # path encoder z^a = FFN_path(x^path), x^path = [r, q_rem, d_j, gamma_j, p_{j-1}, m_{j-1}]
+    x_path = dbg["x_path"]
+    pre_p = x_path @ R.w_p1.T
+    G.w_p2 += dza.T @ silu(pre_p)
+    dpre_p = (dza @ R.w_p2) * silu_grad(pre_p)
+    G.w_p1 += dpre_p.T @ x_path
+    dx = dpre_p @ R.w_p1
+    dp_prev = dx[:, 4]
+    dm_prev = dm_prev + dx[:, 5]
+    # residual transitions delta_j = hbar_j - hbar_{j-1}: d_j = |delta_j| (j >= 2),
+    # gamma_j = cos(delta_j, delta_{j-1}) (j >= 3)
+    dh1 = dh2 = None
+    if j >= 2:
+        delta = hbar - hbar_prev1
+        nd = np.linalg.norm(delta, axis=-1)
+        ddelta = np.divide(dx[:, 2:3] * delta, nd[:, None], out=np.zeros_like(delta),
+                           where=nd[:, None] > 0)
+        dh1 = np.zeros_like(hbar)
+        if j >= 3:
+            delta_prev = hbar_prev1 - hbar_prev2
+            dd1, dd0 = cosine_eps_backward(delta, delta_prev, dims.eps, dx[:, 3])
+            ddelta += dd1
+            dh1 += dd0
+            dh2 = -dd0
+        dhbar += ddelta
+        dh1 -= ddelta
+    # hidden encoder z^h = W_hu SiLU(W_hd RMSNorm(hbar)) (unit gain)
+    hh = rmsnorm(hbar, None, dims.eps_norm)
+    pre_h = hh @ R.w_hd.T
+    G.w_hu += dzh.T @ silu(pre_h)
+    dpre_h = (dzh @ R.w_hu) * silu_grad(pre_h)
+    G.w_hd += dpre_h.T @ hh
+    dhbar += rmsnorm_backward(hbar, 1.0, dims.eps_norm, dpre_h @ R.w_hd)
+    return dhbar, dh1, dh2, drho, dS_prev, dz_prev, dp_prev, dm_prev
+
+
+def routed_stack_backward(dims: Dims, h_in, ffns: List[FFNParams], R: RouterParams,
+                          adapters: List[AdapterParams], etas, use_ffn, dh_out, dgates_in=None,
+                          beta=None) -> StackGrad:
+    """Gradients of J = <dh_out, h_{L_R}> + sum_j <dgates_in[j], g_j> through the routed stack
+    with every layer's branch fixed (routed_stack_f64 is the forward).  Layer by layer from the
+    last: the block's backward gives dL/dhbar_j and dL/dlogit_j; the router's backward turns
+    dL/dlogit_j and the gradients over the state it handed on into its weight gradients, the
+    post-attention states' share (hbar_j, and hbar_{j-1}, hbar_{j-2} through the residual
+    transitions) and the gradients over the state it received.  hbar_{j+1} = h_j, so dL/dh_j is
+    everything that reached hbar_{j+1}.  The initial state is a constant."""
+    tr = routed_stack_f64(dims, h_in, ffns, R, adapters, etas, use_ffn, beta)
+    L, T = dims.L_R, tr.h_out.shape[0]
+    dHB = [np.zeros((T, dims.d)) for _ in range(L + 2)]     # dHB[j]: dL/dhbar_j, j = 1 .. L + 1
+    dHB[L + 1] = np.asarray(dh_out, dtype=f64).copy()
+    G = _zero_router(R)
+    deta = np.zeros(L)
+    dw1, dw2, dlogits = [None] * L, [None] * L, [None] * L
+    dS = np.zeros((T, dims.d_m, dims.d_m))
+    dz = np.zeros((T, dims.d_m))
+    dp = np.zeros(T)
+    dm = np.zeros(T)
+    for j in range(L, 0, -1):
+        res = tr.layers[j - 1]
+        hbar = tr.hbars[j - 1]
+        dgi = None if dgates_in is None else dgates_in[j - 1]
+        bg = routed_block_backward(hbar, res.gate, use_ffn[j - 1], ffns[j - 1], adapters[j - 1], dims,
+                                   dHB[j + 1], dgi)
+        dHB[j] += bg.dhbar
+        dw1[j - 1], dw2[j - 1], dlogits[j - 1] = bg.dw1, bg.dw2, bg.dlogit
+        h1 = tr.hbars[j - 2] if j >= 2 else None
+        h2 = tr.hbars[j - 3] if j >= 3 else None
+        dhb, dh1, dh2, drho, dS, dz, dp, dm = router_layer_backward(
+            j, dims, hbar, h1, h2, tr.states[j - 1], res, R, bg.dlogit, dS, dz, dp, dm, G)
+        dHB[j] += dhb
+        if dh1 is not None:
+            dHB[j - 1] += dh1
+        if dh2 is not None:
+            dHB[j - 2] += dh2
+        rho = res.debug["rho"]
+        deta[j - 1] = drho * rho * (1.0 - rho)
+    return StackGrad(dHB[1], G, deta, dw1, dw2, dlogits)
