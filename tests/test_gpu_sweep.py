@@ -1,0 +1,75 @@
+"""GPU parity of hero_routed_layer against the CPU oracle over a seeded random sweep of the shapes
+the library accepts: model and FFN widths, adapter ranks (register-tiled and wide), memory widths,
+the router's sub-network widths (d_h + d_a = d_s, d_e, d_p, d_head), layer index, token count
+(ragged, down to one), budget or threshold routing, and S stored in fp32 or bf16.
+
+The cases are drawn once on the host from a fixed seed, so the list is the same on every run; each
+is printed before it runs."""
+import numpy as np
+import pytest
+
+from paper_2609_08189_amd import synth
+from tests.test_gpu_layer import _run
+
+
+def _cases(n_bf16=10, n_f32=4, seed=20260):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n_bf16 + n_f32):
+        bf16 = i < n_bf16
+        if bf16:
+            d = int(rng.choice([256, 512, 768, 1024, 1280]))
+            d_ff = 128 * int(rng.integers(2, 25))
+            d_r = int(rng.choice([32, 64, 96, 128, 256, 384]))
+            d_e = int(rng.choice([64, 128, 192, 256]))
+            d_head = int(rng.choice([x for x in (64, 128, 192, 256) if (d_e + x) % 128 == 0]))
+            d_s = 8 * int(rng.integers(1, 17))
+        else:
+            d = int(rng.choice([128, 256, 384]))
+            d_ff = int(rng.integers(40, 700))
+            d_r = int(rng.integers(4, 80))
+            d_e = int(rng.integers(8, 257))
+            d_head = int(rng.integers(8, 257))
+            d_s = int(rng.integers(2, 129))
+        d_h = int(rng.integers(1, d_s))
+        d_m = int(rng.choice([32, 64, 128, 256]))
+        L_R = int(rng.integers(2, 13))
+        j = int(rng.integers(1, L_R + 1))
+        T = int(rng.integers(1, 1201)) if i % 3 else int(rng.integers(1, 40))
+        if i in (n_bf16 - 1, n_bf16 + n_f32 - 1):
+            T = 1                                   # one token per dtype
+        mode = "budget" if rng.uniform() < 0.6 else "threshold"
+        state = "bf16" if (d_m >= 64 and rng.uniform() < 0.3) else "f32"
+        w = synth.Workload(f"sweep{i}", "bf16" if bf16 else "f32", d=d, d_ff=d_ff, d_r=d_r, L_R=L_R, d_m=d_m,
+                           T=T, mode=mode, budget=float(rng.uniform()) if mode == "budget" else 0.0,
+                           tau=float(rng.choice([0.45, 0.5, 0.55])), d_s=d_s, d_h=d_h, d_a=d_s - d_h, d_e=d_e,
+                           d_p=int(rng.integers(4, 129)), d_head=d_head, state_dtype=state)
+        out.append((w, j, int(rng.integers(0, 1 << 16))))
+    return out
+
+
+CASES = _cases()
+
+
+def test_sweep_cases_are_valid_shapes():
+    """Every drawn case passes the library's host checks (no GPU work), and the sweep reaches
+    both dtypes, both routing modes, both state storages, wide adapter ranks and one-token calls."""
+    from paper_2609_08189_amd import hero as H
+    from paper_2609_08189_amd.device import dims_struct
+    for w, j, _ in CASES:
+        assert H.hero_workspace_size(dims_struct(w), w.T, False) > 0, w
+        assert 1 <= j <= w.L_R
+    assert {w.dtype for w, _, _ in CASES} == {"bf16", "f32"}
+    assert {w.mode for w, _, _ in CASES} == {"budget", "threshold"}
+    assert {w.state_dtype for w, _, _ in CASES} == {"f32", "bf16"}
+    assert any(w.d_r > 128 for w, _, _ in CASES if w.dtype == "bf16")
+    assert {w.dtype for w, _, _ in CASES if w.T == 1} == {"bf16", "f32"}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("k", range(len(CASES)))
+def test_layer_sweep(k):
+    w, j, seed = CASES[k]
+    print(f"sweep case {k}: d_s={w.d_s} d_h={w.d_h} d_e={w.d_e} d_p={w.d_p} d_head={w.d_head} "
+          f"d_r={w.d_r} L_R={w.L_R} state={w.state_dtype} budget={w.budget:.3f} tau={w.tau}", flush=True)
+    _run(w, j, seed=seed)
