@@ -73,3 +73,47 @@ def test_layer_sweep(k):
     print(f"sweep case {k}: d_s={w.d_s} d_h={w.d_h} d_e={w.d_e} d_p={w.d_p} d_head={w.d_head} "
           f"d_r={w.d_r} L_R={w.L_R} state={w.state_dtype} budget={w.budget:.3f} tau={w.tau}", flush=True)
     _run(w, j, seed=seed)
+
+
+def _bwd_cases(n_bf16=7, n_f32=3, seed=20261):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n_bf16 + n_f32):
+        bf16 = i < n_bf16
+        if bf16:
+            d = int(rng.choice([256, 512, 768, 1024, 1280]))
+            d_ff = 128 * int(rng.integers(2, 25))
+            d_r = int(rng.choice([32, 64, 96, 128, 256, 384]))
+        else:
+            d = int(rng.choice([128, 256, 384]))
+            d_ff = int(rng.integers(40, 700))
+            d_r = int(rng.integers(4, 80))
+        T = 1 if i in (0, n_bf16) else int(rng.integers(2, 1500))
+        w = synth.Workload(f"bwd_sweep{i}", "bf16" if bf16 else "f32", d=d, d_ff=d_ff, d_r=d_r, L_R=4,
+                           d_m=64, T=T, mode="budget", budget=float(rng.uniform()))
+        out.append((w, int(rng.integers(0, 1 << 16)), bool(rng.uniform() < 0.5), bool(rng.uniform() < 0.5)))
+    return out
+
+
+BWD_CASES = _bwd_cases()
+
+
+def test_backward_sweep_cases_are_valid_shapes():
+    from paper_2609_08189_amd import hero as H
+    from paper_2609_08189_amd.device import dims_struct
+    import ctypes
+    for w, _, _, _ in BWD_CASES:
+        out = ctypes.c_size_t(0)
+        assert H.lib().hero_backward_workspace_size(ctypes.byref(dims_struct(w)), w.T,
+                                                    ctypes.byref(out)) == H.HERO_OK, w
+    assert {w.dtype for w, *_ in BWD_CASES} == {"bf16", "f32"}
+    assert any(bm for *_, bm in BWD_CASES) and not all(bm for *_, bm in BWD_CASES)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("k", range(len(BWD_CASES)))
+def test_block_backward_sweep(k):
+    from tests.test_gpu_backward import _run_small
+    w, seed, gin, bm = BWD_CASES[k]
+    print(f"backward sweep case {k}", flush=True)
+    _run_small(w, seed, dgate_in=gin, budget_mode=bm)
