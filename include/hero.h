@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define HERO_ABI_VERSION 5
+#define HERO_ABI_VERSION 6
 
 typedef enum hero_status {
   HERO_OK = 0,
@@ -213,7 +213,12 @@ typedef enum hero_kernel {
   HERO_K_BWD_ADAPTER_WGRAD = 19, /* dW_1, dW_2                                                  */
   HERO_K_BWD_ROWS = 20,     /* dL/dhbar (RMSNorm backward + residual), dL/dg, dL/dlogit          */
   HERO_K_SKIP_PENALTY = 21, /* alpha L_skip and its gradient                                    */
-  HERO_K_COUNT = 22
+  /* backward of the router at one routed layer (hero_router_backward) */
+  HERO_K_ROUTER_BWD_GEMM = 22,     /* P = hbar [W_hd; psi_1]^T recomputed                         */
+  HERO_K_ROUTER_BWD_TOKEN = 23,    /* the router's forward recomputed and reversed, per token     */
+  HERO_K_ROUTER_BWD_PRODUCTS = 24, /* weight gradients (tokens as K) and dP [W_hd; psi_1]         */
+  HERO_K_ROUTER_BWD_ROWS = 25,     /* RMSNorm and transition terms of dL/dhbar; dL/deta           */
+  HERO_K_COUNT = 26
 } hero_kernel;
 
 /*
@@ -464,6 +469,46 @@ int hero_routed_block_backward(const hero_dims *dims, int T, const void *hbar, c
  */
 int hero_skip_penalty(int L_R, int batch, int seq, const float *gates, float alpha, float *loss,
                       float *dgates, void *stream);
+
+/* Gradients of the router weights (fp32, the shapes and row pitches of hero_router_weights,
+ * th1 with its padded pitch); hero_router_backward adds into them. */
+typedef struct hero_router_grads {
+  float *w_hd, *w_hu, *w_p1, *w_p2, *w_q, *w_k, *w_v, *w_n, *w_c, *th1, *th2, *ps1, *ps2;
+} hero_router_grads;
+
+/* The gradient over the router state carried backwards across routed layers (fp32, in place):
+ * on entry dL/dS_j [T][d_m][d_m], dL/dzeta_j [T][d_m], dL/dp_j [T], dL/dm_j [T] for the state
+ * routed layer j hands on (zeros at the last layer); on return the same for the state it
+ * received (S_{j-1}, zeta_{j-1}, p_{j-1}, m_{j-1}). */
+typedef struct hero_router_carry {
+  float *dS, *dzeta, *dp, *dm;
+} hero_router_carry;
+
+/* Workspace bytes for hero_router_backward with T tokens.  Host-only; validates dims. */
+int hero_router_backward_workspace_size(const hero_dims *dims, int T, size_t *bytes);
+
+/*
+ * Backward of the router at routed layer j (Sec. 3.2 in reverse order; the gradient reaches
+ * the router through the gate scaling, Sec. 3.1 remark after eq:ffn_route).  Given dL/dlogit
+ * (e.g. hero_routed_block_backward's) and the carried state gradient, it
+ *   - adds dL/d(router weights) into grads (the weights are shared by every routed layer, so a
+ *     caller sums them over layers by calling for j = L_R .. 1 on the same buffers);
+ *   - adds the post-attention states' share into dhbar (hbar_j: hidden encoder, local head,
+ *     residual transitions), dhbar_prev1 (hbar_{j-1}, j >= 2) and dhbar_prev2 (hbar_{j-2},
+ *     j >= 3): fp32 [T][d], three distinct buffers;
+ *   - writes dL/deta_j into deta[0] (device fp32; rho_j = sigma(eta));
+ *   - turns carry into the gradient over the state the layer received.
+ * state_in is the router state entering layer j (fp32 S, zeta, p, m as the forward call read
+ * them; ignored at j = 1, where the state is the initial one and carry's return is rho dL/dS_1).
+ * hbar_prev1 / hbar_prev2: as in hero_routed_layer.  The full router with S in fp32
+ * (dims->state_dtype HERO_F32, else HERO_E_UNSUPPORTED); branch decisions are constants.
+ * Deterministic: every sum runs in a fixed order.
+ */
+int hero_router_backward(const hero_dims *dims, int j, int T, const void *hbar, const void *hbar_prev1,
+                         const void *hbar_prev2, const hero_state *state_in, const hero_router_weights *router,
+                         float eta, const float *dlogit, const hero_router_carry *carry, float *dhbar,
+                         float *dhbar_prev1, float *dhbar_prev2, const hero_router_grads *grads, float *deta,
+                         void *workspace, size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

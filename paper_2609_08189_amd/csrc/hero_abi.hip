@@ -1115,3 +1115,222 @@ int hero_skip_penalty(int L_R, int batch, int seq, const float* gates, float alp
              ? HERO_OK
              : HERO_E_LAUNCH;
 }
+
+// ---------------------------------------------------------------------------
+// Backward of the router at one routed layer
+// ---------------------------------------------------------------------------
+namespace {
+
+struct RouterBwdLayout {
+  size_t P, dP, dPT, rowcoef, rho_part, vec, hbT, wT, total;
+};
+
+RouterBwdLayout router_bwd_layout_of(const hero_dims& d, int T) {
+  RouterBwdLayout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + 255) & ~static_cast<size_t>(255);
+    return at;
+  };
+  const size_t t = static_cast<size_t>(T), np = static_cast<size_t>(d.d_e + d.d_head);
+  L.P = take(t * np * 4 * hero::router_gemm_splits(d.dtype, d.d));
+  L.dP = take(t * np * 4);
+  L.dPT = take(np * t * 4);
+  L.rowcoef = take(t * 8 * 4);
+  L.rho_part = take(t * 4);
+  L.vec = take(hero::router_bwd_vector_floats(d.d_m, d.d_s, d.d_h, d.d_a, d.d_e, d.d_p, d.d_head) * t * 4);
+  L.hbT = take(static_cast<size_t>(d.d) * t * 4);
+  L.wT = take(static_cast<size_t>(d.d) * np * 4);
+  L.total = off;
+  return L;
+}
+
+int check_router(const hero_router_weights* r) {
+  if (!r) return HERO_E_NULL;
+  const void* p[] = {r->w_hd, r->w_hu, r->w_p1, r->w_p2, r->w_q, r->w_k, r->w_v,
+                     r->w_n, r->w_c, r->th1, r->th2, r->ps1, r->ps2};
+  for (const void* x : p)
+    if (!x) return HERO_E_NULL;
+  for (const void* x : p)
+    if (!aligned16(x)) return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+}  // namespace
+
+int hero_router_backward_workspace_size(const hero_dims* dims, int T, size_t* bytes) {
+  if (!bytes) return HERO_E_NULL;
+  const int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if (T <= 0) return HERO_E_DIM;
+  *bytes = router_bwd_layout_of(*dims, T).total;
+  return HERO_OK;
+}
+
+int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, const void* hbar_prev1,
+                         const void* hbar_prev2, const hero_state* state_in, const hero_router_weights* router,
+                         float eta, const float* dlogit, const hero_router_carry* carry, float* dhbar,
+                         float* dhbar_prev1, float* dhbar_prev2, const hero_router_grads* grads, float* deta,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if (T <= 0) return HERO_E_DIM;
+  if (j < 1 || j > dims->L_R) return HERO_E_RANGE;
+  if (dims->state_dtype != HERO_F32 || !fwd_fits(*dims, T)) return HERO_E_UNSUPPORTED;
+  if (!(eta == eta)) return HERO_E_RANGE;
+  if (!hbar || !dlogit || !carry || !dhbar || !grads || !deta) return HERO_E_NULL;
+  if ((j >= 2 && (!hbar_prev1 || !dhbar_prev1)) || (j >= 3 && (!hbar_prev2 || !dhbar_prev2))) return HERO_E_NULL;
+  if ((st = check_state(state_in)) != HERO_OK) return st;
+  if ((st = check_router(router)) != HERO_OK) return st;
+  const float* gp[] = {grads->w_hd, grads->w_hu, grads->w_p1, grads->w_p2, grads->w_q, grads->w_k, grads->w_v,
+                       grads->w_n, grads->w_c, grads->th1, grads->th2, grads->ps1, grads->ps2};
+  for (const float* x : gp)
+    if (!x) return HERO_E_NULL;
+  if (!carry->dS || !carry->dzeta || !carry->dp || !carry->dm) return HERO_E_NULL;
+  const void* al[] = {hbar, j >= 2 ? hbar_prev1 : nullptr, j >= 3 ? hbar_prev2 : nullptr, dlogit, carry->dS,
+                      carry->dzeta, carry->dp, carry->dm, dhbar, j >= 2 ? dhbar_prev1 : nullptr,
+                      j >= 3 ? dhbar_prev2 : nullptr, deta, workspace};
+  for (const void* x : al)
+    if (x && !aligned16(x)) return HERO_E_ALIGN;
+  for (const float* x : gp)
+    if (!aligned16(x)) return HERO_E_ALIGN;
+  const hero_dims& D = *dims;
+  const size_t t = static_cast<size_t>(T), dm = static_cast<size_t>(D.d_m);
+  const size_t hb = t * D.d * 4, sb = t * dm * dm * 4, zb = t * dm * 4, tb = t * 4;
+  float* outs[] = {dhbar, j >= 2 ? dhbar_prev1 : nullptr, j >= 3 ? dhbar_prev2 : nullptr};
+  for (int a = 0; a < 3; ++a)
+    for (int b = a + 1; b < 3; ++b)
+      if (overlap(outs[a], hb, outs[b], hb)) return HERO_E_ALIAS;
+  // the memory pass reads S_{j-1} while it writes dL/dS_{j-1} over dL/dS_j
+  if (j > 1 && (overlap(carry->dS, sb, state_in->S, sb) || overlap(carry->dzeta, zb, state_in->zeta, zb)))
+    return HERO_E_ALIAS;
+  const RouterBwdLayout L = router_bwd_layout_of(D, T);
+  if (!workspace || workspace_bytes < L.total) return HERO_E_WORKSPACE;
+  const void* in_out[][2] = {{carry->dS, reinterpret_cast<const void*>(sb)},
+                             {carry->dzeta, reinterpret_cast<const void*>(zb)},
+                             {carry->dp, reinterpret_cast<const void*>(tb)},
+                             {carry->dm, reinterpret_cast<const void*>(tb)},
+                             {dhbar, reinterpret_cast<const void*>(hb)},
+                             {j >= 2 ? dhbar_prev1 : nullptr, reinterpret_cast<const void*>(hb)},
+                             {j >= 3 ? dhbar_prev2 : nullptr, reinterpret_cast<const void*>(hb)},
+                             {deta, reinterpret_cast<const void*>(static_cast<size_t>(4))}};
+  for (const auto& x : in_out)
+    if (overlap(workspace, L.total, x[0], reinterpret_cast<size_t>(x[1]))) return HERO_E_ALIAS;
+  if ((st = check_device()) != HERO_OK) return st;
+
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  const int NP = D.d_e + D.d_head, dx = D.d_s + D.d_m + 1, ld_th1 = HERO_TH1_PITCH(D.d_s, D.d_m);
+  hero::RouterBwdArgs a{};
+  a.dtype = D.dtype;
+  a.T = T;
+  a.j = j;
+  a.L_R = D.L_R;
+  a.d = D.d;
+  a.d_m = D.d_m;
+  a.d_s = D.d_s;
+  a.d_h = D.d_h;
+  a.d_a = D.d_a;
+  a.d_e = D.d_e;
+  a.d_p = D.d_p;
+  a.d_head = D.d_head;
+  a.ld_th1 = ld_th1;
+  a.eps_norm = D.eps_norm;
+  a.eps = D.eps;
+  a.T_hist = D.T_hist;
+  a.rho = 1.0f / (1.0f + expf(-eta));
+  a.hbar = hbar;
+  a.prev1 = hbar_prev1;
+  a.prev2 = hbar_prev2;
+  a.P = reinterpret_cast<float*>(ws + L.P);
+  a.p_splits = hero::router_gemm_splits(D.dtype, D.d);
+  a.w_hu = router->w_hu;
+  a.w_p1 = router->w_p1;
+  a.w_p2 = router->w_p2;
+  a.w_q = router->w_q;
+  a.w_k = router->w_k;
+  a.w_v = router->w_v;
+  a.w_n = router->w_n;
+  a.w_c = router->w_c;
+  a.th1 = router->th1;
+  a.th2 = router->th2;
+  a.ps2 = router->ps2;
+  a.S_in = static_cast<const float*>(state_in->S);
+  a.zeta_in = state_in->zeta;
+  a.p_in = state_in->p_hist;
+  a.m_in = state_in->m_hist;
+  a.dlogit = dlogit;
+  a.dS = carry->dS;
+  a.dzeta = carry->dzeta;
+  a.dp = carry->dp;
+  a.dm = carry->dm;
+  a.dP = reinterpret_cast<float*>(ws + L.dP);
+  a.dPT = reinterpret_cast<float*>(ws + L.dPT);
+  a.rowcoef = reinterpret_cast<float*>(ws + L.rowcoef);
+  a.rho_part = reinterpret_cast<float*>(ws + L.rho_part);
+  float* v = reinterpret_cast<float*>(ws + L.vec);
+  auto rows = [&](int n) {
+    float* at = v;
+    v += static_cast<size_t>(n) * T;
+    return at;
+  };
+  a.XT = rows(dx);
+  a.dQT = rows(D.d_m);
+  a.dKT = rows(D.d_m);
+  a.dVT = rows(D.d_m);
+  a.dU1T = rows(D.d_m);
+  a.dU2T = rows(D.d_m);
+  a.dPAT = rows(D.d_head);
+  a.SAT = rows(D.d_head);
+  a.DA = rows(1);
+  a.DB = rows(1);
+  a.SBT = rows(D.d_head);
+  a.dPPT = rows(D.d_p);
+  a.SPT = rows(D.d_p);
+  a.XPT = rows(8);
+  a.dZAT = rows(D.d_a);
+  a.dZHT = rows(D.d_h);
+  a.SHT = rows(D.d_e);
+  a.dhbar = dhbar;
+  a.dhbar1 = dhbar_prev1;
+  a.dhbar2 = dhbar_prev2;
+  a.deta = deta;
+  float* hbT = reinterpret_cast<float*>(ws + L.hbT);
+  float* wT = reinterpret_cast<float*>(ws + L.wT);
+
+  hipError_t e = timed(HERO_K_ROUTER_BWD_GEMM, s, [&] {
+    return hero::launch_router_gemm(D.dtype, hbar, router->w_hd, router->ps1, T, D.d, D.d_e, D.d_head,
+                                     const_cast<float*>(a.P), s);
+  });
+  if (e == hipSuccess) e = timed(HERO_K_ROUTER_BWD_TOKEN, s, [&] { return hero::launch_router_bwd_token(a, s); });
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = timed(HERO_K_ROUTER_BWD_PRODUCTS, s, [&] {
+    // the weight gradients: products with the tokens as K (every operand token-contiguous)
+    auto acc = [&](const float* A, int M, const float* B, int N, float* C, int ldc) {
+      return hero::launch_gemm_acc_f32(A, T, M, B, T, N, T, C, ldc, s);
+    };
+    hipError_t x = hero::launch_to_f32_transpose(D.dtype, hbar, T, D.d, D.d, hbT, T, s);
+    if (x == hipSuccess) x = acc(a.dQT, D.d_m, a.XT, D.d_s, grads->w_q, D.d_s);
+    if (x == hipSuccess) x = acc(a.dKT, D.d_m, a.XT, D.d_s, grads->w_k, D.d_s);
+    if (x == hipSuccess) x = acc(a.dVT, D.d_m, a.XT, D.d_s, grads->w_v, D.d_s);
+    if (x == hipSuccess) x = acc(a.dU1T, D.d_m, a.XT, D.d_s, grads->w_n, D.d_s);
+    if (x == hipSuccess) x = acc(a.dU2T, D.d_m, a.XT + static_cast<size_t>(D.d_s) * T, D.d_m, grads->w_c, D.d_m);
+    if (x == hipSuccess) x = acc(a.dPAT, D.d_head, a.XT, dx, grads->th1, ld_th1);
+    if (x == hipSuccess) x = acc(a.SAT, D.d_head, a.DA, 1, grads->th2, 1);
+    if (x == hipSuccess) x = acc(a.SBT, D.d_head, a.DB, 1, grads->ps2, 1);
+    if (x == hipSuccess) x = acc(a.dPPT, D.d_p, a.XPT, 6, grads->w_p1, 6);
+    if (x == hipSuccess) x = acc(a.dZAT, D.d_a, a.SPT, D.d_p, grads->w_p2, D.d_p);
+    if (x == hipSuccess) x = acc(a.dZHT, D.d_h, a.SHT, D.d_e, grads->w_hu, D.d_e);
+    if (x == hipSuccess) x = acc(a.dPT, D.d_e, hbT, D.d, grads->w_hd, D.d);
+    if (x == hipSuccess) x = acc(a.dPT + static_cast<size_t>(D.d_e) * T, D.d_head, hbT, D.d, grads->ps1, D.d);
+    // the hidden encoder's and the local head's share of dL/dhbar_j: dP [W_hd; psi_1]
+    if (x == hipSuccess) x = hero::launch_to_f32_transpose(D.dtype, router->w_hd, D.d_e, D.d, D.d, wT, NP, s);
+    if (x == hipSuccess) x = hero::launch_to_f32_transpose(D.dtype, router->ps1, D.d_head, D.d, D.d, wT + D.d_e, NP, s);
+    if (x == hipSuccess) x = hero::launch_gemm_acc_f32(a.dP, NP, T, wT, NP, D.d, NP, dhbar, D.d, s);
+    return x;
+  });
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = timed(HERO_K_ROUTER_BWD_ROWS, s, [&] { return hero::launch_router_bwd_rows(a, s); });
+  return e == hipSuccess ? HERO_OK : HERO_E_LAUNCH;
+}

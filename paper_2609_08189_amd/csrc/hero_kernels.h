@@ -215,6 +215,38 @@ hipError_t launch_adapter_wgrad_stage(const BlockBwdArgs& a, int kp, void* uaT, 
 // C[m][n] = sum_k A[m][k] B[n][k] (bf16 A [M][K], B [N][K]; fp32 C with row pitch ldc); N % 128 == 0,
 // K % 64 == 0
 hipError_t launch_gemm_nt_f32(const void* A, int M, const void* B, int N, int K, float* C, int ldc, hipStream_t s);
+// C[m][n] += sum_k A[m][k] B[n][k] in fp32 (rows of A and B with leading dims lda, ldb)
+hipError_t launch_gemm_acc_f32(const float* A, int lda, int M, const float* B, int ldb, int N, int K, float* C,
+                               int ldc, hipStream_t s);
+
+// Backward of the router at routed layer j (k_router_bwd.hip).
+struct RouterBwdArgs {
+  int dtype, T, j, L_R, d, d_m, d_s, d_h, d_a, d_e, d_p, d_head, ld_th1;
+  float eps_norm, eps, T_hist, rho;
+  const void *hbar, *prev1, *prev2;          // [T][d]: hbar_j, hbar_{j-1} (j >= 2), hbar_{j-2} (j >= 3)
+  const float* P;                            // [p_splits][T][d_e + d_head] partial pre-activations
+  int p_splits;
+  const void *w_hu, *w_p1, *w_p2, *w_q, *w_k, *w_v, *w_n, *w_c, *th1, *th2, *ps2;
+  const float *S_in, *zeta_in, *p_in, *m_in; // the state entering layer j
+  const float* dlogit;                       // [T]
+  float *dS, *dzeta, *dp, *dm;               // carried gradient, in place: state leaving -> entering
+  float* dP;                                 // [T][d_e + d_head]: [ir dL/dpre_h; dL/dpre_b]
+  float* dPT;                                // the same, [d_e + d_head][T]
+  float* rowcoef;                            // [T][8]: c_norm, c1, c2, c3, c4
+  float* rho_part;                           // [T]
+  // token-contiguous ([rows][T]) operands of the weight-gradient products
+  float *XT, *dQT, *dKT, *dVT, *dU1T, *dU2T, *dPAT, *SAT, *DA, *DB, *SBT, *dPPT, *SPT, *XPT, *dZAT, *dZHT, *SHT;
+  float *dhbar, *dhbar1, *dhbar2;            // [T][d] fp32, accumulated
+  float* deta;                               // [1]
+};
+// rows of the token-contiguous operands above, per token
+size_t router_bwd_vector_floats(int d_m, int d_s, int d_h, int d_a, int d_e, int d_p, int d_head);
+hipError_t launch_router_bwd_token(const RouterBwdArgs& a, hipStream_t s);
+// the RMSNorm / transition terms of dL/dhbar, then dL/deta
+hipError_t launch_router_bwd_rows(const RouterBwdArgs& a, hipStream_t s);
+// out[c][r] = float(in[r][c])
+hipError_t launch_to_f32_transpose(int dtype, const void* in, int R, int C, int ld_in, float* out, int ld_out,
+                                   hipStream_t s);
 // alpha L_skip (Eq. 18) into loss[0] and its gradient over gates [L_R][batch seq]
 hipError_t launch_skip_penalty(const float* gates, int L_R, int batch, int seq, float alpha, float* loss,
                                float* dgates, hipStream_t s);

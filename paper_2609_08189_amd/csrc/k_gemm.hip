@@ -1646,6 +1646,21 @@ hipError_t launch_adapter_du(int dtype, const void* dz, const int* counts, int n
   return run_f32<false>(A, B, EpiStoreF32{du, d, 0}, counts, n_max, d, k, s);
 }
 
+namespace {
+struct EpiAccF32 {  // C[m][n] += acc
+  float* out;
+  int ld;
+  __device__ __forceinline__ void store(int m, int n, float v) const { out[static_cast<size_t>(m) * ld + n] += v; }
+};
+}  // namespace
+
+hipError_t launch_gemm_acc_f32(const float* A, int lda, int M, const float* B, int ldb, int N, int K, float* C,
+                               int ldc, hipStream_t s) {
+  ARows<float> a{A, nullptr, lda};
+  BRows<float> b{B, nullptr, INT_MAX, ldb};
+  return run_f32<false>(a, b, EpiAccF32{C, ldc}, nullptr, M, N, K, s);
+}
+
 hipError_t launch_gemm_nt_f32(const void* A, int M, const void* B, int N, int K, float* C, int ldc, hipStream_t s) {
   if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
   ARows<bf16_t> a{static_cast<const bf16_t*>(A), nullptr, K};

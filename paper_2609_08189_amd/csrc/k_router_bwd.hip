@@ -1,0 +1,447 @@
+// Backward of the router at one routed layer (Sec. 3.2 in reverse order): the gradient that
+// reaches the router through the gate scaling (Sec. 3.1, the remark after eq:ffn_route) flows
+// through the local head, the history head, the history dissimilarity, the memory read and
+// write, the projections q, k, v, the router state, the path encoder and the hidden encoder.
+//
+// router_bwd_token (one workgroup per token, fp32):
+//   forward recompute of the layer's router from P = hbar [W_hd; psi_1]^T (recomputed on the
+//   GEMM core) and the state entering the layer; then the reverse:
+//     dL/da = dL/dlogit + (dL/dp_j + dL/dm_j m_{j-1}) p (1 - p) / T_hist,  dL/db = dL/dlogit,
+//     heads, nu (cosine backward), one streaming pass over S_{j-1} and the carried dL/dS_j that
+//     forms dL/dphi(k), dL/dv, dL/dphi(q) and dL/drho and writes dL/dS_{j-1} in place,
+//     projections, path encoder (dL/dp_{j-1}, dL/dm_{j-1}, and the transition features'
+//     gradients as coefficients of delta_j, delta_{j-1}), hidden encoder;
+//   writes the gradient over P ([ir dL/dpre_h; dL/dpre_b], row- and token-major), the per-row
+//   coefficients of the RMSNorm and transition terms, and every (vector, token) pair the weight
+//   gradients need, token-contiguous, so that each weight gradient is one product with the
+//   tokens as K (run by the caller on the fp32 GEMM, fixed summation order).
+// router_bwd_rows: dL/dhbar_j += c_norm hbar_j + ddelta_j, dL/dhbar_{j-1} += ddelta_{j-1} -
+//   ddelta_j, dL/dhbar_{j-2} -= ddelta_{j-1}, with ddelta_j = c1 delta_j + c2 delta_{j-1} and
+//   ddelta_{j-1} = c3 delta_j + c4 delta_{j-1}.
+// At j = 1 the state entering the layer is the initial one (S = 0, zeta = 0, p = m = 1) whatever
+// the buffers hold; the carried gradient written there is rho dL/dS_1 (the state is a constant).
+#include "hero_device.h"
+#include "hero_kernels.h"
+
+namespace hero {
+namespace {
+
+constexpr int RB_NT = 256;
+constexpr int RB_NW = RB_NT / kWave;
+constexpr int RB_MAXE = 256, RB_MAXH = 256, RB_MAXS = 128, RB_MAXM = 256, RB_MAXP = 128;
+constexpr int RB_MAXX = RB_MAXS + RB_MAXM + 1;
+
+__device__ __forceinline__ float silu_grad_(float x) {
+  const float s = sigmoidf_(x);
+  return s * (1.0f + x * (1.0f - s));
+}
+__device__ __forceinline__ float phi_grad_(float x) { return x > 0.0f ? 1.0f : expf(x); }
+
+// sum over the workgroup (every thread calls it; every thread gets the result, the same bits)
+__device__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = v;
+  __syncthreads();
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < RB_NW; ++i) s += red[i];
+  return s;
+}
+
+// y[o] = sum_k w[o][k] x[k] for o < O (a wave per row, lanes over k)
+template <typename W>
+__device__ void mv_rows(const W* w, int ld, int O, int I, const float* x, float* y) {
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  for (int o = wv; o < O; o += RB_NW) {
+    const W* r = w + static_cast<size_t>(o) * ld;
+    float acc = 0.0f;
+    for (int k = lane; k < I; k += kWave) acc = fmaf(ldf(r + k), x[k], acc);
+    acc = wave_sum(acc);
+    if (lane == 0) y[o] = acc;
+  }
+}
+
+// x[k] (+)= sum_o w[o][k] y[o] for k < I (a thread per column)
+template <typename W>
+__device__ void mv_cols(const W* w, int ld, int O, int I, const float* y, float* x, bool accumulate) {
+  for (int k = threadIdx.x; k < I; k += RB_NT) {
+    float acc = accumulate ? x[k] : 0.0f;
+    for (int o = 0; o < O; ++o) acc = fmaf(ldf(w + static_cast<size_t>(o) * ld + k), y[o], acc);
+    x[k] = acc;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
+  __shared__ float red[RB_NW];
+  __shared__ float Ph[RB_MAXE], sh[RB_MAXE], dsh[RB_MAXE];
+  __shared__ float Pb[RB_MAXH], pa[RB_MAXH], dpa[RB_MAXH];
+  __shared__ float ppre[RB_MAXP], psil[RB_MAXP], dpp[RB_MAXP];
+  __shared__ float xp[8], dx[8], sc[16];
+  __shared__ float xth[RB_MAXX], dxth[RB_MAXX];   // [s; c; nu] and its gradient (ds, dc, dnu)
+  __shared__ float qkvu[4][RB_MAXM];                // q, k, v (pre-activation), u1 = W_n s
+  __shared__ float u2[RB_MAXM], du1[RB_MAXM], du2[RB_MAXM], dnum[RB_MAXM];
+  __shared__ float dfk[RB_MAXM], dfq[RB_MAXM], dvw[RB_NW][RB_MAXM];
+  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const int T_ = a.T, j = a.j, d = a.d, DM = a.d_m, d_s = a.d_s, d_h = a.d_h, d_a = a.d_a;
+  const int d_e = a.d_e, d_p = a.d_p, d_head = a.d_head, NP = d_e + d_head, d_x = d_s + DM + 1;
+  const T* hb = static_cast<const T*>(a.hbar) + static_cast<size_t>(t) * d;
+  const T* h1 = j >= 2 ? static_cast<const T*>(a.prev1) + static_cast<size_t>(t) * d : nullptr;
+  const T* h2 = j >= 3 ? static_cast<const T*>(a.prev2) + static_cast<size_t>(t) * d : nullptr;
+  auto colT = [&](float* base, int r) -> float& { return base[static_cast<size_t>(r) * T_ + t]; };
+
+  // ---- forward recompute -------------------------------------------------------------
+  // row statistics: inv_rms and the residual transitions
+  float s2 = 0.0f, dd = 0.0f, dpv = 0.0f, pp2 = 0.0f;
+  for (int i = tid; i < d; i += RB_NT) {
+    const float x = ldf(hb + i);
+    s2 = fmaf(x, x, s2);
+    if (j >= 2) {
+      const float y = ldf(h1 + i), del = x - y;
+      dd = fmaf(del, del, dd);
+      if (j >= 3) {
+        const float dp_ = y - ldf(h2 + i);
+        dpv = fmaf(del, dp_, dpv);
+        pp2 = fmaf(dp_, dp_, pp2);
+      }
+    }
+  }
+  s2 = block_sum(s2, red);
+  dd = block_sum(dd, red);
+  dpv = block_sum(dpv, red);
+  pp2 = block_sum(pp2, red);
+  const float ir = 1.0f / sqrtf(s2 / static_cast<float>(d) + a.eps_norm);
+  // pre-activations: the K slices of P added in slice order
+  for (int e = tid; e < NP; e += RB_NT) {
+    float v = 0.0f;
+    for (int z = 0; z < a.p_splits; ++z) v += a.P[(static_cast<size_t>(z) * T_ + t) * NP + e];
+    if (e < d_e) {
+      Ph[e] = v;
+      sh[e] = siluf_(ir * v);
+    } else {
+      Pb[e - d_e] = v;
+    }
+  }
+  if (tid == 0) {
+    const float dj = j >= 2 ? sqrtf(dd) : 0.0f;
+    const float np_ = sqrtf(pp2);
+    xp[0] = static_cast<float>(j) / static_cast<float>(a.L_R);
+    xp[1] = static_cast<float>(a.L_R - j) / static_cast<float>(a.L_R);
+    xp[2] = dj;
+    xp[3] = j >= 3 ? dpv / (dj * np_ + a.eps) : 0.0f;
+    xp[4] = j > 1 ? a.p_in[t] : 1.0f;
+    xp[5] = j > 1 ? a.m_in[t] : 1.0f;
+    xp[6] = xp[7] = 0.0f;
+    sc[0] = dj;
+    sc[1] = np_;
+  }
+  __syncthreads();
+  // hidden encoder z^h (s[0:d_h]) and path encoder z^a (s[d_h:d_s])
+  mv_rows(static_cast<const T*>(a.w_hu), d_e, d_h, d_e, sh, xth);
+  mv_rows(static_cast<const T*>(a.w_p1), 6, d_p, 6, xp, ppre);
+  __syncthreads();
+  for (int o = tid; o < d_p; o += RB_NT) psil[o] = siluf_(ppre[o]);
+  __syncthreads();
+  mv_rows(static_cast<const T*>(a.w_p2), d_p, d_a, d_p, psil, xth + d_h);
+  __syncthreads();
+  // q, k, v, W_n s
+  mv_rows(static_cast<const T*>(a.w_q), d_s, DM, d_s, xth, qkvu[0]);
+  mv_rows(static_cast<const T*>(a.w_k), d_s, DM, d_s, xth, qkvu[1]);
+  mv_rows(static_cast<const T*>(a.w_v), d_s, DM, d_s, xth, qkvu[2]);
+  mv_rows(static_cast<const T*>(a.w_n), d_s, DM, d_s, xth, qkvu[3]);
+  __syncthreads();
+  // memory read c = phi(q)^T S_{j-1} / (phi(q)^T zeta_{j-1} + eps)
+  const float* Sin = a.S_in + static_cast<size_t>(t) * DM * DM;
+  const float* zin = a.zeta_in + static_cast<size_t>(t) * DM;
+  float den = 0.0f;
+  for (int k = tid; k < DM; k += RB_NT) den += j > 1 ? phif_(qkvu[0][k]) * zin[k] : 0.0f;
+  den = block_sum(den, red) + a.eps;
+  for (int v = tid; v < DM; v += RB_NT) {
+    float acc = 0.0f;
+    if (j > 1)
+      for (int k = 0; k < DM; ++k) acc = fmaf(phif_(qkvu[0][k]), Sin[static_cast<size_t>(k) * DM + v], acc);
+    xth[d_s + v] = acc / den;
+  }
+  __syncthreads();
+  // history dissimilarity nu = 1 - cos(W_n s, W_c c)
+  mv_rows(static_cast<const T*>(a.w_c), DM, DM, DM, xth + d_s, u2);
+  __syncthreads();
+  float n1 = 0.0f, n2 = 0.0f, nn = 0.0f;
+  for (int k = tid; k < DM; k += RB_NT) {
+    n1 = fmaf(qkvu[3][k], qkvu[3][k], n1);
+    n2 = fmaf(u2[k], u2[k], n2);
+    nn = fmaf(qkvu[3][k], u2[k], nn);
+  }
+  n1 = sqrtf(block_sum(n1, red));
+  n2 = sqrtf(block_sum(n2, red));
+  nn = block_sum(nn, red);
+  const float Dc = n1 * n2 + a.eps;
+  if (tid == 0) xth[d_s + DM] = j > 1 ? 1.0f - nn / Dc : 0.0f;
+  __syncthreads();
+  // history head a = f_theta([s; c; nu]), p = sigma(a / T_hist); local head's SiLU
+  mv_rows(static_cast<const T*>(a.th1), a.ld_th1, d_head, d_x, xth, pa);
+  __syncthreads();
+  float aa = 0.0f;
+  for (int o = tid; o < d_head; o += RB_NT) aa = fmaf(ldf(static_cast<const T*>(a.th2) + o), siluf_(pa[o]), aa);
+  aa = block_sum(aa, red);
+  const float p = sigmoidf_(aa / a.T_hist);
+
+  // ---- reverse -------------------------------------------------------------------------
+  const float dl = a.dlogit[t];
+  const float dp_in = a.dp[t], dm_in = a.dm[t];
+  const float m_prev = xp[5];
+  const float da = dl + (dp_in + dm_in * m_prev) * p * (1.0f - p) / a.T_hist;
+  const float db = dl;
+  if (tid == 0) {
+    colT(a.DA, 0) = da;
+    colT(a.DB, 0) = db;
+  }
+  // heads: dL/dpre_a, dL/dpre_b (the latter is the psi_1 part of dL/dP)
+  for (int o = tid; o < d_head; o += RB_NT) {
+    const float sa = siluf_(pa[o]);
+    dpa[o] = da * ldf(static_cast<const T*>(a.th2) + o) * silu_grad_(pa[o]);
+    colT(a.dPAT, o) = dpa[o];
+    colT(a.SAT, o) = sa;
+    const float dpb = db * ldf(static_cast<const T*>(a.ps2) + o) * silu_grad_(Pb[o]);
+    a.dP[static_cast<size_t>(t) * NP + d_e + o] = dpb;
+    colT(a.dPT, d_e + o) = dpb;
+    colT(a.SBT, o) = siluf_(Pb[o]);
+  }
+  __syncthreads();
+  // [ds; dc; dnu] = f_theta's first layer transposed times dL/dpre_a
+  mv_cols(static_cast<const T*>(a.th1), a.ld_th1, d_head, d_x, dpa, dxth, false);
+  for (int k = tid; k < d_x; k += RB_NT) colT(a.XT, k) = xth[k];
+  __syncthreads();
+  // nu's cosine backward (a constant at j = 1)
+  {
+    const float dcos = j > 1 ? -dxth[d_s + DM] : 0.0f;
+    const float q_ = nn / (Dc * Dc);
+    for (int k = tid; k < DM; k += RB_NT) {
+      const float a1 = qkvu[3][k], a2 = u2[k];
+      du1[k] = dcos * (a2 / Dc - q_ * n2 * (n1 > 0.0f ? a1 / n1 : 0.0f));
+      du2[k] = dcos * (a1 / Dc - q_ * n1 * (n2 > 0.0f ? a2 / n2 : 0.0f));
+      colT(a.dU1T, k) = du1[k];
+      colT(a.dU2T, k) = du2[k];
+    }
+  }
+  __syncthreads();
+  mv_cols(static_cast<const T*>(a.w_n), d_s, DM, d_s, du1, dxth, true);            // ds += W_n^T du1
+  mv_cols(static_cast<const T*>(a.w_c), DM, DM, DM, du2, dxth + d_s, true);        // dc += W_c^T du2
+  __syncthreads();
+  // memory read: dL/dnum = dc / den, dL/dden = -<dc, c> / den (no read at j = 1)
+  float dden = 0.0f;
+  for (int v = tid; v < DM; v += RB_NT) {
+    dnum[v] = j > 1 ? dxth[d_s + v] / den : 0.0f;
+    dden += j > 1 ? -dxth[d_s + v] * xth[d_s + v] / den : 0.0f;
+  }
+  dden = block_sum(dden, red);   // (its barriers also publish dnum)
+  // one pass over S_{j-1} and dL/dS_j: waves take rows k, lanes columns v
+  float* dS = a.dS + static_cast<size_t>(t) * DM * DM;
+  float* dz = a.dzeta + static_cast<size_t>(t) * DM;
+  const float rho = a.rho;
+  float rho_acc = 0.0f;
+  float dva[RB_MAXM / kWave];
+#pragma unroll
+  for (int i = 0; i < RB_MAXM / kWave; ++i) dva[i] = 0.0f;
+  for (int k = wv; k < DM; k += RB_NW) {
+    const float fqk = phif_(qkvu[0][k]), fkk = phif_(qkvu[1][k]);
+    float sk = 0.0f, sq = 0.0f;
+#pragma unroll
+    for (int i = 0; i < RB_MAXM / kWave; ++i) {
+      const int v = lane + kWave * i;
+      if (v < DM) {
+        const size_t o = static_cast<size_t>(k) * DM + v;
+        const float g = dS[o];
+        const float sv = j > 1 ? Sin[o] : 0.0f;
+        sk = fmaf(g, qkvu[2][v], sk);
+        sq = fmaf(sv, dnum[v], sq);
+        dva[i] = fmaf(g, fkk, dva[i]);
+        rho_acc = fmaf(g, sv, rho_acc);
+        dS[o] = fmaf(rho, g, fqk * dnum[v]);
+      }
+    }
+    sk = wave_sum(sk);
+    sq = wave_sum(sq);
+    if (lane == 0) {
+      dfk[k] = sk + dz[k];
+      dfq[k] = sq + (j > 1 ? zin[k] : 0.0f) * dden;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < RB_MAXM / kWave; ++i) {
+    const int v = lane + kWave * i;
+    if (v < DM) dvw[wv][v] = dva[i];
+  }
+  __syncthreads();
+  // zeta: its share of dL/drho, and dL/dzeta_{j-1} in place (dfk above read the incoming value)
+  for (int k = tid; k < DM; k += RB_NT) {
+    const float g = dz[k];
+    rho_acc = fmaf(g, j > 1 ? zin[k] : 0.0f, rho_acc);
+    dz[k] = fmaf(rho, g, phif_(qkvu[0][k]) * dden);
+  }
+  rho_acc = block_sum(rho_acc, red);
+  if (tid == 0) a.rho_part[t] = rho_acc;
+  // q, k, v gradients; the router state's gradient gets the projections' share
+  for (int k = tid; k < DM; k += RB_NT) {
+    float dv = 0.0f;
+#pragma unroll
+    for (int w = 0; w < RB_NW; ++w) dv += dvw[w][k];
+    const float dq = dfq[k] * phi_grad_(qkvu[0][k]);
+    const float dk = dfk[k] * phi_grad_(qkvu[1][k]);
+    dfq[k] = dq;
+    dfk[k] = dk;
+    dnum[k] = dv;     // dnum is free: it now holds dL/dv
+    colT(a.dQT, k) = dq;
+    colT(a.dKT, k) = dk;
+    colT(a.dVT, k) = dv;
+  }
+  __syncthreads();
+  mv_cols(static_cast<const T*>(a.w_q), d_s, DM, d_s, dfq, dxth, true);
+  mv_cols(static_cast<const T*>(a.w_k), d_s, DM, d_s, dfk, dxth, true);
+  mv_cols(static_cast<const T*>(a.w_v), d_s, DM, d_s, dnum, dxth, true);
+  __syncthreads();
+  // path encoder: dL/dSiLU(pre_p) = W_p2^T dz^a, then W_p1^T for the six features
+  mv_cols(static_cast<const T*>(a.w_p2), d_p, d_a, d_p, dxth + d_h, dpp, false);
+  __syncthreads();
+  for (int o = tid; o < d_p; o += RB_NT) {
+    dpp[o] *= silu_grad_(ppre[o]);
+    colT(a.dPPT, o) = dpp[o];
+    colT(a.SPT, o) = psil[o];
+  }
+  for (int o = tid; o < d_a; o += RB_NT) colT(a.dZAT, o) = dxth[d_h + o];
+  for (int o = tid; o < d_h; o += RB_NT) colT(a.dZHT, o) = dxth[o];
+  if (tid < 6) colT(a.XPT, tid) = xp[tid];
+  __syncthreads();
+  mv_cols(static_cast<const T*>(a.w_p1), 6, d_p, 6, dpp, dx, false);
+  // hidden encoder: dL/dSiLU(pre_h) = W_hu^T dz^h
+  mv_cols(static_cast<const T*>(a.w_hu), d_e, d_h, d_e, dxth, dsh, false);
+  __syncthreads();
+  float cn = 0.0f;
+  for (int e = tid; e < d_e; e += RB_NT) {
+    const float dph = dsh[e] * silu_grad_(ir * Ph[e]);
+    cn = fmaf(dph, Ph[e], cn);
+    a.dP[static_cast<size_t>(t) * NP + e] = ir * dph;
+    colT(a.dPT, e) = ir * dph;
+    colT(a.SHT, e) = sh[e];
+  }
+  cn = block_sum(cn, red);
+  if (tid == 0) {
+    // transitions: d_j = |delta_j| (j >= 2), gamma_j = cos(delta_j, delta_{j-1}) (j >= 3)
+    const float nd = sc[0], np_ = sc[1], ddj = dx[2], dg = dx[3];
+    float c1 = 0.0f, c2 = 0.0f, c3 = 0.0f, c4 = 0.0f;
+    if (j >= 2 && nd > 0.0f) c1 += ddj / nd;
+    if (j >= 3) {
+      const float D = nd * np_ + a.eps, q_ = dpv / (D * D);
+      c2 += dg / D;
+      c3 += dg / D;
+      if (nd > 0.0f) c1 -= dg * q_ * np_ / nd;
+      if (np_ > 0.0f) c4 -= dg * q_ * nd / np_;
+    }
+    float* rc = a.rowcoef + static_cast<size_t>(t) * 8;
+    rc[0] = -(ir * ir * ir / static_cast<float>(d)) * cn;
+    rc[1] = c1;
+    rc[2] = c2;
+    rc[3] = c3;
+    rc[4] = c4;
+    a.dp[t] = dx[4];
+    a.dm[t] = dm_in * p + dx[5];
+  }
+}
+
+// the per-row RMSNorm and transition terms of dL/dhbar (one workgroup per token)
+template <typename T>
+__global__ __launch_bounds__(256) void router_bwd_rows(RouterBwdArgs a) {
+  const int t = blockIdx.x, j = a.j, d = a.d;
+  const float* rc = a.rowcoef + static_cast<size_t>(t) * 8;
+  const float cnorm = rc[0], c1 = rc[1], c2 = rc[2], c3 = rc[3], c4 = rc[4];
+  const size_t row = static_cast<size_t>(t) * d;
+  const T* hb = static_cast<const T*>(a.hbar) + row;
+  const T* h1 = j >= 2 ? static_cast<const T*>(a.prev1) + row : nullptr;
+  const T* h2 = j >= 3 ? static_cast<const T*>(a.prev2) + row : nullptr;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    const float x = ldf(hb + i);
+    const float y = j >= 2 ? ldf(h1 + i) : x;
+    const float z = j >= 3 ? ldf(h2 + i) : y;
+    const float del = x - y, delp = y - z;
+    const float gj = c1 * del + c2 * delp, gp = c3 * del + c4 * delp;
+    a.dhbar[row + i] += cnorm * x + gj;
+    if (j >= 2) a.dhbar1[row + i] += gp - gj;
+    if (j >= 3) a.dhbar2[row + i] -= gp;
+  }
+}
+
+// dL/deta = rho (1 - rho) sum_t rho_part[t], summed in a fixed order (one workgroup)
+__global__ __launch_bounds__(256) void router_bwd_deta(const float* __restrict__ part, int T, float rho,
+                                                      float* __restrict__ deta) {
+  __shared__ float red[256 / kWave];
+  float s = 0.0f;
+  for (int t = threadIdx.x; t < T; t += 256) s += part[t];
+  s = wave_sum(s);
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float tot = 0.0f;
+    for (int w = 0; w < 256 / kWave; ++w) tot += red[w];
+    deta[0] = rho * (1.0f - rho) * tot;
+  }
+}
+
+// out[c][r] = float(in[r][c]) for r < R, c < C (64 x 64 tiles through LDS)
+template <typename T>
+__global__ __launch_bounds__(256) void to_f32_transpose(const T* __restrict__ in, int R, int C, int ld_in,
+                                                       float* __restrict__ out, int ld_out) {
+  __shared__ float tile[64][65];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    tile[i][tx] = (r < R && c < C) ? ldf(in + static_cast<size_t>(r) * ld_in + c) : 0.0f;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < C && r < R) out[static_cast<size_t>(c) * ld_out + r] = tile[tx][i];
+  }
+}
+
+}  // namespace
+
+size_t router_bwd_vector_floats(int d_m, int d_s, int d_h, int d_a, int d_e, int d_p, int d_head) {
+  // XT, dQT, dKT, dVT, dU1T, dU2T, dPAT, SAT, DA, DB, SBT, dPPT, SPT, XPT, dZAT, dZHT, SHT
+  return static_cast<size_t>(d_s + d_m + 1) + 5 * d_m + 3 * d_head + 2 + 2 * d_p + 8 + d_a + d_h + d_e;
+}
+
+hipError_t launch_router_bwd_token(const RouterBwdArgs& a, hipStream_t s) {
+  if (a.d_e > RB_MAXE || a.d_head > RB_MAXH || a.d_s > RB_MAXS || a.d_m > RB_MAXM || a.d_p > RB_MAXP)
+    return hipErrorInvalidValue;
+  if (a.dtype == 1)
+    router_bwd_token<bf16_t><<<a.T, RB_NT, 0, s>>>(a);
+  else
+    router_bwd_token<float><<<a.T, RB_NT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_router_bwd_rows(const RouterBwdArgs& a, hipStream_t s) {
+  if (a.dtype == 1)
+    router_bwd_rows<bf16_t><<<a.T, 256, 0, s>>>(a);
+  else
+    router_bwd_rows<float><<<a.T, 256, 0, s>>>(a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  router_bwd_deta<<<1, 256, 0, s>>>(a.rho_part, a.T, a.rho, a.deta);
+  return hipGetLastError();
+}
+
+hipError_t launch_to_f32_transpose(int dtype, const void* in, int R, int C, int ld_in, float* out, int ld_out,
+                                   hipStream_t s) {
+  if (R <= 0 || C <= 0) return hipSuccess;
+  const dim3 grid((C + 63) / 64, (R + 63) / 64);
+  if (dtype == 1)
+    to_f32_transpose<bf16_t><<<grid, 256, 0, s>>>(static_cast<const bf16_t*>(in), R, C, ld_in, out, ld_out);
+  else
+    to_f32_transpose<float><<<grid, 256, 0, s>>>(static_cast<const float*>(in), R, C, ld_in, out, ld_out);
+  return hipGetLastError();
+}
+
+}  // namespace hero

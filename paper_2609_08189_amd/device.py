@@ -376,3 +376,43 @@ class DeviceBackward:
         return dict(dhbar=download_f64(self.dhbar), dgate=self.dgate.cpu().numpy().astype(np.float64),
                     dlogit=self.dlogit.cpu().numpy().astype(np.float64),
                     dw1=self.dw1.cpu().numpy().astype(np.float64), dw2=self.dw2.cpu().numpy().astype(np.float64))
+
+
+class DeviceRouterBackward:
+    """The router's backward at routed layer j on the GPU, on a DeviceProblem's inputs (its hbar,
+    hbar_{j-1}, hbar_{j-2}, router weights and the state entering the layer), given dL/dlogit and
+    the carried state gradient; the fp32 gradient buffers start at zero."""
+
+    def __init__(self, dp: "DeviceProblem", j: int, dlogit: np.ndarray, dS: np.ndarray, dzeta: np.ndarray,
+                 dp_hist: np.ndarray, dm_hist: np.ndarray):
+        w, dev, T = dp.w, dp.device, dp.T
+        self.dp_, self.j, self.T, self.w = dp, j, T, w
+        f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+        zeros = lambda *shape: torch.zeros(*shape, dtype=torch.float32, device=dev)
+        self.dlogit = f32(dlogit)
+        self.dS, self.dzeta, self.dpc, self.dmc = f32(dS), f32(dzeta), f32(dp_hist), f32(dm_hist)
+        self.carry_s = H.hero_router_carry(self.dS.data_ptr(), self.dzeta.data_ptr(), self.dpc.data_ptr(),
+                                           self.dmc.data_ptr())
+        self.dh = [zeros(T, w.d) for _ in range(3)]
+        self.grads = {k: zeros(*dp.router[k].shape) for k in H.ROUTER_FIELDS}
+        self.grads_s = H.hero_router_grads(**{k: v.data_ptr() for k, v in self.grads.items()})
+        self.deta = zeros(4)
+        self.ws_bytes = H.hero_router_backward_workspace_size(dp.dims, T)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
+
+    def run(self) -> None:
+        dp, j = self.dp_, self.j
+        H.check(H.hero_router_backward(dp.dims, j, self.T, dp.hbar, dp.prev1 if j >= 2 else None,
+                                       dp.prev2 if j >= 3 else None, dp.state_s, dp.router_s, dp.eta[j - 1],
+                                       self.dlogit, self.carry_s, self.dh[0], self.dh[1] if j >= 2 else None,
+                                       self.dh[2] if j >= 3 else None, self.grads_s, self.deta, self.ws,
+                                       self.ws_bytes, dp.stream()), "hero_router_backward")
+
+    def results(self) -> Dict[str, np.ndarray]:
+        torch.cuda.synchronize()
+        f64 = lambda t: t.cpu().numpy().astype(np.float64)
+        g = {k: f64(v) for k, v in self.grads.items()}
+        g["th1"] = g["th1"][:, :self.w.d_s + self.w.d_m + 1]
+        return dict(dhbar=f64(self.dh[0]), dhbar1=f64(self.dh[1]), dhbar2=f64(self.dh[2]), grads=g,
+                    deta=float(self.deta[0].item()), dS=f64(self.dS), dzeta=f64(self.dzeta), dp=f64(self.dpc),
+                    dm=f64(self.dmc))

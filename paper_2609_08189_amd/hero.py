@@ -14,7 +14,7 @@ from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhero.so")
-ABI_VERSION = 5          # the struct layouts below follow include/hero.h of this version
+ABI_VERSION = 6          # the struct layouts below follow include/hero.h of this version
 
 HERO_OK = 0
 HERO_E_NULL = 1
@@ -41,7 +41,8 @@ KERNELS = ("rowstats", "router_gemm", "router_pre", "router_mem", "router_post",
            "ffn_gate_up", "ffn_down", "adapter_down", "adapter_up",
            "attn_norm", "attn_qkv", "attn_core", "attn_out",
            "bwd_norm", "bwd_ffn_e", "bwd_ffn_gate_up", "bwd_ffn_du", "bwd_adapter", "bwd_adapter_wgrad",
-           "bwd_rows", "skip_penalty")
+           "bwd_rows", "skip_penalty",
+           "router_bwd_gemm", "router_bwd_token", "router_bwd_products", "router_bwd_rows")
 HERO_K = {name: i for i, name in enumerate(KERNELS)}
 
 _vp = ctypes.c_void_p
@@ -74,6 +75,14 @@ class hero_router_weights(ctypes.Structure):
 
 class hero_state(ctypes.Structure):
     _fields_ = [("S", _vp), ("zeta", _vp), ("p_hist", _vp), ("m_hist", _vp)]
+
+
+class hero_router_grads(ctypes.Structure):
+    _fields_ = [(n, _vp) for n in ROUTER_FIELDS]
+
+
+class hero_router_carry(ctypes.Structure):
+    _fields_ = [("dS", _vp), ("dzeta", _vp), ("dp", _vp), ("dm", _vp)]
 
 
 class hero_history(ctypes.Structure):
@@ -175,6 +184,12 @@ def lib() -> ctypes.CDLL:
         L.hero_skip_penalty.restype = ctypes.c_int
         L.hero_skip_penalty.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, ctypes.c_float, _vp, _vp,
                                         _vp]
+        L.hero_router_backward_workspace_size.restype = ctypes.c_int
+        L.hero_router_backward_workspace_size.argtypes = [P(hero_dims), ctypes.c_int, P(ctypes.c_size_t)]
+        L.hero_router_backward.restype = ctypes.c_int
+        L.hero_router_backward.argtypes = [P(hero_dims), ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, P(hero_state),
+                                           P(hero_router_weights), ctypes.c_float, _vp, P(hero_router_carry), _vp,
+                                           _vp, _vp, P(hero_router_grads), _vp, _vp, ctypes.c_size_t, _vp]
         _lib = L
     return _lib
 
@@ -355,3 +370,21 @@ def hero_routed_block_backward(dims: hero_dims, T: int, hbar, dh_out, gate, idx_
 def hero_skip_penalty(L_R: int, batch: int, seq: int, gates, alpha: float, loss, dgates, stream=None) -> int:
     """alpha L_skip (Eq. 18) into loss[0] and its gradient over gates [L_R][batch seq]."""
     return lib().hero_skip_penalty(L_R, batch, seq, ptr(gates), float(alpha), ptr(loss), ptr(dgates), stream)
+
+
+def hero_router_backward_workspace_size(dims: hero_dims, T: int) -> int:
+    out = ctypes.c_size_t(0)
+    check(lib().hero_router_backward_workspace_size(ctypes.byref(dims), T, ctypes.byref(out)),
+          "hero_router_backward_workspace_size")
+    return out.value
+
+
+def hero_router_backward(dims: hero_dims, j: int, T: int, hbar, hbar_prev1, hbar_prev2, state_in: hero_state,
+                         router: hero_router_weights, eta: float, dlogit, carry: hero_router_carry, dhbar,
+                         dhbar_prev1, dhbar_prev2, grads: hero_router_grads, deta, workspace, workspace_bytes: int,
+                         stream=None) -> int:
+    """Enqueue the router's backward at routed layer j; returns the hero_status code."""
+    return lib().hero_router_backward(ctypes.byref(dims), j, T, ptr(hbar), ptr(hbar_prev1), ptr(hbar_prev2),
+                                      _byref(state_in), _byref(router), float(eta), ptr(dlogit), _byref(carry),
+                                      ptr(dhbar), ptr(dhbar_prev1), ptr(dhbar_prev2), _byref(grads), ptr(deta),
+                                      ptr(workspace), workspace_bytes, stream)

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_function():
     lib = H.lib()
     for n in names:
         assert hasattr(lib, n), f"{n} declared in include/hero.h but not exported"
-    assert H.hero_abi_version() == H.ABI_VERSION == 5
+    assert H.hero_abi_version() == H.ABI_VERSION == 6
 
 
 def test_status_strings():
@@ -373,3 +373,43 @@ def test_backward_entry_points_validate():
     assert H.hero_skip_penalty(4, 2, 5, gates, 1.0, loss, gates + 16) == H.HERO_E_ALIAS
     assert H.hero_skip_penalty(4, 2, 5, gates, 1.0, loss + 4, dg) == H.HERO_E_ALIGN
     assert H.hero_skip_penalty(4, 2, 5, gates, 1.0, loss, dg) == H.HERO_E_DEVICE
+
+
+def test_router_backward_entry_validates():
+    """hero_router_backward checks everything on the host before any launch (fake addresses)."""
+    dims = good_dims(L_R=4)
+    T = 64
+    need = H.hero_router_backward_workspace_size(dims, T)
+    assert need > 0
+    _, _, rt, st = fake_structs()
+    import itertools
+    base = FAKE + (1 << 36)
+    nxt = itertools.count(1)
+    at = lambda: base + (next(nxt) << 28)
+    grads = H.hero_router_grads(**{k: at() for k in H.ROUTER_FIELDS})
+    carry = H.hero_router_carry(at(), at(), at(), at())
+
+    def call(**kw):
+        a = dict(d=dims, j=3, T=T, hb=at(), h1=at(), h2=at(), st=st, rt=rt, eta=3.9, dl=at(), carry=carry,
+                 dh=at(), dh1=at(), dh2=at(), g=grads, deta=at(), ws=at(), n=need)
+        a.update(kw)
+        return H.hero_router_backward(a["d"], a["j"], a["T"], a["hb"], a["h1"], a["h2"], a["st"], a["rt"], a["eta"],
+                                      a["dl"], a["carry"], a["dh"], a["dh1"], a["dh2"], a["g"], a["deta"], a["ws"],
+                                      a["n"], None)
+
+    assert call(j=0) == H.HERO_E_RANGE and call(j=5) == H.HERO_E_RANGE
+    assert call(T=0) == H.HERO_E_DIM
+    assert call(eta=float("nan")) == H.HERO_E_RANGE
+    assert call(d=good_dims(L_R=4, state_dtype=H.HERO_BF16)) == H.HERO_E_UNSUPPORTED
+    assert call(dl=None) == H.HERO_E_NULL
+    assert call(h2=None) == H.HERO_E_NULL and call(j=2, h2=None, dh2=None) != H.HERO_E_NULL
+    assert call(g=H.hero_router_grads(**{**{k: at() for k in H.ROUTER_FIELDS}, "th1": None})) == H.HERO_E_NULL
+    assert call(carry=H.hero_router_carry(at(), None, at(), at())) == H.HERO_E_NULL
+    assert call(dh=FAKE + 8) == H.HERO_E_ALIGN
+    same = at()
+    assert call(dh=same, dh1=same) == H.HERO_E_ALIAS
+    # dL/dS_{j-1} is written over dL/dS_j while S_{j-1} is read: they may not overlap
+    st2 = H.hero_state(carry.dS, st.zeta, st.p_hist, st.m_hist)
+    assert call(st=st2) == H.HERO_E_ALIAS
+    assert call(n=need - 1) == H.HERO_E_WORKSPACE
+    assert call(ws=None) == H.HERO_E_WORKSPACE
