@@ -536,6 +536,166 @@ def bench_backward(args, w):
     print(json.dumps(result), flush=True)
 
 
+RBWD_KERNELS = ("router_bwd_gemm", "router_bwd_token", "router_bwd_products", "router_bwd_rows")
+
+
+def router_backward_work(w, j):
+    """Algorithmic FLOPs and HBM bytes of hero_router_backward's kernel groups for T tokens at
+    routed layer j (fp32 state; the token kernel streams S_{j-1} once and dL/dS in and out)."""
+    T, d, dm, es = w.T, w.d, w.d_m, (2 if w.dtype == "bf16" else 4)
+    NP = w.d_e + w.d_head
+    splits = 4 if w.dtype == "bf16" else 1
+    d_x = w.d_s + dm + 1
+    vec = d_x + 5 * dm + 3 * w.d_head + 2 + 2 * w.d_p + 8 + w.d_a + w.d_h + w.d_e
+    small = 2 * T * (4 * dm * w.d_s + dm * dm + w.d_head * d_x + 2 * w.d_head + 6 * w.d_p + w.d_a * w.d_p
+                     + w.d_h * w.d_e)
+    n_prev = min(j - 1, 2)
+    return {
+        "router_bwd_gemm": dict(flops=2 * T * d * NP, bytes=T * d * es + NP * d * es + splits * T * NP * 4),
+        "router_bwd_token": dict(flops=0, bytes=T * ((3 if j > 1 else 2) * dm * dm * 4 + (1 + n_prev) * d * es
+                                                     + splits * NP * 4 + (2 * NP + vec + 8) * 4)),
+        "router_bwd_products": dict(flops=4 * T * NP * d + small, bytes=(2 * NP + vec) * T * 4 + T * d * (es + 4)
+                                    + 2 * T * d * 4),
+        "router_bwd_rows": dict(flops=0, bytes=T * d * ((1 + n_prev) * es + 2 * (1 + n_prev) * 4)),
+    }
+
+
+def bench_router_backward(args, w):
+    """A step is one hero_router_backward call at the workload's routed layer over its T tokens
+    (post-attention states, router weights, the state entering the layer, dL/dlogit and a carried
+    state gradient resident in HBM)."""
+    import numpy as np
+    import torch
+    from paper_2609_08189_amd import hero as H
+    from paper_2609_08189_amd import synth
+    from paper_2609_08189_amd.device import DeviceProblem, DeviceRouterBackward
+
+    j = w.layer_j
+    if j <= 0 or w.n_layers > 0 or w.state_dtype != "f32":
+        sys.exit("--router-backward times one routed layer's router with S in fp32")
+    print(f"# preparing the router backward at {describe(w, j)}", file=sys.stderr, flush=True)
+    prob = synth.make_problem(w, seed=args.seed, layer_j=j)
+    rng = np.random.default_rng(args.seed + 77)
+    T, dm = w.T, w.d_m
+    dl = rng.standard_normal(T).astype(np.float32)
+    dS = (0.05 * rng.standard_normal((T, dm, dm))).astype(np.float32)
+    dz = (0.1 * rng.standard_normal((T, dm))).astype(np.float32)
+    dph = rng.standard_normal(T).astype(np.float32)
+    dmh = rng.standard_normal(T).astype(np.float32)
+    dp = DeviceProblem(prob, stats=False)
+    rb = DeviceRouterBackward(dp, j, dl, dS, dz, dph, dmh)
+    stream = dp.stream()
+    ev = HipEvents()
+    for _ in range(1 + args.warmup):
+        rb.run()
+    torch.cuda.synchronize()
+    K = args.steps
+    works = router_backward_work(w, j)
+    per, handles = {}, {}
+    for name in RBWD_KERNELS:
+        handles[name] = (ev.create(K), ev.create(K))
+        H.hero_kernel_timer(H.HERO_K[name], *handles[name])
+    for _ in range(K):
+        rb.run()
+    torch.cuda.synchronize()
+    for name, (a, b) in handles.items():
+        H.hero_kernel_timer(H.HERO_K[name], [], [])
+        us = 1000.0 * sum(ev.elapsed_ms(x, y) for x, y in zip(a, b)) / K
+        wk = works[name]
+        per[name] = {"us": round(us, 2), "tflops": round(wk["flops"] / us * 1e-6, 1) if wk["flops"] else None,
+                     "gbs": round(wk["bytes"] / us * 1e-3, 1)}
+        ev.destroy(a + b)
+    dom = max(per, key=lambda k: per[k]["us"])
+    ks, ke = ev.create(K), ev.create(K)
+    H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
+    t_start, t_stop = ev.create(2)
+    marks = ev.create(K - 1)
+    torch.cuda.synchronize()
+    ev.record(t_start, stream)
+    for i in range(K):
+        rb.run()
+        if i < K - 1:
+            ev.record(marks[i], stream)
+    ev.record(t_stop, stream)
+    torch.cuda.synchronize()
+    H.hero_kernel_timer(H.HERO_K[dom], [], [])
+    ms_step = ev.elapsed_ms(t_start, t_stop) / K
+    bounds = [t_start] + marks + [t_stop]
+    step_ms = sorted(ev.elapsed_ms(a, b) for a, b in zip(bounds[:-1], bounds[1:]))
+    dom_ms = sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
+    if dom == "router_bwd_products":      # fp32 products on the vector ALUs
+        achieved, peak, unit, bound = works[dom]["flops"] / (dom_ms * 1e-3) * 1e-12, PEAK_F32_TFLOPS, "TFLOP/s", "alu"
+        wpl = f"4 T (d_e + d_head) d FLOP (dW_hd, dpsi_1 and dP [W_hd; psi_1]) + the small weights' products"
+    elif works[dom]["flops"]:
+        achieved, peak, unit, bound = (works[dom]["flops"] / (dom_ms * 1e-3) * 1e-12,
+                                       PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS, "TFLOP/s", "mfma")
+        wpl = "2 T d (d_e + d_head) FLOP"
+    else:
+        achieved, peak, unit, bound = works[dom]["bytes"] / (dom_ms * 1e-3) * 1e-9, PEAK_HBM_GBS, "GB/s", "hbm"
+        wpl = "per token: S_{j-1} read, dL/dS read and written (4 d_m^2 B each), rows and vectors"
+    result = {
+        "metric": "router backward tokens/sec at Llama-3.1-8B shape; % roofline",
+        "value": round(T / (ms_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": (f"backward of the router (Sec. 3.2 in reverse) at {describe(w, j)}; dL/dlogit "
+                                f"N(0,1), carried dL/dS N(0,0.05^2), dL/dzeta N(0,0.1^2), dL/dp, dL/dm N(0,1)"),
+                   "global_batch": w.batch, "seq_len": w.seq, "tokens": T, "parallelism": "none"},
+        "roofline": {"bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": unit,
+                     "frac": round(achieved / peak, 4), "traffic": None, "kernel": dom,
+                     "avg_launch_us": round(1000 * dom_ms, 2),
+                     "work_per_launch": f"{wpl}: {works[dom]['flops'] / 1e9:.1f} GFLOP, {works[dom]['bytes'] / 1e6:.1f} MB"},
+        "step_ms": step_stats(step_ms),
+        "kernels": per,
+    }
+    if not args.no_cpu_baseline:
+        print("# timing the CPU oracle on a token sample", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline_router_backward(w, prob, j, dl, dS, dz, dph, dmh, args.cpu_target_s)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline_router_backward(w, prob, j, dl, dS, dz, dph, dmh, target_s=12.0):
+    """The float64 oracle's router forward and router_layer_backward on the first n tokens, n
+    growing until the call takes >= target_s or covers all T (then repeated, up to 8 runs)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import hero_oracle as O
+    from tests.oracle_inputs import adapter_of, dims_of, ffn_of, router_of
+
+    T = w.T
+    dims, R = dims_of(w), router_of(prob)
+    F, A = ffn_of(prob.ffn[0]), adapter_of(prob.adapter[0])
+    eta = float(prob.eta[j - 1])
+
+    def run(n):
+        st = O.State(prob.S[:n].astype("f8"), prob.zeta[:n].astype("f8"), prob.p_hist[:n].astype("f8"),
+                     prob.m_hist[:n].astype("f8"))
+        h1 = prob.hbar_prev1.f64[:n] if j >= 2 else None
+        h2 = prob.hbar_prev2.f64[:n] if j >= 3 else None
+        t0 = time.perf_counter()
+        fwd = O.routed_layer(j, dims, prob.hbar.f64[:n], h1, h2, st, F, R, A, eta, mode="threshold",
+                             round_output=False, compute_rows=np.zeros(n, dtype=bool))
+        O.router_layer_backward(j, dims, prob.hbar.f64[:n], h1, h2, st, fwd, R, dl[:n].astype("f8"),
+                                dS[:n].astype("f8"), dz[:n].astype("f8"), dph[:n].astype("f8"),
+                                dmh[:n].astype("f8"), O._zero_router(R))
+        return time.perf_counter() - t0
+
+    n = 64
+    while True:
+        dt = run(n)
+        if dt >= target_s or n >= T:
+            break
+        n = min(T, max(2 * n, int(n * target_s / max(dt, 1e-3) * 1.1)))
+    reps = 1
+    while dt < target_s and reps < 8:
+        dt += run(n)
+        reps += 1
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": n * reps / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"the first {n} of {T} tokens (the router's forward and backward at this layer, float64 "
+                      f"numpy)" + (f", run {reps} times" if reps > 1 else "") + f", {dt:.1f} s"}
+
+
 # the paper's two Llama-3.1-8B operating points (Table 1: 26.87 % and 38.82 % skip)
 PAPER_SKIPS = (0.2687, 0.3882)
 
@@ -601,6 +761,8 @@ def main():
                          "from the instrumented pass)")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward of the routed block (training side) instead of the forward")
+    ap.add_argument("--router-backward", action="store_true",
+                    help="time the backward of the router at the workload's routed layer instead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-target-s", type=float, default=12.0)
     ap.add_argument("--memory", choices=("matrix", "history"), default="matrix",
@@ -642,6 +804,8 @@ def main():
         w = w.replace(state_dtype="bf16")
     if args.backward:
         return bench_backward(args, w)
+    if args.router_backward:
+        return bench_router_backward(args, w)
     if w.n_layers > 0:
         return bench_decoder(args, w)
     stack = w.layer_j <= 0          # a stack workload: a step is one hero_routed_stack call

@@ -1122,7 +1122,12 @@ int hero_skip_penalty(int L_R, int batch, int seq, const float* gates, float alp
 namespace {
 
 struct RouterBwdLayout {
-  size_t P, dP, dPT, rowcoef, rho_part, vec, hbT, wT, total;
+  size_t P, dP, dPT, rowcoef, rho_part, vec, hbT, wT;
+  // bf16: the big products on the GEMM core, dP split into bf16 hi + lo, K padded to kp
+  size_t dPT_hi, dPT_lo, dP_hi, dP_lo, hbT16, wT16;
+  size_t tn_part, tn_floats;   // K-split partials of the small weight-gradient products
+  int kp;
+  size_t total;
 };
 
 RouterBwdLayout router_bwd_layout_of(const hero_dims& d, int T) {
@@ -1140,8 +1145,26 @@ RouterBwdLayout router_bwd_layout_of(const hero_dims& d, int T) {
   L.rowcoef = take(t * 8 * 4);
   L.rho_part = take(t * 4);
   L.vec = take(hero::router_bwd_vector_floats(d.d_m, d.d_s, d.d_h, d.d_a, d.d_e, d.d_p, d.d_head) * t * 4);
-  L.hbT = take(static_cast<size_t>(d.d) * t * 4);
-  L.wT = take(static_cast<size_t>(d.d) * np * 4);
+  const bool mfma = d.dtype == HERO_BF16;
+  L.kp = (T + 63) / 64 * 64;
+  const size_t kp = static_cast<size_t>(L.kp);
+  L.hbT = take(mfma ? 0 : static_cast<size_t>(d.d) * t * 4);
+  L.wT = take(mfma ? 0 : static_cast<size_t>(d.d) * np * 4);
+  L.dPT_hi = take(mfma ? np * kp * 2 : 0);
+  L.dPT_lo = take(mfma ? np * kp * 2 : 0);
+  L.dP_hi = take(mfma ? t * np * 2 : 0);
+  L.dP_lo = take(mfma ? t * np * 2 : 0);
+  L.hbT16 = take(mfma ? static_cast<size_t>(d.d) * kp * 2 : 0);
+  L.wT16 = take(mfma ? static_cast<size_t>(d.d) * np * 2 : 0);
+  // the largest small product: f_theta's first layer [d_head][d_s + d_m + 1] (or W_c, W_hu, W_q ...)
+  const size_t mn = std::max({static_cast<size_t>(d.d_head) * (d.d_s + d.d_m + 1),
+                              mfma ? 0 : static_cast<size_t>(std::max(d.d_e, d.d_head)) * d.d, static_cast<size_t>(d.d_m) * d.d_m,
+                              static_cast<size_t>(d.d_m) * d.d_s, static_cast<size_t>(d.d_h) * d.d_e,
+                              static_cast<size_t>(d.d_a) * d.d_p, static_cast<size_t>(d.d_p) * 6,
+                              static_cast<size_t>(d.d_head)});
+  // K chunks for the small products: up to one per 64 tokens, at most 16 M floats (64 MB) of partials
+  L.tn_floats = std::min(static_cast<size_t>(hero::tn_chunks(T)) * mn, std::max<size_t>(mn, 16u << 20));
+  L.tn_part = take(L.tn_floats * 4);
   L.total = off;
   return L;
 }
@@ -1307,10 +1330,42 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
   if (e != hipSuccess) return HERO_E_LAUNCH;
   e = timed(HERO_K_ROUTER_BWD_PRODUCTS, s, [&] {
     // the weight gradients: products with the tokens as K (every operand token-contiguous)
+    float* tn_part = reinterpret_cast<float*>(ws + L.tn_part);
     auto acc = [&](const float* A, int M, const float* B, int N, float* C, int ldc) {
-      return hero::launch_gemm_acc_f32(A, T, M, B, T, N, T, C, ldc, s);
+      return hero::launch_gemm_tn_acc_f32(A, T, M, B, T, N, T, C, ldc, tn_part, L.tn_floats, s);
     };
-    hipError_t x = hero::launch_to_f32_transpose(D.dtype, hbar, T, D.d, D.d, hbT, T, s);
+    hipError_t x = hipSuccess;
+    if (D.dtype == HERO_BF16) {
+      // dW_hd, dpsi_1 = dP^T hbar and dL/dhbar_j += dP [W_hd; psi_1] on the GEMM core: hbar and the
+      // weights are exact in bf16, dP enters as bf16 hi + lo (two accumulating products each)
+      const int kp = L.kp;
+      unsigned char *ph = ws + L.dPT_hi, *pl = ws + L.dPT_lo, *qh = ws + L.dP_hi, *ql = ws + L.dP_lo;
+      unsigned char *h16 = ws + L.hbT16, *w16 = ws + L.wT16;
+      const size_t re = static_cast<size_t>(D.d_e) * kp * 2;
+      x = hero::launch_split_bf16(a.dPT, NP, T, T, ph, pl, kp, s);
+      if (x == hipSuccess) x = hero::launch_transpose(D.dtype, hbar, T, D.d, D.d, h16, kp, kp, s);
+      for (unsigned char* part : {ph, pl}) {
+        if (x == hipSuccess)
+          x = hero::launch_gemm_nt_acc_bf16(part, kp, D.d_e, h16, kp, D.d, kp, grads->w_hd, D.d, s);
+        if (x == hipSuccess)
+          x = hero::launch_gemm_nt_acc_bf16(part + re, kp, D.d_head, h16, kp, D.d, kp, grads->ps1, D.d, s);
+      }
+      if (x == hipSuccess) x = hero::launch_split_bf16(a.dP, T, NP, NP, qh, ql, NP, s);
+      if (x == hipSuccess) x = hero::launch_transpose(D.dtype, router->w_hd, D.d_e, D.d, D.d, w16, NP, D.d_e, s);
+      if (x == hipSuccess)
+        x = hero::launch_transpose(D.dtype, router->ps1, D.d_head, D.d, D.d, w16 + static_cast<size_t>(D.d_e) * 2, NP,
+                                   D.d_head, s);
+      for (unsigned char* part : {qh, ql})
+        if (x == hipSuccess) x = hero::launch_gemm_nt_acc_bf16(part, NP, T, w16, NP, D.d, NP, dhbar, D.d, s);
+    } else {
+      x = hero::launch_to_f32_transpose(D.dtype, hbar, T, D.d, D.d, hbT, T, s);
+      if (x == hipSuccess) x = acc(a.dPT, D.d_e, hbT, D.d, grads->w_hd, D.d);
+      if (x == hipSuccess) x = acc(a.dPT + static_cast<size_t>(D.d_e) * T, D.d_head, hbT, D.d, grads->ps1, D.d);
+      if (x == hipSuccess) x = hero::launch_to_f32_transpose(D.dtype, router->w_hd, D.d_e, D.d, D.d, wT, NP, s);
+      if (x == hipSuccess)
+        x = hero::launch_to_f32_transpose(D.dtype, router->ps1, D.d_head, D.d, D.d, wT + D.d_e, NP, s);
+      if (x == hipSuccess) x = hero::launch_gemm_acc_f32(a.dP, NP, T, wT, NP, D.d, NP, dhbar, D.d, s);
+    }
     if (x == hipSuccess) x = acc(a.dQT, D.d_m, a.XT, D.d_s, grads->w_q, D.d_s);
     if (x == hipSuccess) x = acc(a.dKT, D.d_m, a.XT, D.d_s, grads->w_k, D.d_s);
     if (x == hipSuccess) x = acc(a.dVT, D.d_m, a.XT, D.d_s, grads->w_v, D.d_s);
@@ -1322,12 +1377,6 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
     if (x == hipSuccess) x = acc(a.dPPT, D.d_p, a.XPT, 6, grads->w_p1, 6);
     if (x == hipSuccess) x = acc(a.dZAT, D.d_a, a.SPT, D.d_p, grads->w_p2, D.d_p);
     if (x == hipSuccess) x = acc(a.dZHT, D.d_h, a.SHT, D.d_e, grads->w_hu, D.d_e);
-    if (x == hipSuccess) x = acc(a.dPT, D.d_e, hbT, D.d, grads->w_hd, D.d);
-    if (x == hipSuccess) x = acc(a.dPT + static_cast<size_t>(D.d_e) * T, D.d_head, hbT, D.d, grads->ps1, D.d);
-    // the hidden encoder's and the local head's share of dL/dhbar_j: dP [W_hd; psi_1]
-    if (x == hipSuccess) x = hero::launch_to_f32_transpose(D.dtype, router->w_hd, D.d_e, D.d, D.d, wT, NP, s);
-    if (x == hipSuccess) x = hero::launch_to_f32_transpose(D.dtype, router->ps1, D.d_head, D.d, D.d, wT + D.d_e, NP, s);
-    if (x == hipSuccess) x = hero::launch_gemm_acc_f32(a.dP, NP, T, wT, NP, D.d, NP, dhbar, D.d, s);
     return x;
   });
   if (e != hipSuccess) return HERO_E_LAUNCH;

@@ -219,6 +219,21 @@ hipError_t launch_gemm_nt_f32(const void* A, int M, const void* B, int N, int K,
 hipError_t launch_gemm_acc_f32(const float* A, int lda, int M, const float* B, int ldb, int N, int K, float* C,
                                int ldc, hipStream_t s);
 
+// C[m][n] += sum_k A[m][k] B[n][k] on the bf16 GEMM core (fp32 accumulators; K a multiple of 64,
+// N of the tile's 128 columns, C rows 16-byte aligned)
+hipError_t launch_gemm_nt_acc_bf16(const void* A, int lda, int M, const void* B, int ldb, int N, int K, float* C,
+                                   int ldc, hipStream_t s);
+// C[m][n] += sum_k A[m][k] B[n][k] in fp32 for small M x N and long K (the tokens): K split into up to
+// tn_chunks(K) chunks of at least kTnChunk (as many as part_floats holds, nz M N), partial sums added
+// in chunk order
+constexpr int kTnChunk = 64;
+int tn_chunks(int K);
+hipError_t launch_gemm_tn_acc_f32(const float* A, int lda, int M, const float* B, int ldb, int N, int K, float* C,
+                                  int ldc, float* part, size_t part_floats, hipStream_t s);
+// x [R][C] fp32 (row pitch ld_in) as bf16 hi = bf16(x), lo = bf16(x - hi), [R][C_pad] with zero columns
+// from C to C_pad: hi + lo carries x to about 2^-16 relative
+hipError_t launch_split_bf16(const float* x, int R, int C, int ld_in, void* hi, void* lo, int C_pad, hipStream_t s);
+
 // Backward of the router at routed layer j (k_router_bwd.hip).
 struct RouterBwdArgs {
   int dtype, T, j, L_R, d, d_m, d_s, d_h, d_a, d_e, d_p, d_head, ld_th1;

@@ -1654,6 +1654,34 @@ struct EpiAccF32 {  // C[m][n] += acc
 };
 }  // namespace
 
+namespace {
+struct EpiAccF32Mfma {  // C[m][n] += acc on the MFMA path (each element owned by one lane)
+  float* out;
+  int ld;
+  struct Pre {};
+  __device__ __forceinline__ Pre prep(int, int) const { return {}; }
+  __device__ __forceinline__ void emit8(const Pre&, int m, int n, const float* v) const {
+    float* o = out + static_cast<size_t>(m) * ld + n;
+    f32x4 a = *reinterpret_cast<const f32x4*>(o), b = *reinterpret_cast<const f32x4*>(o + 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      a[i] += v[i];
+      b[i] += v[4 + i];
+    }
+    *reinterpret_cast<f32x4*>(o) = a;
+    *reinterpret_cast<f32x4*>(o + 4) = b;
+  }
+};
+}  // namespace
+
+hipError_t launch_gemm_nt_acc_bf16(const void* A, int lda, int M, const void* B, int ldb, int N, int K, float* C,
+                                   int ldc, hipStream_t s) {
+  if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
+  ARows<bf16_t> a{static_cast<const bf16_t*>(A), nullptr, lda};
+  BRows<bf16_t> b{static_cast<const bf16_t*>(B), nullptr, INT_MAX, ldb};
+  return run_tile<TileWide>(a, b, EpiAccF32Mfma{C, ldc}, nullptr, M, N, K, s);
+}
+
 hipError_t launch_gemm_acc_f32(const float* A, int lda, int M, const float* B, int ldb, int N, int K, float* C,
                                int ldc, hipStream_t s) {
   ARows<float> a{A, nullptr, lda};

@@ -14,12 +14,15 @@
 //   writes the gradient over P ([ir dL/dpre_h; dL/dpre_b], row- and token-major), the per-row
 //   coefficients of the RMSNorm and transition terms, and every (vector, token) pair the weight
 //   gradients need, token-contiguous, so that each weight gradient is one product with the
-//   tokens as K (run by the caller on the fp32 GEMM, fixed summation order).
+//   tokens as K (run by the caller with a fixed summation order: tn_part / tn_reduce below for the
+//   small ones, the GEMM core with dP split into bf16 hi + lo for dW_hd, dpsi_1 and dP [W_hd; psi_1]).
 // router_bwd_rows: dL/dhbar_j += c_norm hbar_j + ddelta_j, dL/dhbar_{j-1} += ddelta_{j-1} -
 //   ddelta_j, dL/dhbar_{j-2} -= ddelta_{j-1}, with ddelta_j = c1 delta_j + c2 delta_{j-1} and
 //   ddelta_{j-1} = c3 delta_j + c4 delta_{j-1}.
 // At j = 1 the state entering the layer is the initial one (S = 0, zeta = 0, p = m = 1) whatever
 // the buffers hold; the carried gradient written there is rho dL/dS_1 (the state is a constant).
+#include <algorithm>
+
 #include "hero_device.h"
 #include "hero_kernels.h"
 
@@ -49,25 +52,46 @@ __device__ float block_sum(float v, float* red) {
   return s;
 }
 
-// y[o] = sum_k w[o][k] x[k] for o < O (a wave per row, lanes over k)
+// y[o] = sum_k w[o][k] x[k] for o < O (a wave per row, lanes over k; four rows' loads in flight
+// before their reductions)
 template <typename W>
 __device__ void mv_rows(const W* w, int ld, int O, int I, const float* x, float* y) {
   const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
-  for (int o = wv; o < O; o += RB_NW) {
-    const W* r = w + static_cast<size_t>(o) * ld;
-    float acc = 0.0f;
-    for (int k = lane; k < I; k += kWave) acc = fmaf(ldf(r + k), x[k], acc);
-    acc = wave_sum(acc);
-    if (lane == 0) y[o] = acc;
+  for (int o0 = wv; o0 < O; o0 += 4 * RB_NW) {
+    float acc[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      acc[u] = 0.0f;
+      const int o = o0 + u * RB_NW;
+      if (o < O) {
+        const W* r = w + static_cast<size_t>(o) * ld;
+        for (int k = lane; k < I; k += kWave) acc[u] = fmaf(ldf(r + k), x[k], acc[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float v = wave_sum(acc[u]);
+      const int o = o0 + u * RB_NW;
+      if (lane == 0 && o < O) y[o] = v;
+    }
   }
 }
 
-// x[k] (+)= sum_o w[o][k] y[o] for k < I (a thread per column)
+// x[k] (+)= sum_o w[o][k] y[o] for k < I (a thread per column; sixteen loads issued before their
+// FMAs, which still add in ascending o)
 template <typename W>
 __device__ void mv_cols(const W* w, int ld, int O, int I, const float* y, float* x, bool accumulate) {
   for (int k = threadIdx.x; k < I; k += RB_NT) {
     float acc = accumulate ? x[k] : 0.0f;
-    for (int o = 0; o < O; ++o) acc = fmaf(ldf(w + static_cast<size_t>(o) * ld + k), y[o], acc);
+    int o = 0;
+    for (; o + 16 <= O; o += 16) {
+      float wv[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) wv[u] = ldf(w + static_cast<size_t>(o + u) * ld + k);
+#pragma unroll
+      for (int u = 0; u < 16; ++u) acc = fmaf(wv[u], y[o + u], acc);
+    }
+    for (; o < O; ++o) acc = fmaf(ldf(w + static_cast<size_t>(o) * ld + k), y[o], acc);
     x[k] = acc;
   }
 }
@@ -405,7 +429,93 @@ __global__ __launch_bounds__(256) void to_f32_transpose(const T* __restrict__ in
   }
 }
 
+// part[z][m][n] = sum_{k in chunk z} A[m][k] B[n][k] (64 x 64 output tiles, 4 x 4 per thread, every
+// access bounds-checked; chunk z covers k in [z kc, min(K, (z + 1) kc)))
+__global__ __launch_bounds__(256) void tn_part_kernel(const float* __restrict__ A, int lda, int M,
+                                                     const float* __restrict__ B, int ldb, int N, int K, int kc,
+                                                     float* __restrict__ part) {
+  __shared__ float As[16][68];
+  __shared__ float Bs[16][68];
+  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64, z = blockIdx.z;
+  const int k_lo = z * kc, k_hi = min(K, k_lo + kc);
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  float acc[4][4] = {};
+  for (int k0 = k_lo; k0 < k_hi; k0 += 16) {
+    for (int e = threadIdx.x; e < 64 * 16; e += 256) {
+      const int r = e >> 4, kk = e & 15, k = k0 + kk;
+      As[kk][r] = (m0 + r < M && k < k_hi) ? A[static_cast<size_t>(m0 + r) * lda + k] : 0.0f;
+      Bs[kk][r] = (n0 + r < N && k < k_hi) ? B[static_cast<size_t>(n0 + r) * ldb + k] : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) acc[i][jj] = fmaf(As[kk][ty * 4 + i], Bs[kk][tx * 4 + jj], acc[i][jj]);
+    __syncthreads();
+  }
+  float* P = part + static_cast<size_t>(z) * M * N;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + jj;
+      if (m < M && n < N) P[static_cast<size_t>(m) * N + n] = acc[i][jj];
+    }
+}
+
+// C[m][n] += sum_z part[z][m][n], z in order
+__global__ __launch_bounds__(256) void tn_reduce_kernel(const float* __restrict__ part, int nz, int M, int N,
+                                                       float* __restrict__ C, int ldc) {
+  const size_t e = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= static_cast<size_t>(M) * N) return;
+  float v = 0.0f;
+  for (int z = 0; z < nz; ++z) v += part[static_cast<size_t>(z) * M * N + e];
+  const size_t m = e / N, n = e % N;
+  C[m * ldc + n] += v;
+}
+
+__global__ __launch_bounds__(256) void split_bf16_kernel(const float* __restrict__ x, int R, int C, int ld_in,
+                                                        bf16_t* __restrict__ hi, bf16_t* __restrict__ lo, int C_pad) {
+  const size_t n = static_cast<size_t>(R) * C_pad;
+  for (size_t e = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; e < n;
+       e += static_cast<size_t>(gridDim.x) * 256) {
+    const size_t r = e / C_pad;
+    const int c = static_cast<int>(e % C_pad);
+    const float v = c < C ? x[r * ld_in + c] : 0.0f;
+    const bf16_t h = f32_to_bf16(v);
+    hi[e] = h;
+    lo[e] = f32_to_bf16(v - bf16_to_f32(h));
+  }
+}
+
 }  // namespace
+
+int tn_chunks(int K) { return (K + kTnChunk - 1) / kTnChunk; }
+
+hipError_t launch_gemm_tn_acc_f32(const float* A, int lda, int M, const float* B, int ldb, int N, int K, float* C,
+                                  int ldc, float* part, size_t part_floats, hipStream_t s) {
+  if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
+  // as many K chunks of at least kTnChunk as the partial buffer holds for this M x N
+  const size_t mn = static_cast<size_t>(M) * N;
+  const int nz = static_cast<int>(std::max<size_t>(1, std::min<size_t>(tn_chunks(K), part_floats / mn)));
+  const int kc = ((K + nz - 1) / nz + 15) / 16 * 16;
+  tn_part_kernel<<<dim3((N + 63) / 64, (M + 63) / 64, nz), 256, 0, s>>>(A, lda, M, B, ldb, N, K, kc, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t n = static_cast<size_t>(M) * N;
+  tn_reduce_kernel<<<static_cast<unsigned>((n + 255) / 256), 256, 0, s>>>(part, nz, M, N, C, ldc);
+  return hipGetLastError();
+}
+
+hipError_t launch_split_bf16(const float* x, int R, int C, int ld_in, void* hi, void* lo, int C_pad, hipStream_t s) {
+  const size_t n = static_cast<size_t>(R) * C_pad;
+  if (n == 0) return hipSuccess;
+  const unsigned blocks = static_cast<unsigned>(std::min<size_t>((n + 255) / 256, 8192));
+  split_bf16_kernel<<<blocks, 256, 0, s>>>(x, R, C, ld_in, static_cast<bf16_t*>(hi), static_cast<bf16_t*>(lo), C_pad);
+  return hipGetLastError();
+}
 
 size_t router_bwd_vector_floats(int d_m, int d_s, int d_h, int d_a, int d_e, int d_p, int d_head) {
   // XT, dQT, dKT, dVT, dU1T, dU2T, dPAT, SAT, DA, DB, SBT, dPPT, SPT, XPT, dZAT, dZHT, SHT

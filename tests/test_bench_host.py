@@ -98,3 +98,17 @@ def test_cpu_baseline_repeats_a_short_whole_call():
     r = bench.cpu_baseline(prob, {"mask": ref.use_ffn, "lam": ref.lam}, 3, target_s=30.0)
     assert r["kind"] == "oracle" and r["value"] > 0
     assert r["sample"].startswith(f"{w.T} of {w.T} tokens") and "run 8 times" in r["sample"]
+
+
+def test_router_backward_work_counts():
+    """The router backward's algorithmic work at the Llama-3.1-8B layer: the recomputed
+    pre-activations 2 T d (d_e + d_head) FLOP; the products 4 T (d_e + d_head) d FLOP plus the small
+    weights'; the token pass streams S_{j-1} once and dL/dS in and out (3 x 64 KiB per token)."""
+    from paper_2609_08189_amd import synth
+    w = synth.WORKLOADS["llama31_8b_layer"]
+    wk = bench.router_backward_work(w, w.layer_j)
+    assert set(wk) == set(bench.RBWD_KERNELS)
+    assert wk["router_bwd_gemm"]["flops"] == 2 * 4096 * 4096 * 512
+    assert 4 * 4096 * 512 * 4096 < wk["router_bwd_products"]["flops"] < 1.1 * 4 * 4096 * 512 * 4096
+    assert wk["router_bwd_token"]["bytes"] > 4096 * 3 * 128 * 128 * 4
+    assert bench.router_backward_work(w, 1)["router_bwd_token"]["bytes"] < wk["router_bwd_token"]["bytes"]
