@@ -499,7 +499,8 @@ int hero_router_backward_workspace_size(const hero_dims *dims, int T, size_t *by
  *   - writes dL/deta_j into deta[0] (device fp32; rho_j = sigma(eta));
  *   - turns carry into the gradient over the state the layer received.
  * state_in is the router state entering layer j (fp32 S, zeta, p, m as the forward call read
- * them; ignored at j = 1, where the state is the initial one and carry's return is rho dL/dS_1).
+ * them; not read at j = 1, where the state is the initial one and may be NULL, and carry's
+ * return there is rho dL/dS_1).
  * hbar_prev1 / hbar_prev2: as in hero_routed_layer.  The full router with S in fp32
  * (dims->state_dtype HERO_F32, else HERO_E_UNSUPPORTED); branch decisions are constants.
  * Deterministic: every sum runs in a fixed order.

@@ -1204,7 +1204,7 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
   if (!(eta == eta)) return HERO_E_RANGE;
   if (!hbar || !dlogit || !carry || !dhbar || !grads || !deta) return HERO_E_NULL;
   if ((j >= 2 && (!hbar_prev1 || !dhbar_prev1)) || (j >= 3 && (!hbar_prev2 || !dhbar_prev2))) return HERO_E_NULL;
-  if ((st = check_state(state_in)) != HERO_OK) return st;
+  if ((j > 1 || state_in) && (st = check_state(state_in)) != HERO_OK) return st;   // not read at j = 1
   if ((st = check_router(router)) != HERO_OK) return st;
   const float* gp[] = {grads->w_hd, grads->w_hu, grads->w_p1, grads->w_p2, grads->w_q, grads->w_k, grads->w_v,
                        grads->w_n, grads->w_c, grads->th1, grads->th2, grads->ps1, grads->ps2};
@@ -1279,10 +1279,10 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
   a.th1 = router->th1;
   a.th2 = router->th2;
   a.ps2 = router->ps2;
-  a.S_in = static_cast<const float*>(state_in->S);
-  a.zeta_in = state_in->zeta;
-  a.p_in = state_in->p_hist;
-  a.m_in = state_in->m_hist;
+  a.S_in = state_in ? static_cast<const float*>(state_in->S) : nullptr;
+  a.zeta_in = state_in ? state_in->zeta : nullptr;
+  a.p_in = state_in ? state_in->p_hist : nullptr;
+  a.m_in = state_in ? state_in->m_hist : nullptr;
   a.dlogit = dlogit;
   a.dS = carry->dS;
   a.dzeta = carry->dzeta;

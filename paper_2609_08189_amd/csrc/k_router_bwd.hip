@@ -176,8 +176,9 @@ __global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
   mv_rows(static_cast<const T*>(a.w_n), d_s, DM, d_s, xth, qkvu[3]);
   __syncthreads();
   // memory read c = phi(q)^T S_{j-1} / (phi(q)^T zeta_{j-1} + eps)
-  const float* Sin = a.S_in + static_cast<size_t>(t) * DM * DM;
-  const float* zin = a.zeta_in + static_cast<size_t>(t) * DM;
+  // the received state is read only from j = 2 (it may be absent at j = 1)
+  const float* Sin = j > 1 ? a.S_in + static_cast<size_t>(t) * DM * DM : nullptr;
+  const float* zin = j > 1 ? a.zeta_in + static_cast<size_t>(t) * DM : nullptr;
   float den = 0.0f;
   for (int k = tid; k < DM; k += RB_NT) den += j > 1 ? phif_(qkvu[0][k]) * zin[k] : 0.0f;
   den = block_sum(den, red) + a.eps;

@@ -413,3 +413,6 @@ def test_router_backward_entry_validates():
     assert call(st=st2) == H.HERO_E_ALIAS
     assert call(n=need - 1) == H.HERO_E_WORKSPACE
     assert call(ws=None) == H.HERO_E_WORKSPACE
+    # the received state is not read at j = 1 and may be absent there, not later
+    assert call(j=1, st=None, h1=None, h2=None, dh1=None, dh2=None, ws=None) == H.HERO_E_WORKSPACE
+    assert call(j=2, st=None) == H.HERO_E_NULL

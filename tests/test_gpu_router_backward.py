@@ -118,3 +118,35 @@ def test_router_backward_llama31_8b_layer_full_shape():
     every token, every weight gradient."""
     w = synth.WORKLOADS["llama31_8b_layer"]
     _run(w, w.layer_j, seed=3)
+
+
+def test_router_backward_first_layer_without_state():
+    """At j = 1 the received state is the initial one and need not be passed: the same results with
+    and without it, bit for bit."""
+    import torch
+    from paper_2609_08189_amd import hero as H
+    from paper_2609_08189_amd.device import DeviceProblem, DeviceRouterBackward
+    w = BF16.replace(T=77)
+    prob = synth.make_problem(w, seed=51, layer_j=1)
+    rng = np.random.default_rng(52)
+    T, dm = w.T, w.d_m
+    args = (rng.standard_normal(T).astype(np.float32), (0.05 * rng.standard_normal((T, dm, dm))).astype(np.float32),
+            (0.1 * rng.standard_normal((T, dm))).astype(np.float32), rng.standard_normal(T).astype(np.float32),
+            rng.standard_normal(T).astype(np.float32))
+    dp = DeviceProblem(prob, stats=False)
+    outs = []
+    for with_state in (True, False):
+        rb = DeviceRouterBackward(dp, 1, *args)
+        if not with_state:
+            dp.state_s, saved = None, dp.state_s
+        rb.run()
+        if not with_state:
+            dp.state_s = saved
+        outs.append(rb.results())
+    a, b = outs
+    for k in ("dhbar", "dS", "dzeta", "dp", "dm"):
+        np.testing.assert_array_equal(a[k], b[k])
+    for k in a["grads"]:
+        np.testing.assert_array_equal(a["grads"][k], b["grads"][k])
+    del dp
+    torch.cuda.empty_cache()
