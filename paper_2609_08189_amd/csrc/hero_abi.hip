@@ -1230,16 +1230,14 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
     return HERO_E_ALIAS;
   const RouterBwdLayout L = router_bwd_layout_of(D, T);
   if (!workspace || workspace_bytes < L.total) return HERO_E_WORKSPACE;
-  const void* in_out[][2] = {{carry->dS, reinterpret_cast<const void*>(sb)},
-                             {carry->dzeta, reinterpret_cast<const void*>(zb)},
-                             {carry->dp, reinterpret_cast<const void*>(tb)},
-                             {carry->dm, reinterpret_cast<const void*>(tb)},
-                             {dhbar, reinterpret_cast<const void*>(hb)},
-                             {j >= 2 ? dhbar_prev1 : nullptr, reinterpret_cast<const void*>(hb)},
-                             {j >= 3 ? dhbar_prev2 : nullptr, reinterpret_cast<const void*>(hb)},
-                             {deta, reinterpret_cast<const void*>(static_cast<size_t>(4))}};
-  for (const auto& x : in_out)
-    if (overlap(workspace, L.total, x[0], reinterpret_cast<size_t>(x[1]))) return HERO_E_ALIAS;
+  struct Span {
+    const void* p;
+    size_t bytes;
+  };
+  const Span written[] = {{carry->dS, sb}, {carry->dzeta, zb}, {carry->dp, tb}, {carry->dm, tb}, {dhbar, hb},
+                          {j >= 2 ? dhbar_prev1 : nullptr, hb}, {j >= 3 ? dhbar_prev2 : nullptr, hb}, {deta, 4}};
+  for (const Span& x : written)
+    if (overlap(workspace, L.total, x.p, x.bytes)) return HERO_E_ALIAS;
   if ((st = check_device()) != HERO_OK) return st;
 
   const hipStream_t s = static_cast<hipStream_t>(stream);
