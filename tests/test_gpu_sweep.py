@@ -117,3 +117,59 @@ def test_block_backward_sweep(k):
     w, seed, gin, bm = BWD_CASES[k]
     print(f"backward sweep case {k}", flush=True)
     _run_small(w, seed, dgate_in=gin, budget_mode=bm)
+
+
+def _rbwd_cases(n_bf16=6, n_f32=4, seed=20262):
+    """Router backward over drawn router shapes (sub-network widths, memory width, layer index,
+    token count), fp32 state storage (the only one the backward accepts)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n_bf16 + n_f32):
+        bf16 = i < n_bf16
+        if bf16:
+            d = int(rng.choice([256, 512, 768, 1024]))
+            d_e = int(rng.choice([64, 128, 192, 256]))
+            d_head = int(rng.choice([x for x in (64, 128, 192, 256) if (d_e + x) % 128 == 0]))
+            d_s = 8 * int(rng.integers(1, 17))
+        else:
+            d = int(rng.choice([128, 256, 384]))
+            d_e = int(rng.integers(8, 257))
+            d_head = int(rng.integers(8, 257))
+            d_s = int(rng.integers(2, 129))
+        d_h = int(rng.integers(1, d_s))
+        d_m = (32, 64, 128, 256)[i % 4]
+        L_R = int(rng.integers(2, 13))
+        j = int(rng.integers(1, L_R + 1)) if i % 2 else int(rng.integers(2, L_R + 1))
+        T = int(rng.integers(1, 600 if d_m < 256 else 160))
+        w = synth.Workload(f"rbwd_sweep{i}", "bf16" if bf16 else "f32", d=d, d_ff=256, d_r=32, L_R=L_R, d_m=d_m,
+                           T=T, mode="budget", budget=float(rng.uniform()), d_s=d_s, d_h=d_h, d_a=d_s - d_h,
+                           d_e=d_e, d_p=int(rng.integers(4, 129)), d_head=d_head)
+        out.append((w, j, int(rng.integers(0, 1 << 16))))
+    return out
+
+
+RBWD_CASES = _rbwd_cases()
+
+
+def test_router_backward_sweep_cases_are_valid_shapes():
+    import ctypes
+    from paper_2609_08189_amd import hero as H
+    from paper_2609_08189_amd.device import dims_struct
+    for w, j, _ in RBWD_CASES:
+        out = ctypes.c_size_t(0)
+        assert H.lib().hero_router_backward_workspace_size(ctypes.byref(dims_struct(w)), w.T,
+                                                           ctypes.byref(out)) == H.HERO_OK, w
+        assert 1 <= j <= w.L_R
+    assert {w.dtype for w, _, _ in RBWD_CASES} == {"bf16", "f32"}
+    assert {w.d_m for w, _, _ in RBWD_CASES} >= {32, 64, 128}
+    assert sum(j >= 3 for _, j, _ in RBWD_CASES) >= 4
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("k", range(len(RBWD_CASES)))
+def test_router_backward_sweep(k):
+    from tests.test_gpu_router_backward import _run as _run_rbwd
+    w, j, seed = RBWD_CASES[k]
+    print(f"router backward sweep case {k}: d_s={w.d_s} d_h={w.d_h} d_e={w.d_e} d_p={w.d_p} "
+          f"d_head={w.d_head} L_R={w.L_R}", flush=True)
+    _run_rbwd(w, j, seed=seed)
