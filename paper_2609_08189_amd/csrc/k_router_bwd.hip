@@ -52,48 +52,69 @@ __device__ float block_sum(float v, float* red) {
   return s;
 }
 
-// y[o] = sum_k w[o][k] x[k] for o < O (a wave per row, lanes over k; four rows' loads in flight
-// before their reductions)
+// y[o] = sum_k w[o][k] x[k] for o < O: G lanes per row (G = 16, or 8 for I <= 32), so one wave
+// works on 64 / G rows at once and each row's reduction takes log2(G) shuffles
+template <typename W, int G>
+__device__ void mv_rows_g(const W* w, int ld, int O, int I, const float* x, float* y) {
+  constexpr int R = kWave / G;
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave, gl = lane & (G - 1);
+  for (int o0 = wv * R; o0 < O; o0 += RB_NW * R) {   // uniform per wave
+    const int o = o0 + lane / G;
+    float acc = 0.0f;
+    if (o < O) {
+      const W* r = w + static_cast<size_t>(o) * ld;
+#pragma unroll 4
+      for (int k = gl; k < I; k += G) acc = fmaf(ldf(r + k), x[k], acc);
+    }
+#pragma unroll
+    for (int off = G / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, kWave);
+    if (gl == 0 && o < O) y[o] = acc;
+  }
+}
 template <typename W>
 __device__ void mv_rows(const W* w, int ld, int O, int I, const float* x, float* y) {
-  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
-  for (int o0 = wv; o0 < O; o0 += 4 * RB_NW) {
-    float acc[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      acc[u] = 0.0f;
-      const int o = o0 + u * RB_NW;
-      if (o < O) {
-        const W* r = w + static_cast<size_t>(o) * ld;
-        for (int k = lane; k < I; k += kWave) acc[u] = fmaf(ldf(r + k), x[k], acc[u]);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float v = wave_sum(acc[u]);
-      const int o = o0 + u * RB_NW;
-      if (lane == 0 && o < O) y[o] = v;
-    }
-  }
+  if (I > 32)
+    mv_rows_g<W, 16>(w, ld, O, I, x, y);
+  else
+    mv_rows_g<W, 8>(w, ld, O, I, x, y);
 }
 
 // x[k] (+)= sum_o w[o][k] y[o] for k < I (a thread per column; sixteen loads issued before their
-// FMAs, which still add in ascending o)
+// FMAs, which add in ascending o).  For I <= RB_NT / 2 the rows are split into RB_NT / I' parts
+// (I' = I rounded up to a power of two) whose partial sums meet in part, added in part order.
+// Every thread calls it; with the split it ends on a barrier.
 template <typename W>
-__device__ void mv_cols(const W* w, int ld, int O, int I, const float* y, float* x, bool accumulate) {
-  for (int k = threadIdx.x; k < I; k += RB_NT) {
-    float acc = accumulate ? x[k] : 0.0f;
-    int o = 0;
-    for (; o + 16 <= O; o += 16) {
-      float wv[16];
+__device__ float mv_cols_range(const W* w, int ld, int o_begin, int o_end, int k, const float* y, float acc) {
+  int o = o_begin;
+  for (; o + 16 <= o_end; o += 16) {
+    float wv[16];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) wv[u] = ldf(w + static_cast<size_t>(o + u) * ld + k);
+    for (int u = 0; u < 16; ++u) wv[u] = ldf(w + static_cast<size_t>(o + u) * ld + k);
 #pragma unroll
-      for (int u = 0; u < 16; ++u) acc = fmaf(wv[u], y[o + u], acc);
-    }
-    for (; o < O; ++o) acc = fmaf(ldf(w + static_cast<size_t>(o) * ld + k), y[o], acc);
-    x[k] = acc;
+    for (int u = 0; u < 16; ++u) acc = fmaf(wv[u], y[o + u], acc);
   }
+  for (; o < o_end; ++o) acc = fmaf(ldf(w + static_cast<size_t>(o) * ld + k), y[o], acc);
+  return acc;
+}
+template <typename W>
+__device__ void mv_cols(const W* w, int ld, int O, int I, const float* y, float* x, bool accumulate,
+                        float* part) {
+  int Ip = 1;
+  while (Ip < I) Ip <<= 1;
+  if (2 * Ip > RB_NT) {
+    for (int k = threadIdx.x; k < I; k += RB_NT) x[k] = mv_cols_range(w, ld, 0, O, k, y, accumulate ? x[k] : 0.0f);
+    return;
+  }
+  const int np = RB_NT / Ip, oc = (O + np - 1) / np;
+  const int k = threadIdx.x % Ip, q = threadIdx.x / Ip;
+  if (k < I) part[q * Ip + k] = mv_cols_range(w, ld, min(O, q * oc), min(O, (q + 1) * oc), k, y, 0.0f);
+  __syncthreads();
+  if (threadIdx.x < I) {
+    float acc = accumulate ? x[threadIdx.x] : 0.0f;
+    for (int u = 0; u < np; ++u) acc += part[u * Ip + threadIdx.x];
+    x[threadIdx.x] = acc;
+  }
+  __syncthreads();
 }
 
 template <typename T>
@@ -107,6 +128,7 @@ __global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
   __shared__ float qkvu[4][RB_MAXM];                // q, k, v (pre-activation), u1 = W_n s
   __shared__ float u2[RB_MAXM], du1[RB_MAXM], du2[RB_MAXM], dnum[RB_MAXM];
   __shared__ float dfk[RB_MAXM], dfq[RB_MAXM], dvw[RB_NW][RB_MAXM];
+  __shared__ float fq[RB_MAXM], part[RB_NT];      // phi(q); partial sums of mv_cols and the memory read
   const int t = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
   const int T_ = a.T, j = a.j, d = a.d, DM = a.d_m, d_s = a.d_s, d_h = a.d_h, d_a = a.d_a;
   const int d_e = a.d_e, d_p = a.d_p, d_head = a.d_head, NP = d_e + d_head, d_x = d_s + DM + 1;
@@ -180,13 +202,24 @@ __global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
   const float* Sin = j > 1 ? a.S_in + static_cast<size_t>(t) * DM * DM : nullptr;
   const float* zin = j > 1 ? a.zeta_in + static_cast<size_t>(t) * DM : nullptr;
   float den = 0.0f;
-  for (int k = tid; k < DM; k += RB_NT) den += j > 1 ? phif_(qkvu[0][k]) * zin[k] : 0.0f;
-  den = block_sum(den, red) + a.eps;
-  for (int v = tid; v < DM; v += RB_NT) {
+  for (int k = tid; k < DM; k += RB_NT) {
+    fq[k] = phif_(qkvu[0][k]);
+    den += j > 1 ? fq[k] * zin[k] : 0.0f;
+  }
+  den = block_sum(den, red) + a.eps;   // (its barriers also publish fq)
+  {
+    // RB_NT / DM parts of the k range (d_m is 32, 64, 128 or 256), added in part order
+    const int np = RB_NT / DM, kc = DM / np, v = tid % DM, q = tid / DM;
     float acc = 0.0f;
     if (j > 1)
-      for (int k = 0; k < DM; ++k) acc = fmaf(phif_(qkvu[0][k]), Sin[static_cast<size_t>(k) * DM + v], acc);
-    xth[d_s + v] = acc / den;
+      for (int k = q * kc; k < (q + 1) * kc; ++k) acc = fmaf(fq[k], Sin[static_cast<size_t>(k) * DM + v], acc);
+    part[tid] = acc;
+    __syncthreads();
+    for (int u = tid; u < DM; u += RB_NT) {
+      float c = 0.0f;
+      for (int r = 0; r < np; ++r) c += part[r * DM + u];
+      xth[d_s + u] = c / den;
+    }
   }
   __syncthreads();
   // history dissimilarity nu = 1 - cos(W_n s, W_c c)
@@ -235,7 +268,7 @@ __global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
   }
   __syncthreads();
   // [ds; dc; dnu] = f_theta's first layer transposed times dL/dpre_a
-  mv_cols(static_cast<const T*>(a.th1), a.ld_th1, d_head, d_x, dpa, dxth, false);
+  mv_cols(static_cast<const T*>(a.th1), a.ld_th1, d_head, d_x, dpa, dxth, false, part);
   for (int k = tid; k < d_x; k += RB_NT) colT(a.XT, k) = xth[k];
   __syncthreads();
   // nu's cosine backward (a constant at j = 1)
@@ -251,8 +284,8 @@ __global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
     }
   }
   __syncthreads();
-  mv_cols(static_cast<const T*>(a.w_n), d_s, DM, d_s, du1, dxth, true);            // ds += W_n^T du1
-  mv_cols(static_cast<const T*>(a.w_c), DM, DM, DM, du2, dxth + d_s, true);        // dc += W_c^T du2
+  mv_cols(static_cast<const T*>(a.w_n), d_s, DM, d_s, du1, dxth, true, part);            // ds += W_n^T du1
+  mv_cols(static_cast<const T*>(a.w_c), DM, DM, DM, du2, dxth + d_s, true, part);        // dc += W_c^T du2
   __syncthreads();
   // memory read: dL/dnum = dc / den, dL/dden = -<dc, c> / den (no read at j = 1)
   float dden = 0.0f;
@@ -270,7 +303,7 @@ __global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
 #pragma unroll
   for (int i = 0; i < RB_MAXM / kWave; ++i) dva[i] = 0.0f;
   for (int k = wv; k < DM; k += RB_NW) {
-    const float fqk = phif_(qkvu[0][k]), fkk = phif_(qkvu[1][k]);
+    const float fqk = fq[k], fkk = phif_(qkvu[1][k]);
     float sk = 0.0f, sq = 0.0f;
 #pragma unroll
     for (int i = 0; i < RB_MAXM / kWave; ++i) {
@@ -303,7 +336,7 @@ __global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
   for (int k = tid; k < DM; k += RB_NT) {
     const float g = dz[k];
     rho_acc = fmaf(g, j > 1 ? zin[k] : 0.0f, rho_acc);
-    dz[k] = fmaf(rho, g, phif_(qkvu[0][k]) * dden);
+    dz[k] = fmaf(rho, g, fq[k] * dden);
   }
   rho_acc = block_sum(rho_acc, red);
   if (tid == 0) a.rho_part[t] = rho_acc;
@@ -322,12 +355,12 @@ __global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
     colT(a.dVT, k) = dv;
   }
   __syncthreads();
-  mv_cols(static_cast<const T*>(a.w_q), d_s, DM, d_s, dfq, dxth, true);
-  mv_cols(static_cast<const T*>(a.w_k), d_s, DM, d_s, dfk, dxth, true);
-  mv_cols(static_cast<const T*>(a.w_v), d_s, DM, d_s, dnum, dxth, true);
+  mv_cols(static_cast<const T*>(a.w_q), d_s, DM, d_s, dfq, dxth, true, part);
+  mv_cols(static_cast<const T*>(a.w_k), d_s, DM, d_s, dfk, dxth, true, part);
+  mv_cols(static_cast<const T*>(a.w_v), d_s, DM, d_s, dnum, dxth, true, part);
   __syncthreads();
   // path encoder: dL/dSiLU(pre_p) = W_p2^T dz^a, then W_p1^T for the six features
-  mv_cols(static_cast<const T*>(a.w_p2), d_p, d_a, d_p, dxth + d_h, dpp, false);
+  mv_cols(static_cast<const T*>(a.w_p2), d_p, d_a, d_p, dxth + d_h, dpp, false, part);
   __syncthreads();
   for (int o = tid; o < d_p; o += RB_NT) {
     dpp[o] *= silu_grad_(ppre[o]);
@@ -338,9 +371,9 @@ __global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
   for (int o = tid; o < d_h; o += RB_NT) colT(a.dZHT, o) = dxth[o];
   if (tid < 6) colT(a.XPT, tid) = xp[tid];
   __syncthreads();
-  mv_cols(static_cast<const T*>(a.w_p1), 6, d_p, 6, dpp, dx, false);
+  mv_cols(static_cast<const T*>(a.w_p1), 6, d_p, 6, dpp, dx, false, part);
   // hidden encoder: dL/dSiLU(pre_h) = W_hu^T dz^h
-  mv_cols(static_cast<const T*>(a.w_hu), d_e, d_h, d_e, dxth, dsh, false);
+  mv_cols(static_cast<const T*>(a.w_hu), d_e, d_h, d_e, dxth, dsh, false, part);
   __syncthreads();
   float cn = 0.0f;
   for (int e = tid; e < d_e; e += RB_NT) {
