@@ -52,6 +52,13 @@ __device__ float block_sum(float v, float* red) {
   return s;
 }
 
+// w[i] with i a 32-bit element index from a workgroup-uniform base (the router weights are far below
+// 4 GiB), so the load takes the scalar base plus a 32-bit lane offset instead of 64-bit lane addresses
+template <typename W>
+__device__ __forceinline__ float ldw(const W* w, unsigned i) {
+  return ldf(reinterpret_cast<const W*>(reinterpret_cast<const char*>(w) + i * static_cast<unsigned>(sizeof(W))));
+}
+
 // y[o] = sum_k w[o][k] x[k] for o < O: G lanes per row (G = 16, or 8 for I <= 32), so one wave
 // works on 64 / G rows at once and each row's reduction takes log2(G) shuffles
 template <typename W, int G>
@@ -62,9 +69,9 @@ __device__ void mv_rows_g(const W* w, int ld, int O, int I, const float* x, floa
     const int o = o0 + lane / G;
     float acc = 0.0f;
     if (o < O) {
-      const W* r = w + static_cast<size_t>(o) * ld;
+      const unsigned r = static_cast<unsigned>(o) * ld;
 #pragma unroll 4
-      for (int k = gl; k < I; k += G) acc = fmaf(ldf(r + k), x[k], acc);
+      for (int k = gl; k < I; k += G) acc = fmaf(ldw(w, r + k), x[k], acc);
     }
 #pragma unroll
     for (int off = G / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, kWave);
@@ -89,11 +96,11 @@ __device__ float mv_cols_range(const W* w, int ld, int o_begin, int o_end, int k
   for (; o + 16 <= o_end; o += 16) {
     float wv[16];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) wv[u] = ldf(w + static_cast<size_t>(o + u) * ld + k);
+    for (int u = 0; u < 16; ++u) wv[u] = ldw(w, static_cast<unsigned>(o + u) * ld + k);
 #pragma unroll
     for (int u = 0; u < 16; ++u) acc = fmaf(wv[u], y[o + u], acc);
   }
-  for (; o < o_end; ++o) acc = fmaf(ldf(w + static_cast<size_t>(o) * ld + k), y[o], acc);
+  for (; o < o_end; ++o) acc = fmaf(ldw(w, static_cast<unsigned>(o) * ld + k), y[o], acc);
   return acc;
 }
 template <typename W>
