@@ -125,7 +125,7 @@ __device__ void mv_cols(const W* w, int ld, int O, int I, const float* y, float*
 }
 
 template <typename T>
-__global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
+__global__ __launch_bounds__(RB_NT) __attribute__((amdgpu_waves_per_eu(6))) void router_bwd_token(RouterBwdArgs a) {
   __shared__ float red[RB_NW];
   __shared__ float Ph[RB_MAXE], sh[RB_MAXE], dsh[RB_MAXE];
   __shared__ float Pb[RB_MAXH], pa[RB_MAXH], dpa[RB_MAXH];
@@ -135,7 +135,10 @@ __global__ __launch_bounds__(RB_NT) void router_bwd_token(RouterBwdArgs a) {
   __shared__ float qkvu[4][RB_MAXM];                // q, k, v (pre-activation), u1 = W_n s
   __shared__ float u2[RB_MAXM], du1[RB_MAXM], du2[RB_MAXM], dnum[RB_MAXM];
   __shared__ float dfk[RB_MAXM], dfq[RB_MAXM], dvw[RB_NW][RB_MAXM];
-  __shared__ float fq[RB_MAXM], part[RB_NT];      // phi(q); partial sums of mv_cols and the memory read
+  __shared__ float fq[RB_MAXM];                   // phi(q)
+  // partial sums of mv_cols and the memory read: dvw's first RB_NT floats, which hold dL/dv only from the
+  // memory pass to the q, k, v gradients, where no partial sum is live (26 KiB of LDS: six workgroups a CU)
+  float* const part = &dvw[0][0];
   const int t = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
   const int T_ = a.T, j = a.j, d = a.d, DM = a.d_m, d_s = a.d_s, d_h = a.d_h, d_a = a.d_a;
   const int d_e = a.d_e, d_p = a.d_p, d_head = a.d_head, NP = d_e + d_head, d_x = d_s + DM + 1;
