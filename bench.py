@@ -150,7 +150,11 @@ def cpu_baseline(prob, gpu_stats, j, target_s=12.0, max_tokens=None):
                       (f", run {reps} times" if reps > 1 else "") + f", {dt:.1f} s"}
 
 
-COUNTERS_MD = os.path.join(ROOT, "profiles", "routed_layer_llama31_8b_hbm_counters.md")
+# committed rocprofv3 FETCH_SIZE / WRITE_SIZE summaries, per workload
+COUNTERS_MD = {
+    "llama31_8b_layer": os.path.join(ROOT, "profiles", "routed_layer_llama31_8b_hbm_counters.md"),
+    "llama31_8b_stack": os.path.join(ROOT, "profiles", "routed_stack_llama31_8b_hbm_counters.md"),
+}
 GEMM_SOURCES = ("paper_2609_08189_amd/csrc/k_gemm.hip", "paper_2609_08189_amd/csrc/hero_device.h")
 
 
@@ -163,12 +167,13 @@ def gemm_source_hash():
     return h.hexdigest()
 
 
-def counted_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary
-    (scaled by the copy calibration there), or None when the GEMM sources changed since."""
+def counted_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the workload's committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary (scaled by the copy calibration there), or None when there is none or the
+    GEMM sources changed since it was taken."""
     try:
-        text = open(COUNTERS_MD).read()
-    except OSError:
+        text = open(COUNTERS_MD[workload]).read()
+    except (KeyError, OSError):
         return None
     if f"`{gemm_source_hash()}`" not in text:
         return None
@@ -226,17 +231,29 @@ def summarize_rocprof(root, window=None):
             print()
     counters = sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True))
     for path in counters:
-        agg = {}
+        agg, seq = {}, {}
         with open(path) as f:
-            for r in csv.DictReader(f):
+            for n, r in enumerate(csv.DictReader(f)):
                 key = (r["Kernel_Name"], r["Counter_Name"])
                 agg.setdefault(key, []).append(float(r["Counter_Value"]))
+                seq.setdefault(key, []).append((int(r.get("Dispatch_Id", n)), float(r["Counter_Value"])))
         print(f"### counters ({os.path.relpath(path, root)}), KiB per dispatch as reported\n")
         print("| kernel | counter | dispatches | mean | max |")
         print("|---|---|---|---|---|")
         for (k, c), v in sorted(agg.items()):
             print(f"| {_short(k)} | {c} | {len(v)} | {sum(v) / len(v):.1f} | {max(v):.1f} |")
         print()
+        if window is not None:
+            skip, count = window
+            print(f"### counters over dispatches {skip}..{skip + count - 1} of each kernel "
+                  f"({os.path.relpath(path, root)})\n")
+            print("| kernel | counter | dispatches | mean | max |")
+            print("|---|---|---|---|---|")
+            for (k, c), v in sorted(seq.items()):
+                sel = [x for _, x in sorted(v)][skip:skip + count]
+                if sel:
+                    print(f"| {_short(k)} | {c} | {len(sel)} | {sum(sel) / len(sel):.1f} | {max(sel):.1f} |")
+            print()
 
 
 _GRAPHS = []
@@ -698,57 +715,312 @@ def cpu_baseline_router_backward(w, prob, j, dl, dS, dz, dph, dmh, target_s=12.0
 
 # the paper's two Llama-3.1-8B operating points (Table 1: 26.87 % and 38.82 % skip)
 PAPER_SKIPS = (0.2687, 0.3882)
+# the router, compaction and memory kernels (timed and judged as one group against HBM)
+ROUTER_GROUP = ("rowstats", "router_gemm", "router_pre", "router_mem", "router_post", "select")
+BAND = 1e-3          # decision band on the gate around the layer's threshold
 
 
-def other_skip_point(dp, stats, w, j, budget, K, warmup):
-    """One more layer measurement at another skip budget on the same device problem (the inputs
-    do not depend on the budget; only the call's routing argument changes): tokens/s, the step time
-    and the dominant kernel's roofline fraction (HIP events on the call's stream)."""
+def measure_forward(w, dp, K, warmup, memory="matrix", graph=False, kernels=True):
+    """Time K steps of the workload's call (a hero_routed_layer call at the workload's j, or one
+    hero_routed_stack call) with every input resident in HBM.
+
+    One checked call with the optional stats outputs comes first (realized branch sizes, masks,
+    logits, lambda per layer); the timed steps run without them.  The dominant kernel (FFN gate/up)
+    is bracketed live by HIP events on the call's stream.  With kernels=True a second, untimed pass
+    instruments every kernel of the layer for the per-kernel table."""
     import torch
     from paper_2609_08189_amd import hero as H
-    saved_budget, saved_stats = dp.routing_s.budget, dp.stats
-    dp.routing_s.budget = budget
+    stack = w.layer_j <= 0
+    j = w.layer_j
+    L = w.L_R if stack else 1
+    stream = dp.stream()
+    ev = HipEvents()
+    step = dp.run_stack if stack else (lambda: dp.run_layer(j))
+    stats_saved = dp.stats
+    step()
+    torch.cuda.synchronize()
+    layer_stats = [s.host() for s in dp.stats]
+    nfs = [ls["n_ffn"] for ls in layer_stats]
+    nas = [ls["n_ad"] for ls in layer_stats]
+    dp.stats = None
     try:
-        stream = dp.stream()
-        ev = HipEvents()
-        dp.stats = stats
-        dp.run_layer(j)
-        torch.cuda.synchronize()
-        st = dp.stats[0].host()
-        dp.stats = None
         for _ in range(warmup):
-            dp.run_layer(j)
-        dom = "ffn_gate_up"
-        ks, ke = ev.create(K), ev.create(K)
-        t0, t1 = ev.create(2)
-        H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
+            step()
         torch.cuda.synchronize()
-        ev.record(t0, stream)
-        for _ in range(K):
-            dp.run_layer(j)
-        ev.record(t1, stream)
+        dom = "ffn_gate_up"
+        n_dom = K * sum(1 for x in nfs if x > 0)   # launches of the dominant kernel in the timed steps
+        run = graphed(step) if graph else step
+        ks, ke = ev.create(n_dom), ev.create(n_dom)
+        if not graph:
+            H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
+        t_start, t_stop = ev.create(2)
+        torch.cuda.synchronize()
+        marks = ev.create(K - 1)            # step boundaries inside the timed region
+        ev.record(t_start, stream)
+        for i in range(K):
+            run()
+            if i < K - 1:
+                ev.record(marks[i], stream)
+        ev.record(t_stop, stream)
         torch.cuda.synchronize()
         H.hero_kernel_timer(H.HERO_K[dom], [], [])
-        ms = ev.elapsed_ms(t0, t1) / K
-        dom_us = 1000.0 * sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
-        ev.destroy(ks + ke + [t0, t1])
+        total_ms = ev.elapsed_ms(t_start, t_stop)
+        bounds = [t_start] + marks + [t_stop]
+        step_ms = sorted(ev.elapsed_ms(a, b) for a, b in zip(bounds[:-1], bounds[1:]))
+        dom_ms_step = 0.0 if graph else sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
+        ev.destroy(ks + ke + [t_start, t_stop] + marks)
+        ms_step = total_ms / K
+
+        layers = list(range(1, L + 1)) if stack else [j]
+        works = [kernel_work(w, nf, na, w.T, jj, memory) for nf, na, jj in zip(nfs, nas, layers)]
+        if w.ablation & 12:            # no memory pass under the memory-less ablations
+            for wk in works:
+                wk["router_mem"] = dict(flops=0, bytes=0)
+        per = {}
+        if kernels or graph:
+            names = [k for k in H.KERNELS[:H.HERO_K["adapter_up"] + 1]
+                     if not (k == "router_mem" and w.ablation & 12)]
+            handles = {}
+            for name in names:
+                a, b = ev.create(K * L), ev.create(K * L)
+                handles[name] = (a, b)
+                H.hero_kernel_timer(H.HERO_K[name], a, b)
+            for _ in range(K):
+                step()
+            torch.cuda.synchronize()
+            for name in names:
+                H.hero_kernel_timer(H.HERO_K[name], [], [])
+                a, b = handles[name]
+                active = [i for i in range(L) if not ((name.startswith("ffn") and nfs[i] == 0) or
+                                                       (name.startswith("adapter") and nas[i] == 0))]
+                if active:
+                    n_launch = K * len(active)
+                    us = 1000.0 * sum(ev.elapsed_ms(x, y) for x, y in zip(a[:n_launch], b[:n_launch])) / n_launch
+                    fl = sum(works[i][name]["flops"] for i in active) / len(active)
+                    by = sum(works[i][name]["bytes"] for i in active) / len(active)
+                    per[name] = {"us": round(us, 2), "tflops": round(fl / us * 1e-6, 1) if fl else None,
+                                 "gbs": round(by / us * 1e-3, 1)}
+                ev.destroy(a + b)
+        if graph:
+            dom_ms_step = per[dom]["us"] * sum(1 for x in nfs if x > 0) / 1000.0
     finally:
-        dp.routing_s.budget, dp.stats = saved_budget, saved_stats
-    wb = w.replace(budget=budget)
-    fl = kernel_work(wb, st["n_ffn"], st["n_ad"], wb.T, j)[dom]["flops"]
-    peak = PEAK_BF16_TFLOPS if wb.dtype == "bf16" else PEAK_F32_TFLOPS
-    return {"budget": budget, "value": round(wb.T / (ms * 1e-3), 1), "unit": "tokens/s",
-            "ms_per_step": round(ms, 4), "steps": K, "n_ffn": st["n_ffn"], "n_adapter": st["n_ad"],
-            "ffn_gate_up_us": round(dom_us, 2),
-            "ffn_gate_up_frac": round(fl / (dom_us * 1e-6) * 1e-12 / peak, 4)}
+        dp.stats = stats_saved
+    return dict(ms_step=ms_step, step_ms=step_ms, dom_ms_step=dom_ms_step, layer_stats=layer_stats,
+                nfs=nfs, nas=nas, works=works, per=per, K=K, L=L, stack=stack, j=j)
+
+
+def dominant_roofline(w, m, traffic=None):
+    """Roofline of the FFN gate/up product: algorithmic work per step over its live-timed duration,
+    against the tighter roof for the row count (MFMA at prefill sizes, HBM for decode batches)."""
+    dom = "ffn_gate_up"
+    nfs, K = m["nfs"], m["K"]
+    dflops = sum(wk[dom]["flops"] for wk in m["works"])          # per step
+    dbytes = sum(wk[dom]["bytes"] for wk in m["works"])
+    peak_f = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    n_launch_step = max(1, sum(1 for x in nfs if x > 0))
+    dom_ms = m["dom_ms_step"]
+    hbm_bound = dbytes / (PEAK_HBM_GBS * 1e9) > dflops / (peak_f * 1e12)
+    if hbm_bound:
+        achieved, peak, unit = dbytes / (dom_ms * 1e-3) * 1e-9, PEAK_HBM_GBS, "GB/s"
+        per_unit = "weights 2*d*d_ff*2 B per launch + (d + d_ff)*2 B per FFN token"
+        total = f"{dbytes / n_launch_step / 1e6:.1f} MB"
+    else:
+        achieved, peak, unit = dflops / (dom_ms * 1e-3) * 1e-12, peak_f, "TFLOP/s"
+        per_unit = "4*d*d_ff FLOP per FFN token"
+        total = f"{dflops / n_launch_step / 1e9:.1f} GFLOP"
+    nf_mean = sum(nfs) / n_launch_step
+    return {"bound": "hbm" if hbm_bound else "mfma", "achieved": round(achieved, 1), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
+            "kernel": dom, "avg_launch_us": round(dom_ms * 1e3 / n_launch_step, 2),
+            "launches_per_step": n_launch_step,
+            "work_per_launch": f"{per_unit} x {nf_mean:.0f} FFN tokens = {total}",
+            "traffic_note": "HBM bytes read + written per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1, "
+                            "calibrated on a 1 GiB copy) from profiles/, null if the GEMM sources changed "
+                            "since or for workloads the counters were not taken on"}
+
+
+def router_group(m):
+    """The router, compaction and memory kernels as one group: algorithmic bytes of a mean layer
+    over the group's summed mean launch times, against the HBM peak."""
+    per, works = m["per"], m["works"]
+    if not all(k in per for k in ROUTER_GROUP if k != "router_mem") or not per:
+        return None
+    names = [k for k in ROUTER_GROUP if k in per]
+    us = sum(per[k]["us"] for k in names)
+    by = sum(wk[k]["bytes"] for wk in works for k in names) / len(works)
+    return {"kernels": names, "us": round(us, 2), "bytes": int(by), "gbs": round(by / us * 1e-3, 1),
+            "frac_hbm": round(by / us * 1e-3 / PEAK_HBM_GBS, 4)}
+
+
+def routing_report(w, layer_stats):
+    """Realized skip per layer and the number of tokens whose gate lies within BAND of the layer's
+    threshold (sigma(lambda_j) in budget mode, tau in threshold mode): decisions the rounding of
+    the logit could flip."""
+    import numpy as np
+    skip, band, lam = [], [], []
+    for ls in layer_stats:
+        T = ls["n_ffn"] + ls["n_ad"]
+        skip.append(round(ls["n_ad"] / max(T, 1), 5))
+        g = 1.0 / (1.0 + np.exp(-ls["logit"].astype(np.float64)))
+        thr = 1.0 / (1.0 + math.exp(-ls["lam"])) if w.mode == "budget" else w.tau
+        band.append(int(np.sum(np.abs(g - thr) < BAND)))
+        lam.append(round(ls["lam"], 6))
+    out = {"mode": w.mode, "realized_skip_per_layer": skip,
+           "realized_skip_mean": round(sum(skip) / len(skip), 5),
+           "band_count_per_layer": band, "band_count_total": sum(band), "band": BAND}
+    if w.mode == "budget":
+        out["lambda_per_layer"] = lam
+    return out
+
+
+def cpu_baseline_stack(prob, layer_stats, n_tokens=256, target_s=12.0, single_tokens=16):
+    """Time the float64 oracle on a token sample of the stack call: n_tokens spread evenly over the
+    sequences go through all L_R layers, teacher-forced at each layer to the GPU's branch decision
+    (and, in budget mode, given the GPU's lambda_j in place of the sample's own quantile).  Tokens are
+    independent given these, so tokens/s of the sample is the oracle's rate on the whole call.  The
+    weights' float64 decoding is data preparation and is not timed.  A one-thread figure runs
+    single_tokens tokens through the first two layers with BLAS held to one thread, scaled to L_R
+    layers."""
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+    from oracle import hero_oracle as O
+    from tests.oracle_inputs import adapter_of, dims_of, ffn_of, router_of
+
+    w = prob.w
+    T = prob.hbar.shape[0]
+    dims, R = dims_of(w), router_of(prob)
+    beta_all = None if prob.beta is None else prob.beta.astype("f8")
+
+    def chain(rows, n_layers):
+        h = prob.hbar.f64[rows]
+        prev1 = prev2 = None
+        st = O.State.initial(len(rows), w.d_m)
+        beta = None if beta_all is None else beta_all[rows]
+        dt = 0.0
+        for jj in range(1, n_layers + 1):
+            F, A = ffn_of(prob.ffn[jj - 1]), adapter_of(prob.adapter[jj - 1])
+            ls = layer_stats[jj - 1]
+            t0 = time.perf_counter()
+            res = O.routed_layer(jj, dims, h, prev1, prev2, st, F, R, A, float(prob.eta[jj - 1]),
+                                 mode=w.mode, budget=w.budget, tau=w.tau, beta=beta,
+                                 forced_ffn=ls["mask"][rows],
+                                 lam_given=ls["lam"] if w.mode == "budget" else None)
+            dt += time.perf_counter() - t0
+            prev2, prev1, h, st = prev1, h, res.h, res.state
+        return dt
+
+    rows = np.linspace(0, T - 1, min(n_tokens, T)).astype(np.int64)
+    dt = chain(rows, w.L_R)
+    reps = 1
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    with threadpool_limits(limits=1):
+        srows = rows[:: max(1, len(rows) // single_tokens)][:single_tokens]
+        n1 = min(2, w.L_R)
+        dt1 = chain(srows, n1) * w.L_R / n1
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), cpu_model)
+    except OSError:
+        pass
+    return {"value": round(len(rows) * reps / dt, 2), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "nproc": os.cpu_count(), "omp_num_threads": os.environ.get("OMP_NUM_THREADS"), "cpu_model": cpu_model,
+            "single_thread_value": round(len(srows) / dt1, 3),
+            "sample": f"{len(rows)} of {T} tokens spread evenly over the {w.batch} sequences, through all "
+                      f"{w.L_R} routed layers of the stack call (router, memory, branch; float64 numpy), each "
+                      f"layer teacher-forced to the GPU's branch decisions" +
+                      (" and lambda_j" if w.mode == "budget" else "") + f": {dt:.1f} s on {threads} BLAS threads; "
+                      f"single thread: {len(srows)} tokens through layers 1-{n1}, scaled by {w.L_R}/{n1}"}
+
+
+def other_skip_point(w, dp, budget, K, warmup):
+    """The same call measured at another skip budget on the same device problem (the inputs do not
+    depend on the budget; only the call's routing argument changes): tokens/s, the step time, branch
+    sizes and the dominant kernel's roofline fraction."""
+    saved_budget = dp.routing_s.budget
+    dp.routing_s.budget = budget
+    try:
+        m = measure_forward(w.replace(budget=budget), dp, K, warmup, kernels=False)
+    finally:
+        dp.routing_s.budget = saved_budget
+    roof = dominant_roofline(w.replace(budget=budget), m)
+    return {"budget": budget, "value": round(w.T / (m["ms_step"] * 1e-3), 1), "unit": "tokens/s",
+            "ms_per_step": round(m["ms_step"], 4), "steps": K, "n_ffn": sum(m["nfs"]),
+            "n_adapter": sum(m["nas"]), "ffn_gate_up_us": roof["avg_launch_us"],
+            "ffn_gate_up_frac": roof["frac"],
+            "realized_skip_mean": routing_report(w, m["layer_stats"])["realized_skip_mean"]}
+
+
+def layer_point(args, name="llama31_8b_layer"):
+    """The single routed layer (Llama-3.1-8B shape, j = 17 of 32, T = 4096, 26.87 % skip) measured
+    beside the stack: tokens/s, the gate/up roofline and the router group's HBM rate."""
+    import torch
+    from paper_2609_08189_amd import synth
+    from paper_2609_08189_amd.device import DeviceProblem
+    w = synth.WORKLOADS[name]
+    print(f"# preparing {describe(w, w.layer_j)}", file=sys.stderr, flush=True)
+    prob = synth.make_problem(w, seed=args.seed)
+    dp = DeviceProblem(prob, device="cuda:0", stats=True)
+    m = measure_forward(w, dp, args.steps, args.warmup)
+    out = {"workload": describe(w, w.layer_j), "value": round(w.T / (m["ms_step"] * 1e-3), 1),
+           "unit": "tokens/s", "ms_per_step": round(m["ms_step"], 4), "n_ffn": m["nfs"][0], "n_adapter": m["nas"][0],
+           "roofline": dominant_roofline(w, m, counted_traffic("ffn_gate_up", name)),
+           "router_group": router_group(m), "whole_call": ideal_fraction(m["works"], m["ms_step"], w.dtype, False),
+           "kernels": m["per"]}
+    del dp
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_peaks(args):
+    """The board's practical ceilings, measured live: the bf16 matrix-core loop of hero_peak_mfma
+    (register operands, two waves per SIMD on all 256 CUs) with zero and with random operands, and a
+    plain 1 GiB device-to-device copy (read + write).  The roofline fractions in the other lines use
+    the published peaks (2.5 PFLOP/s, 8 TB/s); these say how much of them a kernel can reach here."""
+    import torch
+    from paper_2609_08189_amd import hero as H
+    ev = HipEvents()
+    stream = torch.cuda.current_stream().cuda_stream
+    sink = torch.zeros(16, dtype=torch.float32, device="cuda:0")
+    out = {"metric": "practical ceilings of the board", "n_gpus": 1}
+    iters, wgs, reps = 20000, 256, 5
+    for name, rnd in (("mfma_bf16_zeros", False), ("mfma_bf16_random", True)):
+        H.hero_peak_mfma(rnd, iters, wgs, sink, stream)          # warm-up launch
+        torch.cuda.synchronize()
+        a, b = ev.create(2)
+        ev.record(a, stream)
+        flop = sum(H.hero_peak_mfma(rnd, iters, wgs, sink, stream) for _ in range(reps))
+        ev.record(b, stream)
+        ms = ev.elapsed_ms(a, b)
+        ev.destroy([a, b])
+        tf = flop / (ms * 1e-3) * 1e-12
+        out[name] = {"tflops": round(tf, 1), "frac_of_2500": round(tf / PEAK_BF16_TFLOPS, 4),
+                     "implied_clock_ghz": round(tf / PEAK_BF16_TFLOPS * 2.4, 3),
+                     "launch_us": round(1000 * ms / reps, 1), "launches": reps}
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = ev.create(2)
+    ev.record(a, stream)
+    for _ in range(reps):
+        dst.copy_(src)
+    ev.record(b, stream)
+    ms = ev.elapsed_ms(a, b) / reps
+    ev.destroy([a, b])
+    gbs = 2 * n / (ms * 1e-3) * 1e-9
+    out["device_copy_1gib"] = {"gbs_read_plus_write": round(gbs, 1), "frac_of_8000": round(gbs / PEAK_HBM_GBS, 4),
+                               "copy_us": round(1000 * ms, 1), "launches": reps}
+    print(json.dumps(out), flush=True)
 
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="llama31_8b_layer")
+    ap.add_argument("--workload", default="llama31_8b_stack")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--ablation", type=int, default=0,
                     help="router ablation bits (1 w/o Pos State, 2 w/o Aux State, 4 w/o MemRead, 8 w/o History)")
@@ -764,11 +1036,17 @@ def main():
     ap.add_argument("--router-backward", action="store_true",
                     help="time the backward of the router at the workload's routed layer instead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-layer-point", action="store_true",
+                    help="skip the single-layer measurement that accompanies the stack line")
     ap.add_argument("--cpu-target-s", type=float, default=12.0)
+    ap.add_argument("--cpu-tokens", type=int, default=1024,
+                    help="token sample of the stack call for the CPU oracle")
     ap.add_argument("--memory", choices=("matrix", "history"), default="matrix",
                     help="router memory as the matrix S (the paper's form) or in depth-history form")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device-to-device copy of this many MiB (HBM counter calibration)")
+    ap.add_argument("--peaks", action="store_true",
+                    help="measure the chip's practical ceilings instead (MFMA loop, device copy) and exit")
     ap.add_argument("--summarize", metavar="DIR",
                     help="print a summary of rocprofv3 CSV output found under DIR and exit (no GPU)")
     ap.add_argument("--window", type=int, nargs=2, metavar=("SKIP", "COUNT"),
@@ -782,14 +1060,16 @@ def main():
               f"communication in threshold mode, and runs on several GPUs are not implemented "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
+    if args.peaks:
+        return bench_peaks(args)
 
-    import numpy as np
     import torch
-    from paper_2609_08189_amd import hero as H
     from paper_2609_08189_amd import synth
     from paper_2609_08189_amd.device import DeviceProblem
 
     w = synth.WORKLOADS[args.workload]
+    default_line = (args.budget is None and not args.ablation and args.state == "f32"
+                    and args.memory == "matrix" and not args.graph)
     if args.budget is not None:
         if w.mode != "budget" or not 0.0 <= args.budget <= 1.0:
             sys.exit("--budget needs a budget-mode workload and a fraction in [0, 1]")
@@ -810,148 +1090,47 @@ def main():
         return bench_decoder(args, w)
     stack = w.layer_j <= 0          # a stack workload: a step is one hero_routed_stack call
     j = w.layer_j
-    L = w.L_R if stack else 1       # routed layers per step
     print(f"# preparing {describe(w, j)}", file=sys.stderr, flush=True)
     prob = synth.make_problem(w, seed=args.seed)
     dp = DeviceProblem(prob, device="cuda:0", stats=True, history=args.memory == "history")
-    stream = dp.stream()
-    ev = HipEvents()
-    step = dp.run_stack if stack else (lambda: dp.run_layer(j))
-
-    # one checked call with stats for the realized branch sizes (and the CPU baseline)
-    step()
-    torch.cuda.synchronize()
-    layer_stats = [s.host() for s in dp.stats]
-    st0 = layer_stats[0]
-    nfs = [ls["n_ffn"] for ls in layer_stats]
-    nas = [ls["n_ad"] for ls in layer_stats]
-    n_f, n_a = st0["n_ffn"], st0["n_ad"]
-    # the timed steps run without the optional stats outputs
-    stats_saved, dp.stats = dp.stats, None
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    K = args.steps
-    dom = "ffn_gate_up"
-    n_dom = K * sum(1 for x in nfs if x > 0)   # launches of the dominant kernel in the timed steps
-    # graph mode: the timed steps replay the call captured once; the dominant kernel's time then
-    # comes from the instrumented pass below
-    run = graphed(step) if args.graph else step
-    ks, ke = ev.create(n_dom), ev.create(n_dom)
-    if not args.graph:
-        H.hero_kernel_timer(H.HERO_K[dom], ks, ke)
-    t_start, t_stop = ev.create(2)
-    torch.cuda.synchronize()
-    marks = ev.create(K - 1)            # step boundaries inside the timed region
-    ev.record(t_start, stream)
-    for i in range(K):
-        run()
-        if i < K - 1:
-            ev.record(marks[i], stream)
-    ev.record(t_stop, stream)
-    torch.cuda.synchronize()
-    H.hero_kernel_timer(H.HERO_K[dom], [], [])
-    total_ms = ev.elapsed_ms(t_start, t_stop)
-    bounds = [t_start] + marks + [t_stop]
-    step_ms = sorted(ev.elapsed_ms(a, b) for a, b in zip(bounds[:-1], bounds[1:]))
-    dom_ms_step = 0.0 if args.graph else sum(ev.elapsed_ms(a, b) for a, b in zip(ks, ke)) / K
-    ms_step = total_ms / K
-    print(f"# timed {K} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
-
-    # per-kernel breakdown (untimed pass, every kernel instrumented): mean per launch, with the
-    # algorithmic work of the mean layer
-    layers = list(range(1, L + 1)) if stack else [j]
-    works = [kernel_work(w, nf, na, w.T, jj, args.memory) for nf, na, jj in zip(nfs, nas, layers)]
-    per = {}
-    handles = {}
-    names = [k for k in H.KERNELS[:H.HERO_K["adapter_up"] + 1] if not (k == "router_mem" and w.ablation & 12)]
-    if w.ablation & 12:            # no memory pass under the memory-less ablations
-        for wk in works:
-            wk["router_mem"] = dict(flops=0, bytes=0)
-    for name in names:
-        a, b = ev.create(K * L), ev.create(K * L)
-        handles[name] = (a, b)
-        H.hero_kernel_timer(H.HERO_K[name], a, b)
-    for _ in range(K):
-        step()
-    torch.cuda.synchronize()
-    for name in names:
-        H.hero_kernel_timer(H.HERO_K[name], [], [])
-        a, b = handles[name]
-        active = [i for i in range(L) if not ((name.startswith("ffn") and nfs[i] == 0) or
-                                               (name.startswith("adapter") and nas[i] == 0))]
-        if active:
-            n_launch = K * len(active)
-            us = 1000.0 * sum(ev.elapsed_ms(x, y) for x, y in zip(a[:n_launch], b[:n_launch])) / n_launch
-            fl = sum(works[i][name]["flops"] for i in active) / len(active)
-            by = sum(works[i][name]["bytes"] for i in active) / len(active)
-            per[name] = {"us": round(us, 2), "tflops": round(fl / us * 1e-6, 1) if fl else None,
-                         "gbs": round(by / us * 1e-3, 1)}
-        ev.destroy(a + b)
-
-    if args.graph:
-        dom_ms_step = per[dom]["us"] * sum(1 for x in nfs if x > 0) / 1000.0
-    tokens_per_s = w.T / (ms_step * 1e-3)
-    dflops = sum(wk[dom]["flops"] for wk in works)          # per step
-    dbytes = sum(wk[dom]["bytes"] for wk in works)
-    peak_f = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
-    n_launch_step = max(1, n_dom // K)
-    # the tighter roof for this row count: MFMA for prefill-sized products, HBM for decode
-    # batches, whose weight bytes take longer at 8 TB/s than their FLOPs at the MFMA peak
-    hbm_bound = dbytes / (PEAK_HBM_GBS * 1e9) > dflops / (peak_f * 1e12)
-    if hbm_bound:
-        achieved, peak, unit = dbytes / (dom_ms_step * 1e-3) * 1e-9, PEAK_HBM_GBS, "GB/s"
-        per_unit = "weights 2*d*d_ff*2 B per launch + (d + d_ff)*2 B per FFN token"
-        total = f"{dbytes / 1e6:.1f} MB"
-    else:
-        achieved, peak, unit = dflops / (dom_ms_step * 1e-3) * 1e-12, peak_f, "TFLOP/s"
-        per_unit = "4*d*d_ff FLOP per FFN token"
-        total = f"{dflops / 1e9:.1f} GFLOP"
-    roof = {"bound": "hbm" if hbm_bound else "mfma", "achieved": round(achieved, 1), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 4),
-            "traffic": counted_traffic(dom) if (args.workload == "llama31_8b_layer" and args.memory == "matrix"
-                                                  and args.budget is None and args.state == "f32"
-                                                  and not args.ablation) else None,
-            "kernel": dom, "avg_launch_us": round(dom_ms_step * 1e3 / n_launch_step, 2),
-            "work_per_launch": (f"{per_unit} x {n_f} FFN tokens = {total}"
-                                if not stack else
-                                f"{per_unit} x {sum(nfs)} FFN tokens over {L} layers = "
-                                f"{total} per step, {n_launch_step} launches"),
-            "traffic_note": "HBM bytes read + written per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1, "
-                            "calibrated on a 1 GiB copy) from profiles/, null if the GEMM changed since or "
-                            "for workloads the counters were not taken on"}
-
+    m = measure_forward(w, dp, args.steps, args.warmup, memory=args.memory, graph=args.graph)
+    K, L, nfs, nas = m["K"], m["L"], m["nfs"], m["nas"]
+    print(f"# timed {K} steps: {m['ms_step']:.4f} ms/step", file=sys.stderr, flush=True)
     result = {
         "metric": "routed-FFN-stack tokens/sec at Llama-3.1-8B shape; % MFMA/HBM roofline",
-        "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
-        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "value": round(w.T / (m["ms_step"] * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(m["ms_step"], 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": describe(w, j) + ("" if args.state == "f32" else ", S stored in bf16") +
                                ("" if not args.ablation else f", router ablation bits {args.ablation}") +
-                               ("" if args.memory == "matrix" else
-                                                 ", router memory in depth-history form"),
+                               ("" if args.memory == "matrix" else ", router memory in depth-history form"),
                    "memory": args.memory, "state": args.state, "global_batch": w.batch, "seq_len": w.seq,
                    "tokens": w.T, "layers_per_step": L, "parallelism": "none", "hip_graph": bool(args.graph),
-                   "n_ffn": n_f if not stack else sum(nfs), "n_adapter": n_a if not stack else sum(nas)},
-        "roofline": roof,
-        "step_ms": step_stats(step_ms),
-        "whole_call": ideal_fraction(works, ms_step, w.dtype, stack),
-        "kernels": per,
+                   "n_ffn": sum(nfs), "n_adapter": sum(nas)},
+        "roofline": dominant_roofline(w, m, counted_traffic("ffn_gate_up", args.workload) if default_line else None),
+        "router_group": router_group(m),
+        "step_ms": step_stats(m["step_ms"]),
+        "whole_call": ideal_fraction(m["works"], m["ms_step"], w.dtype, stack),
+        "routing": routing_report(w, m["layer_stats"]),
+        "kernels": m["per"],
     }
-    # the paper's other operating point, when the default layer workload runs at one of them
+    # the paper's other Llama-3.1-8B operating point (Table 1: 26.87 % and 38.82 % skip), on the
+    # same device problem
     others = [b for b in PAPER_SKIPS if abs(b - w.budget) > 1e-6]
-    if (not stack and w.mode == "budget" and args.budget is None and args.workload == "llama31_8b_layer"
-            and not args.graph and args.memory == "matrix" and others):
-        print(f"# timing the layer at skip budget {others[0]}", file=sys.stderr, flush=True)
-        result["other_skip"] = other_skip_point(dp, stats_saved, w, j, others[0], K, args.warmup)
-    if not args.no_cpu_baseline and not stack:
-        dp.stats = stats_saved
+    if w.mode == "budget" and default_line and args.workload.startswith("llama31_8b") and others:
+        print(f"# timing the call at skip budget {others[0]}", file=sys.stderr, flush=True)
+        result["other_skip"] = other_skip_point(w, dp, others[0], K, args.warmup)
+    if not args.no_cpu_baseline:
         print("# timing the CPU oracle on a token sample", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(prob, st0, j, target_s=args.cpu_target_s)
+        if stack:
+            result["cpu_baseline"] = cpu_baseline_stack(prob, m["layer_stats"], args.cpu_tokens, args.cpu_target_s)
+        else:
+            result["cpu_baseline"] = cpu_baseline(prob, m["layer_stats"][0], j, target_s=args.cpu_target_s)
+    if stack and default_line and args.workload == "llama31_8b_stack" and not args.no_layer_point:
+        del dp
+        torch.cuda.empty_cache()
+        result["layer"] = layer_point(args)
     print(json.dumps(result), flush=True)
-    ev.destroy(ks + ke + [t_start, t_stop])
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib << 20
         src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)

@@ -230,6 +230,19 @@ typedef enum hero_kernel {
  */
 int hero_kernel_timer(int kernel, void *const *start_events, void *const *stop_events, int n_slots);
 
+/*
+ * Measurement hook, not part of the method: the practical bf16 matrix-core rate of the board.
+ * Launches `workgroups` workgroups of 8 waves (two per SIMD; 256 = one per compute unit of an
+ * MI355X) on hip_stream, each wave running 8 independent v_mfma_f32_32x32x16_bf16 chains for
+ * `iters` iterations on register operands: zeros (random_operands = 0, the issue limit) or
+ * hashed values in [-0.5, 0.5) (the power-limited rate on realistic data).  *flop (host)
+ * receives the floating-point operations the launch performs.  sink (device, >= 1 float) is
+ * never written in practice.  Time the launch with the caller's events.
+ * Errors: HERO_E_NULL, HERO_E_RANGE (iters outside 1..2^24, workgroups outside 1..65536),
+ * HERO_E_LAUNCH.
+ */
+int hero_peak_mfma(int random_operands, int iters, int workgroups, float *sink, void *hip_stream, double *flop);
+
 /* Static string for a status code (host). */
 const char *hero_status_string(int status);
 

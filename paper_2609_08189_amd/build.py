@@ -9,7 +9,7 @@ CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(PKG, "libhero.so")
 SOURCES = ["hero_abi.hip", "k_rowstats.hip", "k_gemm.hip", "k_router.hip", "k_select.hip", "k_attn.hip",
-           "k_backward.hip", "k_router_bwd.hip"]
+           "k_backward.hip", "k_router_bwd.hip", "k_peaks.hip"]
 # Packed fp32 instructions are disabled for all device code; hipcc's host pass warns that it
 # does not know the feature, which is harmless.
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",

@@ -190,6 +190,8 @@ def lib() -> ctypes.CDLL:
         L.hero_router_backward.argtypes = [P(hero_dims), ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, P(hero_state),
                                            P(hero_router_weights), ctypes.c_float, _vp, P(hero_router_carry), _vp,
                                            _vp, _vp, P(hero_router_grads), _vp, _vp, ctypes.c_size_t, _vp]
+        L.hero_peak_mfma.restype = ctypes.c_int
+        L.hero_peak_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, P(ctypes.c_double)]
         _lib = L
     return _lib
 
@@ -220,6 +222,14 @@ def hero_status_string(status: int) -> str:
 
 def hero_abi_version() -> int:
     return lib().hero_abi_version()
+
+
+def hero_peak_mfma(random_operands: bool, iters: int, workgroups: int, sink, stream) -> float:
+    """Launch the matrix-core rate probe on `stream`; returns the FLOPs the launch performs."""
+    flop = ctypes.c_double()
+    check(lib().hero_peak_mfma(int(bool(random_operands)), iters, workgroups, ptr(sink), stream,
+                               ctypes.byref(flop)), "hero_peak_mfma")
+    return flop.value
 
 
 def hero_kernel_timer(kernel: int, start_events: Sequence[int], stop_events: Sequence[int]) -> None:

@@ -80,6 +80,10 @@ class Workload:
     ablation: int = 0
     # storage of the router memory S between layers: "f32" or "bf16" (zeta, p, m stay fp32)
     state_dtype: str = "f32"
+    # standard deviation of the frozen FFN's and the adapters' weights (0.02 everywhere but in
+    # high-contrast parity cases, where larger branch outputs make scaling mistakes visible)
+    ffn_std: float = 0.02
+    adapter_std: float = 0.02
     # full decoder (n_layers > 0): every block has dense attention, the last L_R are routed
     n_layers: int = 0
     n_heads: int = 32
@@ -181,7 +185,7 @@ _TID = {
     "w_hd": 30, "w_hu": 31, "w_p1": 32, "w_p2": 33, "w_q": 34, "w_k": 35, "w_v": 36,
     "w_n": 37, "w_c": 38, "th1": 39, "th2": 40, "ps1": 41, "ps2": 42,
     "state_a": 50, "state_b": 51, "p_hist": 52, "m_hist": 53,
-    "bias_runs": 60, "bias_vals": 61,
+    "bias_runs": 60, "bias_vals": 61, "bias_spread": 62,
     "attn_norm": 70, "w_qkv": 71, "w_o": 72,
     "dh_out": 80, "bwd_gate": 81, "bwd_branch": 82,
 }
@@ -279,16 +283,16 @@ def router_weights(w: Workload, seed: int = 0, std: float = 0.02) -> Dict[str, T
 def ffn_layer(w: Workload, layer: int, seed: int = 0) -> Dict[str, Tensor]:
     return {
         "norm_w": _t(normal32(seed, "norm_w", (w.d,), 0.02, 1.0, layer), w.dtype),
-        "w_gate": _t(normal32(seed, "w_gate", (w.d_ff, w.d), 0.02, layer=layer), w.dtype),
-        "w_up": _t(normal32(seed, "w_up", (w.d_ff, w.d), 0.02, layer=layer), w.dtype),
-        "w_down": _t(normal32(seed, "w_down", (w.d, w.d_ff), 0.02, layer=layer), w.dtype),
+        "w_gate": _t(normal32(seed, "w_gate", (w.d_ff, w.d), w.ffn_std, layer=layer), w.dtype),
+        "w_up": _t(normal32(seed, "w_up", (w.d_ff, w.d), w.ffn_std, layer=layer), w.dtype),
+        "w_down": _t(normal32(seed, "w_down", (w.d, w.d_ff), w.ffn_std, layer=layer), w.dtype),
     }
 
 
 def adapter_layer(w: Workload, layer: int, seed: int = 0) -> Dict[str, Tensor]:
     return {
-        "w1": _t(normal32(seed, "w1", (w.d_r, w.d), 0.02, layer=layer), w.dtype),
-        "w2": _t(normal32(seed, "w2", (w.d, w.d_r), 0.02, layer=layer), w.dtype),
+        "w1": _t(normal32(seed, "w1", (w.d_r, w.d), w.adapter_std, layer=layer), w.dtype),
+        "w2": _t(normal32(seed, "w2", (w.d, w.d_r), w.adapter_std, layer=layer), w.dtype),
     }
 
 
@@ -364,10 +368,13 @@ def incoming_state(w: Workload, j: int, T: int, seed: int = 0, decay: float = 0.
 
 
 def logit_bias(w: Workload, seed: int = 0, T: Optional[int] = None) -> Optional[np.ndarray]:
-    """Per-token logit bias for the position-clustered bimodal workload, else None."""
+    """Per-token logit bias: position-clustered bimodal runs ("bimodal_runs"), or U(-3, 3) drawn
+    per token ("spread": gates spread over about (0.05, 0.95) whatever the router gives); else None."""
     if w.bias == "none":
         return None
     T = w.T if T is None else T
+    if w.bias == "spread":
+        return _rng(seed, "bias_spread").uniform(-3.0, 3.0, size=T).astype(np.float32)
     run = 64
     n_runs = (T + run - 1) // run
     n_neg = int(math.floor(0.29 * n_runs + 0.5))

@@ -19,14 +19,23 @@ from tests.oracle_inputs import adapter_of, dims_of, ffn_of, router_of, state_of
 
 BAND = 1e-3
 TOL = {"f32": 1e-4, "bf16": 2e-2}
+# the router's outputs are fp32 arithmetic on exactly stored inputs in every workload, so they are
+# held to the fp32 tolerance even where hidden states and weights are bf16
+ROUTER_KEYS = ("logit", "gate", "p", "m", "S", "zeta")
 
 
-def tol_of(w, key):
-    """Tolerance of one output: the workload dtype's, except that a memory matrix stored in
-    bf16 is a bf16 quantity (the GPU rounds its fp32 value, the oracle its fp64 one, so the
-    two may differ by one bf16 ulp)."""
+def tol_of(w, key, own_inputs=True):
+    """Tolerance of one output: the workload dtype's, except that
+    * a memory matrix stored in bf16 is a bf16 quantity (the GPU rounds its fp32 value, the
+      oracle its fp64 one, so the two may differ by one bf16 ulp);
+    * the router's outputs are held to the fp32 tolerance when the layer ran on the same inputs on
+      both sides (a single layer call, or each layer of a stack fed the GPU's own inputs).  Through
+      a bf16 stack compared end to end, the hidden states the router reads differ by bf16
+      rounding from layer 2 on, and the workload's tolerance applies."""
     if key == "S" and w.state_dtype == "bf16":
         return TOL["bf16"]
+    if key in ROUTER_KEYS and own_inputs:
+        return TOL["f32"]
     return TOL[w.dtype]
 
 
@@ -198,7 +207,7 @@ def check_stack(prob, gpu_res, rows=None, report=None):
     if report is not None:
         report.update(errs)
     for k in ("logit", "gate", "h", "S", "zeta", "p", "m"):
-        t = tol_of(w, k)
+        t = tol_of(w, k, own_inputs=False)
         assert errs[k] <= t, f"{k}: max rel err {errs[k]:.3e} > {t:.0e} ({errs})"
     return errs
 
@@ -300,6 +309,6 @@ def check_decoder(prob, gpu_res, report=None):
     if report is not None:
         report.update(errs)
     for k in ("logit", "gate", "h", "S", "zeta", "p", "m"):
-        t = tol_of(w, k)
+        t = tol_of(w, k, own_inputs=False)
         assert errs[k] <= t, f"{k}: max rel err {errs[k]:.3e} > {t:.0e} ({errs})"
     return errs

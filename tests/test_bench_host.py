@@ -18,16 +18,63 @@ def test_more_than_one_gpu_exits_with_message():
 
 def test_traffic_from_committed_counters(monkeypatch):
     import re
-    text = open(bench.COUNTERS_MD).read()
+    text = open(bench.COUNTERS_MD["llama31_8b_layer"]).read()
     recorded = re.search(r"= `([0-9a-f]{64})`", text).group(1)
     # with the sources the counters were taken with, the gate/up row is reported
     monkeypatch.setattr(bench, "gemm_source_hash", lambda: recorded)
-    t = bench.counted_traffic("ffn_gate_up")
+    t = bench.counted_traffic("ffn_gate_up", "llama31_8b_layer")
     assert t is not None and t > 260e6       # at least the algorithmic bytes of the launch
-    assert bench.counted_traffic("no_such_kernel") is None
+    assert bench.counted_traffic("no_such_kernel", "llama31_8b_layer") is None
+    assert bench.counted_traffic("ffn_gate_up", "no_such_workload") is None
     # any other source hash makes the committed counters stale
     monkeypatch.setattr(bench, "gemm_source_hash", lambda: "0" * 64)
-    assert bench.counted_traffic("ffn_gate_up") is None
+    assert bench.counted_traffic("ffn_gate_up", "llama31_8b_layer") is None
+
+
+def test_default_workload_is_the_8b_stack():
+    """The headline line times the metric's own configuration: the 32-layer Llama-3.1-8B routed
+    stack over 16 x 2048 tokens at 38.82 % skip."""
+    import argparse
+    from paper_2609_08189_amd import synth
+    src = open(os.path.join(ROOT, "bench.py")).read()
+    assert 'ap.add_argument("--workload", default="llama31_8b_stack")' in src
+    w = synth.WORKLOADS["llama31_8b_stack"]
+    assert (w.d, w.d_ff, w.d_r, w.d_m, w.L_R, w.batch, w.seq, w.T) == (4096, 14336, 64, 128, 32, 16, 2048, 32768)
+    assert w.mode == "budget" and w.budget == 0.3882 and w.layer_j == 0
+
+
+def test_routing_report_band_and_skip():
+    import numpy as np
+    from paper_2609_08189_amd import synth
+    w = synth.WORKLOADS["tiny_f32_stack"]
+    lam = 0.25
+    logit = np.array([lam - 1e-3, lam, lam + 1e-3, lam + 1.0, lam - 1.0, lam + 3.9e-3, lam + 4.1e-3],
+                     dtype=np.float32)
+    mask = logit >= lam
+    ls = {"logit": logit, "lam": lam, "n_ffn": int(mask.sum()), "n_ad": int((~mask).sum())}
+    r = bench.routing_report(w, [ls, ls])
+    # sigma'(0.25) ~ 0.2461, so |dsigma| < 1e-3 <=> |dlogit| < ~4.06e-3
+    assert r["band_count_per_layer"] == [4, 4] and r["band_count_total"] == 8
+    assert r["realized_skip_per_layer"] == [round(2 / 7, 5)] * 2
+    assert r["lambda_per_layer"] == [0.25, 0.25]
+
+
+def test_cpu_baseline_stack_follows_the_gpu_decisions():
+    """The stack's oracle baseline runs a token sample through every layer, forced at each layer to
+    the given decisions; it reports the multi-thread and the one-thread rate."""
+    import numpy as np
+    from paper_2609_08189_amd import synth
+    from oracle import hero_oracle as O
+    from tests.oracle_inputs import adapter_of, dims_of, ffn_of, router_of
+    w = synth.WORKLOADS["tiny_f32_stack"]
+    prob = synth.make_problem(w, seed=2)
+    ref = O.routed_stack(dims_of(w), prob.hbar.f64, [ffn_of(l) for l in prob.ffn], router_of(prob),
+                         [adapter_of(l) for l in prob.adapter], prob.eta.astype("f8"),
+                         mode=w.mode, budget=w.budget)
+    stats = [{"mask": L.use_ffn, "lam": L.lam} for L in ref.layers]
+    r = bench.cpu_baseline_stack(prob, stats, n_tokens=32, single_tokens=4)
+    assert r["kind"] == "oracle" and r["value"] > 0 and r["single_thread_value"] > 0
+    assert r["sample"].startswith(f"32 of {w.T} tokens") and f"all {w.L_R} routed layers" in r["sample"]
 
 
 def test_summarize_reads_rocprof_csv(tmp_path, capsys):
@@ -73,13 +120,14 @@ def test_graph_flag_and_backward_flag_parse():
 
 
 def test_both_paper_skip_points_are_reported():
-    """The default layer workload runs at one of the paper's two Llama-3.1-8B operating points
+    """The default stack workload runs at one of the paper's two Llama-3.1-8B operating points
     (Table 1: 26.87 % and 38.82 % skip); the bench line adds the other as `other_skip`."""
     from paper_2609_08189_amd import synth
     assert bench.PAPER_SKIPS == (0.2687, 0.3882)
-    w = synth.WORKLOADS["llama31_8b_layer"]
-    assert w.mode == "budget" and w.budget in bench.PAPER_SKIPS
-    assert [b for b in bench.PAPER_SKIPS if abs(b - w.budget) > 1e-6] == [0.3882]
+    for name, other in (("llama31_8b_stack", 0.2687), ("llama31_8b_layer", 0.3882)):
+        w = synth.WORKLOADS[name]
+        assert w.mode == "budget" and w.budget in bench.PAPER_SKIPS
+        assert [b for b in bench.PAPER_SKIPS if abs(b - w.budget) > 1e-6] == [other]
 
 
 def test_cpu_baseline_repeats_a_short_whole_call():
