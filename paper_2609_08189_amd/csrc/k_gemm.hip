@@ -396,20 +396,49 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   };
   // order within the current scheduling region: MFMA, then (while any remain) one stage load
   // and one fragment read after each
-  auto interleave = [&](auto nl_) {
-    constexpr int nl = decltype(nl_)::value;
+  auto interleave = [&](auto nl_, auto nr_) {
+    constexpr int nl = decltype(nl_)::value, nr = decltype(nr_)::value;
 #pragma unroll
     for (int i = 0; i < NM; ++i) {
       __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
       if (i < nl) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, 1, 0);
-      if (i < NR) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+      if (i < nr) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
     }
     if constexpr (nl > NM) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, nl - NM, 0);
-    if constexpr (NR > NM) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, NR - NM, 0);
+    if constexpr (nr > NM) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, nr - NM, 0);
   };
 
   const int nk = kt1 - kt0;
   constexpr int NS = C::NS;
+  // One k-tile.  MODE 2 (steady state): the loads of tile kt + NS go into the stage just
+  // consumed and the first fragments of tile kt + 1 are read, both interleaved with the MFMAs
+  // of the last k-step; MODE 1: no tile left to load; MODE 0: the last tile.  Each mode is its
+  // own straight-line code, so that the scheduler can interleave the loads with the MFMAs
+  // (a load under a run-time condition would sit in a block of its own and issue as a burst).
+  auto ktile = [&](int kt, auto mode_) {
+    constexpr int mode = decltype(mode_)::value;
+    const unsigned char* st = smem + (kt % NS) * C::STAGE;
+#pragma unroll
+    for (int ks = 0; ks < KS - 1; ++ks) {
+      read_frags((ks + 1) & 1, st, ks + 1);
+      mfmas(ks & 1);
+      interleave(std::integral_constant<int, 0>(), std::integral_constant<int, NR>());
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // every wave has read all of stage kt and the loads of tile kt+1 have landed (tiles
+    // kt+2 .. kt+NS-1 may still be in flight; near the end, fewer were issued)
+    if constexpr (mode == 2)
+      wait_vm_lgkm<(NS - 2) * NL>();
+    else
+      wait_vm_lgkm<0>();
+    __syncthreads();
+    if constexpr (mode == 2) issue(kt % NS, (kt + NS) * BK);
+    if constexpr (mode >= 1) read_frags(KS & 1, smem + ((kt + 1) % NS) * C::STAGE, 0);
+    mfmas((KS - 1) & 1);
+    interleave(std::integral_constant<int, mode == 2 ? NL : 0>(), std::integral_constant<int, mode >= 1 ? NR : 0>());
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
   // tiles 0 .. NS-1 into the NS stages; wait for tile 0 (the others may still be landing)
 #pragma unroll
   for (int i = 0; i < NS; ++i)
@@ -420,28 +449,10 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
     wait_vm_lgkm<0>();
   __syncthreads();
   read_frags(0, smem, 0);
-  for (int kt = 0; kt < nk; ++kt) {
-    const unsigned char* st = smem + (kt % NS) * C::STAGE;
-#pragma unroll
-    for (int ks = 0; ks < KS - 1; ++ks) {
-      read_frags((ks + 1) & 1, st, ks + 1);
-      mfmas(ks & 1);
-      interleave(std::integral_constant<int, 0>());
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // every wave has read all of stage kt and the loads of tile kt+1 have landed (tiles
-    // kt+2 .. kt+NS-1 may still be in flight; near the end, fewer were issued)
-    if (kt + NS - 1 < nk)
-      wait_vm_lgkm<(NS - 2) * NL>();
-    else
-      wait_vm_lgkm<0>();
-    __syncthreads();
-    if (kt + NS < nk) issue(kt % NS, (kt + NS) * BK);
-    if (kt + 1 < nk) read_frags(KS & 1, smem + ((kt + 1) % NS) * C::STAGE, 0);
-    mfmas((KS - 1) & 1);
-    interleave(std::integral_constant<int, NL>());
-    __builtin_amdgcn_sched_barrier(0);
-  }
+  int kt = 0;
+  for (; kt + NS < nk; ++kt) ktile(kt, std::integral_constant<int, 2>());
+  for (; kt + 1 < nk; ++kt) ktile(kt, std::integral_constant<int, 1>());
+  if (kt < nk) ktile(kt, std::integral_constant<int, 0>());
 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
