@@ -59,7 +59,9 @@ typedef enum hero_status {
   HERO_E_WORKSPACE = 7,   /* workspace NULL or smaller than hero_workspace_size()      */
   HERO_E_UNSUPPORTED = 8, /* valid shape that the kernels do not implement            */
   HERO_E_LAUNCH = 9,      /* a kernel launch was rejected by the runtime              */
-  HERO_E_DEVICE = 10      /* no usable gfx950 device is current                       */
+  HERO_E_DEVICE = 10,     /* no usable gfx950 device is current                       */
+  HERO_E_SCRATCH = 11     /* hero_routed_layer_noalloc: the call needs more scratch than
+                             the library's fixed device area (HERO_NOALLOC_SCRATCH_BYTES) */
 } hero_status;
 
 typedef enum hero_dtype { HERO_F32 = 0, HERO_BF16 = 1 } hero_dtype;
@@ -280,6 +282,30 @@ int hero_routed_layer(const hero_dims *dims, int j, int T,
                       const hero_adapter_weights *adapter, float eta,
                       const hero_routing *routing, const hero_layer_stats *stats,
                       void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * hero_routed_layer for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same arguments, results and
+ * errors as hero_routed_layer, without the workspace: the call's scratch (the layer's
+ * intermediates: normalised rows, router pre-activations and state, logits, index lists, the FFN
+ * activation, partial sums) lives in a fixed device array of HERO_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every device it runs on until the process ends.  The call allocates nothing
+ * and issues no memset (no region of the scratch must start at zero: every kernel writes what it
+ * later reads within the same call).  A call whose workspace (hero_workspace_size with
+ * for_stack = 0) exceeds the area returns HERO_E_SCRATCH before any launch; at the
+ * Llama-3.1-8B shape (d = 4096, d_ff = 14336, r = 64, d_m = 128) that allows up to 473 tokens,
+ * and a 256-token decode batch of the Llama-2-7B shape needs 42.5 MiB of it.  The first call on a device looks the area up on that device (it must be
+ * current); later calls reuse it.  Every call on one device shares that device's area: calls that
+ * overlap in time on one device (two streams, two threads) race and must be serialised by the
+ * caller.
+ */
+#define HERO_NOALLOC_SCRATCH_BYTES (64u << 20)
+int hero_routed_layer_noalloc(const hero_dims *dims, int j, int T,
+                              const void *hbar, const void *hbar_prev1, const void *hbar_prev2,
+                              void *h_out, const hero_state *state,
+                              const hero_ffn_weights *ffn, const hero_router_weights *router,
+                              const hero_adapter_weights *adapter, float eta,
+                              const hero_routing *routing, const hero_layer_stats *stats, void *stream);
 
 /*
  * The whole routed stack: L_R chained routed layers with no attention between

@@ -8,6 +8,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 #include <new>
 
 #include "../../include/hero.h"
@@ -25,6 +26,9 @@ size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 size_t esize(int dtype) { return dtype == HERO_BF16 ? 2 : 4; }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// a workspace argument that tells check_layer_call the entry point brings its own scratch
+void* const kNoWorkspace = reinterpret_cast<void*>(static_cast<uintptr_t>(-256));
 
 bool overlap(const void* a, size_t na, const void* b, size_t nb) {
   if (!a || !b || na == 0 || nb == 0) return false;
@@ -380,6 +384,7 @@ const char* hero_status_string(int status) {
     case HERO_E_UNSUPPORTED: return "shape not supported by the kernels";
     case HERO_E_LAUNCH: return "kernel launch failed";
     case HERO_E_DEVICE: return "no usable gfx950 device";
+    case HERO_E_SCRATCH: return "the call needs more device scratch than the fixed no-alloc area holds";
     default: return "unknown status";
   }
 }
@@ -448,9 +453,33 @@ int check_layer_call(const hero_dims* dims, int j, int T, const void* hbar, cons
       (j >= 3 && overlap(h_out, hb, hbar_prev2, hb)))
     return HERO_E_ALIAS;
   *L = layout_of(*dims, T, false);
+  if (workspace == kNoWorkspace) return HERO_OK;      // the no-alloc entry point brings its own
   if (!workspace) return HERO_E_WORKSPACE;
   if (workspace_bytes < L->total) return HERO_E_WORKSPACE;
   if (!aligned16(workspace)) return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+// The no-alloc entry point's scratch: one fixed device array per device, for the life of the
+// process.  In host code the name `noalloc_scratch` is only a host-side stand-in for the array;
+// the device address comes from hipGetSymbolAddress, looked up once per device with that device
+// current, and only that address is ever handed to kernels.
+__device__ __align__(256) unsigned char noalloc_scratch[HERO_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+int scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return HERO_E_DEVICE;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(noalloc_scratch)) != hipSuccess || !p) return HERO_E_DEVICE;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return HERO_OK;
 }
 
@@ -472,6 +501,26 @@ int hero_routed_layer(const hero_dims* dims, int j, int T, const void* hbar, con
   LayerCall c{dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, state, ffn, router, adapter, eta,
               routing, stats, static_cast<unsigned char*>(workspace), &L,
               static_cast<hipStream_t>(stream)};
+  return run_layer(c);
+}
+
+int hero_routed_layer_noalloc(const hero_dims* dims, int j, int T, const void* hbar, const void* hbar_prev1,
+                              const void* hbar_prev2, void* h_out, const hero_state* state,
+                              const hero_ffn_weights* ffn, const hero_router_weights* router,
+                              const hero_adapter_weights* adapter, float eta, const hero_routing* routing,
+                              const hero_layer_stats* stats, void* stream) {
+  Layout L;
+  int st = check_layer_call(dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, ffn, router, adapter, routing,
+                            stats, kNoWorkspace, 0, &L);
+  if (st != HERO_OK) return st;
+  if (L.total > HERO_NOALLOC_SCRATCH_BYTES) return HERO_E_SCRATCH;
+  if ((st = check_state(state)) != HERO_OK) return st;
+  if (!(eta == eta)) return HERO_E_RANGE;
+  if ((st = check_device()) != HERO_OK) return st;
+  void* scratch = nullptr;
+  if ((st = scratch_of_current_device(&scratch)) != HERO_OK) return st;
+  LayerCall c{dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, state, ffn, router, adapter, eta,
+              routing, stats, static_cast<unsigned char*>(scratch), &L, static_cast<hipStream_t>(stream)};
   return run_layer(c);
 }
 

@@ -27,6 +27,8 @@ HERO_E_WORKSPACE = 7
 HERO_E_UNSUPPORTED = 8
 HERO_E_LAUNCH = 9
 HERO_E_DEVICE = 10
+HERO_E_SCRATCH = 11
+HERO_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 HERO_F32 = 0
 HERO_BF16 = 1
@@ -142,6 +144,11 @@ def lib() -> ctypes.CDLL:
                                         P(hero_state), P(hero_ffn_weights), P(hero_router_weights),
                                         P(hero_adapter_weights), ctypes.c_float, P(hero_routing),
                                         P(hero_layer_stats), _vp, ctypes.c_size_t, _vp]
+        L.hero_routed_layer_noalloc.restype = ctypes.c_int
+        L.hero_routed_layer_noalloc.argtypes = [P(hero_dims), ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp,
+                                                P(hero_state), P(hero_ffn_weights), P(hero_router_weights),
+                                                P(hero_adapter_weights), ctypes.c_float, P(hero_routing),
+                                                P(hero_layer_stats), _vp]
         L.hero_routed_stack.restype = ctypes.c_int
         L.hero_routed_stack.argtypes = [P(hero_dims), ctypes.c_int, _vp, _vp, P(hero_state),
                                         P(hero_ffn_weights), P(hero_router_weights),
@@ -261,6 +268,18 @@ def hero_routed_layer(dims: hero_dims, j: int, T: int, hbar, hbar_prev1, hbar_pr
                                    ptr(h_out), _byref(state), _byref(ffn), _byref(router), _byref(adapter),
                                    float(eta), _byref(routing), _byref(stats), ptr(workspace),
                                    int(workspace_bytes), stream)
+
+
+def hero_routed_layer_noalloc(dims: hero_dims, j: int, T: int, hbar, hbar_prev1, hbar_prev2, h_out,
+                              state: hero_state, ffn: hero_ffn_weights, router: hero_router_weights,
+                              adapter: hero_adapter_weights, eta: float, routing: hero_routing,
+                              stats: Optional[hero_layer_stats], stream=None) -> int:
+    """Enqueue one routed layer on the library's fixed device scratch (no workspace, nothing
+    allocated); returns the hero_status code."""
+    return lib().hero_routed_layer_noalloc(ctypes.byref(dims), j, T, ptr(hbar), ptr(hbar_prev1),
+                                           ptr(hbar_prev2), ptr(h_out), _byref(state), _byref(ffn),
+                                           _byref(router), _byref(adapter), float(eta), _byref(routing),
+                                           _byref(stats), stream)
 
 
 def hero_routed_stack(dims: hero_dims, T: int, h_in, h_out, state: hero_state,

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_status_strings():
-    for code in range(11):
+    for code in range(12):
         assert H.hero_status_string(code) != "unknown status"
     assert H.hero_status_string(99) == "unknown status"
 
@@ -416,3 +416,26 @@ def test_router_backward_entry_validates():
     # the received state is not read at j = 1 and may be absent there, not later
     assert call(j=1, st=None, h1=None, h2=None, dh1=None, dh2=None, ws=None) == H.HERO_E_WORKSPACE
     assert call(j=2, st=None) == H.HERO_E_NULL
+
+
+def test_noalloc_rejects_a_call_beyond_its_scratch_before_any_launch():
+    """The no-alloc entry point's fixed scratch holds a 256-token decode batch of the Llama-2-7B
+    shape but not a 4096-token Llama-3.1-8B layer: that call returns HERO_E_SCRATCH from the host
+    checks (fake pointers, nothing launched); an argument error keeps its own status."""
+    from paper_2609_08189_amd import synth
+    from paper_2609_08189_amd.device import dims_struct
+    assert H.HERO_NOALLOC_SCRATCH_BYTES == 64 << 20
+    assert H.hero_workspace_size(dims_struct(synth.WORKLOADS["llama2_7b_decode"]), 256, False) \
+        <= H.HERO_NOALLOC_SCRATCH_BYTES
+    w = synth.WORKLOADS["llama31_8b_layer"]
+    dims = dims_struct(w)
+    assert H.hero_workspace_size(dims, 4096, False) > H.HERO_NOALLOC_SCRATCH_BYTES
+    ffn, ad, rt, st = fake_structs()
+    routing = H.hero_routing(H.HERO_MODE_BUDGET, 0.5, 0.27, None)
+    call = lambda T, hbar: H.hero_routed_layer_noalloc(dims, 3, T, hbar, FAKE + (2 << 30), FAKE + (3 << 30),
+                                                       FAKE + (4 << 30), st, ffn[0], rt, ad[0], 3.89,
+                                                       routing, None, None)
+    assert call(4096, FAKE + (1 << 30)) == H.HERO_E_SCRATCH
+    assert call(4096, None) == H.HERO_E_NULL
+    assert call(0, FAKE + (1 << 30)) == H.HERO_E_DIM
+    assert H.hero_status_string(H.HERO_E_SCRATCH) != "unknown status"
