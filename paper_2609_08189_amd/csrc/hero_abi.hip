@@ -50,7 +50,7 @@ Layout layout_of(const hero_dims& d, int T, bool stack) {
     return o;
   };
   L.u = take(t * d.d * es);
-  L.P = take(t * (d.d_e + d.d_head) * 4 * hero::router_gemm_splits(d.dtype, d.d));
+  L.P = take(t * (d.d_e + d.d_head) * 4 * hero::router_gemm_splits(d.dtype, d.d, T, d.d_e + d.d_head));
   L.rowstat = take(t * 16);
   L.logit = take(t * 4);
   L.gate = take(t * 4);
@@ -268,7 +268,7 @@ int run_layer(const LayerCall& c) {
   ra.T_hist = D.T_hist;
   ra.eta = c.eta;
   ra.P = P;
-  ra.p_splits = router_gemm_splits(D.dtype, D.d);
+  ra.p_splits = router_gemm_splits(D.dtype, D.d, c.T, D.d_e + D.d_head);
   ra.rowstat = rowstat;
   ra.w_hu = c.rt->w_hu;
   ra.w_p1 = c.rt->w_p1;
@@ -1188,7 +1188,7 @@ RouterBwdLayout router_bwd_layout_of(const hero_dims& d, int T) {
     return at;
   };
   const size_t t = static_cast<size_t>(T), np = static_cast<size_t>(d.d_e + d.d_head);
-  L.P = take(t * np * 4 * hero::router_gemm_splits(d.dtype, d.d));
+  L.P = take(t * np * 4 * hero::router_gemm_splits(d.dtype, d.d, T, d.d_e + d.d_head));
   L.dP = take(t * np * 4);
   L.dPT = take(np * t * 4);
   L.rowcoef = take(t * 8 * 4);
@@ -1314,7 +1314,7 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
   a.prev1 = hbar_prev1;
   a.prev2 = hbar_prev2;
   a.P = reinterpret_cast<float*>(ws + L.P);
-  a.p_splits = hero::router_gemm_splits(D.dtype, D.d);
+  a.p_splits = hero::router_gemm_splits(D.dtype, D.d, T, D.d_e + D.d_head);
   a.w_hu = router->w_hu;
   a.w_p1 = router->w_p1;
   a.w_p2 = router->w_p2;

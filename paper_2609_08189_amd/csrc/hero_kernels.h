@@ -17,8 +17,9 @@ hipError_t launch_rowstats(int dtype, const void* hbar, const void* prev1, const
                            float* rowstat, void* u, hipStream_t s);
 
 // Router pre-activations P[t] = [W_hd hbar_t ; psi_1 hbar_t] (fp32, [T][d_e + d_head]),
-// written as router_gemm_splits(dtype, d) partial sums over K slices, slice z at P + z T (d_e + d_head).
-int router_gemm_splits(int dtype, int d);
+// written as router_gemm_splits(dtype, d, T, d_e + d_head) partial sums over K slices, slice z at
+// P + z T (d_e + d_head).
+int router_gemm_splits(int dtype, int d, int T, int N);
 hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, const void* ps1,
                               int T, int d, int d_e, int d_head, float* P, hipStream_t s);
 

@@ -1097,7 +1097,17 @@ using TileRouterSmall = Tile<64, 128, 1, 4, false>;
 
 }  // namespace
 
-int router_gemm_splits(int dtype, int d) { return dtype == 1 && d % (4 * 64) == 0 ? 4 : 1; }
+// K split of the router pre-activation product: four slices while the tiles alone would leave
+// most CUs idle (a 4096-token layer has 64 tiles of 128 x 256), fewer as the token count grows,
+// none from one full round of tiles on (32768 tokens: 512 tiles), where the slices would only add
+// fp32 partial traffic for the router's pre pass to read.
+int router_gemm_splits(int dtype, int d, int T, int N) {
+  if (dtype != 1 || d % (4 * 64) != 0) return 1;
+  if (T <= 1024) return 4;
+  const long long tiles = static_cast<long long>((T + TileRouter::BM - 1) / TileRouter::BM) *
+                          ((N + TileRouter::BN - 1) / TileRouter::BN);
+  return static_cast<int>(std::max(1LL, std::min(4LL, kCUs / std::max(1LL, tiles))));
+}
 
 hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, const void* ps1, int T,
                               int d, int d_e, int d_head, float* P, hipStream_t s) {
@@ -1106,7 +1116,7 @@ hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, con
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(hbar), nullptr, d};
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_hd), static_cast<const bf16_t*>(ps1), d_e, d};
-    const int splits = router_gemm_splits(dtype, d);
+    const int splits = router_gemm_splits(dtype, d, T, N);
     if (T <= 1024 && N % TileRouterSmall::OUT_N == 0)
       return run_tile<TileRouterSmall>(A, B, epi, nullptr, T, N, d, s, splits);
     if (N % TileRouter::OUT_N == 0) return run_tile<TileRouter>(A, B, epi, nullptr, T, N, d, s, splits);
