@@ -252,29 +252,62 @@ __device__ __forceinline__ void swiglu_bwd_tile(const Epi& epi, f32x16 (&acc)[C:
 
 // NS_: LDS stages of the k-loop; the loads of tile k + NS - 1 are in flight while tile k is
 // consumed (2 for the big products, more where streaming weights from HBM needs more bytes in
-// flight per CU)
-template <int BM_, int BN_, int WM_, int WN_, bool DUAL_, int NS_ = 2>
+// flight per CU).
+// MI_: the matrix instruction, v_mfma_f32_32x32x16_bf16 (32) or v_mfma_f32_16x16x32_bf16 (16).
+// Both run at the same nominal rate; on random data the 16 x 16 x 32 form sustains a markedly
+// higher clock under the board's power limit (2.20 against 1.83-1.91 PFLOP/s in a register-only
+// loop on all CUs), so the FFN products use it.
+template <int BM_, int BN_, int WM_, int WN_, bool DUAL_, int NS_ = 2, int MI_ = 32>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr bool DUAL = DUAL_;
   static constexpr int NS = NS_;
+  static constexpr int MI = MI_;
+  static constexpr int NACC = MI * MI / 64;           // accumulator registers per MFMA tile
+  using Acc = typename std::conditional<MI == 32, f32x16, f32x4>::type;
+  static constexpr int KSTEP = MI == 32 ? 16 : 32;    // k per MFMA
   static constexpr int NT = 64 * WM * WN;
   static constexpr int NW = WM * WN;
   static constexpr int WTM = BM / WM, WTN = BN / WN;
-  static constexpr int TM = WTM / 32, TN = WTN / 32;
+  static constexpr int TM = WTM / MI, TN = WTN / MI;
   static constexpr int STAGE = (BM + BN) * ROWB;
   static constexpr int OUT_N = DUAL ? BN / 2 : BN;   // output columns per tile
   static constexpr int ON = DUAL ? WTN / 2 : WTN;     // output columns per wave
   static constexpr int OPAD = ON + 4;                 // fp32 staging row pitch (floats)
   static constexpr int SPAD = ON + 8;                 // bf16 staging row pitch (elements)
-  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole MFMA tiles");
+  static_assert(MI == 32 || MI == 16, "matrix instruction");
+  static_assert(WTM % MI == 0 && WTN % MI == 0, "wave tile must be whole MFMA tiles");
   static_assert(!DUAL || TN % 2 == 0, "gate/up tiles come in pairs");
   static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "loader split");
-  static_assert(DUAL ? NW * WTM * SPAD * 2 <= 2 * STAGE : NW * 32 * OPAD * 4 <= 2 * STAGE,
+  static_assert(DUAL ? NW * WTM * SPAD * 2 <= 2 * STAGE : NW * MI * OPAD * 4 <= 2 * STAGE,
                 "epilogue staging must fit in the stages");
-  static_assert((32 * (ON / 8)) % 64 == 0, "epilogue pieces split evenly over the lanes");
+  static_assert((MI * (ON / 8)) % 64 == 0, "epilogue pieces split evenly over the lanes");
   static_assert(NS >= 2 && NS * STAGE <= 160 * 1024, "stages fit in LDS");
 };
+
+// Lane layout of the two matrix instructions (wave64).  Operands: lane l holds 8 consecutive k of
+// row (l mod MI) of its 16 x 32 (MI 16) or 32 x 16 (MI 32) block, at k-chunk l / MI.  Result:
+// element r of lane l is row frag_out_row(r, l), column (l mod MI) of the MI x MI tile.
+template <int MI>
+__device__ __forceinline__ int out_row(int r, int lane) {
+  if constexpr (MI == 32)
+    return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+  else
+    return 4 * (lane >> 4) + r;
+}
+template <int MI>
+__device__ __forceinline__ int in_chunk(int ks, int lane) {   // 16-byte chunk of a 128-byte row
+  if constexpr (MI == 32)
+    return 2 * ks + (lane >> 5);
+  else
+    return 4 * ks + (lane >> 4);
+}
+__device__ __forceinline__ f32x16 mfma_op(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_op(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
 
 // s_waitcnt vmcnt(N) lgkmcnt(0) for a compile-time N
 template <int N>
@@ -290,7 +323,8 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   constexpr int NW = C::NW;
   constexpr int A_LD = C::BM / 8 / NW;  // wave-wide loads per k-tile, A
   constexpr int B_LD = C::BN / 8 / NW;
-  constexpr int KS = BK / 16;
+  constexpr int KS = BK / C::KSTEP;     // k-steps per k-tile
+  constexpr int MI = C::MI;
   constexpr int NM = C::TM * C::TN;     // MFMAs per k-step
   constexpr int NR = C::TM + C::TN;     // fragment reads per k-step
   constexpr int NL = A_LD + B_LD;       // stage loads per k-tile
@@ -365,23 +399,22 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
       load_lds16(b_base[i] + b_off[i] + kb, sa + C::BM * ROWB + (i * NW + wave) * 1024);
   };
 
-  f32x16 acc[C::TM][C::TN];
+  typename C::Acc acc[C::TM][C::TN];
 #pragma unroll
   for (int a = 0; a < C::TM; ++a)
 #pragma unroll
     for (int b = 0; b < C::TN; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+      for (int r = 0; r < C::NACC; ++r) acc[a][b][r] = 0.f;
 
   int fa_row[C::TM], fb_row[C::TN];
 #pragma unroll
-  for (int a = 0; a < C::TM; ++a) fa_row[a] = wm * C::WTM + a * 32 + (lane & 31);
+  for (int a = 0; a < C::TM; ++a) fa_row[a] = wm * C::WTM + a * MI + (lane & (MI - 1));
 #pragma unroll
-  for (int b = 0; b < C::TN; ++b) fb_row[b] = C::BM + wn * C::WTN + b * 32 + (lane & 31);
-  const int khalf = lane >> 5;
+  for (int b = 0; b < C::TN; ++b) fb_row[b] = C::BM + wn * C::WTN + b * MI + (lane & (MI - 1));
   bf16x8 fa[2][C::TM], fb[2][C::TN];
   auto read_frags = [&](int buf, const unsigned char* st, int ks) {
-    const int c = 2 * ks + khalf;
+    const int c = in_chunk<MI>(ks, lane);
 #pragma unroll
     for (int a = 0; a < C::TM; ++a) fa[buf][a] = *reinterpret_cast<const bf16x8*>(st + swz(fa_row[a], c));
 #pragma unroll
@@ -392,7 +425,7 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
     for (int a = 0; a < C::TM; ++a)
 #pragma unroll
       for (int b = 0; b < C::TN; ++b)
-        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][a], fb[buf][b], acc[a][b], 0, 0, 0);
+        acc[a][b] = mfma_op(fa[buf][a], fb[buf][b], acc[a][b]);
   };
   // order within the current scheduling region: MFMA, then (while any remain) one stage load
   // and one fragment read after each
@@ -457,6 +490,7 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if constexpr (DualHook<Epi>::value) {
+    static_assert(MI == 32, "the backward SwiGLU epilogue takes 32 x 32 accumulator tiles");
     swiglu_bwd_tile<C>(epi, acc, smem, m0, nt, wave, wm, wn, M, lane);
   } else if constexpr (C::DUAL) {
     // the wave's finished tile, SiLU(gate) * up in bf16, staged at once
@@ -464,12 +498,12 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
 #pragma unroll
     for (int a = 0; a < C::TM; ++a)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      for (int r = 0; r < C::NACC; ++r) {
+        const int i = a * MI + out_row<MI>(r, lane);
 #pragma unroll
         for (int b = 0; b < C::TN / 2; ++b) {
           const float g = acc[a][b][r], u = acc[a][b + C::TN / 2][r];
-          stg[i * C::SPAD + b * 32 + (lane & 31)] =
+          stg[i * C::SPAD + b * MI + (lane & (MI - 1))] =
               f32_to_bf16(g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u);
         }
       }
@@ -485,26 +519,34 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
     }
   } else {
     constexpr int CPR = C::ON / 8;                 // 8-column pieces per staged row
-    constexpr int PPB = 32 * CPR / kWave;          // pieces per lane per 32-row block
+    constexpr int PPB = MI * CPR / kWave;          // pieces per lane per MI-row block
+    // what the epilogue combines with (hbar rows) is fetched ahead of the staging, so those loads
+    // are in flight together: the whole wave tile with 32 x 32 tiles, 64 rows ahead with 16 x 16
+    // tiles (whose narrower blocks would otherwise hold twice the registers)
+    constexpr int AHEAD = MI == 32 ? C::TM : ((64 / MI) < C::TM ? (64 / MI) : C::TM);
     typename Epi::Pre pre[C::TM][PPB];
-#pragma unroll
-    for (int a = 0; a < C::TM; ++a)
+    auto fetch = [&](int a) {
 #pragma unroll
       for (int q = 0; q < PPB; ++q) {
         const int e = lane + kWave * q;
-        const int m = m0 + wm * C::WTM + a * 32 + e / CPR;
+        const int m = m0 + wm * C::WTM + a * MI + e / CPR;
         pre[a][q] = epi.prep(min(m, M - 1), nt * C::OUT_N + wn * C::ON + (e % CPR) * 8);
       }
-    float* stg = reinterpret_cast<float*>(smem) + wave * (32 * C::OPAD);
+    };
+#pragma unroll
+    for (int a = 0; a < AHEAD; ++a) fetch(a);
+    float* stg = reinterpret_cast<float*>(smem) + wave * (MI * C::OPAD);
 #pragma unroll
     for (int a = 0; a < C::TM; ++a) {
+      if (a + AHEAD < C::TM) fetch(a + AHEAD);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      for (int r = 0; r < C::NACC; ++r) {
+        const int i = out_row<MI>(r, lane);
 #pragma unroll
-        for (int b = 0; b < C::TN; ++b) stg[i * C::OPAD + b * 32 + (lane & 31)] = acc[a][b][r];
+        for (int b = 0; b < C::TN; ++b) stg[i * C::OPAD + b * MI + (lane & (MI - 1))] = acc[a][b][r];
       }
       if constexpr (BlockEpilogue<Epi>::value) {
+        static_assert(MI == 32, "block epilogues take 32-row blocks");
         // the epilogue takes the whole staged 32-row block (any lane may read any element)
         epi.block(stg, C::OPAD, C::ON, m0 + wm * C::WTM + a * 32, nt * C::OUT_N + wn * C::ON, M, lane);
       } else {
@@ -512,7 +554,7 @@ __global__ __launch_bounds__(C::NT) void mfma_gemm(ARows<bf16_t> A, BRows<bf16_t
         for (int q = 0; q < PPB; ++q) {
           const int e = lane + kWave * q;
           const int i = e / CPR, c8 = (e % CPR) * 8;
-          const int m = m0 + wm * C::WTM + a * 32 + i;
+          const int m = m0 + wm * C::WTM + a * MI + i;
           if (m < M) epi.emit8(pre[a][q], m, nt * C::OUT_N + wn * C::ON + c8, stg + i * C::OPAD + c8);
         }
       }
@@ -624,7 +666,8 @@ __global__ __launch_bounds__(C::NT) void gateup_persist(ARows<bf16_t> A, BRows<b
   constexpr int NW = C::NW;
   constexpr int A_LD = C::BM / 8 / NW;
   constexpr int B_LD = C::BN / 8 / NW;
-  constexpr int KS = BK / 16;
+  constexpr int KS = BK / C::KSTEP;
+  constexpr int MI = C::MI;
   constexpr int NM = C::TM * C::TN;
   constexpr int NR = C::TM + C::TN;
   constexpr int NL = A_LD + B_LD;
@@ -641,19 +684,18 @@ __global__ __launch_bounds__(C::NT) void gateup_persist(ARows<bf16_t> A, BRows<b
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int wm = wave / C::WN, wn = wave % C::WN;
   const int rsub = lane >> 3;
-  const int khalf = lane >> 5;
   bf16_t* ostg = reinterpret_cast<bf16_t*>(smem + 2 * C::STAGE) + wave * OUT_W;
   const int nk = K / BK;
 
   int fa_row[C::TM], fb_row[C::TN];
 #pragma unroll
-  for (int a = 0; a < C::TM; ++a) fa_row[a] = wm * C::WTM + a * 32 + (lane & 31);
+  for (int a = 0; a < C::TM; ++a) fa_row[a] = wm * C::WTM + a * MI + (lane & (MI - 1));
 #pragma unroll
-  for (int b = 0; b < C::TN; ++b) fb_row[b] = C::BM + wn * C::WTN + b * 32 + (lane & 31);
+  for (int b = 0; b < C::TN; ++b) fb_row[b] = C::BM + wn * C::WTN + b * MI + (lane & (MI - 1));
   bf16x8 fa[2][C::TM], fb[2][C::TN];
-  f32x16 acc[C::TM][C::TN];
+  typename C::Acc acc[C::TM][C::TN];
   auto read_frags = [&](int buf, const unsigned char* st, int ks) {
-    const int c = 2 * ks + khalf;
+    const int c = in_chunk<MI>(ks, lane);
 #pragma unroll
     for (int a = 0; a < C::TM; ++a) fa[buf][a] = *reinterpret_cast<const bf16x8*>(st + swz(fa_row[a], c));
 #pragma unroll
@@ -664,18 +706,18 @@ __global__ __launch_bounds__(C::NT) void gateup_persist(ARows<bf16_t> A, BRows<b
     for (int a = 0; a < C::TM; ++a)
 #pragma unroll
       for (int b = 0; b < C::TN; ++b)
-        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][a], fb[buf][b], acc[a][b], 0, 0, 0);
+        acc[a][b] = mfma_op(fa[buf][a], fb[buf][b], acc[a][b]);
   };
-  auto interleave = [&](auto nl_) {
-    constexpr int nl = decltype(nl_)::value;
+  auto interleave = [&](auto nl_, auto nr_) {
+    constexpr int nl = decltype(nl_)::value, nr = decltype(nr_)::value;
 #pragma unroll
     for (int i = 0; i < NM; ++i) {
       __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
       if (i < nl) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, 1, 0);
-      if (i < NR) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+      if (i < nr) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
     }
     if constexpr (nl > NM) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, nl - NM, 0);
-    if constexpr (NR > NM) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, NR - NM, 0);
+    if constexpr (nr > NM) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, nr - NM, 0);
   };
   // write this wave's staged block of the tile at (m0, nt) to act
   auto store_staged = [&](int m0, int nt) {
@@ -736,7 +778,7 @@ __global__ __launch_bounds__(C::NT) void gateup_persist(ARows<bf16_t> A, BRows<b
 #pragma unroll
       for (int b = 0; b < C::TN; ++b)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+        for (int r = 0; r < C::NACC; ++r) acc[a][b][r] = 0.f;
 
     // every wave is past the previous tile's last barrier: the stages are free
     issue(0, 0);
@@ -746,33 +788,42 @@ __global__ __launch_bounds__(C::NT) void gateup_persist(ARows<bf16_t> A, BRows<b
     // the previous tile's results leave while this tile computes
     if (prev_m0 >= 0) store_staged(prev_m0, prev_nt);
     read_frags(0, smem, 0);
-    for (int kt = 0; kt < nk; ++kt) {
+    // one k-tile; the modes are straight-line code as in mfma_gemm (2: the loads of tile kt + 2
+    // and the first fragments of tile kt + 1 interleave with the last k-step; 1: no tile left to
+    // load; 0: the last tile)
+    auto ktile = [&](int kt, auto mode_) {
+      constexpr int mode = decltype(mode_)::value;
       const unsigned char* st = smem + (kt & 1) * C::STAGE;
 #pragma unroll
       for (int ks = 0; ks < KS - 1; ++ks) {
         read_frags((ks + 1) & 1, st, ks + 1);
         mfmas(ks & 1);
-        interleave(std::integral_constant<int, 0>());
+        interleave(std::integral_constant<int, 0>(), std::integral_constant<int, NR>());
         __builtin_amdgcn_sched_barrier(0);
       }
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
       __syncthreads();
-      if (kt + 2 < nk) issue(kt & 1, (kt + 2) * BK);
-      if (kt + 1 < nk) read_frags(KS & 1, smem + ((kt + 1) & 1) * C::STAGE, 0);
+      if constexpr (mode == 2) issue(kt & 1, (kt + 2) * BK);
+      if constexpr (mode >= 1) read_frags(KS & 1, smem + ((kt + 1) & 1) * C::STAGE, 0);
       mfmas((KS - 1) & 1);
-      interleave(std::integral_constant<int, NL>());
+      interleave(std::integral_constant<int, mode == 2 ? NL : 0>(),
+                 std::integral_constant<int, mode >= 1 ? NR : 0>());
       __builtin_amdgcn_sched_barrier(0);
-    }
+    };
+    int kt = 0;
+    for (; kt + 2 < nk; ++kt) ktile(kt, std::integral_constant<int, 2>());
+    for (; kt + 1 < nk; ++kt) ktile(kt, std::integral_constant<int, 1>());
+    if (kt < nk) ktile(kt, std::integral_constant<int, 0>());
     // stage SiLU(gate) * up of this wave's block (its previous contents were stored above)
 #pragma unroll
     for (int a = 0; a < C::TM; ++a)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      for (int r = 0; r < C::NACC; ++r) {
+        const int i = a * MI + out_row<MI>(r, lane);
 #pragma unroll
         for (int b = 0; b < C::TN / 2; ++b) {
           const float g = acc[a][b][r], u = acc[a][b + C::TN / 2][r];
-          ostg[i * C::ON + b * 32 + (lane & 31)] = f32_to_bf16(g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u);
+          ostg[i * C::ON + b * MI + (lane & (MI - 1))] = f32_to_bf16(g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u);
         }
       }
     prev_m0 = m0;
@@ -816,12 +867,13 @@ double tile_cost(int M, int BM, int n_tiles) {
   return static_cast<double>((tiles + kCUs - 1) / kCUs) * (BM == 256 ? 1.23 : 1.0);
 }
 
-// Big-tile launch: 256 or 192 rows per tile, whichever finishes in fewer CU-rounds.
-template <int BN, bool DUAL, class Epi>
+// Big-tile launch: 256 or 192 rows per tile, whichever finishes in fewer CU-rounds.  The FFN
+// products run the 16 x 16 x 32 instruction (MI = 16); other users keep 32 x 32 x 16 tiles.
+template <int BN, bool DUAL, class Epi, int MI = 32>
 hipError_t run_big(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_count, int M_max,
                    int N_out, int K, hipStream_t s) {
-  using T256 = Tile<256, BN, 2, 4, DUAL>;
-  using T192 = Tile<192, BN, 2, 4, DUAL>;
+  using T256 = Tile<256, BN, 2, 4, DUAL, 2, MI>;
+  using T192 = Tile<192, BN, 2, 4, DUAL, 2, MI>;
   const int n_tiles = N_out / T256::OUT_N;
   if (tile_cost(M_max, 192, n_tiles) < tile_cost(M_max, 256, n_tiles)) {
     if constexpr (DUAL) {
@@ -1261,8 +1313,8 @@ hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const
       return hipGetLastError();
     }
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), INT_MAX, d};
-    return run_big<256, true>(A, B, EpiSwiGLU<bf16_t>{static_cast<bf16_t*>(act), d_ff}, counts,
-                              n_max, d_ff, d, s);
+    return run_big<256, true, EpiSwiGLU<bf16_t>, 16>(A, B, EpiSwiGLU<bf16_t>{static_cast<bf16_t*>(act), d_ff},
+                                                     counts, n_max, d_ff, d, s);
   }
   ARows<float> A{static_cast<const float*>(u), idx_ffn, d};
   BRows<float> B{static_cast<const float*>(w_gate), static_cast<const float*>(w_up), INT_MAX, d};
@@ -1291,7 +1343,7 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
     }
     EpiScatter<bf16_t, false> epi{idx_ffn, static_cast<const bf16_t*>(hbar), gate,
                                   static_cast<bf16_t*>(h_out), d};
-    return run_big<256, false>(A, B, epi, counts, n_max, d, d_ff, s);
+    return run_big<256, false, EpiScatter<bf16_t, false>, 16>(A, B, epi, counts, n_max, d, d_ff, s);
   }
   ARows<float> A{static_cast<const float*>(act), nullptr, d_ff};
   BRows<float> B{static_cast<const float*>(w_down), nullptr, INT_MAX, d_ff};
