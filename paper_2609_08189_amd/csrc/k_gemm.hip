@@ -1140,6 +1140,15 @@ int adapter_groups(int K) {
   return G;
 }
 int adapter_batch(int K, int G) { return (K / G) % 512 == 0 ? 8 : 4; }
+// The forward's K-slices for a call of up to n_max adapter rows: fewer as the rows alone give
+// enough workgroups (the up-projection reads every slice once per 256-column block, so at the
+// 8B stack's 12.7k adapter rows eight slices would be read 16 times over for nothing).
+int adapter_groups_rows(int K, int n_max) {
+  int G = adapter_groups(K);
+  const long long row_tiles = (static_cast<long long>(n_max) + 31) / 32;
+  while (G > 1 && row_tiles * G > 2048) G >>= 1;
+  return G;
+}
 
 // router pre-activations: 128-row tiles over all 8 waves, K split four ways
 using TileRouter = Tile<128, 256, 2, 4, false>;
@@ -1532,8 +1541,7 @@ namespace {
 // second product over the same rows in the same launch (gridDim.z = 2)
 hipError_t adapter_down_small(const bf16_t* uu, const int* idx_ad, const int* counts, int n_max, const bf16_t* ww,
                               float* part, int d, int d_r, hipStream_t s, const bf16_t* u2, const bf16_t* w2_,
-                              float* p2) {
-  const int G = adapter_groups(d);
+                              float* p2, int G) {
   dim3 g1((n_max + 31) / 32, G, u2 ? 2 : 1);
   // the adapter rank is a compile-time count of 32-column MFMA tiles
   const bool b8 = adapter_batch(d, G) == 8;
@@ -1570,7 +1578,7 @@ hipError_t launch_adapter_down(int dtype, const void* u, const int* idx_ad, cons
   }
   if (dtype == 1)
     return adapter_down_small(static_cast<const bf16_t*>(u), idx_ad, counts, n_max, static_cast<const bf16_t*>(w1),
-                              part, d, d_r, s, nullptr, nullptr, nullptr);
+                              part, d, d_r, s, nullptr, nullptr, nullptr, adapter_groups_rows(d, n_max));
   // fp32: hid = SiLU(u W_1^T) into part[m][n]
   ARows<float> A{static_cast<const float*>(u), idx_ad, d};
   BRows<float> B{static_cast<const float*>(w1), nullptr, INT_MAX, d};
@@ -1590,7 +1598,7 @@ hipError_t launch_adapter_up(int dtype, const float* part, const int* idx_ad, co
     return run_tile<TileWide>(A, B, epi, counts, n_max, d, d_r, s);
   }
   if (dtype == 1) {
-    const int G = adapter_groups(d);
+    const int G = adapter_groups_rows(d, n_max);
     dim3 g2((n_max + 31) / 32, d / 256);
     const bf16_t* ww = static_cast<const bf16_t*>(w2);
     const bf16_t* hb = static_cast<const bf16_t*>(hbar);
@@ -1684,7 +1692,7 @@ hipError_t launch_adapter_proj2(int dtype, const void* rows0, const void* w0, fl
   if (dtype == 1 && !adapter_wide(d_r))
     return adapter_down_small(static_cast<const bf16_t*>(rows0), idx_ad, counts, n_max, static_cast<const bf16_t*>(w0),
                               part0, d, d_r, s, static_cast<const bf16_t*>(rows1), static_cast<const bf16_t*>(w1),
-                              part1);
+                              part1, adapter_groups(d));
   hipError_t e = launch_adapter_proj(dtype, rows0, idx_ad, counts, n_max, w0, part0, d, d_r, s);
   if (e != hipSuccess) return e;
   return launch_adapter_proj(dtype, rows1, idx_ad, counts, n_max, w1, part1, d, d_r, s);
@@ -1700,7 +1708,10 @@ hipError_t launch_adapter_proj(int dtype, const void* rows, const int* idx_ad, c
     const size_t stride = static_cast<size_t>(n_max) * d_r;
     return run_tile<TileWide>(A, B, EpiStoreF32{part, d_r, stride}, counts, n_max, d_r, d, s, WIDE_SPLIT);
   }
-  if (dtype == 1) return launch_adapter_down(1, rows, idx_ad, counts, n_max, w, part, d, d_r, s);
+  // the backward's consumers sum adapter_proj_splits() = adapter_groups(d) slices
+  if (dtype == 1)
+    return adapter_down_small(static_cast<const bf16_t*>(rows), idx_ad, counts, n_max, static_cast<const bf16_t*>(w),
+                              part, d, d_r, s, nullptr, nullptr, nullptr, adapter_groups(d));
   ARows<float> A{static_cast<const float*>(rows), idx_ad, d};
   BRows<float> B{static_cast<const float*>(w), nullptr, INT_MAX, d};
   return run_f32<false>(A, B, EpiStoreF32{part, d_r, 0}, counts, n_max, d_r, d, s);
