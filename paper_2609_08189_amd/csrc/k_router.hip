@@ -526,11 +526,17 @@ struct SProj {
 // PF2 output tiles per wave), the local head's weights and the path-vector inputs; what follows
 // works from registers and LDS between four barriers.
 constexpr int NTP = 512;
+constexpr unsigned kCUsRouter = 256;   // compute units of an MI355X
 constexpr int NWP = NTP / kWave;
 constexpr int PF2 = 6;
 
-template <int KSS>   // k-steps over d_s (ceil(d_s / 32))
-__global__ __launch_bounds__(NTP) void router_pre_mfma(RouterTailArgs a) {
+// KSS: k-steps over d_s (ceil(d_s / 32)).  WPE: waves per SIMD the kernel is compiled for (2: one
+// workgroup per CU with every weight fragment loaded up front, for launches of about one round of
+// workgroups; 4: two workgroups per CU, each hiding the other's latencies, for many rounds)
+// NSPL: the most K-slice partials of P the launch may have (p_splits <= NSPL); PF: output tiles
+// of the s-projections per wave whose weight fragments are loaded up front
+template <int KSS, int WPE = 2, int NSPL = MAXSPLIT, int PF = PF2>
+__global__ __launch_bounds__(NTP, WPE) void router_pre_mfma(RouterTailArgs a) {
   LDS16 bf16x8 ax[2][KS_E][kWave];   // SiLU(inv_rms W_hd hbar): hi, lo
   LDS16 bf16x8 as[2][KS_S][kWave];   // s: hi, lo
   LDS16 float s[MT][MAXS + 4];
@@ -560,12 +566,12 @@ __global__ __launch_bounds__(NTP) void router_pre_mfma(RouterTailArgs a) {
   const int tt = tid >> 5, pc = tid & 31;
   const bool has_p = 16 * pc < NP;
   const bool head = has_p && 16 * pc >= d_e;
-  f32x4 pz[MAXSPLIT][4];
+  f32x4 pz[NSPL][4];
   if (has_p) {
     const float* src = a.P + static_cast<size_t>(min(t0 + tt, a.T - 1)) * NP + 16 * pc;
     const size_t zs = static_cast<size_t>(a.T) * NP;
 #pragma unroll
-    for (int z = 0; z < MAXSPLIT; ++z)
+    for (int z = 0; z < NSPL; ++z)
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         pz[z][q] = *reinterpret_cast<const f32x4*>(src + (z < a.p_splits ? z : 0) * zs + 4 * q);
@@ -586,10 +592,10 @@ __global__ __launch_bounds__(NTP) void router_pre_mfma(RouterTailArgs a) {
     for (int st = 0; st < KS_E; ++st)
       if (st < ks1) b1[st] = bfrag(static_cast<const bf16_t*>(a.w_hu), d_e, d_h, 16 * wave, 32 * st, d_e, lane);
   }
-  // (4) s-projections: this wave's first PF2 output tiles ct = wave + NWP c
-  bf16x8 b2[PF2][KSS];
+  // (4) s-projections: this wave's first PF output tiles ct = wave + NWP c
+  bf16x8 b2[PF][KSS];
 #pragma unroll
-  for (int c = 0; c < PF2; ++c) {
+  for (int c = 0; c < PF; ++c) {
     const int ct = wave + NWP * c;
     if (ct < nct) {
       const SProj p = proj(ct);
@@ -635,7 +641,7 @@ __global__ __launch_bounds__(NTP) void router_pre_mfma(RouterTailArgs a) {
       for (int e = 0; e < 4; ++e) {
         float v = pz[0][q][e];
 #pragma unroll
-        for (int z = 1; z < MAXSPLIT; ++z)
+        for (int z = 1; z < NSPL; ++z)
           if (z < a.p_splits) v += pz[z][q][e];
         x[4 * q + e] = v;
       }
@@ -729,9 +735,9 @@ __global__ __launch_bounds__(NTP) void router_pre_mfma(RouterTailArgs a) {
     }
   };
 #pragma unroll
-  for (int c = 0; c < PF2; ++c)
+  for (int c = 0; c < PF; ++c)
     if (wave + NWP * c < nct) finish(wave + NWP * c, b2[c]);
-  for (int ct = wave + NWP * PF2; ct < nct; ct += NWP) {
+  for (int ct = wave + NWP * PF; ct < nct; ct += NWP) {
     const SProj p = proj(ct);
     bf16x8 bw[KSS];
 #pragma unroll
@@ -994,11 +1000,14 @@ hipError_t launch_pre_post(const RouterTailArgs& a, bool post, hipStream_t s) {
         default: return hipErrorInvalidValue;
       }
     } else {
+      // many rounds of workgroups (more than two per CU) with an unsplit P: two resident
+      // workgroups per CU, weight fragments loaded as they are needed
+      const bool many = grid.x > 2u * kCUsRouter && a.p_splits == 1;
       switch ((a.d_s + 31) / 32) {
-        case 1: router_pre_mfma<1><<<grid, NTP, 0, s>>>(a); break;
-        case 2: router_pre_mfma<2><<<grid, NTP, 0, s>>>(a); break;
-        case 3: router_pre_mfma<3><<<grid, NTP, 0, s>>>(a); break;
-        case 4: router_pre_mfma<4><<<grid, NTP, 0, s>>>(a); break;
+        case 1: many ? router_pre_mfma<1, 4, 1, 1><<<grid, NTP, 0, s>>>(a) : router_pre_mfma<1><<<grid, NTP, 0, s>>>(a); break;
+        case 2: many ? router_pre_mfma<2, 4, 1, 1><<<grid, NTP, 0, s>>>(a) : router_pre_mfma<2><<<grid, NTP, 0, s>>>(a); break;
+        case 3: many ? router_pre_mfma<3, 4, 1, 1><<<grid, NTP, 0, s>>>(a) : router_pre_mfma<3><<<grid, NTP, 0, s>>>(a); break;
+        case 4: many ? router_pre_mfma<4, 4, 1, 1><<<grid, NTP, 0, s>>>(a) : router_pre_mfma<4><<<grid, NTP, 0, s>>>(a); break;
         default: return hipErrorInvalidValue;
       }
     }
