@@ -1155,6 +1155,8 @@ using TileRouter = Tile<128, 256, 2, 4, false>;
 using TileRouterNarrow = Tile<128, 128, 2, 4, false>;
 // few tokens (a decode batch): 64-row tiles of 4 waves, four times the workgroups
 using TileRouterSmall = Tile<64, 128, 1, 4, false>;
+// many tokens: 256 x 256 tiles on v_mfma_f32_16x16x32_bf16
+using TileRouterBig = Tile<256, 256, 2, 4, false, 2, 16>;
 
 }  // namespace
 
@@ -1180,6 +1182,10 @@ hipError_t launch_router_gemm(int dtype, const void* hbar, const void* w_hd, con
     const int splits = router_gemm_splits(dtype, d, T, N);
     if (T <= 1024 && N % TileRouterSmall::OUT_N == 0)
       return run_tile<TileRouterSmall>(A, B, epi, nullptr, T, N, d, s, splits);
+    // a full round or more of tiles: the FFN products' 256 x 256 tiles on the 16 x 16 x 32
+    // instruction (32768 tokens: 256 tiles, no K split)
+    if (splits == 1 && T >= 16384 && N % TileRouterBig::OUT_N == 0)
+      return run_tile<TileRouterBig>(A, B, epi, nullptr, T, N, d, s);
     if (N % TileRouter::OUT_N == 0) return run_tile<TileRouter>(A, B, epi, nullptr, T, N, d, s, splits);
     return run_tile<TileRouterNarrow>(A, B, epi, nullptr, T, N, d, s, splits);
   }
