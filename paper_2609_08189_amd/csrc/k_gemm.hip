@@ -858,6 +858,238 @@ hipError_t run_tile(ARows<bf16_t> A, BRows<bf16_t> B, Epi epi, const int* m_coun
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Skinny products: a batch of at most 256 rows (a decode step) against weights streamed once
+// from HBM.  The output columns are cut into 16-column blocks spread evenly over the workgroups
+// (block group x takes the contiguous blocks [x nb / G, (x + 1) nb / G), and for the gate/up
+// product the same blocks of W_u); S K-slices per block group where one workgroup per group
+// would pull the activation rows through L2 too many times.
+// Eight waves, one workgroup per CU.  Four consumers run the MFMAs (16 x 16 x 32), each on 16 RB
+// rows against every weight block of the workgroup; four producers stage tiles into LDS, two the
+// activation rows and two the weight rows, each pair into a ring of its own depth (weights come
+// from HBM and need more bytes in flight than the L2-resident activations).  A producer's waits
+// count only its own loads.  One barrier per k-tile, placed before the consumers' last k-step: by
+// then they hold the whole stage in registers, so the producers refill it and the first
+// fragments of the next tile are read while the last MFMAs run.
+// What bounds it (measured on cold weights): a 64-deep k-tile takes 128 bytes from each weight
+// row, and HBM serves such row-strided visits at ~3.5 TB/s (4.5 at 256 bytes, 5.3 at 512); with
+// three or more row blocks the per-tile LDS traffic (DMA writes plus every consumer's fragment
+// reads, ~108 KiB at 192 x 96) takes longer still, so deeper weight visits (which cost the
+// activation ring its stages) and activation loads straight to registers both measured slower.
+// ---------------------------------------------------------------------------
+template <int NB_, int RB_, int NSA_, int NSB_, bool DUAL_>
+struct Skinny {
+  static constexpr int NB = NB_, RB = RB_, NSA = NSA_, NSB = NSB_;
+  static constexpr bool DUAL = DUAL_;
+  static constexpr int SL = DUAL ? 2 * NB : NB;   // 16-row weight blocks per stage
+  static constexpr int MP = 64 * RB;              // rows covered (4 consumer waves x 16 RB)
+  static constexpr int A_STAGE = MP * ROWB, B_STAGE = SL * 16 * ROWB;
+  static constexpr int LDS = NSA * A_STAGE + NSB * B_STAGE;
+  static constexpr int AL = MP / 16;              // 1 KiB loads per stage per A producer
+  static constexpr int BL = SL;                   // 1 KiB loads per stage per B producer
+  static_assert(LDS <= 160 * 1024, "stages fit in LDS");
+  static_assert((NSA - 1) * AL < 64 && (NSB - 1) * BL < 64, "loads in flight within vmcnt");
+  static_assert(NSA >= 2 && NSB >= 2 && RB >= 1 && RB <= 4 && NB >= 1, "shape");
+};
+
+// deepest weight ring that fits beside NSA activation stages
+constexpr int skinny_nsb(int NB, int RB, bool dual, int NSA) {
+  const int sl = dual ? 2 * NB : NB;
+  int n = (160 * 1024 - NSA * 64 * RB * ROWB) / (sl * 16 * ROWB);
+  n = n < 8 ? n : 8;
+  return n < 63 / sl + 1 ? n : 63 / sl + 1;
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Epilogue: gate/up writes act[m][c] = bf16(SiLU(g) u) (out = act, ld = d_ff); otherwise the
+// K-slice y writes fp32 sums to part + y split_stride (out = part, ld = N).
+template <class C>
+__global__ __launch_bounds__(512) void skinny_gemm(ARows<bf16_t> A, const bf16_t* __restrict__ b0,
+                                                  const bf16_t* __restrict__ b1, int ldb,
+                                                  void* __restrict__ out, int ld, size_t split_stride,
+                                                  const int* __restrict__ m_count, int n_max, int K,
+                                                  int nb, int G, int S) {
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
+  unsigned char* const sa = smem;
+  unsigned char* const sb = smem + C::NSA * C::A_STAGE;
+  // G block groups x S K-slices in slice-major order, laid over the 8 XCDs (round-robin dispatch)
+  // in contiguous runs: the workgroups of one XCD share one or two K-slices of the activations
+  // in its L2
+  const int id = static_cast<int>(blockIdx.x), N = G * S;
+  const int L = N % 8 == 0 ? (id & 7) * (N >> 3) + (id >> 3) : id;
+  const int x = L % G, y = L / G;
+  const int blk0 = x * nb / G;
+  const int cnt = (x + 1) * nb / G - blk0;
+  const int M = m_count ? min(*m_count, n_max) : n_max;
+  if (M <= 0) return;
+  const int nkt = K / BK;
+  const int kt0 = y * nkt / S;
+  const int nk = (y + 1) * nkt / S - kt0;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  constexpr int NSA = C::NSA, NSB = C::NSB;
+
+  if (wave >= 6) {
+    // weight producer: loads q = 2 i + pw, LDS rows 8q .. 8q + 7 = half (q & 1) of block slot q / 2;
+    // a workgroup with fewer than NB blocks reloads its last one into the spare slots
+    const int pw = wave - 6;
+    const unsigned char* base[C::BL];
+    uint32_t off[C::BL];
+#pragma unroll
+    for (int i = 0; i < C::BL; ++i) {
+      const int q = 2 * i + pw, slot = q >> 1;
+      const int j = slot % C::NB;
+      const int r = 8 * q + (lane >> 3);
+      const int ch = (lane & 7) ^ ((r >> 1) & 7);
+      const int wrow = 16 * (blk0 + min(j, cnt - 1)) + 8 * (q & 1) + (lane >> 3);
+      base[i] = reinterpret_cast<const unsigned char*>(C::DUAL && slot >= C::NB ? b1 : b0);
+      off[i] = static_cast<uint32_t>(wrow) * static_cast<uint32_t>(ldb * 2) + kt0 * ROWB + ch * 16;
+    }
+    auto issue = [&](int t) {
+      unsigned char* st = sb + (t % NSB) * C::B_STAGE;
+#pragma unroll
+      for (int i = 0; i < C::BL; ++i) load_lds16(base[i] + off[i] + t * ROWB, st + (2 * i + pw) * 1024);
+    };
+    for (int t = 0; t < NSB; ++t)
+      if (t < nk) issue(t);
+    // before barrier j tile j + 1 has landed; tiles up to j + NSB - 1 may be in flight
+    for (int j = -1; j < nk; ++j) {
+      if (j < 0) {
+        if (nk >= NSB) wait_vm<(NSB - 1) * C::BL>(); else wait_vm<0>();
+      } else if (j + NSB <= nk) {
+        wait_vm<(NSB - 2) * C::BL>();
+      } else {
+        wait_vm<0>();
+      }
+      __syncthreads();
+      if (j >= 0 && j + NSB < nk) issue(j + NSB);
+    }
+    return;
+  }
+  if (wave >= 4) {
+    // activation producer: loads q = 2 i + pw, LDS rows 8q .. 8q + 7; rows past M repeat row M - 1
+    const int pw = wave - 4;
+    uint32_t off[C::AL];
+#pragma unroll
+    for (int i = 0; i < C::AL; ++i) {
+      const int r = 8 * (2 * i + pw) + (lane >> 3);
+      const int ch = (lane & 7) ^ ((r >> 1) & 7);
+      const int m = min(r, M - 1);
+      const int row = A.idx ? A.idx[m] : m;
+      off[i] = static_cast<uint32_t>(row) * static_cast<uint32_t>(A.ld * 2) + kt0 * ROWB + ch * 16;
+    }
+    const unsigned char* abase = reinterpret_cast<const unsigned char*>(A.base);
+    auto issue = [&](int t) {
+      unsigned char* st = sa + (t % NSA) * C::A_STAGE;
+#pragma unroll
+      for (int i = 0; i < C::AL; ++i) load_lds16(abase + off[i] + t * ROWB, st + (2 * i + pw) * 1024);
+    };
+    for (int t = 0; t < NSA; ++t)
+      if (t < nk) issue(t);
+    for (int j = -1; j < nk; ++j) {
+      if (j < 0) {
+        if (nk >= NSA) wait_vm<(NSA - 1) * C::AL>(); else wait_vm<0>();
+      } else if (j + NSA <= nk) {
+        wait_vm<(NSA - 2) * C::AL>();
+      } else {
+        wait_vm<0>();
+      }
+      __syncthreads();
+      if (j >= 0 && j + NSA < nk) issue(j + NSA);
+    }
+    return;
+  }
+
+  // consumers
+  constexpr int RB = C::RB, SL = C::SL;
+  f32x4 acc[RB][SL];
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int c = 0; c < SL; ++c) acc[r][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 fa[2][RB], fb[2][SL];
+  const int arow0 = wave * 16 * RB + (lane & 15), brow0 = lane & 15;
+  auto read = [&](int buf, const unsigned char* ast, const unsigned char* bst, int ks) {
+    const int c = in_chunk<16>(ks, lane);
+#pragma unroll
+    for (int r = 0; r < RB; ++r) fa[buf][r] = *reinterpret_cast<const bf16x8*>(ast + swz(arow0 + 16 * r, c));
+#pragma unroll
+    for (int b = 0; b < SL; ++b) fb[buf][b] = *reinterpret_cast<const bf16x8*>(bst + swz(brow0 + 16 * b, c));
+  };
+  auto mfmas = [&](int buf) {
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+#pragma unroll
+      for (int b = 0; b < SL; ++b) acc[r][b] = mfma_op(fa[buf][r], fb[buf][b], acc[r][b]);
+  };
+  // the fragment reads of the other k-step go out one after each MFMA; the reads of tile kt + 1
+  // past the last tile hit a stale stage and are never used
+  auto interleave = [&]() {
+#pragma unroll
+    for (int i = 0; i < RB * SL; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+      if (i < RB + SL) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+    }
+    if constexpr (RB + SL > RB * SL) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, RB + SL - RB * SL, 0);
+  };
+  __syncthreads();                       // barrier -1: tile 0 has landed
+  read(0, sa, sb, 0);
+  int ia = 0, ib = 0;                    // stages of tile kt
+  for (int kt = 0; kt < nk; ++kt) {
+    read(1, sa + ia * C::A_STAGE, sb + ib * C::B_STAGE, 1);
+    mfmas(0);
+    interleave();
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __syncthreads();                     // barrier kt: stage kt is free, tile kt + 1 has landed
+    ia = ia + 1 == NSA ? 0 : ia + 1;
+    ib = ib + 1 == NSB ? 0 : ib + 1;
+    read(0, sa + ia * C::A_STAGE, sb + ib * C::B_STAGE, 0);
+    mfmas(1);
+    interleave();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // element i of acc[r][b] in lane l: row 16 (wave RB + r) + 4 (l >> 4) + i, column l & 15
+  const int col = lane & 15;
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = 16 * (wave * RB + r) + 4 * (lane >> 4) + i;
+      if (m >= M) continue;
+      if constexpr (C::DUAL) {
+        bf16_t* o = static_cast<bf16_t*>(out) + static_cast<size_t>(m) * ld;
+#pragma unroll
+        for (int j = 0; j < C::NB; ++j) {
+          if (j >= cnt) break;
+          const float g = acc[r][j][i], u = acc[r][C::NB + j][i];
+          o[16 * (blk0 + j) + col] = f32_to_bf16(g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u);
+        }
+      } else {
+        float* o = static_cast<float*>(out) + y * split_stride + static_cast<size_t>(m) * ld;
+#pragma unroll
+        for (int j = 0; j < C::NB; ++j) {
+          if (j >= cnt) break;
+          o[16 * (blk0 + j) + col] = acc[r][j][i];
+        }
+      }
+    }
+}
+
+template <class C>
+hipError_t run_skinny(ARows<bf16_t> A, const bf16_t* b0, const bf16_t* b1, int ldb, void* out, int ld,
+                      size_t split_stride, const int* m_count, int n_max, int K, int nb, int G, int S,
+                      hipStream_t s) {
+  skinny_gemm<C><<<G * S, 512, 0, s>>>(A, b0, b1, ldb, out, ld, split_stride, m_count, n_max, K, nb, G, S);
+  return hipGetLastError();
+}
+
 // Time of a launch in units of one round of 192-row tiles: CU rounds times the relative
 // duration of a round.  A 256-row tile moves fewer bytes through L2 per FLOP, so its round
 // takes ~1.23x (not 256/192 = 1.33x) a 192-row round on the FFN products (measured on the
@@ -1204,10 +1436,67 @@ namespace {
 // ---------------------------------------------------------------------------
 using TileSplitGU = Tile<192, 256, 2, 4, false>;    // [W_g; W_u] as one 2 d_ff-row operand
 using TileSplitDown = Tile<192, 128, 2, 4, false, 4>;
-// one row tile (a decode batch): gate/up on 4-wave 192 x 128 tiles (64 output columns each), so
-// that d_ff / 64 workgroups cover the CUs without splitting K, with four stages in flight
-using TileDecodeGU = Tile<192, 128, 2, 2, true, 4>;
 constexpr int kMaxSplitGU = 8, kMaxSplitDown = 16;
+
+// At most 256 rows (a decode batch): the skinny products.  Gate/up: one workgroup per CU, each
+// with 2-4 blocks of 16 columns of W_g and W_u and the whole of K.  Down: blocks of 8 x 16 output
+// columns by kSkinnyDownS K-slices, whose fp32 partial sums a pass adds in a fixed order.
+constexpr int kSkinnyRows = 256, kSkinnyDownNB = 8, kSkinnyDownS = 8;
+bool skinny_gateup_fits(int n_max, int d, int d_ff) {
+  const int nb = d_ff / 16;
+  return n_max <= kSkinnyRows && d % BK == 0 && d_ff % 16 == 0 && nb <= 4 * kCUs;
+}
+int skinny_down_splits(int d, int d_ff) {
+  const int G = d / (16 * kSkinnyDownNB), nkt = d_ff / BK;
+  return std::max(1, std::min({kSkinnyDownS, kCUs / std::max(G, 1), nkt}));
+}
+bool skinny_down_fits(int n_max, int d, int d_ff) {
+  return n_max <= kSkinnyRows && d % (16 * kSkinnyDownNB) == 0 && d_ff % BK == 0;
+}
+
+template <int NB, int RB>
+hipError_t skinny_gateup_nb_rb(ARows<bf16_t> A, const bf16_t* wg, const bf16_t* wu, bf16_t* act,
+                               const int* counts, int n_max, int d, int d_ff, hipStream_t s) {
+  using C = Skinny<NB, RB, 3, skinny_nsb(NB, RB, true, 3), true>;
+  const int nb = d_ff / 16, G = std::min(kCUs, nb);
+  return run_skinny<C>(A, wg, wu, d, act, d_ff, 0, counts, n_max, d, nb, G, 1, s);
+}
+template <int NB>
+hipError_t skinny_gateup_nb(ARows<bf16_t> A, const bf16_t* wg, const bf16_t* wu, bf16_t* act,
+                            const int* counts, int n_max, int d, int d_ff, hipStream_t s) {
+  switch ((n_max + 63) / 64) {
+    case 1: return skinny_gateup_nb_rb<NB, 1>(A, wg, wu, act, counts, n_max, d, d_ff, s);
+    case 2: return skinny_gateup_nb_rb<NB, 2>(A, wg, wu, act, counts, n_max, d, d_ff, s);
+    case 3: return skinny_gateup_nb_rb<NB, 3>(A, wg, wu, act, counts, n_max, d, d_ff, s);
+    default: return skinny_gateup_nb_rb<NB, 4>(A, wg, wu, act, counts, n_max, d, d_ff, s);
+  }
+}
+hipError_t skinny_gateup(ARows<bf16_t> A, const bf16_t* wg, const bf16_t* wu, bf16_t* act,
+                         const int* counts, int n_max, int d, int d_ff, hipStream_t s) {
+  const int nb = d_ff / 16, G = std::min(kCUs, nb);
+  switch ((nb + G - 1) / G) {   // most blocks a workgroup takes
+    case 1: return skinny_gateup_nb<1>(A, wg, wu, act, counts, n_max, d, d_ff, s);
+    case 2: return skinny_gateup_nb<2>(A, wg, wu, act, counts, n_max, d, d_ff, s);
+    case 3: return skinny_gateup_nb<3>(A, wg, wu, act, counts, n_max, d, d_ff, s);
+    default: return skinny_gateup_nb<4>(A, wg, wu, act, counts, n_max, d, d_ff, s);
+  }
+}
+template <int RB>
+hipError_t skinny_down_rb(ARows<bf16_t> A, const bf16_t* wd, float* part, size_t stride,
+                          const int* counts, int n_max, int d, int d_ff, int S, hipStream_t s) {
+  using C = Skinny<kSkinnyDownNB, RB, 3, skinny_nsb(kSkinnyDownNB, RB, false, 3), false>;
+  const int nb = d / 16;
+  return run_skinny<C>(A, wd, nullptr, d_ff, part, d, stride, counts, n_max, d_ff, nb, nb / kSkinnyDownNB, S, s);
+}
+hipError_t skinny_down(ARows<bf16_t> A, const bf16_t* wd, float* part, size_t stride, const int* counts,
+                       int n_max, int d, int d_ff, int S, hipStream_t s) {
+  switch ((n_max + 63) / 64) {
+    case 1: return skinny_down_rb<1>(A, wd, part, stride, counts, n_max, d, d_ff, S, s);
+    case 2: return skinny_down_rb<2>(A, wd, part, stride, counts, n_max, d, d_ff, S, s);
+    case 3: return skinny_down_rb<3>(A, wd, part, stride, counts, n_max, d, d_ff, S, s);
+    default: return skinny_down_rb<4>(A, wd, part, stride, counts, n_max, d, d_ff, S, s);
+  }
+}
 
 int split_ways(int tiles, int nkt, int cap) {
   if (tiles <= 0 || 2 * tiles > kCUs) return 1;
@@ -1294,6 +1583,8 @@ size_t ffn_part_floats(int dtype, int d, int d_ff, int T) {
   if (dtype != 1 || T <= 0) return 0;
   // S is fixed per row-tile count and the slices hold n rows: the largest n of each count
   size_t most = 0;
+  const int ns = std::min(T, kSkinnyRows);
+  if (skinny_down_fits(ns, d, d_ff)) most = static_cast<size_t>(skinny_down_splits(d, d_ff)) * ns * d;
   for (int mt = 1; (mt - 1) * TileSplitGU::BM < T; ++mt) {
     const int n = std::min(mt * TileSplitGU::BM, T);
     const int sg = gateup_split(n, d, d_ff), sd = down_split(n, d, d_ff);
@@ -1310,11 +1601,9 @@ hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const
   if (n_max <= 0) return hipSuccess;
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(u), idx_ffn, d};
-    if (n_max <= TileDecodeGU::BM && d_ff % TileDecodeGU::OUT_N == 0 && d_ff / TileDecodeGU::OUT_N <= kCUs) {
-      BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), INT_MAX, d};
-      return run_tile<TileDecodeGU>(A, B, EpiSwiGLU<bf16_t>{static_cast<bf16_t*>(act), d_ff}, counts,
-                                    n_max, d_ff, d, s);
-    }
+    if (skinny_gateup_fits(n_max, d, d_ff))
+      return skinny_gateup(A, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
+                           static_cast<bf16_t*>(act), counts, n_max, d, d_ff, s);
     const int S = gateup_split(n_max, d, d_ff);
     if (S > 1) {
       BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), d_ff, d};
@@ -1344,11 +1633,14 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(act), nullptr, d_ff};
     BRows<bf16_t> B{static_cast<const bf16_t*>(w_down), nullptr, INT_MAX, d_ff};
-    const int S = down_split(n_max, d, d_ff);
-    if (S > 1) {
+    const bool skinny = skinny_down_fits(n_max, d, d_ff);
+    const int S = skinny ? skinny_down_splits(d, d_ff) : down_split(n_max, d, d_ff);
+    if (S > 1 || skinny) {
       const size_t stride = static_cast<size_t>(n_max) * d;
-      hipError_t e = run_tile<TileSplitDown>(A, B, EpiStoreF32{part, d, stride}, counts, n_max, d,
-                                             d_ff, s, S);
+      hipError_t e = skinny ? skinny_down(A, static_cast<const bf16_t*>(w_down), part, stride, counts, n_max, d,
+                                          d_ff, S, s)
+                            : run_tile<TileSplitDown>(A, B, EpiStoreF32{part, d, stride}, counts, n_max, d,
+                                                      d_ff, s, S);
       if (e != hipSuccess) return e;
       const size_t n8 = static_cast<size_t>(n_max) * (d / 8);
       scatter_reduce<<<static_cast<unsigned>((n8 + 255) / 256), 256, 0, s>>>(
