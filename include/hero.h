@@ -294,7 +294,7 @@ int hero_routed_layer(const hero_dims *dims, int j, int T,
  * later reads within the same call).  A call whose workspace (hero_workspace_size with
  * for_stack = 0) exceeds the area returns HERO_E_SCRATCH before any launch; at the
  * Llama-3.1-8B shape (d = 4096, d_ff = 14336, r = 64, d_m = 128) that allows up to 473 tokens,
- * and a 256-token decode batch of the Llama-2-7B shape needs 42.5 MiB of it.  The first call on a device looks the area up on that device (it must be
+ * and a 256-token decode batch of the Llama-2-7B shape needs 43.0 MiB of it.  The first call on a device looks the area up on that device (it must be
  * current); later calls reuse it.  Every call on one device shares that device's area: calls that
  * overlap in time on one device (two streams, two threads) race and must be serialised by the
  * caller.

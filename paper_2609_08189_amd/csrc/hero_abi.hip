@@ -37,8 +37,13 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
 }
 
 struct Layout {
-  size_t u, P, rowstat, logit, gate, mask, idx_ffn, idx_ad, counts, lambda, act, part, rscr, ring, total;
+  size_t u, P, rowstat, logit, gate, mask, idx_ffn, idx_ad, counts, lambda, act, part, part_ad, rscr, ring,
+      total;
 };
+
+// At most this many tokens (a decode batch) the adapter branch runs beside the FFN branch, on a
+// second stream, with a partial-sum region of its own.
+constexpr int kOverlapTokens = 256;
 
 Layout layout_of(const hero_dims& d, int T, bool stack) {
   const size_t es = esize(d.dtype), t = static_cast<size_t>(T);
@@ -60,9 +65,16 @@ Layout layout_of(const hero_dims& d, int T, bool stack) {
   L.counts = take(16);
   L.lambda = take(16);
   L.act = take(t * d.d_ff * es);
-  // the FFN's split-K partials and the adapter's hidden rows share one region (run in turn)
-  L.part = take(std::max(hero::adapter_part_floats(d.dtype, d.d, d.d_r, T),
-                         hero::ffn_part_floats(d.dtype, d.d, d.d_ff, T)) * 4);
+  // the FFN's split-K partials and the adapter's hidden rows: one region used in turn, or two
+  // when the branches overlap
+  const size_t pa = hero::adapter_part_floats(d.dtype, d.d, d.d_r, T) * 4;
+  const size_t pf = hero::ffn_part_floats(d.dtype, d.d, d.d_ff, T) * 4;
+  if (T <= kOverlapTokens) {
+    L.part = take(pf);
+    L.part_ad = take(pa);
+  } else {
+    L.part = L.part_ad = take(std::max(pa, pf));
+  }
   L.rscr = take(hero::router_scratch_floats(d.d_m, d.d_head, T) * 4);
   L.ring = stack ? take(3 * t * d.d * es) : 0;
   L.total = off;
@@ -192,6 +204,33 @@ hipError_t timed(int which, hipStream_t s, F&& launch) {
   return e;
 }
 
+// A second stream of the calling thread on one device, with the events that fork work onto it
+// and join it back (thread-local: calls from different host threads never share one).  Created
+// on a device's first call from the thread, outside any graph capture that follows (a failure
+// leaves the calls on one stream), and kept until the process ends.
+struct Side {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  bool tried = false;
+};
+
+const Side* side_of_current_device() {
+  constexpr int kDevices = 64;
+  thread_local Side sides[kDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevices) return nullptr;
+  Side& sd = sides[dev];
+  if (!sd.tried) {
+    sd.tried = true;
+    // default priority (work on streams of different priorities has hung on this hardware)
+    if (hipStreamCreateWithFlags(&sd.s, hipStreamNonBlocking) != hipSuccess) sd.s = nullptr;
+    if (sd.s && (hipEventCreateWithFlags(&sd.fork, hipEventDisableTiming) != hipSuccess ||
+                 hipEventCreateWithFlags(&sd.join, hipEventDisableTiming) != hipSuccess))
+      sd.s = nullptr;
+  }
+  return sd.s ? &sd : nullptr;
+}
+
 struct LayerCall {
   const hero_dims* dims;
   int j, T;
@@ -210,6 +249,8 @@ struct LayerCall {
   // depth-history form of the memory: the pairs and the weights of the j-1 stored ones
   const hero_history* hist = nullptr;
   const float* hw = nullptr;
+  // the second stream (null: every launch on the call's stream)
+  const Side* side = nullptr;
 };
 
 // rho_l = sigma(eta_l); w[i] = prod_{l=i+2}^{j-1} rho_l is the weight of entry i (routed layer
@@ -242,15 +283,31 @@ int run_layer(const LayerCall& c) {
   float* rowstat = reinterpret_cast<float*>(ws + L.rowstat);
 
   const hipStream_t st = c.stream;
-  hipError_t e = timed(HERO_K_ROWSTATS, st, [&] {
+  // work on the second stream starts after everything issued so far on st, and st waits for it
+  const Side* sd = c.side;
+  auto fork = [&]() {
+    hipError_t x = hipEventRecord(sd->fork, st);
+    return x == hipSuccess ? hipStreamWaitEvent(sd->s, sd->fork, 0) : x;
+  };
+  auto join = [&]() {
+    hipError_t x = hipEventRecord(sd->join, sd->s);
+    return x == hipSuccess ? hipStreamWaitEvent(st, sd->join, 0) : x;
+  };
+  // the row statistics (for the router's path vector and the branches' input) and the router's
+  // pre-activation product both read only hbar: side by side
+  const hipStream_t s_rows = sd ? sd->s : st;
+  hipError_t e = sd ? fork() : hipSuccess;
+  if (e != hipSuccess) return HERO_E_LAUNCH;
+  e = timed(HERO_K_ROWSTATS, s_rows, [&] {
     return launch_rowstats(D.dtype, c.hbar, c.j >= 2 ? c.prev1 : nullptr, c.j >= 3 ? c.prev2 : nullptr,
-                           c.ffn->norm_w, T, D.d, c.j, D.eps_norm, rowstat, u, st);
+                           c.ffn->norm_w, T, D.d, c.j, D.eps_norm, rowstat, u, s_rows);
   });
   if (e != hipSuccess) return HERO_E_LAUNCH;
   e = timed(HERO_K_ROUTER_GEMM, st, [&] {
     return launch_router_gemm(D.dtype, c.hbar, c.rt->w_hd, c.rt->ps1, T, D.d, D.d_e, D.d_head, P, st);
   });
   if (e != hipSuccess) return HERO_E_LAUNCH;
+  if (sd && join() != hipSuccess) return HERO_E_LAUNCH;
 
   RouterTailArgs ra{};
   ra.dtype = D.dtype;
@@ -340,6 +397,12 @@ int run_layer(const LayerCall& c) {
   const int n_ad_max = c.rc->mode == HERO_MODE_BUDGET ? n_skip : T;
   void* act = ws + L.act;
   float* part = reinterpret_cast<float*>(ws + L.part);
+  float* part_ad = reinterpret_cast<float*>(ws + L.part_ad);
+  // the two branches write disjoint rows of h_out and read only hbar, u, the gates and the lists:
+  // for a decode batch the adapter's latency-bound launches run beside the FFN's weight stream
+  const bool ovl = sd && T <= kOverlapTokens && n_ffn_max > 0 && n_ad_max > 0;
+  const hipStream_t s_ad = ovl ? sd->s : st;
+  if (ovl && fork() != hipSuccess) return HERO_E_LAUNCH;
   if (n_ffn_max > 0) {
     e = timed(HERO_K_FFN_GATE_UP, st, [&] {
       return launch_ffn_gateup(D.dtype, u, idx_ffn, counts, n_ffn_max, c.ffn->w_gate, c.ffn->w_up,
@@ -353,17 +416,18 @@ int run_layer(const LayerCall& c) {
     if (e != hipSuccess) return HERO_E_LAUNCH;
   }
   if (n_ad_max > 0) {
-    e = timed(HERO_K_ADAPTER_DOWN, st, [&] {
-      return launch_adapter_down(D.dtype, u, idx_ad, counts + 1, n_ad_max, c.ad->w1, part, D.d,
-                                 D.d_r, st);
+    e = timed(HERO_K_ADAPTER_DOWN, s_ad, [&] {
+      return launch_adapter_down(D.dtype, u, idx_ad, counts + 1, n_ad_max, c.ad->w1, part_ad, D.d,
+                                 D.d_r, s_ad);
     });
     if (e != hipSuccess) return HERO_E_LAUNCH;
-    e = timed(HERO_K_ADAPTER_UP, st, [&] {
-      return launch_adapter_up(D.dtype, part, idx_ad, counts + 1, n_ad_max, c.ad->w2, c.hbar, gate,
-                               c.h_out, D.d, D.d_r, st);
+    e = timed(HERO_K_ADAPTER_UP, s_ad, [&] {
+      return launch_adapter_up(D.dtype, part_ad, idx_ad, counts + 1, n_ad_max, c.ad->w2, c.hbar, gate,
+                               c.h_out, D.d, D.d_r, s_ad);
     });
     if (e != hipSuccess) return HERO_E_LAUNCH;
   }
+  if (ovl && join() != hipSuccess) return HERO_E_LAUNCH;
   return HERO_OK;
 }
 
@@ -501,6 +565,7 @@ int hero_routed_layer(const hero_dims* dims, int j, int T, const void* hbar, con
   LayerCall c{dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, state, ffn, router, adapter, eta,
               routing, stats, static_cast<unsigned char*>(workspace), &L,
               static_cast<hipStream_t>(stream)};
+  c.side = side_of_current_device();
   return run_layer(c);
 }
 
@@ -544,7 +609,7 @@ int hero_routed_layer_hist(const hero_dims* dims, int j, int T, const void* hbar
   history_weights(eta, j, hw);
   LayerCall c{dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, nullptr, ffn, router, adapter, eta[j - 1],
               routing, stats, static_cast<unsigned char*>(workspace), &L,
-              static_cast<hipStream_t>(stream), history, hw};
+              static_cast<hipStream_t>(stream), history, hw, side_of_current_device()};
   return run_layer(c);
 }
 
@@ -588,13 +653,14 @@ int routed_stack(const hero_dims* dims, int T, const void* h_in, void* h_out, co
     return jj == 1 ? h_in : ring[(jj - 2) % 3];
   };
   float hw[64];
+  const Side* side = side_of_current_device();
   for (int j = 1; j <= dims->L_R; ++j) {
     void* out = j == dims->L_R ? h_out : const_cast<void*>(ring[(j - 1) % 3]);
     if (history) history_weights(eta, j, hw);
     LayerCall c{dims, j, T, hbar_of(j), j >= 2 ? hbar_of(j - 1) : nullptr,
                 j >= 3 ? hbar_of(j - 2) : nullptr, out, state, &ffn[j - 1], router,
                 &adapter[j - 1], eta[j - 1], routing, stats ? &stats[j - 1] : nullptr, ws, &L,
-                static_cast<hipStream_t>(stream), history, history ? hw : nullptr};
+                static_cast<hipStream_t>(stream), history, history ? hw : nullptr, side};
     if ((st = run_layer(c)) != HERO_OK) return st;
   }
   return HERO_OK;
@@ -885,6 +951,7 @@ int hero_decoder_stack(const hero_dims* dims, const hero_attn_dims* adims, int n
       LayerCall c{dims, j, T, hbar, j >= 2 ? ring[(j - 2) % 3] : nullptr, j >= 3 ? ring[(j - 3) % 3] : nullptr,
                   out, state, &ffn[l], router, &adapter[j - 1], eta[j - 1], routing,
                   stats ? &stats[j - 1] : nullptr, ws, &DL.L, s};
+      c.side = side_of_current_device();
       if ((st = run_layer(c)) != HERO_OK) return st;
     }
     h = out;

@@ -1385,8 +1385,9 @@ int adapter_groups_rows(int K, int n_max) {
 // router pre-activations: 128-row tiles over all 8 waves, K split four ways
 using TileRouter = Tile<128, 256, 2, 4, false>;
 using TileRouterNarrow = Tile<128, 128, 2, 4, false>;
-// few tokens (a decode batch): 64-row tiles of 4 waves, four times the workgroups
-using TileRouterSmall = Tile<64, 128, 1, 4, false>;
+// few tokens (a decode batch): 64-row tiles of 4 waves, four times the workgroups; each streams
+// a quarter of K, with three k-tiles in flight
+using TileRouterSmall = Tile<64, 128, 1, 4, false, 4>;
 // many tokens: 256 x 256 tiles on v_mfma_f32_16x16x32_bf16
 using TileRouterBig = Tile<256, 256, 2, 4, false, 2, 16>;
 
