@@ -984,12 +984,13 @@ def bench_peaks(args):
     sink = torch.zeros(16, dtype=torch.float32, device="cuda:0")
     out = {"metric": "practical ceilings of the board", "n_gpus": 1}
     iters, wgs, reps = 20000, 256, 5
-    for name, rnd in (("mfma_bf16_zeros", False), ("mfma_bf16_random", True)):
-        H.hero_peak_mfma(rnd, iters, wgs, sink, stream)          # warm-up launch
+    for name, rnd, mi16 in (("mfma_bf16_zeros", False, False), ("mfma_bf16_random", True, False),
+                            ("mfma16_bf16_zeros", False, True), ("mfma16_bf16_random", True, True)):
+        H.hero_peak_mfma(rnd, iters, wgs, sink, stream, mi16)    # warm-up launch
         torch.cuda.synchronize()
         a, b = ev.create(2)
         ev.record(a, stream)
-        flop = sum(H.hero_peak_mfma(rnd, iters, wgs, sink, stream) for _ in range(reps))
+        flop = sum(H.hero_peak_mfma(rnd, iters, wgs, sink, stream, mi16) for _ in range(reps))
         ev.record(b, stream)
         ms = ev.elapsed_ms(a, b)
         ev.destroy([a, b])
@@ -1012,6 +1013,32 @@ def bench_peaks(args):
     gbs = 2 * n / (ms * 1e-3) * 1e-9
     out["device_copy_1gib"] = {"gbs_read_plus_write": round(gbs, 1), "frac_of_8000": round(gbs / PEAK_HBM_GBS, 4),
                                "copy_us": round(1000 * ms, 1), "launches": reps}
+    del src, dst
+    torch.cuda.empty_cache()
+
+    # cold HBM reads: each launch reads a region the previous launches did not touch (regions
+    # rotate through more than the 256 MB MALL holds)
+    def cold_reads(region, nreg, visit):
+        buf = torch.empty(nreg * region, dtype=torch.uint8, device="cuda:0").fill_(1)
+        torch.cuda.synchronize()
+        H.hero_peak_read(buf[:region], region, visit, sink, stream)
+        torch.cuda.synchronize()
+        a, b = ev.create(2)
+        ev.record(a, stream)
+        for r in range(2 * nreg):
+            H.hero_peak_read(buf[((r + 1) % nreg) * region:], region, visit, sink, stream)
+        ev.record(b, stream)
+        us = 1000 * ev.elapsed_ms(a, b) / (2 * nreg)
+        ev.destroy([a, b])
+        del buf
+        torch.cuda.empty_cache()
+        return {"gbs": round(region / (us * 1e-6) * 1e-9, 1), "frac_of_8000": round(region / (us * 1e-6) * 1e-9 / PEAK_HBM_GBS, 4),
+                "launch_us": round(us, 1), "bytes": region, "launches": 2 * nreg}
+    out["hbm_read_contiguous"] = cold_reads(1 << 30, 4, 0)
+    # a decode step's weight stream: 256 workgroups x 96 rows of 8 KiB, visit_bytes of each row per step
+    rows_region = 256 * 96 * 8192
+    for vb in (128, 256, 512):
+        out[f"hbm_read_rows_{vb}B_visits"] = cold_reads(rows_region, 8, vb)
     print(json.dumps(out), flush=True)
 
 
@@ -1046,7 +1073,7 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device-to-device copy of this many MiB (HBM counter calibration)")
     ap.add_argument("--peaks", action="store_true",
-                    help="measure the chip's practical ceilings instead (MFMA loop, device copy) and exit")
+                    help="measure the chip's practical ceilings instead (MFMA loops, device copy, cold HBM reads) and exit")
     ap.add_argument("--summarize", metavar="DIR",
                     help="print a summary of rocprofv3 CSV output found under DIR and exit (no GPU)")
     ap.add_argument("--window", type=int, nargs=2, metavar=("SKIP", "COUNT"),

@@ -235,15 +235,31 @@ int hero_kernel_timer(int kernel, void *const *start_events, void *const *stop_e
 /*
  * Measurement hook, not part of the method: the practical bf16 matrix-core rate of the board.
  * Launches `workgroups` workgroups of 8 waves (two per SIMD; 256 = one per compute unit of an
- * MI355X) on hip_stream, each wave running 8 independent v_mfma_f32_32x32x16_bf16 chains for
- * `iters` iterations on register operands: zeros (random_operands = 0, the issue limit) or
- * hashed values in [-0.5, 0.5) (the power-limited rate on realistic data).  *flop (host)
- * receives the floating-point operations the launch performs.  sink (device, >= 1 float) is
- * never written in practice.  Time the launch with the caller's events.
- * Errors: HERO_E_NULL, HERO_E_RANGE (iters outside 1..2^24, workgroups outside 1..65536),
- * HERO_E_LAUNCH.
+ * MI355X) on hip_stream, each wave running 8 independent MFMA chains for `iters` iterations on
+ * register operands.  mode bit 0: hashed operand values in [-0.5, 0.5) (the power-limited rate on
+ * realistic data) instead of zeros (the issue limit); bit 1: v_mfma_f32_16x16x32_bf16 (the FFN
+ * products' instruction) instead of v_mfma_f32_32x32x16_bf16.  *flop (host) receives the
+ * floating-point operations the launch performs.  sink (device, >= 1 float) is never written in
+ * practice.  Time the launch with the caller's events.
+ * Errors: HERO_E_NULL, HERO_E_RANGE (mode outside 0..3, iters outside 1..2^24, workgroups outside
+ * 1..65536), HERO_E_LAUNCH.
  */
-int hero_peak_mfma(int random_operands, int iters, int workgroups, float *sink, void *hip_stream, double *flop);
+int hero_peak_mfma(int mode, int iters, int workgroups, float *sink, void *hip_stream, double *flop);
+
+/*
+ * Measurement hook, not part of the method: HBM read rates by access pattern, reading `bytes` of
+ * src (device, 16-byte aligned; its contents are irrelevant) once on hip_stream.
+ * visit_bytes = 0: contiguous, plain non-temporal 16-byte loads into registers (256 workgroups of
+ * 256 threads, eight loads in flight per lane, grid-stride; bytes a multiple of 16).
+ * visit_bytes = 128, 256 or 512: the weight stream of a decode step: src is a bf16 matrix of 8 KiB
+ * rows (d = 4096), read by bytes / (96 * 8 KiB) workgroups (bytes a multiple of that, at most
+ * 65536 of them) of four waves, each taking 96 rows and visit_bytes of every row per step through
+ * LDS-DMA (a 64-deep k-tile of bf16 is 128 bytes a row).  sink (device, >= 1 float) is never
+ * written in practice.  Time the launch with the caller's events; use a region that the previous
+ * launches did not touch to measure cold reads (the 256 MB MALL keeps recent lines).
+ * Errors: HERO_E_NULL, HERO_E_ALIGN, HERO_E_DIM (bytes), HERO_E_RANGE (visit_bytes), HERO_E_LAUNCH.
+ */
+int hero_peak_read(const void *src, size_t bytes, int visit_bytes, float *sink, void *hip_stream);
 
 /* Static string for a status code (host). */
 const char *hero_status_string(int status);

@@ -41,8 +41,9 @@ struct Layout {
       total;
 };
 
-// At most this many tokens (a decode batch) the adapter branch runs beside the FFN branch, on a
-// second stream, with a partial-sum region of its own.
+// At most this many tokens (a decode batch) the row statistics run beside the router product and
+// the adapter branch beside the FFN branch, on a second stream (the adapter with a partial-sum
+// region of its own).
 constexpr int kOverlapTokens = 256;
 
 Layout layout_of(const hero_dims& d, int T, bool stack) {
@@ -294,9 +295,11 @@ int run_layer(const LayerCall& c) {
     return x == hipSuccess ? hipStreamWaitEvent(st, sd->join, 0) : x;
   };
   // the row statistics (for the router's path vector and the branches' input) and the router's
-  // pre-activation product both read only hbar: side by side
-  const hipStream_t s_rows = sd ? sd->s : st;
-  hipError_t e = sd ? fork() : hipSuccess;
+  // pre-activation product both read only hbar: side by side for a decode batch (with many
+  // tokens the product fills every CU and the statistics pass, starved, only stretches)
+  const bool ovl_rows = sd && T <= kOverlapTokens;
+  const hipStream_t s_rows = ovl_rows ? sd->s : st;
+  hipError_t e = ovl_rows ? fork() : hipSuccess;
   if (e != hipSuccess) return HERO_E_LAUNCH;
   e = timed(HERO_K_ROWSTATS, s_rows, [&] {
     return launch_rowstats(D.dtype, c.hbar, c.j >= 2 ? c.prev1 : nullptr, c.j >= 3 ? c.prev2 : nullptr,
@@ -307,7 +310,7 @@ int run_layer(const LayerCall& c) {
     return launch_router_gemm(D.dtype, c.hbar, c.rt->w_hd, c.rt->ps1, T, D.d, D.d_e, D.d_head, P, st);
   });
   if (e != hipSuccess) return HERO_E_LAUNCH;
-  if (sd && join() != hipSuccess) return HERO_E_LAUNCH;
+  if (ovl_rows && join() != hipSuccess) return HERO_E_LAUNCH;
 
   RouterTailArgs ra{};
   ra.dtype = D.dtype;

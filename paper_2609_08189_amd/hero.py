@@ -199,6 +199,8 @@ def lib() -> ctypes.CDLL:
                                            _vp, _vp, P(hero_router_grads), _vp, _vp, ctypes.c_size_t, _vp]
         L.hero_peak_mfma.restype = ctypes.c_int
         L.hero_peak_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, P(ctypes.c_double)]
+        L.hero_peak_read.restype = ctypes.c_int
+        L.hero_peak_read.argtypes = [_vp, ctypes.c_size_t, ctypes.c_int, _vp, _vp]
         _lib = L
     return _lib
 
@@ -231,12 +233,17 @@ def hero_abi_version() -> int:
     return lib().hero_abi_version()
 
 
-def hero_peak_mfma(random_operands: bool, iters: int, workgroups: int, sink, stream) -> float:
+def hero_peak_mfma(random_operands: bool, iters: int, workgroups: int, sink, stream, mi16: bool = False) -> float:
     """Launch the matrix-core rate probe on `stream`; returns the FLOPs the launch performs."""
     flop = ctypes.c_double()
-    check(lib().hero_peak_mfma(int(bool(random_operands)), iters, workgroups, ptr(sink), stream,
-                               ctypes.byref(flop)), "hero_peak_mfma")
+    mode = int(bool(random_operands)) | (2 if mi16 else 0)
+    check(lib().hero_peak_mfma(mode, iters, workgroups, ptr(sink), stream, ctypes.byref(flop)), "hero_peak_mfma")
     return flop.value
+
+
+def hero_peak_read(src, nbytes: int, visit_bytes: int, sink, stream) -> None:
+    """Launch the HBM read probe over nbytes of src on `stream` (0: contiguous; 128/256/512: row visits)."""
+    check(lib().hero_peak_read(ptr(src), nbytes, visit_bytes, ptr(sink), stream), "hero_peak_read")
 
 
 def hero_kernel_timer(kernel: int, start_events: Sequence[int], stop_events: Sequence[int]) -> None:

@@ -439,3 +439,19 @@ def test_noalloc_rejects_a_call_beyond_its_scratch_before_any_launch():
     assert call(4096, None) == H.HERO_E_NULL
     assert call(0, FAKE + (1 << 30)) == H.HERO_E_DIM
     assert H.hero_status_string(H.HERO_E_SCRATCH) != "unknown status"
+
+
+def test_peak_hooks_reject_bad_arguments_before_any_launch():
+    """The measurement hooks check their arguments on the host (fake pointers: nothing is launched)."""
+    lib = H.lib()
+    sink = ctypes.c_void_p(FAKE)
+    flop = ctypes.c_double()
+    assert lib.hero_peak_mfma(4, 10, 256, sink, None, ctypes.byref(flop)) == H.HERO_E_RANGE
+    assert lib.hero_peak_mfma(3, 0, 256, sink, None, ctypes.byref(flop)) == H.HERO_E_RANGE
+    assert lib.hero_peak_mfma(0, 10, 256, None, None, ctypes.byref(flop)) == H.HERO_E_NULL
+    rows = 96 * 8192
+    assert lib.hero_peak_read(None, rows, 128, sink, None) == H.HERO_E_NULL
+    assert lib.hero_peak_read(ctypes.c_void_p(FAKE + 8), rows, 128, sink, None) == H.HERO_E_ALIGN
+    assert lib.hero_peak_read(ctypes.c_void_p(FAKE), rows + 8192, 128, sink, None) == H.HERO_E_DIM
+    assert lib.hero_peak_read(ctypes.c_void_p(FAKE), rows, 64, sink, None) == H.HERO_E_RANGE
+    assert lib.hero_peak_read(ctypes.c_void_p(FAKE), 24, 0, sink, None) == H.HERO_E_DIM
