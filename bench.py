@@ -151,6 +151,8 @@ def cpu_baseline(prob, gpu_stats, j, target_s=12.0, max_tokens=None):
 
 
 # committed rocprofv3 FETCH_SIZE / WRITE_SIZE summaries, per workload
+# a call of at most this many tokens is a decode step: timed as HIP-graph replays by default
+DECODE_TOKENS = 256
 COUNTERS_MD = {
     "llama31_8b_layer": os.path.join(ROOT, "profiles", "routed_layer_llama31_8b_hbm_counters.md"),
     "llama31_8b_stack": os.path.join(ROOT, "profiles", "routed_stack_llama31_8b_hbm_counters.md"),
@@ -1055,9 +1057,12 @@ def main():
                     help="storage of the router memory S between layers")
     ap.add_argument("--budget", type=float, default=None,
                     help="skip budget in place of the workload's own (budget-mode workloads)")
-    ap.add_argument("--graph", action="store_true",
+    ap.add_argument("--graph", action="store_true", default=None,
                     help="time replays of the call captured once as a HIP graph (kernel times then come "
-                         "from the instrumented pass)")
+                         "from the instrumented pass); the default for decode-sized calls (at most 256 tokens), "
+                         "whose launch gaps are a visible share of the step")
+    ap.add_argument("--eager", action="store_true",
+                    help="time eager launches even for a decode-sized call")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward of the routed block (training side) instead of the forward")
     ap.add_argument("--router-backward", action="store_true",
@@ -1095,8 +1100,10 @@ def main():
     from paper_2609_08189_amd.device import DeviceProblem
 
     w = synth.WORKLOADS[args.workload]
+    if args.graph is None:
+        args.graph = w.T <= DECODE_TOKENS and not args.eager and w.n_layers == 0
     default_line = (args.budget is None and not args.ablation and args.state == "f32"
-                    and args.memory == "matrix" and not args.graph)
+                    and args.memory == "matrix" and (not args.graph or w.T <= DECODE_TOKENS))
     if args.budget is not None:
         if w.mode != "budget" or not 0.0 <= args.budget <= 1.0:
             sys.exit("--budget needs a budget-mode workload and a fraction in [0, 1]")
