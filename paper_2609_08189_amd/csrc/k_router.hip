@@ -23,6 +23,8 @@
 // The memory kernel moves 2 * 4 * (d_m^2 + d_m) bytes of state per token (2 * (2 d_m^2 + 4 d_m)
 // with S stored in bf16) and is the HBM-bound part; keeping it free of the matrix-vector work lets many workgroups per
 // CU keep HBM busy.  All arithmetic is fp32.
+#include <algorithm>
+
 #include "hero_device.h"
 #include "hero_kernels.h"
 
@@ -547,6 +549,9 @@ __global__ __launch_bounds__(NTP, WPE) void router_pre_mfma(RouterTailArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int t0 = blockIdx.x * MT;
+  // column groups (few tokens): workgroup y of CS takes the output tiles ct = y + CS i of the
+  // s-projections; every group forms s itself
+  const int cs = blockIdx.y, CS = gridDim.y;
   const int nvalid = min(MT, a.T - t0);
   const int j = a.j;
   const int d_e = a.d_e, d_head = a.d_head, NP = d_e + d_head, DM = a.d_m, d_s = a.d_s;
@@ -596,7 +601,7 @@ __global__ __launch_bounds__(NTP, WPE) void router_pre_mfma(RouterTailArgs a) {
   bf16x8 b2[PF][KSS];
 #pragma unroll
   for (int c = 0; c < PF; ++c) {
-    const int ct = wave + NWP * c;
+    const int ct = cs + CS * (wave + NWP * c);
     if (ct < nct) {
       const SProj p = proj(ct);
 #pragma unroll
@@ -714,7 +719,7 @@ __global__ __launch_bounds__(NTP, WPE) void router_pre_mfma(RouterTailArgs a) {
     for (int q = 0; q < 8; ++q) x[q] = k0 + q < d_s ? s[i][k0 + q] : 0.f;
     split8(x, as[0][st][i + 16 * g], as[1][st][i + 16 * g]);
   }
-  if (tid < nvalid) {
+  if (tid < nvalid && cs == 0) {
     float b = 0.f;
     for (int q = 0; q < d_head / 16; ++q) b += bpart[tid][q];
     a.bvec[t0 + tid] = b;
@@ -736,8 +741,8 @@ __global__ __launch_bounds__(NTP, WPE) void router_pre_mfma(RouterTailArgs a) {
   };
 #pragma unroll
   for (int c = 0; c < PF; ++c)
-    if (wave + NWP * c < nct) finish(wave + NWP * c, b2[c]);
-  for (int ct = wave + NWP * PF; ct < nct; ct += NWP) {
+    if (cs + CS * (wave + NWP * c) < nct) finish(cs + CS * (wave + NWP * c), b2[c]);
+  for (int ct = cs + CS * (wave + NWP * PF); ct < nct; ct += CS * NWP) {
     const SProj p = proj(ct);
     bf16x8 bw[KSS];
 #pragma unroll
@@ -1003,6 +1008,10 @@ hipError_t launch_pre_post(const RouterTailArgs& a, bool post, hipStream_t s) {
       // many rounds of workgroups (more than two per CU) with an unsplit P: two resident
       // workgroups per CU, weight fragments loaded as they are needed
       const bool many = grid.x > 2u * kCUsRouter && a.p_splits == 1;
+      // few token groups: the s-projections' output tiles split over up to 16 column groups per
+      // token group, so that the launch covers the CUs (decode, 256 tokens: 16 x 16 workgroups)
+      const int nct = 4 * (a.d_m / 16) + a.d_head / 16;
+      grid.y = static_cast<unsigned>(std::max(1, std::min({16, static_cast<int>(kCUsRouter / grid.x), nct})));
       switch ((a.d_s + 31) / 32) {
         case 1: many ? router_pre_mfma<1, 4, 1, 1><<<grid, NTP, 0, s>>>(a) : router_pre_mfma<1><<<grid, NTP, 0, s>>>(a); break;
         case 2: many ? router_pre_mfma<2, 4, 1, 1><<<grid, NTP, 0, s>>>(a) : router_pre_mfma<2><<<grid, NTP, 0, s>>>(a); break;
