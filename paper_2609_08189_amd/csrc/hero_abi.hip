@@ -1241,7 +1241,7 @@ int hero_skip_penalty(int L_R, int batch, int seq, const float* gates, float alp
 namespace {
 
 struct RouterBwdLayout {
-  size_t P, dP, dPT, rowcoef, rho_part, vec, hbT, wT;
+  size_t P, dP, dPT, rowcoef, rho_part, vec, tok, hbT, wT;
   // bf16: the big products on the GEMM core, dP split into bf16 hi + lo, K padded to kp
   size_t dPT_hi, dPT_lo, dP_hi, dP_lo, hbT16, wT16;
   size_t tn_part, tn_floats;   // K-split partials of the small weight-gradient products
@@ -1264,6 +1264,7 @@ RouterBwdLayout router_bwd_layout_of(const hero_dims& d, int T) {
   L.rowcoef = take(t * 8 * 4);
   L.rho_part = take(t * 4);
   L.vec = take(hero::router_bwd_vector_floats(d.d_m, d.d_s, d.d_h, d.d_a, d.d_e, d.d_p, d.d_head) * t * 4);
+  L.tok = take(hero::router_bwd_token_floats(d.d_m, d.d_s, d.d_p, d.d_e + d.d_head) * t * 4);
   const bool mfma = d.dtype == HERO_BF16;
   L.kp = (T + 63) / 64 * 64;
   const size_t kp = static_cast<size_t>(L.kp);
@@ -1432,6 +1433,23 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
   a.dZAT = rows(D.d_a);
   a.dZHT = rows(D.d_h);
   a.SHT = rows(D.d_e);
+  float* tk = reinterpret_cast<float*>(ws + L.tok);
+  auto per_token = [&](int n) {
+    float* at = tk;
+    tk += static_cast<size_t>(n) * T;
+    return at;
+  };
+  a.RS = per_token(4);
+  a.QKVU = per_token(4 * D.d_m);
+  a.PPRE = per_token(D.d_p);
+  a.Cv = per_token(D.d_m);
+  a.DEN = per_token(1);
+  a.PS = per_token(1);
+  a.DSP = per_token(D.d_s);
+  a.DNUM = per_token(D.d_m);
+  a.DDEN = per_token(1);
+  a.DF = per_token(3 * D.d_m);
+  a.PSUM = per_token(NP);
   a.dhbar = dhbar;
   a.dhbar1 = dhbar_prev1;
   a.dhbar2 = dhbar_prev2;

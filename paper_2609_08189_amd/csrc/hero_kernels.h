@@ -254,9 +254,16 @@ struct RouterBwdArgs {
   float *XT, *dQT, *dKT, *dVT, *dU1T, *dU2T, *dPAT, *SAT, *DA, *DB, *SBT, *dPPT, *SPT, *XPT, *dZAT, *dZHT, *SHT;
   float *dhbar, *dhbar1, *dhbar2;            // [T][d] fp32, accumulated
   float* deta;                               // [1]
+  // per-token intermediates handed from one token pass to the next (token-major scratch):
+  // row statistics (ir, |delta_j|, |delta_{j-1}|, delta_j . delta_{j-1}), q k v W_n s, the path
+  // encoder's pre-activation, c, the read's normaliser, p_j, dL/ds so far, dL/dnum, dL/dden,
+  // [dL/dphi(k); dL/dphi(q); dL/dv], P with its K slices summed
+  float *RS, *QKVU, *PPRE, *Cv, *DEN, *PS, *DSP, *DNUM, *DDEN, *DF, *PSUM;
 };
 // rows of the token-contiguous operands above, per token
 size_t router_bwd_vector_floats(int d_m, int d_s, int d_h, int d_a, int d_e, int d_p, int d_head);
+// floats of the token passes' intermediates, per token
+size_t router_bwd_token_floats(int d_m, int d_s, int d_p, int np);
 hipError_t launch_router_bwd_token(const RouterBwdArgs& a, hipStream_t s);
 // the RMSNorm / transition terms of dL/dhbar, then dL/deta
 hipError_t launch_router_bwd_rows(const RouterBwdArgs& a, hipStream_t s);

@@ -3,7 +3,7 @@
 // through the local head, the history head, the history dissimilarity, the memory read and
 // write, the projections q, k, v, the router state, the path encoder and the hidden encoder.
 //
-// router_bwd_token (one workgroup per token, fp32):
+// The token work (fp32 arithmetic; five passes, described where they are defined below):
 //   forward recompute of the layer's router from P = hbar [W_hd; psi_1]^T (recomputed on the
 //   GEMM core) and the state entering the layer; then the reverse:
 //     dL/da = dL/dlogit + (dL/dp_j + dL/dm_j m_{j-1}) p (1 - p) / T_hist,  dL/db = dL/dlogit,
@@ -59,344 +59,875 @@ __device__ __forceinline__ float ldw(const W* w, unsigned i) {
   return ldf(reinterpret_cast<const W*>(reinterpret_cast<const char*>(w) + i * static_cast<unsigned>(sizeof(W))));
 }
 
-// y[o] = sum_k w[o][k] x[k] for o < O: G lanes per row (G = 16, or 8 for I <= 32), so one wave
-// works on 64 / G rows at once and each row's reduction takes log2(G) shuffles
-template <typename W, int G>
-__device__ void mv_rows_g(const W* w, int ld, int O, int I, const float* x, float* y) {
-  constexpr int R = kWave / G;
-  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave, gl = lane & (G - 1);
-  for (int o0 = wv * R; o0 < O; o0 += RB_NW * R) {   // uniform per wave
-    const int o = o0 + lane / G;
-    float acc = 0.0f;
-    if (o < O) {
-      const unsigned r = static_cast<unsigned>(o) * ld;
-#pragma unroll 4
-      for (int k = gl; k < I; k += G) acc = fmaf(ldw(w, r + k), x[k], acc);
+// ---------------------------------------------------------------------------
+// The token work in six passes.  The three on the router's small products take RB_TB tokens per
+// workgroup, so that every weight element loaded from L2 serves RB_TB tokens (one token per
+// workgroup chained ~100 dependent mat-vec phases, each waiting on its weights); the others stream
+// per-token rows: the residual rows for the row statistics, and one token's d_m x d_m state per
+// workgroup, as the forward's memory pass does.
+//   stats (a wave per token): inv_rms(hbar_j), |delta_j|, |delta_{j-1}|, delta_j . delta_{j-1}, and
+//      P's K slices summed;
+//   F1 (batched): the P partials of the hidden encoder, the path encoder, s, and q, k, v, W_n s;
+//   M1 (per token): the memory read c = phi(q)^T S_{j-1} / (phi(q)^T zeta_{j-1} + eps);
+//   F2 (batched): W_c c, nu, the history head, p, and the reverse from dL/dlogit through the
+//      heads, f_theta's first layer, nu and the read's normaliser: dL/dc as dL/dnum, dL/dden;
+//   M2 (per token): one pass over S_{j-1} and the carried dL/dS_j (dL/dphi(k), dL/dphi(q),
+//      dL/dv, dL/drho, dL/dS_{j-1} in place), then zeta;
+//   F3 (batched): the projections, path and hidden encoders in reverse, the row coefficients.
+// Per-token intermediates go through the scratch named in RouterBwdArgs (token-major).  Loops over
+// (token, row) pairs run token-fastest where they write the token-contiguous operands and
+// row-fastest where they read or write token-major rows, so that both sides coalesce.
+// ---------------------------------------------------------------------------
+constexpr int RB_TB = 16;              // tokens per workgroup of the batched passes
+constexpr int RB_BT = 512;             // threads of the batched passes
+constexpr int RB_BW = RB_BT / kWave;   // their waves
+constexpr int RB_RED = RB_BW * RB_TB * 64;   // floats of bmv_cols' partial sums
+constexpr int RB_PF = 8;                     // weight loads in flight per lane in the batched mat-vecs
+
+// The batched mat-vecs run on the fp32 matrix cores (v_mfma_f32_16x16x4f32: exact fp32 products,
+// so bf16 weights and fp32 activations keep the precision of scalar FMAs).  A product tile is the
+// RB_TB = 16 tokens times 16 outputs; lane l supplies operand row l % 16 at k slot l / 16, and
+// holds the result rows 4 (l / 16) + q, q < 4, of column l % 16.  Every wave of the workgroup calls
+// these; tiles are dealt to the waves round-robin.  Weights come in batches of RB_PF steps, the
+// next batch's loads issued before the current batch's products (across tiles too).  A result
+// column depends on its own weight column alone and a token row on its own operand row alone, so
+// out-of-range outputs read a clamped in-range weight address and are never stored; out-of-range k
+// (or rows o in the transposed form) enter the operand as zeros, since the LDS there may hold
+// anything; token rows b >= nb are computed from whatever the LDS holds there and never stored.
+// the wave's index in the workgroup as a scalar (threadIdx.x / 64 is uniform per wave, but the
+// compiler treats it as varying by lane, which turns every loop over tiles into divergent code)
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave); }
+__device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+// w[i .. i + 3] (i a multiple of 4, the row pitch too) as loaded (raw4), and in fp32 (cvt4).  The
+// batches hold raw words and convert at their products: converting at the load would make the
+// compiler wait for the next batch's loads before the current batch's products.
+template <typename W>
+struct Raw4;
+template <>
+struct Raw4<bf16_t> {
+  using type = uint2;
+};
+template <>
+struct Raw4<float> {
+  using type = f32x4;
+};
+__device__ __forceinline__ uint2 raw4(const bf16_t* w, unsigned i) {
+  return *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(w) + i * 2u);
+}
+__device__ __forceinline__ f32x4 raw4(const float* w, unsigned i) {
+  return *reinterpret_cast<const f32x4*>(reinterpret_cast<const char*>(w) + i * 4u);
+}
+__device__ __forceinline__ f32x4 cvt4(uint2 u) {
+  return f32x4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+               __uint_as_float(u.y & 0xffff0000u)};
+}
+__device__ __forceinline__ f32x4 cvt4(f32x4 v) { return v; }
+
+// Up to four weight matrices of one row pitch stacked by rows: stack row o is row o - m om of
+// matrix m (om rows each, a multiple of 16 when there are several; one matrix: om = its rows)
+template <typename W>
+struct Mats {
+  const W *w0, *w1, *w2, *w3;
+  int om, ld;
+  __device__ __forceinline__ int mat(int o) const { return (o >= om) + (o >= 2 * om) + (o >= 3 * om); }
+  __device__ __forceinline__ const W* base(int m) const { return m == 0 ? w0 : m == 1 ? w1 : m == 2 ? w2 : w3; }
+};
+template <typename W>
+__device__ __forceinline__ Mats<W> mats1(const void* w, int rows, int ld) {
+  return Mats<W>{static_cast<const W*>(w), nullptr, nullptr, nullptr, rows, ld};
+}
+
+// lane's four weights of stack row ot 16 + r (clamped to the last row) from column k, as loaded
+template <typename W>
+__device__ __forceinline__ typename Raw4<W>::type rows_w4(const Mats<W>& M, int O, int ot, int r, int k) {
+  const int m = M.mat(ot * 16), o = min(ot * 16 + r, O - 1);   // a tile lies in one matrix
+  return raw4(M.base(m), static_cast<unsigned>(o - m * M.om) * M.ld + k);
+}
+// the k >= kb steps of tile ot with scalar loads (the ragged end, or every k when the pitch is not a
+// multiple of 4)
+template <typename W>
+__device__ __forceinline__ f32x4 rows_tail(const Mats<W>& M, int O, int ot, int I, int kb, const float* x, int ldx,
+                                           int r, int g, f32x4 acc) {
+  const int m = M.mat(ot * 16), o = min(ot * 16 + r, O - 1);
+  const W* wb = M.base(m);
+  const unsigned wr = static_cast<unsigned>(o - m * M.om) * M.ld;
+  for (int k0 = kb; k0 < I; k0 += 16) {
+    const int kk = k0 + 4 * g;
+    float wa[4], xa[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool kv = kk + i < I;
+      const int kc = kv ? kk + i : I - 1;
+      const float wl = ldw(wb, wr + kc), xl = x[r * ldx + kc];
+      wa[i] = kv ? wl : 0.0f;
+      xa[i] = kv ? xl : 0.0f;
     }
 #pragma unroll
-    for (int off = G / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, kWave);
-    if (gl == 0 && o < O) y[o] = acc;
+    for (int i = 0; i < 4; ++i) acc = mfma4(xa[i], wa[i], acc);
   }
-}
-template <typename W>
-__device__ void mv_rows(const W* w, int ld, int O, int I, const float* x, float* y) {
-  if (I > 32)
-    mv_rows_g<W, 16>(w, ld, O, I, x, y);
-  else
-    mv_rows_g<W, 8>(w, ld, O, I, x, y);
-}
-
-// x[k] (+)= sum_o w[o][k] y[o] for k < I (a thread per column; sixteen loads issued before their
-// FMAs, which add in ascending o).  For I <= RB_NT / 2 the rows are split into RB_NT / I' parts
-// (I' = I rounded up to a power of two) whose partial sums meet in part, added in part order.
-// Every thread calls it; with the split it ends on a barrier.
-template <typename W>
-__device__ float mv_cols_range(const W* w, int ld, int o_begin, int o_end, int k, const float* y, float acc) {
-  int o = o_begin;
-  for (; o + 16 <= o_end; o += 16) {
-    float wv[16];
-#pragma unroll
-    for (int u = 0; u < 16; ++u) wv[u] = ldw(w, static_cast<unsigned>(o + u) * ld + k);
-#pragma unroll
-    for (int u = 0; u < 16; ++u) acc = fmaf(wv[u], y[o + u], acc);
-  }
-  for (; o < o_end; ++o) acc = fmaf(ldw(w, static_cast<unsigned>(o) * ld + k), y[o], acc);
   return acc;
 }
-template <typename W>
-__device__ void mv_cols(const W* w, int ld, int O, int I, const float* y, float* x, bool accumulate,
-                        float* part) {
-  int Ip = 1;
-  while (Ip < I) Ip <<= 1;
-  if (2 * Ip > RB_NT) {
-    for (int k = threadIdx.x; k < I; k += RB_NT) x[k] = mv_cols_range(w, ld, 0, O, k, y, accumulate ? x[k] : 0.0f);
-    return;
-  }
-  const int np = RB_NT / Ip, oc = (O + np - 1) / np;
-  const int k = threadIdx.x % Ip, q = threadIdx.x / Ip;
-  if (k < I) part[q * Ip + k] = mv_cols_range(w, ld, min(O, q * oc), min(O, (q + 1) * oc), k, y, 0.0f);
-  __syncthreads();
-  if (threadIdx.x < I) {
-    float acc = accumulate ? x[threadIdx.x] : 0.0f;
-    for (int u = 0; u < np; ++u) acc += part[u * Ip + threadIdx.x];
-    x[threadIdx.x] = acc;
-  }
-  __syncthreads();
+__device__ __forceinline__ void rows_store(f32x4 acc, int O, int ot, int r, int g, float* y, int ldy, int nb) {
+  const int o = ot * 16 + r;
+  if (o < O)
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (4 * g + q < nb) y[(4 * g + q) * ldy + o] = acc[q];
 }
 
+// y[b][o] = sum_k W[o][k] x[b][k] for b < nb, o < O over a stack W (x in LDS, [RB_TB][ldx]; y in
+// LDS or global).  With a row pitch that is a multiple of 4, each lane loads its four k of a 16-k
+// step at once (slot g takes k0 + 4 g + i in its i-th product); two accumulators alternate.
+template <typename W>
+__device__ __forceinline__ void bmv_rows(const Mats<W>& M, int O, int I, const float* x, int ldx, float* y, int ldy,
+                                         int nb) {
+  const int lane = threadIdx.x & (kWave - 1), r = lane & 15, g = lane >> 4, wv = wave_id();
+  const int ntile = (O + 15) / 16;
+  const int ntw = wv < ntile ? (ntile - 1 - wv) / RB_BW + 1 : 0;   // this wave's tiles (uniform)
+  const int nst = (M.ld & 3) == 0 ? I / 16 : 0, I16 = 16 * nst;
+  const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (nst == 0) {
+    for (int ti = 0; ti < ntw; ++ti) {
+      const int ot = wv + ti * RB_BW;
+      rows_store(rows_tail(M, O, ot, I, 0, x, ldx, r, g, zero), O, ot, r, g, y, ldy, nb);
+    }
+    return;
+  }
+  // the wave's batches in sequence: batch q is batch q % nbt of its tile q / nbt
+  const int nbt = (nst + RB_PF - 1) / RB_PF, total = ntw * nbt;
+  const float* xr = x + r * ldx + 4 * g;
+  typename Raw4<W>::type cur[RB_PF];
+  if (total > 0)
+#pragma unroll
+    for (int u = 0; u < RB_PF; ++u) cur[u] = rows_w4(M, O, wv, r, 16 * min(u, nst - 1) + 4 * g);
+  f32x4 acc0 = zero, acc1 = zero;
+  for (int q = 0; q < total; ++q) {
+    const int ti = q / nbt, c = q - ti * nbt, ot = wv + ti * RB_BW;
+    typename Raw4<W>::type nxt[RB_PF];
+    if (q + 1 < total) {   // uniform
+      const int t1 = (q + 1) / nbt, c1 = q + 1 - t1 * nbt;
+#pragma unroll
+      for (int u = 0; u < RB_PF; ++u)
+        nxt[u] = rows_w4(M, O, wv + t1 * RB_BW, r, 16 * min(c1 * RB_PF + u, nst - 1) + 4 * g);
+    }
+#pragma unroll
+    for (int u = 0; u < RB_PF; ++u) {
+      const int st = c * RB_PF + u;
+      if (st < nst) {   // uniform
+        const float* xk = xr + 16 * st;
+        const f32x4 wv = cvt4(cur[u]);
+        acc0 = mfma4(xk[0], wv[0], acc0);
+        acc1 = mfma4(xk[1], wv[1], acc1);
+        acc0 = mfma4(xk[2], wv[2], acc0);
+        acc1 = mfma4(xk[3], wv[3], acc1);
+      }
+    }
+    if (c == nbt - 1) {   // the tile's last batch
+      rows_store(rows_tail(M, O, ot, I, I16, x, ldx, r, g, acc0 + acc1), O, ot, r, g, y, ldy, nb);
+      acc0 = acc1 = zero;
+    }
+#pragma unroll
+    for (int u = 0; u < RB_PF; ++u) cur[u] = nxt[u];
+  }
+}
+
+// One transposed product x[b][k] (+)= sum_o W[o][k] y[b][o], b < nb, k < I, over a stack W of O rows
+// (y and x in LDS).  With a row pitch that is a multiple of 4 (and at least I rounded up to 4), a
+// tile is 64 columns in four accumulators (lane r of accumulator i: column 64 kt + 4 r + i, so each
+// lane loads four adjacent weights per row) and each product takes four rows o (slot g: o0 + g);
+// otherwise a tile is 16 columns with scalar loads.  When there are fewer tiles than waves, the o
+// range is cut into parts whose partial sums meet in red ([parts][RB_TB][tiles x 64] floats) and
+// are added in part order.
+template <typename W>
+struct Cols {
+  Mats<W> M;
+  int O, I;
+  const float* y;
+  int ldy;
+  float* x;
+  int ldx;
+  bool acc;
+};
+struct ColsPlan {
+  int ntile, parts, ocnt, wid, items;
+  bool vec;
+};
+__device__ __forceinline__ ColsPlan cols_plan(int O, int I, int ld, int waves) {
+  ColsPlan p;
+  p.vec = (ld & 3) == 0;
+  p.ntile = p.vec ? (I + 63) / 64 : (I + 15) / 16;
+  p.parts = (!p.vec || p.ntile >= waves) ? 1 : waves / p.ntile;   // parts x ntile <= waves
+  p.ocnt = ((O + p.parts - 1) / p.parts + 3) & ~3;                  // rows per part, a multiple of 4
+  p.wid = p.ntile * 64;
+  p.items = p.ntile * p.parts;
+  return p;
+}
+template <typename W>
+__device__ __forceinline__ void cols_item(const Cols<W>& J, const ColsPlan& P, int it, int nb, float* red) {
+  const int lane = threadIdx.x & (kWave - 1), r = lane & 15, g = lane >> 4;
+  const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+  const int kt = it % P.ntile, pt = it / P.ntile;
+  const float* yr = J.y + r * J.ldy;
+  if (!P.vec) {
+    const int k = kt * 16 + r;
+    const bool kv = k < J.I;
+    const int kc = kv ? k : J.I - 1;
+    f32x4 acc = zero;
+    for (int o0 = 0; o0 < J.O; o0 += 16) {
+      const int oo = o0 + 4 * g;
+      float wa[4], ya[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ov = oo + i < J.O;
+        const int oc = ov ? oo + i : J.O - 1, m = J.M.mat(oc);
+        wa[i] = ldw(J.M.base(m), static_cast<unsigned>(oc - m * J.M.om) * J.M.ld + kc);
+        const float yl = yr[oc];
+        ya[i] = ov ? yl : 0.0f;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc = mfma4(ya[i], wa[i], acc);
+    }
+    if (kv)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (4 * g + q < nb) {
+          float* xe = J.x + (4 * g + q) * J.ldx + k;
+          *xe = J.acc ? *xe + acc[q] : acc[q];
+        }
+    return;
+  }
+  const int ob = min(J.O, pt * P.ocnt), oe = min(J.O, ob + P.ocnt);
+  const int kc = kt * 64 + 4 * r;
+  const unsigned kl = static_cast<unsigned>(kc < J.I ? kc : (J.I - 1) & ~3);   // columns >= I: any in-row chunk
+  const int nst = (oe - ob + 3) / 4;   // steps of four rows (of one matrix: om is a multiple of 4)
+  f32x4 acc[4] = {zero, zero, zero, zero};
+  if (nst > 0) {
+    typename Raw4<W>::type bc[RB_PF];
+    float ac[RB_PF];
+#pragma unroll
+    for (int u = 0; u < RB_PF; ++u) {
+      const int so = ob + 4 * min(u, nst - 1), m = J.M.mat(so), o = so + g, oc = min(o, oe - 1);
+      bc[u] = raw4(J.M.base(m), static_cast<unsigned>(oc - m * J.M.om) * J.M.ld + kl);
+      const float yl = yr[oc];
+      ac[u] = o < oe ? yl : 0.0f;
+    }
+    for (int s0 = 0; s0 < nst; s0 += RB_PF) {
+      typename Raw4<W>::type bn[RB_PF];
+      float an[RB_PF];
+      if (s0 + RB_PF < nst) {   // uniform
+#pragma unroll
+        for (int u = 0; u < RB_PF; ++u) {
+          const int so = ob + 4 * min(s0 + RB_PF + u, nst - 1), m = J.M.mat(so), o = so + g, oc = min(o, oe - 1);
+          bn[u] = raw4(J.M.base(m), static_cast<unsigned>(oc - m * J.M.om) * J.M.ld + kl);
+          const float yl = yr[oc];
+          an[u] = o < oe ? yl : 0.0f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < RB_PF; ++u)
+        if (s0 + u < nst) {   // uniform
+          const f32x4 bv = cvt4(bc[u]);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[i] = mfma4(ac[u], bv[i], acc[i]);
+        }
+#pragma unroll
+      for (int u = 0; u < RB_PF; ++u) {
+        bc[u] = bn[u];
+        ac[u] = an[u];
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int b = 4 * g + q;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (P.parts > 1) {
+        red[(pt * RB_TB + b) * P.wid + kc + i] = acc[i][q];
+      } else if (b < nb && kc + i < J.I) {
+        float* xe = J.x + b * J.ldx + kc + i;
+        *xe = J.acc ? *xe + acc[i][q] : acc[i][q];
+      }
+    }
+  }
+}
+template <typename W>
+__device__ __forceinline__ void cols_reduce(const Cols<W>& J, const ColsPlan& P, int nb, const float* red) {
+  for (int e = threadIdx.x; e < nb * J.I; e += RB_BT) {
+    const int b = e / J.I, k = e % J.I;
+    float v = J.acc ? J.x[b * J.ldx + k] : 0.0f;
+    for (int pt = 0; pt < P.parts; ++pt) v += red[(pt * RB_TB + b) * P.wid + k];
+    J.x[b * J.ldx + k] = v;
+  }
+}
+// one or two independent transposed products in one phase (two: half the waves' worth of parts
+// each, their partial sums in separate halves of red, at most RB_RED floats); every thread calls
+// it, and when partial sums are used it ends on a barrier
+template <typename W>
+__device__ __forceinline__ void bmv_cols2(const Cols<W>& A, const Cols<W>& B, bool two, int nb, float* red) {
+  const int wv = wave_id(), waves = two ? RB_BW / 2 : RB_BW;
+  const ColsPlan PA = cols_plan(A.O, A.I, A.M.ld, waves);
+  ColsPlan PB = PA;
+  PB.items = 0;
+  PB.parts = 1;
+  if (two) PB = cols_plan(B.O, B.I, B.M.ld, waves);
+  float* redB = red + (PA.parts > 1 ? PA.parts * RB_TB * PA.wid : 0);
+  for (int it = wv; it < PA.items + PB.items; it += RB_BW) {   // uniform per wave
+    if (it < PA.items)
+      cols_item(A, PA, it, nb, red);
+    else
+      cols_item(B, PB, it - PA.items, nb, redB);
+  }
+  if (PA.parts > 1 || PB.parts > 1) {
+    __syncthreads();
+    if (PA.parts > 1) cols_reduce(A, PA, nb, red);
+    if (PB.parts > 1) cols_reduce(B, PB, nb, redB);
+    __syncthreads();
+  }
+}
+template <typename W>
+__device__ __forceinline__ void bmv_cols(const Cols<W>& A, int nb, float* red) {
+  bmv_cols2(A, A, false, nb, red);
+}
+
+// stats: a wave per token over the residual rows (16-byte loads) and P's slices
 template <typename T>
-__global__ __launch_bounds__(RB_NT) __attribute__((amdgpu_waves_per_eu(6))) void router_bwd_token(RouterBwdArgs a) {
-  __shared__ float red[RB_NW];
-  __shared__ float Ph[RB_MAXE], sh[RB_MAXE], dsh[RB_MAXE];
-  __shared__ float Pb[RB_MAXH], pa[RB_MAXH], dpa[RB_MAXH];
-  __shared__ float ppre[RB_MAXP], psil[RB_MAXP], dpp[RB_MAXP];
-  __shared__ float xp[8], dx[8], sc[16];
-  __shared__ float xth[RB_MAXX], dxth[RB_MAXX];   // [s; c; nu] and its gradient (ds, dc, dnu)
-  __shared__ float qkvu[4][RB_MAXM];                // q, k, v (pre-activation), u1 = W_n s
-  __shared__ float u2[RB_MAXM], du1[RB_MAXM], du2[RB_MAXM], dnum[RB_MAXM];
-  __shared__ float dfk[RB_MAXM], dfq[RB_MAXM], dvw[RB_NW][RB_MAXM];
-  __shared__ float fq[RB_MAXM];                   // phi(q)
-  // partial sums of mv_cols and the memory read: dvw's first RB_NT floats, which hold dL/dv only from the
-  // memory pass to the q, k, v gradients, where no partial sum is live (26 KiB of LDS: six workgroups a CU)
-  float* const part = &dvw[0][0];
-  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
-  const int T_ = a.T, j = a.j, d = a.d, DM = a.d_m, d_s = a.d_s, d_h = a.d_h, d_a = a.d_a;
-  const int d_e = a.d_e, d_p = a.d_p, d_head = a.d_head, NP = d_e + d_head, d_x = d_s + DM + 1;
+__global__ __launch_bounds__(RB_NT) void rbwd_stats(RouterBwdArgs a) {
+  const int t = blockIdx.x * RB_NW + static_cast<int>(threadIdx.x) / kWave, lane = threadIdx.x & (kWave - 1);
+  if (t >= a.T) return;   // whole waves; no barrier below
+  const int j = a.j, d = a.d;
   const T* hb = static_cast<const T*>(a.hbar) + static_cast<size_t>(t) * d;
   const T* h1 = j >= 2 ? static_cast<const T*>(a.prev1) + static_cast<size_t>(t) * d : nullptr;
   const T* h2 = j >= 3 ? static_cast<const T*>(a.prev2) + static_cast<size_t>(t) * d : nullptr;
-  auto colT = [&](float* base, int r) -> float& { return base[static_cast<size_t>(r) * T_ + t]; };
-
-  // ---- forward recompute -------------------------------------------------------------
-  // row statistics: inv_rms and the residual transitions
   float s2 = 0.0f, dd = 0.0f, dpv = 0.0f, pp2 = 0.0f;
-  for (int i = tid; i < d; i += RB_NT) {
-    const float x = ldf(hb + i);
-    s2 = fmaf(x, x, s2);
-    if (j >= 2) {
-      const float y = ldf(h1 + i), del = x - y;
-      dd = fmaf(del, del, dd);
-      if (j >= 3) {
-        const float dp_ = y - ldf(h2 + i);
-        dpv = fmaf(del, dp_, dpv);
-        pp2 = fmaf(dp_, dp_, pp2);
+#pragma unroll 2
+  for (int i = lane * 8; i < d; i += kWave * 8) {
+    float x[8], y[8], z[8];
+    ld8(hb + i, x);
+    if (j >= 2) ld8(h1 + i, y);
+    if (j >= 3) ld8(h2 + i, z);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      s2 = fmaf(x[u], x[u], s2);
+      if (j >= 2) {
+        const float del = x[u] - y[u];
+        dd = fmaf(del, del, dd);
+        if (j >= 3) {
+          const float dp_ = y[u] - z[u];
+          dpv = fmaf(del, dp_, dpv);
+          pp2 = fmaf(dp_, dp_, pp2);
+        }
       }
     }
   }
-  s2 = block_sum(s2, red);
-  dd = block_sum(dd, red);
-  dpv = block_sum(dpv, red);
-  pp2 = block_sum(pp2, red);
-  const float ir = 1.0f / sqrtf(s2 / static_cast<float>(d) + a.eps_norm);
-  // pre-activations: the K slices of P added in slice order
-  for (int e = tid; e < NP; e += RB_NT) {
+  s2 = wave_sum(s2);
+  dd = wave_sum(dd);
+  dpv = wave_sum(dpv);
+  pp2 = wave_sum(pp2);
+  if (lane == 0) {
+    float* rs = a.RS + static_cast<size_t>(t) * 4;
+    rs[0] = 1.0f / sqrtf(s2 / static_cast<float>(d) + a.eps_norm);
+    rs[1] = j >= 2 ? sqrtf(dd) : 0.0f;
+    rs[2] = sqrtf(pp2);
+    rs[3] = dpv;
+  }
+  // P's K slices added in slice order, once for the three batched passes
+  const int NP = a.d_e + a.d_head, T_ = a.T;
+  for (int k = lane; k < NP; k += kWave) {
     float v = 0.0f;
-    for (int z = 0; z < a.p_splits; ++z) v += a.P[(static_cast<size_t>(z) * T_ + t) * NP + e];
-    if (e < d_e) {
-      Ph[e] = v;
-      sh[e] = siluf_(ir * v);
-    } else {
-      Pb[e - d_e] = v;
-    }
+    for (int z = 0; z < a.p_splits; ++z) v += a.P[(static_cast<size_t>(z) * T_ + t) * NP + k];
+    a.PSUM[static_cast<size_t>(t) * NP + k] = v;
   }
-  if (tid == 0) {
-    const float dj = j >= 2 ? sqrtf(dd) : 0.0f;
-    const float np_ = sqrtf(pp2);
-    xp[0] = static_cast<float>(j) / static_cast<float>(a.L_R);
-    xp[1] = static_cast<float>(a.L_R - j) / static_cast<float>(a.L_R);
-    xp[2] = dj;
-    xp[3] = j >= 3 ? dpv / (dj * np_ + a.eps) : 0.0f;
-    xp[4] = j > 1 ? a.p_in[t] : 1.0f;
-    xp[5] = j > 1 ? a.m_in[t] : 1.0f;
-    xp[6] = xp[7] = 0.0f;
-    sc[0] = dj;
-    sc[1] = np_;
-  }
-  __syncthreads();
-  // hidden encoder z^h (s[0:d_h]) and path encoder z^a (s[d_h:d_s])
-  mv_rows(static_cast<const T*>(a.w_hu), d_e, d_h, d_e, sh, xth);
-  mv_rows(static_cast<const T*>(a.w_p1), 6, d_p, 6, xp, ppre);
-  __syncthreads();
-  for (int o = tid; o < d_p; o += RB_NT) psil[o] = siluf_(ppre[o]);
-  __syncthreads();
-  mv_rows(static_cast<const T*>(a.w_p2), d_p, d_a, d_p, psil, xth + d_h);
-  __syncthreads();
-  // q, k, v, W_n s
-  mv_rows(static_cast<const T*>(a.w_q), d_s, DM, d_s, xth, qkvu[0]);
-  mv_rows(static_cast<const T*>(a.w_k), d_s, DM, d_s, xth, qkvu[1]);
-  mv_rows(static_cast<const T*>(a.w_v), d_s, DM, d_s, xth, qkvu[2]);
-  mv_rows(static_cast<const T*>(a.w_n), d_s, DM, d_s, xth, qkvu[3]);
-  __syncthreads();
-  // memory read c = phi(q)^T S_{j-1} / (phi(q)^T zeta_{j-1} + eps)
-  // the received state is read only from j = 2 (it may be absent at j = 1)
-  const float* Sin = j > 1 ? a.S_in + static_cast<size_t>(t) * DM * DM : nullptr;
-  const float* zin = j > 1 ? a.zeta_in + static_cast<size_t>(t) * DM : nullptr;
-  float den = 0.0f;
-  for (int k = tid; k < DM; k += RB_NT) {
-    fq[k] = phif_(qkvu[0][k]);
-    den += j > 1 ? fq[k] * zin[k] : 0.0f;
-  }
-  den = block_sum(den, red) + a.eps;   // (its barriers also publish fq)
-  {
-    // RB_NT / DM parts of the k range (d_m is 32, 64, 128 or 256), added in part order
-    const int np = RB_NT / DM, kc = DM / np, v = tid % DM, q = tid / DM;
-    float acc = 0.0f;
-    if (j > 1)
-      for (int k = q * kc; k < (q + 1) * kc; ++k) acc = fmaf(fq[k], Sin[static_cast<size_t>(k) * DM + v], acc);
-    part[tid] = acc;
-    __syncthreads();
-    for (int u = tid; u < DM; u += RB_NT) {
-      float c = 0.0f;
-      for (int r = 0; r < np; ++r) c += part[r * DM + u];
-      xth[d_s + u] = c / den;
-    }
-  }
-  __syncthreads();
-  // history dissimilarity nu = 1 - cos(W_n s, W_c c)
-  mv_rows(static_cast<const T*>(a.w_c), DM, DM, DM, xth + d_s, u2);
-  __syncthreads();
-  float n1 = 0.0f, n2 = 0.0f, nn = 0.0f;
-  for (int k = tid; k < DM; k += RB_NT) {
-    n1 = fmaf(qkvu[3][k], qkvu[3][k], n1);
-    n2 = fmaf(u2[k], u2[k], n2);
-    nn = fmaf(qkvu[3][k], u2[k], nn);
-  }
-  n1 = sqrtf(block_sum(n1, red));
-  n2 = sqrtf(block_sum(n2, red));
-  nn = block_sum(nn, red);
-  const float Dc = n1 * n2 + a.eps;
-  if (tid == 0) xth[d_s + DM] = j > 1 ? 1.0f - nn / Dc : 0.0f;
-  __syncthreads();
-  // history head a = f_theta([s; c; nu]), p = sigma(a / T_hist); local head's SiLU
-  mv_rows(static_cast<const T*>(a.th1), a.ld_th1, d_head, d_x, xth, pa);
-  __syncthreads();
-  float aa = 0.0f;
-  for (int o = tid; o < d_head; o += RB_NT) aa = fmaf(ldf(static_cast<const T*>(a.th2) + o), siluf_(pa[o]), aa);
-  aa = block_sum(aa, red);
-  const float p = sigmoidf_(aa / a.T_hist);
+}
 
-  // ---- reverse -------------------------------------------------------------------------
-  const float dl = a.dlogit[t];
-  const float dp_in = a.dp[t], dm_in = a.dm[t];
-  const float m_prev = xp[5];
-  const float da = dl + (dp_in + dm_in * m_prev) * p * (1.0f - p) / a.T_hist;
-  const float db = dl;
-  if (tid == 0) {
-    colT(a.DA, 0) = da;
-    colT(a.DB, 0) = db;
+// F1
+template <typename T>
+__global__ __launch_bounds__(RB_BT) void rbwd_f1(RouterBwdArgs a) {
+  __shared__ float sh[RB_TB][RB_MAXE + 1];     // SiLU(ir P_h)
+  __shared__ float pp[RB_TB][RB_MAXP + 1];     // SiLU of the path encoder's pre-activation
+  __shared__ float xs[RB_TB][RB_MAXS + 1];     // s
+  __shared__ float xp[RB_TB][8];
+  __shared__ float wp1[RB_MAXP * 6];
+  __shared__ float irs[RB_TB];
+  const int tid = threadIdx.x;
+  const int T_ = a.T, j = a.j, DM = a.d_m, d_s = a.d_s, d_h = a.d_h, d_a = a.d_a;
+  const int d_e = a.d_e, d_p = a.d_p, NP = d_e + a.d_head;
+  const int t0 = blockIdx.x * RB_TB, nb = min(RB_TB, T_ - t0);
+  // P's hidden part (loads first, clamped to the last element), W_p1, the path features
+  constexpr int UE = (RB_TB * RB_MAXE + RB_BT - 1) / RB_BT;
+  const int ne = nb * d_e;
+  float ph[UE];
+#pragma unroll
+  for (int u = 0; u < UE; ++u) {
+    const int e = min(tid + u * RB_BT, ne - 1), b = e / d_e, k = e % d_e;
+    ph[u] = a.PSUM[static_cast<size_t>(t0 + b) * NP + k];
   }
-  // heads: dL/dpre_a, dL/dpre_b (the latter is the psi_1 part of dL/dP)
-  for (int o = tid; o < d_head; o += RB_NT) {
-    const float sa = siluf_(pa[o]);
-    dpa[o] = da * ldf(static_cast<const T*>(a.th2) + o) * silu_grad_(pa[o]);
-    colT(a.dPAT, o) = dpa[o];
-    colT(a.SAT, o) = sa;
-    const float dpb = db * ldf(static_cast<const T*>(a.ps2) + o) * silu_grad_(Pb[o]);
-    a.dP[static_cast<size_t>(t) * NP + d_e + o] = dpb;
-    colT(a.dPT, d_e + o) = dpb;
-    colT(a.SBT, o) = siluf_(Pb[o]);
+  for (int e = tid; e < d_p * 6; e += RB_BT) wp1[e] = ldf(static_cast<const T*>(a.w_p1) + e);
+  if (tid < nb) {
+    const int b = tid, t = t0 + b;
+    const float* rs = a.RS + static_cast<size_t>(t) * 4;
+    const float dj = rs[1], np_ = rs[2], dpv = rs[3];
+    irs[b] = rs[0];
+    xp[b][0] = static_cast<float>(j) / static_cast<float>(a.L_R);
+    xp[b][1] = static_cast<float>(a.L_R - j) / static_cast<float>(a.L_R);
+    xp[b][2] = dj;
+    xp[b][3] = j >= 3 ? dpv / (dj * np_ + a.eps) : 0.0f;
+    xp[b][4] = j > 1 ? a.p_in[t] : 1.0f;
+    xp[b][5] = j > 1 ? a.m_in[t] : 1.0f;
+    xp[b][6] = xp[b][7] = 0.0f;
   }
   __syncthreads();
-  // [ds; dc; dnu] = f_theta's first layer transposed times dL/dpre_a
-  mv_cols(static_cast<const T*>(a.th1), a.ld_th1, d_head, d_x, dpa, dxth, false, part);
-  for (int k = tid; k < d_x; k += RB_NT) colT(a.XT, k) = xth[k];
+  // SiLU(ir P_h); the path encoder W_p1 x^path (six terms) and its SiLU
+#pragma unroll
+  for (int u = 0; u < UE; ++u) {
+    const int e = tid + u * RB_BT, b = e / d_e, k = e % d_e;
+    if (e < ne) sh[b][k] = siluf_(irs[b] * ph[u]);
+  }
+  for (int e = tid; e < nb * d_p; e += RB_BT) {
+    const int b = e / d_p, o = e % d_p;
+    float pre = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 6; ++k) pre = fmaf(wp1[o * 6 + k], xp[b][k], pre);
+    a.PPRE[static_cast<size_t>(t0 + b) * d_p + o] = pre;
+    pp[b][o] = siluf_(pre);
+  }
+  __syncthreads();
+  for (int e = tid; e < nb * d_p; e += RB_BT) {
+    const int o = e / nb, b = e % nb;
+    a.SPT[static_cast<size_t>(o) * T_ + t0 + b] = pp[b][o];
+  }
+  for (int e = tid; e < nb * 6; e += RB_BT) {
+    const int o = e / nb, b = e % nb;
+    a.XPT[static_cast<size_t>(o) * T_ + t0 + b] = xp[b][o];
+  }
+  // s = [W_hu SiLU(ir P_h); W_p2 SiLU(W_p1 x^path)]
+  bmv_rows(mats1<T>(a.w_hu, d_h, d_e), d_h, d_e, &sh[0][0], RB_MAXE + 1, &xs[0][0], RB_MAXS + 1, nb);
+  bmv_rows(mats1<T>(a.w_p2, d_a, d_p), d_a, d_p, &pp[0][0], RB_MAXP + 1, &xs[0][d_h], RB_MAXS + 1, nb);
+  __syncthreads();
+  for (int e = tid; e < nb * d_s; e += RB_BT) {
+    const int k = e / nb, b = e % nb;
+    a.XT[static_cast<size_t>(k) * T_ + t0 + b] = xs[b][k];
+  }
+  // [q; k; v; W_n s] (pre-activations) in one stacked product, token-major
+  const Mats<T> qkvn{static_cast<const T*>(a.w_q), static_cast<const T*>(a.w_k), static_cast<const T*>(a.w_v),
+                     static_cast<const T*>(a.w_n), DM, d_s};
+  bmv_rows(qkvn, 4 * DM, d_s, &xs[0][0], RB_MAXS + 1, a.QKVU + static_cast<size_t>(t0) * 4 * DM, 4 * DM, nb);
+}
+
+// M1: c and the normaliser for one token; thread: 4 columns (a float4) of DM / (RB_NT / (DM / 4))
+// rows, partial sums added over the row groups in order.  S is read once, with the non-temporal
+// hint, so that the stream does not push the router weights out of L2 between the batched passes.
+template <int DM>
+__global__ __launch_bounds__(RB_NT) void rbwd_read(RouterBwdArgs a) {
+  constexpr int CG = DM / 4, RG = RB_NT / CG;   // column groups, row groups
+  constexpr int NR = DM / RG, PF = NR < 16 ? NR : 16;   // rows per thread, rows loaded before phi(q)
+  __shared__ float fq[DM];
+  __shared__ f32x4 part[RG][CG];
+  __shared__ float red[RB_NW];
+  const int t = blockIdx.x, tid = threadIdx.x, j = a.j;
+  const int cg = tid % CG, rg = tid / CG;
+  const f32x4* S = j > 1 ? reinterpret_cast<const f32x4*>(a.S_in + static_cast<size_t>(t) * DM * DM) + cg : nullptr;
+  f32x4 pre[PF];
+  if (S)
+#pragma unroll
+    for (int u = 0; u < PF; ++u) pre[u] = __builtin_nontemporal_load(S + static_cast<size_t>(rg + u * RG) * CG);
+  for (int k = tid; k < DM; k += RB_NT) fq[k] = phif_(a.QKVU[static_cast<size_t>(t) * 4 * DM + k]);
+  __syncthreads();
+  f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  float den = 0.0f;
+  if (S) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) acc += fq[rg + u * RG] * pre[u];
+#pragma unroll 16
+    for (int u = PF; u < NR; ++u) {
+      const int k = rg + u * RG;
+      acc += fq[k] * __builtin_nontemporal_load(S + static_cast<size_t>(k) * CG);
+    }
+    for (int k = tid; k < DM; k += RB_NT) den = fmaf(fq[k], a.zeta_in[static_cast<size_t>(t) * DM + k], den);
+  }
+  part[rg][cg] = acc;
+  den = block_sum(den, red) + a.eps;   // (its barriers also publish part)
+  for (int v = tid; v < DM; v += RB_NT) {
+    float c = 0.0f;
+    for (int r = 0; r < RG; ++r) c += part[r][v / 4][v % 4];
+    a.Cv[static_cast<size_t>(t) * DM + v] = c / den;
+  }
+  if (tid == 0) a.DEN[t] = den;
+}
+
+// F2
+template <typename T>
+__global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
+  constexpr int LX = RB_MAXX + 1, LH = RB_MAXH + 1, LM = RB_MAXM + 1;
+  __shared__ float xth[RB_TB][LX];    // [s; c; nu]
+  __shared__ float dxth[RB_TB][LX];   // P's head part for a while, then [ds; dc; dnu]
+  __shared__ float pa[RB_TB][LH];     // f_theta's hidden pre-activation, then dL/dpre_a
+  __shared__ float u1[RB_TB][LM];     // W_n s, then dL/du1
+  __shared__ float u2[RB_TB][LM];     // W_c c, then dL/du2
+  __shared__ float red[RB_RED];
+  __shared__ float hv[3][RB_MAXH];    // th1's nu column, th2, psi_2
+  __shared__ float nrm[RB_TB][4];     // n1, n2, nn, Dc
+  __shared__ float dab[RB_TB][2];     // dL/da, dL/db
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = wave_id();
+  const int T_ = a.T, j = a.j, DM = a.d_m, d_s = a.d_s, d_e = a.d_e, d_head = a.d_head;
+  const int NP = d_e + d_head, d_x = d_s + DM + 1;
+  const int t0 = blockIdx.x * RB_TB, nb = min(RB_TB, T_ - t0);
+  // s, c, W_n s, P's head part (loads first, clamped to the last element), the heads' vectors
+  {
+    constexpr int US = (RB_TB * RB_MAXS + RB_BT - 1) / RB_BT, UM = (RB_TB * RB_MAXM + RB_BT - 1) / RB_BT;
+    constexpr int UH = (RB_TB * RB_MAXH + RB_BT - 1) / RB_BT;
+    const int ns = nb * d_s, nm = nb * DM, nh = nb * d_head;
+    float vs[US], vc[UM], vu[UM], vh[UH];
+#pragma unroll
+    for (int u = 0; u < US; ++u) {
+      const int e = min(tid + u * RB_BT, ns - 1), k = e / nb, b = e % nb;
+      vs[u] = a.XT[static_cast<size_t>(k) * T_ + t0 + b];
+    }
+#pragma unroll
+    for (int u = 0; u < UM; ++u) {
+      const int e = min(tid + u * RB_BT, nm - 1), b = e / DM, k = e % DM;
+      vc[u] = a.Cv[static_cast<size_t>(t0 + b) * DM + k];
+      vu[u] = a.QKVU[static_cast<size_t>(t0 + b) * 4 * DM + 3 * DM + k];
+    }
+#pragma unroll
+    for (int u = 0; u < UH; ++u) {
+      const int e = min(tid + u * RB_BT, nh - 1), b = e / d_head, o = e % d_head;
+      vh[u] = a.PSUM[static_cast<size_t>(t0 + b) * NP + d_e + o];
+    }
+    for (int o = tid; o < d_head; o += RB_BT) {
+      hv[0][o] = ldf(static_cast<const T*>(a.th1) + static_cast<size_t>(o) * a.ld_th1 + d_s + DM);
+      hv[1][o] = ldf(static_cast<const T*>(a.th2) + o);
+      hv[2][o] = ldf(static_cast<const T*>(a.ps2) + o);
+    }
+#pragma unroll
+    for (int u = 0; u < US; ++u) {
+      const int e = tid + u * RB_BT, k = e / nb, b = e % nb;
+      if (e < ns) xth[b][k] = vs[u];
+    }
+#pragma unroll
+    for (int u = 0; u < UM; ++u) {
+      const int e = tid + u * RB_BT, b = e / DM, k = e % DM;
+      if (e < nm) {
+        xth[b][d_s + k] = vc[u];
+        u1[b][k] = vu[u];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UH; ++u) {
+      const int e = tid + u * RB_BT, b = e / d_head, o = e % d_head;
+      if (e < nh) dxth[b][o] = vh[u];
+    }
+  }
+  __syncthreads();
+  // W_c c and f_theta's first layer over [s; c] (nu's column is added with the head below)
+  for (int e = tid; e < nb * DM; e += RB_BT) {
+    const int k = d_s + e / nb, b = e % nb;
+    a.XT[static_cast<size_t>(k) * T_ + t0 + b] = xth[b][k];
+  }
+  bmv_rows(mats1<T>(a.w_c, DM, DM), DM, DM, &xth[0][d_s], LX, &u2[0][0], LM, nb);
+  bmv_rows(mats1<T>(a.th1, d_head, a.ld_th1), d_head, d_s + DM, &xth[0][0], LX, &pa[0][0], LH, nb);
+  __syncthreads();
+  // a wave per token: nu = 1 - cos(W_n s, W_c c); the history head a = th2 . SiLU(pre_a),
+  // p = sigma(a / T_hist); dL/da, dL/db; dL/dP's head part in its token-major row
+  for (int b = wv; b < nb; b += RB_BW) {
+    const int t = t0 + b;
+    float n1 = 0.0f, n2 = 0.0f, nn = 0.0f;
+    for (int k = lane; k < DM; k += kWave) {
+      n1 = fmaf(u1[b][k], u1[b][k], n1);
+      n2 = fmaf(u2[b][k], u2[b][k], n2);
+      nn = fmaf(u1[b][k], u2[b][k], nn);
+    }
+    n1 = sqrtf(wave_sum(n1));
+    n2 = sqrtf(wave_sum(n2));
+    nn = wave_sum(nn);
+    const float Dc = n1 * n2 + a.eps;
+    const float nu = j > 1 ? 1.0f - nn / Dc : 0.0f;
+    float aa = 0.0f;
+    for (int o = lane; o < d_head; o += kWave) {
+      const float pre = fmaf(hv[0][o], nu, pa[b][o]);
+      pa[b][o] = pre;
+      aa = fmaf(hv[1][o], siluf_(pre), aa);
+    }
+    aa = wave_sum(aa);
+    const float p = sigmoidf_(aa / a.T_hist);
+    const float dl = a.dlogit[t];
+    const float m_prev = j > 1 ? a.m_in[t] : 1.0f;
+    const float da = dl + (a.dp[t] + a.dm[t] * m_prev) * p * (1.0f - p) / a.T_hist;
+    for (int o = lane; o < d_head; o += kWave)
+      a.dP[static_cast<size_t>(t) * NP + d_e + o] = dl * hv[2][o] * silu_grad_(dxth[b][o]);
+    if (lane == 0) {
+      nrm[b][0] = n1;
+      nrm[b][1] = n2;
+      nrm[b][2] = nn;
+      nrm[b][3] = Dc;
+      xth[b][d_s + DM] = nu;
+      dab[b][0] = da;
+      dab[b][1] = dl;
+      a.PS[t] = p;
+      a.DA[t] = da;
+      a.DB[t] = dl;
+    }
+  }
+  __syncthreads();
+  // the heads' pre-activation gradients, token-contiguous: dL/dpre_a (over pa, in place), dL/dpre_b
+  for (int e = tid; e < nb * d_head; e += RB_BT) {
+    const int o = e / nb, b = e % nb, t = t0 + b;
+    const float x = pa[b][o];
+    a.SAT[static_cast<size_t>(o) * T_ + t] = siluf_(x);
+    const float g = dab[b][0] * hv[1][o] * silu_grad_(x);
+    a.dPAT[static_cast<size_t>(o) * T_ + t] = g;
+    pa[b][o] = g;
+    const float pb = dxth[b][o];
+    a.dPT[static_cast<size_t>(d_e + o) * T_ + t] = dab[b][1] * hv[2][o] * silu_grad_(pb);
+    a.SBT[static_cast<size_t>(o) * T_ + t] = siluf_(pb);
+  }
+  if (tid < nb) a.XT[static_cast<size_t>(d_s + DM) * T_ + t0 + tid] = xth[tid][d_s + DM];
+  __syncthreads();
+  // [ds; dc; dnu] = th1^T dL/dpre_a
+  bmv_cols(Cols<T>{mats1<T>(a.th1, d_head, a.ld_th1), d_head, d_x, &pa[0][0], LH, &dxth[0][0], LX, false}, nb, red);
   __syncthreads();
   // nu's cosine backward (a constant at j = 1)
-  {
-    const float dcos = j > 1 ? -dxth[d_s + DM] : 0.0f;
+  for (int e = tid; e < nb * DM; e += RB_BT) {
+    const int k = e / nb, b = e % nb, t = t0 + b;
+    const float n1 = nrm[b][0], n2 = nrm[b][1], nn = nrm[b][2], Dc = nrm[b][3];
+    const float dcos = j > 1 ? -dxth[b][d_s + DM] : 0.0f;
     const float q_ = nn / (Dc * Dc);
-    for (int k = tid; k < DM; k += RB_NT) {
-      const float a1 = qkvu[3][k], a2 = u2[k];
-      du1[k] = dcos * (a2 / Dc - q_ * n2 * (n1 > 0.0f ? a1 / n1 : 0.0f));
-      du2[k] = dcos * (a1 / Dc - q_ * n1 * (n2 > 0.0f ? a2 / n2 : 0.0f));
-      colT(a.dU1T, k) = du1[k];
-      colT(a.dU2T, k) = du2[k];
+    const float a1 = u1[b][k], a2 = u2[b][k];
+    const float g1 = dcos * (a2 / Dc - q_ * n2 * (n1 > 0.0f ? a1 / n1 : 0.0f));
+    const float g2 = dcos * (a1 / Dc - q_ * n1 * (n2 > 0.0f ? a2 / n2 : 0.0f));
+    u1[b][k] = g1;
+    u2[b][k] = g2;
+    a.dU1T[static_cast<size_t>(k) * T_ + t] = g1;
+    a.dU2T[static_cast<size_t>(k) * T_ + t] = g2;
+  }
+  __syncthreads();
+  // ds += W_n^T du1, dc += W_c^T du2
+  bmv_cols2(Cols<T>{mats1<T>(a.w_n, DM, d_s), DM, d_s, &u1[0][0], LM, &dxth[0][0], LX, true},
+            Cols<T>{mats1<T>(a.w_c, DM, DM), DM, DM, &u2[0][0], LM, &dxth[0][d_s], LX, true}, true, nb, red);
+  __syncthreads();
+  // the read's normaliser: dL/dnum = dc / den, dL/dden = -<dc, c> / den (no read at j = 1)
+  for (int b = wv; b < nb; b += RB_BW) {
+    const int t = t0 + b;
+    const float den = a.DEN[t];
+    float dden = 0.0f;
+    for (int v = lane; v < DM; v += kWave) {
+      a.DNUM[static_cast<size_t>(t) * DM + v] = j > 1 ? dxth[b][d_s + v] / den : 0.0f;
+      dden += j > 1 ? -dxth[b][d_s + v] * xth[b][d_s + v] / den : 0.0f;
     }
+    dden = wave_sum(dden);
+    if (lane == 0) a.DDEN[t] = dden;
+  }
+  for (int e = tid; e < nb * d_s; e += RB_BT) {
+    const int b = e / d_s, k = e % d_s;
+    a.DSP[static_cast<size_t>(t0 + b) * d_s + k] = dxth[b][k];
+  }
+}
+
+// M2: the pass over S_{j-1} and dL/dS_j of one token.  LPR lanes hold a row's DM columns as float4s
+// (RPW rows per wave at a time); row sums by shuffles within the LPR lanes, column sums over the
+// waves' row sets added in order.  The three state streams carry the non-temporal hint, as in M1.
+template <int DM>
+__global__ __launch_bounds__(RB_NT) void rbwd_spass(RouterBwdArgs a) {
+  constexpr int LPR = DM / 4 < kWave ? DM / 4 : kWave, RPW = kWave / LPR, RSETS = RB_NW * RPW;
+  __shared__ float fq[DM], fk[DM], vv[DM], dn[DM], zi[DM];
+  __shared__ float sk[DM], sq[DM];
+  __shared__ f32x4 dvp[RSETS][LPR];
+  __shared__ float red[RB_NW];
+  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wv = wave_id(), j = a.j;
+  const float* qkv = a.QKVU + static_cast<size_t>(t) * 4 * DM;
+  for (int k = tid; k < DM; k += RB_NT) {
+    fq[k] = phif_(qkv[k]);
+    fk[k] = phif_(qkv[DM + k]);
+    vv[k] = qkv[2 * DM + k];
+    dn[k] = a.DNUM[static_cast<size_t>(t) * DM + k];
+    zi[k] = j > 1 ? a.zeta_in[static_cast<size_t>(t) * DM + k] : 0.0f;
   }
   __syncthreads();
-  mv_cols(static_cast<const T*>(a.w_n), d_s, DM, d_s, du1, dxth, true, part);            // ds += W_n^T du1
-  mv_cols(static_cast<const T*>(a.w_c), DM, DM, DM, du2, dxth + d_s, true, part);        // dc += W_c^T du2
-  __syncthreads();
-  // memory read: dL/dnum = dc / den, dL/dden = -<dc, c> / den (no read at j = 1)
-  float dden = 0.0f;
-  for (int v = tid; v < DM; v += RB_NT) {
-    dnum[v] = j > 1 ? dxth[d_s + v] / den : 0.0f;
-    dden += j > 1 ? -dxth[d_s + v] * xth[d_s + v] / den : 0.0f;
-  }
-  dden = block_sum(dden, red);   // (its barriers also publish dnum)
-  // one pass over S_{j-1} and dL/dS_j: waves take rows k, lanes columns v
-  float* dS = a.dS + static_cast<size_t>(t) * DM * DM;
-  float* dz = a.dzeta + static_cast<size_t>(t) * DM;
-  const float rho = a.rho;
+  const float dden = a.DDEN[t], rho = a.rho;
+  const int cg = lane % LPR, rset = wv * RPW + lane / LPR;
+  f32x4* dS = reinterpret_cast<f32x4*>(a.dS + static_cast<size_t>(t) * DM * DM) + cg;
+  const f32x4* Sin = j > 1 ? reinterpret_cast<const f32x4*>(a.S_in + static_cast<size_t>(t) * DM * DM) + cg : nullptr;
+  const f32x4 v4 = {vv[4 * cg], vv[4 * cg + 1], vv[4 * cg + 2], vv[4 * cg + 3]};
+  const f32x4 n4 = {dn[4 * cg], dn[4 * cg + 1], dn[4 * cg + 2], dn[4 * cg + 3]};
+  f32x4 dva = {0.0f, 0.0f, 0.0f, 0.0f};
   float rho_acc = 0.0f;
-  float dva[RB_MAXM / kWave];
+#pragma unroll 4
+  for (int it = 0; it < DM / RSETS; ++it) {
+    const int k = rset + it * RSETS;
+    const size_t o = static_cast<size_t>(k) * (DM / 4);
+    const f32x4 g = __builtin_nontemporal_load(dS + o);
+    const f32x4 sv = Sin ? __builtin_nontemporal_load(Sin + o) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    float rk = g[0] * v4[0] + g[1] * v4[1] + g[2] * v4[2] + g[3] * v4[3];
+    float rq = sv[0] * n4[0] + sv[1] * n4[1] + sv[2] * n4[2] + sv[3] * n4[3];
+    rho_acc += g[0] * sv[0] + g[1] * sv[1] + g[2] * sv[2] + g[3] * sv[3];
+    dva += fk[k] * g;
+    __builtin_nontemporal_store(rho * g + fq[k] * n4, dS + o);
 #pragma unroll
-  for (int i = 0; i < RB_MAXM / kWave; ++i) dva[i] = 0.0f;
-  for (int k = wv; k < DM; k += RB_NW) {
-    const float fqk = fq[k], fkk = phif_(qkvu[1][k]);
-    float sk = 0.0f, sq = 0.0f;
-#pragma unroll
-    for (int i = 0; i < RB_MAXM / kWave; ++i) {
-      const int v = lane + kWave * i;
-      if (v < DM) {
-        const size_t o = static_cast<size_t>(k) * DM + v;
-        const float g = dS[o];
-        const float sv = j > 1 ? Sin[o] : 0.0f;
-        sk = fmaf(g, qkvu[2][v], sk);
-        sq = fmaf(sv, dnum[v], sq);
-        dva[i] = fmaf(g, fkk, dva[i]);
-        rho_acc = fmaf(g, sv, rho_acc);
-        dS[o] = fmaf(rho, g, fqk * dnum[v]);
-      }
+    for (int off = LPR / 2; off > 0; off >>= 1) {
+      rk += __shfl_xor(rk, off, kWave);
+      rq += __shfl_xor(rq, off, kWave);
     }
-    sk = wave_sum(sk);
-    sq = wave_sum(sq);
-    if (lane == 0) {
-      dfk[k] = sk + dz[k];
-      dfq[k] = sq + (j > 1 ? zin[k] : 0.0f) * dden;
+    if (cg == 0) {
+      sk[k] = rk;
+      sq[k] = rq;
     }
   }
-#pragma unroll
-  for (int i = 0; i < RB_MAXM / kWave; ++i) {
-    const int v = lane + kWave * i;
-    if (v < DM) dvw[wv][v] = dva[i];
-  }
+  dvp[rset][cg] = dva;
   __syncthreads();
-  // zeta: its share of dL/drho, and dL/dzeta_{j-1} in place (dfk above read the incoming value)
+  // zeta: its share of dL/drho and dL/dzeta_{j-1} in place, after dL/dphi(k) read the incoming value
+  float* dz = a.dzeta + static_cast<size_t>(t) * DM;
+  float* df = a.DF + static_cast<size_t>(t) * 3 * DM;
   for (int k = tid; k < DM; k += RB_NT) {
     const float g = dz[k];
-    rho_acc = fmaf(g, j > 1 ? zin[k] : 0.0f, rho_acc);
+    float dv = 0.0f;
+    for (int r = 0; r < RSETS; ++r) dv += dvp[r][k / 4][k % 4];
+    df[k] = sk[k] + g;
+    df[DM + k] = sq[k] + zi[k] * dden;
+    df[2 * DM + k] = dv;
+    rho_acc = fmaf(g, zi[k], rho_acc);
     dz[k] = fmaf(rho, g, fq[k] * dden);
   }
   rho_acc = block_sum(rho_acc, red);
   if (tid == 0) a.rho_part[t] = rho_acc;
-  // q, k, v gradients; the router state's gradient gets the projections' share
-  for (int k = tid; k < DM; k += RB_NT) {
-    float dv = 0.0f;
+}
+
+// F3
+template <typename T>
+__global__ __launch_bounds__(RB_BT) void rbwd_f3(RouterBwdArgs a) {
+  constexpr int LQ = 3 * RB_MAXM + 1, LS = RB_MAXS + 1, LP = RB_MAXP + 1, LE = RB_MAXE + 1;
+  static_assert(LQ >= RB_MAXE, "dqkv holds P's hidden part at the end");
+  __shared__ float dqkv[RB_TB][LQ];   // [dL/dq; dL/dk; dL/dv], later P's hidden part
+  __shared__ float ds[RB_TB][LS];
+  __shared__ float dpp[RB_TB][LP];
+  __shared__ float dxp[RB_TB][8];
+  __shared__ float dsh[RB_TB][LE];
+  __shared__ float red[RB_RED];
+  __shared__ float wp1[RB_MAXP * 6];
+  __shared__ float cnv[RB_TB], irs[RB_TB];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = wave_id();
+  const int T_ = a.T, j = a.j, DM = a.d_m, d_s = a.d_s, d_h = a.d_h, d_a = a.d_a, d_e = a.d_e, d_p = a.d_p;
+  const int NP = d_e + a.d_head;
+  const int t0 = blockIdx.x * RB_TB, nb = min(RB_TB, T_ - t0);
+  // dL/dq, dL/dk through phi (phi'(x) = 1 for x > 0, exp(x) otherwise), dL/dv, dL/ds so far; P's
+  // hidden part waits in registers (loads first, clamped to the last element)
+  constexpr int UE = (RB_TB * RB_MAXE + RB_BT - 1) / RB_BT;
+  const int ne = nb * d_e;
+  float ph[UE];
+  {
+    constexpr int UM = (RB_TB * RB_MAXM + RB_BT - 1) / RB_BT, US = (RB_TB * RB_MAXS + RB_BT - 1) / RB_BT;
+    const int nm = nb * DM, ns = nb * d_s;
+    float fq_[UM], fk_[UM], gq[UM], gk[UM], gv[UM], gs[US];
 #pragma unroll
-    for (int w = 0; w < RB_NW; ++w) dv += dvw[w][k];
-    const float dq = dfq[k] * phi_grad_(qkvu[0][k]);
-    const float dk = dfk[k] * phi_grad_(qkvu[1][k]);
-    dfq[k] = dq;
-    dfk[k] = dk;
-    dnum[k] = dv;     // dnum is free: it now holds dL/dv
-    colT(a.dQT, k) = dq;
-    colT(a.dKT, k) = dk;
-    colT(a.dVT, k) = dv;
+    for (int u = 0; u < UM; ++u) {
+      const int e = min(tid + u * RB_BT, nm - 1), b = e / DM, k = e % DM, t = t0 + b;
+      const float* qkv = a.QKVU + static_cast<size_t>(t) * 4 * DM;
+      const float* df = a.DF + static_cast<size_t>(t) * 3 * DM;
+      fq_[u] = qkv[k];
+      fk_[u] = qkv[DM + k];
+      gk[u] = df[k];
+      gq[u] = df[DM + k];
+      gv[u] = df[2 * DM + k];
+    }
+#pragma unroll
+    for (int u = 0; u < US; ++u) {
+      const int e = min(tid + u * RB_BT, ns - 1), b = e / d_s, k = e % d_s;
+      gs[u] = a.DSP[static_cast<size_t>(t0 + b) * d_s + k];
+    }
+#pragma unroll
+    for (int u = 0; u < UE; ++u) {
+      const int e = min(tid + u * RB_BT, ne - 1), b = e / d_e, k = e % d_e;
+      ph[u] = a.PSUM[static_cast<size_t>(t0 + b) * NP + k];
+    }
+    for (int e = tid; e < d_p * 6; e += RB_BT) wp1[e] = ldf(static_cast<const T*>(a.w_p1) + e);
+    if (tid < nb) irs[tid] = a.RS[static_cast<size_t>(t0 + tid) * 4];
+#pragma unroll
+    for (int u = 0; u < UM; ++u) {
+      const int e = tid + u * RB_BT, b = e / DM, k = e % DM;
+      if (e < nm) {
+        dqkv[b][k] = gq[u] * phi_grad_(fq_[u]);
+        dqkv[b][DM + k] = gk[u] * phi_grad_(fk_[u]);
+        dqkv[b][2 * DM + k] = gv[u];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < US; ++u) {
+      const int e = tid + u * RB_BT, b = e / d_s, k = e % d_s;
+      if (e < ns) ds[b][k] = gs[u];
+    }
   }
   __syncthreads();
-  mv_cols(static_cast<const T*>(a.w_q), d_s, DM, d_s, dfq, dxth, true, part);
-  mv_cols(static_cast<const T*>(a.w_k), d_s, DM, d_s, dfk, dxth, true, part);
-  mv_cols(static_cast<const T*>(a.w_v), d_s, DM, d_s, dnum, dxth, true, part);
-  __syncthreads();
-  // path encoder: dL/dSiLU(pre_p) = W_p2^T dz^a, then W_p1^T for the six features
-  mv_cols(static_cast<const T*>(a.w_p2), d_p, d_a, d_p, dxth + d_h, dpp, false, part);
-  __syncthreads();
-  for (int o = tid; o < d_p; o += RB_NT) {
-    dpp[o] *= silu_grad_(ppre[o]);
-    colT(a.dPPT, o) = dpp[o];
-    colT(a.SPT, o) = psil[o];
+  for (int e = tid; e < nb * DM; e += RB_BT) {
+    const int k = e / nb, b = e % nb, t = t0 + b;
+    a.dQT[static_cast<size_t>(k) * T_ + t] = dqkv[b][k];
+    a.dKT[static_cast<size_t>(k) * T_ + t] = dqkv[b][DM + k];
+    a.dVT[static_cast<size_t>(k) * T_ + t] = dqkv[b][2 * DM + k];
   }
-  for (int o = tid; o < d_a; o += RB_NT) colT(a.dZAT, o) = dxth[d_h + o];
-  for (int o = tid; o < d_h; o += RB_NT) colT(a.dZHT, o) = dxth[o];
-  if (tid < 6) colT(a.XPT, tid) = xp[tid];
+  // ds += [W_q; W_k; W_v]^T [dq; dk; dv] in one stacked product
+  const Mats<T> qkv{static_cast<const T*>(a.w_q), static_cast<const T*>(a.w_k), static_cast<const T*>(a.w_v), nullptr,
+                    DM, d_s};
+  bmv_cols(Cols<T>{qkv, 3 * DM, d_s, &dqkv[0][0], LQ, &ds[0][0], LS, true}, nb, red);
   __syncthreads();
-  mv_cols(static_cast<const T*>(a.w_p1), 6, d_p, 6, dpp, dx, false, part);
-  // hidden encoder: dL/dSiLU(pre_h) = W_hu^T dz^h
-  mv_cols(static_cast<const T*>(a.w_hu), d_e, d_h, d_e, dxth, dsh, false, part);
-  __syncthreads();
-  float cn = 0.0f;
-  for (int e = tid; e < d_e; e += RB_NT) {
-    const float dph = dsh[e] * silu_grad_(ir * Ph[e]);
-    cn = fmaf(dph, Ph[e], cn);
-    a.dP[static_cast<size_t>(t) * NP + e] = ir * dph;
-    colT(a.dPT, e) = ir * dph;
-    colT(a.SHT, e) = sh[e];
+  for (int e = tid; e < nb * d_s; e += RB_BT) {
+    const int k = e / nb, b = e % nb, t = t0 + b;
+    if (k < d_h)
+      a.dZHT[static_cast<size_t>(k) * T_ + t] = ds[b][k];
+    else
+      a.dZAT[static_cast<size_t>(k - d_h) * T_ + t] = ds[b][k];
   }
-  cn = block_sum(cn, red);
-  if (tid == 0) {
+  // dL/dSiLU(pre_p) = W_p2^T dz^a and dL/dSiLU(pre_h) = W_hu^T dz^h
+  bmv_cols2(Cols<T>{mats1<T>(a.w_p2, d_a, d_p), d_a, d_p, &ds[0][d_h], LS, &dpp[0][0], LP, false},
+            Cols<T>{mats1<T>(a.w_hu, d_h, d_e), d_h, d_e, &ds[0][0], LS, &dsh[0][0], LE, false}, true, nb, red);
+  __syncthreads();
+  for (int e = tid; e < nb * d_p; e += RB_BT) {
+    const int o = e / nb, b = e % nb, t = t0 + b;
+    const float g = dpp[b][o] * silu_grad_(a.PPRE[static_cast<size_t>(t) * d_p + o]);
+    dpp[b][o] = g;
+    a.dPPT[static_cast<size_t>(o) * T_ + t] = g;
+  }
+  // dL/dP's hidden part, ir SiLU'(ir P_h) dL/dSiLU, in the token-major rows (P_h waits in dqkv,
+  // dL/dpre_h in dsh, for the token-contiguous writes)
+#pragma unroll
+  for (int u = 0; u < UE; ++u) {
+    const int e = tid + u * RB_BT, b = e / d_e, k = e % d_e, t = t0 + b;
+    if (e < ne) {
+      const float ir = irs[b];
+      const float dph = dsh[b][k] * silu_grad_(ir * ph[u]);
+      dqkv[b][k] = ph[u];
+      dsh[b][k] = dph;
+      a.dP[static_cast<size_t>(t) * NP + k] = ir * dph;
+    }
+  }
+  __syncthreads();
+  // the six path features' gradients W_p1^T dL/dpre_p and the RMSNorm coefficient's
+  // sum_e dph_e P_h,e, a wave per (token, feature) and per token
+  for (int idx = wv; idx < nb * 6; idx += RB_BW) {
+    const int b = idx / 6, k = idx % 6;
+    float sacc = 0.0f;
+    for (int o = lane; o < d_p; o += kWave) sacc = fmaf(wp1[o * 6 + k], dpp[b][o], sacc);
+    sacc = wave_sum(sacc);
+    if (lane == 0) dxp[b][k] = sacc;
+  }
+  for (int b = wv; b < nb; b += RB_BW) {
+    float cn = 0.0f;
+    for (int k = lane; k < d_e; k += kWave) cn = fmaf(dsh[b][k], dqkv[b][k], cn);
+    cn = wave_sum(cn);
+    if (lane == 0) cnv[b] = cn;
+  }
+  for (int e = tid; e < nb * d_e; e += RB_BT) {
+    const int k = e / nb, b = e % nb, t = t0 + b;
+    const float ir = irs[b];
+    a.dPT[static_cast<size_t>(k) * T_ + t] = ir * dsh[b][k];
+    a.SHT[static_cast<size_t>(k) * T_ + t] = siluf_(ir * dqkv[b][k]);
+  }
+  __syncthreads();
+  if (tid < nb) {
+    const int b = tid, t = t0 + b;
+    const float* rs = a.RS + static_cast<size_t>(t) * 4;
+    const float ir = rs[0], nd = rs[1], np_ = rs[2], dpv = rs[3];
     // transitions: d_j = |delta_j| (j >= 2), gamma_j = cos(delta_j, delta_{j-1}) (j >= 3)
-    const float nd = sc[0], np_ = sc[1], ddj = dx[2], dg = dx[3];
+    const float ddj = dxp[b][2], dg = dxp[b][3];
     float c1 = 0.0f, c2 = 0.0f, c3 = 0.0f, c4 = 0.0f;
     if (j >= 2 && nd > 0.0f) c1 += ddj / nd;
     if (j >= 3) {
@@ -407,13 +938,14 @@ __global__ __launch_bounds__(RB_NT) __attribute__((amdgpu_waves_per_eu(6))) void
       if (np_ > 0.0f) c4 -= dg * q_ * nd / np_;
     }
     float* rc = a.rowcoef + static_cast<size_t>(t) * 8;
-    rc[0] = -(ir * ir * ir / static_cast<float>(d)) * cn;
+    rc[0] = -(ir * ir * ir / static_cast<float>(a.d)) * cnv[b];
     rc[1] = c1;
     rc[2] = c2;
     rc[3] = c3;
     rc[4] = c4;
-    a.dp[t] = dx[4];
-    a.dm[t] = dm_in * p + dx[5];
+    const float p = a.PS[t];
+    a.dm[t] = a.dm[t] * p + dxp[b][5];
+    a.dp[t] = dxp[b][4];
   }
 }
 
@@ -566,13 +1098,53 @@ size_t router_bwd_vector_floats(int d_m, int d_s, int d_h, int d_a, int d_e, int
   return static_cast<size_t>(d_s + d_m + 1) + 5 * d_m + 3 * d_head + 2 + 2 * d_p + 8 + d_a + d_h + d_e;
 }
 
+size_t router_bwd_token_floats(int d_m, int d_s, int d_p, int np) {
+  // RS, QKVU, PPRE, Cv, DEN, PS, DSP, DNUM, DDEN, DF, PSUM
+  return 4 + 4 * static_cast<size_t>(d_m) + d_p + d_m + 1 + 1 + d_s + d_m + 1 + 3 * static_cast<size_t>(d_m) + np;
+}
+
 hipError_t launch_router_bwd_token(const RouterBwdArgs& a, hipStream_t s) {
   if (a.d_e > RB_MAXE || a.d_head > RB_MAXH || a.d_s > RB_MAXS || a.d_m > RB_MAXM || a.d_p > RB_MAXP)
     return hipErrorInvalidValue;
-  if (a.dtype == 1)
-    router_bwd_token<bf16_t><<<a.T, RB_NT, 0, s>>>(a);
+  if (a.T <= 0) return hipSuccess;
+  if (a.d_m != 32 && a.d_m != 64 && a.d_m != 128 && a.d_m != 256) return hipErrorInvalidValue;
+  const unsigned nbat = static_cast<unsigned>((a.T + RB_TB - 1) / RB_TB), nt = static_cast<unsigned>(a.T);
+  const bool bf = a.dtype == 1;
+  const unsigned nst = static_cast<unsigned>((a.T + RB_NW - 1) / RB_NW);
+  hipError_t e;
+  if (bf)
+    rbwd_stats<bf16_t><<<nst, RB_NT, 0, s>>>(a);
   else
-    router_bwd_token<float><<<a.T, RB_NT, 0, s>>>(a);
+    rbwd_stats<float><<<nst, RB_NT, 0, s>>>(a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (bf)
+    rbwd_f1<bf16_t><<<nbat, RB_BT, 0, s>>>(a);
+  else
+    rbwd_f1<float><<<nbat, RB_BT, 0, s>>>(a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  switch (a.d_m) {
+    case 32: rbwd_read<32><<<nt, RB_NT, 0, s>>>(a); break;
+    case 64: rbwd_read<64><<<nt, RB_NT, 0, s>>>(a); break;
+    case 128: rbwd_read<128><<<nt, RB_NT, 0, s>>>(a); break;
+    default: rbwd_read<256><<<nt, RB_NT, 0, s>>>(a); break;
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (bf)
+    rbwd_f2<bf16_t><<<nbat, RB_BT, 0, s>>>(a);
+  else
+    rbwd_f2<float><<<nbat, RB_BT, 0, s>>>(a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  switch (a.d_m) {
+    case 32: rbwd_spass<32><<<nt, RB_NT, 0, s>>>(a); break;
+    case 64: rbwd_spass<64><<<nt, RB_NT, 0, s>>>(a); break;
+    case 128: rbwd_spass<128><<<nt, RB_NT, 0, s>>>(a); break;
+    default: rbwd_spass<256><<<nt, RB_NT, 0, s>>>(a); break;
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (bf)
+    rbwd_f3<bf16_t><<<nbat, RB_BT, 0, s>>>(a);
+  else
+    rbwd_f3<float><<<nbat, RB_BT, 0, s>>>(a);
   return hipGetLastError();
 }
 
