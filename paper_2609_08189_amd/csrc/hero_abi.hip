@@ -1244,10 +1244,38 @@ struct RouterBwdLayout {
   size_t P, dP, dPT, rowcoef, rho_part, vec, tok, hbT, wT;
   // bf16: the big products on the GEMM core, dP split into bf16 hi + lo, K padded to kp
   size_t dPT_hi, dPT_lo, dP_hi, dP_lo, hbT16, wT16;
-  size_t tn_part, tn_floats;   // K-split partials of the small weight-gradient products
+  size_t tn_part, tn_floats;   // K-split partials of the fp32 path's large weight-gradient products
+  size_t sp_part, sp_floats;   // chunk partials of the small weight-gradient products
   int kp;
   size_t total;
 };
+
+// the small weight-gradient products (tokens as K): dW_q, dW_k, dW_v, dW_n, dW_c, dth1, dth2, dpsi_2,
+// dW_p1, dW_p2, dW_hu.  Pointers come from a (operands) and grads (outputs); either may be null when
+// only the shapes are wanted.
+int router_small_products(const hero_dims& D, const hero::RouterBwdArgs* a, const hero_router_grads* g,
+                          hero::SmallProduct* out) {
+  const int T = a ? a->T : 0, dx = D.d_s + D.d_m + 1, ld_th1 = HERO_TH1_PITCH(D.d_s, D.d_m);
+  auto A = [&](float* hero::RouterBwdArgs::*f) -> const float* { return a ? a->*f : nullptr; };
+  const float* xs = A(&hero::RouterBwdArgs::XT);
+  const float* xc = xs ? xs + static_cast<size_t>(D.d_s) * T : nullptr;
+  int n = 0;
+  auto put = [&](const float* Ao, int M, const float* Bo, int N, float* C, int ldc) {
+    out[n++] = hero::SmallProduct{Ao, Bo, C, M, N, ldc};
+  };
+  put(A(&hero::RouterBwdArgs::dQT), D.d_m, xs, D.d_s, g ? g->w_q : nullptr, D.d_s);
+  put(A(&hero::RouterBwdArgs::dKT), D.d_m, xs, D.d_s, g ? g->w_k : nullptr, D.d_s);
+  put(A(&hero::RouterBwdArgs::dVT), D.d_m, xs, D.d_s, g ? g->w_v : nullptr, D.d_s);
+  put(A(&hero::RouterBwdArgs::dU1T), D.d_m, xs, D.d_s, g ? g->w_n : nullptr, D.d_s);
+  put(A(&hero::RouterBwdArgs::dU2T), D.d_m, xc, D.d_m, g ? g->w_c : nullptr, D.d_m);
+  put(A(&hero::RouterBwdArgs::dPAT), D.d_head, xs, dx, g ? g->th1 : nullptr, ld_th1);
+  put(A(&hero::RouterBwdArgs::SAT), D.d_head, A(&hero::RouterBwdArgs::DA), 1, g ? g->th2 : nullptr, 1);
+  put(A(&hero::RouterBwdArgs::SBT), D.d_head, A(&hero::RouterBwdArgs::DB), 1, g ? g->ps2 : nullptr, 1);
+  put(A(&hero::RouterBwdArgs::dPPT), D.d_p, A(&hero::RouterBwdArgs::XPT), 6, g ? g->w_p1 : nullptr, 6);
+  put(A(&hero::RouterBwdArgs::dZAT), D.d_a, A(&hero::RouterBwdArgs::SPT), D.d_p, g ? g->w_p2 : nullptr, D.d_p);
+  put(A(&hero::RouterBwdArgs::dZHT), D.d_h, A(&hero::RouterBwdArgs::SHT), D.d_e, g ? g->w_hu : nullptr, D.d_e);
+  return n;
+}
 
 RouterBwdLayout router_bwd_layout_of(const hero_dims& d, int T) {
   RouterBwdLayout L{};
@@ -1285,6 +1313,10 @@ RouterBwdLayout router_bwd_layout_of(const hero_dims& d, int T) {
   // K chunks for the small products: up to one per 64 tokens, at most 16 M floats (64 MB) of partials
   L.tn_floats = std::min(static_cast<size_t>(hero::tn_chunks(T)) * mn, std::max<size_t>(mn, 16u << 20));
   L.tn_part = take(L.tn_floats * 4);
+  hero::SmallProduct sp[hero::kSmallProducts];
+  const int nsp = router_small_products(d, nullptr, nullptr, sp);
+  L.sp_floats = hero::small_products_floats(sp, nsp, T);
+  L.sp_part = take(L.sp_floats * 4);
   L.total = off;
   return L;
 }
@@ -1470,21 +1502,34 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
       return hero::launch_gemm_tn_acc_f32(A, T, M, B, T, N, T, C, ldc, tn_part, L.tn_floats, s);
     };
     hipError_t x = hipSuccess;
+    hero::SmallProduct sp[hero::kSmallProducts];
+    const int nsp = router_small_products(D, &a, grads, sp);
+    float* sp_part = reinterpret_cast<float*>(ws + L.sp_part);
     if (D.dtype == HERO_BF16) {
       // dW_hd, dpsi_1 = dP^T hbar and dL/dhbar_j += dP [W_hd; psi_1] on the GEMM core: hbar and the
-      // weights are exact in bf16, dP enters as bf16 hi + lo (two accumulating products each)
+      // weights are exact in bf16, dP enters as bf16 hi + lo (two accumulating products each).
+      // dW_hd's pair (64 output tiles a product, a quarter of the CUs) and the small products run on
+      // the side stream beside dpsi_1's pair and dL/dhbar's; their outputs are disjoint (measured:
+      // 348 -> 261 us for the group at the 8B layer; dpsi_1's pair on the side too measured 298).
       const int kp = L.kp;
       unsigned char *ph = ws + L.dPT_hi, *pl = ws + L.dPT_lo, *qh = ws + L.dP_hi, *ql = ws + L.dP_lo;
       unsigned char *h16 = ws + L.hbT16, *w16 = ws + L.wT16;
       const size_t re = static_cast<size_t>(D.d_e) * kp * 2;
+      const Side* sd = side_of_current_device();
+      const hipStream_t s2 = sd ? sd->s : s;
       x = hero::launch_split_bf16(a.dPT, NP, T, T, ph, pl, kp, s);
       if (x == hipSuccess) x = hero::launch_transpose(D.dtype, hbar, T, D.d, D.d, h16, kp, kp, s);
-      for (unsigned char* part : {ph, pl}) {
+      if (x == hipSuccess && sd) {
+        x = hipEventRecord(sd->fork, s);
+        if (x == hipSuccess) x = hipStreamWaitEvent(s2, sd->fork, 0);
+      }
+      for (unsigned char* part : {ph, pl})
         if (x == hipSuccess)
-          x = hero::launch_gemm_nt_acc_bf16(part, kp, D.d_e, h16, kp, D.d, kp, grads->w_hd, D.d, s);
+          x = hero::launch_gemm_nt_acc_bf16(part, kp, D.d_e, h16, kp, D.d, kp, grads->w_hd, D.d, s2);
+      if (x == hipSuccess) x = hero::launch_small_products(sp, nsp, T, T, sp_part, L.sp_floats, s2);
+      for (unsigned char* part : {ph, pl})
         if (x == hipSuccess)
           x = hero::launch_gemm_nt_acc_bf16(part + re, kp, D.d_head, h16, kp, D.d, kp, grads->ps1, D.d, s);
-      }
       if (x == hipSuccess) x = hero::launch_split_bf16(a.dP, T, NP, NP, qh, ql, NP, s);
       if (x == hipSuccess) x = hero::launch_transpose(D.dtype, router->w_hd, D.d_e, D.d, D.d, w16, NP, D.d_e, s);
       if (x == hipSuccess)
@@ -1492,6 +1537,12 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
                                    D.d_head, s);
       for (unsigned char* part : {qh, ql})
         if (x == hipSuccess) x = hero::launch_gemm_nt_acc_bf16(part, NP, T, w16, NP, D.d, NP, dhbar, D.d, s);
+      if (sd) {
+        // joined even after a failed launch, so that the side stream holds nothing of this call
+        const hipError_t y = hipEventRecord(sd->join, s2);
+        const hipError_t z = y == hipSuccess ? hipStreamWaitEvent(s, sd->join, 0) : y;
+        if (x == hipSuccess) x = z;
+      }
     } else {
       x = hero::launch_to_f32_transpose(D.dtype, hbar, T, D.d, D.d, hbT, T, s);
       if (x == hipSuccess) x = acc(a.dPT, D.d_e, hbT, D.d, grads->w_hd, D.d);
@@ -1500,18 +1551,8 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
       if (x == hipSuccess)
         x = hero::launch_to_f32_transpose(D.dtype, router->ps1, D.d_head, D.d, D.d, wT + D.d_e, NP, s);
       if (x == hipSuccess) x = hero::launch_gemm_acc_f32(a.dP, NP, T, wT, NP, D.d, NP, dhbar, D.d, s);
+      if (x == hipSuccess) x = hero::launch_small_products(sp, nsp, T, T, sp_part, L.sp_floats, s);
     }
-    if (x == hipSuccess) x = acc(a.dQT, D.d_m, a.XT, D.d_s, grads->w_q, D.d_s);
-    if (x == hipSuccess) x = acc(a.dKT, D.d_m, a.XT, D.d_s, grads->w_k, D.d_s);
-    if (x == hipSuccess) x = acc(a.dVT, D.d_m, a.XT, D.d_s, grads->w_v, D.d_s);
-    if (x == hipSuccess) x = acc(a.dU1T, D.d_m, a.XT, D.d_s, grads->w_n, D.d_s);
-    if (x == hipSuccess) x = acc(a.dU2T, D.d_m, a.XT + static_cast<size_t>(D.d_s) * T, D.d_m, grads->w_c, D.d_m);
-    if (x == hipSuccess) x = acc(a.dPAT, D.d_head, a.XT, dx, grads->th1, ld_th1);
-    if (x == hipSuccess) x = acc(a.SAT, D.d_head, a.DA, 1, grads->th2, 1);
-    if (x == hipSuccess) x = acc(a.SBT, D.d_head, a.DB, 1, grads->ps2, 1);
-    if (x == hipSuccess) x = acc(a.dPPT, D.d_p, a.XPT, 6, grads->w_p1, 6);
-    if (x == hipSuccess) x = acc(a.dZAT, D.d_a, a.SPT, D.d_p, grads->w_p2, D.d_p);
-    if (x == hipSuccess) x = acc(a.dZHT, D.d_h, a.SHT, D.d_e, grads->w_hu, D.d_e);
     return x;
   });
   if (e != hipSuccess) return HERO_E_LAUNCH;

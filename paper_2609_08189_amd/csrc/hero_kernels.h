@@ -231,6 +231,21 @@ constexpr int kTnChunk = 64;
 int tn_chunks(int K);
 hipError_t launch_gemm_tn_acc_f32(const float* A, int lda, int M, const float* B, int ldb, int N, int K, float* C,
                                   int ldc, float* part, size_t part_floats, hipStream_t s);
+// C_p[m][n] += sum_t A_p[m][t] B_p[n][t] for up to kSmallProducts products in one launch (A_p [M][T],
+// B_p [N][T] fp32 with token pitch ldk; C_p fp32 with row pitch ldc) on the fp32 matrix cores.  The
+// tokens are cut into at most kSmallProductChunks chunks of at least 256 whose partial sums (part,
+// small_products_floats of them) are added in chunk order.
+struct SmallProduct {
+  const float* A;
+  const float* B;
+  float* C;
+  int M, N, ldc;
+};
+constexpr int kSmallProducts = 12;
+constexpr int kSmallProductChunks = 16;
+size_t small_products_floats(const SmallProduct* p, int n, int T);
+hipError_t launch_small_products(const SmallProduct* p, int n, int T, int ldk, float* part, size_t part_floats,
+                                 hipStream_t s);
 // x [R][C] fp32 (row pitch ld_in) as bf16 hi = bf16(x), lo = bf16(x - hi), [R][C_pad] with zero columns
 // from C to C_pad: hi + lo carries x to about 2^-16 relative
 hipError_t launch_split_bf16(const float* x, int R, int C, int ld_in, void* hi, void* lo, int C_pad, hipStream_t s);

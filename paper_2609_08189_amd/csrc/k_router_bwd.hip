@@ -1066,9 +1066,190 @@ __global__ __launch_bounds__(256) void split_bf16_kernel(const float* __restrict
   }
 }
 
+
+// The small weight-gradient products in one launch: C_p[m][n] += sum_t A_p[m][t] B_p[n][t] for every
+// product p, on the fp32 matrix cores.  A workgroup takes a 64 x 64 output tile of one product and a
+// chunk of kc tokens; each wave a 32 x 32 quarter as 2 x 2 MFMA tiles of 16 x 16.  Lane (r, g)
+// supplies operand row r at k slot g, tokens t0 + 4 g + i for the i-th of four products, loaded as one
+// float4 per operand row when the token pitch is a multiple of 4.  Rows past M or N read a clamped
+// row and are never stored; tokens past the chunk enter as zeros on both sides.  With one chunk the
+// tile adds into C; otherwise it writes its partial sums to part[chunk][tile][64 x 64], which
+// small_products_reduce adds into C in chunk order.
+struct SmallProductsArgs {
+  SmallProduct p[kSmallProducts];
+  int tile0[kSmallProducts + 1];   // first tile of each product (tile0[n] = tiles in all)
+  int ntn[kSmallProducts];         // column tiles of each product
+  int el0[kSmallProducts + 1];     // first output element of each product (el0[n] = elements in all)
+  int n, T, ldk, kc, nchunks;
+  float* part;
+};
+
+__device__ __forceinline__ int sp_product(const int* first, int n, int x) {
+  int pi = 0;
+  while (pi + 1 < n && first[pi + 1] <= x) ++pi;
+  return pi;
+}
+
+__global__ __launch_bounds__(256) void small_products_kernel(SmallProductsArgs a) {
+  const int nt = a.tile0[a.n];
+  const int tile = static_cast<int>(blockIdx.x) % nt, c = static_cast<int>(blockIdx.x) / nt;
+  const int pi = sp_product(a.tile0, a.n, tile);
+  const SmallProduct P = a.p[pi];
+  const int lt = tile - a.tile0[pi], tm = lt / a.ntn[pi], tn = lt % a.ntn[pi];
+  const int lane = threadIdx.x & (kWave - 1), r = lane & 15, g = lane >> 4, wv = wave_id();
+  const int mb = tm * 64 + (wv >> 1) * 32, nbs = tn * 64 + (wv & 1) * 32;
+  const int ldk = a.ldk;
+  const float* Ar[2];
+  const float* Br[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    Ar[h] = P.A + static_cast<size_t>(min(mb + 16 * h + r, P.M - 1)) * ldk;
+    Br[h] = P.B + static_cast<size_t>(min(nbs + 16 * h + r, P.N - 1)) * ldk;
+  }
+  const int tb = c * a.kc, te = min(a.T, tb + a.kc);
+  const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+  f32x4 acc[2][2] = {{zero, zero}, {zero, zero}};
+  if ((ldk & 3) == 0) {
+    // 16 tokens a step, the next step's operands in flight during the current step's products
+    auto load = [&](int t0, f32x4* av, f32x4* bv) {
+      const int tt = t0 + 4 * g;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (tt + 3 < te) {
+          av[h] = *reinterpret_cast<const f32x4*>(Ar[h] + tt);
+          bv[h] = *reinterpret_cast<const f32x4*>(Br[h] + tt);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const bool in = tt + i < te;
+            const int tc = in ? tt + i : te - 1;
+            const float x = Ar[h][tc], y = Br[h][tc];
+            av[h][i] = in ? x : 0.0f;
+            bv[h][i] = in ? y : 0.0f;
+          }
+        }
+      }
+    };
+    f32x4 ac[2], bc[2];
+    if (tb < te) load(tb, ac, bc);
+    for (int t0 = tb; t0 < te; t0 += 16) {
+      f32x4 an[2], bn[2];
+      if (t0 + 16 < te) load(t0 + 16, an, bn);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int w = 0; w < 2; ++w) acc[h][w] = mfma4(ac[h][i], bc[w][i], acc[h][w]);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        ac[h] = an[h];
+        bc[h] = bn[h];
+      }
+    }
+  } else {
+    for (int t0 = tb; t0 < te; t0 += 16) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = t0 + 4 * g + i;
+        const bool in = t < te;
+        const int tc = in ? t : te - 1;
+        float av[2], bv[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const float x = Ar[h][tc], y = Br[h][tc];
+          av[h] = in ? x : 0.0f;
+          bv[h] = in ? y : 0.0f;
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int w = 0; w < 2; ++w) acc[h][w] = mfma4(av[h], bv[w], acc[h][w]);
+      }
+    }
+  }
+  // lane (r, g) holds rows 4 g + q of column r of each 16 x 16 tile
+  float* pp = a.nchunks > 1 ? a.part + (static_cast<size_t>(c) * nt + tile) * 4096 : nullptr;
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int w = 0; w < 2; ++w)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int ml = (wv >> 1) * 32 + 16 * h + 4 * g + q, nl = (wv & 1) * 32 + 16 * w + r;
+        if (pp) {
+          pp[ml * 64 + nl] = acc[h][w][q];
+        } else {
+          const int m = tm * 64 + ml, n = tn * 64 + nl;
+          if (m < P.M && n < P.N) P.C[static_cast<size_t>(m) * P.ldc + n] += acc[h][w][q];
+        }
+      }
+}
+
+// C_p[m][n] += sum over chunks of part[chunk][tile of (m, n)][local], chunks in order
+__global__ __launch_bounds__(256) void small_products_reduce(SmallProductsArgs a) {
+  const int e = static_cast<int>(blockIdx.x) * 256 + static_cast<int>(threadIdx.x);
+  if (e >= a.el0[a.n]) return;
+  const int pi = sp_product(a.el0, a.n, e);
+  const SmallProduct P = a.p[pi];
+  const int le = e - a.el0[pi], m = le / P.N, n = le % P.N;
+  const int tile = a.tile0[pi] + (m / 64) * a.ntn[pi] + n / 64, local = (m % 64) * 64 + n % 64;
+  const int nt = a.tile0[a.n];
+  float v = 0.0f;
+  for (int c = 0; c < a.nchunks; ++c) v += a.part[(static_cast<size_t>(c) * nt + tile) * 4096 + local];
+  P.C[static_cast<size_t>(m) * P.ldc + n] += v;
+}
 }  // namespace
 
 int tn_chunks(int K) { return (K + kTnChunk - 1) / kTnChunk; }
+
+static int small_products_plan(const SmallProduct* p, int n, int T, SmallProductsArgs* a) {
+  a->n = n;
+  a->T = T;
+  int tiles = 0, els = 0;
+  for (int i = 0; i < n; ++i) {
+    a->p[i] = p[i];
+    a->tile0[i] = tiles;
+    a->el0[i] = els;
+    a->ntn[i] = (p[i].N + 63) / 64;
+    tiles += ((p[i].M + 63) / 64) * a->ntn[i];
+    els += p[i].M * p[i].N;
+  }
+  a->tile0[n] = tiles;
+  a->el0[n] = els;
+  // chunks of at least 256 tokens (a multiple of 16), at most kSmallProductChunks
+  a->nchunks = std::max(1, std::min(kSmallProductChunks, T / 256));
+  a->kc = ((T + a->nchunks - 1) / a->nchunks + 15) / 16 * 16;
+  a->nchunks = (T + a->kc - 1) / a->kc;
+  return tiles;
+}
+
+size_t small_products_floats(const SmallProduct* p, int n, int T) {
+  if (n <= 0 || n > kSmallProducts || T <= 0) return 0;
+  SmallProductsArgs a{};
+  const int tiles = small_products_plan(p, n, T, &a);
+  return a.nchunks > 1 ? static_cast<size_t>(a.nchunks) * tiles * 4096 : 0;
+}
+
+hipError_t launch_small_products(const SmallProduct* p, int n, int T, int ldk, float* part, size_t part_floats,
+                                 hipStream_t s) {
+  if (n <= 0 || T <= 0) return hipSuccess;
+  if (n > kSmallProducts) return hipErrorInvalidValue;
+  for (int i = 0; i < n; ++i)
+    if (p[i].M <= 0 || p[i].N <= 0 || !p[i].A || !p[i].B || !p[i].C) return hipErrorInvalidValue;
+  SmallProductsArgs a{};
+  const int tiles = small_products_plan(p, n, T, &a);
+  a.ldk = ldk;
+  a.part = part;
+  if (a.nchunks > 1 && (!part || part_floats < static_cast<size_t>(a.nchunks) * tiles * 4096))
+    return hipErrorInvalidValue;
+  small_products_kernel<<<static_cast<unsigned>(tiles * a.nchunks), 256, 0, s>>>(a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.nchunks == 1) return e;
+  small_products_reduce<<<static_cast<unsigned>((a.el0[n] + 255) / 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
 
 hipError_t launch_gemm_tn_acc_f32(const float* A, int lda, int M, const float* B, int ldb, int N, int K, float* C,
                                   int ldc, float* part, size_t part_floats, hipStream_t s) {
