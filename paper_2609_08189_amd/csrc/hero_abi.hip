@@ -1304,14 +1304,10 @@ RouterBwdLayout router_bwd_layout_of(const hero_dims& d, int T) {
   L.dP_lo = take(mfma ? t * np * 2 : 0);
   L.hbT16 = take(mfma ? static_cast<size_t>(d.d) * kp * 2 : 0);
   L.wT16 = take(mfma ? static_cast<size_t>(d.d) * np * 2 : 0);
-  // the largest small product: f_theta's first layer [d_head][d_s + d_m + 1] (or W_c, W_hu, W_q ...)
-  const size_t mn = std::max({static_cast<size_t>(d.d_head) * (d.d_s + d.d_m + 1),
-                              mfma ? 0 : static_cast<size_t>(std::max(d.d_e, d.d_head)) * d.d, static_cast<size_t>(d.d_m) * d.d_m,
-                              static_cast<size_t>(d.d_m) * d.d_s, static_cast<size_t>(d.d_h) * d.d_e,
-                              static_cast<size_t>(d.d_a) * d.d_p, static_cast<size_t>(d.d_p) * 6,
-                              static_cast<size_t>(d.d_head)});
-  // K chunks for the small products: up to one per 64 tokens, at most 16 M floats (64 MB) of partials
-  L.tn_floats = std::min(static_cast<size_t>(hero::tn_chunks(T)) * mn, std::max<size_t>(mn, 16u << 20));
+  // K chunks for fp32 storage's dW_hd and dpsi_1 (bf16 runs them on the GEMM core): up to one per 64
+  // tokens, at most 16 M floats (64 MB) of partials
+  const size_t mn = static_cast<size_t>(std::max(d.d_e, d.d_head)) * d.d;
+  L.tn_floats = mfma ? 0 : std::min(static_cast<size_t>(hero::tn_chunks(T)) * mn, std::max<size_t>(mn, 16u << 20));
   L.tn_part = take(L.tn_floats * 4);
   hero::SmallProduct sp[hero::kSmallProducts];
   const int nsp = router_small_products(d, nullptr, nullptr, sp);

@@ -14,8 +14,9 @@
 //   writes the gradient over P ([ir dL/dpre_h; dL/dpre_b], row- and token-major), the per-row
 //   coefficients of the RMSNorm and transition terms, and every (vector, token) pair the weight
 //   gradients need, token-contiguous, so that each weight gradient is one product with the
-//   tokens as K (run by the caller with a fixed summation order: tn_part / tn_reduce below for the
-//   small ones, the GEMM core with dP split into bf16 hi + lo for dW_hd, dpsi_1 and dP [W_hd; psi_1]).
+//   tokens as K (run by the caller with a fixed summation order: small_products_kernel /
+//   small_products_reduce below for the eleven small ones, the GEMM core with dP split into bf16 hi + lo
+//   for dW_hd, dpsi_1 and dP [W_hd; psi_1]; tn_part / tn_reduce for those three in fp32 storage).
 // router_bwd_rows: dL/dhbar_j += c_norm hbar_j + ddelta_j, dL/dhbar_{j-1} += ddelta_{j-1} -
 //   ddelta_j, dL/dhbar_{j-2} -= ddelta_{j-1}, with ddelta_j = c1 delta_j + c2 delta_{j-1} and
 //   ddelta_{j-1} = c3 delta_j + c4 delta_{j-1}.
