@@ -1478,6 +1478,8 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
   a.DDEN = per_token(1);
   a.DF = per_token(3 * D.d_m);
   a.PSUM = per_token(NP);
+  a.t_begin = 0;
+  a.t_end = T;
   a.dhbar = dhbar;
   a.dhbar1 = dhbar_prev1;
   a.dhbar2 = dhbar_prev2;
@@ -1489,7 +1491,14 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
     return hero::launch_router_gemm(D.dtype, hbar, router->w_hd, router->ps1, T, D.d, D.d_e, D.d_head,
                                      const_cast<float*>(a.P), s);
   });
-  if (e == hipSuccess) e = timed(HERO_K_ROUTER_BWD_TOKEN, s, [&] { return hero::launch_router_bwd_token(a, s); });
+  if (e == hipSuccess)
+    e = timed(HERO_K_ROUTER_BWD_TOKEN, s, [&] {
+      // one chain over all tokens (two halves on two streams, each half's batched passes beside the
+      // other's state streams, measured 341 against 336 us at the 8B layer: the batched passes slow
+      // down under the streams' memory traffic)
+      const hipError_t x = hero::launch_router_bwd_stats(a, s);
+      return x == hipSuccess ? hero::launch_router_bwd_chain(a, s, nullptr) : x;
+    });
   if (e != hipSuccess) return HERO_E_LAUNCH;
   e = timed(HERO_K_ROUTER_BWD_PRODUCTS, s, [&] {
     // the weight gradients: products with the tokens as K (every operand token-contiguous)

@@ -274,12 +274,18 @@ struct RouterBwdArgs {
   // encoder's pre-activation, c, the read's normaliser, p_j, dL/ds so far, dL/dnum, dL/dden,
   // [dL/dphi(k); dL/dphi(q); dL/dv], P with its K slices summed
   float *RS, *QKVU, *PPRE, *Cv, *DEN, *PS, *DSP, *DNUM, *DDEN, *DF, *PSUM;
+  // the tokens the token passes take, [t_begin, t_end) (t_begin a multiple of 16 for the chain);
+  // every token-indexed array above keeps its layout over all T tokens
+  int t_begin, t_end;
 };
 // rows of the token-contiguous operands above, per token
 size_t router_bwd_vector_floats(int d_m, int d_s, int d_h, int d_a, int d_e, int d_p, int d_head);
 // floats of the token passes' intermediates, per token
 size_t router_bwd_token_floats(int d_m, int d_s, int d_p, int np);
-hipError_t launch_router_bwd_token(const RouterBwdArgs& a, hipStream_t s);
+// the token passes over [t_begin, t_end): the row statistics (and P's slice sums), then the chain
+// F1, memory read, F2, state pass, F3; after_f1 (optional) is recorded once F1 is queued
+hipError_t launch_router_bwd_stats(const RouterBwdArgs& a, hipStream_t s);
+hipError_t launch_router_bwd_chain(const RouterBwdArgs& a, hipStream_t s, hipEvent_t after_f1);
 // the RMSNorm / transition terms of dL/dhbar, then dL/deta
 hipError_t launch_router_bwd_rows(const RouterBwdArgs& a, hipStream_t s);
 // out[c][r] = float(in[r][c])

@@ -396,8 +396,9 @@ __device__ __forceinline__ void bmv_cols(const Cols<W>& A, int nb, float* red) {
 // stats: a wave per token over the residual rows (16-byte loads) and P's slices
 template <typename T>
 __global__ __launch_bounds__(RB_NT) void rbwd_stats(RouterBwdArgs a) {
-  const int t = blockIdx.x * RB_NW + static_cast<int>(threadIdx.x) / kWave, lane = threadIdx.x & (kWave - 1);
-  if (t >= a.T) return;   // whole waves; no barrier below
+  const int t = a.t_begin + static_cast<int>(blockIdx.x) * RB_NW + static_cast<int>(threadIdx.x) / kWave;
+  const int lane = threadIdx.x & (kWave - 1);
+  if (t >= a.t_end) return;   // whole waves; no barrier below
   const int j = a.j, d = a.d;
   const T* hb = static_cast<const T*>(a.hbar) + static_cast<size_t>(t) * d;
   const T* h1 = j >= 2 ? static_cast<const T*>(a.prev1) + static_cast<size_t>(t) * d : nullptr;
@@ -455,7 +456,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f1(RouterBwdArgs a) {
   const int tid = threadIdx.x;
   const int T_ = a.T, j = a.j, DM = a.d_m, d_s = a.d_s, d_h = a.d_h, d_a = a.d_a;
   const int d_e = a.d_e, d_p = a.d_p, NP = d_e + a.d_head;
-  const int t0 = blockIdx.x * RB_TB, nb = min(RB_TB, T_ - t0);
+  const int t0 = a.t_begin + static_cast<int>(blockIdx.x) * RB_TB, nb = min(RB_TB, a.t_end - t0);
   // P's hidden part (loads first, clamped to the last element), W_p1, the path features
   constexpr int UE = (RB_TB * RB_MAXE + RB_BT - 1) / RB_BT;
   const int ne = nb * d_e;
@@ -527,7 +528,7 @@ __global__ __launch_bounds__(RB_NT) void rbwd_read(RouterBwdArgs a) {
   __shared__ float fq[DM];
   __shared__ f32x4 part[RG][CG];
   __shared__ float red[RB_NW];
-  const int t = blockIdx.x, tid = threadIdx.x, j = a.j;
+  const int t = a.t_begin + static_cast<int>(blockIdx.x), tid = threadIdx.x, j = a.j;
   const int cg = tid % CG, rg = tid / CG;
   const f32x4* S = j > 1 ? reinterpret_cast<const f32x4*>(a.S_in + static_cast<size_t>(t) * DM * DM) + cg : nullptr;
   f32x4 pre[PF];
@@ -574,7 +575,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = wave_id();
   const int T_ = a.T, j = a.j, DM = a.d_m, d_s = a.d_s, d_e = a.d_e, d_head = a.d_head;
   const int NP = d_e + d_head, d_x = d_s + DM + 1;
-  const int t0 = blockIdx.x * RB_TB, nb = min(RB_TB, T_ - t0);
+  const int t0 = a.t_begin + static_cast<int>(blockIdx.x) * RB_TB, nb = min(RB_TB, a.t_end - t0);
   // s, c, W_n s, P's head part (loads first, clamped to the last element), the heads' vectors
   {
     constexpr int US = (RB_TB * RB_MAXS + RB_BT - 1) / RB_BT, UM = (RB_TB * RB_MAXM + RB_BT - 1) / RB_BT;
@@ -736,7 +737,8 @@ __global__ __launch_bounds__(RB_NT) void rbwd_spass(RouterBwdArgs a) {
   __shared__ float sk[DM], sq[DM];
   __shared__ f32x4 dvp[RSETS][LPR];
   __shared__ float red[RB_NW];
-  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wv = wave_id(), j = a.j;
+  const int t = a.t_begin + static_cast<int>(blockIdx.x), tid = threadIdx.x, lane = tid & (kWave - 1), wv = wave_id();
+  const int j = a.j;
   const float* qkv = a.QKVU + static_cast<size_t>(t) * 4 * DM;
   for (int k = tid; k < DM; k += RB_NT) {
     fq[k] = phif_(qkv[k]);
@@ -810,7 +812,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f3(RouterBwdArgs a) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = wave_id();
   const int T_ = a.T, j = a.j, DM = a.d_m, d_s = a.d_s, d_h = a.d_h, d_a = a.d_a, d_e = a.d_e, d_p = a.d_p;
   const int NP = d_e + a.d_head;
-  const int t0 = blockIdx.x * RB_TB, nb = min(RB_TB, T_ - t0);
+  const int t0 = a.t_begin + static_cast<int>(blockIdx.x) * RB_TB, nb = min(RB_TB, a.t_end - t0);
   // dL/dq, dL/dk through phi (phi'(x) = 1 for x > 0, exp(x) otherwise), dL/dv, dL/ds so far; P's
   // hidden part waits in registers (loads first, clamped to the last element)
   constexpr int UE = (RB_TB * RB_MAXE + RB_BT - 1) / RB_BT;
@@ -1305,25 +1307,37 @@ size_t router_bwd_token_floats(int d_m, int d_s, int d_p, int np) {
   return 4 + 4 * static_cast<size_t>(d_m) + d_p + d_m + 1 + 1 + d_s + d_m + 1 + 3 * static_cast<size_t>(d_m) + np;
 }
 
-hipError_t launch_router_bwd_token(const RouterBwdArgs& a, hipStream_t s) {
-  if (a.d_e > RB_MAXE || a.d_head > RB_MAXH || a.d_s > RB_MAXS || a.d_m > RB_MAXM || a.d_p > RB_MAXP)
-    return hipErrorInvalidValue;
-  if (a.T <= 0) return hipSuccess;
-  if (a.d_m != 32 && a.d_m != 64 && a.d_m != 128 && a.d_m != 256) return hipErrorInvalidValue;
-  const unsigned nbat = static_cast<unsigned>((a.T + RB_TB - 1) / RB_TB), nt = static_cast<unsigned>(a.T);
-  const bool bf = a.dtype == 1;
-  const unsigned nst = static_cast<unsigned>((a.T + RB_NW - 1) / RB_NW);
-  hipError_t e;
-  if (bf)
+static bool router_bwd_token_shape_ok(const RouterBwdArgs& a) {
+  if (a.d_e > RB_MAXE || a.d_head > RB_MAXH || a.d_s > RB_MAXS || a.d_m > RB_MAXM || a.d_p > RB_MAXP) return false;
+  if (a.d_m != 32 && a.d_m != 64 && a.d_m != 128 && a.d_m != 256) return false;
+  return 0 <= a.t_begin && a.t_begin <= a.t_end && a.t_end <= a.T;
+}
+
+hipError_t launch_router_bwd_stats(const RouterBwdArgs& a, hipStream_t s) {
+  if (!router_bwd_token_shape_ok(a)) return hipErrorInvalidValue;
+  const int n = a.t_end - a.t_begin;
+  if (n == 0) return hipSuccess;
+  const unsigned nst = static_cast<unsigned>((n + RB_NW - 1) / RB_NW);
+  if (a.dtype == 1)
     rbwd_stats<bf16_t><<<nst, RB_NT, 0, s>>>(a);
   else
     rbwd_stats<float><<<nst, RB_NT, 0, s>>>(a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_router_bwd_chain(const RouterBwdArgs& a, hipStream_t s, hipEvent_t after_f1) {
+  if (!router_bwd_token_shape_ok(a) || (a.t_begin % RB_TB) != 0) return hipErrorInvalidValue;
+  const int n = a.t_end - a.t_begin;
+  if (n == 0) return after_f1 ? hipEventRecord(after_f1, s) : hipSuccess;
+  const unsigned nbat = static_cast<unsigned>((n + RB_TB - 1) / RB_TB), nt = static_cast<unsigned>(n);
+  const bool bf = a.dtype == 1;
+  hipError_t e;
   if (bf)
     rbwd_f1<bf16_t><<<nbat, RB_BT, 0, s>>>(a);
   else
     rbwd_f1<float><<<nbat, RB_BT, 0, s>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (after_f1 && (e = hipEventRecord(after_f1, s)) != hipSuccess) return e;
   switch (a.d_m) {
     case 32: rbwd_read<32><<<nt, RB_NT, 0, s>>>(a); break;
     case 64: rbwd_read<64><<<nt, RB_NT, 0, s>>>(a); break;
