@@ -83,7 +83,8 @@ constexpr int RB_TB = 16;              // tokens per workgroup of the batched pa
 constexpr int RB_BT = 512;             // threads of the batched passes
 constexpr int RB_BW = RB_BT / kWave;   // their waves
 constexpr int RB_RED = RB_BW * RB_TB * 64;   // floats of bmv_cols' partial sums
-constexpr int RB_PF = 8;                     // weight loads in flight per lane in the batched mat-vecs
+constexpr int RB_PF = 8;                     // weight loads in flight per lane in the transposed mat-vecs
+constexpr int RB_PP = 4;                     // pairs of k-steps in flight per lane in the row mat-vecs
 
 // The batched mat-vecs run on the fp32 matrix cores (v_mfma_f32_16x16x4f32: exact fp32 products,
 // so bf16 weights and fp32 activations keep the precision of scalar FMAs).  A product tile is the
@@ -125,6 +126,37 @@ __device__ __forceinline__ f32x4 cvt4(uint2 u) {
                __uint_as_float(u.y & 0xffff0000u)};
 }
 __device__ __forceinline__ f32x4 cvt4(f32x4 v) { return v; }
+// w[i .. i + 7] the same way (i a multiple of 8, the row pitch too): one 16-byte load in bf16
+template <typename W>
+struct Raw8;
+template <>
+struct Raw8<bf16_t> {
+  using type = u32x4;
+};
+struct F32x8 {
+  f32x4 a, b;
+};
+template <>
+struct Raw8<float> {
+  using type = F32x8;
+};
+__device__ __forceinline__ u32x4 raw8(const bf16_t* w, unsigned i) {
+  return *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(w) + i * 2u);
+}
+__device__ __forceinline__ F32x8 raw8(const float* w, unsigned i) {
+  const f32x4* p = reinterpret_cast<const f32x4*>(reinterpret_cast<const char*>(w) + i * 4u);
+  return F32x8{p[0], p[1]};
+}
+__device__ __forceinline__ f32x4 cvt8lo(u32x4 u) {
+  return f32x4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+               __uint_as_float(u.y & 0xffff0000u)};
+}
+__device__ __forceinline__ f32x4 cvt8hi(u32x4 u) {
+  return f32x4{__uint_as_float(u.z << 16), __uint_as_float(u.z & 0xffff0000u), __uint_as_float(u.w << 16),
+               __uint_as_float(u.w & 0xffff0000u)};
+}
+__device__ __forceinline__ f32x4 cvt8lo(const F32x8& v) { return v.a; }
+__device__ __forceinline__ f32x4 cvt8hi(const F32x8& v) { return v.b; }
 
 // Up to four weight matrices of one row pitch stacked by rows: stack row o is row o - m om of
 // matrix m (om rows each, a multiple of 16 when there are several; one matrix: om = its rows)
@@ -140,11 +172,11 @@ __device__ __forceinline__ Mats<W> mats1(const void* w, int rows, int ld) {
   return Mats<W>{static_cast<const W*>(w), nullptr, nullptr, nullptr, rows, ld};
 }
 
-// lane's four weights of stack row ot 16 + r (clamped to the last row) from column k, as loaded
+// lane's eight weights of stack row ot 16 + r (clamped to the last row) from column k, as loaded
 template <typename W>
-__device__ __forceinline__ typename Raw4<W>::type rows_w4(const Mats<W>& M, int O, int ot, int r, int k) {
+__device__ __forceinline__ typename Raw8<W>::type rows_w8(const Mats<W>& M, int O, int ot, int r, int k) {
   const int m = M.mat(ot * 16), o = min(ot * 16 + r, O - 1);   // a tile lies in one matrix
-  return raw4(M.base(m), static_cast<unsigned>(o - m * M.om) * M.ld + k);
+  return raw8(M.base(m), static_cast<unsigned>(o - m * M.om) * M.ld + k);
 }
 // the k >= kb steps of tile ot with scalar loads (the ragged end, or every k when the pitch is not a
 // multiple of 4)
@@ -179,58 +211,64 @@ __device__ __forceinline__ void rows_store(f32x4 acc, int O, int ot, int r, int 
 }
 
 // y[b][o] = sum_k W[o][k] x[b][k] for b < nb, o < O over a stack W (x in LDS, [RB_TB][ldx]; y in
-// LDS or global).  With a row pitch that is a multiple of 4, each lane loads its four k of a 16-k
-// step at once (slot g takes k0 + 4 g + i in its i-th product); two accumulators alternate.
+// LDS or global).  With a row pitch that is a multiple of 8, k goes in pairs of 16-k steps: over the 32
+// k of a pair, slot g takes k0 + 8 g + i in the first step's i-th product and k0 + 8 g + 4 + i in the
+// second's, so each lane loads its eight k of the pair at once (16 bytes in bf16; four lanes cover 64
+// bytes of a weight row per load).  Two accumulators alternate.
 template <typename W>
 __device__ __forceinline__ void bmv_rows(const Mats<W>& M, int O, int I, const float* x, int ldx, float* y, int ldy,
                                          int nb) {
   const int lane = threadIdx.x & (kWave - 1), r = lane & 15, g = lane >> 4, wv = wave_id();
   const int ntile = (O + 15) / 16;
   const int ntw = wv < ntile ? (ntile - 1 - wv) / RB_BW + 1 : 0;   // this wave's tiles (uniform)
-  const int nst = (M.ld & 3) == 0 ? I / 16 : 0, I16 = 16 * nst;
+  const int npr = (M.ld & 7) == 0 ? I / 32 : 0, I32 = 32 * npr;   // pairs of steps
   const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-  if (nst == 0) {
+  if (npr == 0) {
     for (int ti = 0; ti < ntw; ++ti) {
       const int ot = wv + ti * RB_BW;
       rows_store(rows_tail(M, O, ot, I, 0, x, ldx, r, g, zero), O, ot, r, g, y, ldy, nb);
     }
     return;
   }
-  // the wave's batches in sequence: batch q is batch q % nbt of its tile q / nbt
-  const int nbt = (nst + RB_PF - 1) / RB_PF, total = ntw * nbt;
-  const float* xr = x + r * ldx + 4 * g;
-  typename Raw4<W>::type cur[RB_PF];
+  // the wave's batches of RB_PP pairs in sequence: batch q is batch q % nbt of its tile q / nbt
+  const int nbt = (npr + RB_PP - 1) / RB_PP, total = ntw * nbt;
+  const float* xr = x + r * ldx + 8 * g;
+  typename Raw8<W>::type cur[RB_PP];
   if (total > 0)
 #pragma unroll
-    for (int u = 0; u < RB_PF; ++u) cur[u] = rows_w4(M, O, wv, r, 16 * min(u, nst - 1) + 4 * g);
+    for (int u = 0; u < RB_PP; ++u) cur[u] = rows_w8(M, O, wv, r, 32 * min(u, npr - 1) + 8 * g);
   f32x4 acc0 = zero, acc1 = zero;
   for (int q = 0; q < total; ++q) {
     const int ti = q / nbt, c = q - ti * nbt, ot = wv + ti * RB_BW;
-    typename Raw4<W>::type nxt[RB_PF];
+    typename Raw8<W>::type nxt[RB_PP];
     if (q + 1 < total) {   // uniform
       const int t1 = (q + 1) / nbt, c1 = q + 1 - t1 * nbt;
 #pragma unroll
-      for (int u = 0; u < RB_PF; ++u)
-        nxt[u] = rows_w4(M, O, wv + t1 * RB_BW, r, 16 * min(c1 * RB_PF + u, nst - 1) + 4 * g);
+      for (int u = 0; u < RB_PP; ++u)
+        nxt[u] = rows_w8(M, O, wv + t1 * RB_BW, r, 32 * min(c1 * RB_PP + u, npr - 1) + 8 * g);
     }
 #pragma unroll
-    for (int u = 0; u < RB_PF; ++u) {
-      const int st = c * RB_PF + u;
-      if (st < nst) {   // uniform
-        const float* xk = xr + 16 * st;
-        const f32x4 wv = cvt4(cur[u]);
-        acc0 = mfma4(xk[0], wv[0], acc0);
-        acc1 = mfma4(xk[1], wv[1], acc1);
-        acc0 = mfma4(xk[2], wv[2], acc0);
-        acc1 = mfma4(xk[3], wv[3], acc1);
+    for (int u = 0; u < RB_PP; ++u) {
+      const int pr = c * RB_PP + u;
+      if (pr < npr) {   // uniform
+        const float* xk = xr + 32 * pr;
+        const f32x4 w0 = cvt8lo(cur[u]), w1 = cvt8hi(cur[u]);
+        acc0 = mfma4(xk[0], w0[0], acc0);
+        acc1 = mfma4(xk[1], w0[1], acc1);
+        acc0 = mfma4(xk[2], w0[2], acc0);
+        acc1 = mfma4(xk[3], w0[3], acc1);
+        acc0 = mfma4(xk[4], w1[0], acc0);
+        acc1 = mfma4(xk[5], w1[1], acc1);
+        acc0 = mfma4(xk[6], w1[2], acc0);
+        acc1 = mfma4(xk[7], w1[3], acc1);
       }
     }
     if (c == nbt - 1) {   // the tile's last batch
-      rows_store(rows_tail(M, O, ot, I, I16, x, ldx, r, g, acc0 + acc1), O, ot, r, g, y, ldy, nb);
+      rows_store(rows_tail(M, O, ot, I, I32, x, ldx, r, g, acc0 + acc1), O, ot, r, g, y, ldy, nb);
       acc0 = acc1 = zero;
     }
 #pragma unroll
-    for (int u = 0; u < RB_PF; ++u) cur[u] = nxt[u];
+    for (int u = 0; u < RB_PP; ++u) cur[u] = nxt[u];
   }
 }
 
