@@ -1497,7 +1497,7 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
       // other's state streams, measured 341 against 336 us at the 8B layer: the batched passes slow
       // down under the streams' memory traffic)
       const hipError_t x = hero::launch_router_bwd_stats(a, s);
-      return x == hipSuccess ? hero::launch_router_bwd_chain(a, s, nullptr) : x;
+      return x == hipSuccess ? hero::launch_router_bwd_chain(a, s) : x;
     });
   if (e != hipSuccess) return HERO_E_LAUNCH;
   e = timed(HERO_K_ROUTER_BWD_PRODUCTS, s, [&] {

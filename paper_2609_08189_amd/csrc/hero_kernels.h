@@ -283,9 +283,9 @@ size_t router_bwd_vector_floats(int d_m, int d_s, int d_h, int d_a, int d_e, int
 // floats of the token passes' intermediates, per token
 size_t router_bwd_token_floats(int d_m, int d_s, int d_p, int np);
 // the token passes over [t_begin, t_end): the row statistics (and P's slice sums), then the chain
-// F1, memory read, F2, state pass, F3; after_f1 (optional) is recorded once F1 is queued
+// F1, memory read, F2, state pass, F3
 hipError_t launch_router_bwd_stats(const RouterBwdArgs& a, hipStream_t s);
-hipError_t launch_router_bwd_chain(const RouterBwdArgs& a, hipStream_t s, hipEvent_t after_f1);
+hipError_t launch_router_bwd_chain(const RouterBwdArgs& a, hipStream_t s);
 // the RMSNorm / transition terms of dL/dhbar, then dL/deta
 hipError_t launch_router_bwd_rows(const RouterBwdArgs& a, hipStream_t s);
 // out[c][r] = float(in[r][c])

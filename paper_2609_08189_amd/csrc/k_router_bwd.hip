@@ -1363,10 +1363,10 @@ hipError_t launch_router_bwd_stats(const RouterBwdArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_router_bwd_chain(const RouterBwdArgs& a, hipStream_t s, hipEvent_t after_f1) {
+hipError_t launch_router_bwd_chain(const RouterBwdArgs& a, hipStream_t s) {
   if (!router_bwd_token_shape_ok(a) || (a.t_begin % RB_TB) != 0) return hipErrorInvalidValue;
   const int n = a.t_end - a.t_begin;
-  if (n == 0) return after_f1 ? hipEventRecord(after_f1, s) : hipSuccess;
+  if (n == 0) return hipSuccess;
   const unsigned nbat = static_cast<unsigned>((n + RB_TB - 1) / RB_TB), nt = static_cast<unsigned>(n);
   const bool bf = a.dtype == 1;
   hipError_t e;
@@ -1375,7 +1375,6 @@ hipError_t launch_router_bwd_chain(const RouterBwdArgs& a, hipStream_t s, hipEve
   else
     rbwd_f1<float><<<nbat, RB_BT, 0, s>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (after_f1 && (e = hipEventRecord(after_f1, s)) != hipSuccess) return e;
   switch (a.d_m) {
     case 32: rbwd_read<32><<<nt, RB_NT, 0, s>>>(a); break;
     case 64: rbwd_read<64><<<nt, RB_NT, 0, s>>>(a); break;
