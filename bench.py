@@ -558,9 +558,10 @@ def bench_backward(args, w):
 RBWD_KERNELS = ("router_bwd_gemm", "router_bwd_token", "router_bwd_products", "router_bwd_rows")
 
 
-def router_backward_work(w, j):
+def router_backward_work(w, j, c_given=False):
     """Algorithmic FLOPs and HBM bytes of hero_router_backward's kernel groups for T tokens at
-    routed layer j (fp32 state; the token kernel streams S_{j-1} once and dL/dS in and out)."""
+    routed layer j (fp32 state; the token kernels stream S_{j-1} once and dL/dS in and out, and read
+    the forward's memory read c when it is handed over)."""
     T, d, dm, es = w.T, w.d, w.d_m, (2 if w.dtype == "bf16" else 4)
     NP = w.d_e + w.d_head
     splits = 4 if w.dtype == "bf16" else 1
@@ -572,7 +573,8 @@ def router_backward_work(w, j):
     return {
         "router_bwd_gemm": dict(flops=2 * T * d * NP, bytes=T * d * es + NP * d * es + splits * T * NP * 4),
         "router_bwd_token": dict(flops=0, bytes=T * ((3 if j > 1 else 2) * dm * dm * 4 + (1 + n_prev) * d * es
-                                                     + splits * NP * 4 + (2 * NP + vec + 8) * 4)),
+                                                     + splits * NP * 4 + (2 * NP + vec + 8) * 4
+                                                     + (dm * 4 if c_given and j > 1 else 0))),
         "router_bwd_products": dict(flops=4 * T * NP * d + small, bytes=(2 * NP + vec) * T * 4 + T * d * (es + 4)
                                     + 2 * T * d * 4),
         "router_bwd_rows": dict(flops=0, bytes=T * d * ((1 + n_prev) * es + 2 * (1 + n_prev) * 4)),
@@ -602,14 +604,15 @@ def bench_router_backward(args, w):
     dph = rng.standard_normal(T).astype(np.float32)
     dmh = rng.standard_normal(T).astype(np.float32)
     dp = DeviceProblem(prob, stats=False)
-    rb = DeviceRouterBackward(dp, j, dl, dS, dz, dph, dmh)
+    c_given = not args.reread_c
+    rb = DeviceRouterBackward(dp, j, dl, dS, dz, dph, dmh, c_from_forward=c_given)
     stream = dp.stream()
     ev = HipEvents()
     for _ in range(1 + args.warmup):
         rb.run()
     torch.cuda.synchronize()
     K = args.steps
-    works = router_backward_work(w, j)
+    works = router_backward_work(w, j, c_given)
     per, handles = {}, {}
     for name in RBWD_KERNELS:
         handles[name] = (ev.create(K), ev.create(K))
@@ -652,13 +655,17 @@ def bench_router_backward(args, w):
     else:
         achieved, peak, unit, bound = works[dom]["bytes"] / (dom_ms * 1e-3) * 1e-9, PEAK_HBM_GBS, "GB/s", "hbm"
         wpl = "per token: S_{j-1} read, dL/dS read and written (4 d_m^2 B each), rows and vectors"
+        if c_given:
+            wpl += ", the forward's memory read c"
     result = {
         "metric": "router backward tokens/sec at Llama-3.1-8B shape; % roofline",
         "value": round(T / (ms_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": (f"backward of the router (Sec. 3.2 in reverse) at {describe(w, j)}; dL/dlogit "
-                                f"N(0,1), carried dL/dS N(0,0.05^2), dL/dzeta N(0,0.1^2), dL/dp, dL/dm N(0,1)"),
+                                f"N(0,1), carried dL/dS N(0,0.05^2), dL/dzeta N(0,0.1^2), dL/dp, dL/dm N(0,1); "
+                                + ("the forward's memory read c handed over" if c_given
+                                   else "the memory read c recomputed from S_{j-1}")),
                    "global_batch": w.batch, "seq_len": w.seq, "tokens": T, "parallelism": "none"},
         "roofline": {"bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": unit,
                      "frac": round(achieved / peak, 4), "traffic": None, "kernel": dom,
@@ -1067,6 +1074,9 @@ def main():
                     help="time the backward of the routed block (training side) instead of the forward")
     ap.add_argument("--router-backward", action="store_true",
                     help="time the backward of the router at the workload's routed layer instead")
+    ap.add_argument("--reread-c", action="store_true",
+                    help="with --router-backward: recompute the memory read from S_{j-1} instead of taking "
+                         "the forward's (hero_state.c_read)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-layer-point", action="store_true",
                     help="skip the single-layer measurement that accompanies the stack line")

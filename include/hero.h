@@ -130,12 +130,20 @@ typedef struct hero_router_weights {
   const void *th1, *th2, *ps1, *ps2;
 } hero_router_weights;
 
-/* Per-token router state (fp32), read and written in place. */
+/* Per-token router state (fp32), read and written in place.
+ * c_read (optional, NULL when unused): the layer's memory read c_j = phi(q)^T S_{j-1} /
+ * (phi(q)^T zeta_{j-1} + eps) (eq:memory_read), [T][d_m] fp32, 16-byte aligned, disjoint from every
+ * other buffer of the call.  hero_routed_layer and hero_routed_layer_noalloc write it when set (with
+ * the full router; an ablation without the memory read leaves it untouched); the stack and decoder
+ * calls do not use it.  hero_router_backward reads it, when set and j >= 2, in place of re-reading
+ * S_{j-1} for the read, so a training caller that keeps each layer's c (d_m floats per token) saves
+ * the backward one of its four passes over the d_m x d_m state. */
 typedef struct hero_state {
   void *S;        /* [T][d_m][d_m], fp32 or bf16 (dims.state_dtype) */
   float *zeta;    /* [T][d_m]      */
   float *p_hist;  /* [T]           */
   float *m_hist;  /* [T]           */
+  float *c_read;  /* [T][d_m] or NULL */
 } hero_state;
 
 /*
@@ -555,7 +563,9 @@ int hero_router_backward_workspace_size(const hero_dims *dims, int T, size_t *by
  *   - turns carry into the gradient over the state the layer received.
  * state_in is the router state entering layer j (fp32 S, zeta, p, m as the forward call read
  * them; not read at j = 1, where the state is the initial one and may be NULL, and carry's
- * return there is rho dL/dS_1).
+ * return there is rho dL/dS_1).  Its c_read, when set (j >= 2), is the forward's memory read of
+ * this layer, used instead of reading S_{j-1} a second time; it must not overlap the workspace or
+ * any buffer the call writes.
  * hbar_prev1 / hbar_prev2: as in hero_routed_layer.  The full router with S in fp32
  * (dims->state_dtype HERO_F32, else HERO_E_UNSUPPORTED); branch decisions are constants.
  * Deterministic: every sum runs in a fixed order.

@@ -147,8 +147,25 @@ int check_weights(const hero_ffn_weights* f, const hero_router_weights* r, const
 
 int check_state(const hero_state* s) {
   if (!s || !s->S || !s->zeta || !s->p_hist || !s->m_hist) return HERO_E_NULL;
-  if (!aligned16(s->S) || !aligned16(s->zeta) || !aligned16(s->p_hist) || !aligned16(s->m_hist))
+  if (!aligned16(s->S) || !aligned16(s->zeta) || !aligned16(s->p_hist) || !aligned16(s->m_hist) ||
+      (s->c_read && !aligned16(s->c_read)))
     return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
+// the optional memory-read output (hero_state.c_read) may not overlap the state, the layer's
+// activations or the workspace
+int check_c_read(const hero_dims& d, int T, const hero_state* s, const void* hbar, const void* hbar_prev1,
+                 const void* hbar_prev2, const void* h_out, const void* ws, size_t ws_bytes) {
+  if (!s->c_read) return HERO_OK;
+  const size_t t = static_cast<size_t>(T), dm = static_cast<size_t>(d.d_m), cb = t * dm * 4;
+  const size_t sb = t * dm * dm * (d.state_dtype == HERO_BF16 ? 2 : 4);
+  const size_t hb = t * static_cast<size_t>(d.d) * (d.dtype == HERO_BF16 ? 2 : 4);
+  const void* c = s->c_read;
+  if (overlap(c, cb, s->S, sb) || overlap(c, cb, s->zeta, t * dm * 4) || overlap(c, cb, s->p_hist, t * 4) ||
+      overlap(c, cb, s->m_hist, t * 4) || overlap(c, cb, hbar, hb) || overlap(c, cb, hbar_prev1, hb) ||
+      overlap(c, cb, hbar_prev2, hb) || overlap(c, cb, h_out, hb) || overlap(c, cb, ws, ws_bytes))
+    return HERO_E_ALIAS;
   return HERO_OK;
 }
 
@@ -252,6 +269,8 @@ struct LayerCall {
   const float* hw = nullptr;
   // the second stream (null: every launch on the call's stream)
   const Side* side = nullptr;
+  // where the layer's memory read c goes as well (null: nowhere)
+  float* c_read = nullptr;
 };
 
 // rho_l = sigma(eta_l); w[i] = prod_{l=i+2}^{j-1} rho_l is the weight of entry i (routed layer
@@ -374,6 +393,10 @@ int run_layer(const LayerCall& c) {
       return c.hist ? launch_router_mem_hist(ra, st) : launch_router_mem(ra, st);
     });
     if (e != hipSuccess) return HERO_E_LAUNCH;
+    if (c.c_read &&
+        hipMemcpyAsync(c.c_read, ra.cvec, static_cast<size_t>(T) * D.d_m * sizeof(float), hipMemcpyDeviceToDevice,
+                       st) != hipSuccess)
+      return HERO_E_LAUNCH;
   }
   e = timed(HERO_K_ROUTER_POST, st, [&] { return launch_router_post(ra, st); });
   if (e != hipSuccess) return HERO_E_LAUNCH;
@@ -564,11 +587,15 @@ int hero_routed_layer(const hero_dims* dims, int j, int T, const void* hbar, con
   if (st != HERO_OK) return st;
   if ((st = check_state(state)) != HERO_OK) return st;
   if (!(eta == eta)) return HERO_E_RANGE;
+  if ((st = check_c_read(*dims, T, state, hbar, j >= 2 ? hbar_prev1 : nullptr, j >= 3 ? hbar_prev2 : nullptr,
+                         h_out, workspace, L.total)) != HERO_OK)
+    return st;
   if ((st = check_device()) != HERO_OK) return st;
   LayerCall c{dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, state, ffn, router, adapter, eta,
               routing, stats, static_cast<unsigned char*>(workspace), &L,
               static_cast<hipStream_t>(stream)};
   c.side = side_of_current_device();
+  c.c_read = state->c_read;
   return run_layer(c);
 }
 
@@ -587,8 +614,12 @@ int hero_routed_layer_noalloc(const hero_dims* dims, int j, int T, const void* h
   if ((st = check_device()) != HERO_OK) return st;
   void* scratch = nullptr;
   if ((st = scratch_of_current_device(&scratch)) != HERO_OK) return st;
+  if ((st = check_c_read(*dims, T, state, hbar, j >= 2 ? hbar_prev1 : nullptr, j >= 3 ? hbar_prev2 : nullptr,
+                         h_out, scratch, L.total)) != HERO_OK)
+    return st;
   LayerCall c{dims, j, T, hbar, hbar_prev1, hbar_prev2, h_out, state, ffn, router, adapter, eta,
               routing, stats, static_cast<unsigned char*>(scratch), &L, static_cast<hipStream_t>(stream)};
+  c.c_read = state->c_read;
   return run_layer(c);
 }
 
@@ -1386,6 +1417,13 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
                           {j >= 2 ? dhbar_prev1 : nullptr, hb}, {j >= 3 ? dhbar_prev2 : nullptr, hb}, {deta, 4}};
   for (const Span& x : written)
     if (overlap(workspace, L.total, x.p, x.bytes)) return HERO_E_ALIAS;
+  // the forward's memory read, when given, is read after several of these are written
+  const float* c_in = j > 1 && state_in ? state_in->c_read : nullptr;
+  if (c_in) {
+    if (overlap(c_in, zb, workspace, L.total)) return HERO_E_ALIAS;
+    for (const Span& x : written)
+      if (overlap(c_in, zb, x.p, x.bytes)) return HERO_E_ALIAS;
+  }
   if ((st = check_device()) != HERO_OK) return st;
 
   const hipStream_t s = static_cast<hipStream_t>(stream);
@@ -1480,6 +1518,10 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
   a.PSUM = per_token(NP);
   a.t_begin = 0;
   a.t_end = T;
+  if (c_in) {
+    a.Cv = const_cast<float*>(c_in);   // read only: the memory read pass is skipped
+    a.c_given = 1;
+  }
   a.dhbar = dhbar;
   a.dhbar1 = dhbar_prev1;
   a.dhbar2 = dhbar_prev2;

@@ -277,6 +277,9 @@ struct RouterBwdArgs {
   // the tokens the token passes take, [t_begin, t_end) (t_begin a multiple of 16 for the chain);
   // every token-indexed array above keeps its layout over all T tokens
   int t_begin, t_end;
+  // nonzero: Cv holds the forward's memory read (j >= 2); the read pass is skipped and F2 forms
+  // the normaliser phi(q)^T zeta_{j-1} + eps itself
+  int c_given;
 };
 // rows of the token-contiguous operands above, per token
 size_t router_bwd_vector_floats(int d_m, int d_s, int d_h, int d_a, int d_e, int d_p, int d_head);

@@ -609,6 +609,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
   __shared__ float red[RB_RED];
   __shared__ float hv[3][RB_MAXH];    // th1's nu column, th2, psi_2
   __shared__ float nrm[RB_TB][4];     // n1, n2, nn, Dc
+  __shared__ float dens[RB_TB];       // the memory read's normaliser
   __shared__ float dab[RB_TB][2];     // dL/da, dL/db
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = wave_id();
   const int T_ = a.T, j = a.j, DM = a.d_m, d_s = a.d_s, d_e = a.d_e, d_head = a.d_head;
@@ -673,6 +674,16 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
   // p = sigma(a / T_hist); dL/da, dL/db; dL/dP's head part in its token-major row
   for (int b = wv; b < nb; b += RB_BW) {
     const int t = t0 + b;
+    float den;
+    if (a.c_given) {   // phi(q)^T zeta_{j-1} + eps (j >= 2), as the read pass forms it
+      const float* q = a.QKVU + static_cast<size_t>(t) * 4 * DM;
+      const float* z = a.zeta_in + static_cast<size_t>(t) * DM;
+      float dz = 0.0f;
+      for (int k = lane; k < DM; k += kWave) dz = fmaf(phif_(q[k]), z[k], dz);
+      den = wave_sum(dz) + a.eps;
+    } else {
+      den = a.DEN[t];
+    }
     float n1 = 0.0f, n2 = 0.0f, nn = 0.0f;
     for (int k = lane; k < DM; k += kWave) {
       n1 = fmaf(u1[b][k], u1[b][k], n1);
@@ -698,6 +709,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
     for (int o = lane; o < d_head; o += kWave)
       a.dP[static_cast<size_t>(t) * NP + d_e + o] = dl * hv[2][o] * silu_grad_(dxth[b][o]);
     if (lane == 0) {
+      dens[b] = den;
       nrm[b][0] = n1;
       nrm[b][1] = n2;
       nrm[b][2] = nn;
@@ -750,7 +762,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
   // the read's normaliser: dL/dnum = dc / den, dL/dden = -<dc, c> / den (no read at j = 1)
   for (int b = wv; b < nb; b += RB_BW) {
     const int t = t0 + b;
-    const float den = a.DEN[t];
+    const float den = dens[b];
     float dden = 0.0f;
     for (int v = lane; v < DM; v += kWave) {
       a.DNUM[static_cast<size_t>(t) * DM + v] = j > 1 ? dxth[b][d_s + v] / den : 0.0f;
@@ -1375,13 +1387,15 @@ hipError_t launch_router_bwd_chain(const RouterBwdArgs& a, hipStream_t s) {
   else
     rbwd_f1<float><<<nbat, RB_BT, 0, s>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  switch (a.d_m) {
-    case 32: rbwd_read<32><<<nt, RB_NT, 0, s>>>(a); break;
-    case 64: rbwd_read<64><<<nt, RB_NT, 0, s>>>(a); break;
-    case 128: rbwd_read<128><<<nt, RB_NT, 0, s>>>(a); break;
-    default: rbwd_read<256><<<nt, RB_NT, 0, s>>>(a); break;
+  if (!a.c_given) {
+    switch (a.d_m) {
+      case 32: rbwd_read<32><<<nt, RB_NT, 0, s>>>(a); break;
+      case 64: rbwd_read<64><<<nt, RB_NT, 0, s>>>(a); break;
+      case 128: rbwd_read<128><<<nt, RB_NT, 0, s>>>(a); break;
+      default: rbwd_read<256><<<nt, RB_NT, 0, s>>>(a); break;
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
   if (bf)
     rbwd_f2<bf16_t><<<nbat, RB_BT, 0, s>>>(a);
   else

@@ -381,12 +381,28 @@ class DeviceBackward:
 class DeviceRouterBackward:
     """The router's backward at routed layer j on the GPU, on a DeviceProblem's inputs (its hbar,
     hbar_{j-1}, hbar_{j-2}, router weights and the state entering the layer), given dL/dlogit and
-    the carried state gradient; the fp32 gradient buffers start at zero."""
+    the carried state gradient; the fp32 gradient buffers start at zero.  With c_from_forward (j >= 2)
+    the layer's forward runs once first, on a copy of the entering state, with hero_state.c_read set,
+    and the backward is handed that memory read in place of reading S_{j-1} for it again."""
 
     def __init__(self, dp: "DeviceProblem", j: int, dlogit: np.ndarray, dS: np.ndarray, dzeta: np.ndarray,
-                 dp_hist: np.ndarray, dm_hist: np.ndarray):
+                 dp_hist: np.ndarray, dm_hist: np.ndarray, c_from_forward: bool = False):
         w, dev, T = dp.w, dp.device, dp.T
         self.dp_, self.j, self.T, self.w = dp, j, T, w
+        self.c_read = None
+        self.state_s = dp.state_s
+        if c_from_forward and j >= 2:
+            self.c_read = torch.full((T, w.d_m), float("nan"), dtype=torch.float32, device=dev)
+            S, z, p, m = (x.clone() for x in (dp.S, dp.zeta, dp.p_hist, dp.m_hist))
+            st = H.hero_state(S.data_ptr(), z.data_ptr(), p.data_ptr(), m.data_ptr(), self.c_read.data_ptr())
+            out = torch.empty_like(dp.h_out)
+            H.check(H.hero_routed_layer(dp.dims, j, T, dp.hbar, dp.prev1, dp.prev2, out, st, dp.ffn_s[0],
+                                        dp.router_s, dp.adapter_s[0], dp.eta[j - 1], dp.routing_s, None, dp.ws,
+                                        dp.ws_bytes, dp.stream()), "hero_routed_layer")
+            torch.cuda.synchronize()
+            del S, z, p, m, out
+            self.state_s = H.hero_state(dp.S.data_ptr(), dp.zeta.data_ptr(), dp.p_hist.data_ptr(),
+                                        dp.m_hist.data_ptr(), self.c_read.data_ptr())
         f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
         zeros = lambda *shape: torch.zeros(*shape, dtype=torch.float32, device=dev)
         self.dlogit = f32(dlogit)
@@ -403,7 +419,7 @@ class DeviceRouterBackward:
     def run(self) -> None:
         dp, j = self.dp_, self.j
         H.check(H.hero_router_backward(dp.dims, j, self.T, dp.hbar, dp.prev1 if j >= 2 else None,
-                                       dp.prev2 if j >= 3 else None, dp.state_s, dp.router_s, dp.eta[j - 1],
+                                       dp.prev2 if j >= 3 else None, self.state_s, dp.router_s, dp.eta[j - 1],
                                        self.dlogit, self.carry_s, self.dh[0], self.dh[1] if j >= 2 else None,
                                        self.dh[2] if j >= 3 else None, self.grads_s, self.deta, self.ws,
                                        self.ws_bytes, dp.stream()), "hero_router_backward")

@@ -76,7 +76,7 @@ class hero_router_weights(ctypes.Structure):
 
 
 class hero_state(ctypes.Structure):
-    _fields_ = [("S", _vp), ("zeta", _vp), ("p_hist", _vp), ("m_hist", _vp)]
+    _fields_ = [("S", _vp), ("zeta", _vp), ("p_hist", _vp), ("m_hist", _vp), ("c_read", _vp)]
 
 
 class hero_router_grads(ctypes.Structure):

@@ -225,6 +225,23 @@ def test_no_device_means_device_error():
     assert call_layer() == H.HERO_E_DEVICE
 
 
+def test_memory_read_output_validates():
+    """hero_state.c_read (the layer's memory read, T x d_m fp32) must be 16-byte aligned and may not
+    overlap the state, the activations or the workspace; a disjoint one passes the host checks."""
+    import torch
+    _, _, _, st = fake_structs()
+    with_c = lambda c: H.hero_state(st.S, st.zeta, st.p_hist, st.m_hist, c)
+    assert call_layer(state=with_c(FAKE + (6 << 30) + 4)) == H.HERO_E_ALIGN
+    assert call_layer(state=with_c(FAKE + (4 << 30) + 256)) == H.HERO_E_ALIAS    # inside h_out
+    assert call_layer(state=with_c(FAKE + (1 << 30))) == H.HERO_E_ALIAS          # is hbar
+    assert call_layer(state=with_c(FAKE + (8 << 30) + 4096)) == H.HERO_E_ALIAS   # inside the workspace
+    assert call_layer(state=with_c(st.zeta)) == H.HERO_E_ALIAS
+    # hbar_prev2 is not read at j = 2, so a c_read over it is no overlap there
+    assert call_layer(j=2, state=with_c(FAKE + (3 << 30))) != H.HERO_E_ALIAS
+    if torch.cuda.device_count() == 0:
+        assert call_layer(state=with_c(FAKE + (6 << 30))) == H.HERO_E_DEVICE
+
+
 def test_history_entry_points_validate():
     dims = good_dims()
     ffn, ad, rt, st = fake_structs()
@@ -416,6 +433,19 @@ def test_router_backward_entry_validates():
     # the received state is not read at j = 1 and may be absent there, not later
     assert call(j=1, st=None, h1=None, h2=None, dh1=None, dh2=None, ws=None) == H.HERO_E_WORKSPACE
     assert call(j=2, st=None) == H.HERO_E_NULL
+    # the forward's memory read, handed in as state_in.c_read, is read after outputs are written
+    with_c = lambda c: H.hero_state(st.S, st.zeta, st.p_hist, st.m_hist, c)
+    assert call(st=with_c(FAKE + 8)) == H.HERO_E_ALIGN
+    assert call(st=with_c(carry.dzeta)) == H.HERO_E_ALIAS
+    dh = at()
+    assert call(dh=dh, st=with_c(dh + 1024)) == H.HERO_E_ALIAS
+    ws = at()
+    assert call(ws=ws, st=with_c(ws + need - 16)) == H.HERO_E_ALIAS
+    # not read at j = 1
+    assert call(j=1, st=with_c(carry.dzeta), h1=None, h2=None, dh1=None, dh2=None) != H.HERO_E_ALIAS
+    import torch
+    if torch.cuda.device_count() == 0:
+        assert call(st=with_c(at())) == H.HERO_E_DEVICE
 
 
 def test_noalloc_rejects_a_call_beyond_its_scratch_before_any_launch():

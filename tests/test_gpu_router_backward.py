@@ -27,10 +27,11 @@ def _err(x, ref):
     return float(np.max(np.abs(x - ref)) / max(np.max(np.abs(ref)), 1e-30))
 
 
-def _run(w, j, seed):
+def _run(w, j, seed, c_from_forward=False):
     import torch
     from paper_2609_08189_amd.device import DeviceProblem, DeviceRouterBackward
-    print(f"case {w.name} dtype={w.dtype} j={j} T={w.T} d={w.d} d_m={w.d_m} d_s={w.d_s} seed={seed}", flush=True)
+    print(f"case {w.name} dtype={w.dtype} j={j} T={w.T} d={w.d} d_m={w.d_m} d_s={w.d_s} seed={seed} "
+          f"c_from_forward={c_from_forward}", flush=True)
     prob = synth.make_problem(w, seed=seed, layer_j=j)
     T, dm = w.T, w.d_m
     rng = np.random.default_rng(seed + 1000)
@@ -40,7 +41,8 @@ def _run(w, j, seed):
     dph = rng.standard_normal(T).astype(np.float32)
     dmh = rng.standard_normal(T).astype(np.float32)
     dp = DeviceProblem(prob, stats=False)
-    rb = DeviceRouterBackward(dp, j, dl, dS, dz, dph, dmh)
+    rb = DeviceRouterBackward(dp, j, dl, dS, dz, dph, dmh, c_from_forward=c_from_forward)
+    c_gpu = rb.c_read.cpu().numpy().astype(np.float64) if rb.c_read is not None else None
     rb.run()
     res = rb.results()
     del rb, dp
@@ -60,6 +62,10 @@ def _run(w, j, seed):
         j, dims, hb, h1, h2, state, fwd, R, dl.astype(np.float64), dS.astype(np.float64),
         dz.astype(np.float64), dph.astype(np.float64), dmh.astype(np.float64), G)
     rho = fwd.debug["rho"]
+    if c_from_forward and j >= 2:
+        errs_c = _err(c_gpu, fwd.debug["c"])
+        print(f"  forward memory read c: {errs_c:.2e}", flush=True)
+        assert errs_c <= TOL, f"c_read: {errs_c:.3e}"
     errs = {"dhbar": _err(res["dhbar"], dhb), "deta": abs(res["deta"] - drho * rho * (1 - rho)) /
             max(abs(drho * rho * (1 - rho)), 1e-30), "dp": _err(res["dp"], dp_p), "dm": _err(res["dm"], dm_p)}
     if j >= 2:
@@ -118,6 +124,20 @@ def test_router_backward_llama31_8b_layer_full_shape():
     every token, every weight gradient."""
     w = synth.WORKLOADS["llama31_8b_layer"]
     _run(w, w.layer_j, seed=3)
+
+
+@pytest.mark.parametrize("w,j", [(BF16, 2), (BF16, 3), (BF16, 6), (F32, 4), (BF16.replace(T=1), 4),
+                                 (BF16.replace(d_m=256, T=129), 3)],
+                         ids=["bf16-j2", "bf16-j3", "bf16-j6", "f32-j4", "one-token", "d_m256"])
+def test_router_backward_with_the_forwards_memory_read(w, j):
+    """The layer's forward writes its memory read c to hero_state.c_read and the backward takes it
+    instead of reading S_{j-1} for it a second time: c itself and every gradient to the same bar."""
+    _run(w, j, seed=50 + j, c_from_forward=True)
+
+
+def test_router_backward_llama31_8b_layer_with_the_forwards_memory_read():
+    w = synth.WORKLOADS["llama31_8b_layer"]
+    _run(w, w.layer_j, seed=4, c_from_forward=True)
 
 
 def test_router_backward_first_layer_without_state():
