@@ -34,16 +34,43 @@ constexpr int RB_NT = 256;
 constexpr int RB_NW = RB_NT / kWave;
 constexpr int RB_MAXE = 256, RB_MAXH = 256, RB_MAXS = 128, RB_MAXM = 256, RB_MAXP = 128;
 constexpr int RB_MAXX = RB_MAXS + RB_MAXM + 1;
+constexpr int RB_MAXSPL = 4;                            // K-slice partials of P at most
+constexpr int RB_PQ = (RB_MAXE + RB_MAXH) / 4 / 64;     // float4s of a P row per lane
 
-__device__ __forceinline__ float silu_grad_(float x) {
-  const float s = sigmoidf_(x);
+// The activations on the hardware's exp2 and reciprocal (a few ulp each).  The library forms take a
+// range-reduced exp and a correctly rounded division, several times the instructions, and the
+// elementwise phases of the batched passes are bound by instruction issue.
+__device__ __forceinline__ float exp_hw(float x) { return __builtin_amdgcn_exp2f(x * 1.44269504088896341f); }
+__device__ __forceinline__ float sigmoid_hw(float x) { return __builtin_amdgcn_rcpf(1.0f + exp_hw(-x)); }
+__device__ __forceinline__ float silu_hw(float x) { return x * sigmoid_hw(x); }
+__device__ __forceinline__ float silu_grad_hw(float x) {
+  const float s = sigmoid_hw(x);
   return s * (1.0f + x * (1.0f - s));
 }
-__device__ __forceinline__ float phi_grad_(float x) { return x > 0.0f ? 1.0f : expf(x); }
+__device__ __forceinline__ float phi_hw(float x) { return x > 0.0f ? x + 1.0f : exp_hw(x); }   // ELU(x) + 1
+__device__ __forceinline__ float phi_grad_hw(float x) { return x > 0.0f ? 1.0f : exp_hw(x); }
+
+// Sum over the wave's 64 lanes (all active), every lane gets the same bits: within each 16-lane
+// row by DPP moves (the two quad swaps, then the half-row and row mirrors, each lane adding the
+// same pair), then the four row sums read out and added as (r0 + r1) + (r2 + r3).  A chain of
+// LDS permutes would cost several times the latency.
+template <int CTRL>
+__device__ __forceinline__ float dpp_movf(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  v += dpp_movf<0xB1>(v);    // quad_perm [1, 0, 3, 2]
+  v += dpp_movf<0x4E>(v);    // quad_perm [2, 3, 0, 1]
+  v += dpp_movf<0x141>(v);   // row_half_mirror
+  v += dpp_movf<0x140>(v);   // row_mirror
+  const int b = __float_as_int(v);
+  auto row = [b](int l) { return __int_as_float(__builtin_amdgcn_readlane(b, l)); };
+  return (row(0) + row(16)) + (row(32) + row(48));
+}
 
 // sum over the workgroup (every thread calls it; every thread gets the result, the same bits)
 __device__ float block_sum(float v, float* red) {
-  v = wave_sum(v);
+  v = wave_sum_dpp(v);
   __syncthreads();
   if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = v;
   __syncthreads();
@@ -434,38 +461,68 @@ __device__ __forceinline__ void bmv_cols(const Cols<W>& A, int nb, float* red) {
 // stats: a wave per token over the residual rows (16-byte loads) and P's slices
 template <typename T>
 __global__ __launch_bounds__(RB_NT) void rbwd_stats(RouterBwdArgs a) {
+  constexpr int SB = 4;   // 8-element chunks of each row per lane in flight
+  using R8 = typename Raw8<T>::type;
   const int t = a.t_begin + static_cast<int>(blockIdx.x) * RB_NW + static_cast<int>(threadIdx.x) / kWave;
   const int lane = threadIdx.x & (kWave - 1);
   if (t >= a.t_end) return;   // whole waves; no barrier below
-  const int j = a.j, d = a.d;
-  const T* hb = static_cast<const T*>(a.hbar) + static_cast<size_t>(t) * d;
-  const T* h1 = j >= 2 ? static_cast<const T*>(a.prev1) + static_cast<size_t>(t) * d : nullptr;
-  const T* h2 = j >= 3 ? static_cast<const T*>(a.prev2) + static_cast<size_t>(t) * d : nullptr;
-  float s2 = 0.0f, dd = 0.0f, dpv = 0.0f, pp2 = 0.0f;
-#pragma unroll 2
-  for (int i = lane * 8; i < d; i += kWave * 8) {
-    float x[8], y[8], z[8];
-    ld8(hb + i, x);
-    if (j >= 2) ld8(h1 + i, y);
-    if (j >= 3) ld8(h2 + i, z);
+  const int j = a.j, d = a.d, NP = a.d_e + a.d_head, T_ = a.T, ns = a.p_splits;
+  // P's K slices (float4 rows when NP allows), in flight with the rows' first batch
+  const bool v4 = (NP & 3) == 0;
+  f32x4 pv[RB_PQ][RB_MAXSPL];
+  if (v4) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      s2 = fmaf(x[u], x[u], s2);
-      if (j >= 2) {
-        const float del = x[u] - y[u];
-        dd = fmaf(del, del, dd);
-        if (j >= 3) {
-          const float dp_ = y[u] - z[u];
-          dpv = fmaf(del, dp_, dpv);
-          pp2 = fmaf(dp_, dp_, pp2);
+    for (int u = 0; u < RB_PQ; ++u) {
+      const int q = lane + u * kWave;
+#pragma unroll
+      for (int z = 0; z < RB_MAXSPL; ++z)
+        pv[u][z] = 4 * q < NP && z < ns
+                       ? *reinterpret_cast<const f32x4*>(a.P + (static_cast<size_t>(z) * T_ + t) * NP + 4 * q)
+                       : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+  }
+  const T* hb = static_cast<const T*>(a.hbar) + static_cast<size_t>(t) * d;
+  const T* h1 = j >= 2 ? static_cast<const T*>(a.prev1) + static_cast<size_t>(t) * d : hb;
+  const T* h2 = j >= 3 ? static_cast<const T*>(a.prev2) + static_cast<size_t>(t) * d : hb;
+  float s2 = 0.0f, dd = 0.0f, dpv = 0.0f, pp2 = 0.0f;
+  for (int i0 = lane * 8; i0 < d; i0 += kWave * 8 * SB) {
+    R8 x[SB], y[SB], z[SB];
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      const int i = min(i0 + u * kWave * 8, d - 8);   // a clamped chunk is loaded but not used
+      x[u] = raw8(hb, static_cast<unsigned>(i));
+      if (j >= 2) y[u] = raw8(h1, static_cast<unsigned>(i));
+      if (j >= 3) z[u] = raw8(h2, static_cast<unsigned>(i));
+    }
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      if (i0 + u * kWave * 8 >= d) break;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const f32x4 xv = h ? cvt8hi(x[u]) : cvt8lo(x[u]);
+        f32x4 yv = xv, zv = xv;
+        if (j >= 2) yv = h ? cvt8hi(y[u]) : cvt8lo(y[u]);
+        if (j >= 3) zv = h ? cvt8hi(z[u]) : cvt8lo(z[u]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          s2 = fmaf(xv[e], xv[e], s2);
+          if (j >= 2) {
+            const float del = xv[e] - yv[e];
+            dd = fmaf(del, del, dd);
+            if (j >= 3) {
+              const float dp_ = yv[e] - zv[e];
+              dpv = fmaf(del, dp_, dpv);
+              pp2 = fmaf(dp_, dp_, pp2);
+            }
+          }
         }
       }
     }
   }
-  s2 = wave_sum(s2);
-  dd = wave_sum(dd);
-  dpv = wave_sum(dpv);
-  pp2 = wave_sum(pp2);
+  s2 = wave_sum_dpp(s2);
+  dd = wave_sum_dpp(dd);
+  dpv = wave_sum_dpp(dpv);
+  pp2 = wave_sum_dpp(pp2);
   if (lane == 0) {
     float* rs = a.RS + static_cast<size_t>(t) * 4;
     rs[0] = 1.0f / sqrtf(s2 / static_cast<float>(d) + a.eps_norm);
@@ -474,11 +531,23 @@ __global__ __launch_bounds__(RB_NT) void rbwd_stats(RouterBwdArgs a) {
     rs[3] = dpv;
   }
   // P's K slices added in slice order, once for the three batched passes
-  const int NP = a.d_e + a.d_head, T_ = a.T;
-  for (int k = lane; k < NP; k += kWave) {
-    float v = 0.0f;
-    for (int z = 0; z < a.p_splits; ++z) v += a.P[(static_cast<size_t>(z) * T_ + t) * NP + k];
-    a.PSUM[static_cast<size_t>(t) * NP + k] = v;
+  if (v4) {
+#pragma unroll
+    for (int u = 0; u < RB_PQ; ++u) {
+      const int q = lane + u * kWave;
+      if (4 * q >= NP) break;
+      f32x4 v = pv[u][0];
+#pragma unroll
+      for (int z = 1; z < RB_MAXSPL; ++z)
+        if (z < ns) v += pv[u][z];
+      *reinterpret_cast<f32x4*>(a.PSUM + static_cast<size_t>(t) * NP + 4 * q) = v;
+    }
+  } else {
+    for (int k = lane; k < NP; k += kWave) {
+      float v = 0.0f;
+      for (int z = 0; z < ns; ++z) v += a.P[(static_cast<size_t>(z) * T_ + t) * NP + k];
+      a.PSUM[static_cast<size_t>(t) * NP + k] = v;
+    }
   }
 }
 
@@ -523,7 +592,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f1(RouterBwdArgs a) {
 #pragma unroll
   for (int u = 0; u < UE; ++u) {
     const int e = tid + u * RB_BT, b = e / d_e, k = e % d_e;
-    if (e < ne) sh[b][k] = siluf_(irs[b] * ph[u]);
+    if (e < ne) sh[b][k] = silu_hw(irs[b] * ph[u]);
   }
   for (int e = tid; e < nb * d_p; e += RB_BT) {
     const int b = e / d_p, o = e % d_p;
@@ -531,7 +600,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f1(RouterBwdArgs a) {
 #pragma unroll
     for (int k = 0; k < 6; ++k) pre = fmaf(wp1[o * 6 + k], xp[b][k], pre);
     a.PPRE[static_cast<size_t>(t0 + b) * d_p + o] = pre;
-    pp[b][o] = siluf_(pre);
+    pp[b][o] = silu_hw(pre);
   }
   __syncthreads();
   for (int e = tid; e < nb * d_p; e += RB_BT) {
@@ -573,7 +642,7 @@ __global__ __launch_bounds__(RB_NT) void rbwd_read(RouterBwdArgs a) {
   if (S)
 #pragma unroll
     for (int u = 0; u < PF; ++u) pre[u] = __builtin_nontemporal_load(S + static_cast<size_t>(rg + u * RG) * CG);
-  for (int k = tid; k < DM; k += RB_NT) fq[k] = phif_(a.QKVU[static_cast<size_t>(t) * 4 * DM + k]);
+  for (int k = tid; k < DM; k += RB_NT) fq[k] = phi_hw(a.QKVU[static_cast<size_t>(t) * 4 * DM + k]);
   __syncthreads();
   f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
   float den = 0.0f;
@@ -610,7 +679,9 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
   __shared__ float hv[3][RB_MAXH];    // th1's nu column, th2, psi_2
   __shared__ float nrm[RB_TB][4];     // n1, n2, nn, Dc
   __shared__ float dens[RB_TB];       // the memory read's normaliser
+  __shared__ float tsc[RB_TB][4];     // dL/dlogit, m_{j-1}, dL/dp, dL/dm
   __shared__ float dab[RB_TB][2];     // dL/da, dL/db
+  static_assert(RB_RED >= RB_TB * RB_MAXM, "phi(q) zeta products");
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = wave_id();
   const int T_ = a.T, j = a.j, DM = a.d_m, d_s = a.d_s, d_e = a.d_e, d_head = a.d_head;
   const int NP = d_e + d_head, d_x = d_s + DM + 1;
@@ -620,7 +691,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
     constexpr int US = (RB_TB * RB_MAXS + RB_BT - 1) / RB_BT, UM = (RB_TB * RB_MAXM + RB_BT - 1) / RB_BT;
     constexpr int UH = (RB_TB * RB_MAXH + RB_BT - 1) / RB_BT;
     const int ns = nb * d_s, nm = nb * DM, nh = nb * d_head;
-    float vs[US], vc[UM], vu[UM], vh[UH];
+    float vs[US], vc[UM], vu[UM], vh[UH], vq[UM], vz[UM], sc[4] = {0.0f, 1.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int u = 0; u < US; ++u) {
       const int e = min(tid + u * RB_BT, ns - 1), k = e / nb, b = e % nb;
@@ -631,6 +702,18 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
       const int e = min(tid + u * RB_BT, nm - 1), b = e / DM, k = e % DM;
       vc[u] = a.Cv[static_cast<size_t>(t0 + b) * DM + k];
       vu[u] = a.QKVU[static_cast<size_t>(t0 + b) * 4 * DM + 3 * DM + k];
+      if (a.c_given) {   // for the read's normaliser phi(q)^T zeta_{j-1} + eps
+        vq[u] = a.QKVU[static_cast<size_t>(t0 + b) * 4 * DM + k];
+        vz[u] = a.zeta_in[static_cast<size_t>(t0 + b) * DM + k];
+      }
+    }
+    if (tid < nb) {
+      const int t = t0 + tid;
+      sc[0] = a.dlogit[t];
+      if (j > 1) sc[1] = a.m_in[t];
+      sc[2] = a.dp[t];
+      sc[3] = a.dm[t];
+      if (!a.c_given) dens[tid] = a.DEN[t];
     }
 #pragma unroll
     for (int u = 0; u < UH; ++u) {
@@ -653,8 +736,11 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
       if (e < nm) {
         xth[b][d_s + k] = vc[u];
         u1[b][k] = vu[u];
+        if (a.c_given) red[b * DM + k] = phi_hw(vq[u]) * vz[u];
       }
     }
+    if (tid < nb)
+      for (int x = 0; x < 4; ++x) tsc[tid][x] = sc[x];
 #pragma unroll
     for (int u = 0; u < UH; ++u) {
       const int e = tid + u * RB_BT, b = e / d_head, o = e % d_head;
@@ -674,15 +760,10 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
   // p = sigma(a / T_hist); dL/da, dL/db; dL/dP's head part in its token-major row
   for (int b = wv; b < nb; b += RB_BW) {
     const int t = t0 + b;
-    float den;
-    if (a.c_given) {   // phi(q)^T zeta_{j-1} + eps (j >= 2), as the read pass forms it
-      const float* q = a.QKVU + static_cast<size_t>(t) * 4 * DM;
-      const float* z = a.zeta_in + static_cast<size_t>(t) * DM;
-      float dz = 0.0f;
-      for (int k = lane; k < DM; k += kWave) dz = fmaf(phif_(q[k]), z[k], dz);
-      den = wave_sum(dz) + a.eps;
-    } else {
-      den = a.DEN[t];
+    float den = 0.0f;
+    if (a.c_given) {
+      for (int k = lane; k < DM; k += kWave) den += red[b * DM + k];
+      den = wave_sum_dpp(den) + a.eps;
     }
     float n1 = 0.0f, n2 = 0.0f, nn = 0.0f;
     for (int k = lane; k < DM; k += kWave) {
@@ -690,26 +771,25 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
       n2 = fmaf(u2[b][k], u2[b][k], n2);
       nn = fmaf(u1[b][k], u2[b][k], nn);
     }
-    n1 = sqrtf(wave_sum(n1));
-    n2 = sqrtf(wave_sum(n2));
-    nn = wave_sum(nn);
+    n1 = sqrtf(wave_sum_dpp(n1));
+    n2 = sqrtf(wave_sum_dpp(n2));
+    nn = wave_sum_dpp(nn);
     const float Dc = n1 * n2 + a.eps;
     const float nu = j > 1 ? 1.0f - nn / Dc : 0.0f;
     float aa = 0.0f;
     for (int o = lane; o < d_head; o += kWave) {
       const float pre = fmaf(hv[0][o], nu, pa[b][o]);
       pa[b][o] = pre;
-      aa = fmaf(hv[1][o], siluf_(pre), aa);
+      aa = fmaf(hv[1][o], silu_hw(pre), aa);
     }
-    aa = wave_sum(aa);
-    const float p = sigmoidf_(aa / a.T_hist);
-    const float dl = a.dlogit[t];
-    const float m_prev = j > 1 ? a.m_in[t] : 1.0f;
-    const float da = dl + (a.dp[t] + a.dm[t] * m_prev) * p * (1.0f - p) / a.T_hist;
+    aa = wave_sum_dpp(aa);
+    const float p = sigmoid_hw(aa / a.T_hist);
+    const float dl = tsc[b][0], m_prev = tsc[b][1];
+    const float da = dl + (tsc[b][2] + tsc[b][3] * m_prev) * p * (1.0f - p) / a.T_hist;
     for (int o = lane; o < d_head; o += kWave)
-      a.dP[static_cast<size_t>(t) * NP + d_e + o] = dl * hv[2][o] * silu_grad_(dxth[b][o]);
+      a.dP[static_cast<size_t>(t) * NP + d_e + o] = dl * hv[2][o] * silu_grad_hw(dxth[b][o]);
     if (lane == 0) {
-      dens[b] = den;
+      if (a.c_given) dens[b] = den;
       nrm[b][0] = n1;
       nrm[b][1] = n2;
       nrm[b][2] = nn;
@@ -727,13 +807,13 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
   for (int e = tid; e < nb * d_head; e += RB_BT) {
     const int o = e / nb, b = e % nb, t = t0 + b;
     const float x = pa[b][o];
-    a.SAT[static_cast<size_t>(o) * T_ + t] = siluf_(x);
-    const float g = dab[b][0] * hv[1][o] * silu_grad_(x);
+    a.SAT[static_cast<size_t>(o) * T_ + t] = silu_hw(x);
+    const float g = dab[b][0] * hv[1][o] * silu_grad_hw(x);
     a.dPAT[static_cast<size_t>(o) * T_ + t] = g;
     pa[b][o] = g;
     const float pb = dxth[b][o];
-    a.dPT[static_cast<size_t>(d_e + o) * T_ + t] = dab[b][1] * hv[2][o] * silu_grad_(pb);
-    a.SBT[static_cast<size_t>(o) * T_ + t] = siluf_(pb);
+    a.dPT[static_cast<size_t>(d_e + o) * T_ + t] = dab[b][1] * hv[2][o] * silu_grad_hw(pb);
+    a.SBT[static_cast<size_t>(o) * T_ + t] = silu_hw(pb);
   }
   if (tid < nb) a.XT[static_cast<size_t>(d_s + DM) * T_ + t0 + tid] = xth[tid][d_s + DM];
   __syncthreads();
@@ -768,7 +848,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
       a.DNUM[static_cast<size_t>(t) * DM + v] = j > 1 ? dxth[b][d_s + v] / den : 0.0f;
       dden += j > 1 ? -dxth[b][d_s + v] * xth[b][d_s + v] / den : 0.0f;
     }
-    dden = wave_sum(dden);
+    dden = wave_sum_dpp(dden);
     if (lane == 0) a.DDEN[t] = dden;
   }
   for (int e = tid; e < nb * d_s; e += RB_BT) {
@@ -791,8 +871,8 @@ __global__ __launch_bounds__(RB_NT) void rbwd_spass(RouterBwdArgs a) {
   const int j = a.j;
   const float* qkv = a.QKVU + static_cast<size_t>(t) * 4 * DM;
   for (int k = tid; k < DM; k += RB_NT) {
-    fq[k] = phif_(qkv[k]);
-    fk[k] = phif_(qkv[DM + k]);
+    fq[k] = phi_hw(qkv[k]);
+    fk[k] = phi_hw(qkv[DM + k]);
     vv[k] = qkv[2 * DM + k];
     dn[k] = a.DNUM[static_cast<size_t>(t) * DM + k];
     zi[k] = j > 1 ? a.zeta_in[static_cast<size_t>(t) * DM + k] : 0.0f;
@@ -899,8 +979,8 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f3(RouterBwdArgs a) {
     for (int u = 0; u < UM; ++u) {
       const int e = tid + u * RB_BT, b = e / DM, k = e % DM;
       if (e < nm) {
-        dqkv[b][k] = gq[u] * phi_grad_(fq_[u]);
-        dqkv[b][DM + k] = gk[u] * phi_grad_(fk_[u]);
+        dqkv[b][k] = gq[u] * phi_grad_hw(fq_[u]);
+        dqkv[b][DM + k] = gk[u] * phi_grad_hw(fk_[u]);
         dqkv[b][2 * DM + k] = gv[u];
       }
     }
@@ -935,7 +1015,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f3(RouterBwdArgs a) {
   __syncthreads();
   for (int e = tid; e < nb * d_p; e += RB_BT) {
     const int o = e / nb, b = e % nb, t = t0 + b;
-    const float g = dpp[b][o] * silu_grad_(a.PPRE[static_cast<size_t>(t) * d_p + o]);
+    const float g = dpp[b][o] * silu_grad_hw(a.PPRE[static_cast<size_t>(t) * d_p + o]);
     dpp[b][o] = g;
     a.dPPT[static_cast<size_t>(o) * T_ + t] = g;
   }
@@ -946,7 +1026,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f3(RouterBwdArgs a) {
     const int e = tid + u * RB_BT, b = e / d_e, k = e % d_e, t = t0 + b;
     if (e < ne) {
       const float ir = irs[b];
-      const float dph = dsh[b][k] * silu_grad_(ir * ph[u]);
+      const float dph = dsh[b][k] * silu_grad_hw(ir * ph[u]);
       dqkv[b][k] = ph[u];
       dsh[b][k] = dph;
       a.dP[static_cast<size_t>(t) * NP + k] = ir * dph;
@@ -959,20 +1039,20 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f3(RouterBwdArgs a) {
     const int b = idx / 6, k = idx % 6;
     float sacc = 0.0f;
     for (int o = lane; o < d_p; o += kWave) sacc = fmaf(wp1[o * 6 + k], dpp[b][o], sacc);
-    sacc = wave_sum(sacc);
+    sacc = wave_sum_dpp(sacc);
     if (lane == 0) dxp[b][k] = sacc;
   }
   for (int b = wv; b < nb; b += RB_BW) {
     float cn = 0.0f;
     for (int k = lane; k < d_e; k += kWave) cn = fmaf(dsh[b][k], dqkv[b][k], cn);
-    cn = wave_sum(cn);
+    cn = wave_sum_dpp(cn);
     if (lane == 0) cnv[b] = cn;
   }
   for (int e = tid; e < nb * d_e; e += RB_BT) {
     const int k = e / nb, b = e % nb, t = t0 + b;
     const float ir = irs[b];
     a.dPT[static_cast<size_t>(k) * T_ + t] = ir * dsh[b][k];
-    a.SHT[static_cast<size_t>(k) * T_ + t] = siluf_(ir * dqkv[b][k]);
+    a.SHT[static_cast<size_t>(k) * T_ + t] = silu_hw(ir * dqkv[b][k]);
   }
   __syncthreads();
   if (tid < nb) {
@@ -1045,17 +1125,27 @@ __global__ __launch_bounds__(256) void router_bwd_rows(RouterBwdArgs a) {
 }
 
 // dL/deta = rho (1 - rho) sum_t rho_part[t], summed in a fixed order (one workgroup)
-__global__ __launch_bounds__(256) void router_bwd_deta(const float* __restrict__ part, int T, float rho,
-                                                      float* __restrict__ deta) {
-  __shared__ float red[256 / kWave];
+constexpr int RB_DETA_NT = 1024;
+__global__ __launch_bounds__(RB_DETA_NT) void router_bwd_deta(const float* __restrict__ part, int T, float rho,
+                                                             float* __restrict__ deta) {
+  constexpr int U = 8;   // loads in flight per thread
+  __shared__ float red[RB_DETA_NT / kWave];
+  // thread i adds its contiguous run of ceil(T / RB_DETA_NT) entries in order
+  const int C = (T + RB_DETA_NT - 1) / RB_DETA_NT, b0 = static_cast<int>(threadIdx.x) * C, b1 = min(b0 + C, T);
   float s = 0.0f;
-  for (int t = threadIdx.x; t < T; t += 256) s += part[t];
-  s = wave_sum(s);
+  for (int t = b0; t < b1; t += U) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = t + u < b1 ? part[t + u] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) s += v[u];
+  }
+  s = wave_sum_dpp(s);
   if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = s;
   __syncthreads();
   if (threadIdx.x == 0) {
     float tot = 0.0f;
-    for (int w = 0; w < 256 / kWave; ++w) tot += red[w];
+    for (int w = 0; w < RB_DETA_NT / kWave; ++w) tot += red[w];
     deta[0] = rho * (1.0f - rho) * tot;
   }
 }
@@ -1360,6 +1450,7 @@ size_t router_bwd_token_floats(int d_m, int d_s, int d_p, int np) {
 static bool router_bwd_token_shape_ok(const RouterBwdArgs& a) {
   if (a.d_e > RB_MAXE || a.d_head > RB_MAXH || a.d_s > RB_MAXS || a.d_m > RB_MAXM || a.d_p > RB_MAXP) return false;
   if (a.d_m != 32 && a.d_m != 64 && a.d_m != 128 && a.d_m != 256) return false;
+  if (a.p_splits < 1 || a.p_splits > RB_MAXSPL || a.d % 8) return false;
   return 0 <= a.t_begin && a.t_begin <= a.t_end && a.t_end <= a.T;
 }
 
@@ -1422,7 +1513,7 @@ hipError_t launch_router_bwd_rows(const RouterBwdArgs& a, hipStream_t s) {
     router_bwd_rows<float><<<a.T, 256, 0, s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  router_bwd_deta<<<1, 256, 0, s>>>(a.rho_part, a.T, a.rho, a.deta);
+  router_bwd_deta<<<1, RB_DETA_NT, 0, s>>>(a.rho_part, a.T, a.rho, a.deta);
   return hipGetLastError();
 }
 
