@@ -119,6 +119,12 @@ def test_router_backward_one_token():
     _run(BF16.replace(T=1), 4, seed=41)
 
 
+@pytest.mark.parametrize("c_from_forward", [False, True])
+def test_router_backward_1500_tokens(c_from_forward):
+    """94 batches of 16 tokens, the last one ragged (12 tokens)."""
+    _run(BF16.replace(T=1500), 3, seed=61, c_from_forward=c_from_forward)
+
+
 def test_router_backward_llama31_8b_layer_full_shape():
     """The Llama-3.1-8B routed layer's router (d = 4096, d_m = 128, 4096 tokens, routed layer 17):
     every token, every weight gradient."""
