@@ -1277,6 +1277,7 @@ struct RouterBwdLayout {
   size_t dPT_hi, dPT_lo, dP_hi, dP_lo, hbT16, wT16;
   size_t tn_part, tn_floats;   // K-split partials of the fp32 path's large weight-gradient products
   size_t sp_part, sp_floats;   // chunk partials of the small weight-gradient products
+  size_t wt;                   // bf16: the transposed router weights of the batched passes
   int kp;
   size_t total;
 };
@@ -1344,6 +1345,7 @@ RouterBwdLayout router_bwd_layout_of(const hero_dims& d, int T) {
   const int nsp = router_small_products(d, nullptr, nullptr, sp);
   L.sp_floats = hero::small_products_floats(sp, nsp, T);
   L.sp_part = take(L.sp_floats * 4);
+  L.wt = take(mfma ? hero::router_bwd_wt_elems(d.d_m, d.d_s, d.d_h, d.d_a, d.d_e, d.d_p, d.d_head) * 2 : 0);
   L.total = off;
   return L;
 }
@@ -1518,6 +1520,7 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
   a.PSUM = per_token(NP);
   a.t_begin = 0;
   a.t_end = T;
+  if (D.dtype == HERO_BF16) hero::router_bwd_wt_assign(a, reinterpret_cast<uint16_t*>(ws + L.wt));
   if (c_in) {
     a.Cv = const_cast<float*>(c_in);   // read only: the memory read pass is skipped
     a.c_given = 1;
@@ -1538,7 +1541,8 @@ int hero_router_backward(const hero_dims* dims, int j, int T, const void* hbar, 
       // one chain over all tokens (two halves on two streams, each half's batched passes beside the
       // other's state streams, measured 341 against 336 us at the 8B layer: the batched passes slow
       // down under the streams' memory traffic)
-      const hipError_t x = hero::launch_router_bwd_stats(a, s);
+      hipError_t x = hero::launch_router_bwd_wt(a, s);
+      if (x == hipSuccess) x = hero::launch_router_bwd_stats(a, s);
       return x == hipSuccess ? hero::launch_router_bwd_chain(a, s) : x;
     });
   if (e != hipSuccess) return HERO_E_LAUNCH;

@@ -280,7 +280,18 @@ struct RouterBwdArgs {
   // nonzero: Cv holds the forward's memory read (j >= 2); the read pass is skipped and F2 forms
   // the normaliser phi(q)^T zeta_{j-1} + eps itself
   int c_given;
+  // bf16 storage: the router weights transposed for the batched passes' transposed products, bf16,
+  // written by launch_router_bwd_wt (null for fp32 storage): th1^T [d_s + d_m + 1][d_head],
+  // W_n^T [d_s][d_m], W_c^T [d_m][d_m], [W_q; W_k; W_v]^T [d_s][3 d_m], W_p2^T [d_p][ld_ta],
+  // W_hu^T [d_e][ld_th] (ld_ta, ld_th: d_a, d_h rounded up to 8, the pad columns zero)
+  uint16_t *th1T, *wnT, *wcT, *wqkvT, *wp2T, *whuT;
+  int ld_ta, ld_th;
 };
+// bf16 elements of the transposed weights (each array starting on 16 bytes), and their placement
+// in a buffer of that many elements
+size_t router_bwd_wt_elems(int d_m, int d_s, int d_h, int d_a, int d_e, int d_p, int d_head);
+void router_bwd_wt_assign(RouterBwdArgs& a, uint16_t* base);
+hipError_t launch_router_bwd_wt(const RouterBwdArgs& a, hipStream_t s);
 // rows of the token-contiguous operands above, per token
 size_t router_bwd_vector_floats(int d_m, int d_s, int d_h, int d_a, int d_e, int d_p, int d_head);
 // floats of the token passes' intermediates, per token

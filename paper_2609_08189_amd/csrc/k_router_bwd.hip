@@ -23,6 +23,7 @@
 // At j = 1 the state entering the layer is the initial one (S = 0, zeta = 0, p = m = 1) whatever
 // the buffers hold; the carried gradient written there is rho dL/dS_1 (the state is a constant).
 #include <algorithm>
+#include <type_traits>
 
 #include "hero_device.h"
 #include "hero_kernels.h"
@@ -129,28 +130,18 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
-// w[i .. i + 3] (i a multiple of 4, the row pitch too) as loaded (raw4), and in fp32 (cvt4).  The
-// batches hold raw words and convert at their products: converting at the load would make the
-// compiler wait for the next batch's loads before the current batch's products.
+// w[i .. i + 3] (i a multiple of 4, the row pitch too) as loaded (raw4), and in fp32 (cvt4), for the
+// fp32 weights' transposed products.  The batches hold raw words and convert at their products:
+// converting at the load would make the compiler wait for the next batch's loads before the
+// current batch's products.
 template <typename W>
 struct Raw4;
-template <>
-struct Raw4<bf16_t> {
-  using type = uint2;
-};
 template <>
 struct Raw4<float> {
   using type = f32x4;
 };
-__device__ __forceinline__ uint2 raw4(const bf16_t* w, unsigned i) {
-  return *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(w) + i * 2u);
-}
 __device__ __forceinline__ f32x4 raw4(const float* w, unsigned i) {
   return *reinterpret_cast<const f32x4*>(reinterpret_cast<const char*>(w) + i * 4u);
-}
-__device__ __forceinline__ f32x4 cvt4(uint2 u) {
-  return f32x4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
-               __uint_as_float(u.y & 0xffff0000u)};
 }
 __device__ __forceinline__ f32x4 cvt4(f32x4 v) { return v; }
 // w[i .. i + 7] the same way (i a multiple of 8, the row pitch too): one 16-byte load in bf16
@@ -458,6 +449,142 @@ __device__ __forceinline__ void bmv_cols(const Cols<W>& A, int nb, float* red) {
   bmv_cols2(A, A, false, nb, red);
 }
 
+// bf16 weights: the batched products on v_mfma_f32_16x16x32_bf16.  An fp32 activation block (LDS,
+// [RB_TB][ldx]) is split, where it is produced or once before its product, into x = hi + lo, two bf16
+// values with |x - hi - lo| <= 2^-18 |x|, kept in LDS as two [RB_TB][xp] copies; the bf16 weights are exact, so
+// the two products of each 32-k step are exact in fp32 and only the accumulation rounds.  The
+// transposed products run as row products over transposed copies of the weights.
+constexpr int RB_XPAD = 8;   // bf16 entries past a split row's 32-multiple (spreads the rows over LDS banks)
+__host__ __device__ constexpr int rb_round(int x, int m) { return (x + m - 1) / m * m; }
+__host__ __device__ constexpr int rb_split_pitch(int I) { return rb_round(I, 32) + RB_XPAD; }
+
+// v into its split copies at entry i
+__device__ __forceinline__ void put_split(bf16_t* xh, bf16_t* xl, int i, float v) {
+  const __bf16 h = static_cast<__bf16>(v);
+  xh[i] = __builtin_bit_cast(bf16_t, h);
+  xl[i] = __builtin_bit_cast(bf16_t, static_cast<__bf16>(v - static_cast<float>(h)));
+}
+// x[b][k] (b < nb, k < I) into its split copies, zeros for I <= k < Iz (a product's K past the
+// valid entries, where the weights are zero padding); every thread calls it, between barriers
+__device__ __forceinline__ void split_x(const float* x, int ldx, int I, int Iz, int nb, bf16_t* xh, bf16_t* xl,
+                                        int xp) {
+  for (int e = threadIdx.x; e < nb * Iz; e += RB_BT) {
+    const int b = e / Iz, k = e - b * Iz;
+    put_split(xh, xl, b * xp + k, k < I ? x[b * ldx + k] : 0.0f);
+  }
+}
+
+constexpr int RB_P16 = 8;   // 32-k steps of weight loads in flight per lane in the split-bf16 products
+
+// Up to four bf16 matrices of one row pitch stacked by rows (as Mats), held as separate values: a
+// struct in memory selected by a runtime index gets compiled into an indexed load from scratch
+struct Stack16 {
+  const bf16_t *w0, *w1, *w2, *w3;
+  int om, ld;
+};
+__device__ __forceinline__ Stack16 stack16(const Mats<bf16_t>& M) { return Stack16{M.w0, M.w1, M.w2, M.w3, M.om, M.ld}; }
+__device__ __forceinline__ Stack16 one16(const void* w, int rows, int ld) {
+  return Stack16{static_cast<const bf16_t*>(w), nullptr, nullptr, nullptr, rows, ld};
+}
+// lane's weight row in tile ot (stack row ot 16 + r, clamped to the last row; a tile lies in one
+// matrix, so the choice of matrix is uniform)
+__device__ __forceinline__ const bf16_t* w_row16(const bf16_t* w0, const bf16_t* w1, const bf16_t* w2,
+                                                 const bf16_t* w3, int om, int ld, int O, int ot, int r) {
+  const int o0 = ot * 16, m = (o0 >= om) + (o0 >= 2 * om) + (o0 >= 3 * om);
+  const bf16_t* w = m == 0 ? w0 : m == 1 ? w1 : m == 2 ? w2 : w3;
+  return w + static_cast<unsigned>(min(o0 + r, O - 1) - m * om) * ld;
+}
+
+// y[b][o] (+)= sum_{k < I} W[o][k] x[b][k] for b < nb, o < O over a stack W of bf16 rows (pitch a
+// multiple of 8; I a multiple of 8), x given by its split copies (pitch xp at least I rounded up to
+// 32; entries past I and rows past nb may hold anything).  16-row tiles spread over the waves; a tile's k range goes in 32-k steps
+// (slot g: k0 + 8 g .. + 7, one 16-byte weight load a lane), and the wave's steps over all its tiles
+// run as one sequence with RB_P16 steps' loads in flight ahead of the products; hi and lo
+// accumulate apart.  With oh set, each stored value also goes into split copies (oh, ol, pitch osp).
+__device__ __forceinline__ void bmv16(Stack16 M, int O, int I, const bf16_t* xh, const bf16_t* xl, int xp, float* y,
+                                      int ldy, int nb, bool acc, bf16_t* oh = nullptr, bf16_t* ol = nullptr,
+                                      int osp = 0) {
+  const bf16_t *w0 = M.w0, *w1 = M.w1, *w2 = M.w2, *w3 = M.w3;
+  const int om = M.om, ld = M.ld;
+  const int lane = threadIdx.x & (kWave - 1), r = lane & 15, g = lane >> 4, wv = wave_id();
+  const int ntile = (O + 15) / 16;
+  const int ntw = wv < ntile ? (ntile - 1 - wv) / RB_BW + 1 : 0;   // this wave's tiles (uniform)
+  const int nst = (I + 31) / 32, total = ntw * nst;
+  if (total == 0) return;
+  const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+  const bf16x8 zx = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+  const bf16_t* ah = xh + r * xp + 8 * g;
+  const bf16_t* al = xl + r * xp + 8 * g;
+  // load side: the next step to load, as (tile, step), and that tile's weight row.  Every load is
+  // issued unconditionally (columns clamped below I; the products zero the x fragments past I),
+  // which keeps the compiler's count of loads in flight exact: a load under a branch makes it wait
+  // for all of them.
+  int lt = 0, ls = 0;
+  const bf16_t* lrow = w_row16(w0, w1, w2, w3, om, ld, O, wv, r);
+  u32x4 cur[RB_P16];
+#define RB_NEXT_LOAD(dst)                                          \
+  do {                                                             \
+    dst = raw8(lrow, static_cast<unsigned>(min(32 * ls + 8 * g, I - 8))); \
+    if (++ls == nst) {                                             \
+      ls = 0;                                                      \
+      lt = min(lt + 1, ntw - 1); /* past the end: the last tile again (unused) */ \
+      lrow = w_row16(w0, w1, w2, w3, om, ld, O, wv + lt * RB_BW, r);                    \
+    }                                                              \
+  } while (0)
+#pragma unroll
+  for (int u = 0; u < RB_P16; ++u) RB_NEXT_LOAD(cur[u]);
+  f32x4 acc0 = zero, acc1 = zero;
+  int ti = 0, st = 0;   // the step the products are at
+  for (int q0 = 0; q0 < total; q0 += RB_P16) {
+    u32x4 nxt[RB_P16];
+    if (q0 + RB_P16 < total)   // uniform
+#pragma unroll
+      for (int u = 0; u < RB_P16; ++u) RB_NEXT_LOAD(nxt[u]);
+    // the batch's x fragments first (every step's row entries exist, whatever the step), so that
+    // their LDS latency is paid once a batch rather than at every step
+    bf16x8 xhi[RB_P16], xlo[RB_P16];
+    {
+      int sx = st;
+#pragma unroll
+      for (int u = 0; u < RB_P16; ++u) {
+        xhi[u] = *reinterpret_cast<const bf16x8*>(ah + 32 * sx);
+        xlo[u] = *reinterpret_cast<const bf16x8*>(al + 32 * sx);
+        if (32 * sx + 8 * g >= I) xhi[u] = xlo[u] = zx;   // (the split rows hold I rounded up to 32)
+        if (++sx == nst) sx = 0;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < RB_P16; ++u) {
+      if (q0 + u < total) {   // uniform
+        const bf16x8 w = __builtin_bit_cast(bf16x8, cur[u]);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xhi[u], w, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xlo[u], w, acc1, 0, 0, 0);
+        if (++st == nst) {   // the tile's last step
+          const f32x4 v = acc0 + acc1;
+          const int o = (wv + ti * RB_BW) * 16 + r;
+          if (o < O)
+#pragma unroll
+            for (int q2 = 0; q2 < 4; ++q2) {
+              const int b = 4 * g + q2;
+              if (b < nb) {
+                float* ye = y + b * ldy + o;
+                const float f = acc ? *ye + v[q2] : v[q2];
+                *ye = f;
+                if (oh) put_split(oh, ol, b * osp + o, f);
+              }
+            }
+          acc0 = acc1 = zero;
+          st = 0;
+          ++ti;
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < RB_P16; ++u) cur[u] = nxt[u];
+  }
+#undef RB_NEXT_LOAD
+}
+
 // stats: a wave per token over the residual rows (16-byte loads) and P's slices
 template <typename T>
 __global__ __launch_bounds__(RB_NT) void rbwd_stats(RouterBwdArgs a) {
@@ -560,6 +687,15 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f1(RouterBwdArgs a) {
   __shared__ float xp[RB_TB][8];
   __shared__ float wp1[RB_MAXP * 6];
   __shared__ float irs[RB_TB];
+  // bf16: the split copies of SiLU(ir P_h), of the path encoder's SiLU and of s
+  constexpr bool kB = std::is_same<T, bf16_t>::value;
+  constexpr int XE = kB ? rb_split_pitch(RB_MAXE) : 0, XQ = kB ? rb_split_pitch(RB_MAXP) : 0;
+  constexpr int XS = kB ? rb_split_pitch(RB_MAXS) : 0;
+  __shared__ __attribute__((aligned(16))) bf16_t xsp[kB ? 2 * RB_TB * (XE + XQ + XS) : 8];
+  bf16_t *eh = xsp, *el = eh + RB_TB * XE, *qh = el + RB_TB * XE, *ql = qh + RB_TB * XQ, *sh2 = ql + RB_TB * XQ;
+  bf16_t* sl2 = sh2 + RB_TB * XS;
+  const int xe = rb_split_pitch(a.d_e), xq = rb_split_pitch(a.d_p), xsx = rb_split_pitch(a.d_s);
+  const bool p8 = (a.d_p & 7) == 0;   // W_p2's rows as 16-byte loads
   const int tid = threadIdx.x;
   const int T_ = a.T, j = a.j, DM = a.d_m, d_s = a.d_s, d_h = a.d_h, d_a = a.d_a;
   const int d_e = a.d_e, d_p = a.d_p, NP = d_e + a.d_head;
@@ -592,7 +728,11 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f1(RouterBwdArgs a) {
 #pragma unroll
   for (int u = 0; u < UE; ++u) {
     const int e = tid + u * RB_BT, b = e / d_e, k = e % d_e;
-    if (e < ne) sh[b][k] = silu_hw(irs[b] * ph[u]);
+    if (e < ne) {
+      const float v = silu_hw(irs[b] * ph[u]);
+      sh[b][k] = v;
+      if (kB) put_split(eh, el, b * xe + k, v);
+    }
   }
   for (int e = tid; e < nb * d_p; e += RB_BT) {
     const int b = e / d_p, o = e % d_p;
@@ -600,7 +740,9 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f1(RouterBwdArgs a) {
 #pragma unroll
     for (int k = 0; k < 6; ++k) pre = fmaf(wp1[o * 6 + k], xp[b][k], pre);
     a.PPRE[static_cast<size_t>(t0 + b) * d_p + o] = pre;
-    pp[b][o] = silu_hw(pre);
+    const float v = silu_hw(pre);
+    pp[b][o] = v;
+    if (kB && p8) put_split(qh, ql, b * xq + o, v);
   }
   __syncthreads();
   for (int e = tid; e < nb * d_p; e += RB_BT) {
@@ -612,8 +754,18 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f1(RouterBwdArgs a) {
     a.XPT[static_cast<size_t>(o) * T_ + t0 + b] = xp[b][o];
   }
   // s = [W_hu SiLU(ir P_h); W_p2 SiLU(W_p1 x^path)]
-  bmv_rows(mats1<T>(a.w_hu, d_h, d_e), d_h, d_e, &sh[0][0], RB_MAXE + 1, &xs[0][0], RB_MAXS + 1, nb);
-  bmv_rows(mats1<T>(a.w_p2, d_a, d_p), d_a, d_p, &pp[0][0], RB_MAXP + 1, &xs[0][d_h], RB_MAXS + 1, nb);
+  if constexpr (kB) {   // s's split copies as it is stored
+    bmv16(one16(a.w_hu, d_h, d_e), d_h, d_e, eh, el, xe, &xs[0][0], RB_MAXS + 1, nb, false, sh2, sl2,
+          xsx);
+    if (p8)
+      bmv16(one16(a.w_p2, d_a, d_p), d_a, d_p, qh, ql, xq, &xs[0][d_h], RB_MAXS + 1, nb, false, sh2 + d_h,
+            sl2 + d_h, xsx);
+    else
+      bmv_rows(mats1<T>(a.w_p2, d_a, d_p), d_a, d_p, &pp[0][0], RB_MAXP + 1, &xs[0][d_h], RB_MAXS + 1, nb);
+  } else {
+    bmv_rows(mats1<T>(a.w_hu, d_h, d_e), d_h, d_e, &sh[0][0], RB_MAXE + 1, &xs[0][0], RB_MAXS + 1, nb);
+    bmv_rows(mats1<T>(a.w_p2, d_a, d_p), d_a, d_p, &pp[0][0], RB_MAXP + 1, &xs[0][d_h], RB_MAXS + 1, nb);
+  }
   __syncthreads();
   for (int e = tid; e < nb * d_s; e += RB_BT) {
     const int k = e / nb, b = e % nb;
@@ -622,7 +774,16 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f1(RouterBwdArgs a) {
   // [q; k; v; W_n s] (pre-activations) in one stacked product, token-major
   const Mats<T> qkvn{static_cast<const T*>(a.w_q), static_cast<const T*>(a.w_k), static_cast<const T*>(a.w_v),
                      static_cast<const T*>(a.w_n), DM, d_s};
-  bmv_rows(qkvn, 4 * DM, d_s, &xs[0][0], RB_MAXS + 1, a.QKVU + static_cast<size_t>(t0) * 4 * DM, 4 * DM, nb);
+  float* qkvu = a.QKVU + static_cast<size_t>(t0) * 4 * DM;
+  if constexpr (kB) {
+    if (!p8) {   // W_p2's part of s came from the fp32 path
+      split_x(&xs[0][d_h], RB_MAXS + 1, d_a, d_a, nb, sh2 + d_h, sl2 + d_h, xsx);
+      __syncthreads();
+    }
+    bmv16(stack16(qkvn), 4 * DM, d_s, sh2, sl2, xsx, qkvu, 4 * DM, nb, false);
+  } else {
+    bmv_rows(qkvn, 4 * DM, d_s, &xs[0][0], RB_MAXS + 1, qkvu, 4 * DM, nb);
+  }
 }
 
 // M1: c and the normaliser for one token; thread: 4 columns (a float4) of DM / (RB_NT / (DM / 4))
@@ -675,7 +836,15 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
   __shared__ float pa[RB_TB][LH];     // f_theta's hidden pre-activation, then dL/dpre_a
   __shared__ float u1[RB_TB][LM];     // W_n s, then dL/du1
   __shared__ float u2[RB_TB][LM];     // W_c c, then dL/du2
-  __shared__ float red[RB_RED];
+  // bf16: split copies of [s; c], then dL/dpre_a, then dL/du1 and dL/du2, each written where the
+  // value is produced (the transposed products as row products over the transposed weights; red
+  // then only holds the normaliser's products)
+  constexpr bool kB = std::is_same<T, bf16_t>::value;
+  constexpr int XW = kB ? std::max(rb_split_pitch(RB_MAXS + RB_MAXM), 2 * rb_split_pitch(RB_MAXM)) : 0;
+  __shared__ __attribute__((aligned(16))) bf16_t xsp[kB ? 2 * RB_TB * XW : 8];
+  __shared__ float red[kB ? RB_TB * RB_MAXM : RB_RED];
+  bf16_t *bh = xsp, *bl = xsp + RB_TB * XW;
+  const int xpx = rb_split_pitch(a.d_s + a.d_m), xph = rb_split_pitch(a.d_head), xpu = rb_split_pitch(a.d_m);
   __shared__ float hv[3][RB_MAXH];    // th1's nu column, th2, psi_2
   __shared__ float nrm[RB_TB][4];     // n1, n2, nn, Dc
   __shared__ float dens[RB_TB];       // the memory read's normaliser
@@ -728,13 +897,17 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
 #pragma unroll
     for (int u = 0; u < US; ++u) {
       const int e = tid + u * RB_BT, k = e / nb, b = e % nb;
-      if (e < ns) xth[b][k] = vs[u];
+      if (e < ns) {
+        xth[b][k] = vs[u];
+        if (kB) put_split(bh, bl, b * xpx + k, vs[u]);
+      }
     }
 #pragma unroll
     for (int u = 0; u < UM; ++u) {
       const int e = tid + u * RB_BT, b = e / DM, k = e % DM;
       if (e < nm) {
         xth[b][d_s + k] = vc[u];
+        if (kB) put_split(bh, bl, b * xpx + d_s + k, vc[u]);
         u1[b][k] = vu[u];
         if (a.c_given) red[b * DM + k] = phi_hw(vq[u]) * vz[u];
       }
@@ -753,8 +926,13 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
     const int k = d_s + e / nb, b = e % nb;
     a.XT[static_cast<size_t>(k) * T_ + t0 + b] = xth[b][k];
   }
-  bmv_rows(mats1<T>(a.w_c, DM, DM), DM, DM, &xth[0][d_s], LX, &u2[0][0], LM, nb);
-  bmv_rows(mats1<T>(a.th1, d_head, a.ld_th1), d_head, d_s + DM, &xth[0][0], LX, &pa[0][0], LH, nb);
+  if constexpr (kB) {
+    bmv16(one16(a.w_c, DM, DM), DM, DM, bh + d_s, bl + d_s, xpx, &u2[0][0], LM, nb, false);
+    bmv16(one16(a.th1, d_head, a.ld_th1), d_head, d_s + DM, bh, bl, xpx, &pa[0][0], LH, nb, false);
+  } else {
+    bmv_rows(mats1<T>(a.w_c, DM, DM), DM, DM, &xth[0][d_s], LX, &u2[0][0], LM, nb);
+    bmv_rows(mats1<T>(a.th1, d_head, a.ld_th1), d_head, d_s + DM, &xth[0][0], LX, &pa[0][0], LH, nb);
+  }
   __syncthreads();
   // a wave per token: nu = 1 - cos(W_n s, W_c c); the history head a = th2 . SiLU(pre_a),
   // p = sigma(a / T_hist); dL/da, dL/db; dL/dP's head part in its token-major row
@@ -811,6 +989,7 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
     const float g = dab[b][0] * hv[1][o] * silu_grad_hw(x);
     a.dPAT[static_cast<size_t>(o) * T_ + t] = g;
     pa[b][o] = g;
+    if (kB) put_split(bh, bl, b * xph + o, g);
     const float pb = dxth[b][o];
     a.dPT[static_cast<size_t>(d_e + o) * T_ + t] = dab[b][1] * hv[2][o] * silu_grad_hw(pb);
     a.SBT[static_cast<size_t>(o) * T_ + t] = silu_hw(pb);
@@ -818,7 +997,11 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
   if (tid < nb) a.XT[static_cast<size_t>(d_s + DM) * T_ + t0 + tid] = xth[tid][d_s + DM];
   __syncthreads();
   // [ds; dc; dnu] = th1^T dL/dpre_a
-  bmv_cols(Cols<T>{mats1<T>(a.th1, d_head, a.ld_th1), d_head, d_x, &pa[0][0], LH, &dxth[0][0], LX, false}, nb, red);
+  if constexpr (kB) {
+    bmv16(one16(a.th1T, d_x, d_head), d_x, d_head, bh, bl, xph, &dxth[0][0], LX, nb, false);
+  } else {
+    bmv_cols(Cols<T>{mats1<T>(a.th1, d_head, a.ld_th1), d_head, d_x, &pa[0][0], LH, &dxth[0][0], LX, false}, nb, red);
+  }
   __syncthreads();
   // nu's cosine backward (a constant at j = 1)
   for (int e = tid; e < nb * DM; e += RB_BT) {
@@ -831,13 +1014,23 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f2(RouterBwdArgs a) {
     const float g2 = dcos * (a1 / Dc - q_ * n1 * (n2 > 0.0f ? a2 / n2 : 0.0f));
     u1[b][k] = g1;
     u2[b][k] = g2;
+    if (kB) {
+      put_split(bh, bl, b * xpu + k, g1);
+      put_split(bh + RB_TB * xpu, bl + RB_TB * xpu, b * xpu + k, g2);
+    }
     a.dU1T[static_cast<size_t>(k) * T_ + t] = g1;
     a.dU2T[static_cast<size_t>(k) * T_ + t] = g2;
   }
   __syncthreads();
   // ds += W_n^T du1, dc += W_c^T du2
-  bmv_cols2(Cols<T>{mats1<T>(a.w_n, DM, d_s), DM, d_s, &u1[0][0], LM, &dxth[0][0], LX, true},
-            Cols<T>{mats1<T>(a.w_c, DM, DM), DM, DM, &u2[0][0], LM, &dxth[0][d_s], LX, true}, true, nb, red);
+  if constexpr (kB) {
+    const int h2 = RB_TB * xpu;
+    bmv16(one16(a.wnT, d_s, DM), d_s, DM, bh, bl, xpu, &dxth[0][0], LX, nb, true);
+    bmv16(one16(a.wcT, DM, DM), DM, DM, bh + h2, bl + h2, xpu, &dxth[0][d_s], LX, nb, true);
+  } else {
+    bmv_cols2(Cols<T>{mats1<T>(a.w_n, DM, d_s), DM, d_s, &u1[0][0], LM, &dxth[0][0], LX, true},
+              Cols<T>{mats1<T>(a.w_c, DM, DM), DM, DM, &u2[0][0], LM, &dxth[0][d_s], LX, true}, true, nb, red);
+  }
   __syncthreads();
   // the read's normaliser: dL/dnum = dc / den, dL/dden = -<dc, c> / den (no read at j = 1)
   for (int b = wv; b < nb; b += RB_BW) {
@@ -936,7 +1129,16 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f3(RouterBwdArgs a) {
   __shared__ float dpp[RB_TB][LP];
   __shared__ float dxp[RB_TB][8];
   __shared__ float dsh[RB_TB][LE];
-  __shared__ float red[RB_RED];
+  // bf16: split copies of [dq; dk; dv] (written as they are formed), then of dz^a and dz^h (the
+  // transposed products as row products over the transposed weights); fp32: red for the
+  // transposed products' partial sums
+  constexpr bool kB = std::is_same<T, bf16_t>::value;
+  constexpr int XW = kB ? rb_split_pitch(3 * RB_MAXM) : 0;
+  static_assert(!kB || XW >= 2 * rb_split_pitch(RB_MAXS), "dz^a and dz^h side by side");
+  __shared__ __attribute__((aligned(16))) bf16_t xsp[kB ? 2 * RB_TB * XW : 8];
+  __shared__ float red[kB ? 1 : RB_RED];
+  bf16_t *bh = xsp, *bl = xsp + RB_TB * XW;
+  const int xpq = rb_split_pitch(3 * a.d_m);
   __shared__ float wp1[RB_MAXP * 6];
   __shared__ float cnv[RB_TB], irs[RB_TB];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = wave_id();
@@ -979,9 +1181,15 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f3(RouterBwdArgs a) {
     for (int u = 0; u < UM; ++u) {
       const int e = tid + u * RB_BT, b = e / DM, k = e % DM;
       if (e < nm) {
-        dqkv[b][k] = gq[u] * phi_grad_hw(fq_[u]);
-        dqkv[b][DM + k] = gk[u] * phi_grad_hw(fk_[u]);
+        const float q = gq[u] * phi_grad_hw(fq_[u]), kk = gk[u] * phi_grad_hw(fk_[u]);
+        dqkv[b][k] = q;
+        dqkv[b][DM + k] = kk;
         dqkv[b][2 * DM + k] = gv[u];
+        if (kB) {
+          put_split(bh, bl, b * xpq + k, q);
+          put_split(bh, bl, b * xpq + DM + k, kk);
+          put_split(bh, bl, b * xpq + 2 * DM + k, gv[u]);
+        }
       }
     }
 #pragma unroll
@@ -1000,7 +1208,11 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f3(RouterBwdArgs a) {
   // ds += [W_q; W_k; W_v]^T [dq; dk; dv] in one stacked product
   const Mats<T> qkv{static_cast<const T*>(a.w_q), static_cast<const T*>(a.w_k), static_cast<const T*>(a.w_v), nullptr,
                     DM, d_s};
-  bmv_cols(Cols<T>{qkv, 3 * DM, d_s, &dqkv[0][0], LQ, &ds[0][0], LS, true}, nb, red);
+  if constexpr (kB) {
+    bmv16(one16(a.wqkvT, d_s, 3 * DM), d_s, 3 * DM, bh, bl, xpq, &ds[0][0], LS, nb, true);
+  } else {
+    bmv_cols(Cols<T>{qkv, 3 * DM, d_s, &dqkv[0][0], LQ, &ds[0][0], LS, true}, nb, red);
+  }
   __syncthreads();
   for (int e = tid; e < nb * d_s; e += RB_BT) {
     const int k = e / nb, b = e % nb, t = t0 + b;
@@ -1010,8 +1222,18 @@ __global__ __launch_bounds__(RB_BT) void rbwd_f3(RouterBwdArgs a) {
       a.dZAT[static_cast<size_t>(k - d_h) * T_ + t] = ds[b][k];
   }
   // dL/dSiLU(pre_p) = W_p2^T dz^a and dL/dSiLU(pre_h) = W_hu^T dz^h
-  bmv_cols2(Cols<T>{mats1<T>(a.w_p2, d_a, d_p), d_a, d_p, &ds[0][d_h], LS, &dpp[0][0], LP, false},
-            Cols<T>{mats1<T>(a.w_hu, d_h, d_e), d_h, d_e, &ds[0][0], LS, &dsh[0][0], LE, false}, true, nb, red);
+  if constexpr (kB) {
+    const int xa = rb_split_pitch(a.ld_ta), xh = rb_split_pitch(a.ld_th), h2 = RB_TB * xa;
+    split_x(&ds[0][d_h], LS, d_a, a.ld_ta, nb, bh, bl, xa);   // (the weights' pad columns meet zeros)
+    split_x(&ds[0][0], LS, d_h, a.ld_th, nb, bh + h2, bl + h2, xh);
+    __syncthreads();
+    bmv16(one16(a.wp2T, d_p, a.ld_ta), d_p, a.ld_ta, bh, bl, xa, &dpp[0][0], LP, nb, false);
+    bmv16(one16(a.whuT, d_e, a.ld_th), d_e, a.ld_th, bh + h2, bl + h2, xh, &dsh[0][0], LE, nb,
+          false);
+  } else {
+    bmv_cols2(Cols<T>{mats1<T>(a.w_p2, d_a, d_p), d_a, d_p, &ds[0][d_h], LS, &dpp[0][0], LP, false},
+              Cols<T>{mats1<T>(a.w_hu, d_h, d_e), d_h, d_e, &ds[0][0], LS, &dsh[0][0], LE, false}, true, nb, red);
+  }
   __syncthreads();
   for (int e = tid; e < nb * d_p; e += RB_BT) {
     const int o = e / nb, b = e % nb, t = t0 + b;
@@ -1121,6 +1343,39 @@ __global__ __launch_bounds__(256) void router_bwd_rows(RouterBwdArgs a) {
     rows_rmw8(a.dhbar + row + i, g0);
     if (j >= 2) rows_rmw8(a.dhbar1 + row + i, g1);
     if (j >= 3) rows_rmw8(a.dhbar2 + row + i, g2);
+  }
+}
+
+// The transposed bf16 weights of the batched passes (bf16 storage): one element a thread, written
+// in order, gathered from the row-major weights (about 0.1 M elements at the 8B shape)
+__global__ __launch_bounds__(256) void rbwd_wt(RouterBwdArgs a) {
+  const int DM = a.d_m, d_s = a.d_s, d_x = d_s + DM + 1, dh = a.d_head, d_p = a.d_p, d_a = a.d_a, d_h = a.d_h;
+  const int d_e = a.d_e, ta = a.ld_ta, th = a.ld_th;
+  const int n0 = d_x * dh, n1 = n0 + d_s * DM, n2 = n1 + DM * DM, n3 = n2 + d_s * 3 * DM, n4 = n3 + d_p * ta;
+  const int n5 = n4 + d_e * th;
+  const bf16_t* th1 = static_cast<const bf16_t*>(a.th1);
+  for (int e = static_cast<int>(blockIdx.x * blockDim.x + threadIdx.x); e < n5;
+       e += static_cast<int>(gridDim.x * blockDim.x)) {
+    if (e < n0) {
+      const int k = e / dh, o = e % dh;
+      a.th1T[e] = th1[static_cast<size_t>(o) * a.ld_th1 + k];
+    } else if (e < n1) {
+      const int f = e - n0, k = f / DM, o = f % DM;
+      a.wnT[f] = static_cast<const bf16_t*>(a.w_n)[o * d_s + k];
+    } else if (e < n2) {
+      const int f = e - n1, k = f / DM, o = f % DM;
+      a.wcT[f] = static_cast<const bf16_t*>(a.w_c)[o * DM + k];
+    } else if (e < n3) {
+      const int f = e - n2, k = f / (3 * DM), c = f % (3 * DM), m = c / DM, o = c % DM;
+      const void* w = m == 0 ? a.w_q : m == 1 ? a.w_k : a.w_v;
+      a.wqkvT[f] = static_cast<const bf16_t*>(w)[o * d_s + k];
+    } else if (e < n4) {
+      const int f = e - n3, k = f / ta, o = f % ta;
+      a.wp2T[f] = o < d_a ? static_cast<const bf16_t*>(a.w_p2)[o * d_p + k] : bf16_t{0};
+    } else {
+      const int f = e - n4, k = f / th, o = f % th;
+      a.whuT[f] = o < d_h ? static_cast<const bf16_t*>(a.w_hu)[o * d_e + k] : bf16_t{0};
+    }
   }
 }
 
@@ -1447,11 +1702,52 @@ size_t router_bwd_token_floats(int d_m, int d_s, int d_p, int np) {
   return 4 + 4 * static_cast<size_t>(d_m) + d_p + d_m + 1 + 1 + d_s + d_m + 1 + 3 * static_cast<size_t>(d_m) + np;
 }
 
+// the transposed weights' element counts, each rounded up to 8 (16 bytes)
+static void router_bwd_wt_counts(int d_m, int d_s, int d_h, int d_a, int d_e, int d_p, int d_head, size_t n[6]) {
+  const size_t dx = static_cast<size_t>(d_s) + d_m + 1;
+  n[0] = dx * d_head;
+  n[1] = static_cast<size_t>(d_s) * d_m;
+  n[2] = static_cast<size_t>(d_m) * d_m;
+  n[3] = static_cast<size_t>(d_s) * 3 * d_m;
+  n[4] = static_cast<size_t>(d_p) * rb_round(d_a, 8);
+  n[5] = static_cast<size_t>(d_e) * rb_round(d_h, 8);
+  for (int i = 0; i < 6; ++i) n[i] = (n[i] + 7) / 8 * 8;
+}
+
+size_t router_bwd_wt_elems(int d_m, int d_s, int d_h, int d_a, int d_e, int d_p, int d_head) {
+  size_t n[6], tot = 0;
+  router_bwd_wt_counts(d_m, d_s, d_h, d_a, d_e, d_p, d_head, n);
+  for (size_t x : n) tot += x;
+  return tot;
+}
+
+void router_bwd_wt_assign(RouterBwdArgs& a, uint16_t* base) {
+  size_t n[6];
+  router_bwd_wt_counts(a.d_m, a.d_s, a.d_h, a.d_a, a.d_e, a.d_p, a.d_head, n);
+  uint16_t** dst[6] = {&a.th1T, &a.wnT, &a.wcT, &a.wqkvT, &a.wp2T, &a.whuT};
+  for (int i = 0; i < 6; ++i) {
+    *dst[i] = base;
+    base += n[i];
+  }
+  a.ld_ta = rb_round(a.d_a, 8);
+  a.ld_th = rb_round(a.d_h, 8);
+}
+
 static bool router_bwd_token_shape_ok(const RouterBwdArgs& a) {
   if (a.d_e > RB_MAXE || a.d_head > RB_MAXH || a.d_s > RB_MAXS || a.d_m > RB_MAXM || a.d_p > RB_MAXP) return false;
   if (a.d_m != 32 && a.d_m != 64 && a.d_m != 128 && a.d_m != 256) return false;
   if (a.p_splits < 1 || a.p_splits > RB_MAXSPL || a.d % 8) return false;
   return 0 <= a.t_begin && a.t_begin <= a.t_end && a.t_end <= a.T;
+}
+
+hipError_t launch_router_bwd_wt(const RouterBwdArgs& a, hipStream_t s) {
+  if (a.dtype != 1) return hipSuccess;
+  if (!router_bwd_token_shape_ok(a) || !a.th1T || !a.wnT || !a.wcT || !a.wqkvT || !a.wp2T || !a.whuT ||
+      a.ld_ta != rb_round(a.d_a, 8) || a.ld_th != rb_round(a.d_h, 8))
+    return hipErrorInvalidValue;
+  const int n = static_cast<int>(router_bwd_wt_elems(a.d_m, a.d_s, a.d_h, a.d_a, a.d_e, a.d_p, a.d_head));
+  rbwd_wt<<<static_cast<unsigned>((n + 255) / 256), 256, 0, s>>>(a);
+  return hipGetLastError();
 }
 
 hipError_t launch_router_bwd_stats(const RouterBwdArgs& a, hipStream_t s) {
@@ -1468,6 +1764,7 @@ hipError_t launch_router_bwd_stats(const RouterBwdArgs& a, hipStream_t s) {
 
 hipError_t launch_router_bwd_chain(const RouterBwdArgs& a, hipStream_t s) {
   if (!router_bwd_token_shape_ok(a) || (a.t_begin % RB_TB) != 0) return hipErrorInvalidValue;
+  if (a.dtype == 1 && (!a.th1T || !a.wnT || !a.wcT || !a.wqkvT || !a.wp2T || !a.whuT)) return hipErrorInvalidValue;
   const int n = a.t_end - a.t_begin;
   if (n == 0) return hipSuccess;
   const unsigned nbat = static_cast<unsigned>((n + RB_TB - 1) / RB_TB), nt = static_cast<unsigned>(n);
