@@ -1070,6 +1070,9 @@ def main():
                          "whose launch gaps are a visible share of the step")
     ap.add_argument("--eager", action="store_true",
                     help="time eager launches even for a decode-sized call")
+    ap.add_argument("--untiled", action="store_true",
+                    help="a decode-sized call reads the FFN weights row-major instead of the tiled copies "
+                         "of hero_ffn_decode_weights_make")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward of the routed block (training side) instead of the forward")
     ap.add_argument("--router-backward", action="store_true",
@@ -1136,7 +1139,9 @@ def main():
     j = w.layer_j
     print(f"# preparing {describe(w, j)}", file=sys.stderr, flush=True)
     prob = synth.make_problem(w, seed=args.seed)
-    dp = DeviceProblem(prob, device="cuda:0", stats=True, history=args.memory == "history")
+    # a decode step streams every FFN weight once: it reads the copies in the streaming order
+    tiled = w.dtype == "bf16" and w.T <= DECODE_TOKENS and not args.untiled
+    dp = DeviceProblem(prob, device="cuda:0", stats=True, history=args.memory == "history", tiled=tiled)
     m = measure_forward(w, dp, args.steps, args.warmup, memory=args.memory, graph=args.graph)
     K, L, nfs, nas = m["K"], m["L"], m["nfs"], m["nas"]
     print(f"# timed {K} steps: {m['ms_step']:.4f} ms/step", file=sys.stderr, flush=True)
@@ -1150,6 +1155,7 @@ def main():
                                ("" if args.memory == "matrix" else ", router memory in depth-history form"),
                    "memory": args.memory, "state": args.state, "global_batch": w.batch, "seq_len": w.seq,
                    "tokens": w.T, "layers_per_step": L, "parallelism": "none", "hip_graph": bool(args.graph),
+                   "ffn_weights": "tiled" if tiled else "row-major",
                    "n_ffn": sum(nfs), "n_adapter": sum(nas)},
         "roofline": dominant_roofline(w, m, counted_traffic("ffn_gate_up", args.workload) if default_line else None),
         "router_group": router_group(m),

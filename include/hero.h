@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define HERO_ABI_VERSION 6
+#define HERO_ABI_VERSION 7
 
 typedef enum hero_status {
   HERO_OK = 0,
@@ -100,9 +100,17 @@ typedef struct hero_dims {
   int state_dtype;    /* hero_dtype of S                                          */
 } hero_dims;
 
-/* Frozen backbone FFN of one routed layer: LN^ffn gain [d], W_g, W_u [d_ff][d], W_d [d][d_ff]. */
+/*
+ * Frozen backbone FFN of one routed layer: LN^ffn gain [d], W_g, W_u [d_ff][d], W_d [d][d_ff]
+ * (eq:dense_attention, eq:ffn_route).
+ * w_gate_up_tiled, w_down_tiled (optional, NULL when absent; bf16 models only): the same weights
+ * in the streaming order of the products with few rows, made once per model by
+ * hero_ffn_decode_weights_make.  When given, a branch of at most 256 rows (a decode step) reads
+ * them instead of w_gate/w_up (resp. w_down); the results are bit-identical either way.
+ */
 typedef struct hero_ffn_weights {
   const void *norm_w, *w_gate, *w_up, *w_down;
+  const void *w_gate_up_tiled, *w_down_tiled;
 } hero_ffn_weights;
 
 /* Bottleneck adapter of one routed layer (Sec. 3.1): W_1 [d_r][d], W_2 [d][d_r]. */
@@ -481,6 +489,25 @@ typedef struct hero_ffn_backward_weights {
  * weights or each other) from ffn.  Asynchronous on `stream`. */
 int hero_ffn_backward_weights_make(const hero_dims *dims, const hero_ffn_weights *ffn, void *w_down_t,
                                    void *w_gate_up_t, void *stream);
+
+/*
+ * The frozen FFN weights in the streaming order of the products with few rows (the FFN of a
+ * decode step, eq:ffn_route with at most 256 FFN tokens), made once per model.  Those products
+ * stream every weight once per call; read row by row, each 64-deep k-tile visits 128 bytes of
+ * every weight row, 8 KiB apart, a pattern HBM serves at about half its contiguous rate.  In the
+ * tiled order each 16-row block of a matrix is one contiguous run of 16 x 64 tiles:
+ *   w_gate_up_tiled [d_ff/16][d/64][2][16][64]   tile (b, t) of W_g, then tile (b, t) of W_u:
+ *                   element [b][t][0][r][c] = W_g[16 b + r][64 t + c], [b][t][1][r][c] = W_u[...]
+ *   w_down_tiled    [d/16][d_ff/64][16][64]      element [b][t][r][c] = W_d[16 b + r][64 t + c]
+ * Both are bf16 (dims.dtype must be HERO_BF16), 2 d d_ff and d d_ff elements, 16-byte aligned,
+ * caller-owned, not overlapping the weights or each other; d_ff % 64 == 0.  Either may be NULL
+ * (not made).  Asynchronous on `stream`.  Pass them in hero_ffn_weights.
+ * Errors: HERO_E_NULL (dims, ffn or its weights), HERO_E_UNSUPPORTED (fp32 model, d_ff % 64 != 0),
+ * HERO_E_ALIGN, HERO_E_ALIAS, HERO_E_DEVICE, HERO_E_LAUNCH.  The layer and stack calls reject
+ * tiled pointers that are misaligned (HERO_E_ALIGN) or given for such a model (HERO_E_UNSUPPORTED).
+ */
+int hero_ffn_decode_weights_make(const hero_dims *dims, const hero_ffn_weights *ffn, void *w_gate_up_tiled,
+                                 void *w_down_tiled, void *stream);
 
 /* Outputs of hero_routed_block_backward (all required, device, overwritten):
  *   dhbar  [T][d] dims.dtype   dL/dhbar: dL/dh plus LN^ffn's backward of the branch's du

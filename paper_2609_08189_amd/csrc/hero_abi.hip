@@ -133,6 +133,15 @@ int check_routing(const hero_routing* r) {
   return HERO_OK;
 }
 
+// the optional tiled FFN weights (hero_ffn_decode_weights_make): bf16 models with d_ff % 64 == 0
+int check_ffn_tiled(const hero_dims& d, const hero_ffn_weights* f) {
+  if (!f->w_gate_up_tiled && !f->w_down_tiled) return HERO_OK;
+  if (d.dtype != HERO_BF16 || d.d_ff % 64 != 0) return HERO_E_UNSUPPORTED;
+  if ((f->w_gate_up_tiled && !aligned16(f->w_gate_up_tiled)) || (f->w_down_tiled && !aligned16(f->w_down_tiled)))
+    return HERO_E_ALIGN;
+  return HERO_OK;
+}
+
 int check_weights(const hero_ffn_weights* f, const hero_router_weights* r, const hero_adapter_weights* a) {
   if (!f || !r || !a) return HERO_E_NULL;
   const void* ptrs[] = {f->norm_w, f->w_gate, f->w_up, f->w_down, a->w1, a->w2,
@@ -432,12 +441,12 @@ int run_layer(const LayerCall& c) {
   if (n_ffn_max > 0) {
     e = timed(HERO_K_FFN_GATE_UP, st, [&] {
       return launch_ffn_gateup(D.dtype, u, idx_ffn, counts, n_ffn_max, c.ffn->w_gate, c.ffn->w_up,
-                               act, part, D.d, D.d_ff, st);
+                               c.ffn->w_gate_up_tiled, act, part, D.d, D.d_ff, st);
     });
     if (e != hipSuccess) return HERO_E_LAUNCH;
     e = timed(HERO_K_FFN_DOWN, st, [&] {
-      return launch_ffn_down(D.dtype, act, idx_ffn, counts, n_ffn_max, c.ffn->w_down, c.hbar, gate,
-                             c.h_out, part, D.d, D.d_ff, st);
+      return launch_ffn_down(D.dtype, act, idx_ffn, counts, n_ffn_max, c.ffn->w_down, c.ffn->w_down_tiled,
+                             c.hbar, gate, c.h_out, part, D.d, D.d_ff, st);
     });
     if (e != hipSuccess) return HERO_E_LAUNCH;
   }
@@ -536,6 +545,7 @@ int check_layer_call(const hero_dims* dims, int j, int T, const void* hbar, cons
       (j >= 3 && !aligned16(hbar_prev2)))
     return HERO_E_ALIGN;
   if ((st = check_weights(ffn, router, adapter)) != HERO_OK) return st;
+  if ((st = check_ffn_tiled(*dims, ffn)) != HERO_OK) return st;
   if ((st = check_routing(routing)) != HERO_OK) return st;
   if ((st = check_stats(stats)) != HERO_OK) return st;
   const size_t hb = static_cast<size_t>(T) * dims->d * esize(dims->dtype);
@@ -669,6 +679,7 @@ int routed_stack(const hero_dims* dims, int T, const void* h_in, void* h_out, co
   if ((st = check_routing(routing)) != HERO_OK) return st;
   for (int l = 0; l < dims->L_R; ++l) {
     if ((st = check_weights(&ffn[l], router, &adapter[l])) != HERO_OK) return st;
+    if ((st = check_ffn_tiled(*dims, &ffn[l])) != HERO_OK) return st;
     if (!(eta[l] == eta[l])) return HERO_E_RANGE;
     if (stats && (st = check_stats(&stats[l])) != HERO_OK) return st;
   }
@@ -876,12 +887,13 @@ int run_dense_ffn(const hero_dims& dm, int T, const void* hbar, void* h, const h
   });
   if (e != hipSuccess) return HERO_E_LAUNCH;
   e = timed(HERO_K_FFN_GATE_UP, st, [&] {
-    return launch_ffn_gateup(dm.dtype, u, nullptr, nullptr, T, f.w_gate, f.w_up, act, part, dm.d, dm.d_ff, st);
+    return launch_ffn_gateup(dm.dtype, u, nullptr, nullptr, T, f.w_gate, f.w_up, f.w_gate_up_tiled, act, part,
+                             dm.d, dm.d_ff, st);
   });
   if (e != hipSuccess) return HERO_E_LAUNCH;
   e = timed(HERO_K_FFN_DOWN, st, [&] {
-    return launch_ffn_down(dm.dtype, act, nullptr, nullptr, T, f.w_down, hbar, nullptr, h, part, dm.d,
-                           dm.d_ff, st);
+    return launch_ffn_down(dm.dtype, act, nullptr, nullptr, T, f.w_down, f.w_down_tiled, hbar, nullptr, h, part,
+                           dm.d, dm.d_ff, st);
   });
   return e == hipSuccess ? HERO_OK : HERO_E_LAUNCH;
 }
@@ -950,9 +962,11 @@ int hero_decoder_stack(const hero_dims* dims, const hero_attn_dims* adims, int n
       if (!aligned16(ffn[l].norm_w) || !aligned16(ffn[l].w_gate) || !aligned16(ffn[l].w_up) ||
           !aligned16(ffn[l].w_down))
         return HERO_E_ALIGN;
+      if ((st = check_ffn_tiled(*dims, &ffn[l])) != HERO_OK) return st;
     } else {
       const int j = l - first;
       if ((st = check_weights(&ffn[l], router, &adapter[j])) != HERO_OK) return st;
+      if ((st = check_ffn_tiled(*dims, &ffn[l])) != HERO_OK) return st;
       if (!(eta[j] == eta[j])) return HERO_E_RANGE;
       if (stats && (st = check_stats(&stats[j])) != HERO_OK) return st;
     }
@@ -1101,6 +1115,30 @@ int hero_ffn_backward_weights_make(const hero_dims* dims, const hero_ffn_weights
   hipError_t e = hero::launch_transpose(dt, ffn->w_down, d, f, f, w_down_t, d, d, s);
   if (e == hipSuccess) e = hero::launch_transpose(dt, ffn->w_gate, f, d, d, gu, 2 * f, f, s);
   if (e == hipSuccess) e = hero::launch_transpose(dt, ffn->w_up, f, d, d, gu + f * esize(dt), 2 * f, f, s);
+  return e == hipSuccess ? HERO_OK : HERO_E_LAUNCH;
+}
+
+int hero_ffn_decode_weights_make(const hero_dims* dims, const hero_ffn_weights* ffn, void* w_gate_up_tiled,
+                                 void* w_down_tiled, void* stream) {
+  int st = check_dims(dims);
+  if (st != HERO_OK) return st;
+  if ((st = check_ffn(ffn)) != HERO_OK) return st;
+  if (dims->dtype != HERO_BF16 || dims->d_ff % 64 != 0) return HERO_E_UNSUPPORTED;
+  if ((w_gate_up_tiled && !aligned16(w_gate_up_tiled)) || (w_down_tiled && !aligned16(w_down_tiled)))
+    return HERO_E_ALIGN;
+  const size_t wb = static_cast<size_t>(dims->d) * dims->d_ff * 2;
+  const void* in[] = {ffn->w_gate, ffn->w_up, ffn->w_down};
+  for (const void* p : in)
+    if ((w_gate_up_tiled && overlap(w_gate_up_tiled, 2 * wb, p, wb)) || (w_down_tiled && overlap(w_down_tiled, wb, p, wb)))
+      return HERO_E_ALIAS;
+  if (w_gate_up_tiled && w_down_tiled && overlap(w_gate_up_tiled, 2 * wb, w_down_tiled, wb)) return HERO_E_ALIAS;
+  if ((st = check_device()) != HERO_OK) return st;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipSuccess;
+  if (w_gate_up_tiled)
+    e = hero::launch_tile_ffn_weights(ffn->w_gate, ffn->w_up, dims->d_ff, dims->d, w_gate_up_tiled, s);
+  if (e == hipSuccess && w_down_tiled)
+    e = hero::launch_tile_ffn_weights(ffn->w_down, nullptr, dims->d, dims->d_ff, w_down_tiled, s);
   return e == hipSuccess ? HERO_OK : HERO_E_LAUNCH;
 }
 

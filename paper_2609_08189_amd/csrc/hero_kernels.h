@@ -87,13 +87,22 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 // part: fp32 scratch of ffn_part_floats(dtype, d, d_ff, T) floats for any n_max <= T (used
 // when few rows split K).
 size_t ffn_part_floats(int dtype, int d, int d_ff, int T);
+// w_gate_up_tiled (may be null): W_g and W_u in the streaming order of launch_tile_ffn_weights,
+// read instead of w_gate, w_up by the products of at most 256 rows.
 hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const int* counts,
-                             int n_max, const void* w_gate, const void* w_up, void* act,
-                             float* part, int d, int d_ff, hipStream_t s);
+                             int n_max, const void* w_gate, const void* w_up, const void* w_gate_up_tiled,
+                             void* act, float* part, int d, int d_ff, hipStream_t s);
 // FFN branch, down + scatter: h_out[t] = hbar[t] + g[t] * (W_d act[m]), t = idx_ffn[m].
+// w_down_tiled (may be null): W_d in the streaming order, read instead of w_down by the products
+// of at most 256 rows.
 hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const int* counts,
-                           int n_max, const void* w_down, const void* hbar, const float* gate,
-                           void* h_out, float* part, int d, int d_ff, hipStream_t s);
+                           int n_max, const void* w_down, const void* w_down_tiled, const void* hbar,
+                           const float* gate, void* h_out, float* part, int d, int d_ff, hipStream_t s);
+// The frozen FFN weights in the decode products' streaming order (bf16): W [N][K] becomes
+// [N/16][K/64][G][16][64], i.e. for every block of 16 rows its 16 x 64 k-tiles in k order, each
+// a contiguous 2 KiB, with G = 2 matrices alternating tile by tile (W_g then W_u) or G = 1 (W_d).
+// w1 may be null when G = 1.  Needs N % 16 == 0 and K % 64 == 0.
+hipError_t launch_tile_ffn_weights(const void* w0, const void* w1, int N, int K, void* out, hipStream_t s);
 
 // FFN of a non-routed block: the two launchers above with idx_ffn = counts = gate = null
 // (every row, t = m, g = 1).

@@ -909,9 +909,14 @@ __device__ __forceinline__ void wait_vm() {
 
 // Epilogue: gate/up writes act[m][c] = bf16(SiLU(g) u) (out = act, ld = d_ff); otherwise the
 // K-slice y writes fp32 sums to part + y split_stride (out = part, ld = N).
+// tiled != 0: b0 holds the weights in the streaming order of tile_ffn_weights_kernel (16-row
+// blocks, each a contiguous run of 16 x 64 k-tiles; for the gate/up product the W_g and W_u
+// tiles of a block alternate) and b1, ldb are unused.  The same rows land in the same LDS slots
+// either way, so the results are identical; the tiled order turns each block's stream into
+// contiguous 2 KiB tiles instead of 128-byte visits of rows 8 KiB apart.
 template <class C>
 __global__ __launch_bounds__(512) void skinny_gemm(ARows<bf16_t> A, const bf16_t* __restrict__ b0,
-                                                  const bf16_t* __restrict__ b1, int ldb,
+                                                  const bf16_t* __restrict__ b1, int ldb, int tiled,
                                                   void* __restrict__ out, int ld, size_t split_stride,
                                                   const int* __restrict__ m_count, int n_max, int K,
                                                   int nb, int G, int S) {
@@ -941,20 +946,28 @@ __global__ __launch_bounds__(512) void skinny_gemm(ARows<bf16_t> A, const bf16_t
     const int pw = wave - 6;
     const unsigned char* base[C::BL];
     uint32_t off[C::BL];
+    constexpr int GU = C::DUAL ? 2 : 1;                       // matrices interleaved in a tiled block
+    const uint32_t tstride = tiled ? GU * 16 * ROWB : ROWB;  // bytes from one k-tile to the next
 #pragma unroll
     for (int i = 0; i < C::BL; ++i) {
       const int q = 2 * i + pw, slot = q >> 1;
       const int j = slot % C::NB;
       const int r = 8 * q + (lane >> 3);
       const int ch = (lane & 7) ^ ((r >> 1) & 7);
-      const int wrow = 16 * (blk0 + min(j, cnt - 1)) + 8 * (q & 1) + (lane >> 3);
-      base[i] = reinterpret_cast<const unsigned char*>(C::DUAL && slot >= C::NB ? b1 : b0);
-      off[i] = static_cast<uint32_t>(wrow) * static_cast<uint32_t>(ldb * 2) + kt0 * ROWB + ch * 16;
+      const int blk = blk0 + min(j, cnt - 1), rr = 8 * (q & 1) + (lane >> 3);
+      const int second = C::DUAL && slot >= C::NB;
+      if (tiled) {
+        base[i] = reinterpret_cast<const unsigned char*>(b0);
+        off[i] = ((static_cast<uint32_t>(blk) * nkt + kt0) * GU + second) * (16 * ROWB) + rr * ROWB + ch * 16;
+      } else {
+        base[i] = reinterpret_cast<const unsigned char*>(second ? b1 : b0);
+        off[i] = static_cast<uint32_t>(16 * blk + rr) * static_cast<uint32_t>(ldb * 2) + kt0 * ROWB + ch * 16;
+      }
     }
     auto issue = [&](int t) {
       unsigned char* st = sb + (t % NSB) * C::B_STAGE;
 #pragma unroll
-      for (int i = 0; i < C::BL; ++i) load_lds16(base[i] + off[i] + t * ROWB, st + (2 * i + pw) * 1024);
+      for (int i = 0; i < C::BL; ++i) load_lds16(base[i] + off[i] + t * tstride, st + (2 * i + pw) * 1024);
     };
     for (int t = 0; t < NSB; ++t)
       if (t < nk) issue(t);
@@ -1084,10 +1097,10 @@ __global__ __launch_bounds__(512) void skinny_gemm(ARows<bf16_t> A, const bf16_t
 }
 
 template <class C>
-hipError_t run_skinny(ARows<bf16_t> A, const bf16_t* b0, const bf16_t* b1, int ldb, void* out, int ld,
+hipError_t run_skinny(ARows<bf16_t> A, const bf16_t* b0, const bf16_t* b1, int ldb, int tiled, void* out, int ld,
                       size_t split_stride, const int* m_count, int n_max, int K, int nb, int G, int S,
                       hipStream_t s) {
-  skinny_gemm<C><<<G * S, 512, 0, s>>>(A, b0, b1, ldb, out, ld, split_stride, m_count, n_max, K, nb, G, S);
+  skinny_gemm<C><<<G * S, 512, 0, s>>>(A, b0, b1, ldb, tiled, out, ld, split_stride, m_count, n_max, K, nb, G, S);
   return hipGetLastError();
 }
 
@@ -1457,46 +1470,49 @@ bool skinny_down_fits(int n_max, int d, int d_ff) {
 }
 
 template <int NB, int RB>
-hipError_t skinny_gateup_nb_rb(ARows<bf16_t> A, const bf16_t* wg, const bf16_t* wu, bf16_t* act,
-                               const int* counts, int n_max, int d, int d_ff, hipStream_t s) {
+hipError_t skinny_gateup_nb_rb(ARows<bf16_t> A, const bf16_t* wg, const bf16_t* wu, const bf16_t* tiled,
+                               bf16_t* act, const int* counts, int n_max, int d, int d_ff, hipStream_t s) {
   using C = Skinny<NB, RB, 3, skinny_nsb(NB, RB, true, 3), true>;
   const int nb = d_ff / 16, G = std::min(kCUs, nb);
-  return run_skinny<C>(A, wg, wu, d, act, d_ff, 0, counts, n_max, d, nb, G, 1, s);
+  if (tiled) return run_skinny<C>(A, tiled, nullptr, 0, 1, act, d_ff, 0, counts, n_max, d, nb, G, 1, s);
+  return run_skinny<C>(A, wg, wu, d, 0, act, d_ff, 0, counts, n_max, d, nb, G, 1, s);
 }
 template <int NB>
-hipError_t skinny_gateup_nb(ARows<bf16_t> A, const bf16_t* wg, const bf16_t* wu, bf16_t* act,
-                            const int* counts, int n_max, int d, int d_ff, hipStream_t s) {
+hipError_t skinny_gateup_nb(ARows<bf16_t> A, const bf16_t* wg, const bf16_t* wu, const bf16_t* tiled,
+                            bf16_t* act, const int* counts, int n_max, int d, int d_ff, hipStream_t s) {
   switch ((n_max + 63) / 64) {
-    case 1: return skinny_gateup_nb_rb<NB, 1>(A, wg, wu, act, counts, n_max, d, d_ff, s);
-    case 2: return skinny_gateup_nb_rb<NB, 2>(A, wg, wu, act, counts, n_max, d, d_ff, s);
-    case 3: return skinny_gateup_nb_rb<NB, 3>(A, wg, wu, act, counts, n_max, d, d_ff, s);
-    default: return skinny_gateup_nb_rb<NB, 4>(A, wg, wu, act, counts, n_max, d, d_ff, s);
+    case 1: return skinny_gateup_nb_rb<NB, 1>(A, wg, wu, tiled, act, counts, n_max, d, d_ff, s);
+    case 2: return skinny_gateup_nb_rb<NB, 2>(A, wg, wu, tiled, act, counts, n_max, d, d_ff, s);
+    case 3: return skinny_gateup_nb_rb<NB, 3>(A, wg, wu, tiled, act, counts, n_max, d, d_ff, s);
+    default: return skinny_gateup_nb_rb<NB, 4>(A, wg, wu, tiled, act, counts, n_max, d, d_ff, s);
   }
 }
-hipError_t skinny_gateup(ARows<bf16_t> A, const bf16_t* wg, const bf16_t* wu, bf16_t* act,
+hipError_t skinny_gateup(ARows<bf16_t> A, const bf16_t* wg, const bf16_t* wu, const bf16_t* tiled, bf16_t* act,
                          const int* counts, int n_max, int d, int d_ff, hipStream_t s) {
   const int nb = d_ff / 16, G = std::min(kCUs, nb);
   switch ((nb + G - 1) / G) {   // most blocks a workgroup takes
-    case 1: return skinny_gateup_nb<1>(A, wg, wu, act, counts, n_max, d, d_ff, s);
-    case 2: return skinny_gateup_nb<2>(A, wg, wu, act, counts, n_max, d, d_ff, s);
-    case 3: return skinny_gateup_nb<3>(A, wg, wu, act, counts, n_max, d, d_ff, s);
-    default: return skinny_gateup_nb<4>(A, wg, wu, act, counts, n_max, d, d_ff, s);
+    case 1: return skinny_gateup_nb<1>(A, wg, wu, tiled, act, counts, n_max, d, d_ff, s);
+    case 2: return skinny_gateup_nb<2>(A, wg, wu, tiled, act, counts, n_max, d, d_ff, s);
+    case 3: return skinny_gateup_nb<3>(A, wg, wu, tiled, act, counts, n_max, d, d_ff, s);
+    default: return skinny_gateup_nb<4>(A, wg, wu, tiled, act, counts, n_max, d, d_ff, s);
   }
 }
 template <int RB>
-hipError_t skinny_down_rb(ARows<bf16_t> A, const bf16_t* wd, float* part, size_t stride,
+hipError_t skinny_down_rb(ARows<bf16_t> A, const bf16_t* wd, const bf16_t* tiled, float* part, size_t stride,
                           const int* counts, int n_max, int d, int d_ff, int S, hipStream_t s) {
   using C = Skinny<kSkinnyDownNB, RB, 3, skinny_nsb(kSkinnyDownNB, RB, false, 3), false>;
   const int nb = d / 16;
-  return run_skinny<C>(A, wd, nullptr, d_ff, part, d, stride, counts, n_max, d_ff, nb, nb / kSkinnyDownNB, S, s);
+  if (tiled)
+    return run_skinny<C>(A, tiled, nullptr, 0, 1, part, d, stride, counts, n_max, d_ff, nb, nb / kSkinnyDownNB, S, s);
+  return run_skinny<C>(A, wd, nullptr, d_ff, 0, part, d, stride, counts, n_max, d_ff, nb, nb / kSkinnyDownNB, S, s);
 }
-hipError_t skinny_down(ARows<bf16_t> A, const bf16_t* wd, float* part, size_t stride, const int* counts,
-                       int n_max, int d, int d_ff, int S, hipStream_t s) {
+hipError_t skinny_down(ARows<bf16_t> A, const bf16_t* wd, const bf16_t* tiled, float* part, size_t stride,
+                       const int* counts, int n_max, int d, int d_ff, int S, hipStream_t s) {
   switch ((n_max + 63) / 64) {
-    case 1: return skinny_down_rb<1>(A, wd, part, stride, counts, n_max, d, d_ff, S, s);
-    case 2: return skinny_down_rb<2>(A, wd, part, stride, counts, n_max, d, d_ff, S, s);
-    case 3: return skinny_down_rb<3>(A, wd, part, stride, counts, n_max, d, d_ff, S, s);
-    default: return skinny_down_rb<4>(A, wd, part, stride, counts, n_max, d, d_ff, S, s);
+    case 1: return skinny_down_rb<1>(A, wd, tiled, part, stride, counts, n_max, d, d_ff, S, s);
+    case 2: return skinny_down_rb<2>(A, wd, tiled, part, stride, counts, n_max, d, d_ff, S, s);
+    case 3: return skinny_down_rb<3>(A, wd, tiled, part, stride, counts, n_max, d, d_ff, S, s);
+    default: return skinny_down_rb<4>(A, wd, tiled, part, stride, counts, n_max, d, d_ff, S, s);
   }
 }
 
@@ -1579,6 +1595,25 @@ __global__ __launch_bounds__(256) void scatter_reduce(const float* __restrict__ 
   *reinterpret_cast<u32x4*>(out + o) = w;
 }
 
+// out[((nb K/64 + kt) G + g) 16 + r][c] = W_g[16 nb + r][64 kt + c] (w0: g = 0, w1: g = 1); one
+// thread per 16-byte piece of the output, so the writes are contiguous and each group of eight
+// threads reads one 128-byte run of a source row.
+__global__ __launch_bounds__(256) void tile_ffn_weights_kernel(const bf16_t* __restrict__ w0,
+                                                              const bf16_t* __restrict__ w1, int G, int K,
+                                                              size_t pieces, bf16_t* __restrict__ out) {
+  const size_t e = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= pieces) return;
+  const int c8 = static_cast<int>(e & 7), r = static_cast<int>((e >> 3) & 15);
+  const size_t t = e >> 7;                       // (nb nkt + kt) G + g
+  const int g = static_cast<int>(t % G);
+  const size_t bk = t / G;
+  const int nkt = K / BK;
+  const size_t nb = bk / nkt;
+  const int kt = static_cast<int>(bk % nkt);
+  const bf16_t* src = (g ? w1 : w0) + (16 * nb + r) * static_cast<size_t>(K) + kt * BK + 8 * c8;
+  *reinterpret_cast<u32x4*>(out + 8 * e) = *reinterpret_cast<const u32x4*>(src);
+}
+
 }  // namespace
 
 size_t ffn_part_floats(int dtype, int d, int d_ff, int T) {
@@ -1597,15 +1632,25 @@ size_t ffn_part_floats(int dtype, int d, int d_ff, int T) {
   return most;
 }
 
+hipError_t launch_tile_ffn_weights(const void* w0, const void* w1, int N, int K, void* out, hipStream_t s) {
+  if (N <= 0 || K <= 0 || N % 16 != 0 || K % BK != 0) return hipErrorInvalidValue;
+  const int G = w1 ? 2 : 1;
+  const size_t pieces = static_cast<size_t>(N) * (K / 8) * G;
+  tile_ffn_weights_kernel<<<static_cast<unsigned>((pieces + 255) / 256), 256, 0, s>>>(
+      static_cast<const bf16_t*>(w0), static_cast<const bf16_t*>(w1), G, K, pieces, static_cast<bf16_t*>(out));
+  return hipGetLastError();
+}
+
 hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const int* counts,
-                             int n_max, const void* w_gate, const void* w_up, void* act,
-                             float* part, int d, int d_ff, hipStream_t s) {
+                             int n_max, const void* w_gate, const void* w_up, const void* w_gate_up_tiled,
+                             void* act, float* part, int d, int d_ff, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(u), idx_ffn, d};
     if (skinny_gateup_fits(n_max, d, d_ff))
       return skinny_gateup(A, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
-                           static_cast<bf16_t*>(act), counts, n_max, d, d_ff, s);
+                           static_cast<const bf16_t*>(w_gate_up_tiled), static_cast<bf16_t*>(act), counts,
+                           n_max, d, d_ff, s);
     const int S = gateup_split(n_max, d, d_ff);
     if (S > 1) {
       BRows<bf16_t> B{static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up), d_ff, d};
@@ -1629,8 +1674,8 @@ hipError_t launch_ffn_gateup(int dtype, const void* u, const int* idx_ffn, const
 }
 
 hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const int* counts,
-                           int n_max, const void* w_down, const void* hbar, const float* gate,
-                           void* h_out, float* part, int d, int d_ff, hipStream_t s) {
+                           int n_max, const void* w_down, const void* w_down_tiled, const void* hbar,
+                           const float* gate, void* h_out, float* part, int d, int d_ff, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
   if (dtype == 1) {
     ARows<bf16_t> A{static_cast<const bf16_t*>(act), nullptr, d_ff};
@@ -1639,8 +1684,9 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
     const int S = skinny ? skinny_down_splits(d, d_ff) : down_split(n_max, d, d_ff);
     if (S > 1 || skinny) {
       const size_t stride = static_cast<size_t>(n_max) * d;
-      hipError_t e = skinny ? skinny_down(A, static_cast<const bf16_t*>(w_down), part, stride, counts, n_max, d,
-                                          d_ff, S, s)
+      hipError_t e = skinny ? skinny_down(A, static_cast<const bf16_t*>(w_down),
+                                          static_cast<const bf16_t*>(w_down_tiled), part, stride, counts,
+                                          n_max, d, d_ff, S, s)
                             : run_tile<TileSplitDown>(A, B, EpiStoreF32{part, d, stride}, counts, n_max, d,
                                                       d_ff, s, S);
       if (e != hipSuccess) return e;

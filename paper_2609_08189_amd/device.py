@@ -70,11 +70,25 @@ class LayerStats:
                     lam=float(self.lam.cpu().numpy()[0]))
 
 
+def make_tiled(dims: H.hero_dims, ffn: List[Dict[str, torch.Tensor]], ffn_s: List[H.hero_ffn_weights],
+               device) -> None:
+    """The FFN weights' copies in the decode products' streaming order (hero_ffn_decode_weights_make),
+    kept in ffn[i] and pointed at by ffn_s[i]."""
+    stream = torch.cuda.current_stream(torch.device(device)).cuda_stream
+    for f, fs in zip(ffn, ffn_s):
+        f["w_gate_up_tiled"] = torch.empty(2 * f["w_gate"].numel(), dtype=f["w_gate"].dtype, device=device)
+        f["w_down_tiled"] = torch.empty(f["w_down"].numel(), dtype=f["w_down"].dtype, device=device)
+        fs.w_gate_up_tiled = f["w_gate_up_tiled"].data_ptr()
+        fs.w_down_tiled = f["w_down_tiled"].data_ptr()
+        H.check(H.hero_ffn_decode_weights_make(dims, fs, f["w_gate_up_tiled"], f["w_down_tiled"], stream),
+                "hero_ffn_decode_weights_make")
+
+
 class DeviceProblem:
     """A synth.Problem resident on the GPU with the ABI structs that point at it."""
 
     def __init__(self, prob: synth.Problem, device: str = "cuda:0", stats: bool = True,
-                 for_stack: Optional[bool] = None, history: bool = False):
+                 for_stack: Optional[bool] = None, history: bool = False, tiled: bool = False):
         w = prob.w
         self.w = w
         self.device = device
@@ -90,6 +104,9 @@ class DeviceProblem:
         self.ffn = [{k: upload(v, device) for k, v in prob.ffn[i].items()} for i in range(len(prob.ffn))]
         self.ffn_s = [H.hero_ffn_weights(f["norm_w"].data_ptr(), f["w_gate"].data_ptr(),
                                          f["w_up"].data_ptr(), f["w_down"].data_ptr()) for f in self.ffn]
+        self.tiled = tiled
+        if tiled:
+            make_tiled(self.dims, self.ffn, self.ffn_s, device)
         self.adapter = [{k: upload(v, device) for k, v in prob.adapter[i].items()}
                         for i in range(len(prob.adapter))]
         self.adapter_s = [H.hero_adapter_weights(a["w1"].data_ptr(), a["w2"].data_ptr()) for a in self.adapter]

@@ -14,7 +14,7 @@ from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhero.so")
-ABI_VERSION = 6          # the struct layouts below follow include/hero.h of this version
+ABI_VERSION = 7          # the struct layouts below follow include/hero.h of this version
 
 HERO_OK = 0
 HERO_E_NULL = 1
@@ -60,7 +60,8 @@ class hero_dims(ctypes.Structure):
 
 
 class hero_ffn_weights(ctypes.Structure):
-    _fields_ = [("norm_w", _vp), ("w_gate", _vp), ("w_up", _vp), ("w_down", _vp)]
+    _fields_ = [("norm_w", _vp), ("w_gate", _vp), ("w_up", _vp), ("w_down", _vp),
+                ("w_gate_up_tiled", _vp), ("w_down_tiled", _vp)]
 
 
 class hero_adapter_weights(ctypes.Structure):
@@ -179,6 +180,8 @@ def lib() -> ctypes.CDLL:
                                          P(hero_router_weights), P(hero_adapter_weights), P(ctypes.c_float),
                                          P(ctypes.c_float), P(hero_routing), P(hero_layer_stats), _vp,
                                          ctypes.c_size_t, _vp]
+        L.hero_ffn_decode_weights_make.restype = ctypes.c_int
+        L.hero_ffn_decode_weights_make.argtypes = [P(hero_dims), P(hero_ffn_weights), _vp, _vp, _vp]
         L.hero_ffn_backward_weights_make.restype = ctypes.c_int
         L.hero_ffn_backward_weights_make.argtypes = [P(hero_dims), P(hero_ffn_weights), _vp, _vp, _vp]
         L.hero_backward_workspace_size.restype = ctypes.c_int
@@ -375,6 +378,12 @@ def hero_decoder_stack(dims: hero_dims, adims: hero_attn_dims, n_layers: int, ba
                                     _byref(state), at_arr, ffn_arr, _byref(router), ad_arr, _floats(eta),
                                     _floats(inv_freq), _byref(routing), st_arr, ptr(workspace),
                                     int(workspace_bytes), stream)
+
+
+def hero_ffn_decode_weights_make(dims: hero_dims, ffn: hero_ffn_weights, w_gate_up_tiled, w_down_tiled,
+                                 stream=None) -> int:
+    return lib().hero_ffn_decode_weights_make(ctypes.byref(dims), _byref(ffn), ptr(w_gate_up_tiled),
+                                              ptr(w_down_tiled), stream)
 
 
 def hero_ffn_backward_weights_make(dims: hero_dims, ffn: hero_ffn_weights, w_down_t, w_gate_up_t,

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_function():
     lib = H.lib()
     for n in names:
         assert hasattr(lib, n), f"{n} declared in include/hero.h but not exported"
-    assert H.hero_abi_version() == H.ABI_VERSION == 6
+    assert H.hero_abi_version() == H.ABI_VERSION == 7
 
 
 def test_status_strings():
@@ -390,6 +390,30 @@ def test_backward_entry_points_validate():
     assert H.hero_skip_penalty(4, 2, 5, gates, 1.0, loss, gates + 16) == H.HERO_E_ALIAS
     assert H.hero_skip_penalty(4, 2, 5, gates, 1.0, loss + 4, dg) == H.HERO_E_ALIGN
     assert H.hero_skip_penalty(4, 2, 5, gates, 1.0, loss, dg) == H.HERO_E_DEVICE
+
+
+def test_ffn_decode_weights_make_validates():
+    """hero_ffn_decode_weights_make and the layer call's checks of the tiled weights (fake addresses)."""
+    dims = good_dims()
+    ffn, _, _, _ = fake_structs()
+    f = ffn[0]
+    gu, dn = FAKE + (5 << 30), FAKE + (6 << 30)
+    make = lambda f=f, a=gu, b=dn, d=dims: H.hero_ffn_decode_weights_make(d, f, a, b)
+    assert make(d=good_dims(H.HERO_F32)) == H.HERO_E_UNSUPPORTED
+    assert make(f=H.hero_ffn_weights(FAKE, FAKE, None, FAKE)) == H.HERO_E_NULL
+    assert make(a=gu + 8) == H.HERO_E_ALIGN
+    assert make(b=dn + 8) == H.HERO_E_ALIGN
+    assert make(a=f.w_up) == H.HERO_E_ALIAS
+    assert make(b=f.w_down) == H.HERO_E_ALIAS
+    assert make(b=gu + 2 * 512 * 1408 * 2 - 16) == H.HERO_E_ALIAS    # W_d's copy inside [W_g; W_u]'s
+    assert make(b=gu + 2 * 512 * 1408 * 2) == H.HERO_E_DEVICE        # adjacent, not overlapping
+    assert make(a=None) == H.HERO_E_DEVICE
+    assert make() == H.HERO_E_DEVICE
+    tiled = lambda a, b: H.hero_ffn_weights(f.norm_w, f.w_gate, f.w_up, f.w_down, a, b)
+    assert call_layer(ffn=tiled(gu + 8, None)) == H.HERO_E_ALIGN
+    assert call_layer(ffn=tiled(None, dn + 8)) == H.HERO_E_ALIGN
+    assert call_layer(good_dims(H.HERO_F32), ffn=tiled(gu, dn)) == H.HERO_E_UNSUPPORTED
+    assert call_layer(ffn=tiled(gu, dn)) == H.HERO_E_DEVICE
 
 
 def test_router_backward_entry_validates():
