@@ -493,12 +493,13 @@ int hero_ffn_backward_weights_make(const hero_dims *dims, const hero_ffn_weights
 /*
  * The frozen FFN weights in the streaming order of the products with few rows (the FFN of a
  * decode step, eq:ffn_route with at most 256 FFN tokens), made once per model.  Those products
- * stream every weight once per call; read row by row, each 64-deep k-tile visits 128 bytes of
- * every weight row, 8 KiB apart, a pattern HBM serves at about half its contiguous rate.  In the
- * tiled order each 16-row block of a matrix is one contiguous run of 16 x 64 tiles:
- *   w_gate_up_tiled [d_ff/16][d/64][2][16][64]   tile (b, t) of W_g, then tile (b, t) of W_u:
- *                   element [b][t][0][r][c] = W_g[16 b + r][64 t + c], [b][t][1][r][c] = W_u[...]
- *   w_down_tiled    [d/16][d_ff/64][16][64]      element [b][t][r][c] = W_d[16 b + r][64 t + c]
+ * stream every weight once per call, 64-deep k-tile by k-tile; read row by row, each k-tile
+ * visits 128 bytes of every weight row, 8 KiB apart.  In the tiled order the matrix is cut into
+ * 16 x 64 tiles of 2 KiB, stored k-tile by k-tile, so that the weights one k-tile of the products
+ * needs are one contiguous range:
+ *   w_gate_up_tiled [d/64][d_ff/16][2][16][64]   tile (t, b) of W_g, then tile (t, b) of W_u:
+ *                   element [t][b][0][r][c] = W_g[16 b + r][64 t + c], [t][b][1][r][c] = W_u[...]
+ *   w_down_tiled    [d_ff/64][d/16][16][64]      element [t][b][r][c] = W_d[16 b + r][64 t + c]
  * Both are bf16 (dims.dtype must be HERO_BF16), 2 d d_ff and d d_ff elements, 16-byte aligned,
  * caller-owned, not overlapping the weights or each other; d_ff % 64 == 0.  Either may be NULL
  * (not made).  Asynchronous on `stream`.  Pass them in hero_ffn_weights.

@@ -99,8 +99,8 @@ hipError_t launch_ffn_down(int dtype, const void* act, const int* idx_ffn, const
                            int n_max, const void* w_down, const void* w_down_tiled, const void* hbar,
                            const float* gate, void* h_out, float* part, int d, int d_ff, hipStream_t s);
 // The frozen FFN weights in the decode products' streaming order (bf16): W [N][K] becomes
-// [N/16][K/64][G][16][64], i.e. for every block of 16 rows its 16 x 64 k-tiles in k order, each
-// a contiguous 2 KiB, with G = 2 matrices alternating tile by tile (W_g then W_u) or G = 1 (W_d).
+// [K/64][N/16][G][16][64], i.e. 16 x 64 tiles of 2 KiB, k-tile by k-tile, each k-tile's row of
+// 16-row blocks contiguous, with G = 2 matrices alternating tile by tile (W_g then W_u) or G = 1 (W_d).
 // w1 may be null when G = 1.  Needs N % 16 == 0 and K % 64 == 0.
 hipError_t launch_tile_ffn_weights(const void* w0, const void* w1, int N, int K, void* out, hipStream_t s);
 

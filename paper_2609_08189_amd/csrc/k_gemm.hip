@@ -909,11 +909,12 @@ __device__ __forceinline__ void wait_vm() {
 
 // Epilogue: gate/up writes act[m][c] = bf16(SiLU(g) u) (out = act, ld = d_ff); otherwise the
 // K-slice y writes fp32 sums to part + y split_stride (out = part, ld = N).
-// tiled != 0: b0 holds the weights in the streaming order of tile_ffn_weights_kernel (16-row
-// blocks, each a contiguous run of 16 x 64 k-tiles; for the gate/up product the W_g and W_u
-// tiles of a block alternate) and b1, ldb are unused.  The same rows land in the same LDS slots
-// either way, so the results are identical; the tiled order turns each block's stream into
-// contiguous 2 KiB tiles instead of 128-byte visits of rows 8 KiB apart.
+// tiled != 0: b0 holds the weights in the streaming order of tile_ffn_weights_kernel (16 x 64
+// tiles, k-tile by k-tile, each k-tile's row of `tiled` 16-row blocks contiguous; for the
+// gate/up product the W_g and W_u tiles of a block alternate) and b1, ldb are unused.  The same
+// rows land in the same LDS slots either way, so the results are identical.  In the tiled order
+// a workgroup's weights of one k-tile are one contiguous run of 2 KiB tiles, and the workgroups
+// running the same k-tile read neighbouring runs, instead of 128-byte visits of rows 8 KiB apart.
 template <class C>
 __global__ __launch_bounds__(512) void skinny_gemm(ARows<bf16_t> A, const bf16_t* __restrict__ b0,
                                                   const bf16_t* __restrict__ b1, int ldb, int tiled,
@@ -947,7 +948,7 @@ __global__ __launch_bounds__(512) void skinny_gemm(ARows<bf16_t> A, const bf16_t
     const unsigned char* base[C::BL];
     uint32_t off[C::BL];
     constexpr int GU = C::DUAL ? 2 : 1;                       // matrices interleaved in a tiled block
-    const uint32_t tstride = tiled ? GU * 16 * ROWB : ROWB;  // bytes from one k-tile to the next
+    const uint32_t tstride = tiled ? static_cast<uint32_t>(tiled) * GU * 16 * ROWB : ROWB;  // k-tile to k-tile
 #pragma unroll
     for (int i = 0; i < C::BL; ++i) {
       const int q = 2 * i + pw, slot = q >> 1;
@@ -958,7 +959,7 @@ __global__ __launch_bounds__(512) void skinny_gemm(ARows<bf16_t> A, const bf16_t
       const int second = C::DUAL && slot >= C::NB;
       if (tiled) {
         base[i] = reinterpret_cast<const unsigned char*>(b0);
-        off[i] = ((static_cast<uint32_t>(blk) * nkt + kt0) * GU + second) * (16 * ROWB) + rr * ROWB + ch * 16;
+        off[i] = ((static_cast<uint32_t>(kt0) * tiled + blk) * GU + second) * (16 * ROWB) + rr * ROWB + ch * 16;
       } else {
         base[i] = reinterpret_cast<const unsigned char*>(second ? b1 : b0);
         off[i] = static_cast<uint32_t>(16 * blk + rr) * static_cast<uint32_t>(ldb * 2) + kt0 * ROWB + ch * 16;
@@ -1474,7 +1475,7 @@ hipError_t skinny_gateup_nb_rb(ARows<bf16_t> A, const bf16_t* wg, const bf16_t* 
                                bf16_t* act, const int* counts, int n_max, int d, int d_ff, hipStream_t s) {
   using C = Skinny<NB, RB, 3, skinny_nsb(NB, RB, true, 3), true>;
   const int nb = d_ff / 16, G = std::min(kCUs, nb);
-  if (tiled) return run_skinny<C>(A, tiled, nullptr, 0, 1, act, d_ff, 0, counts, n_max, d, nb, G, 1, s);
+  if (tiled) return run_skinny<C>(A, tiled, nullptr, 0, nb, act, d_ff, 0, counts, n_max, d, nb, G, 1, s);
   return run_skinny<C>(A, wg, wu, d, 0, act, d_ff, 0, counts, n_max, d, nb, G, 1, s);
 }
 template <int NB>
@@ -1503,7 +1504,7 @@ hipError_t skinny_down_rb(ARows<bf16_t> A, const bf16_t* wd, const bf16_t* tiled
   using C = Skinny<kSkinnyDownNB, RB, 3, skinny_nsb(kSkinnyDownNB, RB, false, 3), false>;
   const int nb = d / 16;
   if (tiled)
-    return run_skinny<C>(A, tiled, nullptr, 0, 1, part, d, stride, counts, n_max, d_ff, nb, nb / kSkinnyDownNB, S, s);
+    return run_skinny<C>(A, tiled, nullptr, 0, nb, part, d, stride, counts, n_max, d_ff, nb, nb / kSkinnyDownNB, S, s);
   return run_skinny<C>(A, wd, nullptr, d_ff, 0, part, d, stride, counts, n_max, d_ff, nb, nb / kSkinnyDownNB, S, s);
 }
 hipError_t skinny_down(ARows<bf16_t> A, const bf16_t* wd, const bf16_t* tiled, float* part, size_t stride,
@@ -1595,22 +1596,22 @@ __global__ __launch_bounds__(256) void scatter_reduce(const float* __restrict__ 
   *reinterpret_cast<u32x4*>(out + o) = w;
 }
 
-// out[((nb K/64 + kt) G + g) 16 + r][c] = W_g[16 nb + r][64 kt + c] (w0: g = 0, w1: g = 1); one
-// thread per 16-byte piece of the output, so the writes are contiguous and each group of eight
-// threads reads one 128-byte run of a source row.
+// out[((kt NB + b) G + g) 16 + r][c] = W_g[16 b + r][64 kt + c] with NB = N / 16 blocks (w0: g = 0,
+// w1: g = 1); one thread per 16-byte piece of the output, so the writes are contiguous and each
+// group of eight threads reads one 128-byte run of a source row.
 __global__ __launch_bounds__(256) void tile_ffn_weights_kernel(const bf16_t* __restrict__ w0,
                                                               const bf16_t* __restrict__ w1, int G, int K,
                                                               size_t pieces, bf16_t* __restrict__ out) {
   const size_t e = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
   if (e >= pieces) return;
   const int c8 = static_cast<int>(e & 7), r = static_cast<int>((e >> 3) & 15);
-  const size_t t = e >> 7;                       // (nb nkt + kt) G + g
+  const size_t t = e >> 7;                       // (kt NB + b) G + g
   const int g = static_cast<int>(t % G);
   const size_t bk = t / G;
-  const int nkt = K / BK;
-  const size_t nb = bk / nkt;
-  const int kt = static_cast<int>(bk % nkt);
-  const bf16_t* src = (g ? w1 : w0) + (16 * nb + r) * static_cast<size_t>(K) + kt * BK + 8 * c8;
+  const size_t NB = pieces / (static_cast<size_t>(K / BK) * G * 128);
+  const size_t b = bk % NB;
+  const int kt = static_cast<int>(bk / NB);
+  const bf16_t* src = (g ? w1 : w0) + (16 * b + r) * static_cast<size_t>(K) + kt * BK + 8 * c8;
   *reinterpret_cast<u32x4*>(out + 8 * e) = *reinterpret_cast<const u32x4*>(src);
 }
 

@@ -22,7 +22,7 @@ def _bits(t):
 
 
 def test_tiled_layout_is_the_documented_permutation():
-    """w_gate_up_tiled[b][t][0|1][r][c] = W_g|W_u[16 b + r][64 t + c]; w_down_tiled[b][t][r][c] = W_d[16 b + r][64 t + c]."""
+    """w_gate_up_tiled[t][b][0|1][r][c] = W_g|W_u[16 b + r][64 t + c]; w_down_tiled[t][b][r][c] = W_d[16 b + r][64 t + c]."""
     import torch
     from paper_2609_08189_amd.device import DeviceProblem
     w = BF16_DECODE.replace(T=16)
@@ -31,7 +31,7 @@ def test_tiled_layout_is_the_documented_permutation():
     torch.cuda.synchronize()
     f = dp.ffn[0]
     d, d_ff = w.d, w.d_ff
-    tile = lambda m, n, k: m.view(n // 16, 16, k // 64, 64).permute(0, 2, 1, 3)
+    tile = lambda m, n, k: m.view(n // 16, 16, k // 64, 64).permute(2, 0, 1, 3)
     want_gu = torch.stack([tile(f["w_gate"], d_ff, d), tile(f["w_up"], d_ff, d)], dim=2).reshape(-1)
     want_d = tile(f["w_down"], d, d_ff).reshape(-1)
     assert torch.equal(_bits(f["w_gate_up_tiled"]), _bits(want_gu))
