@@ -1048,6 +1048,32 @@ def bench_peaks(args):
     rows_region = 256 * 96 * 8192
     for vb in (128, 256, 512):
         out[f"hbm_read_rows_{vb}B_visits"] = cold_reads(rows_region, 8, vb)
+
+    # the vendor library (hipBLASLt through torch.matmul, bf16 in, fp32 accumulation, bf16 out) on
+    # the plain, ungathered FFN shapes of the Llama-3.1-8B stack and layer workloads: the FFN rows of
+    # one routed layer (T minus the budget's skipped tokens) by [W_g; W_u] (N = 2 d_ff) and by W_d
+    from paper_2609_08189_amd import synth
+    gen = torch.Generator(device="cuda:0").manual_seed(0)
+    for wname in ("llama31_8b_stack", "llama31_8b_layer"):
+        w = synth.WORKLOADS[wname]
+        m = w.T - int(math.floor(w.budget * w.T + 0.5))
+        for pname, n, k in (("gate_up", 2 * w.d_ff, w.d), ("down", w.d, w.d_ff)):
+            x = torch.randn(m, k, device="cuda:0", generator=gen).to(torch.bfloat16)
+            wt = (0.02 * torch.randn(n, k, device="cuda:0", generator=gen)).to(torch.bfloat16)
+            y = x @ wt.t()
+            torch.cuda.synchronize()
+            a, b = ev.create(2)
+            ev.record(a, stream)
+            for _ in range(reps):
+                y = x @ wt.t()
+            ev.record(b, stream)
+            us = 1000 * ev.elapsed_ms(a, b) / reps
+            ev.destroy([a, b])
+            tf = 2.0 * m * n * k / (us * 1e-6) * 1e-12
+            out[f"vendor_gemm_{wname}_{pname}"] = {"m": m, "n": n, "k": k, "us": round(us, 1), "tflops": round(tf, 1),
+                                                  "frac_of_2500": round(tf / PEAK_BF16_TFLOPS, 4), "launches": reps}
+            del x, wt, y
+            torch.cuda.empty_cache()
     print(json.dumps(out), flush=True)
 
 
