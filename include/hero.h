@@ -11,8 +11,14 @@
  *
  * This library runs that hot path on one GPU.  It is a plain C interface:
  *   - every tensor argument is a DEVICE pointer to caller-owned memory unless a
- *     comment says "host"; the library allocates nothing and keeps no state
- *     between calls;
+ *     comment says "host"; the calls allocate no device memory (the caller passes
+ *     a workspace; hero_routed_layer_noalloc uses a fixed device array of the
+ *     library's).  What the library keeps between calls: per calling thread and
+ *     device, a second stream and two events, created on the first call (outside
+ *     any graph capture that follows) for the work it forks beside the call's
+ *     stream; per device, the address of the no-allocation scratch; and the
+ *     process-global registry of the measurement hook hero_kernel_timer (empty
+ *     unless a caller attaches events).  No data of one call is read by another;
  *   - calls are asynchronous: they validate their arguments on the host, enqueue
  *     kernels on `stream` (a hipStream_t passed as void*, NULL = the null
  *     stream) and return; results are valid once the stream has synchronised;
