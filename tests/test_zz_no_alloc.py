@@ -31,12 +31,12 @@ def _host(dp, stats):
     return out
 
 
-def _case(w, j, seed):
+def _case(w, j, seed, tiled=False):
     import torch
     from paper_2609_08189_amd.device import DeviceProblem, LayerStats
-    print(f"case noalloc d={w.d} d_ff={w.d_ff} T={w.T} j={j} seed={seed}", flush=True)
+    print(f"case noalloc d={w.d} d_ff={w.d_ff} T={w.T} j={j} seed={seed} tiled={tiled}", flush=True)
     prob = synth.make_problem(w, seed=seed, layer_j=j)
-    dp = DeviceProblem(prob)
+    dp = DeviceProblem(prob, tiled=tiled)
     state0 = [x.clone() for x in (dp.S, dp.zeta, dp.p_hist, dp.m_hist)]
     # the workspace entry point
     dp.h_out.fill_(7)
@@ -68,3 +68,9 @@ def _case(w, j, seed):
 def test_noalloc_equals_workspace_call_twice():
     _case(W, 3, seed=11)
     _case(W.replace(T=97, budget=0.39), 2, seed=12)
+
+
+def test_noalloc_with_tiled_decode_weights():
+    """The same comparison with the FFN weights' tiled copies (hero_ffn_decode_weights_make), which
+    the decode-sized products of both entry points read."""
+    _case(W.replace(T=200), 4, seed=13, tiled=True)
