@@ -500,7 +500,7 @@ int hero_ffn_backward_weights_make(const hero_dims *dims, const hero_ffn_weights
  * The frozen FFN weights in the streaming order of the products with few rows (the FFN of a
  * decode step, eq:ffn_route with at most 256 FFN tokens), made once per model.  Those products
  * stream every weight once per call, 64-deep k-tile by k-tile; read row by row, each k-tile
- * visits 128 bytes of every weight row, 8 KiB apart.  In the tiled order the matrix is cut into
+ * visits 128 bytes of every weight row, a whole row (2 K bytes) apart.  In the tiled order the matrix is cut into
  * 16 x 64 tiles of 2 KiB, stored k-tile by k-tile, so that the weights one k-tile of the products
  * needs are one contiguous range:
  *   w_gate_up_tiled [d/64][d_ff/16][2][16][64]   tile (t, b) of W_g, then tile (t, b) of W_u:
